@@ -1,0 +1,264 @@
+/*
+ * CPU oracle for the pvMVMD hot path (Maverick, arxiv 2609.10264).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the bench's
+ * CPU-baseline leg may load this library.  The product (the HIP library under
+ * paper_2609_10264_amd/) shares no code with it and never calls it.
+ *
+ * Plain, slow, obviously-correct C.  Every field operation is done with the
+ * '%' operator on 64-bit unsigned integers; nothing is blocked, fused or
+ * reordered beyond what the paper's definitions state.  Indices are 0-based.
+ *
+ * Field: F_p with p = 2^31 - 1.  Field arrays are uint32 in [0, p).
+ * Signed int8 weights are embedded as w mod p (Sec. 7.2, "Model quantization":
+ * signed integers are embedded into the field).
+ *
+ * RAA code (App. B): G = R * Pi1 * V1 * A * Pi2 * V2 * A, G in F^{k x N},
+ * N = r*k, with
+ *   R_{i,j}  = 1 iff position j lies in the i-th block of r positions,
+ *   Pi_{i,j} = 1 iff pi(j) = i,
+ *   V        = diag(v),
+ *   A_{i,j}  = 1 iff i <= j (upper triangular).
+ * Hence (0-based):  R^T w  : out[j] = w[j / r]           (repeat)
+ *                   Pi^T w : out[j] = w[pi[j]]           (gather)
+ *                   Pi v   : out[pi[j]] = v[j]           (scatter)
+ *                   A^T w  : out[j] = sum_{i<=j} w[i]    (prefix sum)
+ *                   A v    : out[i] = sum_{j>=i} v[j]    (suffix sum)
+ *                   R v    : out[i] = sum_{q<r} v[i*r+q] (fold)
+ *
+ * Functions:
+ *   orc_encT        G^T w  (App. B, "Linear-time encoding")
+ *   orc_syn         G v    (App. B, transposition principle)
+ *   orc_server_eval Y^ = W X^ mod p                (Protocol pvMVMD, server step)
+ *   orc_keygen      P^T = (W Gx)^T, Q = Gy^T W     (Protocol pvMVMD, Preprocess)
+ *   orc_encode      X^ = X + Gx e_x                (Protocol pvMVMD, Encrypt)
+ *   orc_decode      Y = Y^ - P e_x                 (Protocol pvMVMD, Decrypt)
+ *   orc_verify      sparse coded Freivalds check   (Protocol pvMVMD, Verify;
+ *                                                   Protocol vMVMD, Verify)
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_P 2147483647ULL
+
+static uint64_t fadd(uint64_t a, uint64_t b) { return (a + b) % ORC_P; }
+static uint64_t fsub(uint64_t a, uint64_t b) { return (a + ORC_P - b) % ORC_P; }
+static uint64_t fmul(uint64_t a, uint64_t b) { return (a * b) % ORC_P; }
+
+/* Embedding of a signed integer into F_p. */
+static uint64_t emb(int64_t w) {
+    int64_t r = w % (int64_t)ORC_P;
+    if (r < 0) r += (int64_t)ORC_P;
+    return (uint64_t)r;
+}
+
+uint32_t orc_prime(void) { return (uint32_t)ORC_P; }
+
+/*
+ * Encoding w -> G^T w, F^k -> F^N (App. B).  G^T = A^T V2 Pi2^T A^T V1 Pi1^T R^T,
+ * applied right to left: repeat, gather by pi1, scale by v1, prefix sum,
+ * gather by pi2, scale by v2, prefix sum.
+ */
+void orc_encT(uint32_t k, uint32_t r, const uint32_t *pi1, const uint32_t *pi2,
+              const uint32_t *v1, const uint32_t *v2, const uint32_t *w, uint32_t *out) {
+    uint64_t N = (uint64_t)k * r;
+    uint64_t *t0 = (uint64_t *)malloc(N * sizeof(uint64_t));
+    uint64_t *t1 = (uint64_t *)malloc(N * sizeof(uint64_t));
+    /* R^T: repeat */
+    for (uint64_t j = 0; j < N; j++) t0[j] = w[j / r];
+    /* Pi1^T: gather */
+    for (uint64_t j = 0; j < N; j++) t1[j] = t0[pi1[j]];
+    /* V1 */
+    for (uint64_t j = 0; j < N; j++) t1[j] = fmul(v1[j], t1[j]);
+    /* A^T: prefix sum */
+    for (uint64_t j = 1; j < N; j++) t1[j] = fadd(t1[j - 1], t1[j]);
+    /* Pi2^T: gather */
+    for (uint64_t j = 0; j < N; j++) t0[j] = t1[pi2[j]];
+    /* V2 */
+    for (uint64_t j = 0; j < N; j++) t0[j] = fmul(v2[j], t0[j]);
+    /* A^T: prefix sum */
+    for (uint64_t j = 1; j < N; j++) t0[j] = fadd(t0[j - 1], t0[j]);
+    for (uint64_t j = 0; j < N; j++) out[j] = (uint32_t)t0[j];
+    free(t0);
+    free(t1);
+}
+
+/*
+ * Syndrome v -> G v, F^N -> F^k (App. B).  G = R Pi1 V1 A Pi2 V2 A, applied
+ * right to left: suffix sum, scale by v2, scatter by pi2, suffix sum, scale
+ * by v1, scatter by pi1, fold blocks of r.
+ */
+void orc_syn(uint32_t k, uint32_t r, const uint32_t *pi1, const uint32_t *pi2,
+             const uint32_t *v1, const uint32_t *v2, const uint32_t *v, uint32_t *out) {
+    uint64_t N = (uint64_t)k * r;
+    uint64_t *s0 = (uint64_t *)malloc(N * sizeof(uint64_t));
+    uint64_t *s1 = (uint64_t *)malloc(N * sizeof(uint64_t));
+    for (uint64_t j = 0; j < N; j++) s0[j] = v[j] % ORC_P;
+    /* A: suffix sum */
+    for (uint64_t j = N - 1; j-- > 0;) s0[j] = fadd(s0[j], s0[j + 1]);
+    /* V2 */
+    for (uint64_t j = 0; j < N; j++) s0[j] = fmul(v2[j], s0[j]);
+    /* Pi2: scatter */
+    for (uint64_t j = 0; j < N; j++) s1[pi2[j]] = s0[j];
+    /* A: suffix sum */
+    for (uint64_t j = N - 1; j-- > 0;) s1[j] = fadd(s1[j], s1[j + 1]);
+    /* V1 */
+    for (uint64_t j = 0; j < N; j++) s1[j] = fmul(v1[j], s1[j]);
+    /* Pi1: scatter */
+    for (uint64_t j = 0; j < N; j++) s0[pi1[j]] = s1[j];
+    /* R: fold */
+    for (uint64_t i = 0; i < k; i++) {
+        uint64_t acc = 0;
+        for (uint64_t q = 0; q < r; q++) acc = fadd(acc, s0[i * r + q]);
+        out[i] = (uint32_t)acc;
+    }
+    free(s0);
+    free(s1);
+}
+
+/*
+ * Server evaluation: Yhat[b][i] = sum_k emb(W[i][k]) * Xhat[b][k] mod p,
+ * for rows i in [row0, row1).  W is m x n row-major int8; Xhat is B x n
+ * (query b at Xhat + b*n); Yhat is B x m.  Protocol pvMVMD: the server
+ * returns y^ = M x^ (one field matrix-vector product per query).
+ */
+void orc_server_eval_rows(const int8_t *W, uint32_t m, uint32_t n, const uint32_t *Xhat,
+                          uint32_t B, uint32_t *Yhat, uint32_t row0, uint32_t row1) {
+    for (uint32_t b = 0; b < B; b++) {
+        const uint32_t *x = Xhat + (uint64_t)b * n;
+        for (uint32_t i = row0; i < row1 && i < m; i++) {
+            const int8_t *w = W + (uint64_t)i * n;
+            uint64_t acc = 0;
+            for (uint32_t k = 0; k < n; k++) acc = fadd(acc, fmul(emb(w[k]), x[k]));
+            Yhat[(uint64_t)b * m + i] = (uint32_t)acc;
+        }
+    }
+}
+
+void orc_server_eval(const int8_t *W, uint32_t m, uint32_t n, const uint32_t *Xhat,
+                     uint32_t B, uint32_t *Yhat) {
+    orc_server_eval_rows(W, m, n, Xhat, B, Yhat, 0, m);
+}
+
+/*
+ * Preprocess (Protocol pvMVMD): P = W Gx in F^{m x Nx}, Q = Gy^T W in F^{Ny x n}.
+ * P^T = Gx^T W^T is m encodings of the rows of W; Q is n encodings of the
+ * columns of W (Sec. 6.3, "Preprocessing time").
+ * PT is stored Nx x m row-major (PT[j*m + i] = P[i][j]); Q is Ny x n row-major.
+ * Either output pointer may be NULL to skip it.
+ */
+void orc_keygen(const int8_t *W, uint32_t m, uint32_t n,
+                uint32_t rx, const uint32_t *xpi1, const uint32_t *xpi2, const uint32_t *xv1, const uint32_t *xv2,
+                uint32_t ry, const uint32_t *ypi1, const uint32_t *ypi2, const uint32_t *yv1, const uint32_t *yv2,
+                uint32_t *PT, uint32_t *Q) {
+    uint64_t Nx = (uint64_t)rx * n, Ny = (uint64_t)ry * m;
+    if (PT) {
+        uint32_t *row = (uint32_t *)malloc((uint64_t)n * sizeof(uint32_t));
+        uint32_t *enc = (uint32_t *)malloc(Nx * sizeof(uint32_t));
+        for (uint32_t i = 0; i < m; i++) {
+            for (uint32_t k = 0; k < n; k++) row[k] = (uint32_t)emb(W[(uint64_t)i * n + k]);
+            orc_encT(n, rx, xpi1, xpi2, xv1, xv2, row, enc);
+            for (uint64_t j = 0; j < Nx; j++) PT[j * m + i] = enc[j];
+        }
+        free(row);
+        free(enc);
+    }
+    if (Q) {
+        uint32_t *col = (uint32_t *)malloc((uint64_t)m * sizeof(uint32_t));
+        uint32_t *enc = (uint32_t *)malloc(Ny * sizeof(uint32_t));
+        for (uint32_t k = 0; k < n; k++) {
+            for (uint32_t i = 0; i < m; i++) col[i] = (uint32_t)emb(W[(uint64_t)i * n + k]);
+            orc_encT(m, ry, ypi1, ypi2, yv1, yv2, col, enc);
+            for (uint64_t j = 0; j < Ny; j++) Q[j * n + k] = enc[j];
+        }
+        free(col);
+        free(enc);
+    }
+}
+
+/*
+ * Encrypt (Protocol pvMVMD): e_x <- E_{tx}^{Nx} (given as tx (index, value)
+ * pairs per column), x' = Gx e_x, x^ = x + x'.  X, Xhat are B x n.
+ */
+void orc_encode(uint32_t n, uint32_t rx, const uint32_t *pi1, const uint32_t *pi2,
+                const uint32_t *v1, const uint32_t *v2, const uint32_t *X, uint32_t B,
+                const uint32_t *ex_idx, const uint32_t *ex_val, uint32_t tx, uint32_t *Xhat) {
+    uint64_t Nx = (uint64_t)rx * n;
+    uint32_t *e = (uint32_t *)malloc(Nx * sizeof(uint32_t));
+    uint32_t *xp = (uint32_t *)malloc((uint64_t)n * sizeof(uint32_t));
+    for (uint32_t b = 0; b < B; b++) {
+        memset(e, 0, Nx * sizeof(uint32_t));
+        for (uint32_t s = 0; s < tx; s++) {
+            uint64_t j = ex_idx[(uint64_t)b * tx + s];
+            e[j] = (uint32_t)fadd(e[j], ex_val[(uint64_t)b * tx + s]);
+        }
+        orc_syn(n, rx, pi1, pi2, v1, v2, e, xp);
+        for (uint32_t k = 0; k < n; k++)
+            Xhat[(uint64_t)b * n + k] = (uint32_t)fadd(X[(uint64_t)b * n + k], xp[k]);
+    }
+    free(e);
+    free(xp);
+}
+
+/*
+ * Decrypt (Protocol pvMVMD): y = y^ - P e_x = y^ - sum_{j in supp(e_x)} e_j P[:, j]
+ * (Table "Cost tally for the client online phase of pvMVMD").
+ * PT is Nx x m (row j is column j of P).  Yhat, Y are B x m.
+ */
+void orc_decode(const uint32_t *PT, uint32_t m, const uint32_t *Yhat, uint32_t B,
+                const uint32_t *ex_idx, const uint32_t *ex_val, uint32_t tx, uint32_t *Y) {
+    for (uint32_t b = 0; b < B; b++) {
+        for (uint32_t i = 0; i < m; i++) {
+            uint64_t mask = 0;
+            for (uint32_t s = 0; s < tx; s++) {
+                uint64_t j = ex_idx[(uint64_t)b * tx + s];
+                mask = fadd(mask, fmul(ex_val[(uint64_t)b * tx + s], PT[j * m + i]));
+            }
+            Y[(uint64_t)b * m + i] = (uint32_t)fsub(Yhat[(uint64_t)b * m + i], mask);
+        }
+    }
+}
+
+/*
+ * Verify (Protocol pvMVMD, which runs the Verify of Protocol vMVMD on the
+ * ciphertexts):
+ *   z_b = Gy^T y^_b;  for each repetition q: e <- E_{ty}^{Ny};
+ *   v_L = (e^T Q) x^_b,  v_R = e^T z_b;  reject iff v_L != v_R.
+ * One challenge per repetition is shared by all B columns (Sec. 5.4: the same
+ * sparse challenge may be shared across claims).  ey_idx/ey_val are ell x ty.
+ * Outputs: vL, vR (ell x B, may be NULL), accept (B): 1 iff every repetition
+ * matched for that column.
+ */
+void orc_verify(uint32_t m, uint32_t n, uint32_t ry, const uint32_t *pi1, const uint32_t *pi2,
+                const uint32_t *v1, const uint32_t *v2, const uint32_t *Q,
+                const uint32_t *Xhat, const uint32_t *Yhat, uint32_t B,
+                const uint32_t *ey_idx, const uint32_t *ey_val, uint32_t ty, uint32_t ell,
+                uint32_t *vL, uint32_t *vR, uint8_t *accept) {
+    uint64_t Ny = (uint64_t)ry * m;
+    uint32_t *z = (uint32_t *)malloc(Ny * (uint64_t)B * sizeof(uint32_t));
+    uint64_t *u = (uint64_t *)malloc((uint64_t)n * sizeof(uint64_t));
+    for (uint32_t b = 0; b < B; b++) {
+        orc_encT(m, ry, pi1, pi2, v1, v2, Yhat + (uint64_t)b * m, z + (uint64_t)b * Ny);
+        accept[b] = 1;
+    }
+    for (uint32_t q = 0; q < ell; q++) {
+        const uint32_t *ei = ey_idx + (uint64_t)q * ty;
+        const uint32_t *ev = ey_val + (uint64_t)q * ty;
+        /* u = e^T Q = sum_{j in supp(e)} e_j Q[j, :] */
+        for (uint32_t k = 0; k < n; k++) u[k] = 0;
+        for (uint32_t s = 0; s < ty; s++)
+            for (uint32_t k = 0; k < n; k++) u[k] = fadd(u[k], fmul(ev[s], Q[(uint64_t)ei[s] * n + k]));
+        for (uint32_t b = 0; b < B; b++) {
+            const uint32_t *x = Xhat + (uint64_t)b * n;
+            uint64_t l = 0, rr = 0;
+            for (uint32_t k = 0; k < n; k++) l = fadd(l, fmul(u[k], x[k]));
+            for (uint32_t s = 0; s < ty; s++) rr = fadd(rr, fmul(ev[s], z[(uint64_t)b * Ny + ei[s]]));
+            if (vL) vL[(uint64_t)q * B + b] = (uint32_t)l;
+            if (vR) vR[(uint64_t)q * B + b] = (uint32_t)rr;
+            if (l != rr) accept[b] = 0;
+        }
+    }
+    free(z);
+    free(u);
+}

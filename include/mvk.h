@@ -1,0 +1,191 @@
+/*
+ * mvk.h -- C ABI of the MI355X (gfx950) library for the data-parallel hot path
+ * of private and verifiable matrix-vector multiplication delegation (pvMVMD,
+ * "Maverick", arxiv 2609.10264).
+ *
+ * Field: F_p with p = 2^31 - 1.  A "field array" is uint32 in canonical form
+ * [0, p).  The public matrix W is int8 (each entry w is the field element
+ * w mod p; Sec. 7.2 embeds quantised signed integers into the field).
+ *
+ * Conventions shared by every call
+ *  - Pointers marked "device" are HIP device pointers (any allocator); the
+ *    caller owns every buffer it passes and must keep it alive until the work
+ *    enqueued on `stream` has completed.  Pointers marked "host" are ordinary
+ *    host memory read during the call.
+ *  - `stream` is a hipStream_t passed as void*; NULL means the default stream.
+ *    All calls only enqueue work on `stream` and return without waiting for it.
+ *  - Matrices are row-major.  A batch of B vectors of length L is B x L (vector b
+ *    starts at element b*L).
+ *  - Return value: MVK_OK, or a negative mvk_status.  On an error nothing has
+ *    been enqueued unless the status is MVK_EHIP (a launch failed; the stream
+ *    may hold part of the work and the outputs are undefined).
+ *  - Inputs are not validated on the device: field inputs must be < p and
+ *    permutations / sparse positions must be in range, or the outputs are
+ *    undefined (out-of-range indices are clamped, never dereferenced).
+ *  - The library keeps a per-(device, stream) workspace that grows on demand
+ *    (hipMalloc at first use and when a larger size is needed); calls enqueued
+ *    on two different streams never share workspace memory.
+ */
+#ifndef MVK_H_
+#define MVK_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MVK_PRIME 2147483647u
+#define MVK_ABI_VERSION 1
+
+typedef int32_t mvk_status;
+#define MVK_OK 0
+#define MVK_EINVAL (-1) /* missing pointer, zero or inconsistent size */
+#define MVK_ERANGE (-2) /* a size beyond the exactness limit of a kernel */
+#define MVK_ENOMEM (-3) /* workspace allocation failed */
+#define MVK_EHIP (-4)   /* a HIP runtime call or kernel launch failed */
+
+/* Largest column count n of W for which server_eval's int8-limb accumulation
+ * is exact: n * 128 * 128 < 2^31. */
+#define MVK_MAX_N 131071u
+
+/*
+ * Description of an RAA code (App. B): G = R Pi1 V1 A Pi2 V2 A in F^{k x N},
+ * N = r*k.  R repeats every entry r times (positions i*r .. i*r+r-1 hold entry
+ * i), Pi has Pi[i][j] = 1 iff pi(j) = i, V = diag(v), A is upper triangular
+ * all-ones.  pi1, pi2: device, N uint32 each, permutations of [0, N).
+ * v1, v2: device, N uint32 each, values in [1, p-1].
+ */
+typedef struct mvk_code {
+    uint32_t k;
+    uint32_t r;
+    const uint32_t *pi1;
+    const uint32_t *pi2;
+    const uint32_t *v1;
+    const uint32_t *v2;
+} mvk_code;
+
+/*
+ * Public parameters pp of Protocol pvMVMD (Preprocess):
+ *   cx : privacy code, k = n, block length Nx = cx.r * n
+ *   cy : verification code, k = m, block length Ny = cy.r * m
+ *   PT : device, Nx x m field array, PT[j*m + i] = P[i][j] with P = W Gx
+ *   Q  : device, Ny x n field array, Q = Gy^T W
+ * PT and Q are written by mvk_keygen and read by mvk_decode_verify.
+ */
+typedef struct mvk_key {
+    uint32_t m;
+    uint32_t n;
+    mvk_code cx;
+    mvk_code cy;
+    uint32_t *PT;
+    uint32_t *Q;
+} mvk_key;
+
+/*
+ * `count` sparse vectors of E_t^N (Sec. 3 notation: exactly t nonzeros).
+ * idx, val: device, count x t uint32.  Row c lists the t distinct positions
+ * (< N) and their nonzero values (in [1, p-1]) of vector c.
+ */
+typedef struct mvk_sparse {
+    const uint32_t *idx;
+    const uint32_t *val;
+    uint32_t t;
+    uint32_t count;
+} mvk_sparse;
+
+/* Human-readable name of a status code (static string). */
+const char *mvk_status_str(mvk_status s);
+
+/* MVK_ABI_VERSION of the loaded library. */
+int32_t mvk_abi_version(void);
+
+/*
+ * Server evaluation (Protocol pvMVMD: the server's only work is the field
+ * matrix-vector product y^ = M x^, once per query column).
+ *   W    : device, m x n int8, row-major (row i at W + i*n)
+ *   Xhat : device, B x n field array (the masked queries)
+ *   Yhat : device, B x m field array, written: Yhat[b][i] = sum_k W[i][k] Xhat[b][k] mod p
+ * m == 0 or B == 0: no work.  n == 0: Yhat is zeroed.
+ * Errors: MVK_EINVAL (null pointer), MVK_ERANGE (n > MVK_MAX_N).
+ */
+mvk_status mvk_server_eval(const int8_t *W, uint32_t m, uint32_t n, const uint32_t *Xhat,
+                           uint32_t B, uint32_t *Yhat, void *stream);
+
+/* Kernel family for mvk_server_eval_path. */
+#define MVK_PATH_AUTO 0 /* the library's choice (matrix-core path) */
+#define MVK_PATH_VALU 1 /* v_dot4_i32_i8 on the vector ALUs, cross-lane reduction in software */
+#define MVK_PATH_MFMA 2 /* v_mfma_i32_16x16x64_i8 on the matrix cores */
+
+/*
+ * mvk_server_eval with an explicit kernel family (same result bit for bit;
+ * used to compare the two designs).  path: one of MVK_PATH_*.
+ * Errors: as mvk_server_eval, plus MVK_EINVAL for an unknown path.
+ */
+mvk_status mvk_server_eval_path(const int8_t *W, uint32_t m, uint32_t n, const uint32_t *Xhat,
+                                uint32_t B, uint32_t *Yhat, int32_t path, void *stream);
+
+/*
+ * Preprocess (Protocol pvMVMD): writes key->PT = (W Gx)^T and key->Q = Gy^T W
+ * (m encodings of the rows and n encodings of the columns of W, Sec. 6.3).
+ *   key : host struct; key->m, key->n, the two codes and the PT, Q buffers
+ *         must be set (cx.k == n, cy.k == m)
+ *   W   : device, m x n int8
+ * Uses a workspace of about m*n + max(Nx*m, Ny*n)*4 bytes.
+ * Errors: MVK_EINVAL, MVK_ENOMEM.
+ */
+mvk_status mvk_keygen(const mvk_key *key, const int8_t *W, void *stream);
+
+/*
+ * Encrypt (Protocol pvMVMD): for every column b, x'_b = Gx e_b and
+ * Xhat_b = X_b + x'_b, where e_b is sparse vector b of `ex`
+ * (ex->count == B, positions < Nx).  The caller keeps `ex` as the secret
+ * state st for decode.
+ *   X    : device, B x n field array (plaintext queries)
+ *   Xhat : device, B x n field array, written
+ * Errors: MVK_EINVAL, MVK_ENOMEM.
+ */
+mvk_status mvk_encode(const mvk_key *key, const uint32_t *X, uint32_t B, const mvk_sparse *ex,
+                      uint32_t *Xhat, void *stream);
+
+/*
+ * Verify + Decrypt (Protocol pvMVMD) for B columns.
+ *   Verify: for each repetition q < ey->count (= ell) with challenge e_q in
+ *     E_ty^Ny (positions < Ny), v_L = (e_q^T Q) Xhat_b and
+ *     v_R = e_q^T (Gy^T Yhat_b); column b is accepted iff v_L == v_R for every q.
+ *     One challenge per repetition is shared by all columns (Sec. 5.4).
+ *     Challenges must be drawn after the responses Yhat are fixed.
+ *   Decrypt: Y_b = Yhat_b - P e_b with e_b sparse vector b of `ex`
+ *     (the state returned by encode).
+ *   Xhat   : device, B x n;  Yhat : device, B x m (the server's responses)
+ *   Y      : device, B x m, written (must be discarded where accept is 0)
+ *   vL, vR : device, ell x B, written; may be NULL
+ *   accept : device, B uint32, written 1 (accept) or 0 (reject)
+ * A rejection is a result, not an error.
+ * Errors: MVK_EINVAL, MVK_ENOMEM.
+ */
+mvk_status mvk_decode_verify(const mvk_key *key, const uint32_t *Xhat, const uint32_t *Yhat,
+                             uint32_t B, const mvk_sparse *ex, const mvk_sparse *ey,
+                             uint32_t *Y, uint32_t *vL, uint32_t *vR, uint32_t *accept,
+                             void *stream);
+
+/*
+ * RAA encoding w -> G^T w (App. B, "Linear-time encoding") for `count`
+ * vectors.  w: device, count x k field array; out: device, count x N.
+ */
+mvk_status mvk_raa_encode(const mvk_code *code, const uint32_t *w, uint32_t count, uint32_t *out,
+                          void *stream);
+
+/*
+ * RAA syndrome v -> G v (App. B, transposition principle) for `count` dense
+ * vectors.  v: device, count x N field array; out: device, count x k.
+ */
+mvk_status mvk_raa_syndrome(const mvk_code *code, const uint32_t *v, uint32_t count,
+                            uint32_t *out, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MVK_H_ */

@@ -1,0 +1,199 @@
+"""MI355X (gfx950) library for the hot path of private and verifiable
+matrix-vector multiplication delegation (pvMVMD, Maverick, arxiv 2609.10264).
+
+Thin Python binding over the C ABI in include/mvk.h: every function only
+checks tensor shapes/dtypes, passes raw device pointers and the current HIP
+stream, and raises on a non-zero status.  All computation runs in the HIP
+kernels of libmvk.so; there is no CPU fallback.
+
+Tensors: field arrays are torch.int32 on the GPU holding canonical values in
+[0, p), p = 2^31 - 1 (these fit a non-negative int32); W is torch.int8.
+"""
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+
+import torch
+
+from . import _lib
+from ._lib import MVK_MAX_N, MVK_PRIME, MvkCode, MvkError, MvkKey, MvkSparse
+
+P = MVK_PRIME
+
+__all__ = ["P", "MVK_MAX_N", "MvkError", "Code", "Key", "server_eval", "keygen", "encode",
+           "decode_verify", "raa_encode", "raa_syndrome", "library_path"]
+
+
+def library_path() -> str:
+    return _lib.LIB_PATH
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _dev(t: torch.Tensor, dtype: torch.dtype, shape: tuple | None, name: str) -> int:
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must have dtype {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    return t.data_ptr()
+
+
+@dataclass
+class Code:
+    """RAA code description (App. B) held on the device: N = r * k."""
+    k: int
+    r: int
+    pi1: torch.Tensor
+    pi2: torch.Tensor
+    v1: torch.Tensor
+    v2: torch.Tensor
+
+    @property
+    def N(self) -> int:
+        return self.k * self.r
+
+    @classmethod
+    def from_arrays(cls, k, r, pi1, pi2, v1, v2, device="cuda") -> "Code":
+        def t(a):
+            return torch.as_tensor(a).to(torch.int64).to(torch.int32).to(device).contiguous()
+        return cls(int(k), int(r), t(pi1), t(pi2), t(v1), t(v2))
+
+    def struct(self) -> MvkCode:
+        N = self.N
+        return MvkCode(self.k, self.r,
+                       _dev(self.pi1, torch.int32, (N,), "pi1"), _dev(self.pi2, torch.int32, (N,), "pi2"),
+                       _dev(self.v1, torch.int32, (N,), "v1"), _dev(self.v2, torch.int32, (N,), "v2"))
+
+
+@dataclass
+class Key:
+    """Public parameters pp = (Gx, Gy, P^T, Q) of Protocol pvMVMD."""
+    m: int
+    n: int
+    cx: Code
+    cy: Code
+    PT: torch.Tensor  # Nx x m
+    Q: torch.Tensor   # Ny x n
+
+    @classmethod
+    def allocate(cls, m: int, n: int, cx: Code, cy: Code, device="cuda") -> "Key":
+        PT = torch.empty((cx.N, m), dtype=torch.int32, device=device)
+        Q = torch.empty((cy.N, n), dtype=torch.int32, device=device)
+        return cls(int(m), int(n), cx, cy, PT, Q)
+
+    def struct(self) -> MvkKey:
+        return MvkKey(self.m, self.n, self.cx.struct(), self.cy.struct(),
+                      _dev(self.PT, torch.int32, (self.cx.N, self.m), "PT"),
+                      _dev(self.Q, torch.int32, (self.cy.N, self.n), "Q"))
+
+
+def _sparse(idx: torch.Tensor, val: torch.Tensor, name: str) -> MvkSparse:
+    if idx.dim() != 2 or idx.shape != val.shape:
+        raise ValueError(f"{name}: idx and val must be 2-D of equal shape")
+    count, t = idx.shape
+    return MvkSparse(_dev(idx, torch.int32, None, name + "_idx"), _dev(val, torch.int32, None, name + "_val"),
+                     int(t), int(count))
+
+
+PATHS = {"auto": _lib.MVK_PATH_AUTO, "valu": _lib.MVK_PATH_VALU, "mfma": _lib.MVK_PATH_MFMA}
+
+
+def server_eval(W: torch.Tensor, Xhat: torch.Tensor, out: torch.Tensor | None = None, stream=None,
+                path: str = "auto") -> torch.Tensor:
+    """Yhat = W Xhat mod p.  W: m x n int8; Xhat: B x n int32 field; returns B x m.
+
+    path selects the kernel family ("auto", "valu" or "mfma"); results are identical.
+    """
+    m, n = W.shape
+    B = Xhat.shape[0]
+    if out is None:
+        out = torch.empty((B, m), dtype=torch.int32, device=W.device)
+    L = _lib.load()
+    args = (_dev(W, torch.int8, (m, n), "W"), m, n, _dev(Xhat, torch.int32, (B, n), "Xhat"), B,
+            _dev(out, torch.int32, (B, m), "Yhat"))
+    if path == "auto":
+        _lib.check("mvk_server_eval", L.mvk_server_eval(*args, _stream(stream)))
+    else:
+        _lib.check("mvk_server_eval_path", L.mvk_server_eval_path(*args, PATHS[path], _stream(stream)))
+    return out
+
+
+def keygen(key: Key, W: torch.Tensor, stream=None) -> Key:
+    """Preprocess: fills key.PT = (W Gx)^T and key.Q = Gy^T W."""
+    _dev(W, torch.int8, (key.m, key.n), "W")
+    ks = key.struct()
+    _lib.check("mvk_keygen", _lib.load().mvk_keygen(ctypes.byref(ks), W.data_ptr(), _stream(stream)))
+    return key
+
+
+def encode(key: Key, X: torch.Tensor, ex_idx: torch.Tensor, ex_val: torch.Tensor,
+           out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Encrypt: Xhat_b = X_b + Gx e_b.  X: B x n; ex_idx/ex_val: B x t_x."""
+    B = X.shape[0]
+    if out is None:
+        out = torch.empty_like(X)
+    ks = key.struct()
+    ex = _sparse(ex_idx, ex_val, "ex")
+    _lib.check("mvk_encode", _lib.load().mvk_encode(
+        ctypes.byref(ks), _dev(X, torch.int32, (B, key.n), "X"), B, ctypes.byref(ex),
+        _dev(out, torch.int32, (B, key.n), "Xhat"), _stream(stream)))
+    return out
+
+
+def decode_verify(key: Key, Xhat: torch.Tensor, Yhat: torch.Tensor, ex_idx: torch.Tensor, ex_val: torch.Tensor,
+                  ey_idx: torch.Tensor, ey_val: torch.Tensor, Y: torch.Tensor | None = None,
+                  vL: torch.Tensor | None = None, vR: torch.Tensor | None = None,
+                  accept: torch.Tensor | None = None, stream=None):
+    """Verify + Decrypt.  Returns (Y, accept, vL, vR); accept is int32 0/1 per column."""
+    B = Xhat.shape[0]
+    ell = ey_idx.shape[0]
+    dev = Xhat.device
+    if Y is None:
+        Y = torch.empty((B, key.m), dtype=torch.int32, device=dev)
+    if accept is None:
+        accept = torch.empty((B,), dtype=torch.int32, device=dev)
+    ks = key.struct()
+    ex = _sparse(ex_idx, ex_val, "ex")
+    ey = _sparse(ey_idx, ey_val, "ey")
+    vLp = _dev(vL, torch.int32, (ell, B), "vL") if vL is not None else None
+    vRp = _dev(vR, torch.int32, (ell, B), "vR") if vR is not None else None
+    _lib.check("mvk_decode_verify", _lib.load().mvk_decode_verify(
+        ctypes.byref(ks), _dev(Xhat, torch.int32, (B, key.n), "Xhat"), _dev(Yhat, torch.int32, (B, key.m), "Yhat"),
+        B, ctypes.byref(ex), ctypes.byref(ey), _dev(Y, torch.int32, (B, key.m), "Y"), vLp, vRp,
+        _dev(accept, torch.int32, (B,), "accept"), _stream(stream)))
+    return Y, accept, vL, vR
+
+
+def raa_encode(code: Code, w: torch.Tensor, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """G^T w for each row of w (count x k) -> count x N."""
+    w2 = w if w.dim() == 2 else w.reshape(1, -1)
+    count = w2.shape[0]
+    if out is None:
+        out = torch.empty((count, code.N), dtype=torch.int32, device=w.device)
+    cs = code.struct()
+    _lib.check("mvk_raa_encode", _lib.load().mvk_raa_encode(
+        ctypes.byref(cs), _dev(w2, torch.int32, (count, code.k), "w"), count,
+        _dev(out, torch.int32, (count, code.N), "out"), _stream(stream)))
+    return out
+
+
+def raa_syndrome(code: Code, v: torch.Tensor, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """G v for each row of v (count x N) -> count x k."""
+    v2 = v if v.dim() == 2 else v.reshape(1, -1)
+    count = v2.shape[0]
+    if out is None:
+        out = torch.empty((count, code.k), dtype=torch.int32, device=v.device)
+    cs = code.struct()
+    _lib.check("mvk_raa_syndrome", _lib.load().mvk_raa_syndrome(
+        ctypes.byref(cs), _dev(v2, torch.int32, (count, code.N), "v"), count,
+        _dev(out, torch.int32, (count, code.k), "out"), _stream(stream)))
+    return out

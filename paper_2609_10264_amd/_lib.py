@@ -1,0 +1,115 @@
+"""ctypes loader and C struct layouts for libmvk.so (include/mvk.h)."""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmvk.so")
+
+MVK_OK = 0
+MVK_EINVAL = -1
+MVK_ERANGE = -2
+MVK_ENOMEM = -3
+MVK_EHIP = -4
+MVK_PRIME = 2147483647
+MVK_MAX_N = 131071
+MVK_PATH_AUTO = 0
+MVK_PATH_VALU = 1
+MVK_PATH_MFMA = 2
+ABI_VERSION = 1
+
+# Every symbol include/mvk.h declares.
+EXPORTS = (
+    "mvk_status_str",
+    "mvk_abi_version",
+    "mvk_server_eval",
+    "mvk_server_eval_path",
+    "mvk_keygen",
+    "mvk_encode",
+    "mvk_decode_verify",
+    "mvk_raa_encode",
+    "mvk_raa_syndrome",
+)
+
+
+class MvkCode(ctypes.Structure):
+    _fields_ = [
+        ("k", ctypes.c_uint32),
+        ("r", ctypes.c_uint32),
+        ("pi1", ctypes.c_void_p),
+        ("pi2", ctypes.c_void_p),
+        ("v1", ctypes.c_void_p),
+        ("v2", ctypes.c_void_p),
+    ]
+
+
+class MvkKey(ctypes.Structure):
+    _fields_ = [
+        ("m", ctypes.c_uint32),
+        ("n", ctypes.c_uint32),
+        ("cx", MvkCode),
+        ("cy", MvkCode),
+        ("PT", ctypes.c_void_p),
+        ("Q", ctypes.c_void_p),
+    ]
+
+
+class MvkSparse(ctypes.Structure):
+    _fields_ = [
+        ("idx", ctypes.c_void_p),
+        ("val", ctypes.c_void_p),
+        ("t", ctypes.c_uint32),
+        ("count", ctypes.c_uint32),
+    ]
+
+
+class MvkError(RuntimeError):
+    def __init__(self, fn: str, status: int, msg: str):
+        super().__init__(f"{fn} failed: {msg} (status {status})")
+        self.status = status
+
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load the built library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} not found: build it with `python -m paper_2609_10264_amd.build` "
+                          "(there is no fallback implementation)")
+    L = ctypes.CDLL(LIB_PATH)
+    st = ctypes.c_int32
+    vp = ctypes.c_void_p
+    u32 = ctypes.c_uint32
+    L.mvk_status_str.argtypes = [st]
+    L.mvk_status_str.restype = ctypes.c_char_p
+    L.mvk_abi_version.argtypes = []
+    L.mvk_abi_version.restype = ctypes.c_int32
+    L.mvk_server_eval.argtypes = [vp, u32, u32, vp, u32, vp, vp]
+    L.mvk_server_eval.restype = st
+    L.mvk_server_eval_path.argtypes = [vp, u32, u32, vp, u32, vp, ctypes.c_int32, vp]
+    L.mvk_server_eval_path.restype = st
+    L.mvk_keygen.argtypes = [ctypes.POINTER(MvkKey), vp, vp]
+    L.mvk_keygen.restype = st
+    L.mvk_encode.argtypes = [ctypes.POINTER(MvkKey), vp, u32, ctypes.POINTER(MvkSparse), vp, vp]
+    L.mvk_encode.restype = st
+    L.mvk_decode_verify.argtypes = [ctypes.POINTER(MvkKey), vp, vp, u32, ctypes.POINTER(MvkSparse),
+                                    ctypes.POINTER(MvkSparse), vp, vp, vp, vp, vp]
+    L.mvk_decode_verify.restype = st
+    L.mvk_raa_encode.argtypes = [ctypes.POINTER(MvkCode), vp, u32, vp, vp]
+    L.mvk_raa_encode.restype = st
+    L.mvk_raa_syndrome.argtypes = [ctypes.POINTER(MvkCode), vp, u32, vp, vp]
+    L.mvk_raa_syndrome.restype = st
+    if L.mvk_abi_version() != ABI_VERSION:
+        raise ImportError("libmvk.so ABI version mismatch; rebuild the library")
+    _lib = L
+    return L
+
+
+def check(fn: str, status: int) -> None:
+    if status != MVK_OK:
+        raise MvkError(fn, status, load().mvk_status_str(status).decode())

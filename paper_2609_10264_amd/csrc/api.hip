@@ -1,0 +1,210 @@
+// C ABI of the pvMVMD hot-path library (declared in include/mvk.h).
+//
+// This layer validates sizes, owns the per-(device, stream) workspace and
+// enqueues the kernels; all arithmetic happens in the kernels.
+#include <hip/hip_runtime.h>
+
+#include <map>
+#include <mutex>
+#include <utility>
+
+#include "mvk.h"
+#include "mvk_internal.h"
+
+namespace mvk {
+namespace {
+
+struct Workspace {
+    void* ptr = nullptr;
+    size_t size = 0;
+};
+
+std::mutex g_ws_mu;
+std::map<std::pair<int, hipStream_t>, Workspace>* g_ws = nullptr;
+
+// Returns a device buffer of at least `bytes` private to (current device, s).
+// Growing waits for the work already enqueued on `s` before freeing the old
+// buffer, so earlier calls on the same stream can still be using it.
+mvk_status workspace(hipStream_t s, size_t bytes, void** out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return MVK_EHIP;
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    if (!g_ws) g_ws = new std::map<std::pair<int, hipStream_t>, Workspace>();
+    Workspace& w = (*g_ws)[std::make_pair(dev, s)];
+    if (w.size < bytes) {
+        if (w.ptr) {
+            if (hipStreamSynchronize(s) != hipSuccess) return MVK_EHIP;
+            (void)hipFree(w.ptr);
+            w.ptr = nullptr;
+            w.size = 0;
+        }
+        size_t sz = bytes < ((size_t)1 << 20) ? ((size_t)1 << 20) : bytes;
+        sz = (sz + 4095) & ~(size_t)4095;
+        if (hipMalloc(&w.ptr, sz) != hipSuccess) {
+            (void)hipGetLastError();
+            w.ptr = nullptr;
+            return MVK_ENOMEM;
+        }
+        w.size = sz;
+    }
+    *out = w.ptr;
+    return MVK_OK;
+}
+
+inline mvk_status hip_status(hipError_t e) { return e == hipSuccess ? MVK_OK : MVK_EHIP; }
+
+inline size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+mvk_status check_code(const mvk_code* c, uint32_t k) {
+    if (!c || !c->pi1 || !c->pi2 || !c->v1 || !c->v2) return MVK_EINVAL;
+    if (c->k != k || c->r == 0 || k == 0) return MVK_EINVAL;
+    if ((uint64_t)c->k * c->r > 0x7fffffffull) return MVK_ERANGE;
+    return MVK_OK;
+}
+
+mvk_status check_key(const mvk_key* key) {
+    if (!key || key->m == 0 || key->n == 0) return MVK_EINVAL;
+    if (key->n > MVK_MAX_N) return MVK_ERANGE;
+    mvk_status st = check_code(&key->cx, key->n);
+    if (st) return st;
+    return check_code(&key->cy, key->m);
+}
+
+}  // namespace
+}  // namespace mvk
+
+using namespace mvk;
+
+extern "C" {
+
+const char* mvk_status_str(mvk_status s) {
+    switch (s) {
+        case MVK_OK: return "ok";
+        case MVK_EINVAL: return "invalid argument";
+        case MVK_ERANGE: return "size out of range";
+        case MVK_ENOMEM: return "out of device memory";
+        case MVK_EHIP: return "HIP runtime error";
+        default: return "unknown status";
+    }
+}
+
+int32_t mvk_abi_version(void) { return MVK_ABI_VERSION; }
+
+mvk_status mvk_server_eval(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* Xhat, uint32_t B,
+                           uint32_t* Yhat, void* stream) {
+    return mvk_server_eval_path(W, m, n, Xhat, B, Yhat, MVK_PATH_AUTO, stream);
+}
+
+mvk_status mvk_server_eval_path(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* Xhat, uint32_t B,
+                                uint32_t* Yhat, int32_t path, void* stream) {
+    if (path != MVK_PATH_AUTO && path != MVK_PATH_VALU && path != MVK_PATH_MFMA) return MVK_EINVAL;
+    if (m == 0 || B == 0) return MVK_OK;
+    if (!Yhat) return MVK_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    if (n == 0) return hip_status(launch_fill_u32(Yhat, (size_t)m * B, 0u, s));
+    if (!W || !Xhat) return MVK_EINVAL;
+    if (n > MVK_MAX_N) return MVK_ERANGE;
+    return hip_status(launch_server_eval(W, m, n, Xhat, B, Yhat, path, s));
+}
+
+mvk_status mvk_keygen(const mvk_key* key, const int8_t* W, void* stream) {
+    mvk_status st = check_key(key);
+    if (st) return st;
+    if (!W || !key->PT || !key->Q) return MVK_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    const uint32_t m = key->m, n = key->n;
+    const size_t Nx = (size_t)key->cx.r * n, Ny = (size_t)key->cy.r * m;
+    const size_t wt_bytes = align_up((size_t)m * n);
+    const size_t t3_bytes = (Nx * m > Ny * n ? Nx * m : Ny * n) * sizeof(uint32_t);
+    void* ws = nullptr;
+    st = workspace(s, wt_bytes + t3_bytes, &ws);
+    if (st) return st;
+    int8_t* WT = (int8_t*)ws;
+    uint32_t* t3 = (uint32_t*)((char*)ws + wt_bytes);
+    // P^T = Gx^T W^T: vector i is row i of W = column i of W^T (n positions).
+    hipError_t e = launch_transpose_i8(W, m, n, WT, s);
+    if (e == hipSuccess) e = launch_encT_i8(key->cx, WT, (size_t)m, 1, m, t3, key->PT, (size_t)m, 1, s);
+    // Q = Gy^T W: vector k is column k of W (m positions).
+    if (e == hipSuccess) e = launch_encT_i8(key->cy, W, (size_t)n, 1, n, t3, key->Q, (size_t)n, 1, s);
+    return hip_status(e);
+}
+
+mvk_status mvk_encode(const mvk_key* key, const uint32_t* X, uint32_t B, const mvk_sparse* ex, uint32_t* Xhat,
+                      void* stream) {
+    mvk_status st = check_key(key);
+    if (st) return st;
+    if (B == 0) return MVK_OK;
+    if (!X || !Xhat || !ex || ex->count != B || (ex->t && (!ex->idx || !ex->val))) return MVK_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    const size_t Nx = (size_t)key->cx.r * key->n;
+    if (ex->t > Nx) return MVK_EINVAL;
+    void* ws = nullptr;
+    st = workspace(s, (size_t)B * 2 * Nx * sizeof(uint32_t), &ws);
+    if (st) return st;
+    return hip_status(launch_syn_sparse(key->cx, ex->idx, ex->val, ex->t, B, X, (uint32_t*)ws, Xhat, s));
+}
+
+mvk_status mvk_decode_verify(const mvk_key* key, const uint32_t* Xhat, const uint32_t* Yhat, uint32_t B,
+                             const mvk_sparse* ex, const mvk_sparse* ey, uint32_t* Y, uint32_t* vL, uint32_t* vR,
+                             uint32_t* accept, void* stream) {
+    mvk_status st = check_key(key);
+    if (st) return st;
+    if (B == 0) return MVK_OK;
+    if (!key->PT || !key->Q || !Xhat || !Yhat || !Y || !accept || !ex || !ey) return MVK_EINVAL;
+    if (ex->count != B || (ex->t && (!ex->idx || !ex->val))) return MVK_EINVAL;
+    if (ey->count == 0 || ey->t == 0 || !ey->idx || !ey->val) return MVK_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    const uint32_t m = key->m, n = key->n, ell = ey->count;
+    const uint32_t Nx = key->cx.r * n, Ny = key->cy.r * m;
+    if (ex->t > Nx || ey->t > Ny) return MVK_EINVAL;
+    const uint32_t nblkR = ceil_div(m, kClientCols), nblkL = ceil_div(n, kClientCols);
+    const size_t r_bytes = align_up((size_t)ell * m * 4);
+    const size_t syn_bytes = align_up((size_t)ell * 2 * Ny * 4);
+    const size_t pl_bytes = align_up((size_t)ell * B * nblkL * 4);
+    const size_t pr_bytes = align_up((size_t)ell * B * nblkR * 4);
+    void* ws = nullptr;
+    st = workspace(s, r_bytes + syn_bytes + pl_bytes + pr_bytes, &ws);
+    if (st) return st;
+    char* base = (char*)ws;
+    uint32_t* rv = (uint32_t*)base;
+    uint32_t* syn_scratch = (uint32_t*)(base + r_bytes);
+    uint32_t* partL = (uint32_t*)(base + r_bytes + syn_bytes);
+    uint32_t* partR = (uint32_t*)(base + r_bytes + syn_bytes + pl_bytes);
+    // r_q = Gy e_q for every repetition (shared by all columns)
+    hipError_t e = launch_syn_sparse(key->cy, ey->idx, ey->val, ey->t, ell, nullptr, syn_scratch, rv, s);
+    if (e == hipSuccess)
+        e = launch_decode_vr(key->PT, m, Nx, Yhat, B, ex->idx, ex->val, ex->t, rv, ell, Y, partR, s);
+    if (e == hipSuccess) e = launch_verify_vl(key->Q, n, Ny, Xhat, B, ey->idx, ey->val, ey->t, ell, partL, s);
+    if (e == hipSuccess) e = launch_verify_finalize(partL, nblkL, partR, nblkR, B, ell, vL, vR, accept, s);
+    return hip_status(e);
+}
+
+mvk_status mvk_raa_encode(const mvk_code* code, const uint32_t* w, uint32_t count, uint32_t* out, void* stream) {
+    if (!code) return MVK_EINVAL;
+    mvk_status st = check_code(code, code->k);
+    if (st) return st;
+    if (count == 0) return MVK_OK;
+    if (!w || !out) return MVK_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    const size_t N = (size_t)code->k * code->r;
+    void* ws = nullptr;
+    st = workspace(s, N * count * sizeof(uint32_t), &ws);
+    if (st) return st;
+    return hip_status(launch_encT_u32(*code, w, 1, code->k, count, (uint32_t*)ws, out, 1, N, s));
+}
+
+mvk_status mvk_raa_syndrome(const mvk_code* code, const uint32_t* v, uint32_t count, uint32_t* out, void* stream) {
+    if (!code) return MVK_EINVAL;
+    mvk_status st = check_code(code, code->k);
+    if (st) return st;
+    if (count == 0) return MVK_OK;
+    if (!v || !out) return MVK_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    const size_t N = (size_t)code->k * code->r;
+    void* ws = nullptr;
+    st = workspace(s, (size_t)count * 2 * N * sizeof(uint32_t), &ws);
+    if (st) return st;
+    return hip_status(launch_syn_dense(*code, v, count, (uint32_t*)ws, out, s));
+}
+
+}  // extern "C"

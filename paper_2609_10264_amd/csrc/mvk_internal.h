@@ -1,0 +1,54 @@
+// Internal launch interface between the C-ABI layer (api.hip) and the kernel
+// translation units.  Every launcher only enqueues work on `s` and returns the
+// status of hipGetLastError().
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "mvk.h"
+
+namespace mvk {
+
+// server_eval.hip
+hipError_t launch_server_eval(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t B,
+                              uint32_t* Y, int path, hipStream_t s);
+
+// raa.hip -------------------------------------------------------------------
+// G^T applied to `nvec` vectors whose element i of vector v sits at
+// in[i*ld_in + v*vs_in]; result element j of vector v goes to
+// out[j*ld_out + v*vs_out].  t3: scratch of N*nvec uint32 (N = r*k).
+hipError_t launch_encT_u32(const mvk_code& c, const uint32_t* in, size_t ld_in, size_t vs_in, uint32_t nvec,
+                           uint32_t* t3, uint32_t* out, size_t ld_out, size_t vs_out, hipStream_t s);
+hipError_t launch_encT_i8(const mvk_code& c, const int8_t* in, size_t ld_in, size_t vs_in, uint32_t nvec,
+                          uint32_t* t3, uint32_t* out, size_t ld_out, size_t vs_out, hipStream_t s);
+// G v for `count` vectors: dense (v: count x N) or sparse (idx/val: count x t).
+// If X != nullptr the result is added to X (out = X + G v), as in Encrypt.
+// scratch: count * 2N uint32.
+hipError_t launch_syn_dense(const mvk_code& c, const uint32_t* v, uint32_t count, uint32_t* scratch,
+                            uint32_t* out, hipStream_t s);
+hipError_t launch_syn_sparse(const mvk_code& c, const uint32_t* idx, const uint32_t* val, uint32_t t,
+                             uint32_t count, const uint32_t* X, uint32_t* scratch, uint32_t* out,
+                             hipStream_t s);
+// W (m x n int8) -> WT (n x m int8)
+hipError_t launch_transpose_i8(const int8_t* W, uint32_t m, uint32_t n, int8_t* WT, hipStream_t s);
+hipError_t launch_fill_u32(uint32_t* p, size_t count, uint32_t value, hipStream_t s);
+
+// client.hip ----------------------------------------------------------------
+constexpr uint32_t kClientBlock = 256;  // threads per workgroup of the gather kernels
+constexpr uint32_t kClientCols = 64;    // output columns per workgroup of the gather kernels
+// Decrypt plus per-block partial sums of r_q . Yhat_b (r: ell x m).
+hipError_t launch_decode_vr(const uint32_t* PT, uint32_t m, uint32_t Nx, const uint32_t* Yhat, uint32_t B,
+                            const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx, const uint32_t* r,
+                            uint32_t ell, uint32_t* Y, uint32_t* partR, hipStream_t s);
+// u_q = e_q^T Q and per-block partial sums of u_q . Xhat_b.
+hipError_t launch_verify_vl(const uint32_t* Q, uint32_t n, uint32_t Ny, const uint32_t* Xhat, uint32_t B,
+                            const uint32_t* ey_idx, const uint32_t* ey_val, uint32_t ty, uint32_t ell,
+                            uint32_t* partL, hipStream_t s);
+hipError_t launch_verify_finalize(const uint32_t* partL, uint32_t nblkL, const uint32_t* partR, uint32_t nblkR,
+                                  uint32_t B, uint32_t ell, uint32_t* vL, uint32_t* vR, uint32_t* accept,
+                                  hipStream_t s);
+
+inline uint32_t ceil_div(uint32_t a, uint32_t b) { return (a + b - 1) / b; }
+
+}  // namespace mvk

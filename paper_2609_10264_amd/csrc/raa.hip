@@ -1,0 +1,277 @@
+// RAA code maps (App. B) on gfx950.
+//
+//   encoding  G^T w = A^T V2 Pi2^T A^T V1 Pi1^T R^T w   (repeat, gather by pi1,
+//             scale, prefix sum, gather by pi2, scale, prefix sum)
+//   syndrome  G v   = R Pi1 V1 A Pi2 V2 A v             (suffix sum, scale,
+//             scatter by pi2, suffix sum, scale, scatter by pi1, fold r)
+//
+// Two kernel shapes:
+//  * encT_lanes: many vectors at once (Preprocess encodes every row and every
+//    column of W).  One lane owns one vector and walks its N positions in order,
+//    so each prefix sum is a plain running sum per lane and every access to the
+//    batch (vector index innermost) is a coalesced 64-lane row.  The code arrays
+//    are indexed by the position only, which is uniform across the wave, so they
+//    come through scalar loads.
+//  * syn_block: few vectors (Encrypt: one per query column; Verify: one per
+//    repetition).  One 1024-thread workgroup owns one vector and runs the two
+//    suffix sums as tiled block scans.
+#include "field.h"
+#include "mvk_internal.h"
+
+namespace mvk {
+
+namespace {
+
+__device__ __forceinline__ uint32_t load_elem(const uint32_t* p, size_t i) { return p[i]; }
+__device__ __forceinline__ uint32_t load_elem(const int8_t* p, size_t i) { return femb(p[i]); }
+
+template <int RR>
+__device__ __forceinline__ uint32_t div_r(uint32_t x, uint32_t r) {
+    if constexpr (RR > 0)
+        return x / RR;
+    else
+        return x / r;
+}
+
+template <typename T, int RR>
+__global__ __launch_bounds__(64) void encT_lanes(uint32_t k, uint32_t r, const uint32_t* __restrict__ pi1,
+                                                 const uint32_t* __restrict__ pi2,
+                                                 const uint32_t* __restrict__ v1,
+                                                 const uint32_t* __restrict__ v2, const T* __restrict__ in,
+                                                 size_t ld_in, size_t vs_in, uint32_t nvec,
+                                                 uint32_t* __restrict__ t3, uint32_t* __restrict__ out,
+                                                 size_t ld_out, size_t vs_out) {
+    const uint32_t v = blockIdx.x * 64 + threadIdx.x;
+    const bool act = v < nvec;
+    const uint32_t N = k * (RR ? RR : r);
+    const T* src = in + (size_t)(act ? v : 0) * vs_in;
+    uint32_t* tcol = t3 + (size_t)(act ? v : 0);
+    const size_t ldt = nvec;
+    // pass 1: a = prefix(v1 .* (Pi1^T R^T w))
+    uint32_t s = 0;
+#pragma unroll 8
+    for (uint32_t j = 0; j < N; ++j) {
+        uint32_t pj = pi1[j];
+        if (pj >= N) pj = N - 1;
+        const uint32_t i = div_r<RR>(pj, r);
+        const uint32_t x = act ? load_elem(src, (size_t)i * ld_in) : 0u;
+        s = fadd(s, fmul(v1[j], x));
+        if (act) tcol[(size_t)j * ldt] = s;
+    }
+    // pass 2: out = prefix(v2 .* (Pi2^T a))
+    uint32_t* dst = out + (size_t)(act ? v : 0) * vs_out;
+    s = 0;
+#pragma unroll 8
+    for (uint32_t j = 0; j < N; ++j) {
+        uint32_t pj = pi2[j];
+        if (pj >= N) pj = N - 1;
+        const uint32_t a = act ? tcol[(size_t)pj * ldt] : 0u;
+        s = fadd(s, fmul(v2[j], a));
+        if (act) dst[(size_t)j * ld_out] = s;
+    }
+}
+
+template <typename T>
+hipError_t launch_encT(const mvk_code& c, const T* in, size_t ld_in, size_t vs_in, uint32_t nvec, uint32_t* t3,
+                       uint32_t* out, size_t ld_out, size_t vs_out, hipStream_t s) {
+    if (nvec == 0) return hipSuccess;
+    const dim3 grid(ceil_div(nvec, 64)), block(64);
+#define MVK_ENC(RRV)                                                                                         \
+    hipLaunchKernelGGL((encT_lanes<T, RRV>), grid, block, 0, s, c.k, c.r, c.pi1, c.pi2, c.v1, c.v2, in, ld_in, \
+                       vs_in, nvec, t3, out, ld_out, vs_out)
+    switch (c.r) {
+        case 1: MVK_ENC(1); break;
+        case 2: MVK_ENC(2); break;
+        case 3: MVK_ENC(3); break;
+        case 4: MVK_ENC(4); break;
+        case 8: MVK_ENC(8); break;
+        default: MVK_ENC(0); break;
+    }
+#undef MVK_ENC
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Block scan (1024 threads, 4 consecutive elements per thread per tile).
+// ---------------------------------------------------------------------------
+constexpr int kSynThreads = 1024;
+constexpr int kSynWaves = kSynThreads / 64;
+
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x, int lane) {
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const uint32_t y = (uint32_t)__shfl_up((int)x, d);
+        if (lane >= d) x = fadd(x, y);
+    }
+    return x;
+}
+
+// Inclusive scan of a[0..N) in place; SUFFIX scans from the end.
+template <bool SUFFIX>
+__device__ void block_scan(uint32_t* a, uint32_t N, uint32_t* wsum /* kSynWaves + 1 */) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    uint32_t carry = 0;
+    for (uint32_t base = 0; base < N; base += 4 * kSynThreads) {
+        uint32_t x[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const uint32_t sidx = base + 4 * tid + e;
+            x[e] = sidx < N ? a[SUFFIX ? N - 1 - sidx : sidx] : 0u;
+        }
+        x[1] = fadd(x[1], x[0]);
+        x[2] = fadd(x[2], x[1]);
+        x[3] = fadd(x[3], x[2]);
+        const uint32_t incl = wave_incl_scan(x[3], lane);
+        if (lane == 63) wsum[wave] = incl;
+        __syncthreads();
+        uint32_t t = 0, ti = 0;
+        if (wave == 0) {
+            t = lane < kSynWaves ? wsum[lane] : 0u;
+            ti = wave_incl_scan(t, lane);
+        }
+        __syncthreads();
+        if (wave == 0) {
+            if (lane < kSynWaves) wsum[lane] = fsub(ti, t);  // exclusive offset of each wave
+            if (lane == kSynWaves - 1) wsum[kSynWaves] = ti;  // tile total
+        }
+        __syncthreads();
+        const uint32_t off = fadd(carry, fadd(wsum[wave], fsub(incl, x[3])));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const uint32_t sidx = base + 4 * tid + e;
+            if (sidx < N) a[SUFFIX ? N - 1 - sidx : sidx] = fadd(x[e], off);
+        }
+        carry = fadd(carry, wsum[kSynWaves]);
+        __syncthreads();
+    }
+}
+
+// Largest block length kept entirely in LDS (two arrays of N words).
+constexpr uint32_t kSynLdsN = 20224;
+
+// One workgroup per vector.  LDS_RES: both length-N work arrays live in LDS;
+// otherwise they live in the global scratch (count x 2N words).
+template <bool SPARSE, bool LDS_RES>
+__global__ __launch_bounds__(kSynThreads) void syn_block(uint32_t k, uint32_t r, const uint32_t* __restrict__ pi1,
+                                                         const uint32_t* __restrict__ pi2,
+                                                         const uint32_t* __restrict__ v1,
+                                                         const uint32_t* __restrict__ v2,
+                                                         const uint32_t* __restrict__ vin,
+                                                         const uint32_t* __restrict__ idx,
+                                                         const uint32_t* __restrict__ val, uint32_t t,
+                                                         const uint32_t* __restrict__ X, uint32_t* scratch,
+                                                         uint32_t* __restrict__ out) {
+    __shared__ uint32_t wsum[kSynWaves + 1];
+    __shared__ uint32_t lds[LDS_RES ? 2 * kSynLdsN : 1];
+    const uint32_t c = blockIdx.x;
+    const int tid = threadIdx.x;
+    const uint32_t N = k * r;
+    uint32_t* a = LDS_RES ? lds : scratch + (size_t)c * 2 * N;
+    uint32_t* b = a + N;
+    if (SPARSE) {
+        for (uint32_t j = tid; j < N; j += kSynThreads) a[j] = 0u;
+        __syncthreads();
+        for (uint32_t q = tid; q < t; q += kSynThreads) {
+            uint32_t j = idx[(size_t)c * t + q];
+            if (j >= N) j = N - 1;
+            a[j] = val[(size_t)c * t + q];
+        }
+    } else {
+        const uint32_t* src = vin + (size_t)c * N;
+        for (uint32_t j = tid; j < N; j += kSynThreads) a[j] = src[j];
+    }
+    __syncthreads();
+    block_scan<true>(a, N, wsum);  // A
+    for (uint32_t j = tid; j < N; j += kSynThreads) {
+        uint32_t pj = pi2[j];
+        if (pj >= N) pj = N - 1;
+        b[pj] = fmul(v2[j], a[j]);  // V2, then Pi2 scatter
+    }
+    __syncthreads();
+    block_scan<true>(b, N, wsum);  // A
+    for (uint32_t j = tid; j < N; j += kSynThreads) {
+        uint32_t pj = pi1[j];
+        if (pj >= N) pj = N - 1;
+        a[pj] = fmul(v1[j], b[j]);  // V1, then Pi1 scatter
+    }
+    __syncthreads();
+    for (uint32_t i = tid; i < k; i += kSynThreads) {  // R: fold blocks of r
+        uint32_t s = 0;
+        for (uint32_t q = 0; q < r; ++q) s = fadd(s, a[(size_t)i * r + q]);
+        if (X) s = fadd(X[(size_t)c * k + i], s);
+        out[(size_t)c * k + i] = s;
+    }
+}
+
+__global__ __launch_bounds__(256) void transpose_i8(const int8_t* __restrict__ W, uint32_t m, uint32_t n,
+                                                    int8_t* __restrict__ WT) {
+    __shared__ int8_t tile[64][65];
+    const uint32_t r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    for (int i = ty; i < 64; i += 4) {
+        const uint32_t r = r0 + i, c = c0 + tx;
+        tile[i][tx] = (r < m && c < n) ? W[(size_t)r * n + c] : (int8_t)0;
+    }
+    __syncthreads();
+    for (int i = ty; i < 64; i += 4) {
+        const uint32_t c = c0 + i, r = r0 + tx;  // WT[c][r] = W[r][c]
+        if (c < n && r < m) WT[(size_t)c * m + r] = tile[tx][i];
+    }
+}
+
+__global__ void fill_u32(uint32_t* p, size_t count, uint32_t value) {
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += (size_t)gridDim.x * blockDim.x)
+        p[i] = value;
+}
+
+}  // namespace
+
+hipError_t launch_encT_u32(const mvk_code& c, const uint32_t* in, size_t ld_in, size_t vs_in, uint32_t nvec,
+                           uint32_t* t3, uint32_t* out, size_t ld_out, size_t vs_out, hipStream_t s) {
+    return launch_encT<uint32_t>(c, in, ld_in, vs_in, nvec, t3, out, ld_out, vs_out, s);
+}
+
+hipError_t launch_encT_i8(const mvk_code& c, const int8_t* in, size_t ld_in, size_t vs_in, uint32_t nvec,
+                          uint32_t* t3, uint32_t* out, size_t ld_out, size_t vs_out, hipStream_t s) {
+    return launch_encT<int8_t>(c, in, ld_in, vs_in, nvec, t3, out, ld_out, vs_out, s);
+}
+
+hipError_t launch_syn_dense(const mvk_code& c, const uint32_t* v, uint32_t count, uint32_t* scratch, uint32_t* out,
+                            hipStream_t s) {
+    if (count == 0) return hipSuccess;
+    if ((size_t)c.k * c.r <= kSynLdsN)
+        hipLaunchKernelGGL((syn_block<false, true>), dim3(count), dim3(kSynThreads), 0, s, c.k, c.r, c.pi1, c.pi2,
+                           c.v1, c.v2, v, nullptr, nullptr, 0u, nullptr, scratch, out);
+    else
+        hipLaunchKernelGGL((syn_block<false, false>), dim3(count), dim3(kSynThreads), 0, s, c.k, c.r, c.pi1, c.pi2,
+                           c.v1, c.v2, v, nullptr, nullptr, 0u, nullptr, scratch, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_syn_sparse(const mvk_code& c, const uint32_t* idx, const uint32_t* val, uint32_t t,
+                             uint32_t count, const uint32_t* X, uint32_t* scratch, uint32_t* out, hipStream_t s) {
+    if (count == 0) return hipSuccess;
+    if ((size_t)c.k * c.r <= kSynLdsN)
+        hipLaunchKernelGGL((syn_block<true, true>), dim3(count), dim3(kSynThreads), 0, s, c.k, c.r, c.pi1, c.pi2,
+                           c.v1, c.v2, nullptr, idx, val, t, X, scratch, out);
+    else
+        hipLaunchKernelGGL((syn_block<true, false>), dim3(count), dim3(kSynThreads), 0, s, c.k, c.r, c.pi1, c.pi2,
+                           c.v1, c.v2, nullptr, idx, val, t, X, scratch, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_transpose_i8(const int8_t* W, uint32_t m, uint32_t n, int8_t* WT, hipStream_t s) {
+    if (m == 0 || n == 0) return hipSuccess;
+    hipLaunchKernelGGL(transpose_i8, dim3(ceil_div(n, 64), ceil_div(m, 64)), dim3(256), 0, s, W, m, n, WT);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_u32(uint32_t* p, size_t count, uint32_t value, hipStream_t s) {
+    if (count == 0) return hipSuccess;
+    size_t blocks = (count + 255) / 256;
+    if (blocks > 4096) blocks = 4096;
+    hipLaunchKernelGGL(fill_u32, dim3((uint32_t)blocks), dim3(256), 0, s, p, count, value);
+    return hipGetLastError();
+}
+
+}  // namespace mvk

@@ -1,0 +1,76 @@
+"""The C-ABI library loads and exports every symbol include/mvk.h declares;
+host-side argument checks (no device work is enqueued on these paths)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mvk.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mvk_[a-z0-9_]+)\s*\(", text)))
+
+
+def _lib():
+    from paper_2609_10264_amd import _lib as L
+    if not os.path.exists(L.LIB_PATH):
+        pytest.skip("libmvk.so not built (run __graft_entry__.build())")
+    return L
+
+
+def test_header_declares_expected_calls():
+    names = _declared()
+    for fn in ("mvk_server_eval", "mvk_keygen", "mvk_encode", "mvk_decode_verify"):
+        assert fn in names
+
+
+def test_library_exports_every_declared_symbol():
+    L = _lib()
+    lib = ctypes.CDLL(L.LIB_PATH)
+    missing = [n for n in _declared() if not hasattr(lib, n)]
+    assert not missing, missing
+    assert sorted(L.EXPORTS) == _declared()
+
+
+def test_abi_version_and_status_strings():
+    L = _lib()
+    lib = L.load()
+    assert lib.mvk_abi_version() == L.ABI_VERSION
+    assert lib.mvk_status_str(0) == b"ok"
+    assert lib.mvk_status_str(L.MVK_ERANGE) == b"size out of range"
+    assert lib.mvk_status_str(12345) == b"unknown status"
+
+
+def test_struct_layouts_match_header():
+    L = _lib()
+    # two uint32 then four pointers
+    assert ctypes.sizeof(L.MvkCode) == 8 + 4 * 8
+    assert ctypes.sizeof(L.MvkKey) == 8 + 2 * ctypes.sizeof(L.MvkCode) + 16
+    assert ctypes.sizeof(L.MvkSparse) == 16 + 8
+
+
+def test_host_argument_checks_without_device_work():
+    L = _lib()
+    lib = L.load()
+    fake = ctypes.c_void_p(0x1000)
+    # empty problems are no-ops
+    assert lib.mvk_server_eval(None, 0, 16, None, 1, None, None) == L.MVK_OK
+    assert lib.mvk_server_eval(None, 16, 16, None, 0, None, None) == L.MVK_OK
+    # missing output
+    assert lib.mvk_server_eval(fake, 4, 16, fake, 1, None, None) == L.MVK_EINVAL
+    # n beyond the int32 exactness bound of the limb accumulation
+    assert lib.mvk_server_eval(fake, 4, L.MVK_MAX_N + 1, fake, 1, fake, None) == L.MVK_ERANGE
+    # inconsistent key: code dimension must equal n / m
+    code = L.MvkCode(5, 3, 0x1000, 0x1000, 0x1000, 0x1000)
+    key = L.MvkKey(8, 8, code, code, 0x1000, 0x1000)
+    assert lib.mvk_keygen(ctypes.byref(key), fake, None) == L.MVK_EINVAL
+    assert lib.mvk_keygen(None, fake, None) == L.MVK_EINVAL
+    bad = L.MvkCode(8, 0, 0x1000, 0x1000, 0x1000, 0x1000)
+    assert lib.mvk_raa_encode(ctypes.byref(bad), fake, 1, fake, None) == L.MVK_EINVAL
+    nullcode = L.MvkCode(8, 2, 0, 0x1000, 0x1000, 0x1000)
+    assert lib.mvk_raa_syndrome(ctypes.byref(nullcode), fake, 1, fake, None) == L.MVK_EINVAL

@@ -1,0 +1,255 @@
+"""GPU parity: every call of the C ABI against the CPU oracle, bit-exact.
+
+All arithmetic is integer mod p, so every comparison is exact equality.
+Sizes span several workgroup tiles with ragged tails; the full-size LLM-layer
+shapes compare either the whole output or oracle-computable samples.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from tests.gpu_util import Instance, code, dev, host
+
+pytestmark = pytest.mark.gpu
+P = synth.P
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_10264_amd as mvk  # noqa: F401  (raises if libmvk.so is missing)
+    mvk._lib.load()
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+import paper_2609_10264_amd as mvk  # noqa: E402
+
+
+# ---------------------------------------------------------------------------
+# server_eval
+# ---------------------------------------------------------------------------
+SERVER_SHAPES = [
+    (1, 1, 1), (3, 5, 1), (17, 33, 2), (256, 256, 1), (257, 4099, 1), (64, 4096, 3), (16, 8192, 1),
+    (100, 160, 5), (300, 1000, 16), (31, 2048, 64), (4096, 4096, 1), (33, 12345, 4), (50, 4112, 7),
+]
+
+
+PATHS = ["auto", "valu", "mfma"]
+
+
+@pytest.mark.parametrize("path", PATHS)
+@pytest.mark.parametrize("m,n,B", SERVER_SHAPES)
+def test_server_eval_matches_oracle(m, n, B, path):
+    _say(f"server_eval m={m} n={n} B={B} path={path}")
+    W = synth.weights(11 * m + n, m, n, lo=-128, hi=127)
+    X = synth.field_uniform(13 * n + B, (B, n))
+    got = host(mvk.server_eval(dev(W), dev(X), path=path))
+    assert np.array_equal(got, oracle.server_eval(W, X))
+
+
+@pytest.mark.parametrize("path", ["valu", "mfma"])
+@pytest.mark.parametrize("wv,xv", [(-128, P - 8421504), (127, P - 1), (-127, P - 1), (-128, 1073741823),
+                                   (127, 1073741824), (-1, 0)])
+def test_server_eval_extremes(wv, xv, path):
+    # n at the exactness limit: every digit-plane sum reaches n * 128 * 128 - 1 < 2^31
+    m, n = 5, mvk.MVK_MAX_N
+    _say(f"server_eval extreme w={wv} x={xv} n={n} path={path}")
+    W = np.full((m, n), wv, dtype=np.int8)
+    X = np.full((2, n), xv, dtype=np.uint32)
+    X[1, ::3] = 0
+    got = host(mvk.server_eval(dev(W), dev(X), path=path))
+    assert np.array_equal(got, oracle.server_eval(W, X))
+
+
+def test_server_eval_empty_and_limits():
+    W = dev(synth.weights(1, 8, 0))
+    X = torch.zeros((2, 0), dtype=torch.int32, device="cuda")
+    Y = mvk.server_eval(W, X, out=torch.full((2, 8), 7, dtype=torch.int32, device="cuda"))
+    assert not Y.any()  # empty sum
+    Y0 = torch.full((0, 8), 7, dtype=torch.int32, device="cuda")
+    mvk.server_eval(dev(synth.weights(1, 8, 4)), torch.zeros((0, 4), dtype=torch.int32, device="cuda"), out=Y0)
+    with pytest.raises(mvk.MvkError):
+        mvk.server_eval(torch.zeros((2, mvk.MVK_MAX_N + 1), dtype=torch.int8, device="cuda"),
+                        torch.zeros((1, mvk.MVK_MAX_N + 1), dtype=torch.int32, device="cuda"))
+
+
+def test_server_eval_closed_forms():
+    n = 1000
+    X = synth.field_uniform(5, (3, n))
+    I = np.eye(n, dtype=np.int8)
+    assert np.array_equal(host(mvk.server_eval(dev(I), dev(X))), X)
+    M = np.full((7, n), -1, dtype=np.int8)
+    want = np.array([[(-sum(int(v) for v in x)) % P] * 7 for x in X], dtype=np.uint32)
+    assert np.array_equal(host(mvk.server_eval(dev(M), dev(X))), want)
+
+
+def test_server_eval_repeatable_and_noncontiguous_offsets():
+    # outputs written at an offset inside a larger buffer; repeated runs are bitwise equal
+    m, n, B = 130, 520, 3
+    W = synth.weights(21, m, n)
+    X = synth.field_uniform(22, (B, n))
+    big = torch.zeros((B * m + 64,), dtype=torch.int32, device="cuda")
+    out = big[64:].view(B, m)
+    a = host(mvk.server_eval(dev(W), dev(X), out=out))
+    b = host(mvk.server_eval(dev(W), dev(X)))
+    assert np.array_equal(a, b) and np.array_equal(a, oracle.server_eval(W, X))
+    assert not big[:64].any()
+
+
+# ---------------------------------------------------------------------------
+# RAA encoding / syndrome
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("k,r,count", [(1, 1, 1), (5, 2, 3), (256, 2, 2), (1000, 3, 4), (4097, 4, 2), (700, 5, 65),
+                                         (6000, 4, 2), (5056, 4, 1)])
+def test_raa_encode_and_syndrome(k, r, count):
+    _say(f"raa k={k} r={r} count={count}")
+    c = synth.raa_code(300 + k + r, k, r)
+    w = synth.field_uniform(301 + k, (count, k))
+    v = synth.field_uniform(302 + k, (count, k * r))
+    dc = code(c)
+    got_e = host(mvk.raa_encode(dc, dev(w)))
+    got_s = host(mvk.raa_syndrome(dc, dev(v)))
+    for i in range(count):
+        assert np.array_equal(got_e[i], oracle.encT(c, w[i]))
+        assert np.array_equal(got_s[i], oracle.syn(c, v[i]))
+
+
+def test_raa_identity_closed_form():
+    N = 5000
+    c = synth.identity_code(N, 1)
+    e0 = np.zeros((1, N), dtype=np.uint32)
+    e0[0, 0] = 1
+    assert host(mvk.raa_encode(code(c), dev(e0)))[0].tolist() == list(range(1, N + 1))
+    assert host(mvk.raa_syndrome(code(c), dev(e0[:, ::-1].copy())))[0].tolist() == [N - i for i in range(N)]
+
+
+# ---------------------------------------------------------------------------
+# keygen / encode / decode_verify on small and ragged shapes
+# ---------------------------------------------------------------------------
+SMALL = [  # cid, m, n, B, r, tx
+    (0, 256, 256, 1, 2, 8),
+    (50, 257, 130, 3, 3, 5),
+    (51, 64, 1000, 2, 4, 17),
+    (52, 1000, 64, 5, 1, 3),
+]
+
+
+@pytest.mark.parametrize("cid,m,n,B,r,tx", SMALL)
+def test_protocol_small(cid, m, n, B, r, tx):
+    _say(f"protocol cid={cid} m={m} n={n} B={B} r={r} tx={tx}")
+    inst = Instance(cid, m, n, B, r, tx).to_device()
+    mvk.keygen(inst.key, inst.dW)
+    PT, Q = oracle.keygen(inst.W, inst.cx, inst.cy)
+    assert np.array_equal(host(inst.key.PT), PT)
+    assert np.array_equal(host(inst.key.Q), Q)
+    dXh = mvk.encode(inst.key, inst.dX, inst.dexi, inst.dexv)
+    Xh = oracle.encode(inst.cx, inst.X, inst.exi, inst.exv)
+    assert np.array_equal(host(dXh), Xh)
+    dYh = mvk.server_eval(inst.dW, dXh)
+    Yh = oracle.server_eval(inst.W, Xh)
+    assert np.array_equal(host(dYh), Yh)
+    ell = inst.eyi.shape[0]
+    vL = torch.empty((ell, B), dtype=torch.int32, device="cuda")
+    vR = torch.empty_like(vL)
+    Y, acc, vL, vR = mvk.decode_verify(inst.key, dXh, dYh, inst.dexi, inst.dexv, inst.deyi, inst.deyv, vL=vL, vR=vR)
+    oacc, ovL, ovR = oracle.verify(inst.cy, Q, Xh, Yh, inst.eyi, inst.eyv)
+    assert np.array_equal(host(vL), ovL) and np.array_equal(host(vR), ovR)
+    assert host(acc).tolist() == oacc.astype(np.uint32).tolist() == [1] * B
+    assert np.array_equal(host(Y), oracle.decode(PT, Yh, inst.exi, inst.exv))
+    assert np.array_equal(host(Y), oracle.server_eval(inst.W, inst.X))
+
+    # tampered responses: one changed coordinate per column in turn
+    pos, delta = synth.tamper_delta(synth.seed_for(cid, synth.PURPOSE_TAMPER), B, m)
+    for b in range(B):
+        bad = Yh.copy()
+        bad[b, pos[b]] = (int(bad[b, pos[b]]) + int(delta[b])) % P
+        Yb, accb, vLb, vRb = mvk.decode_verify(inst.key, dXh, dev(bad), inst.dexi, inst.dexv, inst.deyi, inst.deyv,
+                                               vL=vL, vR=vR)
+        oacc, ovL, ovR = oracle.verify(inst.cy, Q, Xh, bad, inst.eyi, inst.eyv)
+        assert host(accb).tolist() == oacc.astype(np.uint32).tolist()
+        assert not oacc[b]
+        assert np.array_equal(host(vLb), ovL) and np.array_equal(host(vRb), ovR)
+        assert np.array_equal(host(Yb), oracle.decode(PT, bad, inst.exi, inst.exv))
+
+
+def test_encode_without_noise_is_identity():
+    inst = Instance(60, 40, 50, 2, 3, 0).to_device()
+    empty = torch.zeros((2, 0), dtype=torch.int32, device="cuda")
+    Xh = mvk.encode(inst.key, inst.dX, empty, empty)
+    assert np.array_equal(host(Xh), inst.X)
+
+
+# ---------------------------------------------------------------------------
+# LLM-layer shapes at full size
+# ---------------------------------------------------------------------------
+def test_attn4096_full():
+    """4096 x 4096, one query column, r = 3, t_x = 64: whole outputs compared."""
+    cfg = synth.CONFIGS["attn4096"]
+    _say("attn4096 full compare")
+    inst = Instance(cfg["cid"], cfg["m"], cfg["n"], cfg["B"], cfg["r"], cfg["tx"], cfg["ty"], cfg["ell"]).to_device()
+    mvk.keygen(inst.key, inst.dW)
+    PT, Q = oracle.keygen(inst.W, inst.cx, inst.cy)
+    assert np.array_equal(host(inst.key.PT), PT)
+    assert np.array_equal(host(inst.key.Q), Q)
+    dXh = mvk.encode(inst.key, inst.dX, inst.dexi, inst.dexv)
+    Xh = oracle.encode(inst.cx, inst.X, inst.exi, inst.exv)
+    assert np.array_equal(host(dXh), Xh)
+    dYh = mvk.server_eval(inst.dW, dXh)
+    Yh = oracle.server_eval(inst.W, Xh)
+    assert np.array_equal(host(dYh), Yh)
+    vL = torch.empty((2, 1), dtype=torch.int32, device="cuda")
+    vR = torch.empty_like(vL)
+    Y, acc, vL, vR = mvk.decode_verify(inst.key, dXh, dYh, inst.dexi, inst.dexv, inst.deyi, inst.deyv, vL=vL, vR=vR)
+    oacc, ovL, ovR = oracle.verify(inst.cy, Q, Xh, Yh, inst.eyi, inst.eyv)
+    assert np.array_equal(host(vL), ovL) and np.array_equal(host(vR), ovR) and host(acc).tolist() == [1]
+    assert np.array_equal(host(Y), oracle.decode(PT, Yh, inst.exi, inst.exv))
+
+
+def _sampled_layer_check(name, sample_rows=96, sample_cols=24):
+    cfg = synth.CONFIGS[name]
+    m, n, B = cfg["m"], cfg["n"], cfg["B"]
+    _say(f"{name} sampled compare m={m} n={n} B={B}")
+    inst = Instance(cfg["cid"], m, n, B, cfg["r"], cfg["tx"], cfg["ty"], cfg["ell"]).to_device()
+    mvk.keygen(inst.key, inst.dW)
+    g = synth.rng(synth.seed_for(cfg["cid"], 99))
+    rows = np.unique(np.concatenate([[0, m - 1], g.integers(0, m, sample_rows)]))
+    cols = np.unique(np.concatenate([[0, n - 1], g.integers(0, n, sample_cols)]))
+    # P^T column i = Gx^T W[i, :]; Q column k = Gy^T W[:, k]
+    PTd = inst.key.PT
+    Qd = inst.key.Q
+    for i in rows[:24]:
+        want = oracle.encT(inst.cx, (inst.W[i].astype(np.int64) % P).astype(np.uint32))
+        assert np.array_equal(host(PTd[:, int(i)]), want)
+    for k in cols:
+        want = oracle.encT(inst.cy, (inst.W[:, k].astype(np.int64) % P).astype(np.uint32))
+        assert np.array_equal(host(Qd[:, int(k)]), want)
+    dXh = mvk.encode(inst.key, inst.dX, inst.dexi, inst.dexv)
+    Xh = oracle.encode(inst.cx, inst.X, inst.exi, inst.exv)
+    assert np.array_equal(host(dXh), Xh)
+    dYh = mvk.server_eval(inst.dW, dXh)
+    Yh_s = oracle.server_eval(inst.W[rows], Xh)
+    assert np.array_equal(host(dYh)[:, rows], Yh_s)
+    Y, acc, _, _ = mvk.decode_verify(inst.key, dXh, dYh, inst.dexi, inst.dexv, inst.deyi, inst.deyv)
+    assert host(acc).tolist() == [1] * B
+    assert np.array_equal(host(Y)[:, rows], oracle.server_eval(inst.W[rows], inst.X))
+    bad = dYh.clone()
+    b = B // 2
+    bad[b, int(rows[1])] = (int(bad[b, int(rows[1])]) + 12345) % P
+    _, acc2, _, _ = mvk.decode_verify(inst.key, dXh, bad, inst.dexi, inst.dexv, inst.deyi, inst.deyv)
+    want = [1] * B
+    want[b] = 0
+    assert host(acc2).tolist() == want
+
+
+def test_mlp_up_11008x4096_sampled():
+    _sampled_layer_check("mlp_up_11008x4096")
+
+
+def test_mlp_large_28672x8192_sampled():
+    _sampled_layer_check("mlp_large_28672x8192", sample_rows=48)

@@ -43,6 +43,11 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=2609)
     ap.add_argument("--path", default="auto", choices=["auto", "valu", "mfma"], help="server_eval kernel family")
+    ap.add_argument("--m", type=int, default=0, help="override the workload's row count (server-only)")
+    ap.add_argument("--n", type=int, default=0, help="override the workload's column count (server-only)")
+    ap.add_argument("--B", type=int, default=0, help="override the workload's query count (server-only)")
+    ap.add_argument("--server-only", action="store_true",
+                    help="time server_eval alone (no client steps) on the chosen workload")
     return ap.parse_args()
 
 
@@ -60,7 +65,11 @@ def main():
     import synth
 
     torch.cuda.set_device(0)
-    cfg = synth.CONFIGS[args.config]
+    cfg = dict(synth.CONFIGS[args.config])
+    if args.server_only:
+        for key in ("m", "n", "B"):
+            if getattr(args, key):
+                cfg[key] = getattr(args, key)
     m, n, B, r, tx, ty, ell = (cfg[k] for k in ("m", "n", "B", "r", "tx", "ty", "ell"))
     cid = cfg["cid"]
     w_bytes = m * n
@@ -71,6 +80,9 @@ def main():
     def d(a):
         a = np.ascontiguousarray(a)
         return torch.from_numpy(a.astype(np.int32) if a.dtype != np.int8 else a).to(dev)
+
+    if args.server_only:
+        return server_only(args, cfg, pool, total_steps, dev)
 
     # ---- setup (untimed) ---------------------------------------------------
     cx_h = synth.raa_code(synth.seed_for(cid, synth.PURPOSE_CX), n, r)
@@ -160,6 +172,48 @@ def main():
     print(json.dumps(out), flush=True)
     if not accepted:
         sys.exit(1)
+
+
+def server_only(args, cfg, pool, total_steps, dev):
+    """server_eval alone over a rotated pool of W; events around every launch."""
+    import numpy as np
+    import torch
+
+    import paper_2609_10264_amd as mvk
+
+    m, n, B = cfg["m"], cfg["n"], cfg["B"]
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(args.seed)
+    Ws = [torch.randint(-127, 128, (m, n), generator=gen, device=dev, dtype=torch.int8) for _ in range(pool)]
+    X = torch.randint(0, mvk.P, (pool, B, n), generator=gen, device=dev, dtype=torch.int32)
+    Y = torch.empty((B, m), dtype=torch.int32, device=dev)
+    for i in range(args.warmup):
+        mvk.server_eval(Ws[i % pool], X[i % pool], out=Y, path=args.path)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record()
+        mvk.server_eval(Ws[i % pool], X[i % pool], out=Y, path=args.path)
+        ev[i][1].record()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms = np.array([a.elapsed_time(b) for a, b in ev])
+    mean_s = 1e-3 * float(ms.mean())
+    alg_bytes = m * n + 4 * n * B + 4 * m * B
+    macs = m * n * B
+    out = {"metric": METRIC, "value": macs / mean_s, "unit": "modMAC/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": 1e3 * elapsed / args.steps, "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "i8xi8->i32 limb dot products, mod 2^31-1",
+           "data": "synthetic",
+           "config": {"workload": f"{args.config}: server_eval only, W {m}x{n} int8-valued, B={B}",
+                      "global_batch": B, "w_pool": pool},
+           "roofline": {"bound": "hbm", "achieved": alg_bytes / mean_s / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                        "frac": alg_bytes / mean_s / 1e9 / HBM_PEAK_GBS, "traffic": None,
+                        "kernel": f"server_eval ({args.path})", "alg_bytes_per_launch": alg_bytes,
+                        "mean_launch_us": 1e6 * mean_s, "median_launch_us": 1e3 * float(np.median(ms))},
+           "mfma_int8_tops": 2 * 4 * macs / mean_s / 1e12}
+    print(json.dumps(out), flush=True)
 
 
 def cpu_baseline(args, cfg, cx_h, cy_h):

@@ -22,10 +22,16 @@ struct Workspace {
 std::mutex g_ws_mu;
 std::map<std::pair<int, hipStream_t>, Workspace>* g_ws = nullptr;
 
-// Returns a device buffer of at least `bytes` private to (current device, s).
-// Growing waits for the work already enqueued on `s` before freeing the old
-// buffer, so earlier calls on the same stream can still be using it.
-mvk_status workspace(hipStream_t s, size_t bytes, void** out) {
+// Bytes at the start of every workspace reserved for control words (zeroed
+// when the workspace is allocated; kernels that use them leave them zero).
+constexpr size_t kCtrlBytes = 256;
+
+// Returns a device buffer of at least `bytes` private to (current device, s),
+// placed after the control words (*ctrl, may be null).  Growing waits for the
+// work already enqueued on `s` before freeing the old buffer, so earlier calls
+// on the same stream can still be using it.
+mvk_status workspace(hipStream_t s, size_t bytes, void** out, uint32_t** ctrl = nullptr) {
+    bytes += kCtrlBytes;
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return MVK_EHIP;
     std::lock_guard<std::mutex> lk(g_ws_mu);
@@ -45,9 +51,11 @@ mvk_status workspace(hipStream_t s, size_t bytes, void** out) {
             w.ptr = nullptr;
             return MVK_ENOMEM;
         }
+        if (hipMemset(w.ptr, 0, kCtrlBytes) != hipSuccess) return MVK_EHIP;
         w.size = sz;
     }
-    *out = w.ptr;
+    *out = (char*)w.ptr + kCtrlBytes;
+    if (ctrl) *ctrl = (uint32_t*)w.ptr;
     return MVK_OK;
 }
 
@@ -104,7 +112,13 @@ mvk_status mvk_server_eval_path(const int8_t* W, uint32_t m, uint32_t n, const u
     if (n == 0) return hip_status(launch_fill_u32(Yhat, (size_t)m * B, 0u, s));
     if (!W || !Xhat) return MVK_EINVAL;
     if (n > MVK_MAX_N) return MVK_ERANGE;
-    return hip_status(launch_server_eval(W, m, n, Xhat, B, Yhat, path, s));
+    void* ws = nullptr;
+    const size_t wsb = server_eval_workspace(n, B, path);
+    if (wsb) {
+        const mvk_status st = workspace(s, wsb, &ws);
+        if (st) return st;
+    }
+    return hip_status(launch_server_eval(W, m, n, Xhat, B, Yhat, path, ws, s));
 }
 
 mvk_status mvk_keygen(const mvk_key* key, const int8_t* W, void* stream) {
@@ -139,7 +153,7 @@ mvk_status mvk_encode(const mvk_key* key, const uint32_t* X, uint32_t B, const m
     const size_t Nx = (size_t)key->cx.r * key->n;
     if (ex->t > Nx) return MVK_EINVAL;
     void* ws = nullptr;
-    st = workspace(s, (size_t)B * 2 * Nx * sizeof(uint32_t), &ws);
+    st = workspace(s, Nx > kSynLdsLimit ? (size_t)B * 2 * Nx * sizeof(uint32_t) : 0, &ws);
     if (st) return st;
     return hip_status(launch_syn_sparse(key->cx, ex->idx, ex->val, ex->t, B, X, (uint32_t*)ws, Xhat, s));
 }
@@ -157,13 +171,15 @@ mvk_status mvk_decode_verify(const mvk_key* key, const uint32_t* Xhat, const uin
     const uint32_t m = key->m, n = key->n, ell = ey->count;
     const uint32_t Nx = key->cx.r * n, Ny = key->cy.r * m;
     if (ex->t > Nx || ey->t > Ny) return MVK_EINVAL;
+    if (B > 65535u) return MVK_ERANGE;
     const uint32_t nblkR = ceil_div(m, kClientCols), nblkL = ceil_div(n, kClientCols);
     const size_t r_bytes = align_up((size_t)ell * m * 4);
-    const size_t syn_bytes = align_up((size_t)ell * 2 * Ny * 4);
+    const size_t syn_bytes = (size_t)Ny > kSynLdsLimit ? align_up((size_t)ell * 2 * Ny * 4) : 0;
     const size_t pl_bytes = align_up((size_t)ell * B * nblkL * 4);
     const size_t pr_bytes = align_up((size_t)ell * B * nblkR * 4);
     void* ws = nullptr;
-    st = workspace(s, r_bytes + syn_bytes + pl_bytes + pr_bytes, &ws);
+    uint32_t* ctrl = nullptr;
+    st = workspace(s, r_bytes + syn_bytes + pl_bytes + pr_bytes, &ws, &ctrl);
     if (st) return st;
     char* base = (char*)ws;
     uint32_t* rv = (uint32_t*)base;
@@ -173,9 +189,8 @@ mvk_status mvk_decode_verify(const mvk_key* key, const uint32_t* Xhat, const uin
     // r_q = Gy e_q for every repetition (shared by all columns)
     hipError_t e = launch_syn_sparse(key->cy, ey->idx, ey->val, ey->t, ell, nullptr, syn_scratch, rv, s);
     if (e == hipSuccess)
-        e = launch_decode_vr(key->PT, m, Nx, Yhat, B, ex->idx, ex->val, ex->t, rv, ell, Y, partR, s);
-    if (e == hipSuccess) e = launch_verify_vl(key->Q, n, Ny, Xhat, B, ey->idx, ey->val, ey->t, ell, partL, s);
-    if (e == hipSuccess) e = launch_verify_finalize(partL, nblkL, partR, nblkR, B, ell, vL, vR, accept, s);
+        e = launch_decode_verify(key->PT, key->Q, m, n, Nx, Ny, Xhat, Yhat, B, ex->idx, ex->val, ex->t, ey->idx,
+                                 ey->val, ey->t, ell, rv, Y, partL, partR, &ctrl[0], vL, vR, accept, s);
     return hip_status(e);
 }
 

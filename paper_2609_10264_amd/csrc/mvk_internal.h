@@ -11,8 +11,10 @@
 namespace mvk {
 
 // server_eval.hip
+// Workspace bytes launch_server_eval needs for (n, B, path) (0: none).
+size_t server_eval_workspace(uint32_t n, uint32_t B, int path);
 hipError_t launch_server_eval(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t B,
-                              uint32_t* Y, int path, hipStream_t s);
+                              uint32_t* Y, int path, void* ws, hipStream_t s);
 
 // raa.hip -------------------------------------------------------------------
 // G^T applied to `nvec` vectors whose element i of vector v sits at
@@ -22,6 +24,8 @@ hipError_t launch_encT_u32(const mvk_code& c, const uint32_t* in, size_t ld_in, 
                            uint32_t* t3, uint32_t* out, size_t ld_out, size_t vs_out, hipStream_t s);
 hipError_t launch_encT_i8(const mvk_code& c, const int8_t* in, size_t ld_in, size_t vs_in, uint32_t nvec,
                           uint32_t* t3, uint32_t* out, size_t ld_out, size_t vs_out, hipStream_t s);
+// Block lengths up to this value run the syndrome entirely in LDS (no scratch).
+constexpr size_t kSynLdsLimit = 20224;
 // G v for `count` vectors: dense (v: count x N) or sparse (idx/val: count x t).
 // If X != nullptr the result is added to X (out = X + G v), as in Encrypt.
 // scratch: count * 2N uint32.
@@ -37,17 +41,15 @@ hipError_t launch_fill_u32(uint32_t* p, size_t count, uint32_t value, hipStream_
 // client.hip ----------------------------------------------------------------
 constexpr uint32_t kClientBlock = 256;  // threads per workgroup of the gather kernels
 constexpr uint32_t kClientCols = 64;    // output columns per workgroup of the gather kernels
-// Decrypt plus per-block partial sums of r_q . Yhat_b (r: ell x m).
-hipError_t launch_decode_vr(const uint32_t* PT, uint32_t m, uint32_t Nx, const uint32_t* Yhat, uint32_t B,
-                            const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx, const uint32_t* r,
-                            uint32_t ell, uint32_t* Y, uint32_t* partR, hipStream_t s);
-// u_q = e_q^T Q and per-block partial sums of u_q . Xhat_b.
-hipError_t launch_verify_vl(const uint32_t* Q, uint32_t n, uint32_t Ny, const uint32_t* Xhat, uint32_t B,
-                            const uint32_t* ey_idx, const uint32_t* ey_val, uint32_t ty, uint32_t ell,
-                            uint32_t* partL, hipStream_t s);
-hipError_t launch_verify_finalize(const uint32_t* partL, uint32_t nblkL, const uint32_t* partR, uint32_t nblkR,
-                                  uint32_t B, uint32_t ell, uint32_t* vL, uint32_t* vR, uint32_t* accept,
-                                  hipStream_t s);
+// Decrypt + Verify in one launch (see client.hip).  partL: ell*B*ceil(n/64),
+// partR: ell*B*ceil(m/64) words; counter: one word that must be zero before
+// the first launch (every launch leaves it at zero).
+hipError_t launch_decode_verify(const uint32_t* PT, const uint32_t* Q, uint32_t m, uint32_t n, uint32_t Nx,
+                                uint32_t Ny, const uint32_t* Xhat, const uint32_t* Yhat, uint32_t B,
+                                const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx, const uint32_t* ey_idx,
+                                const uint32_t* ey_val, uint32_t ty, uint32_t ell, const uint32_t* r, uint32_t* Y,
+                                uint32_t* partL, uint32_t* partR, uint32_t* counter, uint32_t* vL, uint32_t* vR,
+                                uint32_t* accept, hipStream_t s);
 
 inline uint32_t ceil_div(uint32_t a, uint32_t b) { return (a + b - 1) / b; }
 

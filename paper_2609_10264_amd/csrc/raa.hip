@@ -146,27 +146,134 @@ __device__ void block_scan(uint32_t* a, uint32_t N, uint32_t* wsum /* kSynWaves 
     }
 }
 
-// Largest block length kept entirely in LDS (two arrays of N words).
-constexpr uint32_t kSynLdsN = 20224;
+// Inclusive scan of one value per lane across the wave with DPP moves
+// (row shifts inside each 16-lane row, then row broadcasts across rows).
+__device__ __forceinline__ uint32_t wave_incl_scan_dpp(uint32_t x) {
+    x = fadd(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, true));  // row_shr:1
+    x = fadd(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, true));  // row_shr:2
+    x = fadd(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, true));  // row_shr:4
+    x = fadd(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, true));  // row_shr:8
+    x = fadd(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false));  // row_bcast:15
+    x = fadd(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false));  // row_bcast:31
+    return x;
+}
 
-// One workgroup per vector.  LDS_RES: both length-N work arrays live in LDS;
-// otherwise they live in the global scratch (count x 2N words).
-template <bool SPARSE, bool LDS_RES>
-__global__ __launch_bounds__(kSynThreads) void syn_block(uint32_t k, uint32_t r, const uint32_t* __restrict__ pi1,
-                                                         const uint32_t* __restrict__ pi2,
-                                                         const uint32_t* __restrict__ v1,
-                                                         const uint32_t* __restrict__ v2,
-                                                         const uint32_t* __restrict__ vin,
-                                                         const uint32_t* __restrict__ idx,
-                                                         const uint32_t* __restrict__ val, uint32_t t,
-                                                         const uint32_t* __restrict__ X, uint32_t* scratch,
-                                                         uint32_t* __restrict__ out) {
-    __shared__ uint32_t wsum[kSynWaves + 1];
-    __shared__ uint32_t lds[LDS_RES ? 2 * kSynLdsN : 1];
+// Largest block length kept entirely in LDS (two arrays of N words) and the
+// matching number of consecutive elements owned by one of the 1024 threads.
+constexpr uint32_t kSynLdsN = (uint32_t)kSynLdsLimit;
+constexpr int kSynMaxE = (kSynLdsN + kSynThreads - 1) / kSynThreads;
+
+// In-place inclusive suffix sum of a[0..N) held in LDS; thread t owns the E
+// consecutive elements [t*E, t*E + E).  The carry into a thread is the sum of
+// the totals of all later threads = grand total - inclusive prefix of totals.
+template <int E>
+__device__ __forceinline__ void lds_suffix_scan(uint32_t* a, uint32_t N, uint32_t* wsum) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const uint32_t base = (uint32_t)tid * E;
+    uint32_t x[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) x[e] = (base + e < N) ? a[base + e] : 0u;
+#pragma unroll
+    for (int e = E - 2; e >= 0; --e) x[e] = fadd(x[e], x[e + 1]);
+    const uint32_t incl = wave_incl_scan_dpp(x[0]);
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    if (wave == 0) {
+        const uint32_t t = lane < kSynWaves ? wsum[lane] : 0u;
+        const uint32_t ti = wave_incl_scan_dpp(t);
+        if (lane < kSynWaves) wsum[kSynWaves + 1 + lane] = ti;  // inclusive prefix of wave totals
+        if (lane == kSynWaves - 1) wsum[kSynWaves] = ti;        // grand total
+    }
+    __syncthreads();
+    const uint32_t before = wave ? wsum[kSynWaves + wave] : 0u;  // totals of earlier waves
+    const uint32_t prefix = fadd(before, incl);                   // totals of threads <= t
+    const uint32_t carry = fsub(wsum[kSynWaves], prefix);
+#pragma unroll
+    for (int e = 0; e < E; ++e)
+        if (base + e < N) a[base + e] = fadd(x[e], carry);
+    __syncthreads();
+}
+
+// One workgroup per vector with both work arrays in LDS.  The four code arrays
+// are loaded into registers first (position j = tid + 1024*e), so their
+// latency overlaps the initialisation of the first array.
+template <bool SPARSE, int E>
+__global__ __launch_bounds__(kSynThreads) void syn_lds(uint32_t k, uint32_t r, const uint32_t* __restrict__ pi1,
+                                                       const uint32_t* __restrict__ pi2,
+                                                       const uint32_t* __restrict__ v1,
+                                                       const uint32_t* __restrict__ v2,
+                                                       const uint32_t* __restrict__ vin,
+                                                       const uint32_t* __restrict__ idx,
+                                                       const uint32_t* __restrict__ val, uint32_t t,
+                                                       const uint32_t* __restrict__ X, uint32_t* __restrict__ out) {
+    __shared__ uint32_t A[kSynLdsN], Bv[kSynLdsN];
+    __shared__ uint32_t wsum[2 * kSynWaves + 2];
     const uint32_t c = blockIdx.x;
     const int tid = threadIdx.x;
     const uint32_t N = k * r;
-    uint32_t* a = LDS_RES ? lds : scratch + (size_t)c * 2 * N;
+    // Unconditional loads at an in-range position (j < N, else 0), so all 4E
+    // loads are in flight together; positions >= N are never used below.
+    uint32_t p1[E], p2[E], w1[E], w2[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const uint32_t j = tid + kSynThreads * e;
+        const uint32_t js = j < N ? j : 0u;
+        p1[e] = pi1[js];
+        p2[e] = pi2[js];
+        w1[e] = v1[js];
+        w2[e] = v2[js];
+    }
+    if (SPARSE) {
+        for (uint32_t j = tid; j < N; j += kSynThreads) A[j] = 0u;
+        __syncthreads();
+        for (uint32_t q = tid; q < t; q += kSynThreads) {
+            const uint32_t j = idx[(size_t)c * t + q];
+            A[j < N ? j : N - 1] = val[(size_t)c * t + q];
+        }
+    } else {
+        const uint32_t* src = vin + (size_t)c * N;
+        for (uint32_t j = tid; j < N; j += kSynThreads) A[j] = src[j];
+    }
+    __syncthreads();
+    lds_suffix_scan<E>(A, N, wsum);  // A
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const uint32_t j = tid + kSynThreads * e;
+        if (j < N) Bv[p2[e] < N ? p2[e] : N - 1] = fmul(w2[e], A[j]);  // V2, then Pi2 scatter
+    }
+    __syncthreads();
+    lds_suffix_scan<E>(Bv, N, wsum);  // A
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const uint32_t j = tid + kSynThreads * e;
+        if (j < N) A[p1[e] < N ? p1[e] : N - 1] = fmul(w1[e], Bv[j]);  // V1, then Pi1 scatter
+    }
+    __syncthreads();
+    for (uint32_t i = tid; i < k; i += kSynThreads) {  // R: fold blocks of r
+        uint32_t s = 0;
+        for (uint32_t q = 0; q < r; ++q) s = fadd(s, A[(size_t)i * r + q]);
+        if (X) s = fadd(X[(size_t)c * k + i], s);
+        out[(size_t)c * k + i] = s;
+    }
+}
+
+// Same computation with the work arrays in the global scratch (count x 2N
+// words), for block lengths beyond the LDS capacity.
+template <bool SPARSE>
+__global__ __launch_bounds__(kSynThreads) void syn_global(uint32_t k, uint32_t r, const uint32_t* __restrict__ pi1,
+                                                          const uint32_t* __restrict__ pi2,
+                                                          const uint32_t* __restrict__ v1,
+                                                          const uint32_t* __restrict__ v2,
+                                                          const uint32_t* __restrict__ vin,
+                                                          const uint32_t* __restrict__ idx,
+                                                          const uint32_t* __restrict__ val, uint32_t t,
+                                                          const uint32_t* __restrict__ X, uint32_t* scratch,
+                                                          uint32_t* __restrict__ out) {
+    __shared__ uint32_t wsum[kSynWaves + 1];
+    const uint32_t c = blockIdx.x;
+    const int tid = threadIdx.x;
+    const uint32_t N = k * r;
+    uint32_t* a = scratch + (size_t)c * 2 * N;
     uint32_t* b = a + N;
     if (SPARSE) {
         for (uint32_t j = tid; j < N; j += kSynThreads) a[j] = 0u;
@@ -201,6 +308,32 @@ __global__ __launch_bounds__(kSynThreads) void syn_block(uint32_t k, uint32_t r,
         if (X) s = fadd(X[(size_t)c * k + i], s);
         out[(size_t)c * k + i] = s;
     }
+}
+
+template <bool SPARSE>
+hipError_t launch_syn(const mvk_code& c, const uint32_t* v, const uint32_t* idx, const uint32_t* val, uint32_t t,
+                      uint32_t count, const uint32_t* X, uint32_t* scratch, uint32_t* out, hipStream_t s) {
+    if (count == 0) return hipSuccess;
+    const size_t N = (size_t)c.k * c.r;
+    const dim3 grid(count), block(kSynThreads);
+    if (N <= kSynLdsN) {
+        const int E = (int)((N + kSynThreads - 1) / kSynThreads);
+#define MVK_SYN(EV)                                                                                         \
+    hipLaunchKernelGGL((syn_lds<SPARSE, EV>), grid, block, 0, s, c.k, c.r, c.pi1, c.pi2, c.v1, c.v2, v, idx, val, \
+                       t, X, out)
+        if (E <= 1) MVK_SYN(1);
+        else if (E <= 2) MVK_SYN(2);
+        else if (E <= 4) MVK_SYN(4);
+        else if (E <= 8) MVK_SYN(8);
+        else if (E <= 12) MVK_SYN(12);
+        else if (E <= 16) MVK_SYN(16);
+        else MVK_SYN(kSynMaxE);
+#undef MVK_SYN
+    } else {
+        hipLaunchKernelGGL((syn_global<SPARSE>), grid, block, 0, s, c.k, c.r, c.pi1, c.pi2, c.v1, c.v2, v, idx, val,
+                           t, X, scratch, out);
+    }
+    return hipGetLastError();
 }
 
 __global__ __launch_bounds__(256) void transpose_i8(const int8_t* __restrict__ W, uint32_t m, uint32_t n,
@@ -238,26 +371,12 @@ hipError_t launch_encT_i8(const mvk_code& c, const int8_t* in, size_t ld_in, siz
 
 hipError_t launch_syn_dense(const mvk_code& c, const uint32_t* v, uint32_t count, uint32_t* scratch, uint32_t* out,
                             hipStream_t s) {
-    if (count == 0) return hipSuccess;
-    if ((size_t)c.k * c.r <= kSynLdsN)
-        hipLaunchKernelGGL((syn_block<false, true>), dim3(count), dim3(kSynThreads), 0, s, c.k, c.r, c.pi1, c.pi2,
-                           c.v1, c.v2, v, nullptr, nullptr, 0u, nullptr, scratch, out);
-    else
-        hipLaunchKernelGGL((syn_block<false, false>), dim3(count), dim3(kSynThreads), 0, s, c.k, c.r, c.pi1, c.pi2,
-                           c.v1, c.v2, v, nullptr, nullptr, 0u, nullptr, scratch, out);
-    return hipGetLastError();
+    return launch_syn<false>(c, v, nullptr, nullptr, 0u, count, nullptr, scratch, out, s);
 }
 
 hipError_t launch_syn_sparse(const mvk_code& c, const uint32_t* idx, const uint32_t* val, uint32_t t,
                              uint32_t count, const uint32_t* X, uint32_t* scratch, uint32_t* out, hipStream_t s) {
-    if (count == 0) return hipSuccess;
-    if ((size_t)c.k * c.r <= kSynLdsN)
-        hipLaunchKernelGGL((syn_block<true, true>), dim3(count), dim3(kSynThreads), 0, s, c.k, c.r, c.pi1, c.pi2,
-                           c.v1, c.v2, nullptr, idx, val, t, X, scratch, out);
-    else
-        hipLaunchKernelGGL((syn_block<true, false>), dim3(count), dim3(kSynThreads), 0, s, c.k, c.r, c.pi1, c.pi2,
-                           c.v1, c.v2, nullptr, idx, val, t, X, scratch, out);
-    return hipGetLastError();
+    return launch_syn<true>(c, nullptr, idx, val, t, count, X, scratch, out, s);
 }
 
 hipError_t launch_transpose_i8(const int8_t* W, uint32_t m, uint32_t n, int8_t* WT, hipStream_t s) {

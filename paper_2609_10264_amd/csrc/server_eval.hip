@@ -223,58 +223,96 @@ __global__ __launch_bounds__(KW * 64) void server_eval_mfma_small(const int8_t* 
     const int arow = lane & 15;
     const int8_t* wbase = W + (size_t)(wrow < m ? wrow : 0) * n;
 
+    // Query elements converted per thread and chunk (four consecutive k each).
+    constexpr int NXG = QB * (KC / 4) / (KW * 64);
+    static_assert(NXG * KW * 64 == QB * (KC / 4), "chunk must split evenly over the workgroup");
     v4i acc = {0, 0, 0, 0};
     for (uint32_t kc0 = 0; kc0 < n; kc0 += KC) {
+        // 1. query loads first (needed first), 2. W loads (in flight during the
+        // conversion), 3. convert the query chunk into LDS digit planes.
+        uint32_t xq[NXG][4];
+        uint32_t xok[NXG];  // bit e set: element e of the group is in range
+#pragma unroll
+        for (int it = 0; it < NXG; ++it) {
+            const int idx = tid + it * KW * 64;
+            const int q = idx / (KC / 4);
+            const int k4 = idx % (KC / 4);
+            const uint32_t k = kc0 + 4 * k4;
+            const bool okq = q0 + q < B;
+            const uint32_t* xr = X + (size_t)(okq ? q0 + q : 0) * n;
+            if (VEC) {
+                const uint4 t = *reinterpret_cast<const uint4*>(xr + (k < n ? k : 0));
+                xok[it] = (okq && k < n) ? 0xfu : 0u;
+                xq[it][0] = t.x;
+                xq[it][1] = t.y;
+                xq[it][2] = t.z;
+                xq[it][3] = t.w;
+            } else {
+                xok[it] = 0u;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const bool ok = okq && k + e < n;
+                    xok[it] |= ok ? (1u << e) : 0u;
+                    xq[it][e] = xr[ok ? k + e : 0];
+                }
+            }
+        }
+        // Keep the query loads ahead of the W loads in the instruction stream:
+        // the conversion below then waits only for them, not for W.
+        __builtin_amdgcn_sched_barrier(0);
         v4i bw[KBW];
+        int32_t wmask[KBW];
 #pragma unroll
         for (int j = 0; j < KBW; ++j) {
+            // Unconditional load at an in-range address, masked at use: no
+            // branches, so the waits can count outstanding loads.
             const uint32_t k = kc0 + (uint32_t)(wave * KBW + j) * 64 + kg * 16;
+            const bool okw = wrow < m && k < n;
+            wmask[j] = okw ? -1 : 0;
             v4i t = {0, 0, 0, 0};
-            if (wrow < m && k < n) {
-                if (VEC) {
-                    t = *reinterpret_cast<const v4i*>(wbase + k);
-                } else {
+            if (VEC) {
+                t = *reinterpret_cast<const v4i*>(wbase + (okw ? k : 0u));
+            } else {
 #pragma unroll
-                    for (int e = 0; e < 16; ++e) {
-                        const uint32_t b = (k + e < n) ? (uint32_t)(uint8_t)wbase[k + e] : 0u;
-                        t[e >> 2] |= (int32_t)(b << (8 * (e & 3)));
-                    }
+                for (int e = 0; e < 16; ++e) {
+                    const bool ok = okw && k + e < n;
+                    const uint32_t b = (uint32_t)(uint8_t)wbase[ok ? k + e : 0u];
+                    t[e >> 2] |= (int32_t)((ok ? b : 0u) << (8 * (e & 3)));
                 }
             }
             bw[j] = t;
         }
-        for (int idx = tid; idx < QB * (KC / 4); idx += KW * 64) {
+        __builtin_amdgcn_sched_barrier(0);  // all W loads issued before the conversion starts
+#pragma unroll
+        for (int it = 0; it < NXG; ++it) {
+            const int idx = tid + it * KW * 64;
             const int q = idx / (KC / 4);
             const int k4 = idx % (KC / 4);
-            const uint32_t k = kc0 + 4 * k4;
-            uint32_t x[4] = {0u, 0u, 0u, 0u};
-            if (q0 + q < B && k < n) {
-                const uint32_t* xr = X + (size_t)(q0 + q) * n + k;
-                if (VEC) {
-                    const uint4 t = *reinterpret_cast<const uint4*>(xr);
-                    x[0] = t.x;
-                    x[1] = t.y;
-                    x[2] = t.z;
-                    x[3] = t.w;
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) x[e] = (k + e < n) ? xr[e] : 0u;
-                }
-            }
             int32_t p[4];
-            digit_planes(x[0], x[1], x[2], x[3], p[0], p[1], p[2], p[3]);
+            const uint32_t x0 = (xok[it] & 1u) ? xq[it][0] : 0u, x1 = (xok[it] & 2u) ? xq[it][1] : 0u;
+            const uint32_t x2 = (xok[it] & 4u) ? xq[it][2] : 0u, x3 = (xok[it] & 8u) ? xq[it][3] : 0u;
+            digit_planes(x0, x1, x2, x3, p[0], p[1], p[2], p[3]);
 #pragma unroll
             for (int d = 0; d < 4; ++d) *reinterpret_cast<int32_t*>(dig + (q * 4 + d) * STRIDE + 4 * k4) = p[d];
         }
         __syncthreads();
+        // Blocks past the end of the row hold zeros on both operands and add
+        // nothing, so every MFMA runs unconditionally.
 #pragma unroll
         for (int j = 0; j < KBW; ++j) {
             const int kbl = wave * KBW + j;
-            if (kc0 + (uint32_t)kbl * 64 < n) {
-                v4i a = {0, 0, 0, 0};
-                if (arow < ROWS) a = *reinterpret_cast<const v4i*>(dig + arow * STRIDE + kbl * 64 + kg * 16);
-                acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, bw[j], acc, 0, 0, 0);
-            }
+            const v4i araw = *reinterpret_cast<const v4i*>(dig + (arow < ROWS ? arow : 0) * STRIDE + kbl * 64 + kg * 16);
+            const int32_t msk = arow < ROWS ? -1 : 0;
+            v4i a, w;
+            a[0] = araw[0] & msk;
+            a[1] = araw[1] & msk;
+            a[2] = araw[2] & msk;
+            a[3] = araw[3] & msk;
+            w[0] = bw[j][0] & wmask[j];
+            w[1] = bw[j][1] & wmask[j];
+            w[2] = bw[j][2] & wmask[j];
+            w[3] = bw[j][3] & wmask[j];
+            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, w, acc, 0, 0, 0);
         }
         __syncthreads();
     }
@@ -305,6 +343,181 @@ hipError_t launch_mfma_small(const int8_t* W, uint32_t m, uint32_t n, const uint
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Matrix-core GEMM path for batches of query columns (B > 4).
+//
+// C = D W^T, D the digit matrix of the queries (digit row 4q + d = plane d of
+// query q, padded with zero rows to QT*16), W read from HBM exactly once.
+// digits_tiled_kernel stores D in MFMA operand order: granule (kb, qt, l) is
+// the 16 bytes that lane l supplies for digit tile qt and k-block kb (64 k),
+// i.e. digit row 16*qt + l%16 at k = 64*kb + 16*(l/16) + [0, 16).
+//
+// A workgroup of NW waves owns NW*TW*16 rows of W (TW tiles of 16 per wave)
+// over the whole K range and all QT digit tiles.  Operands travel HBM/L2 ->
+// LDS with global_load_lds_dwordx4 (lane i's 16 bytes land at base + 16*i), so
+// no registers hold data in flight and the prefetch depth is set by the ring
+// size S: k-block kb uses ring slot kb % S; the W tiles of a wave live in its
+// private part of the slot, the QT digit tiles are shared (each wave loads
+// QT/NW of them).  Iteration kb: wait until this wave's loads of k-block kb+1
+// have landed (at most S-3 k-blocks of loads may still be outstanding),
+// barrier (all waves' tiles of kb+1 landed and everyone has finished k-block
+// kb-1), refill the slot of k-block kb-1 with k-block kb+S-1, then run the
+// MFMAs of k-block kb from registers while reading k-block kb+1 from LDS.
+// Every operand read is a ds_read_b128 at 16*lane: conflict free.
+// Epilogue: lane l of C tile (qt, t) holds the four digit sums of query
+// 4*qt + l/16 for W row 16*t + l%16, recombined in-lane.
+// ---------------------------------------------------------------------------
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    // s_waitcnt with expcnt and lgkmcnt at their maxima (no wait on them);
+    // vmcnt is split over bits [3:0] and [15:14]
+    static_assert(N >= 0 && N <= 63, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 0xf) | (0x7 << 4) | (0xf << 8) | (((N >> 4) & 3) << 14));
+}
+
+// global_load_lds_dwordx4: lane i's 16 bytes at `src` land at LDS address
+// M0 + 16*i.  Issued as inline assembly so that the compiler does not add its
+// own (conservative, whole-queue) waits before later LDS reads; the ring
+// waits are explicit wait_vmcnt calls.  Vector-memory loads complete in
+// order, so loads the compiler does not know about can only make its own
+// waits longer, never shorter.
+__device__ __forceinline__ void dma16(const void* src, int8_t* lds_base) {
+    const uint32_t lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int8_t*)lds_base;
+    uint32_t saved;  // M0 is restored right after the issue (the load reads it at issue)
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %1\n\t"
+        "global_load_lds_dwordx4 %2, off\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "s"(lds), "v"(src)
+        : "memory");
+}
+
+__global__ __launch_bounds__(256) void digits_tiled_kernel(const uint32_t* __restrict__ X, uint32_t n, uint32_t B,
+                                                           uint32_t QT, uint32_t nkb, int8_t* __restrict__ Dt) {
+    // one thread per 16-byte granule (kb, qt, l)
+    const uint32_t g = blockIdx.x * 256 + threadIdx.x;
+    if (g >= nkb * QT * 64) return;
+    const uint32_t l = g % 64, qt = (g / 64) % QT, kb = g / (64 * QT);
+    const uint32_t dr = qt * 16 + (l & 15);
+    const uint32_t q = dr >> 2, d = dr & 3;
+    const uint32_t k0 = kb * 64 + (l >> 4) * 16;
+    uint32_t out[4] = {0u, 0u, 0u, 0u};
+    if (q < B) {
+        const uint32_t* xr = X + (size_t)q * n;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const uint32_t k = k0 + e;
+            const uint32_t u = digit_word(k < n ? xr[k] : 0u);
+            out[e >> 2] |= ((u >> (8 * d)) & 0xffu) << (8 * (e & 3));
+        }
+    }
+    *reinterpret_cast<uint4*>(Dt + (size_t)g * 16) = make_uint4(out[0], out[1], out[2], out[3]);
+}
+
+template <int QT, int NW, int TW, int S>
+__global__ __launch_bounds__(NW * 64) void server_eval_mfma_dma(const int8_t* __restrict__ W, uint32_t m, uint32_t n,
+                                                                const int8_t* __restrict__ Dt, uint32_t nkb,
+                                                                uint32_t B, uint32_t* __restrict__ Y) {
+    constexpr int AQ = QT / NW;  // digit tiles loaded by each wave per k-block
+    static_assert(AQ * NW == QT, "QT must be a multiple of NW");
+    constexpr int PER = TW + AQ;  // loads per wave per k-block
+    static_assert((S - 2) * PER <= 63, "vmcnt range");
+    static_assert(S >= 3, "the pipeline reads one k-block ahead");
+    __shared__ __align__(16) int8_t Aring[S][QT][1024];
+    __shared__ __align__(16) int8_t Wring[S][NW][TW][1024];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint32_t rowbase = blockIdx.x * (NW * TW * 16) + wave * (TW * 16);
+    const uint32_t kl = (lane >> 4) * 16;
+    const int8_t* wptr[TW];
+#pragma unroll
+    for (int t = 0; t < TW; ++t) {
+        const uint32_t row = rowbase + t * 16 + (lane & 15);
+        wptr[t] = W + (size_t)(row < m ? row : m - 1) * n;
+    }
+    // Issue the loads of k-block kb into ring slot `slot`.  Blocks past the end
+    // re-read the last block (in range; never consumed).  W columns >= n are
+    // read at column 0: they meet zero digits.
+    auto issue = [&](uint32_t kb, int slot) {
+        const uint32_t kbe = kb < nkb ? kb : nkb - 1;
+        const uint32_t k = kbe * 64 + kl;
+        const uint32_t kk = k < n ? k : 0u;
+#pragma unroll
+        for (int t = 0; t < TW; ++t) dma16(wptr[t] + kk, &Wring[slot][wave][t][0]);
+#pragma unroll
+        for (int a = 0; a < AQ; ++a) {
+            const uint32_t qt = wave * AQ + a;
+            dma16(Dt + ((size_t)(kbe * QT + qt) * 64 + lane) * 16, &Aring[slot][qt][0]);
+        }
+    };
+    v4i acc[QT][TW];
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+        for (int t = 0; t < TW; ++t) acc[qt][t] = v4i{0, 0, 0, 0};
+
+    // Software pipeline: the operands of k-block kb+1 are read from LDS into
+    // registers while the MFMAs of k-block kb run.  At the top of iteration kb
+    // every wave has consumed k-block kb-1 (its MFMAs ran in iteration kb-1),
+    // so the slot of kb-1 can be refilled with k-block kb+S-1.
+    v4i cb[TW], ca[QT];
+#pragma unroll
+    for (int j = 0; j < S - 1; ++j) issue(j, j);
+    wait_vmcnt<(S - 2) * PER>();
+    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < TW; ++t) cb[t] = *reinterpret_cast<const v4i*>(&Wring[0][wave][t][16 * lane]);
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) ca[qt] = *reinterpret_cast<const v4i*>(&Aring[0][qt][16 * lane]);
+    for (uint32_t kb = 0; kb < nkb; ++kb) {
+        // k-block kb+1 landed (this wave's loads), and everyone is past kb-1
+        wait_vmcnt<(S - 3) * PER>();
+        __syncthreads();
+        issue(kb + S - 1, (int)((kb + S - 1) % S));
+        const int nslot = (int)((kb + 1) % S);
+        v4i nb[TW], na[QT];
+#pragma unroll
+        for (int t = 0; t < TW; ++t) nb[t] = *reinterpret_cast<const v4i*>(&Wring[nslot][wave][t][16 * lane]);
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) na[qt] = *reinterpret_cast<const v4i*>(&Aring[nslot][qt][16 * lane]);
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+            for (int t = 0; t < TW; ++t)
+                acc[qt][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ca[qt], cb[t], acc[qt][t], 0, 0, 0);
+#pragma unroll
+        for (int t = 0; t < TW; ++t) cb[t] = nb[t];
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) ca[qt] = na[qt];
+    }
+    wait_vmcnt<0>();  // drain the trailing prefetches before the workgroup exits
+
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+        const uint32_t q = qt * 4 + (lane >> 4);
+#pragma unroll
+        for (int t = 0; t < TW; ++t) {
+            const uint32_t row = rowbase + t * 16 + (lane & 15);
+            if (q < B && row < m) {
+                const v4i sum = acc[qt][t];
+                const int64_t v = (int64_t)sum[0] + ((int64_t)sum[1] << 8) + ((int64_t)sum[2] << 16) +
+                                  ((int64_t)sum[3] << 24);
+                Y[(size_t)q * m + row] = fred_s64(v);
+            }
+        }
+    }
+}
+
+template <int QT, int NW, int TW, int S>
+hipError_t launch_dma_cfg(const int8_t* W, uint32_t m, uint32_t n, const int8_t* Dt, uint32_t nkb, uint32_t B,
+                          uint32_t* Y, hipStream_t s) {
+    const dim3 grid(ceil_div(m, NW * TW * 16));
+    hipLaunchKernelGGL((server_eval_mfma_dma<QT, NW, TW, S>), grid, dim3(NW * 64), 0, s, W, m, n, Dt, nkb, B, Y);
+    return hipGetLastError();
+}
+
 template <int R, int BQ>
 hipError_t launch_cfg(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t B, uint32_t* Y,
                       hipStream_t s) {
@@ -319,8 +532,15 @@ hipError_t launch_cfg(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X
 
 }  // namespace
 
+size_t server_eval_workspace(uint32_t n, uint32_t B, int path) {
+    if (path == MVK_PATH_VALU || B <= 4 || n % 16 != 0) return 0;
+    const size_t nkb = ceil_div(n, 64);
+    const size_t qt = B <= 8 ? 2 : B <= 16 ? 4 : B <= 32 ? 8 : 16;  // digit tiles of one launch group
+    return nkb * qt * 64 * 16;
+}
+
 hipError_t launch_server_eval(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t B,
-                              uint32_t* Y, int path, hipStream_t s) {
+                              uint32_t* Y, int path, void* ws, hipStream_t s) {
     if (path == MVK_PATH_VALU) {
         if (B == 1) return launch_cfg<16, 1>(W, m, n, X, B, Y, s);
         if (B == 2) return launch_cfg<8, 2>(W, m, n, X, B, Y, s);
@@ -328,7 +548,40 @@ hipError_t launch_server_eval(const int8_t* W, uint32_t m, uint32_t n, const uin
     }
     if (B == 1) return launch_mfma_small<1, 8, 8>(W, m, n, X, B, Y, s);
     if (B == 2) return launch_mfma_small<2, 8, 8>(W, m, n, X, B, Y, s);
-    return launch_mfma_small<4, 8, 4>(W, m, n, X, B, Y, s);
+    if (B <= 4) return launch_mfma_small<4, 8, 4>(W, m, n, X, B, Y, s);
+    if (n % 16 != 0 || (uintptr_t)W % 16 != 0) {
+        // Rows that are not whole 16-byte granules: the streamed path would read
+        // past the end of W on the last row; use the small path per 4 queries.
+        for (uint32_t b0 = 0; b0 < B; b0 += 4) {
+            const uint32_t nb = (B - b0) < 4 ? (B - b0) : 4;
+            const hipError_t e = launch_mfma_small<4, 8, 4>(W, m, n, X + (size_t)b0 * n, nb, Y + (size_t)b0 * m, s);
+            if (e != hipSuccess) return e;
+        }
+        return hipSuccess;
+    }
+    // Up to 64 queries per launch group; W is streamed once per group.
+    const uint32_t nkb = ceil_div(n, 64);
+    int8_t* Dt = (int8_t*)ws;
+    for (uint32_t b0 = 0; b0 < B; b0 += 64) {
+        const uint32_t nb = (B - b0) < 64 ? (B - b0) : 64;
+        const uint32_t qt = nb <= 8 ? 2 : nb <= 16 ? 4 : nb <= 32 ? 8 : 16;
+        const uint32_t granules = nkb * qt * 64;
+        hipLaunchKernelGGL(digits_tiled_kernel, dim3(ceil_div(granules, 256)), dim3(256), 0, s, X + (size_t)b0 * n,
+                           n, nb, qt, nkb, Dt);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        uint32_t* Yb = Y + (size_t)b0 * m;
+        if (qt == 2)
+            e = launch_dma_cfg<2, 2, 1, 16>(W, m, n, Dt, nkb, nb, Yb, s);
+        else if (qt == 4)
+            e = launch_dma_cfg<4, 4, 1, 12>(W, m, n, Dt, nkb, nb, Yb, s);
+        else if (qt == 8)
+            e = launch_dma_cfg<8, 4, 2, 8>(W, m, n, Dt, nkb, nb, Yb, s);
+        else
+            e = launch_dma_cfg<16, 4, 2, 6>(W, m, n, Dt, nkb, nb, Yb, s);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 }  // namespace mvk

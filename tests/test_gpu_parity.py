@@ -37,6 +37,7 @@ import paper_2609_10264_amd as mvk  # noqa: E402
 SERVER_SHAPES = [
     (1, 1, 1), (3, 5, 1), (17, 33, 2), (256, 256, 1), (257, 4099, 1), (64, 4096, 3), (16, 8192, 1),
     (100, 160, 5), (300, 1000, 16), (31, 2048, 64), (4096, 4096, 1), (33, 12345, 4), (50, 4112, 7),
+    (129, 300, 17), (70, 999, 65), (16, 128, 130), (200, 4096, 32), (1000, 8192, 64),
 ]
 
 

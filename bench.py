@@ -30,6 +30,33 @@ sys.path.insert(0, ROOT)
 
 METRIC = "server_eval mod-MACs/s + achieved HBM GB/s (fraction of peak), 1×MI355X"
 HBM_PEAK_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "server_eval_attn4096_traffic.json")
+KERNEL_SRC = os.path.join(ROOT, "paper_2609_10264_amd", "csrc", "server_eval.hip")
+
+
+def measured_traffic(config: str):
+    """HBM bytes per server_eval launch from the committed counter runs, if they
+    were taken on the current kernel source and this workload; else None."""
+    import hashlib
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+        with open(KERNEL_SRC, "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()
+    except OSError:
+        return None
+    if rec.get("kernel_src_sha256") != sha or rec.get("config") != config:
+        return None
+    return rec.get("traffic_bytes_per_launch")
+
+
+def calib_copy(mib: int):
+    import torch
+    src = torch.ones(mib * 2**20, dtype=torch.int8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
 
 
 def parse():
@@ -37,10 +64,14 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", default="attn4096")
+    ap.add_argument("--config", default="attn4096",
+                    help="attn4096 (default), mlp_up_11008x4096, mlp_large_28672x8192, tiny or stack32")
     ap.add_argument("--pool", type=int, default=0, help="distinct W matrices cycled (0: enough for 2x the LLC)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="time budget of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--eager", action="store_true", help="launch the timed steps one by one instead of a HIP graph")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="after timing, copy this many MiB device-to-device (reference kernel for HBM counters)")
     ap.add_argument("--seed", type=int, default=2609)
     ap.add_argument("--path", default="auto", choices=["auto", "valu", "mfma"], help="server_eval kernel family")
     ap.add_argument("--m", type=int, default=0, help="override the workload's row count (server-only)")
@@ -65,6 +96,8 @@ def main():
     import synth
 
     torch.cuda.set_device(0)
+    if args.config == "stack32":
+        return stack_bench(args)
     cfg = dict(synth.CONFIGS[args.config])
     if args.server_only:
         for key in ("m", "n", "B"):
@@ -112,34 +145,74 @@ def main():
     ACC = torch.zeros((total_steps, B), dtype=torch.int32, device=dev)
     torch.cuda.synchronize()
 
-    ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-
-    def step(i, timed_idx=None):
+    def step(i):
         j = i % pool
         mvk.encode(keys[j], X[i], EXI[i], EXV[i], out=Xh)
-        if timed_idx is not None:
-            ev0[timed_idx].record()
         mvk.server_eval(Ws[j], Xh, out=Yh, path=args.path)
-        if timed_idx is not None:
-            ev1[timed_idx].record()
         mvk.decode_verify(keys[j], Xh, Yh, EXI[i], EXV[i], EYI[i], EYV[i], Y=Y, accept=ACC[i])
 
-    for i in range(args.warmup):
-        step(i)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        # warm-up on the launch stream (also sizes the library's per-stream workspace)
+        for i in range(args.warmup):
+            step(i)
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for s in range(args.steps):
-        step(args.warmup + s, s)
+
+    if args.eager:
+        with torch.cuda.stream(s):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for k in range(args.steps):
+                step(args.warmup + k)
+            torch.cuda.synchronize()
+            elapsed = time.perf_counter() - t0
+    else:
+        # The K timed steps (4 launches each) captured once as a HIP graph and
+        # replayed: identical kernels and inputs, without per-launch host gaps.
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            for k in range(args.steps):
+                step(args.warmup + k)
+        g.replay()  # untimed replay
+        torch.cuda.synchronize()
+        ACC.zero_()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        g.replay()
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+    accepted = bool((ACC[args.warmup:] == 1).all().item())
+    # The buffers hold the last timed step; recompute it eagerly and compare.
+    last = (Xh.clone(), Yh.clone(), Y.clone())
+    with torch.cuda.stream(s):
+        step(args.warmup + args.steps - 1)
     torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    elapsed = t1 - t0
-    se_ms = [a.elapsed_time(b) for a, b in zip(ev0, ev1)]
-    accepted = bool((ACC == 1).all().item())
+    replay_matches_eager = all(bool(torch.equal(a, b)) for a, b in zip(last, (Xh, Yh, Y)))
+
+    # server_eval alone, same W pool and masked queries, captured back to back;
+    # HIP events on the launch stream bracket the replay.
+    reps = args.steps
+    Xs = torch.randint(0, mvk.P, (pool, B, n), generator=gen, device=dev, dtype=torch.int32)
+    ge = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        for j in range(pool):
+            mvk.server_eval(Ws[j], Xs[j], out=Yh, path=args.path)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(ge, stream=s):
+        for k in range(reps):
+            mvk.server_eval(Ws[k % pool], Xs[k % pool], out=Yh, path=args.path)
+    ge.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(s):
+        e0.record()
+        ge.replay()
+        e1.record()
+    torch.cuda.synchronize()
+    se_mean_s = 1e-3 * e0.elapsed_time(e1) / reps
 
     macs = m * n * B
     ms_per_step = 1e3 * elapsed / args.steps
-    se_mean_s = 1e-3 * float(np.mean(se_ms))
     alg_bytes = m * n + 4 * n * B + 4 * m * B
     achieved = alg_bytes / se_mean_s / 1e9
 
@@ -158,18 +231,102 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{args.config}: W {m}x{n} int8-valued in F_p (p=2^31-1), B={B} query column(s), "
                                f"RAA r={r}, t_x={tx}, t_y={ty}, ell={ell}; step = encode+server_eval+decode_verify",
-                   "global_batch": B, "w_pool": pool},
+                   "global_batch": B, "w_pool": pool, "launch": "eager" if args.eager else "hip_graph"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(args.config),
                      "kernel": f"server_eval ({args.path})", "alg_bytes_per_launch": alg_bytes,
-                     "mean_launch_us": 1e6 * se_mean_s, "median_launch_us": 1e3 * float(np.median(se_ms))},
+                     "mean_launch_us": 1e6 * se_mean_s},
         "server_eval": {"modmac_per_s": macs / se_mean_s, "gb_per_s": achieved},
         "all_accepted": accepted,
+        "replay_matches_eager": replay_matches_eager,
     }
 
+    if args.calib_copy_mib:
+        calib_copy(args.calib_copy_mib)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args, cfg, cx_h, cy_h)
     print(json.dumps(out), flush=True)
+    if not (accepted and replay_matches_eager):
+        sys.exit(1)
+
+
+def stack_bench(args):
+    """32 decoder layers (seven projections each, 8 query columns): one step is a
+    full pass (4 encodes, 7 server evaluations, 7 verifications per layer)."""
+    import numpy as np
+    import torch
+
+    import paper_2609_10264_amd as mvk
+    import paper_2609_10264_amd.stack as stack
+    import synth
+
+    cfg = synth.STACK
+    layers, B, r, tx, ty, ell, cid = (cfg[k] for k in ("layers", "B", "r", "tx", "ty", "ell", "cid"))
+    dev = torch.device("cuda")
+
+    def d(a):
+        return torch.from_numpy(np.ascontiguousarray(a).astype(np.int32)).to(dev)
+
+    def make_code(kind, k):
+        purpose = synth.PURPOSE_CX if kind == "x" else synth.PURPOSE_CY
+        c = synth.raa_code(synth.seed_for(cid, purpose, sub=k), k, r)
+        return mvk.Code(c["k"], c["r"], d(c["pi1"]), d(c["pi2"]), d(c["v1"]), d(c["v2"]))
+
+    cx_by_n, cy_by_m = stack.codes_for(make_code)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(args.seed)
+    s = torch.cuda.Stream()
+    built, inputs = [], []
+    with torch.cuda.stream(s):
+        for L in range(layers):
+            Ws = {name: torch.randint(-127, 128, (m, n), generator=gen, device=dev, dtype=torch.int8)
+                  for (name, m, n, _) in stack.PROJECTIONS}
+            built.append(stack.build_layer(Ws, cx_by_n, cy_by_m))
+            X = {grp: torch.randint(0, mvk.P, (B, stack.input_width(grp)), generator=gen, device=dev,
+                                    dtype=torch.int32) for grp in stack.INPUTS}
+            ex = {}
+            for j, grp in enumerate(stack.INPUTS):
+                i_, v_ = synth.sparse(synth.seed_for(cid, synth.PURPOSE_NOISE, 100 * L + j), B,
+                                      r * stack.input_width(grp), tx)
+                ex[grp] = (d(i_), d(v_))
+            ey = {}
+            for i, (name, m, _, _) in enumerate(stack.PROJECTIONS):
+                i_, v_ = synth.sparse(synth.seed_for(cid, synth.PURPOSE_CHAL, 100 * L + i), ell, r * m, ty)
+                ey[name] = (d(i_), d(v_))
+            inputs.append((X, ex, ey))
+        results = []
+
+        def one_pass():
+            results.clear()
+            for L in range(layers):
+                results.append(stack.run_layer(built[L], *inputs[L]))
+
+        for _ in range(max(1, args.warmup // 10)):
+            one_pass()
+    torch.cuda.synchronize()
+    steps = max(1, args.steps // 40)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        one_pass()
+    g.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        g.replay()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    accepted = all(bool((out[name][1] == 1).all().item()) for out in results for name in out)
+    macs = stack.macs_per_layer(B) * layers
+    res = {"metric": METRIC, "value": macs * steps / elapsed, "unit": "modMAC/s", "n_gpus": 1, "steps": steps,
+           "warmup": max(1, args.warmup // 10), "ms_per_step": 1e3 * elapsed / steps, "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "i8xi8->i32 limb dot products, mod 2^31-1",
+           "data": "synthetic",
+           "config": {"workload": f"stack32: {layers} layers x (q,k,v,o 4096x4096; up,gate 11008x4096; "
+                                  f"down 4096x11008), B={B}, r={r}, t_x={tx}, t_y={ty}, ell={ell}; step = one full "
+                                  "pass (4 encodes, 7 server_evals, 7 decode_verifies per layer)",
+                      "global_batch": B, "launch": "hip_graph"},
+           "all_accepted": accepted}
+    print(json.dumps(res), flush=True)
     if not accepted:
         sys.exit(1)
 

@@ -153,7 +153,7 @@ mvk_status mvk_encode(const mvk_key* key, const uint32_t* X, uint32_t B, const m
     const size_t Nx = (size_t)key->cx.r * key->n;
     if (ex->t > Nx) return MVK_EINVAL;
     void* ws = nullptr;
-    st = workspace(s, Nx > kSynLdsLimit ? (size_t)B * 2 * Nx * sizeof(uint32_t) : 0, &ws);
+    st = workspace(s, Nx > kSynScratchAbove ? (size_t)B * 2 * Nx * sizeof(uint32_t) : 0, &ws);
     if (st) return st;
     return hip_status(launch_syn_sparse(key->cx, ex->idx, ex->val, ex->t, B, X, (uint32_t*)ws, Xhat, s));
 }
@@ -174,7 +174,7 @@ mvk_status mvk_decode_verify(const mvk_key* key, const uint32_t* Xhat, const uin
     if (B > 65535u) return MVK_ERANGE;
     const uint32_t nblkR = ceil_div(m, kClientCols), nblkL = ceil_div(n, kClientCols);
     const size_t r_bytes = align_up((size_t)ell * m * 4);
-    const size_t syn_bytes = (size_t)Ny > kSynLdsLimit ? align_up((size_t)ell * 2 * Ny * 4) : 0;
+    const size_t syn_bytes = (size_t)Ny > kSynScratchAbove ? align_up((size_t)ell * 2 * Ny * 4) : 0;
     const size_t pl_bytes = align_up((size_t)ell * B * nblkL * 4);
     const size_t pr_bytes = align_up((size_t)ell * B * nblkR * 4);
     void* ws = nullptr;

@@ -24,8 +24,9 @@ hipError_t launch_encT_u32(const mvk_code& c, const uint32_t* in, size_t ld_in, 
                            uint32_t* t3, uint32_t* out, size_t ld_out, size_t vs_out, hipStream_t s);
 hipError_t launch_encT_i8(const mvk_code& c, const int8_t* in, size_t ld_in, size_t vs_in, uint32_t nvec,
                           uint32_t* t3, uint32_t* out, size_t ld_out, size_t vs_out, hipStream_t s);
-// Block lengths up to this value run the syndrome entirely in LDS (no scratch).
-constexpr size_t kSynLdsLimit = 20224;
+// Block lengths above this value run the syndrome in segments and need a
+// scratch of count x 2N words; up to it the syndrome runs in LDS.
+constexpr size_t kSynScratchAbove = 4096;
 // G v for `count` vectors: dense (v: count x N) or sparse (idx/val: count x t).
 // If X != nullptr the result is added to X (out = X + G v), as in Encrypt.
 // scratch: count * 2N uint32.

@@ -160,7 +160,9 @@ __device__ __forceinline__ uint32_t wave_incl_scan_dpp(uint32_t x) {
 
 // Largest block length kept entirely in LDS (two arrays of N words) and the
 // matching number of consecutive elements owned by one of the 1024 threads.
-constexpr uint32_t kSynLdsN = (uint32_t)kSynLdsLimit;
+// Block lengths up to this run in one workgroup (LDS); longer ones in segments.
+constexpr size_t kSynSingleMax = kSynScratchAbove;
+constexpr uint32_t kSynLdsN = (uint32_t)kSynSingleMax;
 constexpr int kSynMaxE = (kSynLdsN + kSynThreads - 1) / kSynThreads;
 
 // In-place inclusive suffix sum of a[0..N) held in LDS; thread t owns the E
@@ -257,57 +259,162 @@ __global__ __launch_bounds__(kSynThreads) void syn_lds(uint32_t k, uint32_t r, c
     }
 }
 
-// Same computation with the work arrays in the global scratch (count x 2N
-// words), for block lengths beyond the LDS capacity.
+// ---------------------------------------------------------------------------
+// Multi-workgroup syndrome for long blocks (several workgroups per vector).
+// The length-N work array is cut into segments of kSegLen positions, one
+// workgroup each, in three launches:
+//   p1: a = suffix sum of the input (the carry into a segment is the sum of the
+//       input beyond it: for sparse input a sum over the t terms, for dense
+//       input a reduction of the tail), then b[pi2[j]] = v2[j] a[j]
+//   p2: c = suffix sum of b (carry: each workgroup reduces the tail of b
+//       itself, so no workgroup waits for another), then d[pi1[j]] = v1[j] c[j]
+//   p3: out[i] = (X[i] +) sum_{q<r} d[i r + q]
+// b and d live in the global scratch (count x 2N words).
+// ---------------------------------------------------------------------------
+constexpr int kSegThreads = 256;
+constexpr int kSegPer = 4;
+constexpr uint32_t kSegLen = kSegThreads * kSegPer;
+
+__device__ __forceinline__ uint64_t block_sum_u64_256(uint64_t v, uint64_t* red) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int s = 32; s >= 1; s >>= 1) {
+        const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, s);
+        const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), s);
+        v += ((uint64_t)hi << 32) | lo;
+    }
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    const uint64_t t = red[0] + red[1] + red[2] + red[3];
+    __syncthreads();
+    return t;
+}
+
+// Inclusive suffix scan of the kSegPer consecutive values x[] owned by each of
+// the 256 threads (thread t owns positions t*kSegPer ..), plus `carry`.
+__device__ __forceinline__ void seg_suffix_scan(uint32_t (&x)[kSegPer], uint32_t carry, uint32_t* wsum) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int e = kSegPer - 2; e >= 0; --e) x[e] = fadd(x[e], x[e + 1]);
+    const uint32_t incl = wave_incl_scan_dpp(x[0]);  // prefix over lanes of thread totals
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    const uint32_t w0 = wsum[0], w1 = wsum[1], w2 = wsum[2], w3 = wsum[3];
+    __syncthreads();
+    const uint32_t total = fadd(fadd(w0, w1), fadd(w2, w3));
+    uint32_t before = 0;  // totals of earlier waves
+    if (wave > 0) before = w0;
+    if (wave > 1) before = fadd(before, w1);
+    if (wave > 2) before = fadd(before, w2);
+    // sum over later threads = total - (prefix through this thread)
+    const uint32_t after = fsub(total, fadd(before, incl));
+    const uint32_t off = fadd(after, carry);
+#pragma unroll
+    for (int e = 0; e < kSegPer; ++e) x[e] = fadd(x[e], off);
+}
+
 template <bool SPARSE>
-__global__ __launch_bounds__(kSynThreads) void syn_global(uint32_t k, uint32_t r, const uint32_t* __restrict__ pi1,
-                                                          const uint32_t* __restrict__ pi2,
-                                                          const uint32_t* __restrict__ v1,
-                                                          const uint32_t* __restrict__ v2,
-                                                          const uint32_t* __restrict__ vin,
-                                                          const uint32_t* __restrict__ idx,
-                                                          const uint32_t* __restrict__ val, uint32_t t,
-                                                          const uint32_t* __restrict__ X, uint32_t* scratch,
-                                                          uint32_t* __restrict__ out) {
-    __shared__ uint32_t wsum[kSynWaves + 1];
-    const uint32_t c = blockIdx.x;
+__global__ __launch_bounds__(kSegThreads) void syn_p1(uint32_t k, uint32_t r, const uint32_t* __restrict__ pi2,
+                                                      const uint32_t* __restrict__ v2,
+                                                      const uint32_t* __restrict__ vin,
+                                                      const uint32_t* __restrict__ idx,
+                                                      const uint32_t* __restrict__ val, uint32_t t,
+                                                      uint32_t* __restrict__ scratch) {
+    __shared__ uint32_t seg[kSegLen];
+    __shared__ uint64_t red[4];
+    __shared__ uint32_t wsum[4];
+    const uint32_t c = blockIdx.y, N = k * r;
+    const uint32_t j0 = blockIdx.x * kSegLen, j1 = (j0 + kSegLen < N) ? j0 + kSegLen : N;
     const int tid = threadIdx.x;
-    const uint32_t N = k * r;
-    uint32_t* a = scratch + (size_t)c * 2 * N;
-    uint32_t* b = a + N;
+    uint32_t* bbuf = scratch + (size_t)c * 2 * N;
+    // code entries of this thread's positions (in flight during the carry)
+    uint32_t p2[kSegPer], w2[kSegPer];
+#pragma unroll
+    for (int e = 0; e < kSegPer; ++e) {
+        const uint32_t j = j0 + tid * kSegPer + e;
+        const uint32_t js = j < j1 ? j : j0;
+        p2[e] = pi2[js];
+        w2[e] = v2[js];
+    }
+    uint64_t part = 0;
     if (SPARSE) {
-        for (uint32_t j = tid; j < N; j += kSynThreads) a[j] = 0u;
-        __syncthreads();
-        for (uint32_t q = tid; q < t; q += kSynThreads) {
-            uint32_t j = idx[(size_t)c * t + q];
-            if (j >= N) j = N - 1;
-            a[j] = val[(size_t)c * t + q];
+        for (uint32_t q = tid; q < t; q += kSegThreads) {
+            const uint32_t j = idx[(size_t)c * t + q];
+            if (j >= j1 && j < N) part += val[(size_t)c * t + q];
         }
     } else {
         const uint32_t* src = vin + (size_t)c * N;
-        for (uint32_t j = tid; j < N; j += kSynThreads) a[j] = src[j];
+        for (uint32_t j = j1 + tid; j < N; j += kSegThreads) part += src[j];
     }
-    __syncthreads();
-    block_scan<true>(a, N, wsum);  // A
-    for (uint32_t j = tid; j < N; j += kSynThreads) {
-        uint32_t pj = pi2[j];
-        if (pj >= N) pj = N - 1;
-        b[pj] = fmul(v2[j], a[j]);  // V2, then Pi2 scatter
+    const uint32_t carry = fred64(block_sum_u64_256(part, red));
+    uint32_t x[kSegPer];
+    if (SPARSE) {
+#pragma unroll
+        for (int e = 0; e < kSegPer; ++e) seg[tid * kSegPer + e] = 0u;
+        __syncthreads();
+        for (uint32_t q = tid; q < t; q += kSegThreads) {
+            const uint32_t j = idx[(size_t)c * t + q];
+            if (j >= j0 && j < j1) seg[j - j0] = val[(size_t)c * t + q];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int e = 0; e < kSegPer; ++e) x[e] = seg[tid * kSegPer + e];
+    } else {
+#pragma unroll
+        for (int e = 0; e < kSegPer; ++e) {
+            const uint32_t j = j0 + tid * kSegPer + e;
+            x[e] = j < j1 ? vin[(size_t)c * N + j] : 0u;
+        }
     }
-    __syncthreads();
-    block_scan<true>(b, N, wsum);  // A
-    for (uint32_t j = tid; j < N; j += kSynThreads) {
-        uint32_t pj = pi1[j];
-        if (pj >= N) pj = N - 1;
-        a[pj] = fmul(v1[j], b[j]);  // V1, then Pi1 scatter
+    seg_suffix_scan(x, carry, wsum);  // A
+#pragma unroll
+    for (int e = 0; e < kSegPer; ++e) {
+        const uint32_t j = j0 + tid * kSegPer + e;
+        if (j < j1) bbuf[p2[e] < N ? p2[e] : N - 1] = fmul(w2[e], x[e]);  // V2, then Pi2 scatter
     }
-    __syncthreads();
-    for (uint32_t i = tid; i < k; i += kSynThreads) {  // R: fold blocks of r
-        uint32_t s = 0;
-        for (uint32_t q = 0; q < r; ++q) s = fadd(s, a[(size_t)i * r + q]);
-        if (X) s = fadd(X[(size_t)c * k + i], s);
-        out[(size_t)c * k + i] = s;
+}
+
+__global__ __launch_bounds__(kSegThreads) void syn_p2(uint32_t k, uint32_t r, const uint32_t* __restrict__ pi1,
+                                                      const uint32_t* __restrict__ v1, uint32_t* __restrict__ scratch) {
+    __shared__ uint64_t red[4];
+    __shared__ uint32_t wsum[4];
+    const uint32_t c = blockIdx.y, N = k * r;
+    const uint32_t j0 = blockIdx.x * kSegLen, j1 = (j0 + kSegLen < N) ? j0 + kSegLen : N;
+    const int tid = threadIdx.x;
+    const uint32_t* bbuf = scratch + (size_t)c * 2 * N;
+    uint32_t* dbuf = scratch + (size_t)c * 2 * N + N;
+    uint32_t p1[kSegPer], w1[kSegPer], x[kSegPer];
+#pragma unroll
+    for (int e = 0; e < kSegPer; ++e) {
+        const uint32_t j = j0 + tid * kSegPer + e;
+        const uint32_t js = j < j1 ? j : j0;
+        p1[e] = pi1[js];
+        w1[e] = v1[js];
+        const uint32_t b = bbuf[js];
+        x[e] = j < j1 ? b : 0u;
     }
+    uint64_t part = 0;
+#pragma unroll 8
+    for (uint32_t j = j1 + tid; j < N; j += kSegThreads) part += bbuf[j];
+    const uint32_t carry = fred64(block_sum_u64_256(part, red));
+    seg_suffix_scan(x, carry, wsum);  // A
+#pragma unroll
+    for (int e = 0; e < kSegPer; ++e) {
+        const uint32_t j = j0 + tid * kSegPer + e;
+        if (j < j1) dbuf[p1[e] < N ? p1[e] : N - 1] = fmul(w1[e], x[e]);  // V1, then Pi1 scatter
+    }
+}
+
+__global__ __launch_bounds__(256) void syn_p3(uint32_t k, uint32_t r, const uint32_t* __restrict__ scratch,
+                                              const uint32_t* __restrict__ X, uint32_t* __restrict__ out) {
+    const uint32_t c = blockIdx.y, N = k * r;
+    const uint32_t i = blockIdx.x * 256 + threadIdx.x;
+    if (i >= k) return;
+    const uint32_t* dbuf = scratch + (size_t)c * 2 * N + N;
+    uint32_t s = 0;
+    for (uint32_t q = 0; q < r; ++q) s = fadd(s, dbuf[(size_t)i * r + q]);  // R: fold blocks of r
+    if (X) s = fadd(X[(size_t)c * k + i], s);
+    out[(size_t)c * k + i] = s;
 }
 
 template <bool SPARSE>
@@ -315,24 +422,28 @@ hipError_t launch_syn(const mvk_code& c, const uint32_t* v, const uint32_t* idx,
                       uint32_t count, const uint32_t* X, uint32_t* scratch, uint32_t* out, hipStream_t s) {
     if (count == 0) return hipSuccess;
     const size_t N = (size_t)c.k * c.r;
-    const dim3 grid(count), block(kSynThreads);
-    if (N <= kSynLdsN) {
+    if (N <= kSynSingleMax) {
+        // short blocks: one workgroup per vector, everything in LDS
+        const dim3 grid(count), block(kSynThreads);
         const int E = (int)((N + kSynThreads - 1) / kSynThreads);
 #define MVK_SYN(EV)                                                                                         \
     hipLaunchKernelGGL((syn_lds<SPARSE, EV>), grid, block, 0, s, c.k, c.r, c.pi1, c.pi2, c.v1, c.v2, v, idx, val, \
                        t, X, out)
         if (E <= 1) MVK_SYN(1);
         else if (E <= 2) MVK_SYN(2);
-        else if (E <= 4) MVK_SYN(4);
-        else if (E <= 8) MVK_SYN(8);
-        else if (E <= 12) MVK_SYN(12);
-        else if (E <= 16) MVK_SYN(16);
-        else MVK_SYN(kSynMaxE);
+        else MVK_SYN(4);
 #undef MVK_SYN
-    } else {
-        hipLaunchKernelGGL((syn_global<SPARSE>), grid, block, 0, s, c.k, c.r, c.pi1, c.pi2, c.v1, c.v2, v, idx, val,
-                           t, X, scratch, out);
+        return hipGetLastError();
     }
+    const dim3 gseg((uint32_t)((N + kSegLen - 1) / kSegLen), count);
+    hipLaunchKernelGGL((syn_p1<SPARSE>), gseg, dim3(kSegThreads), 0, s, c.k, c.r, c.pi2, c.v2, v, idx, val, t,
+                       scratch);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(syn_p2, gseg, dim3(kSegThreads), 0, s, c.k, c.r, c.pi1, c.v1, scratch);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(syn_p3, dim3(ceil_div(c.k, 256), count), dim3(256), 0, s, c.k, c.r, scratch, X, out);
     return hipGetLastError();
 }
 

@@ -1,0 +1,97 @@
+"""A stack of decoder layers delegated with pvMVMD (Maverick's inference loop
+restricted to its linear operations, Sec. 7.2).
+
+Every layer has seven projections of a 4096-wide decoder block:
+q, k, v, o (4096 x 4096), up, gate (11008 x 4096), down (4096 x 11008).
+Per layer and batch of B query columns the client encodes four inputs
+(q/k/v share one, up/gate share one), the server evaluates the seven products,
+and the client verifies and decrypts the seven responses.  The nonlinear
+operations between projections are outside this library: every input is a
+fresh synthetic query.
+
+Codes are shared per shape (one privacy code per input width n, one
+verification code per output height m); P^T and Q are per matrix.  This module
+only orchestrates calls of the C ABI (through the binding); all arithmetic runs
+in the HIP kernels.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import torch
+
+from . import Code, Key, decode_verify, encode, keygen, server_eval
+
+# (name, m, n, input group)
+PROJECTIONS = (
+    ("q", 4096, 4096, "attn_in"),
+    ("k", 4096, 4096, "attn_in"),
+    ("v", 4096, 4096, "attn_in"),
+    ("o", 4096, 4096, "attn_out"),
+    ("up", 11008, 4096, "mlp_in"),
+    ("gate", 11008, 4096, "mlp_in"),
+    ("down", 4096, 11008, "mlp_out"),
+)
+INPUTS = ("attn_in", "attn_out", "mlp_in", "mlp_out")
+
+
+@dataclass
+class Layer:
+    W: dict = field(default_factory=dict)      # name -> int8 m x n
+    keys: dict = field(default_factory=dict)   # name -> Key
+
+
+def input_width(group: str) -> int:
+    return next(n for (_, _, n, g) in PROJECTIONS if g == group)
+
+
+def build_layer(weights: dict, cx_by_n: dict, cy_by_m: dict, stream=None) -> Layer:
+    """Preprocess every projection of one layer (keygen on the device)."""
+    layer = Layer()
+    for name, m, n, _ in PROJECTIONS:
+        W = weights[name]
+        key = Key.allocate(m, n, cx_by_n[n], cy_by_m[m], device=W.device)
+        keygen(key, W, stream=stream)
+        layer.W[name] = W
+        layer.keys[name] = key
+    return layer
+
+
+def run_layer(layer: Layer, X: dict, ex: dict, ey: dict, tamper=None, stream=None):
+    """One layer for a batch of query columns.
+
+    X[group]: B x n plaintext queries; ex[group] = (idx, val) noise of that
+    input (B x t_x); ey[name] = (idx, val) challenges (ell x t_y).
+    tamper: optional callable(name, Yhat) applied to each response before
+    verification (the test harness's dishonest server).
+    Returns {name: (Y, accept)}.
+    """
+    Xhat = {}
+    for group in INPUTS:
+        # any projection fed by this input has the right privacy code
+        name = next(p for (p, _, _, g) in PROJECTIONS if g == group)
+        Xhat[group] = encode(layer.keys[name], X[group], ex[group][0], ex[group][1], stream=stream)
+    out = {}
+    for name, m, n, group in PROJECTIONS:
+        Yhat = server_eval(layer.W[name], Xhat[group], stream=stream)
+        if tamper is not None:
+            tamper(name, Yhat)
+        Y, acc, _, _ = decode_verify(layer.keys[name], Xhat[group], Yhat, ex[group][0], ex[group][1],
+                                     ey[name][0], ey[name][1], stream=stream)
+        out[name] = (Y, acc, Xhat[group], Yhat)
+    return out
+
+
+def codes_for(make_code) -> tuple[dict, dict]:
+    """Shared codes: privacy code per input width, verification code per output height."""
+    ns = sorted({n for (_, _, n, _) in PROJECTIONS})
+    ms = sorted({m for (_, m, _, _) in PROJECTIONS})
+    return {n: make_code("x", n) for n in ns}, {m: make_code("y", m) for m in ms}
+
+
+def macs_per_layer(B: int) -> int:
+    return sum(m * n for (_, m, n, _) in PROJECTIONS) * B
+
+
+__all__ = ["PROJECTIONS", "INPUTS", "Layer", "build_layer", "run_layer", "codes_for", "input_width",
+           "macs_per_layer", "Code"]

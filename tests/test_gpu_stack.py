@@ -1,0 +1,110 @@
+"""GPU parity of a 32-layer decoder stack delegated with pvMVMD.
+
+Per layer: seven projections (q, k, v, o 4096x4096; up, gate 11008x4096; down
+4096x11008), eight query columns, r = 3, t_x = 64, t_y = 31, ell = 2.  The
+responses are enumerated (layer, projection, column); the one whose index is
+congruent to a seeded offset modulo 1000 is tampered (a nonzero delta at a
+seeded coordinate) and must be rejected while every other column is accepted.
+Checked against the CPU oracle: every masked query in full, P^T / Q columns of
+every projection of layer 0, and sampled rows of every decrypted output.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from tests.gpu_util import code as dev_code
+from tests.gpu_util import dev, host
+
+pytestmark = pytest.mark.gpu
+P = synth.P
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def test_stack_parity_and_tamper_schedule():
+    import paper_2609_10264_amd.stack as stack
+
+    cfg = synth.STACK
+    layers = int(os.environ.get("MVK_STACK_LAYERS", cfg["layers"]))
+    B, r, tx, ty, ell, cid = cfg["B"], cfg["r"], cfg["tx"], cfg["ty"], cfg["ell"], cfg["cid"]
+    host_codes = {}
+
+    def make_code(kind, k):
+        purpose = synth.PURPOSE_CX if kind == "x" else synth.PURPOSE_CY
+        c = synth.raa_code(synth.seed_for(cid, purpose, sub=k), k, r)
+        host_codes[(kind, k)] = c
+        return dev_code(c)
+
+    cx_by_n, cy_by_m = stack.codes_for(make_code)
+    nproj = len(stack.PROJECTIONS)
+    total = layers * nproj * B
+    g = synth.rng(synth.seed_for(cid, synth.PURPOSE_TAMPER))
+    offset = int(g.integers(0, 1000))
+    tampered = {k for k in range(offset, total, 1000)}
+    seen_tampered = 0
+    for L in range(layers):
+        print(f"stack layer {L}", flush=True)
+        sub = 100 * (L + 1)
+        Wh = {name: synth.weights(synth.seed_for(cid, synth.PURPOSE_W, sub + i), m, n)
+              for i, (name, m, n, _) in enumerate(stack.PROJECTIONS)}
+        layer = stack.build_layer({k: dev(v) for k, v in Wh.items()}, cx_by_n, cy_by_m)
+        Xh_host, ex_host = {}, {}
+        for j, grp in enumerate(stack.INPUTS):
+            n = stack.input_width(grp)
+            Xh_host[grp] = synth.field_uniform(synth.seed_for(cid, synth.PURPOSE_X, sub + j), (B, n))
+            ex_host[grp] = synth.sparse(synth.seed_for(cid, synth.PURPOSE_NOISE, sub + j), B, r * n, tx)
+        ey_host = {name: synth.sparse(synth.seed_for(cid, synth.PURPOSE_CHAL, sub + i), ell, r * m, ty)
+                   for i, (name, m, n, _) in enumerate(stack.PROJECTIONS)}
+        X = {k: dev(v) for k, v in Xh_host.items()}
+        ex = {k: (dev(a), dev(b)) for k, (a, b) in ex_host.items()}
+        ey = {k: (dev(a), dev(b)) for k, (a, b) in ey_host.items()}
+
+        planned = {}
+        for i, (name, m, _, _) in enumerate(stack.PROJECTIONS):
+            for b in range(B):
+                if (L * nproj + i) * B + b in tampered:
+                    pos = int(g.integers(0, m))
+                    delta = int(g.integers(1, P))
+                    planned.setdefault(name, []).append((b, pos, delta))
+
+        def tamper(name, Yhat):
+            for b, pos, delta in planned.get(name, []):
+                Yhat[b, pos] = int((int(Yhat[b, pos].item()) + delta) % P)
+
+        out = stack.run_layer(layer, X, ex, ey, tamper=tamper)
+        torch.cuda.synchronize()
+
+        for grp in stack.INPUTS:
+            n = stack.input_width(grp)
+            want = oracle.encode(host_codes[("x", n)], Xh_host[grp], *ex_host[grp])
+            name = next(p for (p, _, _, gg) in stack.PROJECTIONS if gg == grp)
+            assert np.array_equal(host(out[name][2]), want), (L, grp)
+        rs = synth.rng(synth.seed_for(cid, 99, sub))
+        for i, (name, m, n, grp) in enumerate(stack.PROJECTIONS):
+            Y, acc, _, _ = out[name]
+            bad = {b for (b, _, _) in planned.get(name, [])}
+            want_acc = [0 if b in bad else 1 for b in range(B)]
+            assert host(acc).tolist() == want_acc, (L, name)
+            seen_tampered += len(bad)
+            rows = np.unique(np.concatenate([[0, m - 1], rs.integers(0, m, 6)]))
+            good = [b for b in range(B) if b not in bad]
+            want = oracle.server_eval(Wh[name][rows], Xh_host[grp][good])
+            assert np.array_equal(host(Y)[np.ix_(good, rows)], want), (L, name)
+            if L == 0:
+                cx, cy = host_codes[("x", n)], host_codes[("y", m)]
+                key = layer.keys[name]
+                i0, k0 = int(rows[len(rows) // 2]), int(rs.integers(0, n))
+                assert np.array_equal(host(key.PT[:, i0]),
+                                      oracle.encT(cx, (Wh[name][i0].astype(np.int64) % P).astype(np.uint32)))
+                assert np.array_equal(host(key.Q[:, k0]),
+                                      oracle.encT(cy, (Wh[name][:, k0].astype(np.int64) % P).astype(np.uint32)))
+        del layer, out
+    assert seen_tampered == len(tampered) >= (1 if total > offset else 0)

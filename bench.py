@@ -70,6 +70,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="time budget of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true", help="launch the timed steps one by one instead of a HIP graph")
+    ap.add_argument("--chains", type=int, default=1,
+                    help="independent query chains run side by side (step i belongs to chain i mod chains)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after timing, copy this many MiB device-to-device (reference kernel for HBM counters)")
     ap.add_argument("--seed", type=int, default=2609)
@@ -139,55 +141,79 @@ def main():
     eyi, eyv = synth.sparse(synth.seed_for(cid, synth.PURPOSE_CHAL, 7), total_steps * ell, cy.N, ty)
     EXI, EXV = d(exi).view(total_steps, B, tx), d(exv).view(total_steps, B, tx)
     EYI, EYV = d(eyi).view(total_steps, ell, ty), d(eyv).view(total_steps, ell, ty)
-    Xh = torch.empty((B, n), dtype=torch.int32, device=dev)
-    Yh = torch.empty((B, m), dtype=torch.int32, device=dev)
-    Y = torch.empty((B, m), dtype=torch.int32, device=dev)
+    C = max(1, args.chains)
+    if args.warmup < C:
+        raise SystemExit("--warmup must be at least --chains (each chain warms its own stream)")
+    # per chain: its own stream, its own output buffers
+    streams = [torch.cuda.Stream() for _ in range(C)]
+    Xh = [torch.empty((B, n), dtype=torch.int32, device=dev) for _ in range(C)]
+    Yh = [torch.empty((B, m), dtype=torch.int32, device=dev) for _ in range(C)]
+    Y = [torch.empty((B, m), dtype=torch.int32, device=dev) for _ in range(C)]
     ACC = torch.zeros((total_steps, B), dtype=torch.int32, device=dev)
     torch.cuda.synchronize()
 
     def step(i):
-        j = i % pool
-        mvk.encode(keys[j], X[i], EXI[i], EXV[i], out=Xh)
-        mvk.server_eval(Ws[j], Xh, out=Yh, path=args.path)
-        mvk.decode_verify(keys[j], Xh, Yh, EXI[i], EXV[i], EYI[i], EYV[i], Y=Y, accept=ACC[i])
+        """Step i on chain i % C (launched on the current stream = that chain's)."""
+        j, c = i % pool, i % C
+        mvk.encode(keys[j], X[i], EXI[i], EXV[i], out=Xh[c])
+        mvk.server_eval(Ws[j], Xh[c], out=Yh[c], path=args.path)
+        mvk.decode_verify(keys[j], Xh[c], Yh[c], EXI[i], EXV[i], EYI[i], EYV[i], Y=Y[c], accept=ACC[i])
 
-    s = torch.cuda.Stream()
-    with torch.cuda.stream(s):
-        # warm-up on the launch stream (also sizes the library's per-stream workspace)
-        for i in range(args.warmup):
+    # warm-up on the launch streams (also sizes the library's per-stream workspaces)
+    for i in range(args.warmup):
+        with torch.cuda.stream(streams[i % C]):
             step(i)
     torch.cuda.synchronize()
+    timed = [[args.warmup + k for k in range(args.steps) if (args.warmup + k) % C == c] for c in range(C)]
 
     if args.eager:
-        with torch.cuda.stream(s):
-            torch.cuda.synchronize()
-            t0 = time.perf_counter()
-            for k in range(args.steps):
-                step(args.warmup + k)
-            torch.cuda.synchronize()
-            elapsed = time.perf_counter() - t0
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for k in range(args.steps):
+            i = args.warmup + k
+            with torch.cuda.stream(streams[i % C]):
+                step(i)
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
     else:
-        # The K timed steps (4 launches each) captured once as a HIP graph and
-        # replayed: identical kernels and inputs, without per-launch host gaps.
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g, stream=s):
-            for k in range(args.steps):
-                step(args.warmup + k)
-        g.replay()  # untimed replay
+        # Each chain's timed steps are captured once as a HIP graph on its own
+        # stream and replayed: identical kernels and inputs, without per-launch
+        # host gaps.  Steps of one chain run in order; with C > 1 the chains
+        # (independent queries) run side by side.
+        graphs = []
+        for c in range(C):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=streams[c]):
+                for i in timed[c]:
+                    step(i)
+            graphs.append(g)
+
+        def replay_all():
+            for c in range(C):
+                with torch.cuda.stream(streams[c]):
+                    graphs[c].replay()
+
+        replay_all()  # untimed replay
         torch.cuda.synchronize()
         ACC.zero_()
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        g.replay()
+        replay_all()
         torch.cuda.synchronize()
         elapsed = time.perf_counter() - t0
     accepted = bool((ACC[args.warmup:] == 1).all().item())
-    # The buffers hold the last timed step; recompute it eagerly and compare.
-    last = (Xh.clone(), Yh.clone(), Y.clone())
-    with torch.cuda.stream(s):
-        step(args.warmup + args.steps - 1)
+    # The buffers hold the last timed step of every chain; recompute those
+    # steps eagerly and compare.
+    last = [(Xh[c].clone(), Yh[c].clone(), Y[c].clone()) for c in range(C) if timed[c]]
+    for c in range(C):
+        if timed[c]:
+            with torch.cuda.stream(streams[c]):
+                step(timed[c][-1])
     torch.cuda.synchronize()
-    replay_matches_eager = all(bool(torch.equal(a, b)) for a, b in zip(last, (Xh, Yh, Y)))
+    now = [(Xh[c], Yh[c], Y[c]) for c in range(C) if timed[c]]
+    replay_matches_eager = all(bool(torch.equal(a, b)) for la, lb in zip(last, now) for a, b in zip(la, lb))
+    s = streams[0]
+    Yh = Yh[0]
 
     # server_eval alone, same W pool and masked queries, captured back to back;
     # HIP events on the launch stream bracket the replay.
@@ -231,7 +257,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{args.config}: W {m}x{n} int8-valued in F_p (p=2^31-1), B={B} query column(s), "
                                f"RAA r={r}, t_x={tx}, t_y={ty}, ell={ell}; step = encode+server_eval+decode_verify",
-                   "global_batch": B, "w_pool": pool, "launch": "eager" if args.eager else "hip_graph"},
+                   "global_batch": B, "w_pool": pool, "launch": "eager" if args.eager else "hip_graph",
+                   "chains": C},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(args.config),
                      "kernel": f"server_eval ({args.path})", "alg_bytes_per_launch": alg_bytes,

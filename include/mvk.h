@@ -37,7 +37,7 @@ extern "C" {
 #endif
 
 #define MVK_PRIME 2147483647u
-#define MVK_ABI_VERSION 1
+#define MVK_ABI_VERSION 2
 
 typedef int32_t mvk_status;
 #define MVK_OK 0
@@ -162,13 +162,37 @@ mvk_status mvk_encode(const mvk_key *key, const uint32_t *X, uint32_t B, const m
  *   Y      : device, B x m, written (must be discarded where accept is 0)
  *   vL, vR : device, ell x B, written; may be NULL
  *   accept : device, B uint32, written 1 (accept) or 0 (reject)
- * A rejection is a result, not an error.
- * Errors: MVK_EINVAL, MVK_ENOMEM.
+ * A rejection is a result, not an error.  ell = ey->count must be 1..16.
+ * Errors: MVK_EINVAL, MVK_ERANGE (ell > 16 or B > 65535), MVK_ENOMEM.
  */
 mvk_status mvk_decode_verify(const mvk_key *key, const uint32_t *Xhat, const uint32_t *Yhat,
                              uint32_t B, const mvk_sparse *ex, const mvk_sparse *ey,
                              uint32_t *Y, uint32_t *vL, uint32_t *vR, uint32_t *accept,
                              void *stream);
+
+/*
+ * Verify, first half: the challenge syndromes R[q*m + i] = (Gy e_q)[i] for
+ * every repetition q < ey->count (R_q is the vector whose inner product with a
+ * response gives v_R = e_q^T (Gy^T Yhat_b), the transposition identity of
+ * App. B).  R depends only on the challenges, so a client may compute it
+ * before or while the server evaluates; the challenges must stay hidden from
+ * the server until the responses are fixed.
+ *   ey : ell = ey->count (1 <= ell <= 16) challenges of t_y positions < Ny
+ *   R  : device, ell x m field array, written
+ * Errors: MVK_EINVAL, MVK_ERANGE (ell > 16), MVK_ENOMEM.
+ */
+mvk_status mvk_verify_prepare(const mvk_key *key, const mvk_sparse *ey, uint32_t *R, void *stream);
+
+/*
+ * mvk_decode_verify with the challenge syndromes R computed beforehand by
+ * mvk_verify_prepare for the same key and the same ey (R is read, device,
+ * ell x m).  Same outputs, bit for bit.
+ * Errors: as mvk_decode_verify.
+ */
+mvk_status mvk_decode_verify_prepared(const mvk_key *key, const uint32_t *Xhat,
+                                      const uint32_t *Yhat, uint32_t B, const mvk_sparse *ex,
+                                      const mvk_sparse *ey, const uint32_t *R, uint32_t *Y,
+                                      uint32_t *vL, uint32_t *vR, uint32_t *accept, void *stream);
 
 /*
  * RAA encoding w -> G^T w (App. B, "Linear-time encoding") for `count`

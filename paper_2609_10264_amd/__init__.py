@@ -22,7 +22,7 @@ from ._lib import MVK_MAX_N, MVK_PRIME, MvkCode, MvkError, MvkKey, MvkSparse
 P = MVK_PRIME
 
 __all__ = ["P", "MVK_MAX_N", "MvkError", "Code", "Key", "server_eval", "keygen", "encode",
-           "decode_verify", "raa_encode", "raa_syndrome", "library_path"]
+           "decode_verify", "verify_prepare", "raa_encode", "raa_syndrome", "library_path"]
 
 
 def library_path() -> str:
@@ -149,11 +149,27 @@ def encode(key: Key, X: torch.Tensor, ex_idx: torch.Tensor, ex_val: torch.Tensor
     return out
 
 
+def verify_prepare(key: Key, ey_idx: torch.Tensor, ey_val: torch.Tensor, R: torch.Tensor | None = None,
+                   stream=None) -> torch.Tensor:
+    """Challenge syndromes R[q] = Gy e_q (ell x m) for decode_verify(..., R=R)."""
+    ell = ey_idx.shape[0]
+    if R is None:
+        R = torch.empty((ell, key.m), dtype=torch.int32, device=ey_idx.device)
+    ks = key.struct()
+    ey = _sparse(ey_idx, ey_val, "ey")
+    _lib.check("mvk_verify_prepare", _lib.load().mvk_verify_prepare(
+        ctypes.byref(ks), ctypes.byref(ey), _dev(R, torch.int32, (ell, key.m), "R"), _stream(stream)))
+    return R
+
+
 def decode_verify(key: Key, Xhat: torch.Tensor, Yhat: torch.Tensor, ex_idx: torch.Tensor, ex_val: torch.Tensor,
                   ey_idx: torch.Tensor, ey_val: torch.Tensor, Y: torch.Tensor | None = None,
                   vL: torch.Tensor | None = None, vR: torch.Tensor | None = None,
-                  accept: torch.Tensor | None = None, stream=None):
-    """Verify + Decrypt.  Returns (Y, accept, vL, vR); accept is int32 0/1 per column."""
+                  accept: torch.Tensor | None = None, stream=None, R: torch.Tensor | None = None):
+    """Verify + Decrypt.  Returns (Y, accept, vL, vR); accept is int32 0/1 per column.
+
+    R: challenge syndromes from verify_prepare for the same ey (optional; when
+    absent they are computed inside the call)."""
     B = Xhat.shape[0]
     ell = ey_idx.shape[0]
     dev = Xhat.device
@@ -166,10 +182,15 @@ def decode_verify(key: Key, Xhat: torch.Tensor, Yhat: torch.Tensor, ex_idx: torc
     ey = _sparse(ey_idx, ey_val, "ey")
     vLp = _dev(vL, torch.int32, (ell, B), "vL") if vL is not None else None
     vRp = _dev(vR, torch.int32, (ell, B), "vR") if vR is not None else None
-    _lib.check("mvk_decode_verify", _lib.load().mvk_decode_verify(
-        ctypes.byref(ks), _dev(Xhat, torch.int32, (B, key.n), "Xhat"), _dev(Yhat, torch.int32, (B, key.m), "Yhat"),
-        B, ctypes.byref(ex), ctypes.byref(ey), _dev(Y, torch.int32, (B, key.m), "Y"), vLp, vRp,
-        _dev(accept, torch.int32, (B,), "accept"), _stream(stream)))
+    common = (_dev(Xhat, torch.int32, (B, key.n), "Xhat"), _dev(Yhat, torch.int32, (B, key.m), "Yhat"),
+              B, ctypes.byref(ex), ctypes.byref(ey))
+    outs = (_dev(Y, torch.int32, (B, key.m), "Y"), vLp, vRp, _dev(accept, torch.int32, (B,), "accept"),
+            _stream(stream))
+    if R is None:
+        _lib.check("mvk_decode_verify", _lib.load().mvk_decode_verify(ctypes.byref(ks), *common, *outs))
+    else:
+        _lib.check("mvk_decode_verify_prepared", _lib.load().mvk_decode_verify_prepared(
+            ctypes.byref(ks), *common, _dev(R, torch.int32, (ell, key.m), "R"), *outs))
     return Y, accept, vL, vR
 
 

@@ -17,7 +17,7 @@ MVK_MAX_N = 131071
 MVK_PATH_AUTO = 0
 MVK_PATH_VALU = 1
 MVK_PATH_MFMA = 2
-ABI_VERSION = 1
+ABI_VERSION = 2
 
 # Every symbol include/mvk.h declares.
 EXPORTS = (
@@ -28,6 +28,8 @@ EXPORTS = (
     "mvk_keygen",
     "mvk_encode",
     "mvk_decode_verify",
+    "mvk_verify_prepare",
+    "mvk_decode_verify_prepared",
     "mvk_raa_encode",
     "mvk_raa_syndrome",
 )
@@ -100,6 +102,11 @@ def load() -> ctypes.CDLL:
     L.mvk_decode_verify.argtypes = [ctypes.POINTER(MvkKey), vp, vp, u32, ctypes.POINTER(MvkSparse),
                                     ctypes.POINTER(MvkSparse), vp, vp, vp, vp, vp]
     L.mvk_decode_verify.restype = st
+    L.mvk_verify_prepare.argtypes = [ctypes.POINTER(MvkKey), ctypes.POINTER(MvkSparse), vp, vp]
+    L.mvk_verify_prepare.restype = st
+    L.mvk_decode_verify_prepared.argtypes = [ctypes.POINTER(MvkKey), vp, vp, u32, ctypes.POINTER(MvkSparse),
+                                             ctypes.POINTER(MvkSparse), vp, vp, vp, vp, vp, vp]
+    L.mvk_decode_verify_prepared.restype = st
     L.mvk_raa_encode.argtypes = [ctypes.POINTER(MvkCode), vp, u32, vp, vp]
     L.mvk_raa_encode.restype = st
     L.mvk_raa_syndrome.argtypes = [ctypes.POINTER(MvkCode), vp, u32, vp, vp]

@@ -16,45 +16,53 @@ namespace {
 
 struct Workspace {
     void* ptr = nullptr;
-    size_t size = 0;
+    size_t size = 0;  // bytes of the whole buffer
+    size_t ctrl = 0;  // bytes of the control region at its start
 };
 
 std::mutex g_ws_mu;
 std::map<std::pair<int, hipStream_t>, Workspace>* g_ws = nullptr;
 
-// Bytes at the start of every workspace reserved for control words (zeroed
-// when the workspace is allocated; kernels that use them leave them zero).
-constexpr size_t kCtrlBytes = 256;
+// The first kCtrlBase bytes of every workspace hold control words; a call may
+// ask for a larger control region.  The control region is zeroed when the
+// workspace is allocated, and kernels that use it leave it zero.
+constexpr size_t kCtrlBase = 256;
 
 // Returns a device buffer of at least `bytes` private to (current device, s),
-// placed after the control words (*ctrl, may be null).  Growing waits for the
-// work already enqueued on `s` before freeing the old buffer, so earlier calls
-// on the same stream can still be using it.
-mvk_status workspace(hipStream_t s, size_t bytes, void** out, uint32_t** ctrl = nullptr) {
-    bytes += kCtrlBytes;
+// placed after the control region of at least `ctrl_bytes` (>= kCtrlBase;
+// *ctrl, may be null).  Growing waits for the work already enqueued on `s`
+// before freeing the old buffer, so earlier calls on the same stream can still
+// be using it; pointers from earlier calls are then invalid, so a call takes
+// everything it needs from one workspace() request.
+mvk_status workspace(hipStream_t s, size_t bytes, void** out, uint32_t** ctrl = nullptr, size_t ctrl_bytes = 0) {
+    ctrl_bytes = ctrl_bytes < kCtrlBase ? kCtrlBase : (ctrl_bytes + 255) & ~(size_t)255;
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return MVK_EHIP;
     std::lock_guard<std::mutex> lk(g_ws_mu);
     if (!g_ws) g_ws = new std::map<std::pair<int, hipStream_t>, Workspace>();
     Workspace& w = (*g_ws)[std::make_pair(dev, s)];
-    if (w.size < bytes) {
+    const size_t need_ctrl = ctrl_bytes > w.ctrl ? ctrl_bytes : w.ctrl;
+    if (w.size < need_ctrl + bytes || w.ctrl < need_ctrl) {
         if (w.ptr) {
             if (hipStreamSynchronize(s) != hipSuccess) return MVK_EHIP;
             (void)hipFree(w.ptr);
             w.ptr = nullptr;
             w.size = 0;
+            w.ctrl = 0;
         }
-        size_t sz = bytes < ((size_t)1 << 20) ? ((size_t)1 << 20) : bytes;
+        size_t sz = need_ctrl + bytes;
+        sz = sz < ((size_t)1 << 20) ? ((size_t)1 << 20) : sz;
         sz = (sz + 4095) & ~(size_t)4095;
         if (hipMalloc(&w.ptr, sz) != hipSuccess) {
             (void)hipGetLastError();
             w.ptr = nullptr;
             return MVK_ENOMEM;
         }
-        if (hipMemset(w.ptr, 0, kCtrlBytes) != hipSuccess) return MVK_EHIP;
+        if (hipMemset(w.ptr, 0, need_ctrl) != hipSuccess) return MVK_EHIP;
         w.size = sz;
+        w.ctrl = need_ctrl;
     }
-    *out = (char*)w.ptr + kCtrlBytes;
+    *out = (char*)w.ptr + w.ctrl;
     if (ctrl) *ctrl = (uint32_t*)w.ptr;
     return MVK_OK;
 }
@@ -76,6 +84,43 @@ mvk_status check_key(const mvk_key* key) {
     mvk_status st = check_code(&key->cx, key->n);
     if (st) return st;
     return check_code(&key->cy, key->m);
+}
+
+// Challenges of Verify: 1 <= ell <= kMaxEll repetitions of t_y positions < Ny.
+mvk_status check_challenges(const mvk_key* key, const mvk_sparse* ey) {
+    if (!ey || ey->count == 0 || ey->t == 0 || !ey->idx || !ey->val) return MVK_EINVAL;
+    if (ey->count > kMaxEll) return MVK_ERANGE;
+    if ((uint64_t)ey->t > (uint64_t)key->cy.r * key->m) return MVK_EINVAL;
+    return MVK_OK;
+}
+
+mvk_status check_decode_verify(const mvk_key* key, const uint32_t* Xhat, const uint32_t* Yhat, uint32_t B,
+                               const mvk_sparse* ex, const mvk_sparse* ey, const uint32_t* Y,
+                               const uint32_t* accept) {
+    mvk_status st = check_key(key);
+    if (st) return st;
+    if (B == 0) return MVK_OK;
+    if (!key->PT || !key->Q || !Xhat || !Yhat || !Y || !accept || !ex) return MVK_EINVAL;
+    if (ex->count != B || (ex->t && (!ex->idx || !ex->val))) return MVK_EINVAL;
+    if ((uint64_t)ex->t > (uint64_t)key->cx.r * key->n) return MVK_EINVAL;
+    st = check_challenges(key, ey);
+    if (st) return st;
+    if (B > 65535u) return MVK_ERANGE;
+    return MVK_OK;
+}
+
+// Control region of decode_verify: the counter (first 256 bytes), then the
+// 2*ell*B 64-bit accumulators.
+inline size_t dv_ctrl_bytes(uint32_t ell, uint32_t B) { return kCtrlBase + (size_t)2 * ell * B * 8; }
+
+hipError_t launch_dv(const mvk_key* key, const uint32_t* Xhat, const uint32_t* Yhat, uint32_t B,
+                     const mvk_sparse* ex, const mvk_sparse* ey, const uint32_t* R, uint32_t* Y, uint32_t* vL,
+                     uint32_t* vR, uint32_t* accept, uint32_t* ctrl, hipStream_t s) {
+    const uint32_t m = key->m, n = key->n;
+    const uint32_t Nx = key->cx.r * n, Ny = key->cy.r * m;
+    return launch_decode_verify(key->PT, key->Q, m, n, Nx, Ny, Xhat, Yhat, B, ex->idx, ex->val, ex->t, ey->idx,
+                                ey->val, ey->t, ey->count, R, Y, (unsigned long long*)((char*)ctrl + kCtrlBase),
+                                &ctrl[0], vL, vR, accept, s);
 }
 
 }  // namespace
@@ -158,39 +203,53 @@ mvk_status mvk_encode(const mvk_key* key, const uint32_t* X, uint32_t B, const m
     return hip_status(launch_syn_sparse(key->cx, ex->idx, ex->val, ex->t, B, X, (uint32_t*)ws, Xhat, s));
 }
 
+mvk_status mvk_verify_prepare(const mvk_key* key, const mvk_sparse* ey, uint32_t* R, void* stream) {
+    mvk_status st = check_key(key);
+    if (st) return st;
+    if (!R) return MVK_EINVAL;
+    st = check_challenges(key, ey);
+    if (st) return st;
+    hipStream_t s = (hipStream_t)stream;
+    const size_t Ny = (size_t)key->cy.r * key->m;
+    void* ws = nullptr;
+    st = workspace(s, Ny > kSynScratchAbove ? (size_t)ey->count * 2 * Ny * 4 : 0, &ws);
+    if (st) return st;
+    return hip_status(launch_syn_sparse(key->cy, ey->idx, ey->val, ey->t, ey->count, nullptr, (uint32_t*)ws, R, s));
+}
+
+mvk_status mvk_decode_verify_prepared(const mvk_key* key, const uint32_t* Xhat, const uint32_t* Yhat, uint32_t B,
+                                      const mvk_sparse* ex, const mvk_sparse* ey, const uint32_t* R, uint32_t* Y,
+                                      uint32_t* vL, uint32_t* vR, uint32_t* accept, void* stream) {
+    mvk_status st = check_decode_verify(key, Xhat, Yhat, B, ex, ey, Y, accept);
+    if (st || B == 0) return st;
+    if (!R) return MVK_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    void* ws = nullptr;
+    uint32_t* ctrl = nullptr;
+    st = workspace(s, 0, &ws, &ctrl, dv_ctrl_bytes(ey->count, B));
+    if (st) return st;
+    return hip_status(launch_dv(key, Xhat, Yhat, B, ex, ey, R, Y, vL, vR, accept, ctrl, s));
+}
+
 mvk_status mvk_decode_verify(const mvk_key* key, const uint32_t* Xhat, const uint32_t* Yhat, uint32_t B,
                              const mvk_sparse* ex, const mvk_sparse* ey, uint32_t* Y, uint32_t* vL, uint32_t* vR,
                              uint32_t* accept, void* stream) {
-    mvk_status st = check_key(key);
-    if (st) return st;
-    if (B == 0) return MVK_OK;
-    if (!key->PT || !key->Q || !Xhat || !Yhat || !Y || !accept || !ex || !ey) return MVK_EINVAL;
-    if (ex->count != B || (ex->t && (!ex->idx || !ex->val))) return MVK_EINVAL;
-    if (ey->count == 0 || ey->t == 0 || !ey->idx || !ey->val) return MVK_EINVAL;
+    mvk_status st = check_decode_verify(key, Xhat, Yhat, B, ex, ey, Y, accept);
+    if (st || B == 0) return st;
     hipStream_t s = (hipStream_t)stream;
-    const uint32_t m = key->m, n = key->n, ell = ey->count;
-    const uint32_t Nx = key->cx.r * n, Ny = key->cy.r * m;
-    if (ex->t > Nx || ey->t > Ny) return MVK_EINVAL;
-    if (B > 65535u) return MVK_ERANGE;
-    const uint32_t nblkR = ceil_div(m, kClientCols), nblkL = ceil_div(n, kClientCols);
+    const uint32_t m = key->m, ell = ey->count;
+    const size_t Ny = (size_t)key->cy.r * m;
     const size_t r_bytes = align_up((size_t)ell * m * 4);
-    const size_t syn_bytes = (size_t)Ny > kSynScratchAbove ? align_up((size_t)ell * 2 * Ny * 4) : 0;
-    const size_t pl_bytes = align_up((size_t)ell * B * nblkL * 4);
-    const size_t pr_bytes = align_up((size_t)ell * B * nblkR * 4);
+    const size_t syn_bytes = Ny > kSynScratchAbove ? align_up((size_t)ell * 2 * Ny * 4) : 0;
     void* ws = nullptr;
     uint32_t* ctrl = nullptr;
-    st = workspace(s, r_bytes + syn_bytes + pl_bytes + pr_bytes, &ws, &ctrl);
+    st = workspace(s, r_bytes + syn_bytes, &ws, &ctrl, dv_ctrl_bytes(ell, B));
     if (st) return st;
-    char* base = (char*)ws;
-    uint32_t* rv = (uint32_t*)base;
-    uint32_t* syn_scratch = (uint32_t*)(base + r_bytes);
-    uint32_t* partL = (uint32_t*)(base + r_bytes + syn_bytes);
-    uint32_t* partR = (uint32_t*)(base + r_bytes + syn_bytes + pl_bytes);
+    uint32_t* rv = (uint32_t*)ws;
+    uint32_t* syn_scratch = (uint32_t*)((char*)ws + r_bytes);
     // r_q = Gy e_q for every repetition (shared by all columns)
     hipError_t e = launch_syn_sparse(key->cy, ey->idx, ey->val, ey->t, ell, nullptr, syn_scratch, rv, s);
-    if (e == hipSuccess)
-        e = launch_decode_verify(key->PT, key->Q, m, n, Nx, Ny, Xhat, Yhat, B, ex->idx, ex->val, ex->t, ey->idx,
-                                 ey->val, ey->t, ell, rv, Y, partL, partR, &ctrl[0], vL, vR, accept, s);
+    if (e == hipSuccess) e = launch_dv(key, Xhat, Yhat, B, ex, ey, rv, Y, vL, vR, accept, ctrl, s);
     return hip_status(e);
 }
 

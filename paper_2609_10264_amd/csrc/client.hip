@@ -12,9 +12,9 @@
 //           Both forms give the same field element.
 //
 // Dot products are accumulated in 64 bits from folded products (< 2^32 each)
-// and reduced once per workgroup; per-workgroup partials (each < p) are summed
-// by the finalize kernel.  All sums are exact, so results do not depend on
-// the reduction order.
+// and reduced once per workgroup; the per-workgroup partials (each < p) are
+// added into 64-bit accumulators with atomics and reduced by the last
+// workgroup.  All sums are exact, so results do not depend on the order.
 #include "field.h"
 #include "mvk_internal.h"
 
@@ -49,13 +49,20 @@ constexpr int kGroups = kB / kCols;
 // with wave-uniform addresses (scalar loads).
 constexpr int kBatch = 16;
 
+// Prefetch depth of the per-lane values that do not depend on the gathers:
+// the r_q values of the decode role (repetitions q < kPreQ) and the query
+// values of the verify role (the first kPreB columns of each wave).
+constexpr int kPreQ = 4;
+constexpr int kPreB = 4;
+constexpr int kItems = kMaxEll;  // verify work items (repetition, chunk) per workgroup, at most
+
 // Decode role: columns [cb*kCols, cb*kCols + kCols) of response b.
 __device__ __forceinline__ void decode_part(const uint32_t* __restrict__ PT, uint32_t m, uint32_t Nx,
                                             const uint32_t* __restrict__ Yhat, uint32_t B,
                                             const uint32_t* __restrict__ ex_idx, const uint32_t* __restrict__ ex_val,
                                             uint32_t tx, const uint32_t* __restrict__ rv, uint32_t ell,
-                                            uint32_t* __restrict__ Y, uint32_t* __restrict__ partR, uint32_t b,
-                                            uint32_t cb, uint32_t nblkR, uint64_t (*part)[kCols]) {
+                                            uint32_t* __restrict__ Y, unsigned long long* accR, uint32_t b,
+                                            uint32_t cb, uint64_t (*part)[kCols]) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int g = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform group
     const uint32_t i = cb * kCols + lane;
@@ -64,6 +71,11 @@ __device__ __forceinline__ void decode_part(const uint32_t* __restrict__ PT, uin
     const uint32_t* ei = ex_idx + (size_t)b * tx;
     const uint32_t* ev = ex_val + (size_t)b * tx;
     const uint32_t yraw = Yhat[(size_t)b * m + is];
+    uint32_t rq[kPreQ];
+    if (g == 0) {
+#pragma unroll
+        for (int q = 0; q < kPreQ; ++q) rq[q] = rv[(size_t)((uint32_t)q < ell ? q : 0) * m + is];
+    }
     // group g takes the contiguous terms [g*chunk, min(tx, g*chunk + chunk))
     const uint32_t chunk = (tx + kGroups - 1) / kGroups;
     const uint32_t s_beg = (uint32_t)g * chunk;
@@ -92,31 +104,58 @@ __device__ __forceinline__ void decode_part(const uint32_t* __restrict__ PT, uin
         for (int h = 0; h < kGroups; ++h) tot += part[h][lane];
         const uint32_t yh = act ? yraw : 0u;
         if (act) Y[(size_t)b * m + i] = fsub(yh, fred64(tot));
+        // v_R partial: sum over this block's outputs of r_q[i] * yhat[i]
         for (uint32_t q = 0; q < ell; ++q) {
-            const uint64_t prod = ffold((uint64_t)rv[(size_t)q * m + is] * yh);
-            const uint64_t ws = wave_sum_u64(prod);
-            if (lane == 0) partR[((size_t)q * B + b) * nblkR + cb] = fred64(ws);
+            uint32_t r = 0;
+#pragma unroll
+            for (int u = 0; u < kPreQ; ++u)
+                if ((uint32_t)u == q) r = rq[u];
+            if (q >= (uint32_t)kPreQ) r = rv[(size_t)q * m + is];
+            const uint64_t ws = wave_sum_u64(ffold((uint64_t)r * yh));
+            if (lane == 0) atomicAdd(&accR[(size_t)q * B + b], (unsigned long long)fred64(ws));
         }
     }
 }
 
-// Verify role: columns [cb*kCols, cb*kCols + kCols) of u_q = e_q^T Q.
+// v_L partials of one query column: sum over this block's k of u_q[k] * x[k].
+__device__ __forceinline__ void verify_column(const uint32_t (*u_s)[kCols], uint32_t ell, uint32_t B, uint32_t b,
+                                              uint32_t x, unsigned long long* accL) {
+    const int lane = threadIdx.x & 63;
+    for (uint32_t q = 0; q < ell; ++q) {
+        const uint64_t ws = wave_sum_u64(ffold((uint64_t)u_s[q][lane] * x));
+        if (lane == 0) atomicAdd(&accL[(size_t)q * B + b], (unsigned long long)fred64(ws));
+    }
+}
+
+// Verify role: columns [cb*kCols, cb*kCols + kCols) of u_q = e_q^T Q for every
+// repetition q.  The ell*ty terms are cut into work items (repetition q, chunk
+// c), C chunks per repetition so that the kGroups waves are busy, and the waves
+// take the items round robin; every item is one or more batches of gathers.
 __device__ __forceinline__ void verify_part(const uint32_t* __restrict__ Q, uint32_t n, uint32_t Ny,
                                             const uint32_t* __restrict__ Xhat, uint32_t B,
                                             const uint32_t* __restrict__ ey_idx, const uint32_t* __restrict__ ey_val,
-                                            uint32_t ty, uint32_t ell, uint32_t* __restrict__ partL, uint32_t cb,
-                                            uint32_t nblkL, uint64_t (*part)[kCols], uint32_t* u_s) {
+                                            uint32_t ty, uint32_t ell, unsigned long long* accL, uint32_t cb,
+                                            uint64_t (*part)[kCols], uint32_t (*u_s)[kCols]) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int g = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform group
     const uint32_t k = cb * kCols + lane;
     const bool act = k < n;
     const uint32_t ks = act ? k : 0u;
-    const uint32_t chunk = (ty + kGroups - 1) / kGroups;
-    const uint32_t s_beg = (uint32_t)g * chunk;
-    const uint32_t s_end = s_beg + chunk < ty ? s_beg + chunk : ty;
-    for (uint32_t q = 0; q < ell; ++q) {
+    uint32_t xp[kPreB];
+#pragma unroll
+    for (int u = 0; u < kPreB; ++u) {
+        const uint32_t b = (uint32_t)g + kGroups * u;
+        xp[u] = Xhat[(size_t)(b < B ? b : 0u) * n + ks];
+    }
+    const uint32_t C = ell >= (uint32_t)kGroups ? 1u : (uint32_t)kGroups / ell;
+    const uint32_t chunk = (ty + C - 1) / C;
+    const uint32_t items = ell * C;
+    for (uint32_t w = g; w < items; w += kGroups) {
+        const uint32_t q = w / C, c = w % C;
         const uint32_t* ei = ey_idx + (size_t)q * ty;
         const uint32_t* ev = ey_val + (size_t)q * ty;
+        const uint32_t s_beg = c * chunk;
+        const uint32_t s_end = s_beg + chunk < ty ? s_beg + chunk : ty;
         uint64_t acc = 0;
         for (uint32_t s0 = s_beg; s0 < s_end; s0 += kBatch) {
             uint32_t qv[kBatch], ww[kBatch];
@@ -133,74 +172,69 @@ __device__ __forceinline__ void verify_part(const uint32_t* __restrict__ Q, uint
 #pragma unroll
             for (int u = 0; u < kBatch; ++u) acc += ffold((uint64_t)ww[u] * qv[u]);
         }
-        part[g][lane] = acc;
-        __syncthreads();
-        if (g == 0) {
-            uint64_t tot = 0;
-#pragma unroll
-            for (int h = 0; h < kGroups; ++h) tot += part[h][lane];
-            u_s[lane] = act ? fred64(tot) : 0u;  // (e_q^T Q)[k]
-        }
-        __syncthreads();
-        const uint32_t u = u_s[lane];
-        for (uint32_t b = g; b < B; b += kGroups) {
-            const uint32_t x = Xhat[(size_t)b * n + ks];
-            const uint64_t ws = wave_sum_u64(ffold((uint64_t)u * x));
-            if (lane == 0) partL[((size_t)q * B + b) * nblkL + cb] = fred64(ws);
-        }
-        __syncthreads();
+        part[w][lane] = acc;
     }
+    __syncthreads();
+    for (uint32_t q = g; q < ell; q += kGroups) {
+        uint64_t tot = 0;
+        for (uint32_t c = 0; c < C; ++c) tot += part[q * C + c][lane];
+        u_s[q][lane] = act ? fred64(tot) : 0u;  // (e_q^T Q)[k]
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kPreB; ++u) {
+        const uint32_t b = (uint32_t)g + kGroups * u;
+        if (b < B) verify_column(u_s, ell, B, b, xp[u], accL);
+    }
+    for (uint32_t b = (uint32_t)g + kGroups * kPreB; b < B; b += kGroups)
+        verify_column(u_s, ell, B, b, Xhat[(size_t)b * n + ks], accL);
 }
 
 // One launch for Decrypt, the two inner products of Verify and the final
 // comparison.  Workgroups [0, B*nblkR) take the decode role, the next nblkL
-// the verify role.  Every workgroup publishes its partial sums, then counts
-// itself done on `counter`; the workgroup that finishes last (it sees
-// count == gridDim.x - 1) sums all partials, writes vL, vR and accept, and
-// resets the counter to zero for the next launch.
+// the verify role.  Every workgroup adds its partial sums (each < p) into the
+// 64-bit accumulators accL / accR (ell x B each; exact, so the order of the
+// additions does not matter), then counts itself done on `counter`; the
+// workgroup that finishes last (it sees count == gridDim.x - 1) reads and
+// clears the accumulators, writes vL, vR and accept, and resets the counter,
+// so every launch leaves the accumulators and the counter at zero.
 __global__ __launch_bounds__(kB) void decode_verify_fused(
     const uint32_t* __restrict__ PT, const uint32_t* __restrict__ Q, uint32_t m, uint32_t n, uint32_t Nx,
     uint32_t Ny, const uint32_t* __restrict__ Xhat, const uint32_t* __restrict__ Yhat, uint32_t B,
     const uint32_t* __restrict__ ex_idx, const uint32_t* __restrict__ ex_val, uint32_t tx,
     const uint32_t* __restrict__ ey_idx, const uint32_t* __restrict__ ey_val, uint32_t ty, uint32_t ell,
-    const uint32_t* __restrict__ rv, uint32_t* __restrict__ Y, uint32_t* partL, uint32_t* partR,
-    uint32_t nblkL, uint32_t nblkR, uint32_t* counter, uint32_t* __restrict__ vL, uint32_t* __restrict__ vR,
+    const uint32_t* __restrict__ rv, uint32_t* __restrict__ Y, unsigned long long* accL, unsigned long long* accR,
+    uint32_t nblkR, uint32_t* counter, uint32_t* __restrict__ vL, uint32_t* __restrict__ vR,
     uint32_t* __restrict__ accept) {
-    __shared__ uint64_t part[kGroups][kCols];
-    __shared__ uint32_t u_s[kCols];
+    __shared__ uint64_t part[kItems][kCols];
+    __shared__ uint32_t u_s[kMaxEll][kCols];
     __shared__ uint32_t last;
     const uint32_t bid = blockIdx.x;
     const uint32_t ndec = B * nblkR;
     if (bid < ndec)
-        decode_part(PT, m, Nx, Yhat, B, ex_idx, ex_val, tx, rv, ell, Y, partR, bid / nblkR, bid % nblkR, nblkR, part);
+        decode_part(PT, m, Nx, Yhat, B, ex_idx, ex_val, tx, rv, ell, Y, accR, bid / nblkR, bid % nblkR, part);
     else
-        verify_part(Q, n, Ny, Xhat, B, ey_idx, ey_val, ty, ell, partL, bid - ndec, nblkL, part, u_s);
+        verify_part(Q, n, Ny, Xhat, B, ey_idx, ey_val, ty, ell, accL, bid - ndec, part, u_s);
 
     __syncthreads();
     if (threadIdx.x == 0) {
-        __threadfence();  // publish this workgroup's partials
+        __threadfence();  // publish this workgroup's additions
         last = (atomicAdd(counter, 1u) == gridDim.x - 1) ? 1u : 0u;
     }
     __syncthreads();
     if (!last) return;
-    __threadfence();  // see every other workgroup's partials
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    for (uint32_t b = wave; b < B; b += kGroups) {
+    __threadfence();  // see every other workgroup's additions
+    for (uint32_t b = threadIdx.x; b < B; b += kB) {
         uint32_t ok = 1;
         for (uint32_t q = 0; q < ell; ++q) {
-            const uint32_t* pl = partL + ((size_t)q * B + b) * nblkL;
-            const uint32_t* pr = partR + ((size_t)q * B + b) * nblkR;
-            uint64_t l = 0, r = 0;
-            for (uint32_t t = lane; t < nblkL; t += 64) l += pl[t];
-            for (uint32_t t = lane; t < nblkR; t += 64) r += pr[t];
-            const uint32_t L = fred64(wave_sum_u64(l)), R = fred64(wave_sum_u64(r));
-            if (lane == 0) {
-                if (vL) vL[(size_t)q * B + b] = L;
-                if (vR) vR[(size_t)q * B + b] = R;
-            }
+            const size_t o = (size_t)q * B + b;
+            const uint32_t L = fred64(atomicExch(&accL[o], 0ull));
+            const uint32_t R = fred64(atomicExch(&accR[o], 0ull));
+            if (vL) vL[o] = L;
+            if (vR) vR[o] = R;
             ok &= (L == R) ? 1u : 0u;
         }
-        if (lane == 0) accept[b] = ok;
+        accept[b] = ok;
     }
     if (threadIdx.x == 0) atomicExch(counter, 0u);
 }
@@ -211,12 +245,13 @@ hipError_t launch_decode_verify(const uint32_t* PT, const uint32_t* Q, uint32_t 
                                 uint32_t Ny, const uint32_t* Xhat, const uint32_t* Yhat, uint32_t B,
                                 const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx, const uint32_t* ey_idx,
                                 const uint32_t* ey_val, uint32_t ty, uint32_t ell, const uint32_t* r, uint32_t* Y,
-                                uint32_t* partL, uint32_t* partR, uint32_t* counter, uint32_t* vL, uint32_t* vR,
+                                unsigned long long* acc, uint32_t* counter, uint32_t* vL, uint32_t* vR,
                                 uint32_t* accept, hipStream_t s) {
+    if (ell == 0 || ell > (uint32_t)kMaxEll) return hipErrorInvalidValue;
     const uint32_t nblkL = ceil_div(n, kCols), nblkR = ceil_div(m, kCols);
     const uint32_t grid = B * nblkR + nblkL;
     hipLaunchKernelGGL(decode_verify_fused, dim3(grid), dim3(kB), 0, s, PT, Q, m, n, Nx, Ny, Xhat, Yhat, B, ex_idx,
-                       ex_val, tx, ey_idx, ey_val, ty, ell, r, Y, partL, partR, nblkL, nblkR, counter, vL, vR,
+                       ex_val, tx, ey_idx, ey_val, ty, ell, r, Y, acc, acc + (size_t)ell * B, nblkR, counter, vL, vR,
                        accept);
     return hipGetLastError();
 }

@@ -26,7 +26,7 @@ hipError_t launch_encT_i8(const mvk_code& c, const int8_t* in, size_t ld_in, siz
                           uint32_t* t3, uint32_t* out, size_t ld_out, size_t vs_out, hipStream_t s);
 // Block lengths above this value run the syndrome in segments and need a
 // scratch of count x 2N words; up to it the syndrome runs in LDS.
-constexpr size_t kSynScratchAbove = 4096;
+constexpr size_t kSynScratchAbove = 16384;
 // G v for `count` vectors: dense (v: count x N) or sparse (idx/val: count x t).
 // If X != nullptr the result is added to X (out = X + G v), as in Encrypt.
 // scratch: count * 2N uint32.
@@ -42,14 +42,16 @@ hipError_t launch_fill_u32(uint32_t* p, size_t count, uint32_t value, hipStream_
 // client.hip ----------------------------------------------------------------
 constexpr uint32_t kClientBlock = 256;  // threads per workgroup of the gather kernels
 constexpr uint32_t kClientCols = 64;    // output columns per workgroup of the gather kernels
-// Decrypt + Verify in one launch (see client.hip).  partL: ell*B*ceil(n/64),
-// partR: ell*B*ceil(m/64) words; counter: one word that must be zero before
-// the first launch (every launch leaves it at zero).
+// Decrypt + Verify in one launch (see client.hip).  r: ell x m words,
+// r_q = Gy e_q.  acc: 2*ell*B 64-bit accumulators and counter: one word, all
+// zero before the first launch (every launch leaves them at zero).
+// ell <= kMaxEll.
+constexpr uint32_t kMaxEll = 16;
 hipError_t launch_decode_verify(const uint32_t* PT, const uint32_t* Q, uint32_t m, uint32_t n, uint32_t Nx,
                                 uint32_t Ny, const uint32_t* Xhat, const uint32_t* Yhat, uint32_t B,
                                 const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx, const uint32_t* ey_idx,
                                 const uint32_t* ey_val, uint32_t ty, uint32_t ell, const uint32_t* r, uint32_t* Y,
-                                uint32_t* partL, uint32_t* partR, uint32_t* counter, uint32_t* vL, uint32_t* vR,
+                                unsigned long long* acc, uint32_t* counter, uint32_t* vL, uint32_t* vR,
                                 uint32_t* accept, hipStream_t s);
 
 inline uint32_t ceil_div(uint32_t a, uint32_t b) { return (a + b - 1) / b; }

@@ -12,9 +12,10 @@
 //    batch (vector index innermost) is a coalesced 64-lane row.  The code arrays
 //    are indexed by the position only, which is uniform across the wave, so they
 //    come through scalar loads.
-//  * syn_block: few vectors (Encrypt: one per query column; Verify: one per
-//    repetition).  One 1024-thread workgroup owns one vector and runs the two
-//    suffix sums as tiled block scans.
+//  * syn_wg: few vectors (Encrypt: one per query column; Verify: one per
+//    repetition) of length up to 16384.  One 1024-thread workgroup owns one
+//    vector; both work arrays stay in LDS.
+//  * syn_p1/p2/p3: longer vectors, cut into segments over three launches.
 #include "field.h"
 #include "mvk_internal.h"
 
@@ -92,59 +93,21 @@ hipError_t launch_encT(const mvk_code& c, const T* in, size_t ld_in, size_t vs_i
 }
 
 // ---------------------------------------------------------------------------
-// Block scan (1024 threads, 4 consecutive elements per thread per tile).
+// Syndrome of short blocks: one 1024-thread workgroup per vector, N <= 16384.
+//
+// Both work arrays live in LDS as 1024 rows of E+1 words: position j sits at
+// word j + j/E, so row t holds positions [t*E, t*E + E) plus one pad word.
+// The suffix sums run over contiguous rows (thread t scans its own row, then
+// the row totals are scanned across the workgroup); the odd row stride E+1
+// keeps those row accesses free of bank conflicts.  The code arrays are read
+// with the position interleaved across threads (j = tid + 1024*u, coalesced)
+// and are all in flight before the first LDS phase; the scatters of Pi2 and
+// Pi1 use those registers.
 // ---------------------------------------------------------------------------
 constexpr int kSynThreads = 1024;
 constexpr int kSynWaves = kSynThreads / 64;
-
-__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x, int lane) {
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const uint32_t y = (uint32_t)__shfl_up((int)x, d);
-        if (lane >= d) x = fadd(x, y);
-    }
-    return x;
-}
-
-// Inclusive scan of a[0..N) in place; SUFFIX scans from the end.
-template <bool SUFFIX>
-__device__ void block_scan(uint32_t* a, uint32_t N, uint32_t* wsum /* kSynWaves + 1 */) {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    uint32_t carry = 0;
-    for (uint32_t base = 0; base < N; base += 4 * kSynThreads) {
-        uint32_t x[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const uint32_t sidx = base + 4 * tid + e;
-            x[e] = sidx < N ? a[SUFFIX ? N - 1 - sidx : sidx] : 0u;
-        }
-        x[1] = fadd(x[1], x[0]);
-        x[2] = fadd(x[2], x[1]);
-        x[3] = fadd(x[3], x[2]);
-        const uint32_t incl = wave_incl_scan(x[3], lane);
-        if (lane == 63) wsum[wave] = incl;
-        __syncthreads();
-        uint32_t t = 0, ti = 0;
-        if (wave == 0) {
-            t = lane < kSynWaves ? wsum[lane] : 0u;
-            ti = wave_incl_scan(t, lane);
-        }
-        __syncthreads();
-        if (wave == 0) {
-            if (lane < kSynWaves) wsum[lane] = fsub(ti, t);  // exclusive offset of each wave
-            if (lane == kSynWaves - 1) wsum[kSynWaves] = ti;  // tile total
-        }
-        __syncthreads();
-        const uint32_t off = fadd(carry, fadd(wsum[wave], fsub(incl, x[3])));
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const uint32_t sidx = base + 4 * tid + e;
-            if (sidx < N) a[SUFFIX ? N - 1 - sidx : sidx] = fadd(x[e], off);
-        }
-        carry = fadd(carry, wsum[kSynWaves]);
-        __syncthreads();
-    }
-}
+constexpr int kSynMaxU = 16;
+static_assert((size_t)kSynThreads * kSynMaxU == kSynScratchAbove, "LDS syndrome covers the scratch-free range");
 
 // Inclusive scan of one value per lane across the wave with DPP moves
 // (row shifts inside each 16-lane row, then row broadcasts across rows).
@@ -158,23 +121,22 @@ __device__ __forceinline__ uint32_t wave_incl_scan_dpp(uint32_t x) {
     return x;
 }
 
-// Largest block length kept entirely in LDS (two arrays of N words) and the
-// matching number of consecutive elements owned by one of the 1024 threads.
-// Block lengths up to this run in one workgroup (LDS); longer ones in segments.
-constexpr size_t kSynSingleMax = kSynScratchAbove;
-constexpr uint32_t kSynLdsN = (uint32_t)kSynSingleMax;
-constexpr int kSynMaxE = (kSynLdsN + kSynThreads - 1) / kSynThreads;
-
-// In-place inclusive suffix sum of a[0..N) held in LDS; thread t owns the E
-// consecutive elements [t*E, t*E + E).  The carry into a thread is the sum of
-// the totals of all later threads = grand total - inclusive prefix of totals.
 template <int E>
-__device__ __forceinline__ void lds_suffix_scan(uint32_t* a, uint32_t N, uint32_t* wsum) {
+__device__ __forceinline__ uint32_t pad_pos(uint32_t j) {
+    static_assert((E & (E - 1)) == 0, "E is a power of two: the row index is a shift");
+    return j + j / E;
+}
+
+// In-place inclusive suffix sum of the padded array `a` (all 1024*E
+// positions; positions >= N hold zero).  The carry into a row is the sum of
+// the totals of all later rows = grand total - inclusive prefix of totals.
+template <int E>
+__device__ __forceinline__ void row_suffix_scan(uint32_t* a, uint32_t* wsum) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const uint32_t base = (uint32_t)tid * E;
+    uint32_t* row = a + tid * (E + 1);
     uint32_t x[E];
 #pragma unroll
-    for (int e = 0; e < E; ++e) x[e] = (base + e < N) ? a[base + e] : 0u;
+    for (int e = 0; e < E; ++e) x[e] = row[e];
 #pragma unroll
     for (int e = E - 2; e >= 0; --e) x[e] = fadd(x[e], x[e + 1]);
     const uint32_t incl = wave_incl_scan_dpp(x[0]);
@@ -188,73 +150,128 @@ __device__ __forceinline__ void lds_suffix_scan(uint32_t* a, uint32_t N, uint32_
     }
     __syncthreads();
     const uint32_t before = wave ? wsum[kSynWaves + wave] : 0u;  // totals of earlier waves
-    const uint32_t prefix = fadd(before, incl);                   // totals of threads <= t
-    const uint32_t carry = fsub(wsum[kSynWaves], prefix);
+    const uint32_t carry = fsub(wsum[kSynWaves], fadd(before, incl));
 #pragma unroll
-    for (int e = 0; e < E; ++e)
-        if (base + e < N) a[base + e] = fadd(x[e], carry);
+    for (int e = 0; e < E; ++e) row[e] = fadd(x[e], carry);
     __syncthreads();
 }
 
-// One workgroup per vector with both work arrays in LDS.  The four code arrays
-// are loaded into registers first (position j = tid + 1024*e), so their
-// latency overlaps the initialisation of the first array.
-template <bool SPARSE, int E>
-__global__ __launch_bounds__(kSynThreads) void syn_lds(uint32_t k, uint32_t r, const uint32_t* __restrict__ pi1,
-                                                       const uint32_t* __restrict__ pi2,
-                                                       const uint32_t* __restrict__ v1,
-                                                       const uint32_t* __restrict__ v2,
-                                                       const uint32_t* __restrict__ vin,
-                                                       const uint32_t* __restrict__ idx,
-                                                       const uint32_t* __restrict__ val, uint32_t t,
-                                                       const uint32_t* __restrict__ X, uint32_t* __restrict__ out) {
-    __shared__ uint32_t A[kSynLdsN], Bv[kSynLdsN];
+// U: code positions per thread (N <= 1024*U); E: row length, the power of two
+// >= U.  The per-position loops are unconditional (positions >= N read a
+// valid LDS word and write to the writer's own pad word, which no scan
+// reads), so every LDS access of a loop is issued before the first wait.
+template <bool SPARSE, int U>
+__global__ __launch_bounds__(kSynThreads) void syn_wg(uint32_t k, uint32_t r, const uint32_t* __restrict__ pi1,
+                                                      const uint32_t* __restrict__ pi2,
+                                                      const uint32_t* __restrict__ v1,
+                                                      const uint32_t* __restrict__ v2,
+                                                      const uint32_t* __restrict__ vin,
+                                                      const uint32_t* __restrict__ idx,
+                                                      const uint32_t* __restrict__ val, uint32_t t,
+                                                      const uint32_t* __restrict__ X, uint32_t* __restrict__ out) {
+    constexpr int E = U <= 4 ? 4 : U <= 8 ? 8 : 16;
+    constexpr int kRow = E + 1;
+    constexpr int kXF = (U + 1) / 2;  // fold outputs per thread prefetched (all of them when r >= 2)
+    __shared__ uint32_t A[kSynThreads * kRow], Bv[kSynThreads * kRow];
     __shared__ uint32_t wsum[2 * kSynWaves + 2];
     const uint32_t c = blockIdx.x;
     const int tid = threadIdx.x;
     const uint32_t N = k * r;
-    // Unconditional loads at an in-range position (j < N, else 0), so all 4E
-    // loads are in flight together; positions >= N are never used below.
-    uint32_t p1[E], p2[E], w1[E], w2[E];
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-        const uint32_t j = tid + kSynThreads * e;
-        const uint32_t js = j < N ? j : 0u;
-        p1[e] = pi1[js];
-        p2[e] = pi2[js];
-        w1[e] = v1[js];
-        w2[e] = v2[js];
+    const uint32_t pad_slot = (uint32_t)tid * kRow + E;  // this thread's pad word
+    // Unconditional loads at an in-range position (j < N, else 0), so all of
+    // them are in flight together; positions >= N are never used below.  The
+    // first sparse term of this thread is loaded first: it is needed first.
+    uint32_t sj = 0, sv = 0;
+    if (SPARSE && t) {
+        const uint32_t q = (uint32_t)tid < t ? (uint32_t)tid : 0u;
+        sj = idx[(size_t)c * t + q];
+        sv = val[(size_t)c * t + q];
     }
-    if (SPARSE) {
-        for (uint32_t j = tid; j < N; j += kSynThreads) A[j] = 0u;
+    uint32_t p1[U], p2[U], w1[U], w2[U], xin[SPARSE ? 1 : U], xv[kXF];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const uint32_t j = tid + kSynThreads * u;
+        const uint32_t js = j < N ? j : 0u;
+        p1[u] = pi1[js];
+        p2[u] = pi2[js];
+        w1[u] = v1[js];
+        w2[u] = v2[js];
+        if constexpr (!SPARSE) xin[u] = vin[(size_t)c * N + js];
+    }
+    if (X) {
+#pragma unroll
+        for (int f = 0; f < kXF; ++f) {
+            const uint32_t i = tid + kSynThreads * f;
+            xv[f] = X[(size_t)c * k + (i < k ? i : 0u)];
+        }
+    }
+    // A = input, Bv = 0 (the Pi2 scatter fills [0, N); beyond N stays zero)
+    {
+        uint32_t* ra = A + tid * kRow;
+        uint32_t* rb = Bv + tid * kRow;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            if (SPARSE) ra[e] = 0u;
+            rb[e] = 0u;
+        }
+    }
+    if constexpr (SPARSE) {
         __syncthreads();
-        for (uint32_t q = tid; q < t; q += kSynThreads) {
+        if ((uint32_t)tid < t) A[pad_pos<E>(sj < N ? sj : N - 1)] = sv;
+        for (uint32_t q = tid + kSynThreads; q < t; q += kSynThreads) {
             const uint32_t j = idx[(size_t)c * t + q];
-            A[j < N ? j : N - 1] = val[(size_t)c * t + q];
+            A[pad_pos<E>(j < N ? j : N - 1)] = val[(size_t)c * t + q];
         }
     } else {
-        const uint32_t* src = vin + (size_t)c * N;
-        for (uint32_t j = tid; j < N; j += kSynThreads) A[j] = src[j];
-    }
-    __syncthreads();
-    lds_suffix_scan<E>(A, N, wsum);  // A
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-        const uint32_t j = tid + kSynThreads * e;
-        if (j < N) Bv[p2[e] < N ? p2[e] : N - 1] = fmul(w2[e], A[j]);  // V2, then Pi2 scatter
-    }
-    __syncthreads();
-    lds_suffix_scan<E>(Bv, N, wsum);  // A
+        for (int u = 0; u < U; ++u) {
+            const uint32_t j = tid + kSynThreads * u;
+            A[pad_pos<E>(j)] = j < N ? xin[u] : 0u;
+        }
+        // rows past N (positions the loop above does not cover) start at zero
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-        const uint32_t j = tid + kSynThreads * e;
-        if (j < N) A[p1[e] < N ? p1[e] : N - 1] = fmul(w1[e], Bv[j]);  // V1, then Pi1 scatter
+        for (int e = 0; e < E; ++e)
+            if ((uint32_t)tid * E + e >= (uint32_t)kSynThreads * U) A[tid * kRow + e] = 0u;
     }
     __syncthreads();
-    for (uint32_t i = tid; i < k; i += kSynThreads) {  // R: fold blocks of r
-        uint32_t s = 0;
-        for (uint32_t q = 0; q < r; ++q) s = fadd(s, A[(size_t)i * r + q]);
-        if (X) s = fadd(X[(size_t)c * k + i], s);
+    row_suffix_scan<E>(A, wsum);  // A
+#pragma unroll
+    for (int u = 0; u < U; ++u) {  // V2, then Pi2 scatter
+        const uint32_t j = tid + kSynThreads * u;
+        const uint32_t dst = j < N ? pad_pos<E>(p2[u] < N ? p2[u] : N - 1) : pad_slot;
+        Bv[dst] = fmul(w2[u], A[pad_pos<E>(j)]);
+    }
+    __syncthreads();
+    row_suffix_scan<E>(Bv, wsum);  // A
+#pragma unroll
+    for (int u = 0; u < U; ++u) {  // V1, then Pi1 scatter
+        const uint32_t j = tid + kSynThreads * u;
+        const uint32_t dst = j < N ? pad_pos<E>(p1[u] < N ? p1[u] : N - 1) : pad_slot;
+        A[dst] = fmul(w1[u], Bv[pad_pos<E>(j)]);
+    }
+    __syncthreads();
+    // R: fold blocks of r (+ X); reads at clamped positions, masked
+#pragma unroll
+    for (int f = 0; f < kXF; ++f) {
+        const uint32_t i = tid + kSynThreads * f;
+        const uint32_t is = i < k ? i : 0u;
+        uint32_t s = X ? xv[f] : 0u;
+        for (uint32_t q0 = 0; q0 < r; q0 += 4) {
+            uint32_t d[4];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const uint32_t q = q0 + v < r ? q0 + v : r - 1;
+                d[v] = A[pad_pos<E>(is * r + q)];
+            }
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                if (q0 + v < r) s = fadd(s, d[v]);
+        }
+        if (i < k) out[(size_t)c * k + i] = s;
+    }
+    for (uint32_t i = tid + kSynThreads * kXF; i < k; i += kSynThreads) {  // r = 1 only
+        uint32_t s = X ? X[(size_t)c * k + i] : 0u;
+        for (uint32_t q = 0; q < r; ++q) s = fadd(s, A[pad_pos<E>(i * r + q)]);
         out[(size_t)c * k + i] = s;
     }
 }
@@ -422,16 +439,17 @@ hipError_t launch_syn(const mvk_code& c, const uint32_t* v, const uint32_t* idx,
                       uint32_t count, const uint32_t* X, uint32_t* scratch, uint32_t* out, hipStream_t s) {
     if (count == 0) return hipSuccess;
     const size_t N = (size_t)c.k * c.r;
-    if (N <= kSynSingleMax) {
+    if (N <= (size_t)kSynThreads * kSynMaxU) {
         // short blocks: one workgroup per vector, everything in LDS
         const dim3 grid(count), block(kSynThreads);
-        const int E = (int)((N + kSynThreads - 1) / kSynThreads);
-#define MVK_SYN(EV)                                                                                         \
-    hipLaunchKernelGGL((syn_lds<SPARSE, EV>), grid, block, 0, s, c.k, c.r, c.pi1, c.pi2, c.v1, c.v2, v, idx, val, \
+        const size_t U = (N + kSynThreads - 1) / kSynThreads;
+#define MVK_SYN(EV)                                                                                        \
+    hipLaunchKernelGGL((syn_wg<SPARSE, EV>), grid, block, 0, s, c.k, c.r, c.pi1, c.pi2, c.v1, c.v2, v, idx, val, \
                        t, X, out)
-        if (E <= 1) MVK_SYN(1);
-        else if (E <= 2) MVK_SYN(2);
-        else MVK_SYN(4);
+        if (U <= 4) MVK_SYN(4);
+        else if (U <= 8) MVK_SYN(8);
+        else if (U <= 12) MVK_SYN(12);
+        else MVK_SYN(16);
 #undef MVK_SYN
         return hipGetLastError();
     }

@@ -74,3 +74,29 @@ def test_host_argument_checks_without_device_work():
     assert lib.mvk_raa_encode(ctypes.byref(bad), fake, 1, fake, None) == L.MVK_EINVAL
     nullcode = L.MvkCode(8, 2, 0, 0x1000, 0x1000, 0x1000)
     assert lib.mvk_raa_syndrome(ctypes.byref(nullcode), fake, 1, fake, None) == L.MVK_EINVAL
+
+
+def test_verify_argument_checks_without_device_work():
+    L = _lib()
+    lib = L.load()
+    fake = ctypes.c_void_p(0x1000)
+    code = L.MvkCode(8, 3, 0x1000, 0x1000, 0x1000, 0x1000)
+    key = L.MvkKey(8, 8, code, code, 0x1000, 0x1000)
+    ex = L.MvkSparse(0x1000, 0x1000, 2, 1)
+    too_many = L.MvkSparse(0x1000, 0x1000, 2, 17)  # more than 16 repetitions
+    none = L.MvkSparse(0x1000, 0x1000, 2, 0)
+    too_long = L.MvkSparse(0x1000, 0x1000, 25, 2)  # t_y > Ny = 24
+    for ey, want in ((too_many, L.MVK_ERANGE), (none, L.MVK_EINVAL), (too_long, L.MVK_EINVAL)):
+        assert lib.mvk_verify_prepare(ctypes.byref(key), ctypes.byref(ey), fake, None) == want
+        assert lib.mvk_decode_verify(ctypes.byref(key), fake, fake, 1, ctypes.byref(ex), ctypes.byref(ey),
+                                     fake, None, None, fake, None) == want
+        assert lib.mvk_decode_verify_prepared(ctypes.byref(key), fake, fake, 1, ctypes.byref(ex),
+                                              ctypes.byref(ey), fake, fake, None, None, fake, None) == want
+    ey = L.MvkSparse(0x1000, 0x1000, 2, 2)
+    assert lib.mvk_verify_prepare(ctypes.byref(key), ctypes.byref(ey), None, None) == L.MVK_EINVAL
+    assert lib.mvk_decode_verify_prepared(ctypes.byref(key), fake, fake, 1, ctypes.byref(ex), ctypes.byref(ey),
+                                          None, fake, None, None, fake, None) == L.MVK_EINVAL
+    # noise of the wrong column count
+    ex3 = L.MvkSparse(0x1000, 0x1000, 2, 3)
+    assert lib.mvk_decode_verify(ctypes.byref(key), fake, fake, 1, ctypes.byref(ex3), ctypes.byref(ey),
+                                 fake, None, None, fake, None) == L.MVK_EINVAL

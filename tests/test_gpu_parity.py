@@ -106,8 +106,11 @@ def test_server_eval_repeatable_and_noncontiguous_offsets():
 # ---------------------------------------------------------------------------
 # RAA encoding / syndrome
 # ---------------------------------------------------------------------------
+# N = k*r spans every single-workgroup tile size (N <= 4096, 8192, 12288,
+# 16384, each with a ragged last row) and the segmented path above 16384.
 @pytest.mark.parametrize("k,r,count", [(1, 1, 1), (5, 2, 3), (256, 2, 2), (1000, 3, 4), (4097, 4, 2), (700, 5, 65),
-                                         (6000, 4, 2), (5056, 4, 1)])
+                                         (6000, 4, 2), (5056, 4, 1), (2048, 4, 2), (2731, 3, 2), (4096, 3, 3),
+                                         (5461, 3, 1), (4096, 4, 2), (16384, 1, 1), (1366, 6, 2)])
 def test_raa_encode_and_syndrome(k, r, count):
     _say(f"raa k={k} r={r} count={count}")
     c = synth.raa_code(300 + k + r, k, r)
@@ -177,6 +180,72 @@ def test_protocol_small(cid, m, n, B, r, tx):
         assert not oacc[b]
         assert np.array_equal(host(vLb), ovL) and np.array_equal(host(vRb), ovR)
         assert np.array_equal(host(Yb), oracle.decode(PT, bad, inst.exi, inst.exv))
+
+
+# Sparse syndromes (encode: one per column; verify_prepare: one per
+# repetition) at block lengths in every tile size of the single-workgroup
+# kernel and in the segmented range.
+@pytest.mark.parametrize("n,r,B,tx", [(1366, 3, 2, 64), (2048, 4, 3, 7), (4096, 3, 1, 64), (5461, 3, 2, 128),
+                                       (4096, 4, 1, 100), (4097, 4, 2, 64), (8192, 4, 1, 128), (16384, 1, 1, 1)])
+def test_sparse_syndrome_lengths(n, r, B, tx):
+    _say(f"sparse syndrome n={n} r={r} B={B} tx={tx}")
+    # the same shape as privacy code (n) and as verification code (m = n)
+    inst = Instance(70 + r, n, n, B, r, tx, ty=31, ell=3).to_device()
+    Xh = mvk.encode(inst.key, inst.dX, inst.dexi, inst.dexv)
+    assert np.array_equal(host(Xh), oracle.encode(inst.cx, inst.X, inst.exi, inst.exv))
+    R = host(mvk.verify_prepare(inst.key, inst.deyi, inst.deyv))
+    for q in range(inst.eyi.shape[0]):
+        e = np.zeros(inst.cy["N"], dtype=np.uint32)
+        e[inst.eyi[q]] = inst.eyv[q]
+        assert np.array_equal(R[q], oracle.syn(inst.cy, e)), q
+
+
+def test_prepared_verify_matches_unprepared():
+    """decode_verify with R from verify_prepare (on another stream) = decode_verify."""
+    inst = Instance(53, 700, 333, 4, 3, 9, ell=2).to_device()
+    mvk.keygen(inst.key, inst.dW)
+    PT, Q = oracle.keygen(inst.W, inst.cx, inst.cy)
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        R = mvk.verify_prepare(inst.key, inst.deyi, inst.deyv, stream=side)
+    dXh = mvk.encode(inst.key, inst.dX, inst.dexi, inst.dexv)
+    Xh = host(dXh)
+    Yh = oracle.server_eval(inst.W, Xh)
+    pos, delta = synth.tamper_delta(synth.seed_for(53, synth.PURPOSE_TAMPER), 4, 700)
+    Yh[2, pos[2]] = (int(Yh[2, pos[2]]) + int(delta[2])) % P
+    torch.cuda.current_stream().wait_stream(side)
+    outs = []
+    for RR in (None, R):
+        vL = torch.empty((2, 4), dtype=torch.int32, device="cuda")
+        vR = torch.empty_like(vL)
+        Y, acc, vL, vR = mvk.decode_verify(inst.key, dXh, dev(Yh), inst.dexi, inst.dexv, inst.deyi, inst.deyv,
+                                           vL=vL, vR=vR, R=RR)
+        outs.append([host(t) for t in (Y, acc, vL, vR)])
+    oacc, ovL, ovR = oracle.verify(inst.cy, Q, Xh, Yh, inst.eyi, inst.eyv)
+    for Y, acc, vL, vR in outs:
+        assert acc.tolist() == oacc.astype(np.uint32).tolist() == [1, 1, 0, 1]
+        assert np.array_equal(vL, ovL) and np.array_equal(vR, ovR)
+        assert np.array_equal(Y, oracle.decode(PT, Yh, inst.exi, inst.exv))
+
+
+@pytest.mark.parametrize("ell,ty", [(1, 31), (3, 5), (5, 31), (16, 2)])
+def test_verify_repetition_counts(ell, ty):
+    """Work-item split of the verify role for 1..16 repetitions (the maximum)."""
+    _say(f"verify ell={ell} ty={ty}")
+    inst = Instance(54, 130, 200, 3, 2, 4, ty=ty, ell=ell).to_device()
+    mvk.keygen(inst.key, inst.dW)
+    _, Q = oracle.keygen(inst.W, inst.cx, inst.cy)
+    dXh = mvk.encode(inst.key, inst.dX, inst.dexi, inst.dexv)
+    Xh = host(dXh)
+    Yh = oracle.server_eval(inst.W, Xh)
+    Yh[1, 7] = (int(Yh[1, 7]) + 1) % P
+    vL = torch.empty((ell, 3), dtype=torch.int32, device="cuda")
+    vR = torch.empty_like(vL)
+    _, acc, vL, vR = mvk.decode_verify(inst.key, dXh, dev(Yh), inst.dexi, inst.dexv, inst.deyi, inst.deyv,
+                                       vL=vL, vR=vR)
+    oacc, ovL, ovR = oracle.verify(inst.cy, Q, Xh, Yh, inst.eyi, inst.eyv)
+    assert np.array_equal(host(vL), ovL) and np.array_equal(host(vR), ovR)
+    assert host(acc).tolist() == oacc.astype(np.uint32).tolist()
 
 
 def test_encode_without_noise_is_identity():

@@ -76,6 +76,9 @@ def parse():
                     help="after timing, copy this many MiB device-to-device (reference kernel for HBM counters)")
     ap.add_argument("--seed", type=int, default=2609)
     ap.add_argument("--path", default="auto", choices=["auto", "valu", "mfma"], help="server_eval kernel family")
+    ap.add_argument("--weights", default="packed", choices=["packed", "rowmajor"],
+                    help="server weight layout: packed once into matrix-core operand order (untimed, like "
+                         "keygen), or row-major as given")
     ap.add_argument("--m", type=int, default=0, help="override the workload's row count (server-only)")
     ap.add_argument("--n", type=int, default=0, help="override the workload's column count (server-only)")
     ap.add_argument("--B", type=int, default=0, help="override the workload's query count (server-only)")
@@ -134,7 +137,7 @@ def main():
         Wj = torch.randint(-127, 128, (m, n), generator=gen, device=dev, dtype=torch.int8)
         kj = mvk.Key.allocate(m, n, cx, cy)
         mvk.keygen(kj, Wj)
-        Ws.append(Wj)
+        Ws.append(mvk.pack_weights(Wj) if args.weights == "packed" else Wj)
         keys.append(kj)
     X = torch.randint(0, mvk.P, (total_steps, B, n), generator=gen, device=dev, dtype=torch.int32)
     exi, exv = synth.sparse(synth.seed_for(cid, synth.PURPOSE_NOISE, 7), total_steps * B, cx.N, tx)
@@ -258,7 +261,7 @@ def main():
         "config": {"workload": f"{args.config}: W {m}x{n} int8-valued in F_p (p=2^31-1), B={B} query column(s), "
                                f"RAA r={r}, t_x={tx}, t_y={ty}, ell={ell}; step = encode+server_eval+decode_verify",
                    "global_batch": B, "w_pool": pool, "launch": "eager" if args.eager else "hip_graph",
-                   "chains": C},
+                   "chains": C, "weights": args.weights},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(args.config),
                      "kernel": f"server_eval ({args.path})", "alg_bytes_per_launch": alg_bytes,
@@ -359,7 +362,7 @@ def stack_bench(args):
 
 
 def server_only(args, cfg, pool, total_steps, dev):
-    """server_eval alone over a rotated pool of W; events around every launch."""
+    """server_eval alone over a rotated pool of W, as a graph of back-to-back launches."""
     import numpy as np
     import torch
 
@@ -369,21 +372,34 @@ def server_only(args, cfg, pool, total_steps, dev):
     gen = torch.Generator(device=dev)
     gen.manual_seed(args.seed)
     Ws = [torch.randint(-127, 128, (m, n), generator=gen, device=dev, dtype=torch.int8) for _ in range(pool)]
+    if args.weights == "packed":
+        Ws = [mvk.pack_weights(W) for W in Ws]
     X = torch.randint(0, mvk.P, (pool, B, n), generator=gen, device=dev, dtype=torch.int32)
     Y = torch.empty((B, m), dtype=torch.int32, device=dev)
-    for i in range(args.warmup):
-        mvk.server_eval(Ws[i % pool], X[i % pool], out=Y, path=args.path)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        for i in range(max(args.warmup, pool)):
+            mvk.server_eval(Ws[i % pool], X[i % pool], out=Y, path=args.path, stream=s)
     torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    # K launches over the rotated pool captured as one HIP graph; HIP events on
+    # the launch stream around its replay give the mean launch time.
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        for i in range(args.steps):
+            mvk.server_eval(Ws[i % pool], X[i % pool], out=Y, path=args.path, stream=s)
+    with torch.cuda.stream(s):
+        g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
-    for i in range(args.steps):
-        ev[i][0].record()
-        mvk.server_eval(Ws[i % pool], X[i % pool], out=Y, path=args.path)
-        ev[i][1].record()
+    with torch.cuda.stream(s):
+        e0.record()
+        g.replay()
+        e1.record()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    ms = np.array([a.elapsed_time(b) for a, b in ev])
-    mean_s = 1e-3 * float(ms.mean())
+    mean_s = 1e-3 * e0.elapsed_time(e1) / args.steps
+    ms = np.array([1e3 * mean_s])
     alg_bytes = m * n + 4 * n * B + 4 * m * B
     macs = m * n * B
     out = {"metric": METRIC, "value": macs / mean_s, "unit": "modMAC/s", "n_gpus": 1, "steps": args.steps,
@@ -391,7 +407,7 @@ def server_only(args, cfg, pool, total_steps, dev):
            "scaling": "weak", "vs_baseline": None, "dtype": "i8xi8->i32 limb dot products, mod 2^31-1",
            "data": "synthetic",
            "config": {"workload": f"{args.config}: server_eval only, W {m}x{n} int8-valued, B={B}",
-                      "global_batch": B, "w_pool": pool},
+                      "global_batch": B, "w_pool": pool, "weights": args.weights},
            "roofline": {"bound": "hbm", "achieved": alg_bytes / mean_s / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                         "frac": alg_bytes / mean_s / 1e9 / HBM_PEAK_GBS, "traffic": None,
                         "kernel": f"server_eval ({args.path})", "alg_bytes_per_launch": alg_bytes,

@@ -37,7 +37,7 @@ extern "C" {
 #endif
 
 #define MVK_PRIME 2147483647u
-#define MVK_ABI_VERSION 2
+#define MVK_ABI_VERSION 3
 
 typedef int32_t mvk_status;
 #define MVK_OK 0
@@ -125,6 +125,25 @@ mvk_status mvk_server_eval(const int8_t *W, uint32_t m, uint32_t n, const uint32
  */
 mvk_status mvk_server_eval_path(const int8_t *W, uint32_t m, uint32_t n, const uint32_t *Xhat,
                                 uint32_t B, uint32_t *Yhat, int32_t path, void *stream);
+
+/*
+ * Server-side weight layout.  The server may store W once in MFMA operand
+ * order ("packed") instead of row-major: ceil(m/16) * ceil(n/64) tiles of
+ * 1 KiB, tile (rt, kb) holding rows 16*rt .. 16*rt+15 and columns
+ * 64*kb .. 64*kb+63 (zero beyond m and n), so that every W read of the server
+ * product is a contiguous 1 KiB run.  The product is the same field matrix-vector
+ * product as mvk_server_eval (Protocol pvMVMD, server step), bit for bit.
+ *
+ * mvk_packed_weight_bytes: size of the packed buffer (0 if m or n is 0).
+ * mvk_pack_weights: W (device, m x n int8, row-major) -> Wp (device, caller
+ *   allocated, mvk_packed_weight_bytes(m, n) bytes, 16-byte aligned).
+ * mvk_server_eval_packed: as mvk_server_eval with W given packed.
+ * Errors: MVK_EINVAL (null or misaligned pointer), MVK_ERANGE (n > MVK_MAX_N).
+ */
+size_t mvk_packed_weight_bytes(uint32_t m, uint32_t n);
+mvk_status mvk_pack_weights(const int8_t *W, uint32_t m, uint32_t n, int8_t *Wp, void *stream);
+mvk_status mvk_server_eval_packed(const int8_t *Wp, uint32_t m, uint32_t n, const uint32_t *Xhat,
+                                  uint32_t B, uint32_t *Yhat, void *stream);
 
 /*
  * Preprocess (Protocol pvMVMD): writes key->PT = (W Gx)^T and key->Q = Gy^T W

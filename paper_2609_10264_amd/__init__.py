@@ -21,7 +21,7 @@ from ._lib import MVK_MAX_N, MVK_PRIME, MvkCode, MvkError, MvkKey, MvkSparse
 
 P = MVK_PRIME
 
-__all__ = ["P", "MVK_MAX_N", "MvkError", "Code", "Key", "server_eval", "keygen", "encode",
+__all__ = ["P", "MVK_MAX_N", "MvkError", "Code", "Key", "PackedW", "pack_weights", "server_eval", "keygen", "encode",
            "decode_verify", "verify_prepare", "raa_encode", "raa_syndrome", "library_path"]
 
 
@@ -107,9 +107,39 @@ def _sparse(idx: torch.Tensor, val: torch.Tensor, name: str) -> MvkSparse:
 PATHS = {"auto": _lib.MVK_PATH_AUTO, "valu": _lib.MVK_PATH_VALU, "mfma": _lib.MVK_PATH_MFMA}
 
 
-def server_eval(W: torch.Tensor, Xhat: torch.Tensor, out: torch.Tensor | None = None, stream=None,
+class PackedW:
+    """W stored in matrix-core operand order (see mvk_pack_weights): a flat int8
+    device buffer plus the logical shape m x n."""
+
+    def __init__(self, data: torch.Tensor, m: int, n: int):
+        self.data, self.m, self.n = data, m, n
+
+    @property
+    def shape(self):
+        return (self.m, self.n)
+
+    @property
+    def device(self):
+        return self.data.device
+
+
+def pack_weights(W: torch.Tensor, out: torch.Tensor | None = None, stream=None) -> PackedW:
+    """Re-lay W (m x n int8, row-major) once into the packed server layout."""
+    m, n = W.shape
+    L = _lib.load()
+    nbytes = int(L.mvk_packed_weight_bytes(m, n))
+    if out is None:
+        out = torch.empty((max(nbytes, 1),), dtype=torch.int8, device=W.device)
+    if out.dtype != torch.int8 or not out.is_contiguous() or out.numel() < nbytes:
+        raise ValueError(f"out must be a contiguous int8 buffer of at least {nbytes} bytes")
+    _lib.check("mvk_pack_weights", L.mvk_pack_weights(_dev(W, torch.int8, (m, n), "W"), m, n, out.data_ptr(),
+                                                      _stream(stream)))
+    return PackedW(out, m, n)
+
+
+def server_eval(W, Xhat: torch.Tensor, out: torch.Tensor | None = None, stream=None,
                 path: str = "auto") -> torch.Tensor:
-    """Yhat = W Xhat mod p.  W: m x n int8; Xhat: B x n int32 field; returns B x m.
+    """Yhat = W Xhat mod p.  W: m x n int8 (or a PackedW); Xhat: B x n int32 field; returns B x m.
 
     path selects the kernel family ("auto", "valu" or "mfma"); results are identical.
     """
@@ -118,8 +148,13 @@ def server_eval(W: torch.Tensor, Xhat: torch.Tensor, out: torch.Tensor | None = 
     if out is None:
         out = torch.empty((B, m), dtype=torch.int32, device=W.device)
     L = _lib.load()
-    args = (_dev(W, torch.int8, (m, n), "W"), m, n, _dev(Xhat, torch.int32, (B, n), "Xhat"), B,
-            _dev(out, torch.int32, (B, m), "Yhat"))
+    tail = (m, n, _dev(Xhat, torch.int32, (B, n), "Xhat"), B, _dev(out, torch.int32, (B, m), "Yhat"))
+    if isinstance(W, PackedW):
+        if path == "valu":
+            raise ValueError("packed weights use the matrix-core kernels")
+        _lib.check("mvk_server_eval_packed", L.mvk_server_eval_packed(W.data.data_ptr(), *tail, _stream(stream)))
+        return out
+    args = (_dev(W, torch.int8, (m, n), "W"),) + tail
     if path == "auto":
         _lib.check("mvk_server_eval", L.mvk_server_eval(*args, _stream(stream)))
     else:

@@ -17,7 +17,7 @@ MVK_MAX_N = 131071
 MVK_PATH_AUTO = 0
 MVK_PATH_VALU = 1
 MVK_PATH_MFMA = 2
-ABI_VERSION = 2
+ABI_VERSION = 3
 
 # Every symbol include/mvk.h declares.
 EXPORTS = (
@@ -25,6 +25,9 @@ EXPORTS = (
     "mvk_abi_version",
     "mvk_server_eval",
     "mvk_server_eval_path",
+    "mvk_packed_weight_bytes",
+    "mvk_pack_weights",
+    "mvk_server_eval_packed",
     "mvk_keygen",
     "mvk_encode",
     "mvk_decode_verify",
@@ -95,6 +98,12 @@ def load() -> ctypes.CDLL:
     L.mvk_server_eval.restype = st
     L.mvk_server_eval_path.argtypes = [vp, u32, u32, vp, u32, vp, ctypes.c_int32, vp]
     L.mvk_server_eval_path.restype = st
+    L.mvk_packed_weight_bytes.argtypes = [u32, u32]
+    L.mvk_packed_weight_bytes.restype = ctypes.c_size_t
+    L.mvk_pack_weights.argtypes = [vp, u32, u32, vp, vp]
+    L.mvk_pack_weights.restype = st
+    L.mvk_server_eval_packed.argtypes = [vp, u32, u32, vp, u32, vp, vp]
+    L.mvk_server_eval_packed.restype = st
     L.mvk_keygen.argtypes = [ctypes.POINTER(MvkKey), vp, vp]
     L.mvk_keygen.restype = st
     L.mvk_encode.argtypes = [ctypes.POINTER(MvkKey), vp, u32, ctypes.POINTER(MvkSparse), vp, vp]

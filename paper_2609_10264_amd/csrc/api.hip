@@ -128,6 +128,31 @@ hipError_t launch_dv(const mvk_key* key, const uint32_t* Xhat, const uint32_t* Y
 
 using namespace mvk;
 
+namespace {
+mvk_status server_eval_impl(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* Xhat, uint32_t B,
+                            uint32_t* Yhat, int32_t path, bool packed, void* stream) {
+    if (path != MVK_PATH_AUTO && path != MVK_PATH_VALU && path != MVK_PATH_MFMA) return MVK_EINVAL;
+    if (packed && path == MVK_PATH_VALU) return MVK_EINVAL;
+    if (m == 0 || B == 0) return MVK_OK;
+    if (!Yhat) return MVK_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    if (n == 0) return hip_status(launch_fill_u32(Yhat, (size_t)m * B, 0u, s));
+    if (!W || !Xhat) return MVK_EINVAL;
+    if (n > MVK_MAX_N) return MVK_ERANGE;
+    if (packed && (uintptr_t)W % 16 != 0) return MVK_EINVAL;
+    void* ws = nullptr;
+    uint32_t* ctrl = nullptr;
+    const ServerEvalPlan pl = server_eval_plan(m, n, B, path, packed);
+    if (pl.ws_bytes || pl.ctrl_words) {
+        const mvk_status st = workspace(s, pl.ws_bytes, &ws, &ctrl, kCtrlBase + 4 * pl.ctrl_words);
+        if (st) return st;
+    }
+    // the row-block counters follow the first kCtrlBase bytes of the control region
+    uint32_t* counters = ctrl ? (uint32_t*)((char*)ctrl + kCtrlBase) : nullptr;
+    return hip_status(launch_server_eval(W, m, n, Xhat, B, Yhat, path, packed, ws, counters, s));
+}
+}  // namespace
+
 extern "C" {
 
 const char* mvk_status_str(mvk_status s) {
@@ -150,20 +175,21 @@ mvk_status mvk_server_eval(const int8_t* W, uint32_t m, uint32_t n, const uint32
 
 mvk_status mvk_server_eval_path(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* Xhat, uint32_t B,
                                 uint32_t* Yhat, int32_t path, void* stream) {
-    if (path != MVK_PATH_AUTO && path != MVK_PATH_VALU && path != MVK_PATH_MFMA) return MVK_EINVAL;
-    if (m == 0 || B == 0) return MVK_OK;
-    if (!Yhat) return MVK_EINVAL;
-    hipStream_t s = (hipStream_t)stream;
-    if (n == 0) return hip_status(launch_fill_u32(Yhat, (size_t)m * B, 0u, s));
-    if (!W || !Xhat) return MVK_EINVAL;
-    if (n > MVK_MAX_N) return MVK_ERANGE;
-    void* ws = nullptr;
-    const size_t wsb = server_eval_workspace(n, B, path);
-    if (wsb) {
-        const mvk_status st = workspace(s, wsb, &ws);
-        if (st) return st;
-    }
-    return hip_status(launch_server_eval(W, m, n, Xhat, B, Yhat, path, ws, s));
+    return server_eval_impl(W, m, n, Xhat, B, Yhat, path, false, stream);
+}
+
+size_t mvk_packed_weight_bytes(uint32_t m, uint32_t n) { return (m && n) ? packed_w_bytes(m, n) : 0; }
+
+mvk_status mvk_pack_weights(const int8_t* W, uint32_t m, uint32_t n, int8_t* Wp, void* stream) {
+    if (m == 0 || n == 0) return MVK_OK;
+    if (!W || !Wp) return MVK_EINVAL;
+    if ((uintptr_t)Wp % 16 != 0) return MVK_EINVAL;
+    return hip_status(launch_pack_w(W, m, n, Wp, (hipStream_t)stream));
+}
+
+mvk_status mvk_server_eval_packed(const int8_t* Wp, uint32_t m, uint32_t n, const uint32_t* Xhat, uint32_t B,
+                                  uint32_t* Yhat, void* stream) {
+    return server_eval_impl(Wp, m, n, Xhat, B, Yhat, MVK_PATH_AUTO, true, stream);
 }
 
 mvk_status mvk_keygen(const mvk_key* key, const int8_t* W, void* stream) {

@@ -216,14 +216,16 @@ __global__ __launch_bounds__(kB) void decode_verify_fused(
     else
         verify_part(Q, n, Ny, Xhat, B, ey_idx, ey_val, ty, ell, accL, bid - ndec, part, u_s);
 
+    // Ordering without cache-wide fences: the accumulators are touched only by
+    // atomics, which are performed at the device-wide coherence point.  Every
+    // wave waits for its atomics to complete (vmcnt 0) before the barrier, the
+    // counter increment follows the barrier, and the last workgroup reads the
+    // accumulators with atomics after seeing the final count.
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (threadIdx.x == 0) {
-        __threadfence();  // publish this workgroup's additions
-        last = (atomicAdd(counter, 1u) == gridDim.x - 1) ? 1u : 0u;
-    }
+    if (threadIdx.x == 0) last = (atomicAdd(counter, 1u) == gridDim.x - 1) ? 1u : 0u;
     __syncthreads();
     if (!last) return;
-    __threadfence();  // see every other workgroup's additions
     for (uint32_t b = threadIdx.x; b < B; b += kB) {
         uint32_t ok = 1;
         for (uint32_t q = 0; q < ell; ++q) {

@@ -11,10 +11,20 @@
 namespace mvk {
 
 // server_eval.hip
-// Workspace bytes launch_server_eval needs for (n, B, path) (0: none).
-size_t server_eval_workspace(uint32_t n, uint32_t B, int path);
+// What launch_server_eval needs besides its arguments: ws_bytes of workspace
+// and ctrl_words of counters that are zero before the launch (every launch
+// leaves them at zero).
+struct ServerEvalPlan {
+    size_t ws_bytes;
+    size_t ctrl_words;
+};
+ServerEvalPlan server_eval_plan(uint32_t m, uint32_t n, uint32_t B, int path, bool packed);
+// W: row-major m x n, or (packed) the layout written by launch_pack_w.
 hipError_t launch_server_eval(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t B,
-                              uint32_t* Y, int path, void* ws, hipStream_t s);
+                              uint32_t* Y, int path, bool packed, void* ws, uint32_t* counters, hipStream_t s);
+// Packed W: ceil(m/16) * ceil(n/64) tiles of 1 KiB in MFMA operand order.
+size_t packed_w_bytes(uint32_t m, uint32_t n);
+hipError_t launch_pack_w(const int8_t* W, uint32_t m, uint32_t n, int8_t* Wp, hipStream_t s);
 
 // raa.hip -------------------------------------------------------------------
 // G^T applied to `nvec` vectors whose element i of vector v sits at

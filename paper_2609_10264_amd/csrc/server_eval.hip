@@ -22,6 +22,8 @@
 // all R rows.  At the end the R*BQ*4 plane sums per thread are reduced across
 // the wave by a transpose-reduction (each exchange step halves the number of
 // live values) and across the four waves through LDS.
+#include <stdlib.h>
+
 #include "field.h"
 #include "mvk_internal.h"
 
@@ -206,7 +208,12 @@ typedef int32_t v4i __attribute__((ext_vector_type(4)));
 // 16 consecutive k of its quarter of the 64-block), so the k order inside the
 // instruction does not affect the sum.
 // ---------------------------------------------------------------------------
-template <int QB, int KW, int KBW, bool VEC>
+// W operand sources: row-major W read 16 bytes at a time (rows of whole 16-byte
+// granules, 16-byte aligned), row-major W read byte by byte, or W packed in
+// MFMA operand order (see pack_w_kernel).
+enum WLayout { kWRowVec = 0, kWRowScalar = 1, kWPacked = 2 };
+
+template <int QB, int KW, int KBW, bool VEC, int WL>
 __global__ __launch_bounds__(KW * 64) void server_eval_mfma_small(const int8_t* __restrict__ W, uint32_t m,
                                                                   uint32_t n, const uint32_t* __restrict__ X,
                                                                   uint32_t B, uint32_t* __restrict__ Y) {
@@ -267,10 +274,20 @@ __global__ __launch_bounds__(KW * 64) void server_eval_mfma_small(const int8_t* 
             // Unconditional load at an in-range address, masked at use: no
             // branches, so the waits can count outstanding loads.
             const uint32_t k = kc0 + (uint32_t)(wave * KBW + j) * 64 + kg * 16;
+            v4i t = {0, 0, 0, 0};
+            if (WL == kWPacked) {
+                // tile (row block, k-block) is 1 KiB in operand order, zero padded
+                const uint32_t kb = kc0 / 64 + (uint32_t)(wave * KBW + j);
+                const uint32_t nkb = (n + 63) / 64;
+                const bool okw = kb < nkb;
+                wmask[j] = okw ? -1 : 0;
+                t = *reinterpret_cast<const v4i*>(W + (((size_t)blockIdx.x * nkb + (okw ? kb : 0u)) * 64 + lane) * 16);
+                bw[j] = t;
+                continue;
+            }
             const bool okw = wrow < m && k < n;
             wmask[j] = okw ? -1 : 0;
-            v4i t = {0, 0, 0, 0};
-            if (VEC) {
+            if (WL == kWRowVec) {
                 t = *reinterpret_cast<const v4i*>(wbase + (okw ? k : 0u));
             } else {
 #pragma unroll
@@ -332,14 +349,21 @@ __global__ __launch_bounds__(KW * 64) void server_eval_mfma_small(const int8_t* 
 
 template <int QB, int KW, int KBW>
 hipError_t launch_mfma_small(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t B, uint32_t* Y,
-                             hipStream_t s) {
+                             bool packed, hipStream_t s) {
     const dim3 grid(ceil_div(m, 16), ceil_div(B, QB));
-    const bool vec = (n % 16 == 0) && ((uintptr_t)W % 16 == 0) && ((uintptr_t)X % 16 == 0);
-    if (vec)
-        hipLaunchKernelGGL((server_eval_mfma_small<QB, KW, KBW, true>), grid, dim3(KW * 64), 0, s, W, m, n, X, B, Y);
-    else
-        hipLaunchKernelGGL((server_eval_mfma_small<QB, KW, KBW, false>), grid, dim3(KW * 64), 0, s, W, m, n, X, B,
-                           Y);
+    const bool xvec = (n % 16 == 0) && ((uintptr_t)X % 16 == 0);
+    const bool wvec = (n % 16 == 0) && ((uintptr_t)W % 16 == 0);
+#define MVK_SMALL(XV, WLV) \
+    hipLaunchKernelGGL((server_eval_mfma_small<QB, KW, KBW, XV, WLV>), grid, dim3(KW * 64), 0, s, W, m, n, X, B, Y)
+    if (packed) {
+        if (xvec) MVK_SMALL(true, kWPacked);
+        else MVK_SMALL(false, kWPacked);
+    } else if (xvec && wvec) {
+        MVK_SMALL(true, kWRowVec);
+    } else {
+        MVK_SMALL(false, kWRowScalar);
+    }
+#undef MVK_SMALL
     return hipGetLastError();
 }
 
@@ -352,20 +376,28 @@ hipError_t launch_mfma_small(const int8_t* W, uint32_t m, uint32_t n, const uint
 // the 16 bytes that lane l supplies for digit tile qt and k-block kb (64 k),
 // i.e. digit row 16*qt + l%16 at k = 64*kb + 16*(l/16) + [0, 16).
 //
-// A workgroup of NW waves owns NW*TW*16 rows of W (TW tiles of 16 per wave)
-// over the whole K range and all QT digit tiles.  Operands travel HBM/L2 ->
-// LDS with global_load_lds_dwordx4 (lane i's 16 bytes land at base + 16*i), so
-// no registers hold data in flight and the prefetch depth is set by the ring
-// size S: k-block kb uses ring slot kb % S; the W tiles of a wave live in its
-// private part of the slot, the QT digit tiles are shared (each wave loads
-// QT/NW of them).  Iteration kb: wait until this wave's loads of k-block kb+1
-// have landed (at most S-3 k-blocks of loads may still be outstanding),
-// barrier (all waves' tiles of kb+1 landed and everyone has finished k-block
-// kb-1), refill the slot of k-block kb-1 with k-block kb+S-1, then run the
-// MFMAs of k-block kb from registers while reading k-block kb+1 from LDS.
-// Every operand read is a ds_read_b128 at 16*lane: conflict free.
+// A workgroup of eight waves (two per SIMD) owns a block of W rows and all QT
+// digit tiles, over one of `ksplit` equal ranges of k-blocks; the waves form a
+// grid over (digit tiles) x (W tiles).  Operands travel HBM/L2 -> LDS with
+// global_load_lds_dwordx4 (lane i's 16 bytes land at base + 16*i), so no
+// registers hold data in flight and the prefetch depth is set by the ring
+// size S: k-block kb uses ring slot kb % S, which holds the block's W tiles
+// and digit tiles, each loaded by one wave (or two, with identical bytes).
+// Iteration kb: wait until this wave's loads of k-block kb have landed (the
+// S-1 later k-blocks may still be in flight), barrier (everyone's landed),
+// read the operands from LDS and run the MFMAs, barrier (every wave has read
+// the slot), refill the slot with k-block kb+S.  Every operand read is a
+// ds_read_b128 at 16*lane: conflict free.
+//
+// Workgroups are placed so that the eight consecutive workgroup ids (one per
+// XCD under round-robin dispatch) of one group take 8/ksplit row blocks and
+// all ksplit k-ranges, each XCD always the same k-range: an XCD's L2 then
+// holds one k-range of D only.
+//
 // Epilogue: lane l of C tile (qt, t) holds the four digit sums of query
-// 4*qt + l/16 for W row 16*t + l%16, recombined in-lane.
+// 4*qt + l/16 for W row 16*t + l%16, recombined in-lane to a value mod p.
+// With ksplit > 1 the k-ranges of a row block are added by the workgroup that
+// finishes last (see the end of the kernel).
 // ---------------------------------------------------------------------------
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -394,128 +426,313 @@ __device__ __forceinline__ void dma16(const void* src, int8_t* lds_base) {
         : "memory");
 }
 
+// One thread per (k-block kb, query q, 16-element quarter kq): reads the 16
+// query elements once and writes the four granules of digits 0..3, which are
+// consecutive (digit row 4q + d -> lane (4q + d) % 16 + 16*kq of tile q/4).
+// Padded queries (q >= B) and elements past n are zero.
+template <bool VEC>
 __global__ __launch_bounds__(256) void digits_tiled_kernel(const uint32_t* __restrict__ X, uint32_t n, uint32_t B,
                                                            uint32_t QT, uint32_t nkb, int8_t* __restrict__ Dt) {
-    // one thread per 16-byte granule (kb, qt, l)
     const uint32_t g = blockIdx.x * 256 + threadIdx.x;
-    if (g >= nkb * QT * 64) return;
-    const uint32_t l = g % 64, qt = (g / 64) % QT, kb = g / (64 * QT);
-    const uint32_t dr = qt * 16 + (l & 15);
-    const uint32_t q = dr >> 2, d = dr & 3;
-    const uint32_t k0 = kb * 64 + (l >> 4) * 16;
-    uint32_t out[4] = {0u, 0u, 0u, 0u};
-    if (q < B) {
-        const uint32_t* xr = X + (size_t)q * n;
+    const uint32_t nq = QT * 4;
+    if (g >= nkb * nq * 4) return;
+    const uint32_t kq = g % 4, q = (g / 4) % nq, kb = g / (4 * nq);
+    const uint32_t k0 = kb * 64 + kq * 16;
+    uint32_t x[16];
+    const bool okq = q < B;
+    const uint32_t* xr = X + (size_t)(okq ? q : 0u) * n;
+    if (VEC) {  // n % 16 == 0 and X 16-byte aligned: the quarter is wholly in or out
+        const bool ok = okq && k0 < n;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const uint4 t = *reinterpret_cast<const uint4*>(xr + (ok ? k0 : 0u) + 4 * v);
+            x[4 * v] = ok ? t.x : 0u;
+            x[4 * v + 1] = ok ? t.y : 0u;
+            x[4 * v + 2] = ok ? t.z : 0u;
+            x[4 * v + 3] = ok ? t.w : 0u;
+        }
+    } else {
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-            const uint32_t k = k0 + e;
-            const uint32_t u = digit_word(k < n ? xr[k] : 0u);
-            out[e >> 2] |= ((u >> (8 * d)) & 0xffu) << (8 * (e & 3));
+            const bool ok = okq && k0 + e < n;
+            const uint32_t t = xr[ok ? k0 + e : 0u];
+            x[e] = ok ? t : 0u;
         }
     }
-    *reinterpret_cast<uint4*>(Dt + (size_t)g * 16) = make_uint4(out[0], out[1], out[2], out[3]);
+    int32_t pl[4][4];  // pl[d][w]: digit plane d of elements 4w .. 4w+3
+#pragma unroll
+    for (int w = 0; w < 4; ++w)
+        digit_planes(x[4 * w], x[4 * w + 1], x[4 * w + 2], x[4 * w + 3], pl[0][w], pl[1][w], pl[2][w], pl[3][w]);
+    const uint32_t l0 = 4 * (q % 4) + 16 * kq;
+    int8_t* dst = Dt + ((size_t)(kb * QT + q / 4) * 64 + l0) * 16;
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+        *reinterpret_cast<int4*>(dst + 16 * d) = make_int4(pl[d][0], pl[d][1], pl[d][2], pl[d][3]);
 }
 
-template <int QT, int NW, int TW, int S>
-__global__ __launch_bounds__(NW * 64) void server_eval_mfma_dma(const int8_t* __restrict__ W, uint32_t m, uint32_t n,
-                                                                const int8_t* __restrict__ Dt, uint32_t nkb,
-                                                                uint32_t B, uint32_t* __restrict__ Y) {
-    constexpr int AQ = QT / NW;  // digit tiles loaded by each wave per k-block
-    static_assert(AQ * NW == QT, "QT must be a multiple of NW");
-    constexpr int PER = TW + AQ;  // loads per wave per k-block
-    static_assert((S - 2) * PER <= 63, "vmcnt range");
-    static_assert(S >= 3, "the pipeline reads one k-block ahead");
-    __shared__ __align__(16) int8_t Aring[S][QT][1024];
-    __shared__ __align__(16) int8_t Wring[S][NW][TW][1024];
+// sum_d 2^(8d) S_d mod p for four signed digit sums |S_d| < 2^31, in 32-bit
+// arithmetic: S_d mod p, then multiplication by 2^(8d), which modulo
+// p = 2^31 - 1 is a rotation of the 31-bit value by 8d.
+__device__ __forceinline__ uint32_t rotl31(uint32_t x, int k) {
+    return ((x << k) | (x >> (31 - k))) & kP;
+}
+
+__device__ __forceinline__ uint32_t digits_to_field(v4i sum) {
+    uint32_t r[4];
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+        const int32_t v = sum[d];
+        // v >= 0: v <= 2^31 - 1 = p, so v mod p is v or 0; v < 0: p + v >= 0
+        const uint32_t u = v >= 0 ? (uint32_t)v : kP + (uint32_t)v;
+        r[d] = u >= kP ? u - kP : u;
+    }
+    return fadd(fadd(r[0], rotl31(r[1], 8)), fadd(rotl31(r[2], 16), rotl31(r[3], 24)));
+}
+
+template <int QT, int NW, int WQ, int TWW, int SW, int SD, bool PACKED>
+__global__ __launch_bounds__(NW * 64) void server_eval_mfma_stream(
+    const int8_t* __restrict__ W, uint32_t m, uint32_t n, const int8_t* __restrict__ Dt, uint32_t nkb,
+    uint32_t ksplit, uint32_t B, uint32_t* __restrict__ Y, uint32_t* part, uint32_t* counters) {
+    constexpr int WR = NW / WQ;               // waves along the row dimension
+    constexpr int NWT = WR * TWW;             // W tiles per workgroup
+    constexpr int QW = QT / WQ;               // digit tiles per wave
+    constexpr int NLW = NW / 2;               // waves [0, NLW) load W, the others load D
+    constexpr int AW = (NWT + NLW - 1) / NLW;  // W tiles loaded by a W-loading wave per k-block
+    constexpr int AQ = (QT + NLW - 1) / NLW;   // digit tiles loaded by a D-loading wave per k-block
+    static_assert(WQ * WR == NW && QW * WQ == QT, "tile split");
+    static_assert(SW * AW <= 63 && SD * AQ <= 63, "vmcnt range");
+    static_assert(SW >= 2 && SD >= 2, "ring depth");
+    constexpr uint32_t kRows = NWT * 16;
+    __shared__ __align__(16) int8_t Aring[SD][QT][1024];
+    __shared__ __align__(16) int8_t Wring[SW][NWT][1024];
+    // workgroup -> (row block, k-range), see above
+    const uint32_t xcd = blockIdx.x % 8, per_group = 8 / ksplit;
+    const uint32_t rb = (blockIdx.x / 8) * per_group + xcd / ksplit;
+    const uint32_t ks = xcd % ksplit;
+    if (rb * kRows >= m) return;  // padding workgroup of the last group
+    const uint32_t kb_per = (nkb + ksplit - 1) / ksplit;
+    const uint32_t kb0 = ks * kb_per;
+    const uint32_t kb1 = kb0 + kb_per < nkb ? kb0 + kb_per : nkb;
+    const uint32_t nk = kb1 > kb0 ? kb1 - kb0 : 0u;
+
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const uint32_t rowbase = blockIdx.x * (NW * TW * 16) + wave * (TW * 16);
+    const bool wloader = wave < NLW;
+    const int lw = wloader ? wave : wave - NLW;  // index among the waves of its loading role
+    const int wq = wave % WQ, wr = wave / WQ;
     const uint32_t kl = (lane >> 4) * 16;
-    const int8_t* wptr[TW];
+    const int8_t* wptr[AW];  // rows a W-loading wave loads
 #pragma unroll
-    for (int t = 0; t < TW; ++t) {
-        const uint32_t row = rowbase + t * 16 + (lane & 15);
-        wptr[t] = W + (size_t)(row < m ? row : m - 1) * n;
+    for (int a = 0; a < AW; ++a) {
+        const uint32_t row = rb * kRows + ((lw * AW + a) % NWT) * 16 + (lane & 15);
+        wptr[a] = W + (size_t)(row < m ? row : m - 1) * n;
     }
-    // Issue the loads of k-block kb into ring slot `slot`.  Blocks past the end
-    // re-read the last block (in range; never consumed).  W columns >= n are
-    // read at column 0: they meet zero digits.
-    auto issue = [&](uint32_t kb, int slot) {
-        const uint32_t kbe = kb < nkb ? kb : nkb - 1;
+    // In-range global k-block of local block j: blocks past the end of the
+    // range (and every block of an empty range) re-read an in-range block that
+    // is never consumed.
+    auto kblock = [&](uint32_t j) {
+        const uint32_t kbj = kb0 + (j < nk ? j : (nk ? nk - 1 : 0u));
+        return kbj < nkb ? kbj : nkb - 1;
+    };
+    // Row-major W: columns >= n are read at column 0 (they meet zero digits).
+    // Packed W: tile (row tile, k-block) is 1 KiB in operand order, zero padded;
+    // row tiles past the end re-read the last one (their rows are not stored).
+    const uint32_t nrt = (m + 15) / 16;
+    auto issue_w = [&](uint32_t j, int slot) {
+        const uint32_t kbe = kblock(j);
         const uint32_t k = kbe * 64 + kl;
         const uint32_t kk = k < n ? k : 0u;
 #pragma unroll
-        for (int t = 0; t < TW; ++t) dma16(wptr[t] + kk, &Wring[slot][wave][t][0]);
+        for (int a = 0; a < AW; ++a) {
+            const int tile = (lw * AW + a) % NWT;
+            if (PACKED) {
+                const uint32_t rt = rb * (kRows / 16) + tile;
+                dma16(W + (((size_t)(rt < nrt ? rt : nrt - 1) * nkb + kbe) * 64 + lane) * 16, &Wring[slot][tile][0]);
+            } else {
+                dma16(wptr[a] + kk, &Wring[slot][tile][0]);
+            }
+        }
+    };
+    auto issue_d = [&](uint32_t j, int slot) {
+        const uint32_t kbe = kblock(j);
 #pragma unroll
         for (int a = 0; a < AQ; ++a) {
-            const uint32_t qt = wave * AQ + a;
+            const uint32_t qt = (lw * AQ + a) % QT;
             dma16(Dt + ((size_t)(kbe * QT + qt) * 64 + lane) * 16, &Aring[slot][qt][0]);
         }
     };
-    v4i acc[QT][TW];
+    v4i acc[QW][TWW];
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt)
+    for (int i = 0; i < QW; ++i)
 #pragma unroll
-        for (int t = 0; t < TW; ++t) acc[qt][t] = v4i{0, 0, 0, 0};
+        for (int t = 0; t < TWW; ++t) acc[i][t] = v4i{0, 0, 0, 0};
 
-    // Software pipeline: the operands of k-block kb+1 are read from LDS into
-    // registers while the MFMAs of k-block kb run.  At the top of iteration kb
-    // every wave has consumed k-block kb-1 (its MFMAs ran in iteration kb-1),
-    // so the slot of kb-1 can be refilled with k-block kb+S-1.
-    v4i cb[TW], ca[QT];
+    if (wloader) {
 #pragma unroll
-    for (int j = 0; j < S - 1; ++j) issue(j, j);
-    wait_vmcnt<(S - 2) * PER>();
-    __syncthreads();
+        for (int j = 0; j < SW; ++j) issue_w(j, j);
+    } else {
 #pragma unroll
-    for (int t = 0; t < TW; ++t) cb[t] = *reinterpret_cast<const v4i*>(&Wring[0][wave][t][16 * lane]);
-#pragma unroll
-    for (int qt = 0; qt < QT; ++qt) ca[qt] = *reinterpret_cast<const v4i*>(&Aring[0][qt][16 * lane]);
-    for (uint32_t kb = 0; kb < nkb; ++kb) {
-        // k-block kb+1 landed (this wave's loads), and everyone is past kb-1
-        wait_vmcnt<(S - 3) * PER>();
+        for (int j = 0; j < SD; ++j) issue_d(j, j);
+    }
+    for (uint32_t j = 0; j < nk; ++j) {
+        const int wslot = (int)(j % SW), dslot = (int)(j % SD);
+        // this wave's loads of k-block j landed (the later blocks of its ring
+        // may still be in flight), then everyone's landed
+        if (wloader)
+            wait_vmcnt<(SW - 1) * AW>();
+        else
+            wait_vmcnt<(SD - 1) * AQ>();
         __syncthreads();
-        issue(kb + S - 1, (int)((kb + S - 1) % S));
-        const int nslot = (int)((kb + 1) % S);
-        v4i nb[TW], na[QT];
+        v4i cb[TWW], ca[QW];
 #pragma unroll
-        for (int t = 0; t < TW; ++t) nb[t] = *reinterpret_cast<const v4i*>(&Wring[nslot][wave][t][16 * lane]);
+        for (int t = 0; t < TWW; ++t) cb[t] = *reinterpret_cast<const v4i*>(&Wring[wslot][wr * TWW + t][16 * lane]);
 #pragma unroll
-        for (int qt = 0; qt < QT; ++qt) na[qt] = *reinterpret_cast<const v4i*>(&Aring[nslot][qt][16 * lane]);
+        for (int i = 0; i < QW; ++i) ca[i] = *reinterpret_cast<const v4i*>(&Aring[dslot][wq * QW + i][16 * lane]);
 #pragma unroll
-        for (int qt = 0; qt < QT; ++qt)
+        for (int i = 0; i < QW; ++i)
 #pragma unroll
-            for (int t = 0; t < TW; ++t)
-                acc[qt][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ca[qt], cb[t], acc[qt][t], 0, 0, 0);
-#pragma unroll
-        for (int t = 0; t < TW; ++t) cb[t] = nb[t];
-#pragma unroll
-        for (int qt = 0; qt < QT; ++qt) ca[qt] = na[qt];
+            for (int t = 0; t < TWW; ++t)
+                acc[i][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ca[i], cb[t], acc[i][t], 0, 0, 0);
+        __syncthreads();  // every wave has read both slots: refill them
+        if (wloader)
+            issue_w(j + SW, wslot);
+        else
+            issue_d(j + SD, dslot);
     }
     wait_vmcnt<0>();  // drain the trailing prefetches before the workgroup exits
 
+    const uint32_t rowbase = rb * kRows + wr * (TWW * 16) + (lane & 15);
+    const uint32_t qbase = wq * QW * 4 + (lane >> 4);
+    // digit sums of tile (i, t) -> value mod p, recomputed where needed so that
+    // the accumulators need no second copy
+    auto value = [&](int i, int t) { return digits_to_field(acc[i][t]); };
+    if (ksplit == 1) {
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt) {
-        const uint32_t q = qt * 4 + (lane >> 4);
+        for (int i = 0; i < QW; ++i)
 #pragma unroll
-        for (int t = 0; t < TW; ++t) {
-            const uint32_t row = rowbase + t * 16 + (lane & 15);
-            if (q < B && row < m) {
-                const v4i sum = acc[qt][t];
-                const int64_t v = (int64_t)sum[0] + ((int64_t)sum[1] << 8) + ((int64_t)sum[2] << 16) +
-                                  ((int64_t)sum[3] << 24);
-                Y[(size_t)q * m + row] = fred_s64(v);
+            for (int t = 0; t < TWW; ++t) {
+                const uint32_t q = qbase + 4 * i, row = rowbase + 16 * t;
+                if (q < B && row < m) Y[(size_t)q * m + row] = value(i, t);
             }
-        }
+        return;
     }
+    // Several k-ranges: every workgroup stores its values with device-coherent
+    // stores (written through the XCD's L2), waits for them, and counts itself
+    // on its row block's counter; the workgroup that arrives last reads the
+    // other ranges' values with device-coherent loads, adds them, writes Y and
+    // resets the counter.  No cache-wide flush or invalidate is needed.  The
+    // values are exchanged in accumulator-tile order (64 consecutive words per
+    // tile, one per lane), so every store and load covers whole cache lines.
+    const size_t nrb = (m + kRows - 1) / kRows;
+    auto slot = [&](uint32_t o, int i, int t) {
+        return ((((size_t)o * nrb + rb) * NW + wave) * (QW * TWW) + i * TWW + t) * 64 + lane;
+    };
+#pragma unroll
+    for (int i = 0; i < QW; ++i)
+#pragma unroll
+        for (int t = 0; t < TWW; ++t)
+            __hip_atomic_store(&part[slot(ks, i, t)], value(i, t), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's stores are complete
+    __syncthreads();
+    uint32_t* flag = reinterpret_cast<uint32_t*>(&Aring[0][0][0]);  // the ring is idle now
+    if (threadIdx.x == 0) *flag = (atomicAdd(&counters[rb], 1u) == ksplit - 1) ? 1u : 0u;
+    __syncthreads();
+    if (!*flag) return;
+    uint32_t v[QW][TWW];
+#pragma unroll
+    for (int i = 0; i < QW; ++i)
+#pragma unroll
+        for (int t = 0; t < TWW; ++t) v[i][t] = value(i, t);
+    for (uint32_t o = 0; o < ksplit; ++o) {  // one round of independent loads per range
+        if (o == ks) continue;
+#pragma unroll
+        for (int i = 0; i < QW; ++i)
+#pragma unroll
+            for (int t = 0; t < TWW; ++t)
+                v[i][t] = fadd(v[i][t], __hip_atomic_load(&part[slot(o, i, t)], __ATOMIC_RELAXED,
+                                                          __HIP_MEMORY_SCOPE_AGENT));
+    }
+#pragma unroll
+    for (int i = 0; i < QW; ++i)
+#pragma unroll
+        for (int t = 0; t < TWW; ++t) {
+            const uint32_t q = qbase + 4 * i, row = rowbase + 16 * t;
+            if (q < B && row < m) Y[(size_t)q * m + row] = v[i][t];
+        }
+    if (threadIdx.x == 0) atomicExch(&counters[rb], 0u);
 }
 
-template <int QT, int NW, int TW, int S>
-hipError_t launch_dma_cfg(const int8_t* W, uint32_t m, uint32_t n, const int8_t* Dt, uint32_t nkb, uint32_t B,
-                          uint32_t* Y, hipStream_t s) {
-    const dim3 grid(ceil_div(m, NW * TW * 16));
-    hipLaunchKernelGGL((server_eval_mfma_dma<QT, NW, TW, S>), grid, dim3(NW * 64), 0, s, W, m, n, Dt, nkb, B, Y);
+// Streamed-path configurations by digit tiles per launch group (QT): eight
+// waves (two per SIMD, so one wave's LDS reads overlap the other's MFMAs),
+// wave grid, W tiles per wave, ring slots; at most 28 accumulator tiles per
+// wave.  QT = 16: 4 x 2 waves, 7 W tiles each (224 rows); QT = 8: 2 x 4
+// waves, 4 W tiles (256 rows); QT <= 4: 1 x 8 waves, 2 W tiles (256 rows).
+constexpr int kStreamWaves = 8;
+uint32_t stream_rows(uint32_t qt) { return qt == 16 ? 224u : 256u; }
+uint32_t stream_slots(uint32_t qt) { return qt == 16 ? 7u : 8u; }  // W ring depth
+
+// k-range split: the split (1, 2, 4 or 8) that minimises the estimated time
+// ceil(workgroups / 256) * (k-blocks per range + pipeline fill), the smaller
+// on ties, keeping at least 4 k-blocks per range.
+uint32_t stream_ksplit(uint32_t m, uint32_t n, uint32_t qt) {
+    if (const char* e = getenv("MVK_KSPLIT_TUNE")) return (uint32_t)atoi(e);  // TUNING ONLY
+    const uint32_t nrb = ceil_div(m, stream_rows(qt)), nkb = ceil_div(n, 64);
+    const uint32_t fill = stream_slots(qt) + 2;
+    // storing and re-reading the partial values of a split costs about
+    // 4*B / 64 = qt k-blocks of W traffic per workgroup
+    uint32_t best = 1, best_cost = 0xffffffffu;
+    for (uint32_t ks = 1; ks <= 8; ks *= 2) {
+        if (ks > 1 && nkb < 4 * ks) break;
+        const uint32_t cost = ceil_div(nrb * ks, 256) * (ceil_div(nkb, ks) + fill + (ks > 1 ? qt : 0u));
+        if (cost < best_cost) {
+            best_cost = cost;
+            best = ks;
+        }
+    }
+    return best;
+}
+
+template <int QT, int WQ, int TWW, int SW, int SD>
+hipError_t launch_stream_cfg(const int8_t* W, uint32_t m, uint32_t n, const int8_t* Dt, uint32_t nkb, uint32_t B,
+                             uint32_t* Y, uint32_t ksplit, uint32_t* part, uint32_t* counters, bool packed,
+                             hipStream_t s) {
+    constexpr uint32_t rows = (kStreamWaves / WQ) * TWW * 16;
+    const uint32_t nrb = ceil_div(m, rows), per_group = 8 / ksplit;
+    const dim3 grid(ceil_div(nrb, per_group) * 8);
+    if (packed)
+        hipLaunchKernelGGL((server_eval_mfma_stream<QT, kStreamWaves, WQ, TWW, SW, SD, true>), grid,
+                           dim3(kStreamWaves * 64), 0, s, W, m, n, Dt, nkb, ksplit, B, Y, part, counters);
+    else
+        hipLaunchKernelGGL((server_eval_mfma_stream<QT, kStreamWaves, WQ, TWW, SW, SD, false>), grid,
+                           dim3(kStreamWaves * 64), 0, s, W, m, n, Dt, nkb, ksplit, B, Y, part, counters);
     return hipGetLastError();
+}
+
+// Packed W: granule (rt, kb, l) = the 16 bytes lane l supplies as the B
+// operand for rows 16*rt .. 16*rt + 15 and k-block kb, i.e. row 16*rt + l%16 at
+// k = 64*kb + 16*(l/16) + [0, 16); rows >= m and k >= n are zero.
+__global__ __launch_bounds__(256) void pack_w_kernel(const int8_t* __restrict__ W, uint32_t m, uint32_t n,
+                                                     uint32_t nkb, size_t granules, int8_t* __restrict__ Wp) {
+    const size_t g = (size_t)blockIdx.x * 256 + threadIdx.x;
+    if (g >= granules) return;
+    const uint32_t l = (uint32_t)(g % 64), kb = (uint32_t)((g / 64) % nkb);
+    const uint32_t rt = (uint32_t)(g / (64 * (size_t)nkb));
+    const uint32_t row = rt * 16 + (l & 15), k0 = kb * 64 + (l >> 4) * 16;
+    uint32_t w[4] = {0u, 0u, 0u, 0u};
+    if (row < m) {
+        const int8_t* src = W + (size_t)row * n;
+        if (k0 + 16 <= n && (((uintptr_t)(src + k0)) & 15) == 0) {
+            const uint4 t = *reinterpret_cast<const uint4*>(src + k0);
+            w[0] = t.x;
+            w[1] = t.y;
+            w[2] = t.z;
+            w[3] = t.w;
+        } else {
+            for (uint32_t e = 0; e < 16 && k0 + e < n; ++e)
+                w[e >> 2] |= (uint32_t)(uint8_t)src[k0 + e] << (8 * (e & 3));
+        }
+    }
+    *reinterpret_cast<uint4*>(Wp + g * 16) = make_uint4(w[0], w[1], w[2], w[3]);
 }
 
 template <int R, int BQ>
@@ -532,53 +749,90 @@ hipError_t launch_cfg(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X
 
 }  // namespace
 
-size_t server_eval_workspace(uint32_t n, uint32_t B, int path) {
-    if (path == MVK_PATH_VALU || B <= 4 || n % 16 != 0) return 0;
+namespace {
+uint32_t group_qt(uint32_t nb) { return nb <= 8 ? 2 : nb <= 16 ? 4 : nb <= 32 ? 8 : 16; }
+}  // namespace
+
+size_t packed_w_bytes(uint32_t m, uint32_t n) { return (size_t)ceil_div(m, 16) * ceil_div(n, 64) * 1024; }
+
+hipError_t launch_pack_w(const int8_t* W, uint32_t m, uint32_t n, int8_t* Wp, hipStream_t s) {
+    const uint32_t nkb = ceil_div(n, 64);
+    const size_t granules = (size_t)ceil_div(m, 16) * nkb * 64;
+    hipLaunchKernelGGL(pack_w_kernel, dim3((uint32_t)((granules + 255) / 256)), dim3(256), 0, s, W, m, n, nkb,
+                       granules, Wp);
+    return hipGetLastError();
+}
+
+ServerEvalPlan server_eval_plan(uint32_t m, uint32_t n, uint32_t B, int path, bool packed) {
+    ServerEvalPlan pl{0, 0};
+    if (path == MVK_PATH_VALU || B <= 4 || (!packed && n % 16 != 0)) return pl;
     const size_t nkb = ceil_div(n, 64);
-    const size_t qt = B <= 8 ? 2 : B <= 16 ? 4 : B <= 32 ? 8 : 16;  // digit tiles of one launch group
-    return nkb * qt * 64 * 16;
+    const uint32_t nb = B < 64 ? B : 64;  // queries of the largest launch group
+    size_t part_bytes = 0;
+    // launch groups hold 64 queries, the last one B % 64 (if nonzero)
+    const uint32_t sizes[2] = {nb, B > 64 ? B % 64 : 0u};
+    for (uint32_t g : sizes) {
+        if (g == 0) continue;
+        const uint32_t qt = group_qt(g), ks = stream_ksplit(m, n, qt);
+        if (ks > 1) {
+            const size_t pb = (size_t)ks * ceil_div(m, stream_rows(qt)) * stream_rows(qt) * qt * 4 * 4;
+            part_bytes = pb > part_bytes ? pb : part_bytes;
+            const size_t cw = ceil_div(m, stream_rows(qt));
+            pl.ctrl_words = cw > pl.ctrl_words ? cw : pl.ctrl_words;
+        }
+    }
+    pl.ws_bytes = ((nkb * group_qt(nb) * 64 * 16 + 255) & ~(size_t)255) + part_bytes;
+    return pl;
 }
 
 hipError_t launch_server_eval(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t B,
-                              uint32_t* Y, int path, void* ws, hipStream_t s) {
+                              uint32_t* Y, int path, bool packed, void* ws, uint32_t* counters, hipStream_t s) {
     if (path == MVK_PATH_VALU) {
         if (B == 1) return launch_cfg<16, 1>(W, m, n, X, B, Y, s);
         if (B == 2) return launch_cfg<8, 2>(W, m, n, X, B, Y, s);
         return launch_cfg<4, 4>(W, m, n, X, B, Y, s);
     }
-    if (B == 1) return launch_mfma_small<1, 8, 8>(W, m, n, X, B, Y, s);
-    if (B == 2) return launch_mfma_small<2, 8, 8>(W, m, n, X, B, Y, s);
-    if (B <= 4) return launch_mfma_small<4, 8, 4>(W, m, n, X, B, Y, s);
-    if (n % 16 != 0 || (uintptr_t)W % 16 != 0) {
+    if (B == 1) return launch_mfma_small<1, 8, 8>(W, m, n, X, B, Y, packed, s);
+    if (B == 2) return launch_mfma_small<2, 8, 8>(W, m, n, X, B, Y, packed, s);
+    if (B <= 4) return launch_mfma_small<4, 8, 4>(W, m, n, X, B, Y, packed, s);
+    if (!packed && (n % 16 != 0 || (uintptr_t)W % 16 != 0)) {
         // Rows that are not whole 16-byte granules: the streamed path would read
         // past the end of W on the last row; use the small path per 4 queries.
         for (uint32_t b0 = 0; b0 < B; b0 += 4) {
             const uint32_t nb = (B - b0) < 4 ? (B - b0) : 4;
-            const hipError_t e = launch_mfma_small<4, 8, 4>(W, m, n, X + (size_t)b0 * n, nb, Y + (size_t)b0 * m, s);
+            const hipError_t e =
+                launch_mfma_small<4, 8, 4>(W, m, n, X + (size_t)b0 * n, nb, Y + (size_t)b0 * m, false, s);
             if (e != hipSuccess) return e;
         }
         return hipSuccess;
     }
     // Up to 64 queries per launch group; W is streamed once per group.
     const uint32_t nkb = ceil_div(n, 64);
+    const uint32_t nb_max = B < 64 ? B : 64;
     int8_t* Dt = (int8_t*)ws;
+    uint32_t* part = (uint32_t*)((char*)ws + ((nkb * (size_t)group_qt(nb_max) * 64 * 16 + 255) & ~(size_t)255));
     for (uint32_t b0 = 0; b0 < B; b0 += 64) {
         const uint32_t nb = (B - b0) < 64 ? (B - b0) : 64;
-        const uint32_t qt = nb <= 8 ? 2 : nb <= 16 ? 4 : nb <= 32 ? 8 : 16;
-        const uint32_t granules = nkb * qt * 64;
-        hipLaunchKernelGGL(digits_tiled_kernel, dim3(ceil_div(granules, 256)), dim3(256), 0, s, X + (size_t)b0 * n,
-                           n, nb, qt, nkb, Dt);
+        const uint32_t qt = group_qt(nb), ks = stream_ksplit(m, n, qt);
+        const uint32_t threads = nkb * qt * 16;
+        const uint32_t* Xb = X + (size_t)b0 * n;
+        if (n % 16 == 0 && (uintptr_t)Xb % 16 == 0)
+            hipLaunchKernelGGL(digits_tiled_kernel<true>, dim3(ceil_div(threads, 256)), dim3(256), 0, s, Xb, n, nb,
+                               qt, nkb, Dt);
+        else
+            hipLaunchKernelGGL(digits_tiled_kernel<false>, dim3(ceil_div(threads, 256)), dim3(256), 0, s, Xb, n, nb,
+                               qt, nkb, Dt);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         uint32_t* Yb = Y + (size_t)b0 * m;
         if (qt == 2)
-            e = launch_dma_cfg<2, 2, 1, 16>(W, m, n, Dt, nkb, nb, Yb, s);
+            e = launch_stream_cfg<2, 1, 2, 8, 8>(W, m, n, Dt, nkb, nb, Yb, ks, part, counters, packed, s);
         else if (qt == 4)
-            e = launch_dma_cfg<4, 4, 1, 12>(W, m, n, Dt, nkb, nb, Yb, s);
+            e = launch_stream_cfg<4, 1, 2, 8, 6>(W, m, n, Dt, nkb, nb, Yb, ks, part, counters, packed, s);
         else if (qt == 8)
-            e = launch_dma_cfg<8, 4, 2, 8>(W, m, n, Dt, nkb, nb, Yb, s);
+            e = launch_stream_cfg<8, 2, 4, 7, 4>(W, m, n, Dt, nkb, nb, Yb, ks, part, counters, packed, s);
         else
-            e = launch_dma_cfg<16, 4, 2, 6>(W, m, n, Dt, nkb, nb, Yb, s);
+            e = launch_stream_cfg<16, 4, 7, 7, 3>(W, m, n, Dt, nkb, nb, Yb, ks, part, counters, packed, s);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;

@@ -20,7 +20,7 @@ from dataclasses import dataclass, field
 
 import torch
 
-from . import Code, Key, decode_verify, encode, keygen, server_eval
+from . import Code, Key, decode_verify, encode, keygen, pack_weights, server_eval
 
 # (name, m, n, input group)
 PROJECTIONS = (
@@ -37,7 +37,7 @@ INPUTS = ("attn_in", "attn_out", "mlp_in", "mlp_out")
 
 @dataclass
 class Layer:
-    W: dict = field(default_factory=dict)      # name -> int8 m x n
+    W: dict = field(default_factory=dict)      # name -> int8 m x n, or its PackedW
     keys: dict = field(default_factory=dict)   # name -> Key
 
 
@@ -45,14 +45,15 @@ def input_width(group: str) -> int:
     return next(n for (_, _, n, g) in PROJECTIONS if g == group)
 
 
-def build_layer(weights: dict, cx_by_n: dict, cy_by_m: dict, stream=None) -> Layer:
-    """Preprocess every projection of one layer (keygen on the device)."""
+def build_layer(weights: dict, cx_by_n: dict, cy_by_m: dict, stream=None, packed: bool = True) -> Layer:
+    """Preprocess every projection of one layer (keygen on the device); with
+    `packed` the server keeps each W in the packed matrix-core layout."""
     layer = Layer()
     for name, m, n, _ in PROJECTIONS:
         W = weights[name]
         key = Key.allocate(m, n, cx_by_n[n], cy_by_m[m], device=W.device)
         keygen(key, W, stream=stream)
-        layer.W[name] = W
+        layer.W[name] = pack_weights(W, stream=stream) if packed else W
         layer.keys[name] = key
     return layer
 

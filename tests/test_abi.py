@@ -100,3 +100,20 @@ def test_verify_argument_checks_without_device_work():
     ex3 = L.MvkSparse(0x1000, 0x1000, 2, 3)
     assert lib.mvk_decode_verify(ctypes.byref(key), fake, fake, 1, ctypes.byref(ex3), ctypes.byref(ey),
                                  fake, None, None, fake, None) == L.MVK_EINVAL
+
+
+def test_packed_weight_size_and_checks():
+    L = _lib()
+    lib = L.load()
+    assert lib.mvk_packed_weight_bytes(0, 5) == 0 and lib.mvk_packed_weight_bytes(5, 0) == 0
+    assert lib.mvk_packed_weight_bytes(1, 1) == 1024
+    assert lib.mvk_packed_weight_bytes(17, 65) == 2 * 2 * 1024
+    assert lib.mvk_packed_weight_bytes(28672, 8192) == 28672 * 8192
+    fake = ctypes.c_void_p(0x1000)
+    odd = ctypes.c_void_p(0x1001)
+    assert lib.mvk_pack_weights(fake, 0, 4, None, None) == L.MVK_OK
+    assert lib.mvk_pack_weights(fake, 4, 4, None, None) == L.MVK_EINVAL
+    assert lib.mvk_pack_weights(fake, 4, 4, odd, None) == L.MVK_EINVAL
+    assert lib.mvk_server_eval_packed(odd, 4, 16, fake, 1, fake, None) == L.MVK_EINVAL
+    assert lib.mvk_server_eval_packed(fake, 4, L.MVK_MAX_N + 1, fake, 1, fake, None) == L.MVK_ERANGE
+    assert lib.mvk_server_eval_packed(fake, 0, 16, fake, 1, fake, None) == L.MVK_OK

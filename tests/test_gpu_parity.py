@@ -54,6 +54,36 @@ def test_server_eval_matches_oracle(m, n, B, path):
     assert np.array_equal(got, oracle.server_eval(W, X))
 
 
+def _pack_host(W):
+    """The packed server layout written out with numpy (tiles of 16 rows x 64
+    columns, lane l = 16*(column quarter) + row within the tile, zero padded)."""
+    m, n = W.shape
+    nrt, nkb = -(-m // 16), -(-n // 64)
+    pad = np.zeros((nrt * 16, nkb * 64), dtype=np.int8)
+    pad[:m, :n] = W
+    t = pad.reshape(nrt, 16, nkb, 4, 16).transpose(0, 2, 3, 1, 4)
+    return t.reshape(-1)
+
+
+@pytest.mark.parametrize("m,n", [(1, 1), (17, 100), (64, 4096), (33, 12345)])
+def test_pack_weights_layout(m, n):
+    W = synth.weights(400 + m, m, n)
+    pw = mvk.pack_weights(dev(W))
+    want = _pack_host(W)
+    got = pw.data.cpu().numpy()[: want.size]
+    assert got.size == want.size == mvk._lib.load().mvk_packed_weight_bytes(m, n)
+    assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("m,n,B", SERVER_SHAPES)
+def test_server_eval_packed_matches_oracle(m, n, B):
+    _say(f"server_eval packed m={m} n={n} B={B}")
+    W = synth.weights(100 + m + n, m, n)
+    X = synth.field_uniform(200 + B + n, (B, n))
+    got = host(mvk.server_eval(mvk.pack_weights(dev(W)), dev(X)))
+    assert np.array_equal(got, oracle.server_eval(W, X))
+
+
 @pytest.mark.parametrize("path", ["valu", "mfma"])
 @pytest.mark.parametrize("wv,xv", [(-128, P - 8421504), (127, P - 1), (-127, P - 1), (-128, 1073741823),
                                    (127, 1073741824), (-1, 0)])

@@ -34,20 +34,62 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "server_eval_attn4096_traffic.json
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_10264_amd", "csrc", "server_eval.hip")
 
 
-def measured_traffic(config: str):
-    """HBM bytes per server_eval launch from the committed counter runs, if they
-    were taken on the current kernel source and this workload; else None."""
+def kernel_src_sha256() -> str:
     import hashlib
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(config: str, weights: str):
+    """HBM bytes per server_eval launch from the committed counter runs, if they
+    were taken on the current kernel source, this workload and weight layout;
+    else None."""
     try:
         with open(TRAFFIC_FILE) as f:
             rec = json.load(f)
-        with open(KERNEL_SRC, "rb") as f:
-            sha = hashlib.sha256(f.read()).hexdigest()
+        sha = kernel_src_sha256()
     except OSError:
         return None
-    if rec.get("kernel_src_sha256") != sha or rec.get("config") != config:
+    if rec.get("kernel_src_sha256") != sha or rec.get("config") != config or rec.get("weights") != weights:
         return None
     return rec.get("traffic_bytes_per_launch")
+
+
+def write_traffic(fetch_csv: str, write_csv: str, config: str, weights: str, copy_mib: int, kernel_match: str):
+    """Traffic record from two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE; KiB
+    per dispatch) of `bench.py --calib-copy-mib copy_mib`: the server_eval
+    kernel's medians, each scaled by what the same counter reads for the
+    copy_mib MiB device copy (which reads and writes copy_mib MiB)."""
+    import csv
+    import statistics
+
+    def per_kernel(path, counter):
+        vals, copies = [], []
+        with open(path) as f:
+            for row in csv.DictReader(f):
+                if row["Counter_Name"] != counter:
+                    continue
+                v = float(row["Counter_Value"])
+                if kernel_match in row["Kernel_Name"]:
+                    vals.append(v)
+                elif "copyBuffer" in row["Kernel_Name"]:
+                    copies.append(v)
+        if not vals or not copies:
+            raise SystemExit(f"{path}: no {counter} rows for {kernel_match!r} or the copy kernel")
+        return statistics.median(vals), len(vals), max(copies)
+
+    f_med, f_n, f_copy = per_kernel(fetch_csv, "FETCH_SIZE")
+    w_med, w_n, w_copy = per_kernel(write_csv, "WRITE_SIZE")
+    ref_kib = copy_mib * 1024.0
+    fs, ws = ref_kib / f_copy, ref_kib / w_copy
+    rec = {"kernel": kernel_match, "config": config, "weights": weights, "kernel_src_sha256": kernel_src_sha256(),
+           "fetch_size_kib_per_dispatch": f_med, "write_size_kib_per_dispatch": w_med, "dispatches": [f_n, w_n],
+           "copy_reference_mib": copy_mib, "copy_fetch_size_kib": f_copy, "copy_write_size_kib": w_copy,
+           "fetch_scale": fs, "write_scale": ws,
+           "traffic_bytes_per_launch": int(round((f_med * fs + w_med * ws) * 1024))}
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(json.dumps(rec))
 
 
 def calib_copy(mib: int):
@@ -76,6 +118,10 @@ def parse():
                     help="after timing, copy this many MiB device-to-device (reference kernel for HBM counters)")
     ap.add_argument("--seed", type=int, default=2609)
     ap.add_argument("--path", default="auto", choices=["auto", "valu", "mfma"], help="server_eval kernel family")
+    ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write the server_eval traffic record from two rocprofv3 --pmc counter files and exit")
+    ap.add_argument("--traffic-kernel", default="server_eval_mfma_small<1, 8, 8, true, 2>",
+                    help="kernel name fragment the traffic record is taken for")
     ap.add_argument("--weights", default="packed", choices=["packed", "rowmajor"],
                     help="server weight layout: packed once into matrix-core operand order (untimed, like "
                          "keygen), or row-major as given")
@@ -89,6 +135,9 @@ def parse():
 
 def main():
     args = parse()
+    if args.write_traffic:
+        return write_traffic(args.write_traffic[0], args.write_traffic[1], args.config, args.weights,
+                             args.calib_copy_mib or 256, args.traffic_kernel)
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are not supported",
                           "n_gpus": args.gpus}), flush=True)
@@ -263,7 +312,7 @@ def main():
                    "global_batch": B, "w_pool": pool, "launch": "eager" if args.eager else "hip_graph",
                    "chains": C, "weights": args.weights},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(args.config),
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(args.config, args.weights),
                      "kernel": f"server_eval ({args.path})", "alg_bytes_per_launch": alg_bytes,
                      "mean_launch_us": 1e6 * se_mean_s},
         "server_eval": {"modmac_per_s": macs / se_mean_s, "gb_per_s": achieved},

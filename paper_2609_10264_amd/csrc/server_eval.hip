@@ -22,8 +22,6 @@
 // all R rows.  At the end the R*BQ*4 plane sums per thread are reduced across
 // the wave by a transpose-reduction (each exchange step halves the number of
 // live values) and across the four waves through LDS.
-#include <stdlib.h>
-
 #include "field.h"
 #include "mvk_internal.h"
 
@@ -489,6 +487,74 @@ __device__ __forceinline__ uint32_t digits_to_field(v4i sum) {
     return fadd(fadd(r[0], rotl31(r[1], 8)), fadd(rotl31(r[2], 16), rotl31(r[3], 24)));
 }
 
+// Epilogue of the streamed kernels: lane `lane` of wave `wave` holds the
+// accumulator tiles acc[i][t] of queries qbase + 4i and rows rowbase + 16t.
+// With one k-range the values go to Y.  With several, every workgroup stores
+// its values with device-coherent stores (written through the XCD's L2),
+// waits for them, and counts itself on its row block's counter; the workgroup
+// that arrives last reads the other ranges' values with device-coherent loads,
+// adds them, writes Y and resets the counter.  No cache-wide flush or
+// invalidate is needed.  The values are exchanged in accumulator-tile order
+// (64 consecutive words per tile, one per lane), so every store and load
+// covers whole cache lines.  `flag` is a word of idle LDS.
+template <int QW, int TWW, int NW>
+__device__ __forceinline__ void store_tiles(const v4i (&acc)[QW][TWW], uint32_t m, uint32_t B,
+                                            uint32_t* __restrict__ Y, uint32_t* part, uint32_t* counters,
+                                            uint32_t rb, uint32_t nrb, uint32_t ks, uint32_t ksplit, int wave,
+                                            int lane, uint32_t rowbase, uint32_t qbase, uint32_t* flag) {
+    if (ksplit == 1) {
+#pragma unroll
+        for (int i = 0; i < QW; ++i)
+#pragma unroll
+            for (int t = 0; t < TWW; ++t) {
+                const uint32_t q = qbase + 4 * i, row = rowbase + 16 * t;
+                if (q < B && row < m) Y[(size_t)q * m + row] = digits_to_field(acc[i][t]);
+            }
+        return;
+    }
+    auto slot = [&](uint32_t o, int i, int t) {
+        return ((((size_t)o * nrb + rb) * NW + wave) * (QW * TWW) + i * TWW + t) * 64 + lane;
+    };
+#pragma unroll
+    for (int i = 0; i < QW; ++i)
+#pragma unroll
+        for (int t = 0; t < TWW; ++t)
+            __hip_atomic_store(&part[slot(ks, i, t)], digits_to_field(acc[i][t]), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's stores are complete
+    __syncthreads();
+    if (threadIdx.x == 0) *flag = (atomicAdd(&counters[rb], 1u) == ksplit - 1) ? 1u : 0u;
+    __syncthreads();
+    if (!*flag) return;
+    uint32_t v[QW][TWW];
+#pragma unroll
+    for (int i = 0; i < QW; ++i)
+#pragma unroll
+        for (int t = 0; t < TWW; ++t) v[i][t] = digits_to_field(acc[i][t]);
+    for (uint32_t o = 0; o < ksplit; ++o) {  // one round of independent loads per range
+        if (o == ks) continue;
+#pragma unroll
+        for (int i = 0; i < QW; ++i)
+#pragma unroll
+            for (int t = 0; t < TWW; ++t)
+                v[i][t] = fadd(v[i][t], __hip_atomic_load(&part[slot(o, i, t)], __ATOMIC_RELAXED,
+                                                          __HIP_MEMORY_SCOPE_AGENT));
+    }
+#pragma unroll
+    for (int i = 0; i < QW; ++i)
+#pragma unroll
+        for (int t = 0; t < TWW; ++t) {
+            const uint32_t q = qbase + 4 * i, row = rowbase + 16 * t;
+            if (q < B && row < m) Y[(size_t)q * m + row] = v[i][t];
+        }
+    if (threadIdx.x == 0) atomicExch(&counters[rb], 0u);
+}
+
+// QT digit tiles and NWT = (NW/WQ)*TWW W tiles per workgroup; the NW waves
+// form a WQ x (NW/WQ) grid: wave w computes digit tiles [(w%WQ)*QT/WQ, ...)
+// against W tiles [(w/WQ)*TWW, ...).  Waves [0, NW/2) load the W tiles of a
+// k-block, the others its digit tiles, each into its own ring (SW and SD
+// slots), so each wave's in-order load counter covers one stream only.
 template <int QT, int NW, int WQ, int TWW, int SW, int SD, bool PACKED>
 __global__ __launch_bounds__(NW * 64) void server_eval_mfma_stream(
     const int8_t* __restrict__ W, uint32_t m, uint32_t n, const int8_t* __restrict__ Dt, uint32_t nkb,
@@ -603,63 +669,135 @@ __global__ __launch_bounds__(NW * 64) void server_eval_mfma_stream(
 
     const uint32_t rowbase = rb * kRows + wr * (TWW * 16) + (lane & 15);
     const uint32_t qbase = wq * QW * 4 + (lane >> 4);
-    // digit sums of tile (i, t) -> value mod p, recomputed where needed so that
-    // the accumulators need no second copy
-    auto value = [&](int i, int t) { return digits_to_field(acc[i][t]); };
-    if (ksplit == 1) {
+    store_tiles<QW, TWW, NW>(acc, m, B, Y, part, counters, rb, (m + kRows - 1) / kRows, ks, ksplit, wave, lane,
+                             rowbase, qbase, reinterpret_cast<uint32_t*>(&Aring[0][0][0]));
+}
+
+// Digits-stationary variant for small batches (QT <= 4, i.e. B <= 16): the
+// digit matrix of the workgroup's k-range (QT*16 digit rows x at most KBM
+// k-blocks, 64 KiB) is computed from the queries by the workgroup itself,
+// once, straight into LDS; only W streams through the ring.  No separate
+// digit-matrix launch and no digit traffic per k-block.  Eight waves, each
+// with all QT digit tiles and TWW W tiles (rows 128*TWW per workgroup); every
+// wave loads AW = TWW W tiles per k-block.
+template <int QT, int TWW, int KBM, int S, bool PACKED>
+__global__ __launch_bounds__(512) void server_eval_mfma_dstat(const int8_t* __restrict__ W, uint32_t m, uint32_t n,
+                                                              const uint32_t* __restrict__ X, uint32_t nkb,
+                                                              uint32_t ksplit, uint32_t B, uint32_t* __restrict__ Y,
+                                                              uint32_t* part, uint32_t* counters) {
+    constexpr int NW = 8;
+    constexpr int NWT = NW * TWW;  // W tiles per workgroup
+    constexpr int AW = TWW;        // W tiles loaded by each wave per k-block
+    static_assert(S * AW <= 63, "vmcnt range");
+    constexpr uint32_t kRows = NWT * 16;
+    __shared__ __align__(16) int8_t Dst[KBM][QT][1024];
+    __shared__ __align__(16) int8_t Wring[S][NWT][1024];
+    const uint32_t xcd = blockIdx.x % 8, per_group = 8 / ksplit;
+    const uint32_t rb = (blockIdx.x / 8) * per_group + xcd / ksplit;
+    const uint32_t ks = xcd % ksplit;
+    if (rb * kRows >= m) return;  // padding workgroup of the last group
+    const uint32_t kb_per = (nkb + ksplit - 1) / ksplit;  // <= KBM (checked by the launcher)
+    const uint32_t kb0 = ks * kb_per;
+    const uint32_t kb1 = kb0 + kb_per < nkb ? kb0 + kb_per : nkb;
+    const uint32_t nk = kb1 > kb0 ? kb1 - kb0 : 0u;
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint32_t kl = (lane >> 4) * 16;
+    const uint32_t nrt = (m + 15) / 16;
+    const int8_t* wptr[AW];
 #pragma unroll
-        for (int i = 0; i < QW; ++i)
-#pragma unroll
-            for (int t = 0; t < TWW; ++t) {
-                const uint32_t q = qbase + 4 * i, row = rowbase + 16 * t;
-                if (q < B && row < m) Y[(size_t)q * m + row] = value(i, t);
-            }
-        return;
+    for (int a = 0; a < AW; ++a) {
+        const uint32_t row = rb * kRows + (wave * AW + a) * 16 + (lane & 15);
+        wptr[a] = W + (size_t)(row < m ? row : m - 1) * n;
     }
-    // Several k-ranges: every workgroup stores its values with device-coherent
-    // stores (written through the XCD's L2), waits for them, and counts itself
-    // on its row block's counter; the workgroup that arrives last reads the
-    // other ranges' values with device-coherent loads, adds them, writes Y and
-    // resets the counter.  No cache-wide flush or invalidate is needed.  The
-    // values are exchanged in accumulator-tile order (64 consecutive words per
-    // tile, one per lane), so every store and load covers whole cache lines.
-    const size_t nrb = (m + kRows - 1) / kRows;
-    auto slot = [&](uint32_t o, int i, int t) {
-        return ((((size_t)o * nrb + rb) * NW + wave) * (QW * TWW) + i * TWW + t) * 64 + lane;
+    auto issue_w = [&](uint32_t j, int slot) {
+        const uint32_t kbj = kb0 + (j < nk ? j : (nk ? nk - 1 : 0u));
+        const uint32_t kbe = kbj < nkb ? kbj : nkb - 1;
+        const uint32_t k = kbe * 64 + kl;
+        const uint32_t kk = k < n ? k : 0u;
+#pragma unroll
+        for (int a = 0; a < AW; ++a) {
+            const int tile = wave * AW + a;
+            if (PACKED) {
+                const uint32_t rt = rb * (kRows / 16) + tile;
+                dma16(W + (((size_t)(rt < nrt ? rt : nrt - 1) * nkb + kbe) * 64 + lane) * 16, &Wring[slot][tile][0]);
+            } else {
+                dma16(wptr[a] + kk, &Wring[slot][tile][0]);
+            }
+        }
     };
+    // 1. the first S k-blocks of W in flight
 #pragma unroll
-    for (int i = 0; i < QW; ++i)
+    for (int j = 0; j < S; ++j) issue_w(j, j);
+    // 2. digit tiles of this k-range into LDS: unit (local k-block, query,
+    //    16-element quarter) -> the four granules of digits 0..3 (consecutive
+    //    lanes (4q + d) % 16 + 16*kq of tile q/4); queries >= B and elements past
+    //    n are zero.  (Waiting for the query loads also waits for the W loads
+    //    issued above: loads complete in order.)
+    const bool xvec = (n % 16 == 0) && (((uintptr_t)X & 15) == 0);
+    for (uint32_t u = threadIdx.x; u < nk * QT * 16; u += 512) {
+        const uint32_t kq = u % 4, q = (u / 4) % (QT * 4), kbl = u / (QT * 16);
+        const uint32_t k0 = (kb0 + kbl) * 64 + kq * 16;
+        const bool okq = q < B;
+        const uint32_t* xr = X + (size_t)(okq ? q : 0u) * n;
+        uint32_t x[16];
+        if (xvec) {
+            const bool ok = okq && k0 < n;
 #pragma unroll
-        for (int t = 0; t < TWW; ++t)
-            __hip_atomic_store(&part[slot(ks, i, t)], value(i, t), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's stores are complete
-    __syncthreads();
-    uint32_t* flag = reinterpret_cast<uint32_t*>(&Aring[0][0][0]);  // the ring is idle now
-    if (threadIdx.x == 0) *flag = (atomicAdd(&counters[rb], 1u) == ksplit - 1) ? 1u : 0u;
-    __syncthreads();
-    if (!*flag) return;
-    uint32_t v[QW][TWW];
+            for (int v = 0; v < 4; ++v) {
+                const uint4 t = *reinterpret_cast<const uint4*>(xr + (ok ? k0 : 0u) + 4 * v);
+                x[4 * v] = ok ? t.x : 0u;
+                x[4 * v + 1] = ok ? t.y : 0u;
+                x[4 * v + 2] = ok ? t.z : 0u;
+                x[4 * v + 3] = ok ? t.w : 0u;
+            }
+        } else {
 #pragma unroll
-    for (int i = 0; i < QW; ++i)
+            for (int e = 0; e < 16; ++e) {
+                const bool ok = okq && k0 + e < n;
+                const uint32_t t = xr[ok ? k0 + e : 0u];
+                x[e] = ok ? t : 0u;
+            }
+        }
+        int32_t pl[4][4];
 #pragma unroll
-        for (int t = 0; t < TWW; ++t) v[i][t] = value(i, t);
-    for (uint32_t o = 0; o < ksplit; ++o) {  // one round of independent loads per range
-        if (o == ks) continue;
+        for (int w = 0; w < 4; ++w)
+            digit_planes(x[4 * w], x[4 * w + 1], x[4 * w + 2], x[4 * w + 3], pl[0][w], pl[1][w], pl[2][w],
+                         pl[3][w]);
+        int8_t* dst = &Dst[kbl][q / 4][16 * (4 * (q % 4) + 16 * kq)];
 #pragma unroll
-        for (int i = 0; i < QW; ++i)
+        for (int d = 0; d < 4; ++d)
+            *reinterpret_cast<int4*>(dst + 16 * d) = make_int4(pl[d][0], pl[d][1], pl[d][2], pl[d][3]);
+    }
+    v4i acc[QT][TWW];
+#pragma unroll
+    for (int i = 0; i < QT; ++i)
+#pragma unroll
+        for (int t = 0; t < TWW; ++t) acc[i][t] = v4i{0, 0, 0, 0};
+    for (uint32_t j = 0; j < nk; ++j) {
+        const int slot = (int)(j % S);
+        wait_vmcnt<(S - 1) * AW>();  // this wave's loads of k-block j landed
+        __syncthreads();             // everyone's landed (and, the first time, the digit tiles are written)
+        v4i cb[TWW], ca[QT];
+#pragma unroll
+        for (int t = 0; t < TWW; ++t) cb[t] = *reinterpret_cast<const v4i*>(&Wring[slot][wave * TWW + t][16 * lane]);
+#pragma unroll
+        for (int i = 0; i < QT; ++i) ca[i] = *reinterpret_cast<const v4i*>(&Dst[j][i][16 * lane]);
+#pragma unroll
+        for (int i = 0; i < QT; ++i)
 #pragma unroll
             for (int t = 0; t < TWW; ++t)
-                v[i][t] = fadd(v[i][t], __hip_atomic_load(&part[slot(o, i, t)], __ATOMIC_RELAXED,
-                                                          __HIP_MEMORY_SCOPE_AGENT));
+                acc[i][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ca[i], cb[t], acc[i][t], 0, 0, 0);
+        __syncthreads();       // every wave has read the slot
+        issue_w(j + S, slot);  // refill it with k-block j+S
     }
-#pragma unroll
-    for (int i = 0; i < QW; ++i)
-#pragma unroll
-        for (int t = 0; t < TWW; ++t) {
-            const uint32_t q = qbase + 4 * i, row = rowbase + 16 * t;
-            if (q < B && row < m) Y[(size_t)q * m + row] = v[i][t];
-        }
-    if (threadIdx.x == 0) atomicExch(&counters[rb], 0u);
+    wait_vmcnt<0>();  // drain the trailing prefetches before the workgroup exits
+    __syncthreads();  // every wave is past its last ring and digit-tile access
+    const uint32_t rowbase = rb * kRows + wave * (TWW * 16) + (lane & 15);
+    const uint32_t qbase = (uint32_t)(lane >> 4);
+    store_tiles<QT, TWW, NW>(acc, m, B, Y, part, counters, rb, (m + kRows - 1) / kRows, ks, ksplit, wave, lane,
+                             rowbase, qbase, reinterpret_cast<uint32_t*>(&Dst[0][0][0]));
 }
 
 // Streamed-path configurations by digit tiles per launch group (QT): eight
@@ -675,7 +813,6 @@ uint32_t stream_slots(uint32_t qt) { return qt == 16 ? 7u : 8u; }  // W ring dep
 // ceil(workgroups / 256) * (k-blocks per range + pipeline fill), the smaller
 // on ties, keeping at least 4 k-blocks per range.
 uint32_t stream_ksplit(uint32_t m, uint32_t n, uint32_t qt) {
-    if (const char* e = getenv("MVK_KSPLIT_TUNE")) return (uint32_t)atoi(e);  // TUNING ONLY
     const uint32_t nrb = ceil_div(m, stream_rows(qt)), nkb = ceil_div(n, 64);
     const uint32_t fill = stream_slots(qt) + 2;
     // storing and re-reading the partial values of a split costs about
@@ -763,25 +900,79 @@ hipError_t launch_pack_w(const int8_t* W, uint32_t m, uint32_t n, int8_t* Wp, hi
     return hipGetLastError();
 }
 
+namespace {
+// How one launch group of nb queries (4 < nb <= 64) is evaluated.
+struct GroupPlan {
+    bool dstat;     // digits-stationary kernel (else digit matrix + streamed kernel)
+    uint32_t qt;    // digit tiles
+    uint32_t tww;   // W tiles per wave (digits-stationary kernel)
+    uint32_t rows;  // rows per workgroup
+    uint32_t ks;    // k-ranges
+};
+
+constexpr uint32_t kDstatKbm4 = 16, kDstatKbm2 = 32;  // k-blocks of digit tiles in 64 KiB of LDS
+
+GroupPlan group_plan(uint32_t m, uint32_t n, uint32_t nb) {
+    const uint32_t qt = group_qt(nb), nkb = ceil_div(n, 64);
+    GroupPlan g{false, qt, 0, stream_rows(qt), stream_ksplit(m, n, qt)};
+    if (qt > 4) return g;
+    // digits-stationary: rows 128*tww, each k-range's digit tiles fit in LDS;
+    // estimated time ceil(workgroups / 256) * (W k-blocks per workgroup in units
+    // of 128 rows + fill + exchange of the split values)
+    const uint32_t kbm = qt == 4 ? kDstatKbm4 : kDstatKbm2;
+    uint32_t best = 0xffffffffu;
+    for (uint32_t tww = 1; tww <= 2; ++tww)
+        for (uint32_t ks = 1; ks <= 8; ks *= 2) {
+            const uint32_t kb_per = ceil_div(nkb, ks);
+            if (kb_per > kbm) continue;
+            const uint32_t rows = 128 * tww, nwg = ceil_div(m, rows) * ks;
+            const uint32_t cost = ceil_div(nwg, 256) * (kb_per * tww + 6 + (ks > 1 ? qt : 0u));
+            if (cost < best) {
+                best = cost;
+                g = GroupPlan{true, qt, tww, rows, ks};
+            }
+        }
+    return g;
+}
+
+template <int QT, int TWW, int KBM, int S>
+hipError_t launch_dstat_cfg(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t nkb, uint32_t B,
+                            uint32_t* Y, uint32_t ksplit, uint32_t* part, uint32_t* counters, bool packed,
+                            hipStream_t s) {
+    const uint32_t nrb = ceil_div(m, 128 * TWW), per_group = 8 / ksplit;
+    const dim3 grid(ceil_div(nrb, per_group) * 8);
+    if (packed)
+        hipLaunchKernelGGL((server_eval_mfma_dstat<QT, TWW, KBM, S, true>), grid, dim3(512), 0, s, W, m, n, X, nkb,
+                           ksplit, B, Y, part, counters);
+    else
+        hipLaunchKernelGGL((server_eval_mfma_dstat<QT, TWW, KBM, S, false>), grid, dim3(512), 0, s, W, m, n, X, nkb,
+                           ksplit, B, Y, part, counters);
+    return hipGetLastError();
+}
+}  // namespace
+
 ServerEvalPlan server_eval_plan(uint32_t m, uint32_t n, uint32_t B, int path, bool packed) {
     ServerEvalPlan pl{0, 0};
     if (path == MVK_PATH_VALU || B <= 4 || (!packed && n % 16 != 0)) return pl;
     const size_t nkb = ceil_div(n, 64);
-    const uint32_t nb = B < 64 ? B : 64;  // queries of the largest launch group
-    size_t part_bytes = 0;
+    size_t dt_bytes = 0, part_bytes = 0;
     // launch groups hold 64 queries, the last one B % 64 (if nonzero)
-    const uint32_t sizes[2] = {nb, B > 64 ? B % 64 : 0u};
-    for (uint32_t g : sizes) {
-        if (g == 0) continue;
-        const uint32_t qt = group_qt(g), ks = stream_ksplit(m, n, qt);
-        if (ks > 1) {
-            const size_t pb = (size_t)ks * ceil_div(m, stream_rows(qt)) * stream_rows(qt) * qt * 4 * 4;
+    const uint32_t sizes[2] = {B < 64 ? B : 64u, B > 64 ? B % 64 : 0u};
+    for (uint32_t nb : sizes) {
+        if (nb == 0) continue;
+        const GroupPlan g = group_plan(m, n, nb);
+        if (!g.dstat) {
+            const size_t db = (nkb * g.qt * 64 * 16 + 255) & ~(size_t)255;
+            dt_bytes = db > dt_bytes ? db : dt_bytes;
+        }
+        if (g.ks > 1) {
+            const size_t nrb = ceil_div(m, g.rows);
+            const size_t pb = (size_t)g.ks * nrb * g.rows * g.qt * 4 * 4;
             part_bytes = pb > part_bytes ? pb : part_bytes;
-            const size_t cw = ceil_div(m, stream_rows(qt));
-            pl.ctrl_words = cw > pl.ctrl_words ? cw : pl.ctrl_words;
+            pl.ctrl_words = nrb > pl.ctrl_words ? nrb : pl.ctrl_words;
         }
     }
-    pl.ws_bytes = ((nkb * group_qt(nb) * 64 * 16 + 255) & ~(size_t)255) + part_bytes;
+    pl.ws_bytes = dt_bytes + part_bytes;
     return pl;
 }
 
@@ -808,23 +999,46 @@ hipError_t launch_server_eval(const int8_t* W, uint32_t m, uint32_t n, const uin
     }
     // Up to 64 queries per launch group; W is streamed once per group.
     const uint32_t nkb = ceil_div(n, 64);
-    const uint32_t nb_max = B < 64 ? B : 64;
+    size_t dt_bytes = 0;
+    for (uint32_t b0 = 0; b0 < B; b0 += 64) {
+        const GroupPlan g = group_plan(m, n, (B - b0) < 64 ? (B - b0) : 64);
+        if (!g.dstat) {
+            const size_t db = (nkb * g.qt * 64 * 16 + 255) & ~(size_t)255;
+            dt_bytes = db > dt_bytes ? db : dt_bytes;
+        }
+    }
     int8_t* Dt = (int8_t*)ws;
-    uint32_t* part = (uint32_t*)((char*)ws + ((nkb * (size_t)group_qt(nb_max) * 64 * 16 + 255) & ~(size_t)255));
+    uint32_t* part = (uint32_t*)((char*)ws + dt_bytes);
     for (uint32_t b0 = 0; b0 < B; b0 += 64) {
         const uint32_t nb = (B - b0) < 64 ? (B - b0) : 64;
-        const uint32_t qt = group_qt(nb), ks = stream_ksplit(m, n, qt);
-        const uint32_t threads = nkb * qt * 16;
+        const GroupPlan g = group_plan(m, n, nb);
         const uint32_t* Xb = X + (size_t)b0 * n;
+        uint32_t* Yb = Y + (size_t)b0 * m;
+        hipError_t e = hipSuccess;
+        if (g.dstat) {
+            if (g.qt == 4)
+                e = g.tww == 1 ? launch_dstat_cfg<4, 1, kDstatKbm4, 12>(W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
+                                                                         packed, s)
+                               : launch_dstat_cfg<4, 2, kDstatKbm4, 6>(W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
+                                                                        packed, s);
+            else
+                e = g.tww == 1 ? launch_dstat_cfg<2, 1, kDstatKbm2, 12>(W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
+                                                                         packed, s)
+                               : launch_dstat_cfg<2, 2, kDstatKbm2, 6>(W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
+                                                                        packed, s);
+            if (e != hipSuccess) return e;
+            continue;
+        }
+        const uint32_t qt = g.qt, ks = g.ks;
+        const uint32_t threads = nkb * qt * 16;
         if (n % 16 == 0 && (uintptr_t)Xb % 16 == 0)
             hipLaunchKernelGGL(digits_tiled_kernel<true>, dim3(ceil_div(threads, 256)), dim3(256), 0, s, Xb, n, nb,
                                qt, nkb, Dt);
         else
             hipLaunchKernelGGL(digits_tiled_kernel<false>, dim3(ceil_div(threads, 256)), dim3(256), 0, s, Xb, n, nb,
                                qt, nkb, Dt);
-        hipError_t e = hipGetLastError();
+        e = hipGetLastError();
         if (e != hipSuccess) return e;
-        uint32_t* Yb = Y + (size_t)b0 * m;
         if (qt == 2)
             e = launch_stream_cfg<2, 1, 2, 8, 8>(W, m, n, Dt, nkb, nb, Yb, ks, part, counters, packed, s);
         else if (qt == 4)

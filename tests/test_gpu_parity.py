@@ -38,6 +38,9 @@ SERVER_SHAPES = [
     (1, 1, 1), (3, 5, 1), (17, 33, 2), (256, 256, 1), (257, 4099, 1), (64, 4096, 3), (16, 8192, 1),
     (100, 160, 5), (300, 1000, 16), (31, 2048, 64), (4096, 4096, 1), (33, 12345, 4), (50, 4112, 7),
     (129, 300, 17), (70, 999, 65), (16, 128, 130), (200, 4096, 32), (1000, 8192, 64),
+    # 5..16 queries with the digit tiles kept in LDS: split k-ranges, ragged
+    # rows, and a row length whose k-ranges no longer fit (other kernel)
+    (257, 11008, 8), (300, 4096, 12), (64, 16448, 8), (129, 8192, 16),
 ]
 
 

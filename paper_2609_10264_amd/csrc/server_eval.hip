@@ -675,23 +675,20 @@ __global__ __launch_bounds__(NW * 64) void server_eval_mfma_stream(
 
 // Digits-stationary variant for small batches (QT <= 4, i.e. B <= 16): the
 // digit matrix of the workgroup's k-range (QT*16 digit rows x at most KBM
-// k-blocks, 64 KiB) is computed from the queries by the workgroup itself,
-// once, straight into LDS; only W streams through the ring.  No separate
-// digit-matrix launch and no digit traffic per k-block.  Eight waves, each
-// with all QT digit tiles and TWW W tiles (rows 128*TWW per workgroup); every
-// wave loads AW = TWW W tiles per k-block.
-template <int QT, int TWW, int KBM, int S, bool PACKED>
+// k-blocks) is computed from the queries by the workgroup itself, once,
+// straight into LDS; it is read-only afterwards, so the main loop has no
+// barriers.  W needs no sharing between waves (each wave owns TWW row tiles),
+// so it travels HBM -> registers with ordinary loads: chunks of C k-blocks,
+// the next chunk's loads issued before the current chunk's MFMAs (two
+// register sets used in turn).  Eight waves; rows 128*TWW per workgroup.
+template <int QT, int TWW, int KBM, int C, bool PACKED>
 __global__ __launch_bounds__(512) void server_eval_mfma_dstat(const int8_t* __restrict__ W, uint32_t m, uint32_t n,
                                                               const uint32_t* __restrict__ X, uint32_t nkb,
                                                               uint32_t ksplit, uint32_t B, uint32_t* __restrict__ Y,
                                                               uint32_t* part, uint32_t* counters) {
     constexpr int NW = 8;
-    constexpr int NWT = NW * TWW;  // W tiles per workgroup
-    constexpr int AW = TWW;        // W tiles loaded by each wave per k-block
-    static_assert(S * AW <= 63, "vmcnt range");
-    constexpr uint32_t kRows = NWT * 16;
+    constexpr uint32_t kRows = NW * TWW * 16;
     __shared__ __align__(16) int8_t Dst[KBM][QT][1024];
-    __shared__ __align__(16) int8_t Wring[S][NWT][1024];
     const uint32_t xcd = blockIdx.x % 8, per_group = 8 / ksplit;
     const uint32_t rb = (blockIdx.x / 8) * per_group + xcd / ksplit;
     const uint32_t ks = xcd % ksplit;
@@ -705,95 +702,122 @@ __global__ __launch_bounds__(512) void server_eval_mfma_dstat(const int8_t* __re
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const uint32_t kl = (lane >> 4) * 16;
     const uint32_t nrt = (m + 15) / 16;
-    const int8_t* wptr[AW];
+    const int8_t* wptr[TWW];
 #pragma unroll
-    for (int a = 0; a < AW; ++a) {
-        const uint32_t row = rb * kRows + (wave * AW + a) * 16 + (lane & 15);
-        wptr[a] = W + (size_t)(row < m ? row : m - 1) * n;
+    for (int t = 0; t < TWW; ++t) {
+        const uint32_t row = rb * kRows + (wave * TWW + t) * 16 + (lane & 15);
+        wptr[t] = W + (size_t)(row < m ? row : m - 1) * n;
     }
-    auto issue_w = [&](uint32_t j, int slot) {
+    // B operand of row tile t at local k-block j (in range: blocks past the
+    // end re-read the last block of the range, masked out below)
+    auto load_w = [&](uint32_t j, int t) -> v4i {
         const uint32_t kbj = kb0 + (j < nk ? j : (nk ? nk - 1 : 0u));
         const uint32_t kbe = kbj < nkb ? kbj : nkb - 1;
-        const uint32_t k = kbe * 64 + kl;
-        const uint32_t kk = k < n ? k : 0u;
-#pragma unroll
-        for (int a = 0; a < AW; ++a) {
-            const int tile = wave * AW + a;
-            if (PACKED) {
-                const uint32_t rt = rb * (kRows / 16) + tile;
-                dma16(W + (((size_t)(rt < nrt ? rt : nrt - 1) * nkb + kbe) * 64 + lane) * 16, &Wring[slot][tile][0]);
-            } else {
-                dma16(wptr[a] + kk, &Wring[slot][tile][0]);
-            }
+        if (PACKED) {
+            const uint32_t rt = rb * (kRows / 16) + wave * TWW + t;
+            return *reinterpret_cast<const v4i*>(W + (((size_t)(rt < nrt ? rt : nrt - 1) * nkb + kbe) * 64 + lane) * 16);
         }
+        const uint32_t k = kbe * 64 + kl;
+        return *reinterpret_cast<const v4i*>(wptr[t] + (k < n ? k : 0u));  // columns >= n meet zero digits
     };
-    // 1. the first S k-blocks of W in flight
-#pragma unroll
-    for (int j = 0; j < S; ++j) issue_w(j, j);
-    // 2. digit tiles of this k-range into LDS: unit (local k-block, query,
-    //    16-element quarter) -> the four granules of digits 0..3 (consecutive
-    //    lanes (4q + d) % 16 + 16*kq of tile q/4); queries >= B and elements past
-    //    n are zero.  (Waiting for the query loads also waits for the W loads
-    //    issued above: loads complete in order.)
+    // Digit tiles of this k-range into LDS: unit (local k-block, query,
+    // 16-element quarter) -> the four granules of digits 0..3 (consecutive lanes
+    // (4q + d) % 16 + 16*kq of tile q/4); queries >= B and elements past n are
+    // zero.  A thread has at most kUnits units; their query loads are issued
+    // first (needed first), then the first W chunk, then the conversion (which
+    // waits for the query loads only).
+    constexpr int kUnits = (KBM * QT * 16 + 511) / 512;
+    const uint32_t nunits = nk * QT * 16;
     const bool xvec = (n % 16 == 0) && (((uintptr_t)X & 15) == 0);
-    for (uint32_t u = threadIdx.x; u < nk * QT * 16; u += 512) {
+    uint32_t x[kUnits][16];
+#pragma unroll
+    for (int r = 0; r < kUnits; ++r) {
+        const uint32_t u = threadIdx.x + 512u * r;
         const uint32_t kq = u % 4, q = (u / 4) % (QT * 4), kbl = u / (QT * 16);
         const uint32_t k0 = (kb0 + kbl) * 64 + kq * 16;
-        const bool okq = q < B;
+        const bool okq = u < nunits && q < B;
         const uint32_t* xr = X + (size_t)(okq ? q : 0u) * n;
-        uint32_t x[16];
         if (xvec) {
             const bool ok = okq && k0 < n;
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 const uint4 t = *reinterpret_cast<const uint4*>(xr + (ok ? k0 : 0u) + 4 * v);
-                x[4 * v] = ok ? t.x : 0u;
-                x[4 * v + 1] = ok ? t.y : 0u;
-                x[4 * v + 2] = ok ? t.z : 0u;
-                x[4 * v + 3] = ok ? t.w : 0u;
+                x[r][4 * v] = ok ? t.x : 0u;
+                x[r][4 * v + 1] = ok ? t.y : 0u;
+                x[r][4 * v + 2] = ok ? t.z : 0u;
+                x[r][4 * v + 3] = ok ? t.w : 0u;
             }
         } else {
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
                 const bool ok = okq && k0 + e < n;
                 const uint32_t t = xr[ok ? k0 + e : 0u];
-                x[e] = ok ? t : 0u;
+                x[r][e] = ok ? t : 0u;
             }
         }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    v4i wa[C][TWW], wb[C][TWW];
+#pragma unroll
+    for (int c = 0; c < C; ++c)
+#pragma unroll
+        for (int t = 0; t < TWW; ++t) wa[c][t] = load_w(c, t);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int r = 0; r < kUnits; ++r) {
+        const uint32_t u = threadIdx.x + 512u * r;
+        if (u >= nunits) break;
+        const uint32_t kq = u % 4, q = (u / 4) % (QT * 4), kbl = u / (QT * 16);
         int32_t pl[4][4];
 #pragma unroll
         for (int w = 0; w < 4; ++w)
-            digit_planes(x[4 * w], x[4 * w + 1], x[4 * w + 2], x[4 * w + 3], pl[0][w], pl[1][w], pl[2][w],
-                         pl[3][w]);
+            digit_planes(x[r][4 * w], x[r][4 * w + 1], x[r][4 * w + 2], x[r][4 * w + 3], pl[0][w], pl[1][w],
+                         pl[2][w], pl[3][w]);
         int8_t* dst = &Dst[kbl][q / 4][16 * (4 * (q % 4) + 16 * kq)];
 #pragma unroll
         for (int d = 0; d < 4; ++d)
             *reinterpret_cast<int4*>(dst + 16 * d) = make_int4(pl[d][0], pl[d][1], pl[d][2], pl[d][3]);
     }
+    __syncthreads();  // digit tiles written; read-only from here on
     v4i acc[QT][TWW];
 #pragma unroll
     for (int i = 0; i < QT; ++i)
 #pragma unroll
         for (int t = 0; t < TWW; ++t) acc[i][t] = v4i{0, 0, 0, 0};
-    for (uint32_t j = 0; j < nk; ++j) {
-        const int slot = (int)(j % S);
-        wait_vmcnt<(S - 1) * AW>();  // this wave's loads of k-block j landed
-        __syncthreads();             // everyone's landed (and, the first time, the digit tiles are written)
-        v4i cb[TWW], ca[QT];
+    // MFMAs of the chunk starting at local k-block j0 with W operands w
+    // (blocks >= nk contribute nothing: their W operand is masked to zero)
+    auto compute = [&](uint32_t j0, const v4i (&w)[C][TWW]) {
 #pragma unroll
-        for (int t = 0; t < TWW; ++t) cb[t] = *reinterpret_cast<const v4i*>(&Wring[slot][wave * TWW + t][16 * lane]);
+        for (int c = 0; c < C; ++c) {
+            const uint32_t j = j0 + c;
+            const int32_t msk = j < nk ? -1 : 0;
+            const uint32_t jd = j < nk ? j : 0u;
+            v4i ca[QT];
 #pragma unroll
-        for (int i = 0; i < QT; ++i) ca[i] = *reinterpret_cast<const v4i*>(&Dst[j][i][16 * lane]);
+            for (int i = 0; i < QT; ++i) ca[i] = *reinterpret_cast<const v4i*>(&Dst[jd][i][16 * lane]);
 #pragma unroll
-        for (int i = 0; i < QT; ++i)
+            for (int t = 0; t < TWW; ++t) {
+                const v4i bw = w[c][t] & msk;
 #pragma unroll
-            for (int t = 0; t < TWW; ++t)
-                acc[i][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ca[i], cb[t], acc[i][t], 0, 0, 0);
-        __syncthreads();       // every wave has read the slot
-        issue_w(j + S, slot);  // refill it with k-block j+S
+                for (int i = 0; i < QT; ++i)
+                    acc[i][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ca[i], bw, acc[i][t], 0, 0, 0);
+            }
+        }
+    };
+    for (uint32_t j0 = 0; j0 < nk; j0 += 2 * C) {
+#pragma unroll
+        for (int c = 0; c < C; ++c)
+#pragma unroll
+            for (int t = 0; t < TWW; ++t) wb[c][t] = load_w(j0 + C + c, t);
+        compute(j0, wa);
+        if (j0 + C >= nk) break;
+#pragma unroll
+        for (int c = 0; c < C; ++c)
+#pragma unroll
+            for (int t = 0; t < TWW; ++t) wa[c][t] = load_w(j0 + 2 * C + c, t);
+        compute(j0 + C, wb);
     }
-    wait_vmcnt<0>();  // drain the trailing prefetches before the workgroup exits
-    __syncthreads();  // every wave is past its last ring and digit-tile access
+    __syncthreads();  // every wave is past its last digit-tile read
     const uint32_t rowbase = rb * kRows + wave * (TWW * 16) + (lane & 15);
     const uint32_t qbase = (uint32_t)(lane >> 4);
     store_tiles<QT, TWW, NW>(acc, m, B, Y, part, counters, rb, (m + kRows - 1) / kRows, ks, ksplit, wave, lane,
@@ -910,7 +934,7 @@ struct GroupPlan {
     uint32_t ks;    // k-ranges
 };
 
-constexpr uint32_t kDstatKbm4 = 16, kDstatKbm2 = 32;  // k-blocks of digit tiles in 64 KiB of LDS
+constexpr uint32_t kDstatKbm4 = 32, kDstatKbm2 = 64;  // k-blocks of digit tiles in 128 KiB of LDS
 
 GroupPlan group_plan(uint32_t m, uint32_t n, uint32_t nb) {
     const uint32_t qt = group_qt(nb), nkb = ceil_div(n, 64);
@@ -935,17 +959,17 @@ GroupPlan group_plan(uint32_t m, uint32_t n, uint32_t nb) {
     return g;
 }
 
-template <int QT, int TWW, int KBM, int S>
+template <int QT, int TWW, int KBM, int C>
 hipError_t launch_dstat_cfg(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t nkb, uint32_t B,
                             uint32_t* Y, uint32_t ksplit, uint32_t* part, uint32_t* counters, bool packed,
                             hipStream_t s) {
     const uint32_t nrb = ceil_div(m, 128 * TWW), per_group = 8 / ksplit;
     const dim3 grid(ceil_div(nrb, per_group) * 8);
     if (packed)
-        hipLaunchKernelGGL((server_eval_mfma_dstat<QT, TWW, KBM, S, true>), grid, dim3(512), 0, s, W, m, n, X, nkb,
+        hipLaunchKernelGGL((server_eval_mfma_dstat<QT, TWW, KBM, C, true>), grid, dim3(512), 0, s, W, m, n, X, nkb,
                            ksplit, B, Y, part, counters);
     else
-        hipLaunchKernelGGL((server_eval_mfma_dstat<QT, TWW, KBM, S, false>), grid, dim3(512), 0, s, W, m, n, X, nkb,
+        hipLaunchKernelGGL((server_eval_mfma_dstat<QT, TWW, KBM, C, false>), grid, dim3(512), 0, s, W, m, n, X, nkb,
                            ksplit, B, Y, part, counters);
     return hipGetLastError();
 }
@@ -1017,14 +1041,14 @@ hipError_t launch_server_eval(const int8_t* W, uint32_t m, uint32_t n, const uin
         hipError_t e = hipSuccess;
         if (g.dstat) {
             if (g.qt == 4)
-                e = g.tww == 1 ? launch_dstat_cfg<4, 1, kDstatKbm4, 12>(W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
-                                                                         packed, s)
-                               : launch_dstat_cfg<4, 2, kDstatKbm4, 6>(W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
+                e = g.tww == 1 ? launch_dstat_cfg<4, 1, kDstatKbm4, 8>(W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
+                                                                        packed, s)
+                               : launch_dstat_cfg<4, 2, kDstatKbm4, 8>(W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
                                                                         packed, s);
             else
-                e = g.tww == 1 ? launch_dstat_cfg<2, 1, kDstatKbm2, 12>(W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
-                                                                         packed, s)
-                               : launch_dstat_cfg<2, 2, kDstatKbm2, 6>(W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
+                e = g.tww == 1 ? launch_dstat_cfg<2, 1, kDstatKbm2, 8>(W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
+                                                                        packed, s)
+                               : launch_dstat_cfg<2, 2, kDstatKbm2, 8>(W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
                                                                         packed, s);
             if (e != hipSuccess) return e;
             continue;

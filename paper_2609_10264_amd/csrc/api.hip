@@ -273,6 +273,14 @@ mvk_status mvk_decode_verify(const mvk_key* key, const uint32_t* Xhat, const uin
     if (st) return st;
     uint32_t* rv = (uint32_t*)ws;
     uint32_t* syn_scratch = (uint32_t*)((char*)ws + r_bytes);
+    if (Ny <= kSynScratchAbove && dv_syn_fits(m, key->n, (uint32_t)Ny, B, ell)) {
+        // one launch: the syndromes overlap the Decrypt and Verify gathers
+        const mvk_code& cy = key->cy;
+        return hip_status(launch_decode_verify_syn(
+            key->PT, key->Q, m, key->n, key->cx.r * key->n, (uint32_t)Ny, Xhat, Yhat, B, ex->idx, ex->val, ex->t,
+            ey->idx, ey->val, ey->t, ell, cy.r, cy.pi1, cy.pi2, cy.v1, cy.v2, rv, Y,
+            (unsigned long long*)((char*)ctrl + kCtrlBase), ctrl, vL, vR, accept, s));
+    }
     // r_q = Gy e_q for every repetition (shared by all columns)
     hipError_t e = launch_syn_sparse(key->cy, ey->idx, ey->val, ey->t, ell, nullptr, syn_scratch, rv, s);
     if (e == hipSuccess) e = launch_dv(key, Xhat, Yhat, B, ex, ey, rv, Y, vL, vR, accept, ctrl, s);

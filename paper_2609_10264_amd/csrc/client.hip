@@ -17,6 +17,7 @@
 // workgroup.  All sums are exact, so results do not depend on the order.
 #include "field.h"
 #include "mvk_internal.h"
+#include "syn_block.h"
 
 namespace mvk {
 
@@ -36,9 +37,10 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
     return v;
 }
 
-// Workgroup shape of the two gather kernels: kCols consecutive output
-// columns (one per lane) x kGroups thread groups (one wave each), each group
-// taking a contiguous quarter of the sparse terms.
+// Workgroup shape of the gather roles: kCols consecutive output columns (one
+// per lane) x G thread groups (one wave each), each group taking a contiguous
+// share of the sparse terms.  G = kB / kCols in the plain kernel, G = 8 in the
+// kernel that also computes the challenge syndromes.
 constexpr int kCols = kClientCols;
 constexpr int kGroups = kB / kCols;
 
@@ -56,15 +58,29 @@ constexpr int kPreQ = 4;
 constexpr int kPreB = 4;
 constexpr int kItems = kMaxEll;  // verify work items (repetition, chunk) per workgroup, at most
 
-// Decode role: columns [cb*kCols, cb*kCols + kCols) of response b.
+// Workgroup of decode_verify_syn: 512 threads, so that one workgroup holds the
+// syndrome of a block of up to 512 * 32 = 16384 positions in LDS.
+constexpr int kFusedThreads = kDvSynThreads;
+constexpr int kFusedGroups = kFusedThreads / kCols;
+
+// Spin limit of the wait for the challenge syndromes (s_sleep 2 per try, well
+// over a second in total): a wait that does not end is reported, not hung.
+constexpr uint32_t kSpinLimit = 1u << 24;
+
+// Decode role: columns [cb*kCols, cb*kCols + kCols) of response b, by the
+// G*64 threads of the workgroup.  WAIT_R: the r_q are being written by other
+// workgroups of the same launch; thread 0 waits until `rdone` reaches ell (or
+// the spin limit passes, which sets *err), then, after a workgroup barrier,
+// the r_q are read device-coherently.
+template <bool WAIT_R, int G>
 __device__ __forceinline__ void decode_part(const uint32_t* __restrict__ PT, uint32_t m, uint32_t Nx,
                                             const uint32_t* __restrict__ Yhat, uint32_t B,
                                             const uint32_t* __restrict__ ex_idx, const uint32_t* __restrict__ ex_val,
-                                            uint32_t tx, const uint32_t* __restrict__ rv, uint32_t ell,
+                                            uint32_t tx, const uint32_t* rv, uint32_t ell,
                                             uint32_t* __restrict__ Y, unsigned long long* accR, uint32_t b,
-                                            uint32_t cb, uint64_t (*part)[kCols]) {
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int g = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform group
+                                            uint32_t cb, uint64_t (*part)[kCols], uint32_t* rdone, uint32_t* err) {
+    const int lane = threadIdx.x & 63;
+    const int g = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform group
     const uint32_t i = cb * kCols + lane;
     const bool act = i < m;
     const uint32_t is = act ? i : 0u;
@@ -72,12 +88,12 @@ __device__ __forceinline__ void decode_part(const uint32_t* __restrict__ PT, uin
     const uint32_t* ev = ex_val + (size_t)b * tx;
     const uint32_t yraw = Yhat[(size_t)b * m + is];
     uint32_t rq[kPreQ];
-    if (g == 0) {
+    if (!WAIT_R && g == 0) {
 #pragma unroll
         for (int q = 0; q < kPreQ; ++q) rq[q] = rv[(size_t)((uint32_t)q < ell ? q : 0) * m + is];
     }
     // group g takes the contiguous terms [g*chunk, min(tx, g*chunk + chunk))
-    const uint32_t chunk = (tx + kGroups - 1) / kGroups;
+    const uint32_t chunk = (tx + G - 1) / G;
     const uint32_t s_beg = (uint32_t)g * chunk;
     const uint32_t s_end = s_beg + chunk < tx ? s_beg + chunk : tx;
     uint64_t acc = 0;
@@ -98,19 +114,42 @@ __device__ __forceinline__ void decode_part(const uint32_t* __restrict__ PT, uin
     }
     part[g][lane] = acc;
     __syncthreads();
+    const uint32_t yh = act ? yraw : 0u;
     if (g == 0) {
         uint64_t tot = 0;
 #pragma unroll
-        for (int h = 0; h < kGroups; ++h) tot += part[h][lane];
-        const uint32_t yh = act ? yraw : 0u;
+        for (int h = 0; h < G; ++h) tot += part[h][lane];
         if (act) Y[(size_t)b * m + i] = fsub(yh, fred64(tot));
+    }
+    if (WAIT_R) {
+        if (threadIdx.x == 0) {
+            uint32_t it = 0;
+            while (__hip_atomic_load(rdone, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < ell) {
+                if (++it > kSpinLimit) {
+                    atomicOr(err, 1u);
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(2);
+            }
+        }
+        __syncthreads();
+        if (g == 0) {
+#pragma unroll
+            for (int q = 0; q < kPreQ; ++q)
+                rq[q] = __hip_atomic_load(&rv[(size_t)((uint32_t)q < ell ? q : 0) * m + is], __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+    if (g == 0) {
         // v_R partial: sum over this block's outputs of r_q[i] * yhat[i]
         for (uint32_t q = 0; q < ell; ++q) {
             uint32_t r = 0;
 #pragma unroll
             for (int u = 0; u < kPreQ; ++u)
                 if ((uint32_t)u == q) r = rq[u];
-            if (q >= (uint32_t)kPreQ) r = rv[(size_t)q * m + is];
+            if (q >= (uint32_t)kPreQ)
+                r = WAIT_R ? __hip_atomic_load(&rv[(size_t)q * m + is], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                           : rv[(size_t)q * m + is];
             const uint64_t ws = wave_sum_u64(ffold((uint64_t)r * yh));
             if (lane == 0) atomicAdd(&accR[(size_t)q * B + b], (unsigned long long)fred64(ws));
         }
@@ -131,26 +170,28 @@ __device__ __forceinline__ void verify_column(const uint32_t (*u_s)[kCols], uint
 // repetition q.  The ell*ty terms are cut into work items (repetition q, chunk
 // c), C chunks per repetition so that the kGroups waves are busy, and the waves
 // take the items round robin; every item is one or more batches of gathers.
+template <int G>
 __device__ __forceinline__ void verify_part(const uint32_t* __restrict__ Q, uint32_t n, uint32_t Ny,
                                             const uint32_t* __restrict__ Xhat, uint32_t B,
                                             const uint32_t* __restrict__ ey_idx, const uint32_t* __restrict__ ey_val,
                                             uint32_t ty, uint32_t ell, unsigned long long* accL, uint32_t cb,
                                             uint64_t (*part)[kCols], uint32_t (*u_s)[kCols]) {
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int g = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform group
+    static_assert(G <= kItems, "one work item per group at least");
+    const int lane = threadIdx.x & 63;
+    const int g = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform group
     const uint32_t k = cb * kCols + lane;
     const bool act = k < n;
     const uint32_t ks = act ? k : 0u;
     uint32_t xp[kPreB];
 #pragma unroll
     for (int u = 0; u < kPreB; ++u) {
-        const uint32_t b = (uint32_t)g + kGroups * u;
+        const uint32_t b = (uint32_t)g + G * u;
         xp[u] = Xhat[(size_t)(b < B ? b : 0u) * n + ks];
     }
-    const uint32_t C = ell >= (uint32_t)kGroups ? 1u : (uint32_t)kGroups / ell;
+    const uint32_t C = ell >= (uint32_t)G ? 1u : (uint32_t)G / ell;
     const uint32_t chunk = (ty + C - 1) / C;
     const uint32_t items = ell * C;
-    for (uint32_t w = g; w < items; w += kGroups) {
+    for (uint32_t w = g; w < items; w += G) {
         const uint32_t q = w / C, c = w % C;
         const uint32_t* ei = ey_idx + (size_t)q * ty;
         const uint32_t* ev = ey_val + (size_t)q * ty;
@@ -175,7 +216,7 @@ __device__ __forceinline__ void verify_part(const uint32_t* __restrict__ Q, uint
         part[w][lane] = acc;
     }
     __syncthreads();
-    for (uint32_t q = g; q < ell; q += kGroups) {
+    for (uint32_t q = g; q < ell; q += G) {
         uint64_t tot = 0;
         for (uint32_t c = 0; c < C; ++c) tot += part[q * C + c][lane];
         u_s[q][lane] = act ? fred64(tot) : 0u;  // (e_q^T Q)[k]
@@ -183,11 +224,48 @@ __device__ __forceinline__ void verify_part(const uint32_t* __restrict__ Q, uint
     __syncthreads();
 #pragma unroll
     for (int u = 0; u < kPreB; ++u) {
-        const uint32_t b = (uint32_t)g + kGroups * u;
+        const uint32_t b = (uint32_t)g + G * u;
         if (b < B) verify_column(u_s, ell, B, b, xp[u], accL);
     }
-    for (uint32_t b = (uint32_t)g + kGroups * kPreB; b < B; b += kGroups)
+    for (uint32_t b = (uint32_t)g + G * kPreB; b < B; b += G)
         verify_column(u_s, ell, B, b, Xhat[(size_t)b * n + ks], accL);
+}
+
+// End of a decode/verify launch.  Ordering without cache-wide fences: the
+// accumulators are touched only by atomics, which are performed at the
+// device-wide coherence point.  Every wave waits for its atomics to complete
+// (vmcnt 0) before the barrier, the counter increment follows the barrier,
+// and the last workgroup reads the accumulators with atomics after seeing the
+// final count.  It clears them, resets the counter (and rdone / err, when
+// given), and writes vL, vR and accept.
+__device__ __forceinline__ void finish(uint32_t B, uint32_t ell, unsigned long long* accL,
+                                       unsigned long long* accR, uint32_t* counter, uint32_t* rdone, uint32_t* err,
+                                       uint32_t* __restrict__ vL, uint32_t* __restrict__ vR,
+                                       uint32_t* __restrict__ accept, uint32_t* last) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) *last = (atomicAdd(counter, 1u) == gridDim.x - 1) ? 1u : 0u;
+    __syncthreads();
+    if (!*last) return;
+    const uint32_t bad = err ? __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
+    for (uint32_t b = threadIdx.x; b < B; b += blockDim.x) {
+        uint32_t ok = bad ? 0u : 1u;
+        for (uint32_t q = 0; q < ell; ++q) {
+            const size_t o = (size_t)q * B + b;
+            const uint32_t L = fred64(atomicExch(&accL[o], 0ull));
+            const uint32_t R = fred64(atomicExch(&accR[o], 0ull));
+            if (vL) vL[o] = L;
+            if (vR) vR[o] = R;
+            ok &= (L == R) ? 1u : 0u;
+        }
+        accept[b] = ok;
+    }
+    __syncthreads();  // every thread has read err
+    if (threadIdx.x == 0) {
+        if (rdone) atomicExch(rdone, 0u);
+        if (err) atomicExch(err, 0u);
+        atomicExch(counter, 0u);
+    }
 }
 
 // One launch for Decrypt, the two inner products of Verify and the final
@@ -212,36 +290,134 @@ __global__ __launch_bounds__(kB) void decode_verify_fused(
     const uint32_t bid = blockIdx.x;
     const uint32_t ndec = B * nblkR;
     if (bid < ndec)
-        decode_part(PT, m, Nx, Yhat, B, ex_idx, ex_val, tx, rv, ell, Y, accR, bid / nblkR, bid % nblkR, part);
+        decode_part<false, kGroups>(PT, m, Nx, Yhat, B, ex_idx, ex_val, tx, rv, ell, Y, accR, bid / nblkR,
+                                    bid % nblkR, part, nullptr, nullptr);
     else
-        verify_part(Q, n, Ny, Xhat, B, ey_idx, ey_val, ty, ell, accL, bid - ndec, part, u_s);
+        verify_part<kGroups>(Q, n, Ny, Xhat, B, ey_idx, ey_val, ty, ell, accL, bid - ndec, part, u_s);
 
-    // Ordering without cache-wide fences: the accumulators are touched only by
-    // atomics, which are performed at the device-wide coherence point.  Every
-    // wave waits for its atomics to complete (vmcnt 0) before the barrier, the
-    // counter increment follows the barrier, and the last workgroup reads the
-    // accumulators with atomics after seeing the final count.
+    finish(B, ell, accL, accR, counter, nullptr, nullptr, vL, vR, accept, &last);
+}
+
+// Syndrome role of decode_verify_syn: r_c = Gy e_c into rv (device-coherent
+// stores), then rdone += 1 once every store of the workgroup has completed.
+template <int U>
+__device__ __forceinline__ void syn_part(uint32_t c, uint32_t k, uint32_t r, const uint32_t* __restrict__ pi1,
+                                         const uint32_t* __restrict__ pi2, const uint32_t* __restrict__ v1,
+                                         const uint32_t* __restrict__ v2, const uint32_t* __restrict__ ey_idx,
+                                         const uint32_t* __restrict__ ey_val, uint32_t ty, uint32_t* rv,
+                                         uint32_t* rdone, uint32_t* lds) {
+    syn::syn_block<true, U, kFusedThreads, true>(c, k, r, pi1, pi2, v1, v2, nullptr, ey_idx, ey_val, ty, nullptr,
+                                                 rv, lds);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (threadIdx.x == 0) last = (atomicAdd(counter, 1u) == gridDim.x - 1) ? 1u : 0u;
-    __syncthreads();
-    if (!last) return;
-    for (uint32_t b = threadIdx.x; b < B; b += kB) {
-        uint32_t ok = 1;
-        for (uint32_t q = 0; q < ell; ++q) {
-            const size_t o = (size_t)q * B + b;
-            const uint32_t L = fred64(atomicExch(&accL[o], 0ull));
-            const uint32_t R = fred64(atomicExch(&accR[o], 0ull));
-            if (vL) vL[o] = L;
-            if (vR) vR[o] = R;
-            ok &= (L == R) ? 1u : 0u;
-        }
-        accept[b] = ok;
+    if (threadIdx.x == 0) atomicAdd(rdone, 1u);
+}
+
+// LDS words of decode_verify_syn<U>: the syndrome work arrays, or the part and
+// u_s arrays of the gather roles, whichever is larger (a workgroup has one role).
+constexpr size_t kGatherWords = (sizeof(uint64_t) * kItems * kCols + sizeof(uint32_t) * kMaxEll * kCols) / 4;
+template <int U>
+constexpr size_t fused_lds_words() {
+    return syn::lds_words<U, kFusedThreads>() > kGatherWords ? syn::lds_words<U, kFusedThreads>() : kGatherWords;
+}
+
+// decode_verify_fused with the challenge syndromes r_q = Gy e_q computed in the
+// same launch (blocks of length Ny <= kFusedThreads * U).  Workgroups
+// [0, ell) compute r_q (one repetition each, the whole block in LDS), the next
+// nblkL take the verify role (which does not need r), the rest the decode
+// role: their gathers and the Y outputs do not need r either, so only the v_R
+// partials wait for the syndrome workgroups (rdone, counted up to ell).  The
+// syndrome workgroups have the lowest indices and are dispatched first, so the
+// waits end whatever the residency.  The last workgroup also resets rdone and
+// err; if a wait ran into its spin limit, every column is rejected.
+template <int U>
+__global__ __launch_bounds__(kFusedThreads) void decode_verify_syn(
+    const uint32_t* __restrict__ PT, const uint32_t* __restrict__ Q, uint32_t m, uint32_t n, uint32_t Nx,
+    uint32_t Ny, const uint32_t* __restrict__ Xhat, const uint32_t* __restrict__ Yhat, uint32_t B,
+    const uint32_t* __restrict__ ex_idx, const uint32_t* __restrict__ ex_val, uint32_t tx,
+    const uint32_t* __restrict__ ey_idx, const uint32_t* __restrict__ ey_val, uint32_t ty, uint32_t ell,
+    uint32_t cyr, const uint32_t* __restrict__ pi1, const uint32_t* __restrict__ pi2,
+    const uint32_t* __restrict__ v1, const uint32_t* __restrict__ v2, uint32_t* rv, uint32_t* __restrict__ Y,
+    unsigned long long* accL, unsigned long long* accR, uint32_t nblkR, uint32_t nblkL, uint32_t* ctrl,
+    uint32_t* __restrict__ vL, uint32_t* __restrict__ vR, uint32_t* __restrict__ accept) {
+    __shared__ __align__(16) uint32_t lds[fused_lds_words<U>()];
+    __shared__ uint32_t last;
+    auto part = reinterpret_cast<uint64_t (*)[kCols]>(lds);
+    auto u_s = reinterpret_cast<uint32_t (*)[kCols]>(lds + 2 * kItems * kCols);
+    uint32_t* counter = &ctrl[0];
+    uint32_t* rdone = &ctrl[1];
+    uint32_t* err = &ctrl[2];
+    const uint32_t bid = blockIdx.x;
+    if (bid < ell)
+        syn_part<U>(bid, m, cyr, pi1, pi2, v1, v2, ey_idx, ey_val, ty, rv, rdone, lds);
+    else if (bid < ell + nblkL)
+        verify_part<kFusedGroups>(Q, n, Ny, Xhat, B, ey_idx, ey_val, ty, ell, accL, bid - ell, part, u_s);
+    else {
+        const uint32_t d = bid - ell - nblkL;
+        decode_part<true, kFusedGroups>(PT, m, Nx, Yhat, B, ex_idx, ex_val, tx, rv, ell, Y, accR, d / nblkR,
+                                        d % nblkR, part, rdone, err);
     }
-    if (threadIdx.x == 0) atomicExch(counter, 0u);
+    finish(B, ell, accL, accR, counter, rdone, err, vL, vR, accept, &last);
+}
+
+template <int U>
+int fused_blocks_per_cu() {
+    int nb = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, decode_verify_syn<U>, kFusedThreads, 0) != hipSuccess)
+        return 0;
+    return nb;
 }
 
 }  // namespace
+
+uint32_t dv_syn_u(uint32_t Ny) {
+    for (uint32_t U : {8u, 16u, 24u, 32u})
+        if (Ny <= (uint32_t)kFusedThreads * U) return U;
+    return 0;
+}
+
+bool dv_syn_fits(uint32_t m, uint32_t n, uint32_t Ny, uint32_t B, uint32_t ell) {
+    const uint32_t U = dv_syn_u(Ny);
+    if (U == 0 || ell == 0 || ell > (uint32_t)kMaxEll || Ny == 0) return false;
+    // residency of one workgroup per CU at least, per device and U (cached)
+    constexpr int kMaxDevices = 64;
+    static int cache[kMaxDevices][4];  // blocks per CU x CUs, plus one; 0 = not yet known
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return false;
+    const int ui = (int)U / 8 - 1;
+    if (cache[dev][ui] == 0) {
+        int ncu = 0;
+        if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return false;
+        const int nb = U == 8 ? fused_blocks_per_cu<8>() : U == 16 ? fused_blocks_per_cu<16>()
+                     : U == 24 ? fused_blocks_per_cu<24>() : fused_blocks_per_cu<32>();
+        cache[dev][ui] = nb * ncu + 1;
+    }
+    const uint64_t grid = (uint64_t)ell + ceil_div(n, kCols) + (uint64_t)B * ceil_div(m, kCols);
+    return grid <= (uint64_t)(cache[dev][ui] - 1);
+}
+
+hipError_t launch_decode_verify_syn(const uint32_t* PT, const uint32_t* Q, uint32_t m, uint32_t n, uint32_t Nx,
+                                    uint32_t Ny, const uint32_t* Xhat, const uint32_t* Yhat, uint32_t B,
+                                    const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx,
+                                    const uint32_t* ey_idx, const uint32_t* ey_val, uint32_t ty, uint32_t ell,
+                                    uint32_t cyr, const uint32_t* pi1, const uint32_t* pi2, const uint32_t* v1,
+                                    const uint32_t* v2, uint32_t* r, uint32_t* Y, unsigned long long* acc,
+                                    uint32_t* ctrl, uint32_t* vL, uint32_t* vR, uint32_t* accept, hipStream_t s) {
+    const uint32_t U = dv_syn_u(Ny);
+    if (U == 0 || ell == 0 || ell > (uint32_t)kMaxEll || (uint64_t)cyr * m != Ny) return hipErrorInvalidValue;
+    const uint32_t nblkL = ceil_div(n, kCols), nblkR = ceil_div(m, kCols);
+    const uint32_t grid = ell + nblkL + B * nblkR;
+#define MVK_DVS(UU)                                                                                               \
+    hipLaunchKernelGGL(decode_verify_syn<UU>, dim3(grid), dim3(kFusedThreads), 0, s, PT, Q, m, n, Nx, Ny, Xhat,   \
+                       Yhat, B, ex_idx, ex_val, tx, ey_idx, ey_val, ty, ell, cyr, pi1, pi2, v1, v2, r, Y, acc,     \
+                       acc + (size_t)ell * B, nblkR, nblkL, ctrl, vL, vR, accept)
+    if (U == 8) MVK_DVS(8);
+    else if (U == 16) MVK_DVS(16);
+    else if (U == 24) MVK_DVS(24);
+    else MVK_DVS(32);
+#undef MVK_DVS
+    return hipGetLastError();
+}
 
 hipError_t launch_decode_verify(const uint32_t* PT, const uint32_t* Q, uint32_t m, uint32_t n, uint32_t Nx,
                                 uint32_t Ny, const uint32_t* Xhat, const uint32_t* Yhat, uint32_t B,

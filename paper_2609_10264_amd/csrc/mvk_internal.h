@@ -64,6 +64,23 @@ hipError_t launch_decode_verify(const uint32_t* PT, const uint32_t* Q, uint32_t 
                                 unsigned long long* acc, uint32_t* counter, uint32_t* vL, uint32_t* vR,
                                 uint32_t* accept, hipStream_t s);
 
+// The same with the challenge syndromes r_q = Gy e_q computed in the launch
+// (written to r, ell x m words) by 512-thread workgroups that hold a whole
+// block of Ny = cyr * m positions in LDS.  ctrl: words 0 (counter), 1 and 2
+// (syndrome completion count, wait time-out flag), zero before the first
+// launch and left at zero.  dv_syn_fits: the launch applies (Ny small enough,
+// every workgroup resident at once on the current device).
+constexpr uint32_t kDvSynThreads = 512;
+uint32_t dv_syn_u(uint32_t Ny);
+bool dv_syn_fits(uint32_t m, uint32_t n, uint32_t Ny, uint32_t B, uint32_t ell);
+hipError_t launch_decode_verify_syn(const uint32_t* PT, const uint32_t* Q, uint32_t m, uint32_t n, uint32_t Nx,
+                                    uint32_t Ny, const uint32_t* Xhat, const uint32_t* Yhat, uint32_t B,
+                                    const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx,
+                                    const uint32_t* ey_idx, const uint32_t* ey_val, uint32_t ty, uint32_t ell,
+                                    uint32_t cyr, const uint32_t* pi1, const uint32_t* pi2, const uint32_t* v1,
+                                    const uint32_t* v2, uint32_t* r, uint32_t* Y, unsigned long long* acc,
+                                    uint32_t* ctrl, uint32_t* vL, uint32_t* vR, uint32_t* accept, hipStream_t s);
+
 inline uint32_t ceil_div(uint32_t a, uint32_t b) { return (a + b - 1) / b; }
 
 }  // namespace mvk

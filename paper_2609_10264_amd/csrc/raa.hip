@@ -18,6 +18,7 @@
 //  * syn_p1/p2/p3: longer vectors, cut into segments over three launches.
 #include "field.h"
 #include "mvk_internal.h"
+#include "syn_block.h"
 
 namespace mvk {
 
@@ -93,73 +94,14 @@ hipError_t launch_encT(const mvk_code& c, const T* in, size_t ld_in, size_t vs_i
 }
 
 // ---------------------------------------------------------------------------
-// Syndrome of short blocks: one 1024-thread workgroup per vector, N <= 16384.
-//
-// Both work arrays live in LDS as 1024 rows of E+1 words: position j sits at
-// word j + j/E, so row t holds positions [t*E, t*E + E) plus one pad word.
-// The suffix sums run over contiguous rows (thread t scans its own row, then
-// the row totals are scanned across the workgroup); the odd row stride E+1
-// keeps those row accesses free of bank conflicts.  The code arrays are read
-// with the position interleaved across threads (j = tid + 1024*u, coalesced)
-// and are all in flight before the first LDS phase; the scatters of Pi2 and
-// Pi1 use those registers.
+// Syndrome of short blocks (N <= 16384): one 1024-thread workgroup per
+// vector, the work arrays in LDS (syn_block.h).
 // ---------------------------------------------------------------------------
 constexpr int kSynThreads = 1024;
-constexpr int kSynWaves = kSynThreads / 64;
 constexpr int kSynMaxU = 16;
 static_assert((size_t)kSynThreads * kSynMaxU == kSynScratchAbove, "LDS syndrome covers the scratch-free range");
+using syn::wave_incl_scan_dpp;
 
-// Inclusive scan of one value per lane across the wave with DPP moves
-// (row shifts inside each 16-lane row, then row broadcasts across rows).
-__device__ __forceinline__ uint32_t wave_incl_scan_dpp(uint32_t x) {
-    x = fadd(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, true));  // row_shr:1
-    x = fadd(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, true));  // row_shr:2
-    x = fadd(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, true));  // row_shr:4
-    x = fadd(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, true));  // row_shr:8
-    x = fadd(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false));  // row_bcast:15
-    x = fadd(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false));  // row_bcast:31
-    return x;
-}
-
-template <int E>
-__device__ __forceinline__ uint32_t pad_pos(uint32_t j) {
-    static_assert((E & (E - 1)) == 0, "E is a power of two: the row index is a shift");
-    return j + j / E;
-}
-
-// In-place inclusive suffix sum of the padded array `a` (all 1024*E
-// positions; positions >= N hold zero).  The carry into a row is the sum of
-// the totals of all later rows = grand total - inclusive prefix of totals.
-template <int E>
-__device__ __forceinline__ void row_suffix_scan(uint32_t* a, uint32_t* wsum) {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    uint32_t* row = a + tid * (E + 1);
-    uint32_t x[E];
-#pragma unroll
-    for (int e = 0; e < E; ++e) x[e] = row[e];
-#pragma unroll
-    for (int e = E - 2; e >= 0; --e) x[e] = fadd(x[e], x[e + 1]);
-    const uint32_t incl = wave_incl_scan_dpp(x[0]);
-    if (lane == 63) wsum[wave] = incl;
-    __syncthreads();
-    if (wave == 0) {
-        const uint32_t t = lane < kSynWaves ? wsum[lane] : 0u;
-        const uint32_t ti = wave_incl_scan_dpp(t);
-        if (lane < kSynWaves) wsum[kSynWaves + 1 + lane] = ti;  // inclusive prefix of wave totals
-        if (lane == kSynWaves - 1) wsum[kSynWaves] = ti;        // grand total
-    }
-    __syncthreads();
-    const uint32_t before = wave ? wsum[kSynWaves + wave] : 0u;  // totals of earlier waves
-    const uint32_t carry = fsub(wsum[kSynWaves], fadd(before, incl));
-#pragma unroll
-    for (int e = 0; e < E; ++e) row[e] = fadd(x[e], carry);
-    __syncthreads();
-}
-
-// U: code positions per thread (N <= 1024*U); E: row length, the power of two
-// >= U.  The per-position loops are unconditional (positions >= N read a
-// valid LDS word and write to the writer's own pad word, which no scan
-// reads), so every LDS access of a loop is issued before the first wait.
 template <bool SPARSE, int U>
 __global__ __launch_bounds__(kSynThreads) void syn_wg(uint32_t k, uint32_t r, const uint32_t* __restrict__ pi1,
                                                       const uint32_t* __restrict__ pi2,
@@ -169,111 +111,8 @@ __global__ __launch_bounds__(kSynThreads) void syn_wg(uint32_t k, uint32_t r, co
                                                       const uint32_t* __restrict__ idx,
                                                       const uint32_t* __restrict__ val, uint32_t t,
                                                       const uint32_t* __restrict__ X, uint32_t* __restrict__ out) {
-    constexpr int E = U <= 4 ? 4 : U <= 8 ? 8 : 16;
-    constexpr int kRow = E + 1;
-    constexpr int kXF = (U + 1) / 2;  // fold outputs per thread prefetched (all of them when r >= 2)
-    __shared__ uint32_t A[kSynThreads * kRow], Bv[kSynThreads * kRow];
-    __shared__ uint32_t wsum[2 * kSynWaves + 2];
-    const uint32_t c = blockIdx.x;
-    const int tid = threadIdx.x;
-    const uint32_t N = k * r;
-    const uint32_t pad_slot = (uint32_t)tid * kRow + E;  // this thread's pad word
-    // Unconditional loads at an in-range position (j < N, else 0), so all of
-    // them are in flight together; positions >= N are never used below.  The
-    // first sparse term of this thread is loaded first: it is needed first.
-    uint32_t sj = 0, sv = 0;
-    if (SPARSE && t) {
-        const uint32_t q = (uint32_t)tid < t ? (uint32_t)tid : 0u;
-        sj = idx[(size_t)c * t + q];
-        sv = val[(size_t)c * t + q];
-    }
-    uint32_t p1[U], p2[U], w1[U], w2[U], xin[SPARSE ? 1 : U], xv[kXF];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-        const uint32_t j = tid + kSynThreads * u;
-        const uint32_t js = j < N ? j : 0u;
-        p1[u] = pi1[js];
-        p2[u] = pi2[js];
-        w1[u] = v1[js];
-        w2[u] = v2[js];
-        if constexpr (!SPARSE) xin[u] = vin[(size_t)c * N + js];
-    }
-    if (X) {
-#pragma unroll
-        for (int f = 0; f < kXF; ++f) {
-            const uint32_t i = tid + kSynThreads * f;
-            xv[f] = X[(size_t)c * k + (i < k ? i : 0u)];
-        }
-    }
-    // A = input, Bv = 0 (the Pi2 scatter fills [0, N); beyond N stays zero)
-    {
-        uint32_t* ra = A + tid * kRow;
-        uint32_t* rb = Bv + tid * kRow;
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-            if (SPARSE) ra[e] = 0u;
-            rb[e] = 0u;
-        }
-    }
-    if constexpr (SPARSE) {
-        __syncthreads();
-        if ((uint32_t)tid < t) A[pad_pos<E>(sj < N ? sj : N - 1)] = sv;
-        for (uint32_t q = tid + kSynThreads; q < t; q += kSynThreads) {
-            const uint32_t j = idx[(size_t)c * t + q];
-            A[pad_pos<E>(j < N ? j : N - 1)] = val[(size_t)c * t + q];
-        }
-    } else {
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const uint32_t j = tid + kSynThreads * u;
-            A[pad_pos<E>(j)] = j < N ? xin[u] : 0u;
-        }
-        // rows past N (positions the loop above does not cover) start at zero
-#pragma unroll
-        for (int e = 0; e < E; ++e)
-            if ((uint32_t)tid * E + e >= (uint32_t)kSynThreads * U) A[tid * kRow + e] = 0u;
-    }
-    __syncthreads();
-    row_suffix_scan<E>(A, wsum);  // A
-#pragma unroll
-    for (int u = 0; u < U; ++u) {  // V2, then Pi2 scatter
-        const uint32_t j = tid + kSynThreads * u;
-        const uint32_t dst = j < N ? pad_pos<E>(p2[u] < N ? p2[u] : N - 1) : pad_slot;
-        Bv[dst] = fmul(w2[u], A[pad_pos<E>(j)]);
-    }
-    __syncthreads();
-    row_suffix_scan<E>(Bv, wsum);  // A
-#pragma unroll
-    for (int u = 0; u < U; ++u) {  // V1, then Pi1 scatter
-        const uint32_t j = tid + kSynThreads * u;
-        const uint32_t dst = j < N ? pad_pos<E>(p1[u] < N ? p1[u] : N - 1) : pad_slot;
-        A[dst] = fmul(w1[u], Bv[pad_pos<E>(j)]);
-    }
-    __syncthreads();
-    // R: fold blocks of r (+ X); reads at clamped positions, masked
-#pragma unroll
-    for (int f = 0; f < kXF; ++f) {
-        const uint32_t i = tid + kSynThreads * f;
-        const uint32_t is = i < k ? i : 0u;
-        uint32_t s = X ? xv[f] : 0u;
-        for (uint32_t q0 = 0; q0 < r; q0 += 4) {
-            uint32_t d[4];
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const uint32_t q = q0 + v < r ? q0 + v : r - 1;
-                d[v] = A[pad_pos<E>(is * r + q)];
-            }
-#pragma unroll
-            for (int v = 0; v < 4; ++v)
-                if (q0 + v < r) s = fadd(s, d[v]);
-        }
-        if (i < k) out[(size_t)c * k + i] = s;
-    }
-    for (uint32_t i = tid + kSynThreads * kXF; i < k; i += kSynThreads) {  // r = 1 only
-        uint32_t s = X ? X[(size_t)c * k + i] : 0u;
-        for (uint32_t q = 0; q < r; ++q) s = fadd(s, A[pad_pos<E>(i * r + q)]);
-        out[(size_t)c * k + i] = s;
-    }
+    __shared__ uint32_t lds[syn::lds_words<U, kSynThreads>()];
+    syn::syn_block<SPARSE, U, kSynThreads, false>(blockIdx.x, k, r, pi1, pi2, v1, v2, vin, idx, val, t, X, out, lds);
 }
 
 // ---------------------------------------------------------------------------

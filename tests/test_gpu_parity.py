@@ -261,6 +261,36 @@ def test_prepared_verify_matches_unprepared():
         assert np.array_equal(Y, oracle.decode(PT, Yh, inst.exi, inst.exv))
 
 
+# Decrypt + Verify with the challenge syndromes r_q = Gy e_q computed in the
+# same launch: block lengths Ny = ry*m in each tile size of that kernel
+# (<= 4096, 8192, 12288, 16384 positions) and past it, and batches whose grid
+# does not fit one wave of resident workgroups (both of those take the separate
+# syndrome launch).  Two calls in a row, the second with a tampered column,
+# check that each launch leaves its completion counters at zero.
+@pytest.mark.parametrize("m,ry,B,ell", [(1000, 4, 2, 3), (4096, 2, 1, 2), (2731, 3, 3, 5), (4096, 3, 2, 16),
+                                        (4096, 4, 1, 1), (16384, 1, 1, 2), (5462, 3, 1, 2), (4096, 3, 9, 2)])
+def test_decode_verify_syndrome_in_launch(m, ry, B, ell):
+    _say(f"decode_verify m={m} ry={ry} B={B} ell={ell}")
+    inst = Instance(55, m, 64, B, 2, 9, ty=31, ell=ell, ry=ry).to_device()
+    mvk.keygen(inst.key, inst.dW)
+    PT, Q = oracle.keygen(inst.W, inst.cx, inst.cy)
+    dXh = mvk.encode(inst.key, inst.dX, inst.dexi, inst.dexv)
+    Xh = host(dXh)
+    Yh = oracle.server_eval(inst.W, Xh)
+    bad = Yh.copy()
+    bad[0, m - 1] = (int(bad[0, m - 1]) + 1) % P
+    for resp, want in ((Yh, [1] * B), (bad, [0] + [1] * (B - 1))):
+        vL = torch.empty((ell, B), dtype=torch.int32, device="cuda")
+        vR = torch.empty_like(vL)
+        Y, acc, vL, vR = mvk.decode_verify(inst.key, dXh, dev(resp), inst.dexi, inst.dexv, inst.deyi, inst.deyv,
+                                           vL=vL, vR=vR)
+        oacc, ovL, ovR = oracle.verify(inst.cy, Q, Xh, resp, inst.eyi, inst.eyv)
+        assert oacc.astype(np.uint32).tolist() == want
+        assert np.array_equal(host(vL), ovL) and np.array_equal(host(vR), ovR)
+        assert host(acc).tolist() == want
+        assert np.array_equal(host(Y), oracle.decode(PT, resp, inst.exi, inst.exv))
+
+
 @pytest.mark.parametrize("ell,ty", [(1, 31), (3, 5), (5, 31), (16, 2)])
 def test_verify_repetition_counts(ell, ty):
     """Work-item split of the verify role for 1..16 repetitions (the maximum)."""

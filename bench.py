@@ -9,8 +9,21 @@ resident in HBM before the timed region.  A pool of distinct weight matrices
 (each with its own preprocessed P^T and Q) is cycled so that consecutive steps
 never find W in the 256 MB last-level cache.
 
+Two schedules of the same work (--mode):
+  pipelined   the paper's standard mode with pipelining (Sec. 7): the work that
+              depends on neither the query nor the response (masks Gx e_x and
+              P e_x, challenge vectors Gy e_q and e_q^T Q; client_prepare) runs
+              on a preparation stream ahead of the online stream
+              (encode_masked -> server_eval -> decode_verify_masked); stream
+              flags order each step after its own preparation.  Both streams
+              replay one HIP graph each, concurrently.
+  serial      every step's calls back to back on one stream (encode ->
+              server_eval -> decode_verify), one HIP graph.
+Every timed step does all of its work inside the timed region in both.
+
 Printed JSON line:
-  value       modMAC/s of the whole step (m*n*B per step / step time)
+  value       modMAC/s of the whole step (m*n*B per step / step time), in the
+              chosen mode; the other mode's step time is printed beside it
   roofline    server_eval kernel: algorithmic bytes (m*n + 4*n*B + 4*m*B) per
               launch / mean launch duration (HIP events around each launch on
               the launch stream), against 8 TB/s HBM
@@ -113,7 +126,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true", help="launch the timed steps one by one instead of a HIP graph")
     ap.add_argument("--chains", type=int, default=1,
-                    help="independent query chains run side by side (step i belongs to chain i mod chains)")
+                    help="serial schedule: independent query chains run side by side (step i belongs to chain "
+                         "i mod chains)")
+    ap.add_argument("--mode", default="pipelined", choices=["pipelined", "serial"],
+                    help="schedule of the timed steps whose time gives `value` (both are measured)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after timing, copy this many MiB device-to-device (reference kernel for HBM counters)")
     ap.add_argument("--seed", type=int, default=2609)
@@ -264,6 +280,80 @@ def main():
     torch.cuda.synchronize()
     now = [(Xh[c], Yh[c], Y[c]) for c in range(C) if timed[c]]
     replay_matches_eager = all(bool(torch.equal(a, b)) for la, lb in zip(last, now) for a, b in zip(la, lb))
+    elapsed_serial, accepted_serial = elapsed, accepted
+
+    # ---- pipelined standard mode -------------------------------------------
+    # Step i's preparation (client_prepare, then a flag) on the preparation
+    # stream; its online part (wait for the flag, encode_masked, server_eval,
+    # decode_verify_masked) on the online stream.  One graph per stream over
+    # all timed steps; the two replays run side by side.
+    preps = [mvk.Prepared(keys[i % pool], B, ell) for i in range(total_steps)]
+    flags = torch.zeros(total_steps, dtype=torch.int32, device=dev)
+    late = torch.zeros((), dtype=torch.int32, device=dev)
+    ACC2 = torch.zeros((total_steps, B), dtype=torch.int32, device=dev)
+    s_prep, s_on = torch.cuda.Stream(), torch.cuda.Stream()
+    pXh = torch.empty((B, n), dtype=torch.int32, device=dev)
+    pYh = torch.empty((B, m), dtype=torch.int32, device=dev)
+    pY = torch.empty((B, m), dtype=torch.int32, device=dev)
+
+    def prepare(i):
+        j = i % pool
+        mvk.client_prepare(keys[j], EXI[i], EXV[i], EYI[i], EYV[i], out=preps[i])
+        mvk.flag_signal(flags[i], 1)
+
+    def online(i):
+        j = i % pool
+        mvk.flag_wait(flags[i], 1, timeout_us=50_000, timed_out=late)
+        mvk.encode_masked(keys[j], X[i], preps[i], out=pXh)
+        mvk.server_eval(Ws[j], pXh, out=pYh, path=args.path)
+        mvk.decode_verify_masked(keys[j], pXh, pYh, preps[i], Y=pY, accept=ACC2[i])
+
+    for i in range(args.warmup):  # also sizes the library's per-stream workspaces
+        with torch.cuda.stream(s_prep):
+            prepare(i)
+    for i in range(args.warmup):
+        with torch.cuda.stream(s_on):
+            online(i)
+    torch.cuda.synchronize()
+    steps_t = list(range(args.warmup, total_steps))
+    g_prep, g_on = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g_prep, stream=s_prep):
+        for i in steps_t:
+            prepare(i)
+    with torch.cuda.graph(g_on, stream=s_on):
+        for i in steps_t:
+            online(i)
+
+    def replay_pipelined():
+        # The preparation graph is submitted first: HIP multiplexes streams onto
+        # a few hardware queues, and a wait queued ahead of its signal on a
+        # shared queue would only end at its time-out.
+        with torch.cuda.stream(s_prep):
+            g_prep.replay()
+        with torch.cuda.stream(s_on):
+            g_on.replay()
+
+    replay_pipelined()  # untimed replay
+    torch.cuda.synchronize()
+    ACC2.zero_()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    replay_pipelined()
+    torch.cuda.synchronize()
+    elapsed_pipe = time.perf_counter() - t0
+    accepted_pipe = bool((ACC2[args.warmup:] == 1).all().item()) and int(late.item()) == 0
+    # the last timed step again through the one-call path: same Xhat, Yhat, Y
+    i_last = steps_t[-1]
+    got = (pXh.clone(), pYh.clone(), pY.clone())
+    with torch.cuda.stream(s_on):
+        rXh = mvk.encode(keys[i_last % pool], X[i_last], EXI[i_last], EXV[i_last])
+        rYh = mvk.server_eval(Ws[i_last % pool], rXh, path=args.path)
+        rY, _, _, _ = mvk.decode_verify(keys[i_last % pool], rXh, rYh, EXI[i_last], EXV[i_last], EYI[i_last],
+                                        EYV[i_last])
+    torch.cuda.synchronize()
+    pipe_matches = all(bool(torch.equal(a, b)) for a, b in zip(got, (rXh, rYh, rY)))
+    if args.mode == "pipelined":
+        elapsed, accepted = elapsed_pipe, accepted_pipe
     s = streams[0]
     Yh = Yh[0]
 
@@ -310,14 +400,17 @@ def main():
         "config": {"workload": f"{args.config}: W {m}x{n} int8-valued in F_p (p=2^31-1), B={B} query column(s), "
                                f"RAA r={r}, t_x={tx}, t_y={ty}, ell={ell}; step = encode+server_eval+decode_verify",
                    "global_batch": B, "w_pool": pool, "launch": "eager" if args.eager else "hip_graph",
-                   "chains": C, "weights": args.weights},
+                   "mode": args.mode, "chains": C if args.mode == "serial" else 1, "weights": args.weights},
+        "ms_per_step_pipelined": 1e3 * elapsed_pipe / args.steps,
+        "ms_per_step_serial": 1e3 * elapsed_serial / args.steps,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(args.config, args.weights),
                      "kernel": f"server_eval ({args.path})", "alg_bytes_per_launch": alg_bytes,
                      "mean_launch_us": 1e6 * se_mean_s},
         "server_eval": {"modmac_per_s": macs / se_mean_s, "gb_per_s": achieved},
-        "all_accepted": accepted,
+        "all_accepted": accepted_serial and accepted_pipe,
         "replay_matches_eager": replay_matches_eager,
+        "pipelined_matches_one_call_path": pipe_matches,
     }
 
     if args.calib_copy_mib:
@@ -325,7 +418,7 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args, cfg, cx_h, cy_h)
     print(json.dumps(out), flush=True)
-    if not (accepted and replay_matches_eager):
+    if not (accepted_serial and accepted_pipe and replay_matches_eager and pipe_matches):
         sys.exit(1)
 
 

@@ -37,7 +37,7 @@ extern "C" {
 #endif
 
 #define MVK_PRIME 2147483647u
-#define MVK_ABI_VERSION 3
+#define MVK_ABI_VERSION 4
 
 typedef int32_t mvk_status;
 #define MVK_OK 0
@@ -212,6 +212,73 @@ mvk_status mvk_decode_verify_prepared(const mvk_key *key, const uint32_t *Xhat,
                                       const uint32_t *Yhat, uint32_t B, const mvk_sparse *ex,
                                       const mvk_sparse *ey, const uint32_t *R, uint32_t *Y,
                                       uint32_t *vL, uint32_t *vR, uint32_t *accept, void *stream);
+
+/*
+ * Client preparation: every part of Encrypt, Decrypt and Verify that depends
+ * on neither the query nor the server's response (Sec. 7 "boost mode": masks
+ * generated ahead of time; its standard mode pipelines the same work for the
+ * next query while the server evaluates the current one).
+ *   ex (may be NULL or count 0): B = ex->count noise vectors e_b of t_x
+ *       positions < Nx (the secret state of Encrypt/Decrypt);
+ *       Mx : device, B x n, written, input masks   Mx_b = Gx e_b
+ *       My : device, B x m, written, output masks  My_b = P e_b = W Mx_b
+ *   ey (may be NULL or count 0): ell = ey->count (1..16) challenges e_q of
+ *       t_y positions < Ny;
+ *       R  : device, ell x m, written, R_q = Gy e_q (as mvk_verify_prepare)
+ *       U  : device, ell x n, written, U_q = e_q^T Q
+ * The outputs are secret to the client (they determine e); the challenges
+ * never leave the client, so they may be drawn before the responses exist.
+ * One launch when Nx and Ny are at most 16384 (syndromes and row gathers side
+ * by side), else the longer syndromes run first in their own launches.
+ * Errors: MVK_EINVAL, MVK_ERANGE (ell > 16 or B > 65535), MVK_ENOMEM.
+ */
+mvk_status mvk_client_prepare(const mvk_key *key, const mvk_sparse *ex, const mvk_sparse *ey,
+                              uint32_t *Mx, uint32_t *My, uint32_t *R, uint32_t *U, void *stream);
+
+/*
+ * Encrypt with a prepared input mask: Xhat = X + Mx (B x n, element-wise mod p).
+ * Same result as mvk_encode with the noise vectors Mx was prepared from.
+ * X, Mx: device, read; Xhat: device, written (may alias X).
+ */
+mvk_status mvk_encode_masked(const mvk_key *key, const uint32_t *X, uint32_t B, const uint32_t *Mx,
+                             uint32_t *Xhat, void *stream);
+
+/*
+ * Decrypt + Verify with prepared masks and challenge vectors (from
+ * mvk_client_prepare): Y_b = Yhat_b - My_b, v_L = U_q . Xhat_b,
+ * v_R = R_q . Yhat_b, accept[b] = 1 iff v_L == v_R for every q < ell.  Same
+ * outputs, bit for bit, as mvk_decode_verify with the same noise and
+ * challenges; no gathers (every input is read once, coalesced).
+ *   My: B x m;  R: ell x m;  U: ell x n (device, read);  other arguments as
+ *   mvk_decode_verify.
+ * Errors: MVK_EINVAL, MVK_ERANGE (ell > 16 or B > 65535), MVK_ENOMEM.
+ */
+mvk_status mvk_decode_verify_masked(const mvk_key *key, const uint32_t *Xhat, const uint32_t *Yhat,
+                                    uint32_t B, const uint32_t *My, uint32_t ell, const uint32_t *R,
+                                    const uint32_t *U, uint32_t *Y, uint32_t *vL, uint32_t *vR,
+                                    uint32_t *accept, void *stream);
+
+/*
+ * Stream flags: order work on two streams whose launches are captured in two
+ * separate HIP graphs (a graph cannot wait for another graph's work).
+ * mvk_flag_signal: when the stream reaches it (all earlier work on the stream
+ *   complete and visible device-wide), *flag = value (value != 0).
+ * mvk_flag_wait: the stream waits until *flag == value, then sets *flag = 0
+ *   (one wait consumes one signal), and only then runs later work.  The wait
+ *   polls from one thread of one workgroup; after timeout_us microseconds it
+ *   gives up, leaves *flag, sets *timed_out (device word, may be NULL) to
+ *   nonzero and lets the stream continue: the caller must check *timed_out
+ *   before trusting what follows.  flag, timed_out: device words.
+ * HIP multiplexes streams onto a few hardware queues, and a waiting kernel
+ * holds up everything queued behind it on its queue: submit the signalling
+ * stream's work before the waits that depend on it (for two graphs, replay
+ * the signalling graph first), so that a shared queue only serialises the
+ * two streams instead of running the waits into their time-outs.
+ * Errors: MVK_EINVAL (null flag, value 0 or timeout 0).
+ */
+mvk_status mvk_flag_signal(uint32_t *flag, uint32_t value, void *stream);
+mvk_status mvk_flag_wait(uint32_t *flag, uint32_t value, uint32_t timeout_us, uint32_t *timed_out,
+                         void *stream);
 
 /*
  * RAA encoding w -> G^T w (App. B, "Linear-time encoding") for `count`

@@ -229,6 +229,88 @@ def decode_verify(key: Key, Xhat: torch.Tensor, Yhat: torch.Tensor, ex_idx: torc
     return Y, accept, vL, vR
 
 
+class Prepared:
+    """Client preparation for one query batch (secret to the client): input and
+    output masks of B noise vectors and the vectors of ell challenges."""
+
+    def __init__(self, key: Key, B: int, ell: int, device="cuda"):
+        i32 = dict(dtype=torch.int32, device=device)
+        self.B, self.ell = B, ell
+        self.Mx = torch.empty((B, key.n), **i32)
+        self.My = torch.empty((B, key.m), **i32)
+        self.R = torch.empty((ell, key.m), **i32)
+        self.U = torch.empty((ell, key.n), **i32)
+
+
+def client_prepare(key: Key, ex_idx: torch.Tensor, ex_val: torch.Tensor, ey_idx: torch.Tensor,
+                   ey_val: torch.Tensor, out: Prepared | None = None, stream=None) -> Prepared:
+    """Masks Mx = Gx e_b, My = P e_b (per noise vector) and R = Gy e_q,
+    U = e_q^T Q (per challenge): the query- and response-independent work."""
+    B, ell = ex_idx.shape[0], ey_idx.shape[0]
+    if out is None:
+        out = Prepared(key, B, ell, device=ex_idx.device)
+    if (out.B, out.ell) != (B, ell):
+        raise ValueError("Prepared buffers do not match the noise / challenge counts")
+    ks = key.struct()
+    ex = _sparse(ex_idx, ex_val, "ex")
+    ey = _sparse(ey_idx, ey_val, "ey")
+    _lib.check("mvk_client_prepare", _lib.load().mvk_client_prepare(
+        ctypes.byref(ks), ctypes.byref(ex), ctypes.byref(ey),
+        _dev(out.Mx, torch.int32, (B, key.n), "Mx"), _dev(out.My, torch.int32, (B, key.m), "My"),
+        _dev(out.R, torch.int32, (ell, key.m), "R"), _dev(out.U, torch.int32, (ell, key.n), "U"),
+        _stream(stream)))
+    return out
+
+
+def encode_masked(key: Key, X: torch.Tensor, prep: Prepared, out: torch.Tensor | None = None,
+                  stream=None) -> torch.Tensor:
+    """Encrypt with a prepared mask: Xhat = X + Mx."""
+    B = X.shape[0]
+    if out is None:
+        out = torch.empty_like(X)
+    ks = key.struct()
+    _lib.check("mvk_encode_masked", _lib.load().mvk_encode_masked(
+        ctypes.byref(ks), _dev(X, torch.int32, (B, key.n), "X"), B,
+        _dev(prep.Mx, torch.int32, (B, key.n), "Mx"), _dev(out, torch.int32, (B, key.n), "Xhat"),
+        _stream(stream)))
+    return out
+
+
+def decode_verify_masked(key: Key, Xhat: torch.Tensor, Yhat: torch.Tensor, prep: Prepared,
+                         Y: torch.Tensor | None = None, vL: torch.Tensor | None = None,
+                         vR: torch.Tensor | None = None, accept: torch.Tensor | None = None, stream=None):
+    """Verify + Decrypt with prepared masks and challenge vectors.  Returns (Y, accept, vL, vR)."""
+    B, ell = Xhat.shape[0], prep.ell
+    dev = Xhat.device
+    if Y is None:
+        Y = torch.empty((B, key.m), dtype=torch.int32, device=dev)
+    if accept is None:
+        accept = torch.empty((B,), dtype=torch.int32, device=dev)
+    ks = key.struct()
+    vLp = _dev(vL, torch.int32, (ell, B), "vL") if vL is not None else None
+    vRp = _dev(vR, torch.int32, (ell, B), "vR") if vR is not None else None
+    _lib.check("mvk_decode_verify_masked", _lib.load().mvk_decode_verify_masked(
+        ctypes.byref(ks), _dev(Xhat, torch.int32, (B, key.n), "Xhat"), _dev(Yhat, torch.int32, (B, key.m), "Yhat"),
+        B, _dev(prep.My, torch.int32, (B, key.m), "My"), ell, _dev(prep.R, torch.int32, (ell, key.m), "R"),
+        _dev(prep.U, torch.int32, (ell, key.n), "U"), _dev(Y, torch.int32, (B, key.m), "Y"), vLp, vRp,
+        _dev(accept, torch.int32, (B,), "accept"), _stream(stream)))
+    return Y, accept, vL, vR
+
+
+def flag_signal(flag: torch.Tensor, value: int = 1, stream=None) -> None:
+    """Set the device word `flag` to value once the stream's earlier work is done."""
+    _lib.check("mvk_flag_signal", _lib.load().mvk_flag_signal(
+        _dev(flag, torch.int32, (), "flag"), value, _stream(stream)))
+
+
+def flag_wait(flag: torch.Tensor, value: int = 1, timeout_us: int = 200000, timed_out: torch.Tensor | None = None,
+              stream=None) -> None:
+    """Make the stream wait until flag == value (then clear it); on time-out set timed_out."""
+    _lib.check("mvk_flag_wait", _lib.load().mvk_flag_wait(
+        _dev(flag, torch.int32, (), "flag"), value, timeout_us,
+        _dev(timed_out, torch.int32, (), "timed_out") if timed_out is not None else None, _stream(stream)))
+
+
 def raa_encode(code: Code, w: torch.Tensor, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
     """G^T w for each row of w (count x k) -> count x N."""
     w2 = w if w.dim() == 2 else w.reshape(1, -1)

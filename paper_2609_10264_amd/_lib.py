@@ -17,7 +17,7 @@ MVK_MAX_N = 131071
 MVK_PATH_AUTO = 0
 MVK_PATH_VALU = 1
 MVK_PATH_MFMA = 2
-ABI_VERSION = 3
+ABI_VERSION = 4
 
 # Every symbol include/mvk.h declares.
 EXPORTS = (
@@ -33,6 +33,11 @@ EXPORTS = (
     "mvk_decode_verify",
     "mvk_verify_prepare",
     "mvk_decode_verify_prepared",
+    "mvk_client_prepare",
+    "mvk_encode_masked",
+    "mvk_decode_verify_masked",
+    "mvk_flag_signal",
+    "mvk_flag_wait",
     "mvk_raa_encode",
     "mvk_raa_syndrome",
 )
@@ -116,6 +121,17 @@ def load() -> ctypes.CDLL:
     L.mvk_decode_verify_prepared.argtypes = [ctypes.POINTER(MvkKey), vp, vp, u32, ctypes.POINTER(MvkSparse),
                                              ctypes.POINTER(MvkSparse), vp, vp, vp, vp, vp, vp]
     L.mvk_decode_verify_prepared.restype = st
+    L.mvk_client_prepare.argtypes = [ctypes.POINTER(MvkKey), ctypes.POINTER(MvkSparse), ctypes.POINTER(MvkSparse),
+                                     vp, vp, vp, vp, vp]
+    L.mvk_client_prepare.restype = st
+    L.mvk_encode_masked.argtypes = [ctypes.POINTER(MvkKey), vp, u32, vp, vp, vp]
+    L.mvk_encode_masked.restype = st
+    L.mvk_decode_verify_masked.argtypes = [ctypes.POINTER(MvkKey), vp, vp, u32, vp, u32, vp, vp, vp, vp, vp, vp, vp]
+    L.mvk_decode_verify_masked.restype = st
+    L.mvk_flag_signal.argtypes = [vp, u32, vp]
+    L.mvk_flag_signal.restype = st
+    L.mvk_flag_wait.argtypes = [vp, u32, u32, vp, vp]
+    L.mvk_flag_wait.restype = st
     L.mvk_raa_encode.argtypes = [ctypes.POINTER(MvkCode), vp, u32, vp, vp]
     L.mvk_raa_encode.restype = st
     L.mvk_raa_syndrome.argtypes = [ctypes.POINTER(MvkCode), vp, u32, vp, vp]

@@ -287,6 +287,73 @@ mvk_status mvk_decode_verify(const mvk_key* key, const uint32_t* Xhat, const uin
     return hip_status(e);
 }
 
+mvk_status mvk_client_prepare(const mvk_key* key, const mvk_sparse* ex, const mvk_sparse* ey, uint32_t* Mx,
+                              uint32_t* My, uint32_t* R, uint32_t* U, void* stream) {
+    mvk_status st = check_key(key);
+    if (st) return st;
+    const uint32_t nx = ex ? ex->count : 0u;
+    if (nx) {
+        if (!Mx || !My || !key->PT || (ex->t && (!ex->idx || !ex->val))) return MVK_EINVAL;
+        if ((uint64_t)ex->t > (uint64_t)key->cx.r * key->n) return MVK_EINVAL;
+        if (nx > 65535u) return MVK_ERANGE;
+    }
+    const uint32_t ny = ey ? ey->count : 0u;
+    if (ny) {
+        st = check_challenges(key, ey);
+        if (st) return st;
+        if (!R || !U || !key->Q) return MVK_EINVAL;
+    }
+    if (nx == 0 && ny == 0) return MVK_OK;
+    hipStream_t s = (hipStream_t)stream;
+    const size_t Nx = (size_t)key->cx.r * key->n, Ny = (size_t)key->cy.r * key->m;
+    size_t scratch = 0;
+    if (nx && Nx > kSynScratchAbove) scratch = (size_t)nx * 2 * Nx * 4;
+    if (ny && Ny > kSynScratchAbove && (size_t)ny * 2 * Ny * 4 > scratch) scratch = (size_t)ny * 2 * Ny * 4;
+    void* ws = nullptr;
+    st = workspace(s, scratch, &ws);
+    if (st) return st;
+    return hip_status(launch_client_prepare(*key, nx ? ex->idx : nullptr, nx ? ex->val : nullptr, nx ? ex->t : 0u,
+                                            nx, ny ? ey->idx : nullptr, ny ? ey->val : nullptr, ny ? ey->t : 0u, ny,
+                                            Mx, My, R, U, (uint32_t*)ws, s));
+}
+
+mvk_status mvk_encode_masked(const mvk_key* key, const uint32_t* X, uint32_t B, const uint32_t* Mx, uint32_t* Xhat,
+                             void* stream) {
+    mvk_status st = check_key(key);
+    if (st) return st;
+    if (B == 0) return MVK_OK;
+    if (!X || !Mx || !Xhat) return MVK_EINVAL;
+    return hip_status(launch_add_masks(X, Mx, (size_t)B * key->n, Xhat, (hipStream_t)stream));
+}
+
+mvk_status mvk_decode_verify_masked(const mvk_key* key, const uint32_t* Xhat, const uint32_t* Yhat, uint32_t B,
+                                    const uint32_t* My, uint32_t ell, const uint32_t* R, const uint32_t* U,
+                                    uint32_t* Y, uint32_t* vL, uint32_t* vR, uint32_t* accept, void* stream) {
+    mvk_status st = check_key(key);
+    if (st) return st;
+    if (B == 0) return MVK_OK;
+    if (!Xhat || !Yhat || !My || !R || !U || !Y || !accept || ell == 0) return MVK_EINVAL;
+    if (ell > kMaxEll || B > 65535u) return MVK_ERANGE;
+    hipStream_t s = (hipStream_t)stream;
+    void* ws = nullptr;
+    uint32_t* ctrl = nullptr;
+    st = workspace(s, 0, &ws, &ctrl, dv_ctrl_bytes(ell, B));
+    if (st) return st;
+    return hip_status(launch_decode_verify_masked(key->m, key->n, Xhat, Yhat, B, My, ell, R, U, Y,
+                                                  (unsigned long long*)((char*)ctrl + kCtrlBase), &ctrl[0], vL, vR,
+                                                  accept, s));
+}
+
+mvk_status mvk_flag_signal(uint32_t* flag, uint32_t value, void* stream) {
+    if (!flag || value == 0) return MVK_EINVAL;
+    return hip_status(launch_flag_signal(flag, value, (hipStream_t)stream));
+}
+
+mvk_status mvk_flag_wait(uint32_t* flag, uint32_t value, uint32_t timeout_us, uint32_t* timed_out, void* stream) {
+    if (!flag || value == 0 || timeout_us == 0) return MVK_EINVAL;
+    return hip_status(launch_flag_wait(flag, value, timeout_us, timed_out, (hipStream_t)stream));
+}
+
 mvk_status mvk_raa_encode(const mvk_code* code, const uint32_t* w, uint32_t count, uint32_t* out, void* stream) {
     if (!code) return MVK_EINVAL;
     mvk_status st = check_code(code, code->k);

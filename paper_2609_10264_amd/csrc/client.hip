@@ -72,13 +72,17 @@ constexpr uint32_t kSpinLimit = 1u << 24;
 // workgroups of the same launch; thread 0 waits until `rdone` reaches ell (or
 // the spin limit passes, which sets *err), then, after a workgroup barrier,
 // the r_q are read device-coherently.
-template <bool WAIT_R, int G>
+//
+// PRE: the output mask P e_b is given (My, B x m, from client_prepare) and
+// replaces the gathers.
+template <bool WAIT_R, int G, bool PRE = false>
 __device__ __forceinline__ void decode_part(const uint32_t* __restrict__ PT, uint32_t m, uint32_t Nx,
                                             const uint32_t* __restrict__ Yhat, uint32_t B,
                                             const uint32_t* __restrict__ ex_idx, const uint32_t* __restrict__ ex_val,
                                             uint32_t tx, const uint32_t* rv, uint32_t ell,
                                             uint32_t* __restrict__ Y, unsigned long long* accR, uint32_t b,
-                                            uint32_t cb, uint64_t (*part)[kCols], uint32_t* rdone, uint32_t* err) {
+                                            uint32_t cb, uint64_t (*part)[kCols], uint32_t* rdone, uint32_t* err,
+                                            const uint32_t* __restrict__ My = nullptr) {
     const int lane = threadIdx.x & 63;
     const int g = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform group
     const uint32_t i = cb * kCols + lane;
@@ -93,6 +97,7 @@ __device__ __forceinline__ void decode_part(const uint32_t* __restrict__ PT, uin
         for (int q = 0; q < kPreQ; ++q) rq[q] = rv[(size_t)((uint32_t)q < ell ? q : 0) * m + is];
     }
     // group g takes the contiguous terms [g*chunk, min(tx, g*chunk + chunk))
+    if (PRE) tx = 0;
     const uint32_t chunk = (tx + G - 1) / G;
     const uint32_t s_beg = (uint32_t)g * chunk;
     const uint32_t s_end = s_beg + chunk < tx ? s_beg + chunk : tx;
@@ -112,6 +117,7 @@ __device__ __forceinline__ void decode_part(const uint32_t* __restrict__ PT, uin
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) acc += ffold((uint64_t)ww[u] * pv[u]);
     }
+    if (PRE && g == 0) acc = My[(size_t)b * m + is];
     part[g][lane] = acc;
     __syncthreads();
     const uint32_t yh = act ? yraw : 0u;
@@ -170,12 +176,15 @@ __device__ __forceinline__ void verify_column(const uint32_t (*u_s)[kCols], uint
 // repetition q.  The ell*ty terms are cut into work items (repetition q, chunk
 // c), C chunks per repetition so that the kGroups waves are busy, and the waves
 // take the items round robin; every item is one or more batches of gathers.
-template <int G>
+//
+// PRE: u_q is given (U, ell x n, from client_prepare) and replaces the gathers.
+template <int G, bool PRE = false>
 __device__ __forceinline__ void verify_part(const uint32_t* __restrict__ Q, uint32_t n, uint32_t Ny,
                                             const uint32_t* __restrict__ Xhat, uint32_t B,
                                             const uint32_t* __restrict__ ey_idx, const uint32_t* __restrict__ ey_val,
                                             uint32_t ty, uint32_t ell, unsigned long long* accL, uint32_t cb,
-                                            uint64_t (*part)[kCols], uint32_t (*u_s)[kCols]) {
+                                            uint64_t (*part)[kCols], uint32_t (*u_s)[kCols],
+                                            const uint32_t* __restrict__ U = nullptr) {
     static_assert(G <= kItems, "one work item per group at least");
     const int lane = threadIdx.x & 63;
     const int g = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform group
@@ -190,7 +199,7 @@ __device__ __forceinline__ void verify_part(const uint32_t* __restrict__ Q, uint
     }
     const uint32_t C = ell >= (uint32_t)G ? 1u : (uint32_t)G / ell;
     const uint32_t chunk = (ty + C - 1) / C;
-    const uint32_t items = ell * C;
+    const uint32_t items = PRE ? 0u : ell * C;
     for (uint32_t w = g; w < items; w += G) {
         const uint32_t q = w / C, c = w % C;
         const uint32_t* ei = ey_idx + (size_t)q * ty;
@@ -217,9 +226,13 @@ __device__ __forceinline__ void verify_part(const uint32_t* __restrict__ Q, uint
     }
     __syncthreads();
     for (uint32_t q = g; q < ell; q += G) {
-        uint64_t tot = 0;
-        for (uint32_t c = 0; c < C; ++c) tot += part[q * C + c][lane];
-        u_s[q][lane] = act ? fred64(tot) : 0u;  // (e_q^T Q)[k]
+        if (PRE) {
+            u_s[q][lane] = act ? U[(size_t)q * n + ks] : 0u;
+        } else {
+            uint64_t tot = 0;
+            for (uint32_t c = 0; c < C; ++c) tot += part[q * C + c][lane];
+            u_s[q][lane] = act ? fred64(tot) : 0u;  // (e_q^T Q)[k]
+        }
     }
     __syncthreads();
 #pragma unroll
@@ -276,6 +289,10 @@ __device__ __forceinline__ void finish(uint32_t B, uint32_t ell, unsigned long l
 // workgroup that finishes last (it sees count == gridDim.x - 1) reads and
 // clears the accumulators, writes vL, vR and accept, and resets the counter,
 // so every launch leaves the accumulators and the counter at zero.
+//
+// PRE: the output masks My and the vectors u_q (U) come from client_prepare;
+// the workgroups then only stream Yhat, My, r and U, Xhat.
+template <bool PRE>
 __global__ __launch_bounds__(kB) void decode_verify_fused(
     const uint32_t* __restrict__ PT, const uint32_t* __restrict__ Q, uint32_t m, uint32_t n, uint32_t Nx,
     uint32_t Ny, const uint32_t* __restrict__ Xhat, const uint32_t* __restrict__ Yhat, uint32_t B,
@@ -283,17 +300,17 @@ __global__ __launch_bounds__(kB) void decode_verify_fused(
     const uint32_t* __restrict__ ey_idx, const uint32_t* __restrict__ ey_val, uint32_t ty, uint32_t ell,
     const uint32_t* __restrict__ rv, uint32_t* __restrict__ Y, unsigned long long* accL, unsigned long long* accR,
     uint32_t nblkR, uint32_t* counter, uint32_t* __restrict__ vL, uint32_t* __restrict__ vR,
-    uint32_t* __restrict__ accept) {
+    uint32_t* __restrict__ accept, const uint32_t* __restrict__ My, const uint32_t* __restrict__ U) {
     __shared__ uint64_t part[kItems][kCols];
     __shared__ uint32_t u_s[kMaxEll][kCols];
     __shared__ uint32_t last;
     const uint32_t bid = blockIdx.x;
     const uint32_t ndec = B * nblkR;
     if (bid < ndec)
-        decode_part<false, kGroups>(PT, m, Nx, Yhat, B, ex_idx, ex_val, tx, rv, ell, Y, accR, bid / nblkR,
-                                    bid % nblkR, part, nullptr, nullptr);
+        decode_part<false, kGroups, PRE>(PT, m, Nx, Yhat, B, ex_idx, ex_val, tx, rv, ell, Y, accR, bid / nblkR,
+                                         bid % nblkR, part, nullptr, nullptr, My);
     else
-        verify_part<kGroups>(Q, n, Ny, Xhat, B, ey_idx, ey_val, ty, ell, accL, bid - ndec, part, u_s);
+        verify_part<kGroups, PRE>(Q, n, Ny, Xhat, B, ey_idx, ey_val, ty, ell, accL, bid - ndec, part, u_s, U);
 
     finish(B, ell, accL, accR, counter, nullptr, nullptr, vL, vR, accept, &last);
 }
@@ -428,9 +445,22 @@ hipError_t launch_decode_verify(const uint32_t* PT, const uint32_t* Q, uint32_t 
     if (ell == 0 || ell > (uint32_t)kMaxEll) return hipErrorInvalidValue;
     const uint32_t nblkL = ceil_div(n, kCols), nblkR = ceil_div(m, kCols);
     const uint32_t grid = B * nblkR + nblkL;
-    hipLaunchKernelGGL(decode_verify_fused, dim3(grid), dim3(kB), 0, s, PT, Q, m, n, Nx, Ny, Xhat, Yhat, B, ex_idx,
-                       ex_val, tx, ey_idx, ey_val, ty, ell, r, Y, acc, acc + (size_t)ell * B, nblkR, counter, vL, vR,
-                       accept);
+    hipLaunchKernelGGL(decode_verify_fused<false>, dim3(grid), dim3(kB), 0, s, PT, Q, m, n, Nx, Ny, Xhat, Yhat, B,
+                       ex_idx, ex_val, tx, ey_idx, ey_val, ty, ell, r, Y, acc, acc + (size_t)ell * B, nblkR, counter,
+                       vL, vR, accept, nullptr, nullptr);
+    return hipGetLastError();
+}
+
+hipError_t launch_decode_verify_masked(uint32_t m, uint32_t n, const uint32_t* Xhat, const uint32_t* Yhat,
+                                       uint32_t B, const uint32_t* My, uint32_t ell, const uint32_t* r,
+                                       const uint32_t* U, uint32_t* Y, unsigned long long* acc, uint32_t* counter,
+                                       uint32_t* vL, uint32_t* vR, uint32_t* accept, hipStream_t s) {
+    if (ell == 0 || ell > (uint32_t)kMaxEll) return hipErrorInvalidValue;
+    const uint32_t nblkL = ceil_div(n, kCols), nblkR = ceil_div(m, kCols);
+    const uint32_t grid = B * nblkR + nblkL;
+    hipLaunchKernelGGL(decode_verify_fused<true>, dim3(grid), dim3(kB), 0, s, nullptr, nullptr, m, n, 0u, 0u, Xhat,
+                       Yhat, B, nullptr, nullptr, 0u, nullptr, nullptr, 0u, ell, r, Y, acc, acc + (size_t)ell * B,
+                       nblkR, counter, vL, vR, accept, My, U);
     return hipGetLastError();
 }
 

@@ -81,6 +81,26 @@ hipError_t launch_decode_verify_syn(const uint32_t* PT, const uint32_t* Q, uint3
                                     const uint32_t* v2, uint32_t* r, uint32_t* Y, unsigned long long* acc,
                                     uint32_t* ctrl, uint32_t* vL, uint32_t* vR, uint32_t* accept, hipStream_t s);
 
+// decode_verify with the output masks My (B x m) and the vectors u_q (U,
+// ell x n) from client_prepare in place of the gathers.
+hipError_t launch_decode_verify_masked(uint32_t m, uint32_t n, const uint32_t* Xhat, const uint32_t* Yhat,
+                                       uint32_t B, const uint32_t* My, uint32_t ell, const uint32_t* r,
+                                       const uint32_t* U, uint32_t* Y, unsigned long long* acc, uint32_t* counter,
+                                       uint32_t* vL, uint32_t* vR, uint32_t* accept, hipStream_t s);
+
+// prepare.hip ---------------------------------------------------------------
+// Mx, My for nx noise vectors and R, U for ny challenges (either count may
+// be 0).  scratch: max(nx * 2 * Nx, ny * 2 * Ny) words when that block length
+// is above kSynScratchAbove, else unused.
+hipError_t launch_client_prepare(const mvk_key& key, const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx,
+                                 uint32_t nx, const uint32_t* ey_idx, const uint32_t* ey_val, uint32_t ty,
+                                 uint32_t ny, uint32_t* Mx, uint32_t* My, uint32_t* R, uint32_t* Uq,
+                                 uint32_t* scratch, hipStream_t s);
+hipError_t launch_add_masks(const uint32_t* X, const uint32_t* Mx, size_t count, uint32_t* Xhat, hipStream_t s);
+hipError_t launch_flag_signal(uint32_t* flag, uint32_t value, hipStream_t s);
+hipError_t launch_flag_wait(uint32_t* flag, uint32_t value, uint32_t timeout_us, uint32_t* timed_out,
+                            hipStream_t s);
+
 inline uint32_t ceil_div(uint32_t a, uint32_t b) { return (a + b - 1) / b; }
 
 }  // namespace mvk

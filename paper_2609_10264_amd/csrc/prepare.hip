@@ -1,0 +1,246 @@
+// Client preparation of Protocol pvMVMD on gfx950: the parts of Encrypt,
+// Decrypt and Verify that depend on neither the query nor the server's
+// response, so that a client can compute them ahead of time (the paper's
+// boost mode) or for the next query while the server evaluates the current
+// one (the pipelining of its standard mode, Sec. 7):
+//   input mask   Mx_b = Gx e_b                     (Encrypt: Xhat_b = X_b + Mx_b)
+//   output mask  My_b = P e_b = sum_j e_j PT[j, :] (Decrypt: Y_b = Yhat_b - My_b)
+//   R_q = Gy e_q  and  u_q = e_q^T Q = sum_j e_j Q[j, :]
+//                                                  (Verify: v_R = R_q . Yhat_b,
+//                                                           v_L = u_q . Xhat_b)
+// plus the two online element-wise steps and the stream flags that order a
+// preparation stream against the online stream when both are captured in
+// separate HIP graphs.
+#include "field.h"
+#include "mvk_internal.h"
+#include "syn_block.h"
+
+namespace mvk {
+
+namespace {
+
+constexpr int kPrepThreads = 1024;     // syndrome workgroups hold a block of up to 16384 positions
+constexpr int kQuarter = 256;          // gather items per workgroup: kPrepThreads / kQuarter
+constexpr int kQuarters = kPrepThreads / kQuarter;
+constexpr int kQCols = 64;             // columns per gather item, one per lane
+constexpr int kQGroups = kQuarter / kQCols;  // waves per item, each a share of the sparse terms
+constexpr int kQBatch = 16;            // gathers in flight per thread
+
+// One gather item by a 256-thread quarter of the workgroup:
+// out[i] = sum_s val[s] * M[idx[s], i] for the 64 columns i in [col0, col0+64).
+// Every quarter of the workgroup passes the one barrier here; a quarter with
+// no item (live = false) issues no loads and writes nothing.
+__device__ __forceinline__ void gather_item(const uint32_t* __restrict__ M, uint32_t ld, uint32_t nrows,
+                                            const uint32_t* __restrict__ idx, const uint32_t* __restrict__ val,
+                                            uint32_t t, uint32_t* __restrict__ out, uint32_t col0, bool live,
+                                            uint64_t (*part)[kQCols]) {
+    const int ltid = threadIdx.x & (kQuarter - 1);
+    const int lane = ltid & 63;
+    const int g = __builtin_amdgcn_readfirstlane(ltid >> 6);
+    const uint32_t i = col0 + lane;
+    const bool act = live && i < ld;
+    const uint32_t is = act ? i : 0u;
+    const uint32_t tt = live ? t : 0u;
+    const uint32_t chunk = (tt + kQGroups - 1) / kQGroups;
+    const uint32_t s_beg = (uint32_t)g * chunk;
+    const uint32_t s_end = s_beg + chunk < tt ? s_beg + chunk : tt;
+    uint64_t acc = 0;
+    for (uint32_t s0 = s_beg; s0 < s_end; s0 += kQBatch) {
+        uint32_t mv[kQBatch], ww[kQBatch];
+#pragma unroll
+        for (int u = 0; u < kQBatch; ++u) {
+            const uint32_t sx = s0 + (uint32_t)u;
+            const bool ok = sx < s_end;
+            const uint32_t sl = ok ? sx : s_beg;  // in-range term, value masked below
+            uint32_t j = idx[sl];
+            j = j < nrows ? j : nrows - 1;
+            ww[u] = ok ? val[sl] : 0u;
+            mv[u] = M[(size_t)j * ld + is];
+        }
+#pragma unroll
+        for (int u = 0; u < kQBatch; ++u) acc += ffold((uint64_t)ww[u] * mv[u]);
+    }
+    part[g][lane] = acc;
+    __syncthreads();
+    if (g == 0 && act) {
+        uint64_t tot = 0;
+#pragma unroll
+        for (int h = 0; h < kQGroups; ++h) tot += part[h][lane];
+        out[i] = fred64(tot);
+    }
+}
+
+template <int U>
+constexpr size_t prep_lds_words() {
+    constexpr size_t gather = (size_t)kQuarters * kQGroups * kQCols * 2;
+    if constexpr (U > 0)
+        return syn::lds_words<U, kPrepThreads>() > gather ? syn::lds_words<U, kPrepThreads>() : gather;
+    else
+        return gather;
+}
+
+struct PrepArgs {
+    // syndromes in this launch: nsx vectors of code x (Mx), nsy of code y (R)
+    uint32_t nsx, nsy;
+    uint32_t n, rx, m, ry;
+    const uint32_t *xpi1, *xpi2, *xv1, *xv2;
+    const uint32_t *ypi1, *ypi2, *yv1, *yv2;
+    const uint32_t *ex_idx, *ex_val;
+    uint32_t tx, nx;  // nx noise vectors (My items), tx terms each
+    const uint32_t *ey_idx, *ey_val;
+    uint32_t ty, ny;  // ny challenges (U items), ty terms each
+    uint32_t nbm, nbn;  // 64-column blocks of m and n
+    const uint32_t *PT, *Q;
+    uint32_t* Mx;
+    uint32_t* My;
+    uint32_t* R;
+    uint32_t* Uq;
+};
+
+// Workgroups [0, nsx) and [nsx, nsx + nsy): one syndrome each (U > 0; the
+// whole block in LDS); the rest: kQuarters gather items each, first the
+// nx * ceil(m/64) items of My (rows of PT), then the ny * ceil(n/64) items of
+// U (rows of Q).
+template <int U>
+__global__ __launch_bounds__(kPrepThreads) void client_prepare_kernel(PrepArgs a) {
+    __shared__ __align__(16) uint32_t lds[prep_lds_words<U>()];
+    uint32_t bid = blockIdx.x;
+    if constexpr (U > 0) {
+        if (bid < a.nsx) {
+            syn::syn_block<true, U, kPrepThreads, false>(bid, a.n, a.rx, a.xpi1, a.xpi2, a.xv1, a.xv2, nullptr,
+                                                         a.ex_idx, a.ex_val, a.tx, nullptr, a.Mx, lds);
+            return;
+        }
+        if (bid < a.nsx + a.nsy) {
+            syn::syn_block<true, U, kPrepThreads, false>(bid - a.nsx, a.m, a.ry, a.ypi1, a.ypi2, a.yv1, a.yv2,
+                                                         nullptr, a.ey_idx, a.ey_val, a.ty, nullptr, a.R, lds);
+            return;
+        }
+        bid -= a.nsx + a.nsy;
+    }
+    const int quarter = threadIdx.x / kQuarter;
+    auto part = reinterpret_cast<uint64_t (*)[kQCols]>(lds) + quarter * kQGroups;
+    const uint32_t item = bid * kQuarters + (uint32_t)quarter;
+    const uint32_t nbm = a.nbm, nbn = a.nbn;
+    const uint32_t ix = a.nx * nbm, iy = a.ny * nbn;
+    if (item < ix) {
+        const uint32_t b = item / nbm, cb = item % nbm;
+        gather_item(a.PT, a.m, a.rx * a.n, a.ex_idx + (size_t)b * a.tx, a.ex_val + (size_t)b * a.tx, a.tx,
+                    a.My + (size_t)b * a.m, cb * kQCols, true, part);
+    } else if (item < ix + iy) {
+        const uint32_t q = (item - ix) / nbn, cb = (item - ix) % nbn;
+        gather_item(a.Q, a.n, a.ry * a.m, a.ey_idx + (size_t)q * a.ty, a.ey_val + (size_t)q * a.ty, a.ty,
+                    a.Uq + (size_t)q * a.n, cb * kQCols, true, part);
+    } else {
+        gather_item(nullptr, 0u, 1u, nullptr, nullptr, 0u, nullptr, 0u, false, part);
+    }
+}
+
+// Xhat = X + Mx, element-wise over count words.
+__global__ __launch_bounds__(256) void add_masks(const uint32_t* X, const uint32_t* __restrict__ Mx,
+                                                 size_t count, uint32_t* Xhat) {
+    for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < count; i += (size_t)gridDim.x * 256)
+        Xhat[i] = fadd(X[i], Mx[i]);
+}
+
+__global__ void flag_signal_kernel(uint32_t* flag, uint32_t value) {
+    if (threadIdx.x == 0) __hip_atomic_store(flag, value, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// One thread polls the flag (device-coherent loads, a short sleep between
+// polls) until it holds `value`, then clears it; after `ticks` of the constant
+// wall clock it gives up, leaves the flag and sets *timed_out.
+__global__ void flag_wait_kernel(uint32_t* flag, uint32_t value, uint64_t ticks, uint32_t* timed_out) {
+    if (threadIdx.x != 0) return;
+    const uint64_t t0 = wall_clock64();
+    while (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != value) {
+        if (wall_clock64() - t0 > ticks) {
+            if (timed_out) atomicOr(timed_out, 1u);
+            return;
+        }
+        __builtin_amdgcn_s_sleep(4);
+    }
+    __hip_atomic_store(flag, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Syndrome tile per thread of a 1024-thread workgroup for block length N
+// (0: above kSynScratchAbove, not in this launch).
+uint32_t prep_u(uint64_t N) {
+    for (uint32_t U : {4u, 8u, 12u, 16u})
+        if (N <= (uint64_t)kPrepThreads * U) return U;
+    return 0;
+}
+
+}  // namespace
+
+hipError_t launch_client_prepare(const mvk_key& key, const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx,
+                                 uint32_t nx, const uint32_t* ey_idx, const uint32_t* ey_val, uint32_t ty,
+                                 uint32_t ny, uint32_t* Mx, uint32_t* My, uint32_t* R, uint32_t* Uq,
+                                 uint32_t* scratch, hipStream_t s) {
+    const uint64_t Nx = (uint64_t)key.cx.r * key.n, Ny = (uint64_t)key.cy.r * key.m;
+    const uint32_t ux = nx ? prep_u(Nx) : 0u, uy = ny ? prep_u(Ny) : 0u;
+    // syndromes too long for one workgroup run in their own (segmented) launches first
+    if (nx && !ux) {
+        const hipError_t e = launch_syn_sparse(key.cx, ex_idx, ex_val, tx, nx, nullptr, scratch, Mx, s);
+        if (e != hipSuccess) return e;
+    }
+    if (ny && !uy) {
+        const hipError_t e = launch_syn_sparse(key.cy, ey_idx, ey_val, ty, ny, nullptr, scratch, R, s);
+        if (e != hipSuccess) return e;
+    }
+    PrepArgs a;
+    a.nsx = ux ? nx : 0u;
+    a.nsy = uy ? ny : 0u;
+    a.n = key.n;
+    a.rx = key.cx.r;
+    a.m = key.m;
+    a.ry = key.cy.r;
+    a.xpi1 = key.cx.pi1, a.xpi2 = key.cx.pi2, a.xv1 = key.cx.v1, a.xv2 = key.cx.v2;
+    a.ypi1 = key.cy.pi1, a.ypi2 = key.cy.pi2, a.yv1 = key.cy.v1, a.yv2 = key.cy.v2;
+    a.ex_idx = ex_idx, a.ex_val = ex_val, a.tx = tx, a.nx = nx;
+    a.ey_idx = ey_idx, a.ey_val = ey_val, a.ty = ty, a.ny = ny;
+    a.nbm = ceil_div(key.m, kQCols), a.nbn = ceil_div(key.n, kQCols);
+    a.PT = key.PT, a.Q = key.Q;
+    a.Mx = Mx, a.My = My, a.R = R, a.Uq = Uq;
+    const uint64_t items = (uint64_t)nx * ceil_div(key.m, kQCols) + (uint64_t)ny * ceil_div(key.n, kQCols);
+    const uint32_t U = ux > uy ? ux : uy;
+    const uint64_t grid = (U ? a.nsx + a.nsy : 0u) + (items + kQuarters - 1) / kQuarters;
+    if (grid == 0) return hipSuccess;
+    if (grid > 0x7fffffffu) return hipErrorInvalidValue;
+#define MVK_PREP(UU)                                                                                        \
+    hipLaunchKernelGGL(client_prepare_kernel<UU>, dim3((uint32_t)grid), dim3(kPrepThreads), 0, s, a)
+    if (U == 0) MVK_PREP(0);
+    else if (U == 4) MVK_PREP(4);
+    else if (U == 8) MVK_PREP(8);
+    else if (U == 12) MVK_PREP(12);
+    else MVK_PREP(16);
+#undef MVK_PREP
+    return hipGetLastError();
+}
+
+hipError_t launch_add_masks(const uint32_t* X, const uint32_t* Mx, size_t count, uint32_t* Xhat, hipStream_t s) {
+    if (count == 0) return hipSuccess;
+    size_t blocks = (count + 255) / 256;
+    if (blocks > 4096) blocks = 4096;
+    hipLaunchKernelGGL(add_masks, dim3((uint32_t)blocks), dim3(256), 0, s, X, Mx, count, Xhat);
+    return hipGetLastError();
+}
+
+hipError_t launch_flag_signal(uint32_t* flag, uint32_t value, hipStream_t s) {
+    hipLaunchKernelGGL(flag_signal_kernel, dim3(1), dim3(64), 0, s, flag, value);
+    return hipGetLastError();
+}
+
+hipError_t launch_flag_wait(uint32_t* flag, uint32_t value, uint32_t timeout_us, uint32_t* timed_out,
+                            hipStream_t s) {
+    int dev = 0, khz = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev);
+    if (e != hipSuccess) return e;
+    if (khz <= 0) return hipErrorInvalidValue;
+    const uint64_t ticks = (uint64_t)timeout_us * (uint64_t)khz / 1000u;
+    hipLaunchKernelGGL(flag_wait_kernel, dim3(1), dim3(64), 0, s, flag, value, ticks, timed_out);
+    return hipGetLastError();
+}
+
+}  // namespace mvk

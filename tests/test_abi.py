@@ -117,3 +117,45 @@ def test_packed_weight_size_and_checks():
     assert lib.mvk_server_eval_packed(odd, 4, 16, fake, 1, fake, None) == L.MVK_EINVAL
     assert lib.mvk_server_eval_packed(fake, 4, L.MVK_MAX_N + 1, fake, 1, fake, None) == L.MVK_ERANGE
     assert lib.mvk_server_eval_packed(fake, 0, 16, fake, 1, fake, None) == L.MVK_OK
+
+
+def test_prepared_path_argument_checks_without_device_work():
+    L = _lib()
+    lib = L.load()
+    fake = ctypes.c_void_p(0x1000)
+    code = L.MvkCode(8, 3, 0x1000, 0x1000, 0x1000, 0x1000)
+    key = L.MvkKey(8, 8, code, code, 0x1000, 0x1000)
+    ex = L.MvkSparse(0x1000, 0x1000, 2, 1)
+    ey = L.MvkSparse(0x1000, 0x1000, 2, 2)
+    prep = lib.mvk_client_prepare
+    # nothing to prepare
+    assert prep(ctypes.byref(key), None, None, None, None, None, None, None) == L.MVK_OK
+    # masks requested without their outputs
+    assert prep(ctypes.byref(key), ctypes.byref(ex), None, None, fake, None, None, None) == L.MVK_EINVAL
+    assert prep(ctypes.byref(key), ctypes.byref(ex), None, fake, None, None, None, None) == L.MVK_EINVAL
+    # noise longer than Nx = 24; too many noise vectors
+    assert prep(ctypes.byref(key), ctypes.byref(L.MvkSparse(0x1000, 0x1000, 25, 1)), None, fake, fake, None,
+                None, None) == L.MVK_EINVAL
+    assert prep(ctypes.byref(key), ctypes.byref(L.MvkSparse(0x1000, 0x1000, 2, 65536)), None, fake, fake, None,
+                None, None) == L.MVK_ERANGE
+    # challenges: the checks of verify, and both outputs required
+    assert prep(ctypes.byref(key), None, ctypes.byref(L.MvkSparse(0x1000, 0x1000, 2, 17)), None, None, fake,
+                fake, None) == L.MVK_ERANGE
+    assert prep(ctypes.byref(key), None, ctypes.byref(ey), None, None, fake, None, None) == L.MVK_EINVAL
+    assert prep(ctypes.byref(key), None, ctypes.byref(ey), None, None, None, fake, None) == L.MVK_EINVAL
+    # encode with a prepared mask
+    assert lib.mvk_encode_masked(ctypes.byref(key), fake, 0, None, None, None) == L.MVK_OK
+    assert lib.mvk_encode_masked(ctypes.byref(key), fake, 1, None, fake, None) == L.MVK_EINVAL
+    # decode/verify with prepared masks: 1 <= ell <= 16, every input present
+    dvm = lib.mvk_decode_verify_masked
+    assert dvm(ctypes.byref(key), fake, fake, 1, fake, 0, fake, fake, fake, None, None, fake, None) == L.MVK_EINVAL
+    assert dvm(ctypes.byref(key), fake, fake, 1, fake, 17, fake, fake, fake, None, None, fake, None) == L.MVK_ERANGE
+    assert dvm(ctypes.byref(key), fake, fake, 1, fake, 2, fake, None, fake, None, None, fake, None) == L.MVK_EINVAL
+    assert dvm(ctypes.byref(key), fake, fake, 1, None, 2, fake, fake, fake, None, None, fake, None) == L.MVK_EINVAL
+    assert dvm(ctypes.byref(key), fake, fake, 0, None, 2, None, None, None, None, None, None, None) == L.MVK_OK
+    # stream flags
+    assert lib.mvk_flag_signal(None, 1, None) == L.MVK_EINVAL
+    assert lib.mvk_flag_signal(fake, 0, None) == L.MVK_EINVAL
+    assert lib.mvk_flag_wait(None, 1, 10, None, None) == L.MVK_EINVAL
+    assert lib.mvk_flag_wait(fake, 0, 10, None, None) == L.MVK_EINVAL
+    assert lib.mvk_flag_wait(fake, 1, 0, None, None) == L.MVK_EINVAL

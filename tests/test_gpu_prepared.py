@@ -1,0 +1,176 @@
+"""GPU parity of the prepared (boost / pipelined standard mode) path and the
+stream flags: client_prepare, encode_masked and decode_verify_masked against
+the oracle and against the one-call path, bit-exact."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from tests.gpu_util import Instance, dev, host
+
+pytestmark = pytest.mark.gpu
+P = synth.P
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_10264_amd as mvk  # noqa: F401  (raises if libmvk.so is missing)
+    mvk._lib.load()
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+import paper_2609_10264_amd as mvk  # noqa: E402
+
+
+def _dense(N, idx, val):
+    e = np.zeros(N, dtype=np.uint32)
+    e[idx] = val
+    return e
+
+
+# cid, m, n, B, r_x, r_y, t_x, ell: block lengths in the one-launch range and
+# above it (Nx = 16500, Ny = 18000: the syndromes take their own launches),
+# several noise vectors and challenges, ragged 64-column blocks.
+PREP = [
+    (80, 256, 256, 1, 2, 2, 8, 2),
+    (81, 1000, 700, 3, 3, 2, 17, 3),
+    (82, 4096, 4096, 1, 3, 3, 64, 2),
+    (83, 300, 5500, 2, 3, 3, 64, 2),
+    (84, 6000, 200, 1, 1, 3, 5, 16),
+]
+
+
+@pytest.mark.parametrize("cid,m,n,B,rx,ry,tx,ell", PREP)
+def test_client_prepare_matches_oracle(cid, m, n, B, rx, ry, tx, ell):
+    _say(f"client_prepare cid={cid} m={m} n={n} B={B} rx={rx} ry={ry} tx={tx} ell={ell}")
+    inst = Instance(cid, m, n, B, rx, tx, ty=31, ell=ell, ry=ry).to_device()
+    mvk.keygen(inst.key, inst.dW)
+    prep = mvk.client_prepare(inst.key, inst.dexi, inst.dexv, inst.deyi, inst.deyv)
+    torch.cuda.synchronize()
+    # input masks: Encrypt of the zero query
+    Mx = oracle.encode(inst.cx, np.zeros((B, n), dtype=np.uint32), inst.exi, inst.exv)
+    assert np.array_equal(host(prep.Mx), Mx)
+    # output masks: P e = W (Gx e), since P = W Gx
+    assert np.array_equal(host(prep.My), oracle.server_eval(inst.W, Mx))
+    # challenge syndromes and u_q = e_q^T Q = (Gy e_q)^T W, since Q = Gy^T W
+    R = np.stack([oracle.syn(inst.cy, _dense(inst.cy["N"], inst.eyi[q], inst.eyv[q])) for q in range(ell)])
+    assert np.array_equal(host(prep.R), R)
+    assert np.array_equal(host(prep.U), oracle.server_eval(np.ascontiguousarray(inst.W.T), R))
+
+
+@pytest.mark.parametrize("cid,m,n,B,rx,ry,tx,ell", PREP[:2] + PREP[3:4])
+def test_masked_path_matches_one_call_path(cid, m, n, B, rx, ry, tx, ell):
+    _say(f"masked path cid={cid} m={m} n={n} B={B}")
+    inst = Instance(cid, m, n, B, rx, tx, ty=31, ell=ell, ry=ry).to_device()
+    mvk.keygen(inst.key, inst.dW)
+    PT, Q = oracle.keygen(inst.W, inst.cx, inst.cy)
+    prep = mvk.client_prepare(inst.key, inst.dexi, inst.dexv, inst.deyi, inst.deyv)
+    Xh = mvk.encode_masked(inst.key, inst.dX, prep)
+    Xh_ref = oracle.encode(inst.cx, inst.X, inst.exi, inst.exv)
+    assert np.array_equal(host(Xh), Xh_ref)
+    Yh = oracle.server_eval(inst.W, Xh_ref)
+    bad = Yh.copy()
+    bad[B - 1, m // 2] = (int(bad[B - 1, m // 2]) + 12345) % P
+    for resp, want in ((Yh, [1] * B), (bad, [1] * (B - 1) + [0])):
+        vL = torch.empty((ell, B), dtype=torch.int32, device="cuda")
+        vR = torch.empty_like(vL)
+        Y, acc, vL, vR = mvk.decode_verify_masked(inst.key, Xh, dev(resp), prep, vL=vL, vR=vR)
+        oacc, ovL, ovR = oracle.verify(inst.cy, Q, Xh_ref, resp, inst.eyi, inst.eyv)
+        assert oacc.astype(np.uint32).tolist() == want
+        assert host(acc).tolist() == want
+        assert np.array_equal(host(vL), ovL) and np.array_equal(host(vR), ovR)
+        assert np.array_equal(host(Y), oracle.decode(PT, resp, inst.exi, inst.exv))
+    # in place: Xhat may be X's own buffer
+    Xc = inst.dX.clone()
+    mvk.encode_masked(inst.key, Xc, prep, out=Xc)
+    assert np.array_equal(host(Xc), Xh_ref)
+
+
+def test_flags_order_two_streams():
+    flags = torch.zeros(4, dtype=torch.int32, device="cuda")
+    late = torch.zeros(1, dtype=torch.int32, device="cuda")[0]
+    buf = torch.zeros(1 << 20, dtype=torch.int32, device="cuda")
+    side, main = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    # the data written before the signal is seen after the wait (the signalling
+    # stream's work is submitted first: the two streams may share a hardware queue)
+    with torch.cuda.stream(side):
+        buf.fill_(3)
+        mvk.flag_signal(flags[0], 7, stream=side)
+    mvk.flag_wait(flags[0], 7, timeout_us=2_000_000, timed_out=late, stream=main)
+    with torch.cuda.stream(main):
+        total = buf.to(torch.int64).sum()
+    torch.cuda.synchronize()
+    assert int(late.item()) == 0
+    assert int(total.item()) == 3 * buf.numel()
+    assert int(flags[0].item()) == 0  # the wait consumed the signal
+    # a wait that is never signalled ends after its time-out and says so
+    mvk.flag_wait(flags[1], 5, timeout_us=2000, timed_out=late, stream=main)
+    torch.cuda.synchronize()
+    assert int(late.item()) == 1 and int(flags[1].item()) == 0
+
+
+def test_pipelined_graphs_match_one_call_path():
+    """The pipelined standard mode as two HIP graphs (preparation stream ahead of
+    the online stream, ordered by flags) against the one-call path, per step."""
+    cid, m, n, B, r, tx, ell, steps = 85, 1000, 700, 2, 3, 17, 2, 4
+    inst = Instance(cid, m, n, B, r, tx, ty=31, ell=ell).to_device()
+    mvk.keygen(inst.key, inst.dW)
+    exi, exv = synth.sparse(synth.seed_for(cid, synth.PURPOSE_NOISE, 1), steps * B, inst.cx["N"], tx)
+    eyi, eyv = synth.sparse(synth.seed_for(cid, synth.PURPOSE_CHAL, 1), steps * ell, inst.cy["N"], 31)
+    EXI, EXV = dev(exi).view(steps, B, tx), dev(exv).view(steps, B, tx)
+    EYI, EYV = dev(eyi).view(steps, ell, 31), dev(eyv).view(steps, ell, 31)
+    X = dev(synth.field_uniform(synth.seed_for(cid, synth.PURPOSE_X, 1), (steps, B, n)))
+    preps = [mvk.Prepared(inst.key, B, ell) for _ in range(steps)]
+    flags = torch.zeros(steps, dtype=torch.int32, device="cuda")
+    late = torch.zeros((), dtype=torch.int32, device="cuda")
+    Xh = torch.empty((steps, B, n), dtype=torch.int32, device="cuda")
+    Yh = torch.empty((steps, B, m), dtype=torch.int32, device="cuda")
+    Y = torch.empty((steps, B, m), dtype=torch.int32, device="cuda")
+    acc = torch.zeros((steps, B), dtype=torch.int32, device="cuda")
+    side, main = torch.cuda.Stream(), torch.cuda.Stream()
+
+    def prepare(i):
+        mvk.client_prepare(inst.key, EXI[i], EXV[i], EYI[i], EYV[i], out=preps[i])
+        mvk.flag_signal(flags[i], 1)
+
+    def online(i):
+        mvk.flag_wait(flags[i], 1, timeout_us=500_000, timed_out=late)
+        mvk.encode_masked(inst.key, X[i], preps[i], out=Xh[i])
+        mvk.server_eval(inst.dW, Xh[i], out=Yh[i])
+        mvk.decode_verify_masked(inst.key, Xh[i], Yh[i], preps[i], Y=Y[i], accept=acc[i])
+
+    for s, fn in ((side, prepare), (main, online)):  # size the per-stream workspaces outside capture
+        with torch.cuda.stream(s):
+            fn(0)
+    torch.cuda.synchronize()
+    gp, go = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gp, stream=side):
+        for i in range(steps):
+            prepare(i)
+    with torch.cuda.graph(go, stream=main):
+        for i in range(steps):
+            online(i)
+    for rep in range(2):
+        Y.zero_()
+        acc.zero_()
+        torch.cuda.synchronize()
+        with torch.cuda.stream(side):  # the preparation graph is submitted first
+            gp.replay()
+        with torch.cuda.stream(main):
+            go.replay()
+        torch.cuda.synchronize()
+        assert int(late.item()) == 0, rep
+        assert host(acc).tolist() == [[1] * B] * steps
+        for i in range(steps):
+            Xr = mvk.encode(inst.key, X[i], EXI[i], EXV[i])
+            Yr = mvk.server_eval(inst.dW, Xr)
+            Yd, accr, _, _ = mvk.decode_verify(inst.key, Xr, Yr, EXI[i], EXV[i], EYI[i], EYV[i])
+            assert torch.equal(Xh[i], Xr) and torch.equal(Yh[i], Yr) and torch.equal(Y[i], Yd), (rep, i)
+        assert host(flags).tolist() == [0] * steps

@@ -283,8 +283,9 @@ def main():
     elapsed_serial, accepted_serial = elapsed, accepted
 
     # ---- pipelined standard mode -------------------------------------------
-    # Step i's preparation (client_prepare, then a flag) on the preparation
-    # stream; its online part (wait for the flag, encode_masked, server_eval,
+    # Step i's preparation (client_prepare, which sets step i's flag when its
+    # outputs are visible) on the preparation stream; its online part
+    # (encode_masked, which first waits for that flag, then server_eval and
     # decode_verify_masked) on the online stream.  One graph per stream over
     # all timed steps; the two replays run side by side.
     preps = [mvk.Prepared(keys[i % pool], B, ell) for i in range(total_steps)]
@@ -298,13 +299,11 @@ def main():
 
     def prepare(i):
         j = i % pool
-        mvk.client_prepare(keys[j], EXI[i], EXV[i], EYI[i], EYV[i], out=preps[i])
-        mvk.flag_signal(flags[i], 1)
+        mvk.client_prepare(keys[j], EXI[i], EXV[i], EYI[i], EYV[i], out=preps[i], done_flag=flags[i])
 
     def online(i):
         j = i % pool
-        mvk.flag_wait(flags[i], 1, timeout_us=50_000, timed_out=late)
-        mvk.encode_masked(keys[j], X[i], preps[i], out=pXh)
+        mvk.encode_masked(keys[j], X[i], preps[i], out=pXh, ready_flag=flags[i], timeout_us=50_000, timed_out=late)
         mvk.server_eval(Ws[j], pXh, out=pYh, path=args.path)
         mvk.decode_verify_masked(keys[j], pXh, pYh, preps[i], Y=pY, accept=ACC2[i])
 

@@ -230,18 +230,28 @@ mvk_status mvk_decode_verify_prepared(const mvk_key *key, const uint32_t *Xhat,
  * never leave the client, so they may be drawn before the responses exist.
  * One launch when Nx and Ny are at most 16384 (syndromes and row gathers side
  * by side), else the longer syndromes run first in their own launches.
+ * done_flag (device word, may be NULL): set to done_value (!= 0) once every
+ *   output is stored and visible device-wide, as mvk_flag_signal would after
+ *   the call, but without a launch of its own.
  * Errors: MVK_EINVAL, MVK_ERANGE (ell > 16 or B > 65535), MVK_ENOMEM.
  */
 mvk_status mvk_client_prepare(const mvk_key *key, const mvk_sparse *ex, const mvk_sparse *ey,
-                              uint32_t *Mx, uint32_t *My, uint32_t *R, uint32_t *U, void *stream);
+                              uint32_t *Mx, uint32_t *My, uint32_t *R, uint32_t *U,
+                              uint32_t *done_flag, uint32_t done_value, void *stream);
 
 /*
  * Encrypt with a prepared input mask: Xhat = X + Mx (B x n, element-wise mod p).
  * Same result as mvk_encode with the noise vectors Mx was prepared from.
  * X, Mx: device, read; Xhat: device, written (may alias X).
+ * ready_flag (device word, may be NULL): first wait until
+ *   *ready_flag == ready_value, then clear it, as mvk_flag_wait would before
+ *   the call (same time-out rules: timeout_us, timed_out), but without a
+ *   launch of its own.
+ * Errors: MVK_EINVAL (a flag with value 0 or timeout 0).
  */
 mvk_status mvk_encode_masked(const mvk_key *key, const uint32_t *X, uint32_t B, const uint32_t *Mx,
-                             uint32_t *Xhat, void *stream);
+                             uint32_t *Xhat, uint32_t *ready_flag, uint32_t ready_value,
+                             uint32_t timeout_us, uint32_t *timed_out, void *stream);
 
 /*
  * Decrypt + Verify with prepared masks and challenge vectors (from

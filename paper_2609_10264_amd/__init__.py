@@ -243,9 +243,11 @@ class Prepared:
 
 
 def client_prepare(key: Key, ex_idx: torch.Tensor, ex_val: torch.Tensor, ey_idx: torch.Tensor,
-                   ey_val: torch.Tensor, out: Prepared | None = None, stream=None) -> Prepared:
+                   ey_val: torch.Tensor, out: Prepared | None = None, done_flag: torch.Tensor | None = None,
+                   done_value: int = 1, stream=None) -> Prepared:
     """Masks Mx = Gx e_b, My = P e_b (per noise vector) and R = Gy e_q,
-    U = e_q^T Q (per challenge): the query- and response-independent work."""
+    U = e_q^T Q (per challenge): the query- and response-independent work.
+    done_flag: device word set to done_value once every output is visible."""
     B, ell = ex_idx.shape[0], ey_idx.shape[0]
     if out is None:
         out = Prepared(key, B, ell, device=ex_idx.device)
@@ -258,13 +260,16 @@ def client_prepare(key: Key, ex_idx: torch.Tensor, ex_val: torch.Tensor, ey_idx:
         ctypes.byref(ks), ctypes.byref(ex), ctypes.byref(ey),
         _dev(out.Mx, torch.int32, (B, key.n), "Mx"), _dev(out.My, torch.int32, (B, key.m), "My"),
         _dev(out.R, torch.int32, (ell, key.m), "R"), _dev(out.U, torch.int32, (ell, key.n), "U"),
+        _dev(done_flag, torch.int32, (), "done_flag") if done_flag is not None else None, done_value,
         _stream(stream)))
     return out
 
 
 def encode_masked(key: Key, X: torch.Tensor, prep: Prepared, out: torch.Tensor | None = None,
-                  stream=None) -> torch.Tensor:
-    """Encrypt with a prepared mask: Xhat = X + Mx."""
+                  ready_flag: torch.Tensor | None = None, ready_value: int = 1, timeout_us: int = 200000,
+                  timed_out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Encrypt with a prepared mask: Xhat = X + Mx; with ready_flag, first wait
+    for it to hold ready_value (see flag_wait)."""
     B = X.shape[0]
     if out is None:
         out = torch.empty_like(X)
@@ -272,6 +277,8 @@ def encode_masked(key: Key, X: torch.Tensor, prep: Prepared, out: torch.Tensor |
     _lib.check("mvk_encode_masked", _lib.load().mvk_encode_masked(
         ctypes.byref(ks), _dev(X, torch.int32, (B, key.n), "X"), B,
         _dev(prep.Mx, torch.int32, (B, key.n), "Mx"), _dev(out, torch.int32, (B, key.n), "Xhat"),
+        _dev(ready_flag, torch.int32, (), "ready_flag") if ready_flag is not None else None, ready_value,
+        timeout_us, _dev(timed_out, torch.int32, (), "timed_out") if timed_out is not None else None,
         _stream(stream)))
     return out
 

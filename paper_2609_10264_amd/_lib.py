@@ -122,9 +122,9 @@ def load() -> ctypes.CDLL:
                                              ctypes.POINTER(MvkSparse), vp, vp, vp, vp, vp, vp]
     L.mvk_decode_verify_prepared.restype = st
     L.mvk_client_prepare.argtypes = [ctypes.POINTER(MvkKey), ctypes.POINTER(MvkSparse), ctypes.POINTER(MvkSparse),
-                                     vp, vp, vp, vp, vp]
+                                     vp, vp, vp, vp, vp, u32, vp]
     L.mvk_client_prepare.restype = st
-    L.mvk_encode_masked.argtypes = [ctypes.POINTER(MvkKey), vp, u32, vp, vp, vp]
+    L.mvk_encode_masked.argtypes = [ctypes.POINTER(MvkKey), vp, u32, vp, vp, vp, u32, u32, vp, vp]
     L.mvk_encode_masked.restype = st
     L.mvk_decode_verify_masked.argtypes = [ctypes.POINTER(MvkKey), vp, vp, u32, vp, u32, vp, vp, vp, vp, vp, vp, vp]
     L.mvk_decode_verify_masked.restype = st

@@ -287,10 +287,15 @@ mvk_status mvk_decode_verify(const mvk_key* key, const uint32_t* Xhat, const uin
     return hip_status(e);
 }
 
+// Control word of the workgroup counters of client_prepare and encode_masked.
+constexpr int kPrepCounterWord = 4;
+
 mvk_status mvk_client_prepare(const mvk_key* key, const mvk_sparse* ex, const mvk_sparse* ey, uint32_t* Mx,
-                              uint32_t* My, uint32_t* R, uint32_t* U, void* stream) {
+                              uint32_t* My, uint32_t* R, uint32_t* U, uint32_t* done_flag, uint32_t done_value,
+                              void* stream) {
     mvk_status st = check_key(key);
     if (st) return st;
+    if (done_flag && done_value == 0) return MVK_EINVAL;
     const uint32_t nx = ex ? ex->count : 0u;
     if (nx) {
         if (!Mx || !My || !key->PT || (ex->t && (!ex->idx || !ex->val))) return MVK_EINVAL;
@@ -303,27 +308,39 @@ mvk_status mvk_client_prepare(const mvk_key* key, const mvk_sparse* ex, const mv
         if (st) return st;
         if (!R || !U || !key->Q) return MVK_EINVAL;
     }
-    if (nx == 0 && ny == 0) return MVK_OK;
     hipStream_t s = (hipStream_t)stream;
+    if (nx == 0 && ny == 0) return done_flag ? hip_status(launch_flag_signal(done_flag, done_value, s)) : MVK_OK;
     const size_t Nx = (size_t)key->cx.r * key->n, Ny = (size_t)key->cy.r * key->m;
     size_t scratch = 0;
     if (nx && Nx > kSynScratchAbove) scratch = (size_t)nx * 2 * Nx * 4;
     if (ny && Ny > kSynScratchAbove && (size_t)ny * 2 * Ny * 4 > scratch) scratch = (size_t)ny * 2 * Ny * 4;
     void* ws = nullptr;
-    st = workspace(s, scratch, &ws);
+    uint32_t* ctrl = nullptr;
+    st = workspace(s, scratch, &ws, &ctrl);
     if (st) return st;
     return hip_status(launch_client_prepare(*key, nx ? ex->idx : nullptr, nx ? ex->val : nullptr, nx ? ex->t : 0u,
                                             nx, ny ? ey->idx : nullptr, ny ? ey->val : nullptr, ny ? ey->t : 0u, ny,
-                                            Mx, My, R, U, (uint32_t*)ws, s));
+                                            Mx, My, R, U, (uint32_t*)ws, &ctrl[kPrepCounterWord], done_flag,
+                                            done_value, s));
 }
 
 mvk_status mvk_encode_masked(const mvk_key* key, const uint32_t* X, uint32_t B, const uint32_t* Mx, uint32_t* Xhat,
+                             uint32_t* ready_flag, uint32_t ready_value, uint32_t timeout_us, uint32_t* timed_out,
                              void* stream) {
     mvk_status st = check_key(key);
     if (st) return st;
-    if (B == 0) return MVK_OK;
-    if (!X || !Mx || !Xhat) return MVK_EINVAL;
-    return hip_status(launch_add_masks(X, Mx, (size_t)B * key->n, Xhat, (hipStream_t)stream));
+    if (ready_flag && (ready_value == 0 || timeout_us == 0)) return MVK_EINVAL;
+    if (B == 0 && !ready_flag) return MVK_OK;
+    if (B && (!X || !Mx || !Xhat)) return MVK_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    uint32_t* ctrl = nullptr;
+    if (ready_flag) {
+        void* ws = nullptr;
+        st = workspace(s, 0, &ws, &ctrl);
+        if (st) return st;
+    }
+    return hip_status(launch_add_masks(X, Mx, (size_t)B * key->n, Xhat, ready_flag, ready_value, timeout_us,
+                                       timed_out, ctrl ? &ctrl[kPrepCounterWord] : nullptr, s));
 }
 
 mvk_status mvk_decode_verify_masked(const mvk_key* key, const uint32_t* Xhat, const uint32_t* Yhat, uint32_t B,

@@ -61,6 +61,11 @@ constexpr int kItems = kMaxEll;  // verify work items (repetition, chunk) per wo
 // Workgroup of decode_verify_syn: 512 threads, so that one workgroup holds the
 // syndrome of a block of up to 512 * 32 = 16384 positions in LDS.
 constexpr int kFusedThreads = kDvSynThreads;
+
+// decode_verify_masked runs in one workgroup up to this many words of
+// responses plus queries (B * (m + n)) and up to 4 repetitions, else on the
+// multi-workgroup kernel above.
+constexpr uint64_t kSmallDvWords = 32768;
 constexpr int kFusedGroups = kFusedThreads / kCols;
 
 // Spin limit of the wait for the challenge syndromes (s_sleep 2 per try, well
@@ -377,6 +382,90 @@ __global__ __launch_bounds__(kFusedThreads) void decode_verify_syn(
     finish(B, ell, accL, accR, counter, rdone, err, vL, vR, accept, &last);
 }
 
+// decode_verify_masked for small problems, by one workgroup: no atomics and
+// no cross-workgroup counter.  Thread t takes the outputs i = t + 1024 u of
+// every column (Y_b[i] = Yhat_b[i] - My_b[i] and the v_R terms
+// R_q[i] Yhat_b[i]) and the inputs k = t + 1024 u (the v_L terms
+// U_q[k] Xhat_b[k]), kSmallPer of each per pass with all of a pass's loads
+// issued before the first is used (addresses clamped in range, terms masked);
+// the 2 * ell partial sums of a column are reduced across the waves in LDS.
+// ell <= EL.
+constexpr int kSmallThreads = 1024;
+constexpr int kSmallPer = 4;
+template <int EL>
+__global__ __launch_bounds__(kSmallThreads) void decode_verify_small(
+    uint32_t m, uint32_t n, const uint32_t* __restrict__ Xhat, const uint32_t* __restrict__ Yhat, uint32_t B,
+    const uint32_t* __restrict__ My, uint32_t ell, const uint32_t* __restrict__ R, const uint32_t* __restrict__ U,
+    uint32_t* __restrict__ Y, uint32_t* __restrict__ vL, uint32_t* __restrict__ vR, uint32_t* __restrict__ accept) {
+    constexpr int NW = kSmallThreads / 64;
+    constexpr uint32_t kPass = (uint32_t)kSmallThreads * kSmallPer;
+    __shared__ uint64_t red[NW][2 * EL];
+    __shared__ uint32_t fin[2 * EL];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const uint32_t len = m > n ? m : n;
+    for (uint32_t b = 0; b < B; ++b) {
+        uint64_t l[EL], rr[EL];
+#pragma unroll
+        for (int q = 0; q < EL; ++q) l[q] = rr[q] = 0;
+        for (uint32_t base = 0; base < len; base += kPass) {
+            uint32_t yv[kSmallPer], mv[kSmallPer], xv[kSmallPer], rv[EL][kSmallPer], uv[EL][kSmallPer];
+#pragma unroll
+            for (int u = 0; u < kSmallPer; ++u) {
+                const uint32_t j = base + (uint32_t)tid + (uint32_t)kSmallThreads * u;
+                const uint32_t i = j < m ? j : m - 1, k = j < n ? j : n - 1;
+                yv[u] = Yhat[(size_t)b * m + i];
+                mv[u] = My[(size_t)b * m + i];
+                xv[u] = Xhat[(size_t)b * n + k];
+#pragma unroll
+                for (int q = 0; q < EL; ++q) {
+                    const uint32_t qs = (uint32_t)q < ell ? (uint32_t)q : 0u;
+                    rv[q][u] = R[(size_t)qs * m + i];
+                    uv[q][u] = U[(size_t)qs * n + k];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kSmallPer; ++u) {
+                const uint32_t j = base + (uint32_t)tid + (uint32_t)kSmallThreads * u;
+                const uint32_t y = j < m ? yv[u] : 0u, x = j < n ? xv[u] : 0u;
+                if (j < m) Y[(size_t)b * m + j] = fsub(y, mv[u]);
+#pragma unroll
+                for (int q = 0; q < EL; ++q) {
+                    rr[q] += ffold((uint64_t)rv[q][u] * y);
+                    l[q] += ffold((uint64_t)uv[q][u] * x);
+                }
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < EL; ++q) {
+            if ((uint32_t)q < ell) {
+                const uint64_t sl = wave_sum_u64(l[q]), sr = wave_sum_u64(rr[q]);
+                if (lane == 0) {
+                    red[wave][2 * q] = sl;
+                    red[wave][2 * q + 1] = sr;
+                }
+            }
+        }
+        __syncthreads();
+        if ((uint32_t)tid < 2 * ell) {
+            uint64_t tot = 0;
+#pragma unroll
+            for (int w = 0; w < NW; ++w) tot += red[w][tid];
+            fin[tid] = fred64(tot);
+        }
+        __syncthreads();
+        if ((uint32_t)tid < ell) {
+            if (vL) vL[(size_t)tid * B + b] = fin[2 * tid];
+            if (vR) vR[(size_t)tid * B + b] = fin[2 * tid + 1];
+        }
+        if (tid == 0) {
+            uint32_t ok = 1;
+            for (uint32_t q = 0; q < ell; ++q) ok &= fin[2 * q] == fin[2 * q + 1] ? 1u : 0u;
+            accept[b] = ok;
+        }
+        __syncthreads();  // red and fin are reused by the next column
+    }
+}
+
 template <int U>
 int fused_blocks_per_cu() {
     int nb = 0;
@@ -456,6 +545,15 @@ hipError_t launch_decode_verify_masked(uint32_t m, uint32_t n, const uint32_t* X
                                        const uint32_t* U, uint32_t* Y, unsigned long long* acc, uint32_t* counter,
                                        uint32_t* vL, uint32_t* vR, uint32_t* accept, hipStream_t s) {
     if (ell == 0 || ell > (uint32_t)kMaxEll) return hipErrorInvalidValue;
+    if ((uint64_t)B * ((uint64_t)m + n) <= kSmallDvWords && ell <= 4) {
+        if (ell <= 2)
+            hipLaunchKernelGGL(decode_verify_small<2>, dim3(1), dim3(kSmallThreads), 0, s, m, n, Xhat, Yhat, B, My,
+                               ell, r, U, Y, vL, vR, accept);
+        else
+            hipLaunchKernelGGL(decode_verify_small<4>, dim3(1), dim3(kSmallThreads), 0, s, m, n, Xhat, Yhat, B, My,
+                               ell, r, U, Y, vL, vR, accept);
+        return hipGetLastError();
+    }
     const uint32_t nblkL = ceil_div(n, kCols), nblkR = ceil_div(m, kCols);
     const uint32_t grid = B * nblkR + nblkL;
     hipLaunchKernelGGL(decode_verify_fused<true>, dim3(grid), dim3(kB), 0, s, nullptr, nullptr, m, n, 0u, 0u, Xhat,

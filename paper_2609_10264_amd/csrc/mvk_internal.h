@@ -91,12 +91,19 @@ hipError_t launch_decode_verify_masked(uint32_t m, uint32_t n, const uint32_t* X
 // prepare.hip ---------------------------------------------------------------
 // Mx, My for nx noise vectors and R, U for ny challenges (either count may
 // be 0).  scratch: max(nx * 2 * Nx, ny * 2 * Ny) words when that block length
-// is above kSynScratchAbove, else unused.
+// is above kSynScratchAbove, else unused.  done (may be null): set to
+// done_value once every output is stored and visible device-wide; counter:
+// a word that is zero before the launch (left zero).
 hipError_t launch_client_prepare(const mvk_key& key, const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx,
                                  uint32_t nx, const uint32_t* ey_idx, const uint32_t* ey_val, uint32_t ty,
                                  uint32_t ny, uint32_t* Mx, uint32_t* My, uint32_t* R, uint32_t* Uq,
-                                 uint32_t* scratch, hipStream_t s);
-hipError_t launch_add_masks(const uint32_t* X, const uint32_t* Mx, size_t count, uint32_t* Xhat, hipStream_t s);
+                                 uint32_t* scratch, uint32_t* counter, uint32_t* done, uint32_t done_value,
+                                 hipStream_t s);
+// Xhat = X + Mx; with a flag, after waiting for *flag == value (which the
+// launch then clears; counter as above).
+hipError_t launch_add_masks(const uint32_t* X, const uint32_t* Mx, size_t count, uint32_t* Xhat, uint32_t* flag,
+                            uint32_t value, uint32_t timeout_us, uint32_t* timed_out, uint32_t* counter,
+                            hipStream_t s);
 hipError_t launch_flag_signal(uint32_t* flag, uint32_t value, hipStream_t s);
 hipError_t launch_flag_wait(uint32_t* flag, uint32_t value, uint32_t timeout_us, uint32_t* timed_out,
                             hipStream_t s);

@@ -29,7 +29,9 @@ constexpr int kQBatch = 16;            // gathers in flight per thread
 // One gather item by a 256-thread quarter of the workgroup:
 // out[i] = sum_s val[s] * M[idx[s], i] for the 64 columns i in [col0, col0+64).
 // Every quarter of the workgroup passes the one barrier here; a quarter with
-// no item (live = false) issues no loads and writes nothing.
+// no item (live = false) issues no loads and writes nothing.  COHERENT: the
+// results are stored device-coherently.
+template <bool COHERENT>
 __device__ __forceinline__ void gather_item(const uint32_t* __restrict__ M, uint32_t ld, uint32_t nrows,
                                             const uint32_t* __restrict__ idx, const uint32_t* __restrict__ val,
                                             uint32_t t, uint32_t* __restrict__ out, uint32_t col0, bool live,
@@ -66,7 +68,10 @@ __device__ __forceinline__ void gather_item(const uint32_t* __restrict__ M, uint
         uint64_t tot = 0;
 #pragma unroll
         for (int h = 0; h < kQGroups; ++h) tot += part[h][lane];
-        out[i] = fred64(tot);
+        if (COHERENT)
+            __hip_atomic_store(&out[i], fred64(tot), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        else
+            out[i] = fred64(tot);
     }
 }
 
@@ -95,52 +100,120 @@ struct PrepArgs {
     uint32_t* My;
     uint32_t* R;
     uint32_t* Uq;
+    uint32_t* counter;  // SIG: workgroups done (zero before and after the launch)
+    uint32_t* done;     // SIG: set to done_value once every output is stored
+    uint32_t done_value;
 };
 
 // Workgroups [0, nsx) and [nsx, nsx + nsy): one syndrome each (U > 0; the
 // whole block in LDS); the rest: kQuarters gather items each, first the
 // nx * ceil(m/64) items of My (rows of PT), then the ny * ceil(n/64) items of
 // U (rows of Q).
-template <int U>
+// SIG: every output is stored device-coherently; each workgroup waits for its
+// stores to complete (vmcnt 0) before the barrier and then counts itself done;
+// the last one resets the counter and sets the done flag, so a kernel of
+// another stream that sees the flag sees every output.
+template <int U, bool SIG>
 __global__ __launch_bounds__(kPrepThreads) void client_prepare_kernel(PrepArgs a) {
     __shared__ __align__(16) uint32_t lds[prep_lds_words<U>()];
     uint32_t bid = blockIdx.x;
+    bool gather = true;
     if constexpr (U > 0) {
         if (bid < a.nsx) {
-            syn::syn_block<true, U, kPrepThreads, false>(bid, a.n, a.rx, a.xpi1, a.xpi2, a.xv1, a.xv2, nullptr,
-                                                         a.ex_idx, a.ex_val, a.tx, nullptr, a.Mx, lds);
-            return;
+            syn::syn_block<true, U, kPrepThreads, SIG>(bid, a.n, a.rx, a.xpi1, a.xpi2, a.xv1, a.xv2, nullptr,
+                                                       a.ex_idx, a.ex_val, a.tx, nullptr, a.Mx, lds);
+            gather = false;
+        } else if (bid < a.nsx + a.nsy) {
+            syn::syn_block<true, U, kPrepThreads, SIG>(bid - a.nsx, a.m, a.ry, a.ypi1, a.ypi2, a.yv1, a.yv2,
+                                                       nullptr, a.ey_idx, a.ey_val, a.ty, nullptr, a.R, lds);
+            gather = false;
+        } else {
+            bid -= a.nsx + a.nsy;
         }
-        if (bid < a.nsx + a.nsy) {
-            syn::syn_block<true, U, kPrepThreads, false>(bid - a.nsx, a.m, a.ry, a.ypi1, a.ypi2, a.yv1, a.yv2,
-                                                         nullptr, a.ey_idx, a.ey_val, a.ty, nullptr, a.R, lds);
-            return;
-        }
-        bid -= a.nsx + a.nsy;
     }
-    const int quarter = threadIdx.x / kQuarter;
-    auto part = reinterpret_cast<uint64_t (*)[kQCols]>(lds) + quarter * kQGroups;
-    const uint32_t item = bid * kQuarters + (uint32_t)quarter;
-    const uint32_t nbm = a.nbm, nbn = a.nbn;
-    const uint32_t ix = a.nx * nbm, iy = a.ny * nbn;
-    if (item < ix) {
-        const uint32_t b = item / nbm, cb = item % nbm;
-        gather_item(a.PT, a.m, a.rx * a.n, a.ex_idx + (size_t)b * a.tx, a.ex_val + (size_t)b * a.tx, a.tx,
-                    a.My + (size_t)b * a.m, cb * kQCols, true, part);
-    } else if (item < ix + iy) {
-        const uint32_t q = (item - ix) / nbn, cb = (item - ix) % nbn;
-        gather_item(a.Q, a.n, a.ry * a.m, a.ey_idx + (size_t)q * a.ty, a.ey_val + (size_t)q * a.ty, a.ty,
-                    a.Uq + (size_t)q * a.n, cb * kQCols, true, part);
-    } else {
-        gather_item(nullptr, 0u, 1u, nullptr, nullptr, 0u, nullptr, 0u, false, part);
+    if (gather) {
+        const int quarter = threadIdx.x / kQuarter;
+        auto part = reinterpret_cast<uint64_t (*)[kQCols]>(lds) + quarter * kQGroups;
+        const uint32_t item = bid * kQuarters + (uint32_t)quarter;
+        const uint32_t nbm = a.nbm, nbn = a.nbn;
+        const uint32_t ix = a.nx * nbm, iy = a.ny * nbn;
+        if (item < ix) {
+            const uint32_t b = item / nbm, cb = item % nbm;
+            gather_item<SIG>(a.PT, a.m, a.rx * a.n, a.ex_idx + (size_t)b * a.tx, a.ex_val + (size_t)b * a.tx, a.tx,
+                             a.My + (size_t)b * a.m, cb * kQCols, true, part);
+        } else if (item < ix + iy) {
+            const uint32_t q = (item - ix) / nbn, cb = (item - ix) % nbn;
+            gather_item<SIG>(a.Q, a.n, a.ry * a.m, a.ey_idx + (size_t)q * a.ty, a.ey_val + (size_t)q * a.ty, a.ty,
+                             a.Uq + (size_t)q * a.n, cb * kQCols, true, part);
+        } else {
+            gather_item<SIG>(nullptr, 0u, 1u, nullptr, nullptr, 0u, nullptr, 0u, false, part);
+        }
+    }
+    if constexpr (SIG) {
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (threadIdx.x == 0 && atomicAdd(a.counter, 1u) == gridDim.x - 1) {
+            atomicExch(a.counter, 0u);
+            __hip_atomic_store(a.done, a.done_value, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
     }
 }
 
-// Xhat = X + Mx, element-wise over count words.
-__global__ __launch_bounds__(256) void add_masks(const uint32_t* X, const uint32_t* __restrict__ Mx,
-                                                 size_t count, uint32_t* Xhat) {
-    for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < count; i += (size_t)gridDim.x * 256)
-        Xhat[i] = fadd(X[i], Mx[i]);
+// Polls *flag (device-coherent loads, a short sleep between polls) from the
+// calling thread until it holds `value`; false after `ticks` of the constant
+// wall clock.
+__device__ __forceinline__ bool poll_flag(const uint32_t* flag, uint32_t value, uint64_t ticks) {
+    const uint64_t t0 = wall_clock64();
+    while (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != value) {
+        if (wall_clock64() - t0 > ticks) return false;
+        __builtin_amdgcn_s_sleep(4);
+    }
+    return true;
+}
+
+// Xhat = X + Mx, element-wise over count words, kAddPer words per thread and
+// pass with the pass's loads issued first.  WAIT: first every workgroup waits
+// for *flag == value (thread 0 polls), then reads Mx device-coherently; the
+// flag is cleared by the only workgroup, or, with several, by the last one to
+// finish (counted on `counter`, which it also clears).
+constexpr int kAddThreads = 1024;
+constexpr int kAddPer = 4;
+template <bool WAIT>
+__global__ __launch_bounds__(kAddThreads) void add_masks(const uint32_t* X, const uint32_t* __restrict__ Mx,
+                                                         size_t count, uint32_t* Xhat, uint32_t* flag, uint32_t value,
+                                                         uint64_t ticks, uint32_t* timed_out, uint32_t* counter) {
+    if constexpr (WAIT) {
+        if (threadIdx.x == 0) {
+            if (!poll_flag(flag, value, ticks)) {
+                if (timed_out) atomicOr(timed_out, 1u);
+            } else if (gridDim.x == 1) {
+                __hip_atomic_store(flag, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        __syncthreads();
+    }
+    constexpr size_t kPass = (size_t)kAddThreads * kAddPer;
+    for (size_t base = (size_t)blockIdx.x * kPass; base < count; base += (size_t)gridDim.x * kPass) {
+        uint32_t xv[kAddPer], mv[kAddPer];
+#pragma unroll
+        for (int u = 0; u < kAddPer; ++u) {
+            const size_t i = base + threadIdx.x + (size_t)kAddThreads * u;
+            const size_t is = i < count ? i : count - 1;
+            xv[u] = X[is];
+            mv[u] = WAIT ? __hip_atomic_load(&Mx[is], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : Mx[is];
+        }
+#pragma unroll
+        for (int u = 0; u < kAddPer; ++u) {
+            const size_t i = base + threadIdx.x + (size_t)kAddThreads * u;
+            if (i < count) Xhat[i] = fadd(xv[u], mv[u]);
+        }
+    }
+    if constexpr (WAIT) {
+        if (gridDim.x > 1 && threadIdx.x == 0 && atomicAdd(counter, 1u) == gridDim.x - 1) {
+            atomicExch(counter, 0u);
+            __hip_atomic_store(flag, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
 }
 
 __global__ void flag_signal_kernel(uint32_t* flag, uint32_t value) {
@@ -152,15 +225,22 @@ __global__ void flag_signal_kernel(uint32_t* flag, uint32_t value) {
 // wall clock it gives up, leaves the flag and sets *timed_out.
 __global__ void flag_wait_kernel(uint32_t* flag, uint32_t value, uint64_t ticks, uint32_t* timed_out) {
     if (threadIdx.x != 0) return;
-    const uint64_t t0 = wall_clock64();
-    while (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != value) {
-        if (wall_clock64() - t0 > ticks) {
-            if (timed_out) atomicOr(timed_out, 1u);
-            return;
-        }
-        __builtin_amdgcn_s_sleep(4);
+    if (!poll_flag(flag, value, ticks)) {
+        if (timed_out) atomicOr(timed_out, 1u);
+        return;
     }
     __hip_atomic_store(flag, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Wall-clock ticks of timeout_us on the current device.
+hipError_t wait_ticks(uint32_t timeout_us, uint64_t* ticks) {
+    int dev = 0, khz = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev);
+    if (e != hipSuccess) return e;
+    if (khz <= 0) return hipErrorInvalidValue;
+    *ticks = (uint64_t)timeout_us * (uint64_t)khz / 1000u;
+    return hipSuccess;
 }
 
 // Syndrome tile per thread of a 1024-thread workgroup for block length N
@@ -176,7 +256,8 @@ uint32_t prep_u(uint64_t N) {
 hipError_t launch_client_prepare(const mvk_key& key, const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx,
                                  uint32_t nx, const uint32_t* ey_idx, const uint32_t* ey_val, uint32_t ty,
                                  uint32_t ny, uint32_t* Mx, uint32_t* My, uint32_t* R, uint32_t* Uq,
-                                 uint32_t* scratch, hipStream_t s) {
+                                 uint32_t* scratch, uint32_t* counter, uint32_t* done, uint32_t done_value,
+                                 hipStream_t s) {
     const uint64_t Nx = (uint64_t)key.cx.r * key.n, Ny = (uint64_t)key.cy.r * key.m;
     const uint32_t ux = nx ? prep_u(Nx) : 0u, uy = ny ? prep_u(Ny) : 0u;
     // syndromes too long for one workgroup run in their own (segmented) launches first
@@ -202,27 +283,44 @@ hipError_t launch_client_prepare(const mvk_key& key, const uint32_t* ex_idx, con
     a.nbm = ceil_div(key.m, kQCols), a.nbn = ceil_div(key.n, kQCols);
     a.PT = key.PT, a.Q = key.Q;
     a.Mx = Mx, a.My = My, a.R = R, a.Uq = Uq;
+    a.counter = counter, a.done = done, a.done_value = done_value;
     const uint64_t items = (uint64_t)nx * ceil_div(key.m, kQCols) + (uint64_t)ny * ceil_div(key.n, kQCols);
     const uint32_t U = ux > uy ? ux : uy;
     const uint64_t grid = (U ? a.nsx + a.nsy : 0u) + (items + kQuarters - 1) / kQuarters;
     if (grid == 0) return hipSuccess;
     if (grid > 0x7fffffffu) return hipErrorInvalidValue;
 #define MVK_PREP(UU)                                                                                        \
-    hipLaunchKernelGGL(client_prepare_kernel<UU>, dim3((uint32_t)grid), dim3(kPrepThreads), 0, s, a)
-    if (U == 0) MVK_PREP(0);
-    else if (U == 4) MVK_PREP(4);
-    else if (U == 8) MVK_PREP(8);
-    else if (U == 12) MVK_PREP(12);
-    else MVK_PREP(16);
+    if (done)                                                                                               \
+        hipLaunchKernelGGL((client_prepare_kernel<UU, true>), dim3((uint32_t)grid), dim3(kPrepThreads), 0, s, a); \
+    else                                                                                                    \
+        hipLaunchKernelGGL((client_prepare_kernel<UU, false>), dim3((uint32_t)grid), dim3(kPrepThreads), 0, s, a)
+    if (U == 0) { MVK_PREP(0); }
+    else if (U == 4) { MVK_PREP(4); }
+    else if (U == 8) { MVK_PREP(8); }
+    else if (U == 12) { MVK_PREP(12); }
+    else { MVK_PREP(16); }
 #undef MVK_PREP
     return hipGetLastError();
 }
 
-hipError_t launch_add_masks(const uint32_t* X, const uint32_t* Mx, size_t count, uint32_t* Xhat, hipStream_t s) {
-    if (count == 0) return hipSuccess;
-    size_t blocks = (count + 255) / 256;
-    if (blocks > 4096) blocks = 4096;
-    hipLaunchKernelGGL(add_masks, dim3((uint32_t)blocks), dim3(256), 0, s, X, Mx, count, Xhat);
+hipError_t launch_add_masks(const uint32_t* X, const uint32_t* Mx, size_t count, uint32_t* Xhat, uint32_t* flag,
+                            uint32_t value, uint32_t timeout_us, uint32_t* timed_out, uint32_t* counter,
+                            hipStream_t s) {
+    if (count == 0 && !flag) return hipSuccess;
+    const size_t pass = (size_t)kAddThreads * kAddPer;
+    size_t blocks = (count + pass - 1) / pass;
+    if (blocks > 256) blocks = 256;
+    if (blocks == 0) blocks = 1;
+    if (flag) {
+        uint64_t ticks = 0;
+        const hipError_t e = wait_ticks(timeout_us, &ticks);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(add_masks<true>, dim3((uint32_t)blocks), dim3(kAddThreads), 0, s, X, Mx, count, Xhat,
+                           flag, value, ticks, timed_out, counter);
+    } else {
+        hipLaunchKernelGGL(add_masks<false>, dim3((uint32_t)blocks), dim3(kAddThreads), 0, s, X, Mx, count, Xhat,
+                           nullptr, 0u, (uint64_t)0, nullptr, nullptr);
+    }
     return hipGetLastError();
 }
 
@@ -233,12 +331,9 @@ hipError_t launch_flag_signal(uint32_t* flag, uint32_t value, hipStream_t s) {
 
 hipError_t launch_flag_wait(uint32_t* flag, uint32_t value, uint32_t timeout_us, uint32_t* timed_out,
                             hipStream_t s) {
-    int dev = 0, khz = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e == hipSuccess) e = hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev);
+    uint64_t ticks = 0;
+    const hipError_t e = wait_ticks(timeout_us, &ticks);
     if (e != hipSuccess) return e;
-    if (khz <= 0) return hipErrorInvalidValue;
-    const uint64_t ticks = (uint64_t)timeout_us * (uint64_t)khz / 1000u;
     hipLaunchKernelGGL(flag_wait_kernel, dim3(1), dim3(64), 0, s, flag, value, ticks, timed_out);
     return hipGetLastError();
 }

@@ -127,9 +127,14 @@ def test_prepared_path_argument_checks_without_device_work():
     key = L.MvkKey(8, 8, code, code, 0x1000, 0x1000)
     ex = L.MvkSparse(0x1000, 0x1000, 2, 1)
     ey = L.MvkSparse(0x1000, 0x1000, 2, 2)
-    prep = lib.mvk_client_prepare
+    def prep(*a):
+        return lib.mvk_client_prepare(*a[:7], None, 0, a[7])
+
     # nothing to prepare
     assert prep(ctypes.byref(key), None, None, None, None, None, None, None) == L.MVK_OK
+    # a done flag needs a nonzero value
+    assert lib.mvk_client_prepare(ctypes.byref(key), None, None, None, None, None, None, fake, 0,
+                                  None) == L.MVK_EINVAL
     # masks requested without their outputs
     assert prep(ctypes.byref(key), ctypes.byref(ex), None, None, fake, None, None, None) == L.MVK_EINVAL
     assert prep(ctypes.byref(key), ctypes.byref(ex), None, fake, None, None, None, None) == L.MVK_EINVAL
@@ -144,8 +149,11 @@ def test_prepared_path_argument_checks_without_device_work():
     assert prep(ctypes.byref(key), None, ctypes.byref(ey), None, None, fake, None, None) == L.MVK_EINVAL
     assert prep(ctypes.byref(key), None, ctypes.byref(ey), None, None, None, fake, None) == L.MVK_EINVAL
     # encode with a prepared mask
-    assert lib.mvk_encode_masked(ctypes.byref(key), fake, 0, None, None, None) == L.MVK_OK
-    assert lib.mvk_encode_masked(ctypes.byref(key), fake, 1, None, fake, None) == L.MVK_EINVAL
+    enc = lib.mvk_encode_masked
+    assert enc(ctypes.byref(key), fake, 0, None, None, None, 0, 0, None, None) == L.MVK_OK
+    assert enc(ctypes.byref(key), fake, 1, None, fake, None, 0, 0, None, None) == L.MVK_EINVAL
+    assert enc(ctypes.byref(key), fake, 1, fake, fake, fake, 0, 10, None, None) == L.MVK_EINVAL  # value 0
+    assert enc(ctypes.byref(key), fake, 1, fake, fake, fake, 1, 0, None, None) == L.MVK_EINVAL  # no time-out
     # decode/verify with prepared masks: 1 <= ell <= 16, every input present
     dvm = lib.mvk_decode_verify_masked
     assert dvm(ctypes.byref(key), fake, fake, 1, fake, 0, fake, fake, fake, None, None, fake, None) == L.MVK_EINVAL

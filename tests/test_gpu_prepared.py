@@ -64,7 +64,12 @@ def test_client_prepare_matches_oracle(cid, m, n, B, rx, ry, tx, ell):
     assert np.array_equal(host(prep.U), oracle.server_eval(np.ascontiguousarray(inst.W.T), R))
 
 
-@pytest.mark.parametrize("cid,m,n,B,rx,ry,tx,ell", PREP[:2] + PREP[3:4])
+# one-workgroup decode/verify (B * (m + n) <= 32768 and ell <= 4: ell 2 and
+# 3) and the multi-workgroup kernel (8 * 5000 words; ell = 7)
+MASKED = PREP[:2] + PREP[3:4] + [(86, 3000, 2000, 8, 2, 2, 16, 3), (87, 500, 400, 2, 2, 2, 9, 7)]
+
+
+@pytest.mark.parametrize("cid,m,n,B,rx,ry,tx,ell", MASKED)
 def test_masked_path_matches_one_call_path(cid, m, n, B, rx, ry, tx, ell):
     _say(f"masked path cid={cid} m={m} n={n} B={B}")
     inst = Instance(cid, m, n, B, rx, tx, ty=31, ell=ell, ry=ry).to_device()
@@ -136,13 +141,20 @@ def test_pipelined_graphs_match_one_call_path():
     acc = torch.zeros((steps, B), dtype=torch.int32, device="cuda")
     side, main = torch.cuda.Stream(), torch.cuda.Stream()
 
-    def prepare(i):
-        mvk.client_prepare(inst.key, EXI[i], EXV[i], EYI[i], EYV[i], out=preps[i])
-        mvk.flag_signal(flags[i], 1)
+    def prepare(i):  # odd steps: the flag kernels; even steps: the flags fused into the calls
+        if i % 2:
+            mvk.client_prepare(inst.key, EXI[i], EXV[i], EYI[i], EYV[i], out=preps[i])
+            mvk.flag_signal(flags[i], 1)
+        else:
+            mvk.client_prepare(inst.key, EXI[i], EXV[i], EYI[i], EYV[i], out=preps[i], done_flag=flags[i])
 
     def online(i):
-        mvk.flag_wait(flags[i], 1, timeout_us=500_000, timed_out=late)
-        mvk.encode_masked(inst.key, X[i], preps[i], out=Xh[i])
+        if i % 2:
+            mvk.flag_wait(flags[i], 1, timeout_us=500_000, timed_out=late)
+            mvk.encode_masked(inst.key, X[i], preps[i], out=Xh[i])
+        else:
+            mvk.encode_masked(inst.key, X[i], preps[i], out=Xh[i], ready_flag=flags[i], timeout_us=500_000,
+                              timed_out=late)
         mvk.server_eval(inst.dW, Xh[i], out=Yh[i])
         mvk.decode_verify_masked(inst.key, Xh[i], Yh[i], preps[i], Y=Y[i], accept=acc[i])
 

@@ -426,8 +426,13 @@ __global__ __launch_bounds__(kSmallThreads) void decode_verify_small(
 #pragma unroll
             for (int u = 0; u < kSmallPer; ++u) {
                 const uint32_t j = base + (uint32_t)tid + (uint32_t)kSmallThreads * u;
+                // the value is pinned in a register before the guarded store, so
+                // that the compiler does not sink the loads into the branch (where
+                // each would wait on its own)
+                uint32_t yo = fsub(yv[u], mv[u]);
+                asm volatile("" : "+v"(yo));
+                if (j < m) Y[(size_t)b * m + j] = yo;
                 const uint32_t y = j < m ? yv[u] : 0u, x = j < n ? xv[u] : 0u;
-                if (j < m) Y[(size_t)b * m + j] = fsub(y, mv[u]);
 #pragma unroll
                 for (int q = 0; q < EL; ++q) {
                     rr[q] += ffold((uint64_t)rv[q][u] * y);

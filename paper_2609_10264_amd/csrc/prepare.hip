@@ -202,10 +202,18 @@ __global__ __launch_bounds__(kAddThreads) void add_masks(const uint32_t* X, cons
             xv[u] = X[is];
             mv[u] = WAIT ? __hip_atomic_load(&Mx[is], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : Mx[is];
         }
+        uint32_t out[kAddPer];
+#pragma unroll
+        for (int u = 0; u < kAddPer; ++u) {
+            out[u] = fadd(xv[u], mv[u]);
+            // pinned in a register before the guarded store, so that the
+            // compiler does not sink the loads into the branch
+            asm volatile("" : "+v"(out[u]));
+        }
 #pragma unroll
         for (int u = 0; u < kAddPer; ++u) {
             const size_t i = base + threadIdx.x + (size_t)kAddThreads * u;
-            if (i < count) Xhat[i] = fadd(xv[u], mv[u]);
+            if (i < count) Xhat[i] = out[u];
         }
     }
     if constexpr (WAIT) {

@@ -126,14 +126,16 @@ __device__ __forceinline__ void syn_block(uint32_t c, uint32_t k, uint32_t r, co
         sj = idx[(size_t)c * t + q];
         sv = val[(size_t)c * t + q];
     }
+    // Pi2 and V2 (needed after the first suffix sum) now; Pi1 and V1 after the
+    // first suffix sum, so that the initial burst of loads is half as long
+    // (one compute unit issues them all) and the second half overlaps the
+    // Pi2 phase.
     uint32_t p1[U], p2[U], w1[U], w2[U], xin[SPARSE ? 1 : U], xv[kXF];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const uint32_t j = tid + T * u;
         const uint32_t js = j < N ? j : 0u;
-        p1[u] = pi1[js];
         p2[u] = pi2[js];
-        w1[u] = v1[js];
         w2[u] = v2[js];
         if constexpr (!SPARSE) xin[u] = vin[(size_t)c * N + js];
     }
@@ -144,14 +146,14 @@ __device__ __forceinline__ void syn_block(uint32_t c, uint32_t k, uint32_t r, co
             xv[f] = X[(size_t)c * k + (i < k ? i : 0u)];
         }
     }
-    // A = input, Bv = 0 (the Pi2 scatter fills [0, N); beyond N stays zero)
+    // A = input; Bv = 0 at positions >= N (the Pi2 scatter fills [0, N))
     {
         uint32_t* ra = A + tid * kRow;
         uint32_t* rb = Bv + tid * kRow;
 #pragma unroll
         for (int e = 0; e < E; ++e) {
             if (SPARSE) ra[e] = 0u;
-            rb[e] = 0u;
+            if ((uint32_t)tid * E + e >= N) rb[e] = 0u;
         }
     }
     if constexpr (SPARSE) {
@@ -174,6 +176,13 @@ __device__ __forceinline__ void syn_block(uint32_t c, uint32_t k, uint32_t r, co
     }
     __syncthreads();
     row_suffix_scan<E, T>(A, wsum);  // A
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const uint32_t j = tid + T * u;
+        const uint32_t js = j < N ? j : 0u;
+        p1[u] = pi1[js];
+        w1[u] = v1[js];
+    }
     scale_scatter<U, E, T>(A, Bv, p2, w2, N, pad_slot);  // V2, then Pi2
     __syncthreads();
     row_suffix_scan<E, T>(Bv, wsum);  // A

@@ -174,7 +174,7 @@ mvk_status mvk_encode(const mvk_key *key, const uint32_t *X, uint32_t B, const m
  *     E_ty^Ny (positions < Ny), v_L = (e_q^T Q) Xhat_b and
  *     v_R = e_q^T (Gy^T Yhat_b); column b is accepted iff v_L == v_R for every q.
  *     One challenge per repetition is shared by all columns (Sec. 5.4).
- *     Challenges must be drawn after the responses Yhat are fixed.
+ *     The server must not learn the challenges before its responses are fixed.
  *   Decrypt: Y_b = Yhat_b - P e_b with e_b sparse vector b of `ex`
  *     (the state returned by encode).
  *   Xhat   : device, B x n;  Yhat : device, B x m (the server's responses)

@@ -114,6 +114,20 @@ def calib_copy(mib: int):
     torch.cuda.synchronize()
 
 
+def warm(replay, seconds):
+    """Untimed replays until `seconds` have passed: the GPU's clocks ramp up
+    under sustained load, and a timed replay right after setup reads up to
+    ~15% slow."""
+    import torch
+
+    t_end = time.perf_counter() + seconds
+    while True:
+        replay()
+        torch.cuda.synchronize()
+        if time.perf_counter() >= t_end:
+            return
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -133,6 +147,8 @@ def parse():
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after timing, copy this many MiB device-to-device (reference kernel for HBM counters)")
     ap.add_argument("--seed", type=int, default=2609)
+    ap.add_argument("--warm-seconds", type=float, default=0.3,
+                    help="untimed replays of each timed graph before its timed replay")
     ap.add_argument("--path", default="auto", choices=["auto", "valu", "mfma"], help="server_eval kernel family")
     ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write the server_eval traffic record from two rocprofv3 --pmc counter files and exit")
@@ -261,8 +277,7 @@ def main():
                 with torch.cuda.stream(streams[c]):
                     graphs[c].replay()
 
-        replay_all()  # untimed replay
-        torch.cuda.synchronize()
+        warm(replay_all, args.warm_seconds)  # untimed replays
         ACC.zero_()
         torch.cuda.synchronize()
         t0 = time.perf_counter()
@@ -332,8 +347,7 @@ def main():
         with torch.cuda.stream(s_on):
             g_on.replay()
 
-    replay_pipelined()  # untimed replay
-    torch.cuda.synchronize()
+    warm(replay_pipelined, args.warm_seconds)  # untimed replays
     ACC2.zero_()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -368,8 +382,11 @@ def main():
     with torch.cuda.graph(ge, stream=s):
         for k in range(reps):
             mvk.server_eval(Ws[k % pool], Xs[k % pool], out=Yh, path=args.path)
-    ge.replay()
-    torch.cuda.synchronize()
+    def replay_ge():
+        with torch.cuda.stream(s):
+            ge.replay()
+
+    warm(replay_ge, args.warm_seconds)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     with torch.cuda.stream(s):
         e0.record()
@@ -528,9 +545,11 @@ def server_only(args, cfg, pool, total_steps, dev):
     with torch.cuda.graph(g, stream=s):
         for i in range(args.steps):
             mvk.server_eval(Ws[i % pool], X[i % pool], out=Y, path=args.path, stream=s)
-    with torch.cuda.stream(s):
-        g.replay()
-    torch.cuda.synchronize()
+    def replay_g():
+        with torch.cuda.stream(s):
+            g.replay()
+
+    warm(replay_g, args.warm_seconds)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     with torch.cuda.stream(s):

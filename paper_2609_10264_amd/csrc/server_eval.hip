@@ -550,27 +550,38 @@ __device__ __forceinline__ void store_tiles(const v4i (&acc)[QW][TWW], uint32_t 
     if (threadIdx.x == 0) atomicExch(&counters[rb], 0u);
 }
 
+// global_load_dwordx4 into a register quad, as inline assembly like dma16 so
+// that the explicit wait_vmcnt calls count it; the value may only be used
+// after a wait that covers it and a pin_vgpr that orders the use after that
+// wait.
+__device__ __forceinline__ void load16(v4i& dst, const void* src) {
+    asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(dst) : "v"(src) : "memory");
+}
+__device__ __forceinline__ void pin_vgpr(v4i& x) { asm volatile("" : "+v"(x)); }
+
 // QT digit tiles and NWT = (NW/WQ)*TWW W tiles per workgroup; the NW waves
 // form a WQ x (NW/WQ) grid: wave w computes digit tiles [(w%WQ)*QT/WQ, ...)
-// against W tiles [(w/WQ)*TWW, ...).  Waves [0, NW/2) load the W tiles of a
-// k-block, the others its digit tiles, each into its own ring (SW and SD
-// slots), so each wave's in-order load counter covers one stream only.
-template <int QT, int NW, int WQ, int TWW, int SW, int SD, bool PACKED>
+// against W tiles [(w/WQ)*TWW, ...).  W tiles, shared by the WQ waves of a
+// row group, travel HBM -> LDS by global_load_lds into an S-slot ring, every
+// wave issuing AW of a k-block's tiles; each wave loads its own QW digit
+// tiles (16 bytes per lane, already in operand order) straight into
+// registers, S k-blocks ahead, so the DMA path carries W only.  One wait per
+// k-block covers both: the loads complete in order, and S blocks are in
+// flight.
+template <int QT, int NW, int WQ, int TWW, int S, bool PACKED>
 __global__ __launch_bounds__(NW * 64) void server_eval_mfma_stream(
     const int8_t* __restrict__ W, uint32_t m, uint32_t n, const int8_t* __restrict__ Dt, uint32_t nkb,
     uint32_t ksplit, uint32_t B, uint32_t* __restrict__ Y, uint32_t* part, uint32_t* counters) {
     constexpr int WR = NW / WQ;               // waves along the row dimension
     constexpr int NWT = WR * TWW;             // W tiles per workgroup
     constexpr int QW = QT / WQ;               // digit tiles per wave
-    constexpr int NLW = NW / 2;               // waves [0, NLW) load W, the others load D
-    constexpr int AW = (NWT + NLW - 1) / NLW;  // W tiles loaded by a W-loading wave per k-block
-    constexpr int AQ = (QT + NLW - 1) / NLW;   // digit tiles loaded by a D-loading wave per k-block
+    constexpr int AW = (NWT + NW - 1) / NW;   // W tiles a wave loads per k-block
+    constexpr int PER = AW + QW;              // loads per wave per k-block
     static_assert(WQ * WR == NW && QW * WQ == QT, "tile split");
-    static_assert(SW * AW <= 63 && SD * AQ <= 63, "vmcnt range");
-    static_assert(SW >= 2 && SD >= 2, "ring depth");
+    static_assert(S * PER <= 63, "vmcnt range");
+    static_assert(S >= 2, "ring depth");
     constexpr uint32_t kRows = NWT * 16;
-    __shared__ __align__(16) int8_t Aring[SD][QT][1024];
-    __shared__ __align__(16) int8_t Wring[SW][NWT][1024];
+    __shared__ __align__(16) int8_t Wring[S][NWT][1024];
     // workgroup -> (row block, k-range), see above
     const uint32_t xcd = blockIdx.x % 8, per_group = 8 / ksplit;
     const uint32_t rb = (blockIdx.x / 8) * per_group + xcd / ksplit;
@@ -583,14 +594,12 @@ __global__ __launch_bounds__(NW * 64) void server_eval_mfma_stream(
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const bool wloader = wave < NLW;
-    const int lw = wloader ? wave : wave - NLW;  // index among the waves of its loading role
     const int wq = wave % WQ, wr = wave / WQ;
     const uint32_t kl = (lane >> 4) * 16;
-    const int8_t* wptr[AW];  // rows a W-loading wave loads
+    const int8_t* wptr[AW];  // rows this wave loads (row-major W)
 #pragma unroll
     for (int a = 0; a < AW; ++a) {
-        const uint32_t row = rb * kRows + ((lw * AW + a) % NWT) * 16 + (lane & 15);
+        const uint32_t row = rb * kRows + ((wave * AW + a) % NWT) * 16 + (lane & 15);
         wptr[a] = W + (size_t)(row < m ? row : m - 1) * n;
     }
     // In-range global k-block of local block j: blocks past the end of the
@@ -603,29 +612,25 @@ __global__ __launch_bounds__(NW * 64) void server_eval_mfma_stream(
     // Row-major W: columns >= n are read at column 0 (they meet zero digits).
     // Packed W: tile (row tile, k-block) is 1 KiB in operand order, zero padded;
     // row tiles past the end re-read the last one (their rows are not stored).
+    // When NWT is not a multiple of NW some tiles are loaded twice (same bytes).
     const uint32_t nrt = (m + 15) / 16;
-    auto issue_w = [&](uint32_t j, int slot) {
+    v4i dreg[S][QW];
+    auto issue = [&](uint32_t j, int slot) {
         const uint32_t kbe = kblock(j);
-        const uint32_t k = kbe * 64 + kl;
-        const uint32_t kk = k < n ? k : 0u;
 #pragma unroll
         for (int a = 0; a < AW; ++a) {
-            const int tile = (lw * AW + a) % NWT;
+            const int tile = (wave * AW + a) % NWT;
             if (PACKED) {
                 const uint32_t rt = rb * (kRows / 16) + tile;
                 dma16(W + (((size_t)(rt < nrt ? rt : nrt - 1) * nkb + kbe) * 64 + lane) * 16, &Wring[slot][tile][0]);
             } else {
-                dma16(wptr[a] + kk, &Wring[slot][tile][0]);
+                const uint32_t k = kbe * 64 + kl;
+                dma16(wptr[a] + (k < n ? k : 0u), &Wring[slot][tile][0]);
             }
         }
-    };
-    auto issue_d = [&](uint32_t j, int slot) {
-        const uint32_t kbe = kblock(j);
 #pragma unroll
-        for (int a = 0; a < AQ; ++a) {
-            const uint32_t qt = (lw * AQ + a) % QT;
-            dma16(Dt + ((size_t)(kbe * QT + qt) * 64 + lane) * 16, &Aring[slot][qt][0]);
-        }
+        for (int i = 0; i < QW; ++i)
+            load16(dreg[slot][i], Dt + ((size_t)(kbe * QT + wq * QW + i) * 64 + lane) * 16);
     };
     v4i acc[QW][TWW];
 #pragma unroll
@@ -633,44 +638,43 @@ __global__ __launch_bounds__(NW * 64) void server_eval_mfma_stream(
 #pragma unroll
         for (int t = 0; t < TWW; ++t) acc[i][t] = v4i{0, 0, 0, 0};
 
-    if (wloader) {
 #pragma unroll
-        for (int j = 0; j < SW; ++j) issue_w(j, j);
-    } else {
+    for (int j = 0; j < S; ++j) issue(j, j);
+    // k-blocks in groups of S so that the ring slot (and the register set of
+    // the digit tiles) is a compile-time index
+    for (uint32_t j0 = 0; j0 < nk; j0 += S) {
 #pragma unroll
-        for (int j = 0; j < SD; ++j) issue_d(j, j);
+        for (int sl = 0; sl < S; ++sl) {
+            const uint32_t j = j0 + sl;
+            if (j < nk) {
+                wait_vmcnt<(S - 1) * PER>();  // this wave's loads of k-block j landed
+#pragma unroll
+                for (int i = 0; i < QW; ++i) pin_vgpr(dreg[sl][i]);
+                __syncthreads();  // everyone's W tiles landed
+                v4i cb[TWW];
+#pragma unroll
+                for (int t = 0; t < TWW; ++t)
+                    cb[t] = *reinterpret_cast<const v4i*>(&Wring[sl][wr * TWW + t][16 * lane]);
+#pragma unroll
+                for (int i = 0; i < QW; ++i)
+#pragma unroll
+                    for (int t = 0; t < TWW; ++t)
+                        acc[i][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(dreg[sl][i], cb[t], acc[i][t], 0, 0, 0);
+                __syncthreads();  // every wave has read the slot: refill it
+                issue(j + S, sl);
+            }
+        }
     }
-    for (uint32_t j = 0; j < nk; ++j) {
-        const int wslot = (int)(j % SW), dslot = (int)(j % SD);
-        // this wave's loads of k-block j landed (the later blocks of its ring
-        // may still be in flight), then everyone's landed
-        if (wloader)
-            wait_vmcnt<(SW - 1) * AW>();
-        else
-            wait_vmcnt<(SD - 1) * AQ>();
-        __syncthreads();
-        v4i cb[TWW], ca[QW];
+    wait_vmcnt<0>();  // drain the trailing prefetches before the registers are reused or the workgroup exits
 #pragma unroll
-        for (int t = 0; t < TWW; ++t) cb[t] = *reinterpret_cast<const v4i*>(&Wring[wslot][wr * TWW + t][16 * lane]);
+    for (int sl = 0; sl < S; ++sl)
 #pragma unroll
-        for (int i = 0; i < QW; ++i) ca[i] = *reinterpret_cast<const v4i*>(&Aring[dslot][wq * QW + i][16 * lane]);
-#pragma unroll
-        for (int i = 0; i < QW; ++i)
-#pragma unroll
-            for (int t = 0; t < TWW; ++t)
-                acc[i][t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(ca[i], cb[t], acc[i][t], 0, 0, 0);
-        __syncthreads();  // every wave has read both slots: refill them
-        if (wloader)
-            issue_w(j + SW, wslot);
-        else
-            issue_d(j + SD, dslot);
-    }
-    wait_vmcnt<0>();  // drain the trailing prefetches before the workgroup exits
+        for (int i = 0; i < QW; ++i) pin_vgpr(dreg[sl][i]);
 
     const uint32_t rowbase = rb * kRows + wr * (TWW * 16) + (lane & 15);
     const uint32_t qbase = wq * QW * 4 + (lane >> 4);
     store_tiles<QW, TWW, NW>(acc, m, B, Y, part, counters, rb, (m + kRows - 1) / kRows, ks, ksplit, wave, lane,
-                             rowbase, qbase, reinterpret_cast<uint32_t*>(&Aring[0][0][0]));
+                             rowbase, qbase, reinterpret_cast<uint32_t*>(&Wring[0][0][0]));
 }
 
 // Digits-stationary variant for small batches (QT <= 4, i.e. B <= 16): the
@@ -830,8 +834,9 @@ __global__ __launch_bounds__(512) void server_eval_mfma_dstat(const int8_t* __re
 // wave.  QT = 16: 4 x 2 waves, 7 W tiles each (224 rows); QT = 8: 2 x 4
 // waves, 4 W tiles (256 rows); QT <= 4: 1 x 8 waves, 2 W tiles (256 rows).
 constexpr int kStreamWaves = 8;
+constexpr int kStreamSlots = 4;  // k-blocks in flight (W ring slots and digit register sets)
 uint32_t stream_rows(uint32_t qt) { return qt == 16 ? 224u : 256u; }
-uint32_t stream_slots(uint32_t qt) { return qt == 16 ? 7u : 8u; }  // W ring depth
+uint32_t stream_slots(uint32_t) { return kStreamSlots; }
 
 // k-range split: the split (1, 2, 4 or 8) that minimises the estimated time
 // ceil(workgroups / 256) * (k-blocks per range + pipeline fill), the smaller
@@ -853,7 +858,7 @@ uint32_t stream_ksplit(uint32_t m, uint32_t n, uint32_t qt) {
     return best;
 }
 
-template <int QT, int WQ, int TWW, int SW, int SD>
+template <int QT, int WQ, int TWW, int S>
 hipError_t launch_stream_cfg(const int8_t* W, uint32_t m, uint32_t n, const int8_t* Dt, uint32_t nkb, uint32_t B,
                              uint32_t* Y, uint32_t ksplit, uint32_t* part, uint32_t* counters, bool packed,
                              hipStream_t s) {
@@ -861,10 +866,10 @@ hipError_t launch_stream_cfg(const int8_t* W, uint32_t m, uint32_t n, const int8
     const uint32_t nrb = ceil_div(m, rows), per_group = 8 / ksplit;
     const dim3 grid(ceil_div(nrb, per_group) * 8);
     if (packed)
-        hipLaunchKernelGGL((server_eval_mfma_stream<QT, kStreamWaves, WQ, TWW, SW, SD, true>), grid,
+        hipLaunchKernelGGL((server_eval_mfma_stream<QT, kStreamWaves, WQ, TWW, S, true>), grid,
                            dim3(kStreamWaves * 64), 0, s, W, m, n, Dt, nkb, ksplit, B, Y, part, counters);
     else
-        hipLaunchKernelGGL((server_eval_mfma_stream<QT, kStreamWaves, WQ, TWW, SW, SD, false>), grid,
+        hipLaunchKernelGGL((server_eval_mfma_stream<QT, kStreamWaves, WQ, TWW, S, false>), grid,
                            dim3(kStreamWaves * 64), 0, s, W, m, n, Dt, nkb, ksplit, B, Y, part, counters);
     return hipGetLastError();
 }
@@ -1064,13 +1069,13 @@ hipError_t launch_server_eval(const int8_t* W, uint32_t m, uint32_t n, const uin
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         if (qt == 2)
-            e = launch_stream_cfg<2, 1, 2, 8, 8>(W, m, n, Dt, nkb, nb, Yb, ks, part, counters, packed, s);
+            e = launch_stream_cfg<2, 1, 2, kStreamSlots>(W, m, n, Dt, nkb, nb, Yb, ks, part, counters, packed, s);
         else if (qt == 4)
-            e = launch_stream_cfg<4, 1, 2, 8, 6>(W, m, n, Dt, nkb, nb, Yb, ks, part, counters, packed, s);
+            e = launch_stream_cfg<4, 1, 2, kStreamSlots>(W, m, n, Dt, nkb, nb, Yb, ks, part, counters, packed, s);
         else if (qt == 8)
-            e = launch_stream_cfg<8, 2, 4, 7, 4>(W, m, n, Dt, nkb, nb, Yb, ks, part, counters, packed, s);
+            e = launch_stream_cfg<8, 2, 4, kStreamSlots>(W, m, n, Dt, nkb, nb, Yb, ks, part, counters, packed, s);
         else
-            e = launch_stream_cfg<16, 4, 7, 7, 3>(W, m, n, Dt, nkb, nb, Yb, ks, part, counters, packed, s);
+            e = launch_stream_cfg<16, 4, 7, kStreamSlots>(W, m, n, Dt, nkb, nb, Yb, ks, part, counters, packed, s);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;

@@ -190,6 +190,18 @@ mvk_status mvk_decode_verify(const mvk_key *key, const uint32_t *Xhat, const uin
                              void *stream);
 
 /*
+ * Verify alone (Protocol vMVMD, Sec. 5.1; the verification-only mode of
+ * Sec. 7): for plaintext queries X (B x n) and claimed results Y (B x m) of
+ * the key's matrix, v_L = (e_q^T Q) x_b and v_R = (Gy e_q)^T y_b for every
+ * repetition q; accept[b] = 1 iff they agree for every q.  The same check as
+ * mvk_decode_verify without the decryption (the key's privacy code and PT are
+ * not used).  vL, vR: device, ell x B, may be NULL.
+ * Errors: MVK_EINVAL, MVK_ERANGE (ell > 16 or B > 65535), MVK_ENOMEM.
+ */
+mvk_status mvk_verify(const mvk_key *key, const uint32_t *X, const uint32_t *Y, uint32_t B,
+                      const mvk_sparse *ey, uint32_t *vL, uint32_t *vR, uint32_t *accept, void *stream);
+
+/*
  * Verify, first half: the challenge syndromes R[q*m + i] = (Gy e_q)[i] for
  * every repetition q < ey->count (R_q is the vector whose inner product with a
  * response gives v_R = e_q^T (Gy^T Yhat_b), the transposition identity of

@@ -318,6 +318,24 @@ def flag_wait(flag: torch.Tensor, value: int = 1, timeout_us: int = 200000, time
         _dev(timed_out, torch.int32, (), "timed_out") if timed_out is not None else None, _stream(stream)))
 
 
+def verify(key: Key, X: torch.Tensor, Y: torch.Tensor, ey_idx: torch.Tensor, ey_val: torch.Tensor,
+           vL: torch.Tensor | None = None, vR: torch.Tensor | None = None, accept: torch.Tensor | None = None,
+           stream=None):
+    """Verification only (vMVMD): check Y = W X for plaintext X (B x n) and Y (B x m).
+    Returns (accept, vL, vR); accept is int32 0/1 per column."""
+    B, ell = X.shape[0], ey_idx.shape[0]
+    if accept is None:
+        accept = torch.empty((B,), dtype=torch.int32, device=X.device)
+    ks = key.struct()
+    ey = _sparse(ey_idx, ey_val, "ey")
+    _lib.check("mvk_verify", _lib.load().mvk_verify(
+        ctypes.byref(ks), _dev(X, torch.int32, (B, key.n), "X"), _dev(Y, torch.int32, (B, key.m), "Y"), B,
+        ctypes.byref(ey), _dev(vL, torch.int32, (ell, B), "vL") if vL is not None else None,
+        _dev(vR, torch.int32, (ell, B), "vR") if vR is not None else None,
+        _dev(accept, torch.int32, (B,), "accept"), _stream(stream)))
+    return accept, vL, vR
+
+
 def raa_encode(code: Code, w: torch.Tensor, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
     """G^T w for each row of w (count x k) -> count x N."""
     w2 = w if w.dim() == 2 else w.reshape(1, -1)

@@ -31,6 +31,7 @@ EXPORTS = (
     "mvk_keygen",
     "mvk_encode",
     "mvk_decode_verify",
+    "mvk_verify",
     "mvk_verify_prepare",
     "mvk_decode_verify_prepared",
     "mvk_client_prepare",
@@ -116,6 +117,8 @@ def load() -> ctypes.CDLL:
     L.mvk_decode_verify.argtypes = [ctypes.POINTER(MvkKey), vp, vp, u32, ctypes.POINTER(MvkSparse),
                                     ctypes.POINTER(MvkSparse), vp, vp, vp, vp, vp]
     L.mvk_decode_verify.restype = st
+    L.mvk_verify.argtypes = [ctypes.POINTER(MvkKey), vp, vp, u32, ctypes.POINTER(MvkSparse), vp, vp, vp, vp]
+    L.mvk_verify.restype = st
     L.mvk_verify_prepare.argtypes = [ctypes.POINTER(MvkKey), ctypes.POINTER(MvkSparse), vp, vp]
     L.mvk_verify_prepare.restype = st
     L.mvk_decode_verify_prepared.argtypes = [ctypes.POINTER(MvkKey), vp, vp, u32, ctypes.POINTER(MvkSparse),

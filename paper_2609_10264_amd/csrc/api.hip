@@ -257,19 +257,21 @@ mvk_status mvk_decode_verify_prepared(const mvk_key* key, const uint32_t* Xhat, 
     return hip_status(launch_dv(key, Xhat, Yhat, B, ex, ey, R, Y, vL, vR, accept, ctrl, s));
 }
 
-mvk_status mvk_decode_verify(const mvk_key* key, const uint32_t* Xhat, const uint32_t* Yhat, uint32_t B,
+}  // extern "C"
+
+namespace {
+// decode_verify after the argument checks; Y may be null (no decryption
+// output) and ex may have t = 0 (no gathers of Pᵀ).
+mvk_status decode_verify_run(const mvk_key* key, const uint32_t* Xhat, const uint32_t* Yhat, uint32_t B,
                              const mvk_sparse* ex, const mvk_sparse* ey, uint32_t* Y, uint32_t* vL, uint32_t* vR,
-                             uint32_t* accept, void* stream) {
-    mvk_status st = check_decode_verify(key, Xhat, Yhat, B, ex, ey, Y, accept);
-    if (st || B == 0) return st;
-    hipStream_t s = (hipStream_t)stream;
+                             uint32_t* accept, hipStream_t s) {
     const uint32_t m = key->m, ell = ey->count;
     const size_t Ny = (size_t)key->cy.r * m;
     const size_t r_bytes = align_up((size_t)ell * m * 4);
     const size_t syn_bytes = Ny > kSynScratchAbove ? align_up((size_t)ell * 2 * Ny * 4) : 0;
     void* ws = nullptr;
     uint32_t* ctrl = nullptr;
-    st = workspace(s, r_bytes + syn_bytes, &ws, &ctrl, dv_ctrl_bytes(ell, B));
+    const mvk_status st = workspace(s, r_bytes + syn_bytes, &ws, &ctrl, dv_ctrl_bytes(ell, B));
     if (st) return st;
     uint32_t* rv = (uint32_t*)ws;
     uint32_t* syn_scratch = (uint32_t*)((char*)ws + r_bytes);
@@ -285,6 +287,30 @@ mvk_status mvk_decode_verify(const mvk_key* key, const uint32_t* Xhat, const uin
     hipError_t e = launch_syn_sparse(key->cy, ey->idx, ey->val, ey->t, ell, nullptr, syn_scratch, rv, s);
     if (e == hipSuccess) e = launch_dv(key, Xhat, Yhat, B, ex, ey, rv, Y, vL, vR, accept, ctrl, s);
     return hip_status(e);
+}
+}  // namespace
+
+extern "C" {
+
+mvk_status mvk_decode_verify(const mvk_key* key, const uint32_t* Xhat, const uint32_t* Yhat, uint32_t B,
+                             const mvk_sparse* ex, const mvk_sparse* ey, uint32_t* Y, uint32_t* vL, uint32_t* vR,
+                             uint32_t* accept, void* stream) {
+    mvk_status st = check_decode_verify(key, Xhat, Yhat, B, ex, ey, Y, accept);
+    if (st || B == 0) return st;
+    return decode_verify_run(key, Xhat, Yhat, B, ex, ey, Y, vL, vR, accept, (hipStream_t)stream);
+}
+
+mvk_status mvk_verify(const mvk_key* key, const uint32_t* X, const uint32_t* Y, uint32_t B, const mvk_sparse* ey,
+                      uint32_t* vL, uint32_t* vR, uint32_t* accept, void* stream) {
+    mvk_status st = check_key(key);
+    if (st) return st;
+    if (B == 0) return MVK_OK;
+    if (!key->Q || !X || !Y || !accept) return MVK_EINVAL;
+    st = check_challenges(key, ey);
+    if (st) return st;
+    if (B > 65535u) return MVK_ERANGE;
+    const mvk_sparse none = {nullptr, nullptr, 0u, B};  // no noise: nothing to decrypt
+    return decode_verify_run(key, X, Y, B, &none, ey, nullptr, vL, vR, accept, (hipStream_t)stream);
 }
 
 // Control word of the workgroup counters of client_prepare and encode_masked.

@@ -130,7 +130,7 @@ __device__ __forceinline__ void decode_part(const uint32_t* __restrict__ PT, uin
         uint64_t tot = 0;
 #pragma unroll
         for (int h = 0; h < G; ++h) tot += part[h][lane];
-        if (act) Y[(size_t)b * m + i] = fsub(yh, fred64(tot));
+        if (act && Y) Y[(size_t)b * m + i] = fsub(yh, fred64(tot));
     }
     if (WAIT_R) {
         if (threadIdx.x == 0) {

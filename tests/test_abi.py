@@ -167,3 +167,21 @@ def test_prepared_path_argument_checks_without_device_work():
     assert lib.mvk_flag_wait(None, 1, 10, None, None) == L.MVK_EINVAL
     assert lib.mvk_flag_wait(fake, 0, 10, None, None) == L.MVK_EINVAL
     assert lib.mvk_flag_wait(fake, 1, 0, None, None) == L.MVK_EINVAL
+
+
+def test_verify_only_argument_checks_without_device_work():
+    L = _lib()
+    lib = L.load()
+    fake = ctypes.c_void_p(0x1000)
+    code = L.MvkCode(8, 3, 0x1000, 0x1000, 0x1000, 0x1000)
+    key = L.MvkKey(8, 8, code, code, 0x1000, 0x1000)
+    ey = L.MvkSparse(0x1000, 0x1000, 2, 2)
+    assert lib.mvk_verify(ctypes.byref(key), fake, fake, 0, ctypes.byref(ey), None, None, None, None) == L.MVK_OK
+    assert lib.mvk_verify(ctypes.byref(key), None, fake, 1, ctypes.byref(ey), None, None, fake, None) == L.MVK_EINVAL
+    assert lib.mvk_verify(ctypes.byref(key), fake, fake, 1, ctypes.byref(ey), None, None, None, None) == L.MVK_EINVAL
+    assert lib.mvk_verify(ctypes.byref(key), fake, fake, 1, ctypes.byref(L.MvkSparse(0x1000, 0x1000, 2, 17)),
+                          None, None, fake, None) == L.MVK_ERANGE
+    assert lib.mvk_verify(ctypes.byref(key), fake, fake, 1, ctypes.byref(L.MvkSparse(0x1000, 0x1000, 25, 2)),
+                          None, None, fake, None) == L.MVK_EINVAL
+    noq = L.MvkKey(8, 8, code, code, 0x1000, 0)
+    assert lib.mvk_verify(ctypes.byref(noq), fake, fake, 1, ctypes.byref(ey), None, None, fake, None) == L.MVK_EINVAL

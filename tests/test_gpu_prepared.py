@@ -186,3 +186,23 @@ def test_pipelined_graphs_match_one_call_path():
             Yd, accr, _, _ = mvk.decode_verify(inst.key, Xr, Yr, EXI[i], EXV[i], EYI[i], EYV[i])
             assert torch.equal(Xh[i], Xr) and torch.equal(Yh[i], Yr) and torch.equal(Y[i], Yd), (rep, i)
         assert host(flags).tolist() == [0] * steps
+
+
+@pytest.mark.parametrize("cid,m,n,B,ry,ell", [(90, 256, 256, 1, 2, 2), (91, 1000, 700, 3, 3, 5), (92, 6000, 300, 2, 3, 2)])
+def test_verify_only_mode(cid, m, n, B, ry, ell):
+    """Verification without privacy: plaintext queries and results, accepted
+    when Y = W X, rejected column by column when a result is changed."""
+    _say(f"verify only cid={cid} m={m} n={n} B={B}")
+    inst = Instance(cid, m, n, B, 2, 0, ty=31, ell=ell, ry=ry).to_device()
+    mvk.keygen(inst.key, inst.dW)
+    _, Q = oracle.keygen(inst.W, inst.cx, inst.cy, want_P=False)
+    Yp = oracle.server_eval(inst.W, inst.X)
+    bad = Yp.copy()
+    bad[0, 3] = (int(bad[0, 3]) + 1) % P
+    for resp, want in ((Yp, [1] * B), (bad, [0] + [1] * (B - 1))):
+        vL = torch.empty((ell, B), dtype=torch.int32, device="cuda")
+        vR = torch.empty_like(vL)
+        acc, vL, vR = mvk.verify(inst.key, inst.dX, dev(resp), inst.deyi, inst.deyv, vL=vL, vR=vR)
+        oacc, ovL, ovR = oracle.verify(inst.cy, Q, inst.X, resp, inst.eyi, inst.eyv)
+        assert oacc.astype(np.uint32).tolist() == want == host(acc).tolist()
+        assert np.array_equal(host(vL), ovL) and np.array_equal(host(vR), ovR)

@@ -18,6 +18,10 @@ Parity status per function:
                      probability of Lemma 5.1 for t = 1
   noise_weight, verify_params
                      pinned: the values printed in Sec. 7.1
+  batch_aux, batch_project, batch_verify
+                     pinned: dense Qt^T G' and the secondary identity with
+                     dense matrices, completeness, rejection of a wrong claim,
+                     of a wrong projection and of a consistent forgery
 """
 from __future__ import annotations
 
@@ -64,6 +68,11 @@ def lib():
                                      u32, u32p, u32p, u32p, u32p, u32p, u32p]
             L.orc_encode.argtypes = [u32, u32, u32p, u32p, u32p, u32p, u32p, u32, u32p, u32p, u32, u32p]
             L.orc_decode.argtypes = [u32p, u32, u32p, u32, u32p, u32p, u32, u32p]
+            L.orc_batch_aux.argtypes = [u32, u32, u32, u32p, u32, u32p, u32p, u32p, u32p, u32p]
+            L.orc_batch_project.argtypes = [u32, u32, u32, u32p, u32p, u32p, u32, u32, u32p]
+            L.orc_batch_verify.argtypes = [u32, u32, u32, u32, u32p, u32p, u32p, u32p, u32, u32p, u32p, u32p, u32p,
+                                           u32p, u32p, u32p, u32p, u32p, u32, u32, u32p, u32p, u32p, u32, u32,
+                                           u32p, u32p, u32p, u32p]
             L.orc_verify.argtypes = [u32, u32, u32, u32p, u32p, u32p, u32p, u32p, u32p, u32p, u32,
                                      u32p, u32p, u32, u32, u32p, u32p, u8p]
             L.orc_prime.restype = u32
@@ -196,6 +205,63 @@ def verify(cy: dict, Q, Xhat, Yhat, ey_idx, ey_val):
     lib().orc_verify(m, n, cy["r"], *[_p(x) for x in a], _p(Q), _p(Xhat), _p(Yhat), B,
                      _p(ey_idx), _p(ey_val), ty, ell, _p(vL), _p(vR), _p(acc, ctypes.c_uint8))
     return acc.astype(bool), vL, vR
+
+
+# ---------------------------------------------------------------------------
+# Protocol Batch-vMVMD (Sec. 5.4)
+# ---------------------------------------------------------------------------
+def batch_aux(Qs, c2: dict) -> np.ndarray:
+    """Preprocess: Qaux = Qt^T G' (N x N') for Qs = [Q_1, ..., Q_B] (B x N x n)."""
+    Qs = _u32(Qs)
+    B, N, n = Qs.shape
+    assert c2["k"] == B * n
+    a = _code_args(c2)
+    out = np.empty((N, c2["N"]), dtype=np.uint32)
+    lib().orc_batch_aux(B, N, n, _p(Qs), c2["r"], *[_p(x) for x in a], _p(out))
+    return out
+
+
+def batch_project(Qs, e_idx, e_val) -> np.ndarray:
+    """Server step: u~(q) = Qt e(q) (ell x Bn)."""
+    Qs = _u32(Qs)
+    B, N, n = Qs.shape
+    e_idx = _u32(np.atleast_2d(e_idx))
+    e_val = _u32(np.atleast_2d(e_val))
+    ell, t = e_idx.shape
+    assert int(e_idx.max(initial=0)) < N
+    out = np.empty((ell, B * n), dtype=np.uint32)
+    lib().orc_batch_project(B, N, n, _p(Qs), _p(e_idx), _p(e_val), t, ell, _p(out))
+    return out
+
+
+def batch_verify(cy: dict, c2: dict, Qaux, X, Y, e_idx, e_val, ut, e2_idx, e2_val):
+    """Client checks.  Returns (accept[B] bool, batch_ok bool, vL, vR (ell x B),
+    sL, sR (ell x ell2)); claim b is accepted iff every secondary check of the
+    batch and every original check of b passes."""
+    X = _u32(np.atleast_2d(X))
+    Y = _u32(np.atleast_2d(Y))
+    B, n = X.shape
+    m = Y.shape[1]
+    assert cy["k"] == m and c2["k"] == B * n and Y.shape[0] == B
+    Qaux = _u32(Qaux)
+    assert Qaux.shape == (cy["N"], c2["N"])
+    e_idx, e_val = _u32(np.atleast_2d(e_idx)), _u32(np.atleast_2d(e_val))
+    e2_idx, e2_val = _u32(np.atleast_2d(e2_idx)), _u32(np.atleast_2d(e2_val))
+    ell, t = e_idx.shape
+    ell2, t2 = e2_idx.shape
+    ut = _u32(ut)
+    assert ut.shape == (ell, B * n)
+    vL = np.empty((ell, B), dtype=np.uint32)
+    vR = np.empty((ell, B), dtype=np.uint32)
+    sL = np.empty((ell, ell2), dtype=np.uint32)
+    sR = np.empty((ell, ell2), dtype=np.uint32)
+    a, a2 = _code_args(cy), _code_args(c2)
+    lib().orc_batch_verify(m, n, B, cy["r"], *[_p(x) for x in a], c2["r"], *[_p(x) for x in a2], _p(Qaux),
+                           _p(X), _p(Y), _p(e_idx), _p(e_val), t, ell, _p(ut), _p(e2_idx), _p(e2_val), t2, ell2,
+                           _p(vL), _p(vR), _p(sL), _p(sR))
+    batch_ok = bool((sL == sR).all())
+    accept = (vL == vR).all(axis=0) & batch_ok
+    return accept, batch_ok, vL, vR, sL, sR
 
 
 # ---------------------------------------------------------------------------

@@ -262,3 +262,103 @@ void orc_verify(uint32_t m, uint32_t n, uint32_t ry, const uint32_t *pi1, const 
     free(z);
     free(u);
 }
+
+/*
+ * Protocol Batch-vMVMD (Sec. 5.4), Preprocess, auxiliary matrix:
+ *   Qt = [Q_1 | ... | Q_B]^T in F^{Bn x N},  Qaux = Qt^T G' in F^{N x N'}.
+ * Row i of Qt^T is (Q_1[i, :], ..., Q_B[i, :]) (length Bn), so row i of Qaux
+ * is that row times G', i.e. the encoding G'^T of it (App. B).
+ * Qs: B x N x n (Q_b at Qs + b*N*n); the secondary code has k = B*n, block
+ * length N' = r2*B*n.  Qaux: N x N'.
+ */
+void orc_batch_aux(uint32_t B, uint32_t N, uint32_t n, const uint32_t *Qs, uint32_t r2,
+                   const uint32_t *pi1, const uint32_t *pi2, const uint32_t *v1, const uint32_t *v2,
+                   uint32_t *Qaux) {
+    uint64_t k2 = (uint64_t)B * n, N2 = k2 * r2;
+    uint32_t *row = (uint32_t *)malloc(k2 * sizeof(uint32_t));
+    for (uint64_t i = 0; i < N; i++) {
+        for (uint64_t b = 0; b < B; b++)
+            for (uint64_t c = 0; c < n; c++) row[b * n + c] = Qs[(b * N + i) * n + c];
+        orc_encT((uint32_t)k2, r2, pi1, pi2, v1, v2, row, Qaux + i * N2);
+    }
+    free(row);
+}
+
+/*
+ * Batch-vMVMD, Verify, server step: for every primary challenge e(q),
+ * u~(q) = Qt e(q) in F^{Bn}; entry b*n + c is sum_{j in supp(e)} e_j Q_b[j, c].
+ * e_idx, e_val: ell x t; out: ell x Bn.
+ */
+void orc_batch_project(uint32_t B, uint32_t N, uint32_t n, const uint32_t *Qs, const uint32_t *e_idx,
+                       const uint32_t *e_val, uint32_t t, uint32_t ell, uint32_t *out) {
+    (void)N;
+    uint64_t Bn = (uint64_t)B * n;
+    for (uint64_t q = 0; q < ell; q++) {
+        for (uint64_t b = 0; b < B; b++) {
+            for (uint64_t c = 0; c < n; c++) {
+                uint64_t acc = 0;
+                for (uint64_t s = 0; s < t; s++) {
+                    uint64_t j = e_idx[q * t + s];
+                    acc = fadd(acc, fmul(e_val[q * t + s], Qs[(b * N + j) * n + c]));
+                }
+                out[q * Bn + b * n + c] = (uint32_t)acc;
+            }
+        }
+    }
+}
+
+/*
+ * Batch-vMVMD, Verify, client checks:
+ *   z_b = G^T y_b;  r(j) = G' e'(j);
+ *   secondary, every (q, j):  sL = (e(q))^T Qaux e'(j),  sR = (r(j))^T u~(q);
+ *   original, every (q, b):   vL = (u_b(q))^T x_b,       vR = (e(q))^T z_b,
+ * where u_b(q) is entries [b*n, b*n + n) of u~(q).  The batch is accepted iff
+ * every secondary pair agrees; claim b iff, in addition, every original pair
+ * of b agrees (the caller combines them).
+ * Primary code G: k = m, rate r (pi1, pi2, v1, v2); secondary code G': k = B*n,
+ * rate r2 (qi1, qi2, w1, w2).  X: B x n, Y: B x m, Qaux: N x N' (N = r*m,
+ * N' = r2*B*n), e: ell x t, ut: ell x Bn, e2: ell2 x t2.
+ * Outputs vL, vR: ell x B; sL, sR: ell x ell2.
+ */
+void orc_batch_verify(uint32_t m, uint32_t n, uint32_t B, uint32_t r, const uint32_t *pi1, const uint32_t *pi2,
+                      const uint32_t *v1, const uint32_t *v2, uint32_t r2, const uint32_t *qi1, const uint32_t *qi2,
+                      const uint32_t *w1, const uint32_t *w2, const uint32_t *Qaux, const uint32_t *X,
+                      const uint32_t *Y, const uint32_t *e_idx, const uint32_t *e_val, uint32_t t, uint32_t ell,
+                      const uint32_t *ut, const uint32_t *e2_idx, const uint32_t *e2_val, uint32_t t2,
+                      uint32_t ell2, uint32_t *vL, uint32_t *vR, uint32_t *sL, uint32_t *sR) {
+    uint64_t N = (uint64_t)r * m, Bn = (uint64_t)B * n, N2 = Bn * r2;
+    uint32_t *z = (uint32_t *)malloc(N * sizeof(uint32_t));
+    uint32_t *e2 = (uint32_t *)malloc(N2 * sizeof(uint32_t));
+    uint32_t *rj = (uint32_t *)malloc(Bn * sizeof(uint32_t));
+    /* original checks */
+    for (uint64_t b = 0; b < B; b++) {
+        orc_encT(m, r, pi1, pi2, v1, v2, Y + b * m, z);
+        for (uint64_t q = 0; q < ell; q++) {
+            uint64_t l = 0, rr = 0;
+            for (uint64_t c = 0; c < n; c++) l = fadd(l, fmul(ut[q * Bn + b * n + c], X[b * n + c]));
+            for (uint64_t s = 0; s < t; s++) rr = fadd(rr, fmul(e_val[q * t + s], z[e_idx[q * t + s]]));
+            vL[q * B + b] = (uint32_t)l;
+            vR[q * B + b] = (uint32_t)rr;
+        }
+    }
+    /* secondary checks */
+    for (uint64_t j = 0; j < ell2; j++) {
+        for (uint64_t c = 0; c < N2; c++) e2[c] = 0;
+        for (uint64_t s = 0; s < t2; s++) e2[e2_idx[j * t2 + s]] = e2_val[j * t2 + s];
+        orc_syn((uint32_t)Bn, r2, qi1, qi2, w1, w2, e2, rj);
+        for (uint64_t q = 0; q < ell; q++) {
+            uint64_t lhs = 0, rhs = 0;
+            for (uint64_t a = 0; a < t; a++)
+                for (uint64_t s = 0; s < t2; s++) {
+                    uint64_t ent = Qaux[(uint64_t)e_idx[q * t + a] * N2 + e2_idx[j * t2 + s]];
+                    lhs = fadd(lhs, fmul(fmul(e_val[q * t + a], ent), e2_val[j * t2 + s]));
+                }
+            for (uint64_t c = 0; c < Bn; c++) rhs = fadd(rhs, fmul(rj[c], ut[q * Bn + c]));
+            sL[q * ell2 + j] = (uint32_t)lhs;
+            sR[q * ell2 + j] = (uint32_t)rhs;
+        }
+    }
+    free(z);
+    free(e2);
+    free(rj);
+}

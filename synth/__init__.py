@@ -35,6 +35,8 @@ PURPOSE_CY = 4
 PURPOSE_NOISE = 5
 PURPOSE_CHAL = 6
 PURPOSE_TAMPER = 7
+PURPOSE_C2 = 8      # secondary code of batch verification
+PURPOSE_CHAL2 = 9   # secondary challenges of batch verification
 
 
 def rng(seed: int) -> np.random.Generator:

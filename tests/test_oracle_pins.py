@@ -312,6 +312,108 @@ def test_acceptance_probability_lemma(t):
 
 
 # ---------------------------------------------------------------------------
+# Protocol Batch-vMVMD (Sec. 5.4)
+# ---------------------------------------------------------------------------
+def batch_instance(cid, m, n, B, r, r2, t, ell, t2, ell2):
+    """B claims M_b x_b = y_b under one primary code; Q_b = G^T M_b."""
+    Ws = [synth.weights(synth.seed_for(cid, synth.PURPOSE_W, b), m, n) for b in range(B)]
+    X = synth.field_uniform(synth.seed_for(cid, synth.PURPOSE_X), (B, n))
+    cx = synth.raa_code(synth.seed_for(cid, synth.PURPOSE_CX), n, 2)
+    cy = synth.raa_code(synth.seed_for(cid, synth.PURPOSE_CY), m, r)
+    c2 = synth.raa_code(synth.seed_for(cid, synth.PURPOSE_C2), B * n, r2)
+    Qs = np.stack([oracle.keygen(W, cx, cy, want_P=False)[1] for W in Ws])
+    Y = np.concatenate([oracle.server_eval(W, X[b:b + 1]) for b, W in enumerate(Ws)])
+    ei, ev = synth.sparse(synth.seed_for(cid, synth.PURPOSE_CHAL), ell, cy["N"], t)
+    e2i, e2v = synth.sparse(synth.seed_for(cid, synth.PURPOSE_CHAL2), ell2, c2["N"], t2)
+    return Ws, X, Y, cy, c2, Qs, ei, ev, e2i, e2v
+
+
+def test_batch_aux_against_dense():
+    """Qaux = Qt^T G' with Qt = [Q_1 | ... | Q_B]^T and G' built densely."""
+    Ws, X, Y, cy, c2, Qs, *_ = batch_instance(980, 3, 2, 2, 2, 2, 1, 1, 1, 1)
+    B, N, n = Qs.shape
+    QtT = [[int(Qs[b, i, c]) for b in range(B) for c in range(n)] for i in range(N)]  # N x Bn
+    want = _matmul(QtT, dense_G(c2))  # N x N'
+    assert oracle.batch_aux(Qs, c2).tolist() == want
+
+
+def test_batch_identity_with_dense_matrices():
+    """Both sides of each secondary check against Python integers and dense
+    matrices: sL = e^T (Qt^T G') e' and sR = (G' e')^T (Qt e); original
+    sides vR = e^T (G^T y_b), vL = (Q_b^T e)^T x_b."""
+    Ws, X, Y, cy, c2, Qs, ei, ev, e2i, e2v = batch_instance(981, 4, 3, 2, 2, 2, 2, 2, 2, 2)
+    B, N, n = Qs.shape
+    Qaux = oracle.batch_aux(Qs, c2)
+    ut = oracle.batch_project(Qs, ei, ev)
+    acc, ok, vL, vR, sL, sR = oracle.batch_verify(cy, c2, Qaux, X, Y, ei, ev, ut, e2i, e2v)
+    assert acc.all() and ok
+    G2 = dense_G(c2)  # Bn x N'
+    Gy = dense_G(cy)  # m x N
+    QtT = [[int(Qs[b, i, c]) for b in range(B) for c in range(n)] for i in range(N)]
+    for q in range(ei.shape[0]):
+        e = [0] * N
+        for j, v in zip(ei[q], ev[q]):
+            e[int(j)] = int(v)
+        u = matvec(transpose(QtT), e)  # Qt e, length Bn
+        assert ut[q].tolist() == u
+        for j in range(e2i.shape[0]):
+            e2 = [0] * c2["N"]
+            for c, v in zip(e2i[j], e2v[j]):
+                e2[int(c)] = int(v)
+            g = matvec(G2, e2)
+            assert int(sR[q, j]) == sum(a * b for a, b in zip(g, u)) % P
+            aux_e2 = matvec(_matmul(QtT, G2), e2)
+            assert int(sL[q, j]) == sum(a * b for a, b in zip(e, aux_e2)) % P
+        for b in range(B):
+            z = matvec(transpose(Gy), [int(v) for v in Y[b]])
+            assert int(vR[q, b]) == sum(a * b2 for a, b2 in zip(e, z)) % P
+            assert int(vL[q, b]) == sum(int(a) * int(x) for a, x in zip(u[b * n:(b + 1) * n], X[b])) % P
+
+
+def test_batch_completeness_and_rejections():
+    m, n, B = 40, 24, 3
+    Ws, X, Y, cy, c2, Qs, ei, ev, e2i, e2v = batch_instance(982, m, n, B, 3, 2, 31, 2, 31, 2)
+    Qaux = oracle.batch_aux(Qs, c2)
+    ut = oracle.batch_project(Qs, ei, ev)
+    acc, ok, *_ = oracle.batch_verify(cy, c2, Qaux, X, Y, ei, ev, ut, e2i, e2v)
+    assert acc.all() and ok
+    # a wrong claim: only that claim fails the original checks
+    bad = Y.copy()
+    bad[1, 7] = (int(bad[1, 7]) + 5) % P
+    acc, ok, *_ = oracle.batch_verify(cy, c2, Qaux, X, bad, ei, ev, ut, e2i, e2v)
+    assert acc.tolist() == [True, False, True] and ok
+    # a wrong projection: the secondary checks reject the batch
+    ut2 = ut.copy()
+    ut2[0, 30] = (int(ut2[0, 30]) + 1) % P
+    acc, ok, _, _, sL, sR = oracle.batch_verify(cy, c2, Qaux, X, Y, ei, ev, ut2, e2i, e2v)
+    assert not ok and not acc.any() and (sL[0] != sR[0]).all() and (sL[1] == sR[1]).all()
+
+
+def test_batch_consistent_forgery_caught_by_secondary_check():
+    """The server sees the primary challenges (it computes Qt e).  It can change
+    claim b's result by Delta and its projection u_b so that every original
+    check passes; only the secondary check, drawn after, catches it."""
+    m, n, B = 30, 16, 2
+    Ws, X, Y, cy, c2, Qs, ei, ev, e2i, e2v = batch_instance(983, m, n, B, 3, 2, 31, 2, 31, 2)
+    Qaux = oracle.batch_aux(Qs, c2)
+    ut = oracle.batch_project(Qs, ei, ev)
+    bad = Y.copy()
+    bad[0, 2] = (int(bad[0, 2]) + 1000) % P
+    forged = ut.copy()
+    x0 = [int(v) for v in X[0]]
+    inv_x = pow(x0[0], P - 2, P)
+    for q in range(ei.shape[0]):
+        # the original check for claim 0 needs u_0 . x_0 to move by e^T G^T Delta
+        e = np.zeros(cy["N"], dtype=np.uint32)
+        e[ei[q]] = ev[q]
+        shift = (1000 * int(oracle.syn(cy, e)[2])) % P
+        forged[q, 0] = (int(forged[q, 0]) + shift * inv_x) % P
+    acc, ok, vL, vR, _, _ = oracle.batch_verify(cy, c2, Qaux, X, bad, ei, ev, forged, e2i, e2v)
+    assert (vL == vR).all()  # every original check passes
+    assert not ok and not acc.any()
+
+
+# ---------------------------------------------------------------------------
 # Parameters printed in Sec. 7.1
 # ---------------------------------------------------------------------------
 def _golden_params():

@@ -303,6 +303,52 @@ mvk_status mvk_flag_wait(uint32_t *flag, uint32_t value, uint32_t timeout_us, ui
                          void *stream);
 
 /*
+ * Batch verification (Protocol Batch-vMVMD, Sec. 5.4): B claims
+ * M_b x_b = y_b with M_b in F^{m x n}, all keyed with the same verification
+ * code G (k = m, N = r*m): Q_b = G^T M_b from each claim's mvk_keygen.  The
+ * challenge projections u_b = Q_b^T e are computed by the server and checked
+ * with a second RAA code G' (k = B*n, N' = r'*B*n).
+ *
+ * Preprocess, auxiliary part:
+ *   Q     : host array of B device pointers, Q[b] is Q_b (N x n)
+ *   c2    : the secondary code, c2->k == B*n
+ *   QtT   : device, N x Bn, written: row i = (Q_1[i, :], ..., Q_B[i, :])
+ *           (what the server keeps, as the transpose of the stacked Qt)
+ *   Qaux  : device, N x N', written: Qaux = QtT G' (the client's state)
+ * Uses a workspace of N*N' words.  Errors: MVK_EINVAL, MVK_ERANGE, MVK_ENOMEM.
+ */
+mvk_status mvk_batch_preprocess(uint32_t B, const uint32_t *const *Q, uint32_t N, uint32_t n,
+                                const mvk_code *c2, uint32_t *QtT, uint32_t *Qaux, void *stream);
+
+/*
+ * Batch verification, server step: for every primary challenge e_q (shared by
+ * all claims), Ut[q] = Qt e_q = sum_{j in supp(e_q)} e_j QtT[j, :]  (B*n),
+ * whose entries [b*n, b*n + n) are u_b = Q_b^T e_q.
+ *   QtT: device, N x Bn (from mvk_batch_preprocess);  e: ell (1..16)
+ *   challenges of t positions < N;  Ut: device, ell x Bn, written.
+ * Errors: MVK_EINVAL, MVK_ERANGE (ell > 16).
+ */
+mvk_status mvk_batch_project(const uint32_t *QtT, uint32_t N, uint32_t n, uint32_t B,
+                             const mvk_sparse *e, uint32_t *Ut, void *stream);
+
+/*
+ * Batch verification, client checks, with the secondary challenges e2
+ * (ell2 = 1..16 challenges of t' positions < N') drawn after Ut is fixed:
+ *   original   vL[q][b] = (u_b of Ut[q]) . x_b  ==  vR[q][b] = (G e_q) . y_b
+ *   secondary  sL[q][j] = e_q^T Qaux e2_j      ==  sR[q][j] = (G' e2_j) . Ut[q]
+ * accept[b] = 1 iff every secondary pair of the batch and every original pair
+ * of claim b agree (a failed secondary check rejects the whole batch).
+ *   cy: primary code (k = m);  c2: secondary code (k = B*n);  Qaux: N x N';
+ *   X: B x n, Y: B x m (device);  vL, vR: ell x B;  sL, sR: ell x ell2
+ *   (device, may be NULL);  accept: device, B words.
+ * Errors: MVK_EINVAL, MVK_ERANGE (ell or ell2 > 16, B > 65535), MVK_ENOMEM.
+ */
+mvk_status mvk_batch_verify(const mvk_code *cy, const mvk_code *c2, const uint32_t *Qaux, uint32_t m,
+                            uint32_t n, uint32_t B, const uint32_t *X, const uint32_t *Y,
+                            const mvk_sparse *e, const uint32_t *Ut, const mvk_sparse *e2, uint32_t *vL,
+                            uint32_t *vR, uint32_t *sL, uint32_t *sR, uint32_t *accept, void *stream);
+
+/*
  * RAA encoding w -> G^T w (App. B, "Linear-time encoding") for `count`
  * vectors.  w: device, count x k field array; out: device, count x N.
  */

@@ -336,6 +336,57 @@ def verify(key: Key, X: torch.Tensor, Y: torch.Tensor, ey_idx: torch.Tensor, ey_
     return accept, vL, vR
 
 
+def batch_preprocess(Qs: list, c2: Code, stream=None):
+    """Batch verification, preprocessing: Qs = [Q_1, ..., Q_B] (N x n each, from
+    keygen with one verification code); returns (QtT (N x Bn), Qaux (N x N'))."""
+    B = len(Qs)
+    N, n = Qs[0].shape
+    ptrs = (ctypes.c_void_p * B)(*[_dev(Q, torch.int32, (N, n), f"Q[{b}]") for b, Q in enumerate(Qs)])
+    dev = Qs[0].device
+    QtT = torch.empty((N, B * n), dtype=torch.int32, device=dev)
+    Qaux = torch.empty((N, c2.N), dtype=torch.int32, device=dev)
+    cs = c2.struct()
+    _lib.check("mvk_batch_preprocess", _lib.load().mvk_batch_preprocess(
+        B, ptrs, N, n, ctypes.byref(cs), QtT.data_ptr(), Qaux.data_ptr(), _stream(stream)))
+    return QtT, Qaux
+
+
+def batch_project(QtT: torch.Tensor, n: int, e_idx: torch.Tensor, e_val: torch.Tensor,
+                  out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Batch verification, server step: Ut[q] = Qt e_q (ell x Bn)."""
+    N, Bn = QtT.shape
+    B = Bn // n
+    ell = e_idx.shape[0]
+    if out is None:
+        out = torch.empty((ell, Bn), dtype=torch.int32, device=QtT.device)
+    e = _sparse(e_idx, e_val, "e")
+    _lib.check("mvk_batch_project", _lib.load().mvk_batch_project(
+        _dev(QtT, torch.int32, (N, Bn), "QtT"), N, n, B, ctypes.byref(e),
+        _dev(out, torch.int32, (ell, Bn), "Ut"), _stream(stream)))
+    return out
+
+
+def batch_verify(cy: Code, c2: Code, Qaux: torch.Tensor, X: torch.Tensor, Y: torch.Tensor, e_idx: torch.Tensor,
+                 e_val: torch.Tensor, Ut: torch.Tensor, e2_idx: torch.Tensor, e2_val: torch.Tensor,
+                 accept: torch.Tensor | None = None, vL=None, vR=None, sL=None, sR=None, stream=None):
+    """Batch verification, client checks.  Returns (accept, vL, vR, sL, sR)."""
+    B, n = X.shape
+    m = Y.shape[1]
+    ell, ell2 = e_idx.shape[0], e2_idx.shape[0]
+    if accept is None:
+        accept = torch.empty((B,), dtype=torch.int32, device=X.device)
+    c1s, c2s = cy.struct(), c2.struct()
+    e, e2 = _sparse(e_idx, e_val, "e"), _sparse(e2_idx, e2_val, "e2")
+    opt = lambda t, shape, name: _dev(t, torch.int32, shape, name) if t is not None else None  # noqa: E731
+    _lib.check("mvk_batch_verify", _lib.load().mvk_batch_verify(
+        ctypes.byref(c1s), ctypes.byref(c2s), _dev(Qaux, torch.int32, (cy.N, c2.N), "Qaux"), m, n, B,
+        _dev(X, torch.int32, (B, n), "X"), _dev(Y, torch.int32, (B, m), "Y"), ctypes.byref(e),
+        _dev(Ut, torch.int32, (ell, B * n), "Ut"), ctypes.byref(e2), opt(vL, (ell, B), "vL"), opt(vR, (ell, B), "vR"),
+        opt(sL, (ell, ell2), "sL"), opt(sR, (ell, ell2), "sR"), _dev(accept, torch.int32, (B,), "accept"),
+        _stream(stream)))
+    return accept, vL, vR, sL, sR
+
+
 def raa_encode(code: Code, w: torch.Tensor, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
     """G^T w for each row of w (count x k) -> count x N."""
     w2 = w if w.dim() == 2 else w.reshape(1, -1)

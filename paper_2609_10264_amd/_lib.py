@@ -39,6 +39,9 @@ EXPORTS = (
     "mvk_decode_verify_masked",
     "mvk_flag_signal",
     "mvk_flag_wait",
+    "mvk_batch_preprocess",
+    "mvk_batch_project",
+    "mvk_batch_verify",
     "mvk_raa_encode",
     "mvk_raa_syndrome",
 )
@@ -135,6 +138,13 @@ def load() -> ctypes.CDLL:
     L.mvk_flag_signal.restype = st
     L.mvk_flag_wait.argtypes = [vp, u32, u32, vp, vp]
     L.mvk_flag_wait.restype = st
+    L.mvk_batch_preprocess.argtypes = [u32, ctypes.POINTER(vp), u32, u32, ctypes.POINTER(MvkCode), vp, vp, vp]
+    L.mvk_batch_preprocess.restype = st
+    L.mvk_batch_project.argtypes = [vp, u32, u32, u32, ctypes.POINTER(MvkSparse), vp, vp]
+    L.mvk_batch_project.restype = st
+    L.mvk_batch_verify.argtypes = [ctypes.POINTER(MvkCode), ctypes.POINTER(MvkCode), vp, u32, u32, u32, vp, vp,
+                                   ctypes.POINTER(MvkSparse), vp, ctypes.POINTER(MvkSparse), vp, vp, vp, vp, vp, vp]
+    L.mvk_batch_verify.restype = st
     L.mvk_raa_encode.argtypes = [ctypes.POINTER(MvkCode), vp, u32, vp, vp]
     L.mvk_raa_encode.restype = st
     L.mvk_raa_syndrome.argtypes = [ctypes.POINTER(MvkCode), vp, u32, vp, vp]

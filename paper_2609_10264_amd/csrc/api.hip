@@ -397,6 +397,79 @@ mvk_status mvk_flag_wait(uint32_t* flag, uint32_t value, uint32_t timeout_us, ui
     return hip_status(launch_flag_wait(flag, value, timeout_us, timed_out, (hipStream_t)stream));
 }
 
+mvk_status mvk_batch_preprocess(uint32_t B, const uint32_t* const* Q, uint32_t N, uint32_t n, const mvk_code* c2,
+                                uint32_t* QtT, uint32_t* Qaux, void* stream) {
+    if (B == 0 || N == 0 || n == 0 || !Q || !c2 || !QtT || !Qaux) return MVK_EINVAL;
+    const uint64_t Bn = (uint64_t)B * n;
+    if (Bn > 0x7fffffffull) return MVK_ERANGE;
+    mvk_status st = check_code(c2, (uint32_t)Bn);
+    if (st) return st;
+    for (uint32_t b = 0; b < B; ++b)
+        if (!Q[b]) return MVK_EINVAL;
+    const uint64_t N2 = Bn * c2->r;
+    hipStream_t s = (hipStream_t)stream;
+    void* ws = nullptr;
+    st = workspace(s, (size_t)N * N2 * sizeof(uint32_t), &ws);  // column scratch of the batched encoder
+    if (st) return st;
+    for (uint32_t b = 0; b < B; ++b) {
+        const hipError_t e = hipMemcpy2DAsync(QtT + (size_t)b * n, Bn * sizeof(uint32_t), Q[b], (size_t)n * 4,
+                                              (size_t)n * 4, N, hipMemcpyDeviceToDevice, s);
+        if (e != hipSuccess) return MVK_EHIP;
+    }
+    return hip_status(launch_encT_u32(*c2, QtT, 1, Bn, N, (uint32_t*)ws, Qaux, 1, N2, s));
+}
+
+mvk_status mvk_batch_project(const uint32_t* QtT, uint32_t N, uint32_t n, uint32_t B, const mvk_sparse* e,
+                             uint32_t* Ut, void* stream) {
+    if (!QtT || !Ut || !e || N == 0 || n == 0 || B == 0) return MVK_EINVAL;
+    if ((uint64_t)B * n > 0x7fffffffull) return MVK_ERANGE;
+    if (e->count == 0 || e->t == 0 || !e->idx || !e->val || e->t > N) return MVK_EINVAL;
+    if (e->count > kMaxEll) return MVK_ERANGE;
+    return hip_status(launch_gather_rows(QtT, B * n, N, e->idx, e->val, e->t, e->count, Ut, (hipStream_t)stream));
+}
+
+mvk_status mvk_batch_verify(const mvk_code* cy, const mvk_code* c2, const uint32_t* Qaux, uint32_t m, uint32_t n,
+                            uint32_t B, const uint32_t* X, const uint32_t* Y, const mvk_sparse* e, const uint32_t* Ut,
+                            const mvk_sparse* e2, uint32_t* vL, uint32_t* vR, uint32_t* sL, uint32_t* sR,
+                            uint32_t* accept, void* stream) {
+    if (m == 0 || n == 0 || B == 0) return m && n ? MVK_OK : MVK_EINVAL;
+    const uint64_t Bn = (uint64_t)B * n;
+    if (Bn > 0x7fffffffull || B > 65535u) return MVK_ERANGE;
+    mvk_status st = check_code(cy, m);
+    if (st) return st;
+    st = check_code(c2, (uint32_t)Bn);
+    if (st) return st;
+    if (!Qaux || !X || !Y || !Ut || !accept || !e || !e2) return MVK_EINVAL;
+    const uint64_t N = (uint64_t)cy->r * m, N2 = Bn * c2->r;
+    for (const mvk_sparse* v : {e, e2}) {
+        if (v->count == 0 || v->t == 0 || !v->idx || !v->val) return MVK_EINVAL;
+        if (v->count > kMaxEll) return MVK_ERANGE;
+    }
+    if (e->t > N || e2->t > N2 || N2 > 0x7fffffffull) return MVK_EINVAL;
+    const uint32_t ell = e->count, ell2 = e2->count;
+    hipStream_t s = (hipStream_t)stream;
+    const size_t r_bytes = align_up((size_t)ell * m * 4), rs_bytes = align_up((size_t)ell2 * Bn * 4);
+    size_t syn_bytes = 0;
+    if (N > kSynScratchAbove) syn_bytes = (size_t)ell * 2 * N * 4;
+    if (N2 > kSynScratchAbove && (size_t)ell2 * 2 * N2 * 4 > syn_bytes) syn_bytes = (size_t)ell2 * 2 * N2 * 4;
+    void* ws = nullptr;
+    uint32_t* ctrl = nullptr;
+    st = workspace(s, r_bytes + rs_bytes + syn_bytes, &ws, &ctrl,
+                   kCtrlBase + ((size_t)2 * ell * B + (size_t)2 * ell * ell2) * 8);
+    if (st) return st;
+    uint32_t* R = (uint32_t*)ws;
+    uint32_t* Rs = (uint32_t*)((char*)ws + r_bytes);
+    uint32_t* scratch = (uint32_t*)((char*)ws + r_bytes + rs_bytes);
+    // primary syndromes R_q = G e_q and secondary syndromes r_j = G' e'_j
+    hipError_t err = launch_syn_sparse(*cy, e->idx, e->val, e->t, ell, nullptr, scratch, R, s);
+    if (err == hipSuccess) err = launch_syn_sparse(*c2, e2->idx, e2->val, e2->t, ell2, nullptr, scratch, Rs, s);
+    if (err == hipSuccess)
+        err = launch_batch_check(m, n, B, X, Y, Ut, R, Rs, Qaux, (uint32_t)N, (uint32_t)N2, e->idx, e->val, e->t, ell,
+                                 e2->idx, e2->val, e2->t, ell2, (unsigned long long*)((char*)ctrl + kCtrlBase),
+                                 &ctrl[0], vL, vR, sL, sR, accept, s);
+    return hip_status(err);
+}
+
 mvk_status mvk_raa_encode(const mvk_code* code, const uint32_t* w, uint32_t count, uint32_t* out, void* stream) {
     if (!code) return MVK_EINVAL;
     mvk_status st = check_code(code, code->k);

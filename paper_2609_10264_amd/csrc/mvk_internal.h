@@ -104,9 +104,24 @@ hipError_t launch_client_prepare(const mvk_key& key, const uint32_t* ex_idx, con
 hipError_t launch_add_masks(const uint32_t* X, const uint32_t* Mx, size_t count, uint32_t* Xhat, uint32_t* flag,
                             uint32_t value, uint32_t timeout_us, uint32_t* timed_out, uint32_t* counter,
                             hipStream_t s);
+// out[v][:] = sum_s val[v*t+s] * M[idx[v*t+s], :] for `count` sparse vectors
+// (M: nrows x ld, row-major).
+hipError_t launch_gather_rows(const uint32_t* M, uint32_t ld, uint32_t nrows, const uint32_t* idx,
+                              const uint32_t* val, uint32_t t, uint32_t count, uint32_t* out, hipStream_t s);
 hipError_t launch_flag_signal(uint32_t* flag, uint32_t value, hipStream_t s);
 hipError_t launch_flag_wait(uint32_t* flag, uint32_t value, uint32_t timeout_us, uint32_t* timed_out,
                             hipStream_t s);
+
+// batch.hip -----------------------------------------------------------------
+// Client checks of batch verification.  R: ell x m primary syndromes G e_q;
+// Rs: ell2 x Bn secondary syndromes G' e'_j; acc: 2*ell*B + 2*ell*ell2 64-bit
+// accumulators and counter: one word, zero before the launch (left zero).
+hipError_t launch_batch_check(uint32_t m, uint32_t n, uint32_t B, const uint32_t* X, const uint32_t* Y,
+                              const uint32_t* Ut, const uint32_t* R, const uint32_t* Rs, const uint32_t* Qaux,
+                              uint32_t N, uint32_t N2, const uint32_t* e_idx, const uint32_t* e_val, uint32_t t,
+                              uint32_t ell, const uint32_t* e2_idx, const uint32_t* e2_val, uint32_t t2,
+                              uint32_t ell2, unsigned long long* acc, uint32_t* counter, uint32_t* vL, uint32_t* vR,
+                              uint32_t* sL, uint32_t* sR, uint32_t* accept, hipStream_t s);
 
 inline uint32_t ceil_div(uint32_t a, uint32_t b) { return (a + b - 1) / b; }
 

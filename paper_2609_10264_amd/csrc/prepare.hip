@@ -171,6 +171,23 @@ __device__ __forceinline__ bool poll_flag(const uint32_t* flag, uint32_t value, 
     return true;
 }
 
+// out[v][i] = sum_s val[v*t + s] * M[idx[v*t + s], i] for `count` sparse
+// vectors v (M: nrows x ld): nb = ceil(ld/64) items per vector, four per
+// workgroup.
+__global__ __launch_bounds__(kPrepThreads) void gather_rows_kernel(const uint32_t* __restrict__ M, uint32_t ld,
+                                                                   uint32_t nrows, const uint32_t* __restrict__ idx,
+                                                                   const uint32_t* __restrict__ val, uint32_t t,
+                                                                   uint32_t count, uint32_t nb,
+                                                                   uint32_t* __restrict__ out) {
+    __shared__ uint64_t part[kQuarters * kQGroups][kQCols];
+    const int quarter = threadIdx.x / kQuarter;
+    const uint32_t item = blockIdx.x * kQuarters + (uint32_t)quarter;
+    const bool live = item < count * nb;
+    const uint32_t v = live ? item / nb : 0u, cb = live ? item % nb : 0u;
+    gather_item<false>(M, ld, nrows, idx + (size_t)v * t, val + (size_t)v * t, t, out + (size_t)v * ld, cb * kQCols,
+                       live, part + quarter * kQGroups);
+}
+
 // Xhat = X + Mx, element-wise over count words, kAddPer words per thread and
 // pass with the pass's loads issued first.  WAIT: first every workgroup waits
 // for *flag == value (thread 0 polls), then reads Mx device-coherently; the
@@ -308,6 +325,17 @@ hipError_t launch_client_prepare(const mvk_key& key, const uint32_t* ex_idx, con
     else if (U == 12) { MVK_PREP(12); }
     else { MVK_PREP(16); }
 #undef MVK_PREP
+    return hipGetLastError();
+}
+
+hipError_t launch_gather_rows(const uint32_t* M, uint32_t ld, uint32_t nrows, const uint32_t* idx,
+                              const uint32_t* val, uint32_t t, uint32_t count, uint32_t* out, hipStream_t s) {
+    if (count == 0 || ld == 0) return hipSuccess;
+    const uint32_t nb = ceil_div(ld, kQCols);
+    const uint64_t grid = ((uint64_t)count * nb + kQuarters - 1) / kQuarters;
+    if (grid > 0x7fffffffu) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(gather_rows_kernel, dim3((uint32_t)grid), dim3(kPrepThreads), 0, s, M, ld, nrows, idx, val, t,
+                       count, nb, out);
     return hipGetLastError();
 }
 

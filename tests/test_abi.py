@@ -185,3 +185,39 @@ def test_verify_only_argument_checks_without_device_work():
                           None, None, fake, None) == L.MVK_EINVAL
     noq = L.MvkKey(8, 8, code, code, 0x1000, 0)
     assert lib.mvk_verify(ctypes.byref(noq), fake, fake, 1, ctypes.byref(ey), None, None, fake, None) == L.MVK_EINVAL
+
+
+def test_batch_argument_checks_without_device_work():
+    L = _lib()
+    lib = L.load()
+    fake = ctypes.c_void_p(0x1000)
+    cy = L.MvkCode(8, 3, 0x1000, 0x1000, 0x1000, 0x1000)   # k = m = 8, N = 24
+    c2 = L.MvkCode(12, 2, 0x1000, 0x1000, 0x1000, 0x1000)  # k = B*n = 12, N' = 24
+    ptrs = (ctypes.c_void_p * 3)(0x1000, 0x1000, 0x1000)
+    pre = lib.mvk_batch_preprocess
+    assert pre(0, ptrs, 24, 4, ctypes.byref(c2), fake, fake, None) == L.MVK_EINVAL
+    assert pre(3, ptrs, 24, 5, ctypes.byref(c2), fake, fake, None) == L.MVK_EINVAL  # c2.k != B*n
+    assert pre(3, ptrs, 24, 4, ctypes.byref(c2), None, fake, None) == L.MVK_EINVAL
+    nulls = (ctypes.c_void_p * 3)(0x1000, 0, 0x1000)
+    assert pre(3, nulls, 24, 4, ctypes.byref(c2), fake, fake, None) == L.MVK_EINVAL
+    e = L.MvkSparse(0x1000, 0x1000, 2, 2)
+    assert lib.mvk_batch_project(fake, 24, 4, 3, ctypes.byref(L.MvkSparse(0x1000, 0x1000, 2, 17)), fake,
+                                 None) == L.MVK_ERANGE
+    assert lib.mvk_batch_project(fake, 24, 4, 3, ctypes.byref(L.MvkSparse(0x1000, 0x1000, 25, 2)), fake,
+                                 None) == L.MVK_EINVAL
+    assert lib.mvk_batch_project(fake, 24, 4, 3, ctypes.byref(e), None, None) == L.MVK_EINVAL
+    ver = lib.mvk_batch_verify
+    args = lambda **kw: dict(dict(cy=ctypes.byref(cy), c2=ctypes.byref(c2), Qaux=fake, m=8, n=4, B=3, X=fake,  # noqa: E731
+                                  Y=fake, e=ctypes.byref(e), Ut=fake, e2=ctypes.byref(e), acc=fake), **kw)
+
+    def call(a):
+        return ver(a["cy"], a["c2"], a["Qaux"], a["m"], a["n"], a["B"], a["X"], a["Y"], a["e"], a["Ut"], a["e2"],
+                   None, None, None, None, a["acc"], None)
+
+    assert call(args(B=0)) == L.MVK_OK
+    assert call(args(n=5)) == L.MVK_EINVAL               # secondary code dimension != B*n
+    assert call(args(m=9)) == L.MVK_EINVAL               # primary code dimension != m
+    assert call(args(acc=None)) == L.MVK_EINVAL
+    assert call(args(e2=ctypes.byref(L.MvkSparse(0x1000, 0x1000, 2, 17)))) == L.MVK_ERANGE
+    assert call(args(e2=ctypes.byref(L.MvkSparse(0x1000, 0x1000, 25, 2)))) == L.MVK_EINVAL  # t' > N' = 24
+    assert call(args(e=ctypes.byref(L.MvkSparse(0x1000, 0x1000, 25, 2)))) == L.MVK_EINVAL   # t > N = 24

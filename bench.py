@@ -162,6 +162,9 @@ def parse():
     ap.add_argument("--B", type=int, default=0, help="override the workload's query count (server-only)")
     ap.add_argument("--server-only", action="store_true",
                     help="time server_eval alone (no client steps) on the chosen workload")
+    ap.add_argument("--batch-verify", type=int, default=0, metavar="B",
+                    help="time batch verification (Protocol Batch-vMVMD) of B claims of the workload's shape "
+                         "against B one-claim verifications, and exit")
     return ap.parse_args()
 
 
@@ -184,6 +187,8 @@ def main():
     torch.cuda.set_device(0)
     if args.config == "stack32":
         return stack_bench(args)
+    if args.batch_verify:
+        return batch_verify_bench(args)
     cfg = dict(synth.CONFIGS[args.config])
     if args.server_only:
         for key in ("m", "n", "B"):
@@ -574,6 +579,97 @@ def server_only(args, cfg, pool, total_steps, dev):
                         "mean_launch_us": 1e6 * mean_s, "median_launch_us": 1e3 * float(np.median(ms))},
            "mfma_int8_tops": 2 * 4 * macs / mean_s / 1e12}
     print(json.dumps(out), flush=True)
+
+
+def batch_verify_bench(args):
+    """Batch verification of B claims M_b x_b = y_b (B matrices of the
+    workload's shape, one verification code): the server's projection
+    (mvk_batch_project) and the client's checks (mvk_batch_verify), against
+    the client verifying the B claims one by one (mvk_verify, which gathers
+    the rows of each Q_b itself).  Preprocessing untimed."""
+    import numpy as np
+    import torch
+
+    import paper_2609_10264_amd as mvk
+    import synth
+
+    cfg = dict(synth.CONFIGS[args.config])
+    m, n, r, ty, ell = (cfg[k] for k in ("m", "n", "r", "ty", "ell"))
+    B, r2 = args.batch_verify, 2
+    cid, dev = cfg["cid"], torch.device("cuda")
+
+    def d(a):
+        return torch.from_numpy(np.ascontiguousarray(a).astype(np.int32)).to(dev)
+
+    def code(c):
+        return mvk.Code(c["k"], c["r"], d(c["pi1"]), d(c["pi2"]), d(c["v1"]), d(c["v2"]))
+
+    cx_h = synth.raa_code(synth.seed_for(cid, synth.PURPOSE_CX), n, r)
+    cy_h = synth.raa_code(synth.seed_for(cid, synth.PURPOSE_CY), m, r)
+    c2_h = synth.raa_code(synth.seed_for(cid, synth.PURPOSE_C2), B * n, r2)
+    cx, cy, c2 = code(cx_h), code(cy_h), code(c2_h)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(args.seed)
+    Ws = [torch.randint(-127, 128, (m, n), generator=gen, device=dev, dtype=torch.int8) for _ in range(B)]
+    keys = []
+    for W in Ws:
+        k = mvk.Key.allocate(m, n, cx, cy)
+        mvk.keygen(k, W)
+        keys.append(k)
+    QtT, Qaux = mvk.batch_preprocess([k.Q for k in keys], c2)
+    X = torch.randint(0, mvk.P, (B, n), generator=gen, device=dev, dtype=torch.int32)
+    Y = torch.stack([mvk.server_eval(W, X[b:b + 1])[0] for b, W in enumerate(Ws)])
+    steps = args.steps
+    ei, ev = synth.sparse(synth.seed_for(cid, synth.PURPOSE_CHAL, 3), steps * ell, cy_h["N"], ty)
+    e2i, e2v = synth.sparse(synth.seed_for(cid, synth.PURPOSE_CHAL2, 3), steps * ell, c2_h["N"], ty)
+    EI, EV = d(ei).view(steps, ell, ty), d(ev).view(steps, ell, ty)
+    E2I, E2V = d(e2i).view(steps, ell, ty), d(e2v).view(steps, ell, ty)
+    Ut = torch.empty((steps, ell, B * n), dtype=torch.int32, device=dev)
+    acc = torch.zeros((steps, B), dtype=torch.int32, device=dev)
+    acc1 = torch.zeros((steps, B), dtype=torch.int32, device=dev)
+    s = torch.cuda.Stream()
+
+    def one_batch(i):
+        mvk.batch_project(QtT, n, EI[i], EV[i], out=Ut[i])
+        mvk.batch_verify(cy, c2, Qaux, X, Y, EI[i], EV[i], Ut[i], E2I[i], E2V[i], accept=acc[i])
+
+    def one_by_one(i):
+        for b in range(B):
+            mvk.verify(keys[b], X[b:b + 1], Y[b:b + 1], EI[i], EV[i], accept=acc1[i, b:b + 1])
+
+    out = {}
+    for name, fn in (("batch", one_batch), ("one_by_one", one_by_one)):
+        with torch.cuda.stream(s):
+            fn(0)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            for i in range(steps):
+                fn(i)
+
+        def replay():
+            with torch.cuda.stream(s):
+                g.replay()
+
+        warm(replay, args.warm_seconds)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(s):
+            e0.record()
+            g.replay()
+            e1.record()
+        torch.cuda.synchronize()
+        out[name] = 1e3 * e0.elapsed_time(e1) / steps
+    ok = bool((acc == 1).all().item()) and bool((acc1 == 1).all().item())
+    res = {"metric": "batch verification time per batch of claims (Protocol Batch-vMVMD), 1×MI355X",
+           "value": out["batch"], "unit": "us", "n_gpus": 1, "steps": steps, "warmup": args.warmup,
+           "higher_is_better": False, "data": "synthetic",
+           "config": {"workload": f"{B} claims of W {m}x{n} (int8-valued in F_p), primary RAA r={r}, "
+                                  f"secondary RAA r'={r2} over Bn={B * n}, t=t'={ty}, ell=ell'={ell}",
+                      "claims": B},
+           "batch_us": out["batch"], "one_by_one_us": out["one_by_one"], "all_accepted": ok}
+    print(json.dumps(res), flush=True)
+    if not ok:
+        sys.exit(1)
 
 
 def cpu_baseline(args, cfg, cx_h, cy_h):

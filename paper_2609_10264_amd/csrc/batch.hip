@@ -60,7 +60,7 @@ struct CheckArgs {
 
 // Workgroups [0, B*nbL): v_L terms u_b(q)[k] x_b[k]; next B*nbR: v_R terms
 // R_q[i] y_b[i]; next nbS: secondary right sides r_j[c] u~(q)[c]; the last
-// one: the t x t' lookups of every secondary left side.  Partial sums go into
+// ell*ell2: the t x t' lookups of one secondary left side each.  Partial sums go into
 // 64-bit accumulators; the workgroup that finishes last (counter) reads and
 // clears them and writes the results and the accept bits.
 __global__ __launch_bounds__(kBT) void batch_check_kernel(CheckArgs a) {
@@ -95,20 +95,33 @@ __global__ __launch_bounds__(kBT) void batch_check_kernel(CheckArgs a) {
                 block_add(ffold((uint64_t)rj * a.Ut[(size_t)q * Bn + cs]), red, &a.accS[(size_t)q * a.ell2 + j]);
         }
     } else {
+        // one (q, j) pair per workgroup; the t x t' lookups kLook per thread
+        // and pass, every load of a pass issued before the first use
+        constexpr int kLook = 4;
+        const uint32_t qj = bid - nL - nR - a.nbS, q = qj / a.ell2, j = qj % a.ell2;
         const uint32_t pairs = a.t * a.t2;
-        for (uint32_t q = 0; q < a.ell; ++q)
-            for (uint32_t j = 0; j < a.ell2; ++j) {
-                uint64_t s = 0;
-                for (uint32_t p = tid; p < pairs; p += kBT) {
-                    const uint32_t x = p / a.t2, y = p % a.t2;
-                    uint32_t row = a.e_idx[(size_t)q * a.t + x], col = a.e2_idx[(size_t)j * a.t2 + y];
-                    row = row < a.N ? row : a.N - 1;
-                    col = col < a.N2 ? col : a.N2 - 1;
-                    const uint32_t ent = a.Qaux[(size_t)row * a.N2 + col];
-                    s += ffold((uint64_t)fmul(a.e_val[(size_t)q * a.t + x], ent) * a.e2_val[(size_t)j * a.t2 + y]);
-                }
-                block_add(s, red, &a.accA[(size_t)q * a.ell2 + j]);
+        uint64_t s = 0;
+        for (uint32_t p0 = 0; p0 < pairs; p0 += kBT * kLook) {
+            uint32_t row[kLook], col[kLook], w1[kLook], w2[kLook], ent[kLook];
+#pragma unroll
+            for (int u = 0; u < kLook; ++u) {
+                const uint32_t p = p0 + tid + kBT * u;
+                const uint32_t ps = p < pairs ? p : 0u;
+                const uint32_t x = ps / a.t2, y = ps % a.t2;
+                row[u] = a.e_idx[(size_t)q * a.t + x];
+                col[u] = a.e2_idx[(size_t)j * a.t2 + y];
+                w1[u] = a.e_val[(size_t)q * a.t + x];
+                w2[u] = p < pairs ? a.e2_val[(size_t)j * a.t2 + y] : 0u;
             }
+#pragma unroll
+            for (int u = 0; u < kLook; ++u) {
+                const uint32_t rr = row[u] < a.N ? row[u] : a.N - 1, cc = col[u] < a.N2 ? col[u] : a.N2 - 1;
+                ent[u] = a.Qaux[(size_t)rr * a.N2 + cc];
+            }
+#pragma unroll
+            for (int u = 0; u < kLook; ++u) s += ffold((uint64_t)fmul(w1[u], ent[u]) * w2[u]);
+        }
+        block_add(s, red, &a.accA[(size_t)q * a.ell2 + j]);
     }
     // Completion as in the decode/verify kernels: atomics complete (vmcnt 0)
     // before the barrier, the count after it, the last workgroup reads the
@@ -164,7 +177,7 @@ hipError_t launch_batch_check(uint32_t m, uint32_t n, uint32_t B, const uint32_t
     a.counter = counter;
     a.vL = vL, a.vR = vR, a.sL = sL, a.sR = sR, a.accept = accept;
     a.nbL = ceil_div(n, kBT), a.nbR = ceil_div(m, kBT), a.nbS = ceil_div(B * n, kBT);
-    const uint64_t grid = (uint64_t)B * (a.nbL + a.nbR) + a.nbS + 1;
+    const uint64_t grid = (uint64_t)B * (a.nbL + a.nbR) + a.nbS + (uint64_t)ell * ell2;
     if (grid > 0x7fffffffu) return hipErrorInvalidValue;
     hipLaunchKernelGGL(batch_check_kernel, dim3((uint32_t)grid), dim3(kBT), 0, s, a);
     return hipGetLastError();

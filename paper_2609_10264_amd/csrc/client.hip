@@ -382,36 +382,40 @@ __global__ __launch_bounds__(kFusedThreads) void decode_verify_syn(
     finish(B, ell, accL, accR, counter, rdone, err, vL, vR, accept, &last);
 }
 
-// decode_verify_masked for small problems, by one workgroup: no atomics and
-// no cross-workgroup counter.  Thread t takes the outputs i = t + 1024 u of
-// every column (Y_b[i] = Yhat_b[i] - My_b[i] and the v_R terms
-// R_q[i] Yhat_b[i]) and the inputs k = t + 1024 u (the v_L terms
-// U_q[k] Xhat_b[k]), kSmallPer of each per pass with all of a pass's loads
-// issued before the first is used (addresses clamped in range, terms masked);
-// the 2 * ell partial sums of a column are reduced across the waves in LDS.
+// decode_verify_masked for small problems, by a few workgroups (at most 8):
+// thread g of the grid (g = 1024 * workgroup + thread) takes the outputs
+// i = g + 1024 G u of every column (Y_b[i] = Yhat_b[i] - My_b[i] and the v_R
+// terms R_q[i] Yhat_b[i]) and the inputs k = g + 1024 G u (the v_L terms
+// U_q[k] Xhat_b[k]), PER of each per pass with all of a pass's loads issued
+// before the first is used (addresses clamped in range, terms masked).  The
+// 2 * ell partial sums of a column are reduced across the waves in LDS; with
+// one workgroup the results follow directly, with several each adds its sums
+// into 64-bit accumulators and the last one to finish (counter) compares.
 // ell <= EL.
 constexpr int kSmallThreads = 1024;
-constexpr int kSmallPer = 4;
-template <int EL>
+template <int EL, int PER>
 __global__ __launch_bounds__(kSmallThreads) void decode_verify_small(
     uint32_t m, uint32_t n, const uint32_t* __restrict__ Xhat, const uint32_t* __restrict__ Yhat, uint32_t B,
     const uint32_t* __restrict__ My, uint32_t ell, const uint32_t* __restrict__ R, const uint32_t* __restrict__ U,
-    uint32_t* __restrict__ Y, uint32_t* __restrict__ vL, uint32_t* __restrict__ vR, uint32_t* __restrict__ accept) {
+    uint32_t* __restrict__ Y, unsigned long long* acc, uint32_t* counter, uint32_t* __restrict__ vL,
+    uint32_t* __restrict__ vR, uint32_t* __restrict__ accept) {
     constexpr int NW = kSmallThreads / 64;
-    constexpr uint32_t kPass = (uint32_t)kSmallThreads * kSmallPer;
     __shared__ uint64_t red[NW][2 * EL];
     __shared__ uint32_t fin[2 * EL];
+    __shared__ uint32_t last;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const uint32_t G = gridDim.x, gt = blockIdx.x * kSmallThreads + (uint32_t)tid;
+    const uint32_t stride = G * kSmallThreads, pass = stride * PER;
     const uint32_t len = m > n ? m : n;
     for (uint32_t b = 0; b < B; ++b) {
         uint64_t l[EL], rr[EL];
 #pragma unroll
         for (int q = 0; q < EL; ++q) l[q] = rr[q] = 0;
-        for (uint32_t base = 0; base < len; base += kPass) {
-            uint32_t yv[kSmallPer], mv[kSmallPer], xv[kSmallPer], rv[EL][kSmallPer], uv[EL][kSmallPer];
+        for (uint32_t base = 0; base < len; base += pass) {
+            uint32_t yv[PER], mv[PER], xv[PER], rv[EL][PER], uv[EL][PER];
 #pragma unroll
-            for (int u = 0; u < kSmallPer; ++u) {
-                const uint32_t j = base + (uint32_t)tid + (uint32_t)kSmallThreads * u;
+            for (int u = 0; u < PER; ++u) {
+                const uint32_t j = base + gt + stride * u;
                 const uint32_t i = j < m ? j : m - 1, k = j < n ? j : n - 1;
                 yv[u] = Yhat[(size_t)b * m + i];
                 mv[u] = My[(size_t)b * m + i];
@@ -424,8 +428,8 @@ __global__ __launch_bounds__(kSmallThreads) void decode_verify_small(
                 }
             }
 #pragma unroll
-            for (int u = 0; u < kSmallPer; ++u) {
-                const uint32_t j = base + (uint32_t)tid + (uint32_t)kSmallThreads * u;
+            for (int u = 0; u < PER; ++u) {
+                const uint32_t j = base + gt + stride * u;
                 // the value is pinned in a register before the guarded store, so
                 // that the compiler does not sink the loads into the branch (where
                 // each would wait on its own)
@@ -455,20 +459,45 @@ __global__ __launch_bounds__(kSmallThreads) void decode_verify_small(
             uint64_t tot = 0;
 #pragma unroll
             for (int w = 0; w < NW; ++w) tot += red[w][tid];
-            fin[tid] = fred64(tot);
+            if (G == 1)
+                fin[tid] = fred64(tot);
+            else
+                atomicAdd(&acc[(size_t)b * 2 * ell + tid], (unsigned long long)fred64(tot));
         }
         __syncthreads();
-        if ((uint32_t)tid < ell) {
-            if (vL) vL[(size_t)tid * B + b] = fin[2 * tid];
-            if (vR) vR[(size_t)tid * B + b] = fin[2 * tid + 1];
+        if (G == 1) {
+            if ((uint32_t)tid < ell) {
+                if (vL) vL[(size_t)tid * B + b] = fin[2 * tid];
+                if (vR) vR[(size_t)tid * B + b] = fin[2 * tid + 1];
+            }
+            if (tid == 0) {
+                uint32_t ok = 1;
+                for (uint32_t q = 0; q < ell; ++q) ok &= fin[2 * q] == fin[2 * q + 1] ? 1u : 0u;
+                accept[b] = ok;
+            }
+            __syncthreads();  // fin is reused by the next column
         }
-        if (tid == 0) {
-            uint32_t ok = 1;
-            for (uint32_t q = 0; q < ell; ++q) ok &= fin[2 * q] == fin[2 * q + 1] ? 1u : 0u;
-            accept[b] = ok;
-        }
-        __syncthreads();  // red and fin are reused by the next column
     }
+    if (G == 1) return;
+    // several workgroups: the last one to finish reads and clears the
+    // accumulators (ordering as in decode_verify_fused)
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (tid == 0) last = (atomicAdd(counter, 1u) == G - 1) ? 1u : 0u;
+    __syncthreads();
+    if (!last) return;
+    for (uint32_t b = tid; b < B; b += kSmallThreads) {
+        uint32_t ok = 1;
+        for (uint32_t q = 0; q < ell; ++q) {
+            const uint32_t L = fred64(atomicExch(&acc[(size_t)b * 2 * ell + 2 * q], 0ull));
+            const uint32_t Rr = fred64(atomicExch(&acc[(size_t)b * 2 * ell + 2 * q + 1], 0ull));
+            if (vL) vL[(size_t)q * B + b] = L;
+            if (vR) vR[(size_t)q * B + b] = Rr;
+            ok &= (L == Rr) ? 1u : 0u;
+        }
+        accept[b] = ok;
+    }
+    if (tid == 0) atomicExch(counter, 0u);
 }
 
 template <int U>
@@ -551,12 +580,20 @@ hipError_t launch_decode_verify_masked(uint32_t m, uint32_t n, const uint32_t* X
                                        uint32_t* vL, uint32_t* vR, uint32_t* accept, hipStream_t s) {
     if (ell == 0 || ell > (uint32_t)kMaxEll) return hipErrorInvalidValue;
     if ((uint64_t)B * ((uint64_t)m + n) <= kSmallDvWords && ell <= 4) {
-        if (ell <= 2)
-            hipLaunchKernelGGL(decode_verify_small<2>, dim3(1), dim3(kSmallThreads), 0, s, m, n, Xhat, Yhat, B, My,
-                               ell, r, U, Y, vL, vR, accept);
-        else
-            hipLaunchKernelGGL(decode_verify_small<4>, dim3(1), dim3(kSmallThreads), 0, s, m, n, Xhat, Yhat, B, My,
-                               ell, r, U, Y, vL, vR, accept);
+        // one element per thread and pass over up to 8 workgroups, then 4
+        const uint32_t len = m > n ? m : n;
+        const bool one = len <= 8u * kSmallThreads;
+        uint32_t G = one ? ceil_div(len, kSmallThreads) : ceil_div(len, 4u * kSmallThreads);
+        G = G < 1u ? 1u : (G > 8u ? 8u : G);
+#define MVK_DVS(EL, PER)                                                                                   \
+    hipLaunchKernelGGL((decode_verify_small<EL, PER>), dim3(G), dim3(kSmallThreads), 0, s, m, n, Xhat, Yhat, B, \
+                       My, ell, r, U, Y, acc, counter, vL, vR, accept)
+        if (ell <= 2) {
+            if (one) MVK_DVS(2, 1); else MVK_DVS(2, 4);
+        } else {
+            if (one) MVK_DVS(4, 1); else MVK_DVS(4, 4);
+        }
+#undef MVK_DVS
         return hipGetLastError();
     }
     const uint32_t nblkL = ceil_div(n, kCols), nblkR = ceil_div(m, kCols);

@@ -64,9 +64,11 @@ def test_client_prepare_matches_oracle(cid, m, n, B, rx, ry, tx, ell):
     assert np.array_equal(host(prep.U), oracle.server_eval(np.ascontiguousarray(inst.W.T), R))
 
 
-# one-workgroup decode/verify (B * (m + n) <= 32768 and ell <= 4: ell 2 and
-# 3) and the multi-workgroup kernel (8 * 5000 words; ell = 7)
-MASKED = PREP[:2] + PREP[3:4] + [(86, 3000, 2000, 8, 2, 2, 16, 3), (87, 500, 400, 2, 2, 2, 9, 7)]
+# few-workgroup decode/verify (B * (m + n) <= 32768 and ell <= 4: one
+# workgroup, six with one element per thread, three with four, ell 2 and 3)
+# and the general kernel (8 * 5000 words; ell = 7)
+MASKED = PREP[:2] + PREP[3:4] + [(86, 3000, 2000, 8, 2, 2, 16, 3), (87, 500, 400, 2, 2, 2, 9, 7),
+                                 (88, 12000, 300, 2, 2, 2, 9, 2)]
 
 
 @pytest.mark.parametrize("cid,m,n,B,rx,ry,tx,ell", MASKED)

@@ -188,52 +188,63 @@ __global__ __launch_bounds__(kPrepThreads) void gather_rows_kernel(const uint32_
                        live, part + quarter * kQGroups);
 }
 
-// Xhat = X + Mx, element-wise over count words, kAddPer words per thread and
-// pass with the pass's loads issued first.  WAIT: first every workgroup waits
-// for *flag == value (thread 0 polls), then reads Mx device-coherently; the
-// flag is cleared by the only workgroup, or, with several, by the last one to
+// Xhat = X + Mx, element-wise over count words, PER words per thread and
+// pass with the pass's loads issued first.  WAIT: the loads of X (the query,
+// not covered by the flag) are issued before thread 0 of each workgroup
+// polls *flag for `value`; Mx is read device-coherently after it.  The flag
+// is cleared by the only workgroup, or, with several, by the last one to
 // finish (counted on `counter`, which it also clears).
 constexpr int kAddThreads = 1024;
-constexpr int kAddPer = 4;
-template <bool WAIT>
+template <bool WAIT, int PER>
 __global__ __launch_bounds__(kAddThreads) void add_masks(const uint32_t* X, const uint32_t* __restrict__ Mx,
                                                          size_t count, uint32_t* Xhat, uint32_t* flag, uint32_t value,
                                                          uint64_t ticks, uint32_t* timed_out, uint32_t* counter) {
-    if constexpr (WAIT) {
-        if (threadIdx.x == 0) {
-            if (!poll_flag(flag, value, ticks)) {
-                if (timed_out) atomicOr(timed_out, 1u);
-            } else if (gridDim.x == 1) {
-                __hip_atomic_store(flag, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-        }
-        __syncthreads();
-    }
-    constexpr size_t kPass = (size_t)kAddThreads * kAddPer;
-    for (size_t base = (size_t)blockIdx.x * kPass; base < count; base += (size_t)gridDim.x * kPass) {
-        uint32_t xv[kAddPer], mv[kAddPer];
+    const size_t stride = (size_t)gridDim.x * kAddThreads, pass = stride * PER;
+    const size_t g = (size_t)blockIdx.x * kAddThreads + threadIdx.x;
+    bool polled = !WAIT;
+    for (size_t base = 0; base < count; base += pass) {
+        uint32_t xv[PER], mv[PER];
 #pragma unroll
-        for (int u = 0; u < kAddPer; ++u) {
-            const size_t i = base + threadIdx.x + (size_t)kAddThreads * u;
-            const size_t is = i < count ? i : count - 1;
-            xv[u] = X[is];
+        for (int u = 0; u < PER; ++u) {
+            const size_t i = base + g + stride * u;
+            xv[u] = X[i < count ? i : count - 1];
+        }
+        if (WAIT && !polled) {  // first pass only (uniform)
+            if (threadIdx.x == 0) {
+                if (!poll_flag(flag, value, ticks)) {
+                    if (timed_out) atomicOr(timed_out, 1u);
+                } else if (gridDim.x == 1) {
+                    __hip_atomic_store(flag, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+            }
+            __syncthreads();
+            polled = true;
+        }
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+            const size_t i = base + g + stride * u, is = i < count ? i : count - 1;
             mv[u] = WAIT ? __hip_atomic_load(&Mx[is], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : Mx[is];
         }
-        uint32_t out[kAddPer];
+        uint32_t out[PER];
 #pragma unroll
-        for (int u = 0; u < kAddPer; ++u) {
+        for (int u = 0; u < PER; ++u) {
             out[u] = fadd(xv[u], mv[u]);
             // pinned in a register before the guarded store, so that the
             // compiler does not sink the loads into the branch
             asm volatile("" : "+v"(out[u]));
         }
 #pragma unroll
-        for (int u = 0; u < kAddPer; ++u) {
-            const size_t i = base + threadIdx.x + (size_t)kAddThreads * u;
+        for (int u = 0; u < PER; ++u) {
+            const size_t i = base + g + stride * u;
             if (i < count) Xhat[i] = out[u];
         }
     }
     if constexpr (WAIT) {
+        if (!polled) {  // no pass at all (count == 0): still consume the flag
+            if (threadIdx.x == 0 && !poll_flag(flag, value, ticks) && timed_out) atomicOr(timed_out, 1u);
+            if (threadIdx.x == 0 && gridDim.x == 1)
+                __hip_atomic_store(flag, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
         if (gridDim.x > 1 && threadIdx.x == 0 && atomicAdd(counter, 1u) == gridDim.x - 1) {
             atomicExch(counter, 0u);
             __hip_atomic_store(flag, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -343,20 +354,25 @@ hipError_t launch_add_masks(const uint32_t* X, const uint32_t* Mx, size_t count,
                             uint32_t value, uint32_t timeout_us, uint32_t* timed_out, uint32_t* counter,
                             hipStream_t s) {
     if (count == 0 && !flag) return hipSuccess;
-    const size_t pass = (size_t)kAddThreads * kAddPer;
-    size_t blocks = (count + pass - 1) / pass;
+    // one word per thread over up to 8 workgroups; beyond, four per thread
+    const bool one = count <= 8u * kAddThreads;
+    size_t blocks = one ? (count + kAddThreads - 1) / kAddThreads : (count + 4u * kAddThreads - 1) / (4u * kAddThreads);
     if (blocks > 256) blocks = 256;
     if (blocks == 0) blocks = 1;
+    uint64_t ticks = 0;
     if (flag) {
-        uint64_t ticks = 0;
         const hipError_t e = wait_ticks(timeout_us, &ticks);
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(add_masks<true>, dim3((uint32_t)blocks), dim3(kAddThreads), 0, s, X, Mx, count, Xhat,
-                           flag, value, ticks, timed_out, counter);
-    } else {
-        hipLaunchKernelGGL(add_masks<false>, dim3((uint32_t)blocks), dim3(kAddThreads), 0, s, X, Mx, count, Xhat,
-                           nullptr, 0u, (uint64_t)0, nullptr, nullptr);
     }
+#define MVK_ADD(W, P)                                                                                          \
+    hipLaunchKernelGGL((add_masks<W, P>), dim3((uint32_t)blocks), dim3(kAddThreads), 0, s, X, Mx, count, Xhat, flag, \
+                       value, ticks, timed_out, counter)
+    if (flag) {
+        if (one) MVK_ADD(true, 1); else MVK_ADD(true, 4);
+    } else {
+        if (one) MVK_ADD(false, 1); else MVK_ADD(false, 4);
+    }
+#undef MVK_ADD
     return hipGetLastError();
 }
 

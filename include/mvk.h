@@ -3,8 +3,12 @@
  * of private and verifiable matrix-vector multiplication delegation (pvMVMD,
  * "Maverick", arxiv 2609.10264).
  *
- * Field: F_p with p = 2^31 - 1.  A "field array" is uint32 in canonical form
- * [0, p).  The public matrix W is int8 (each entry w is the field element
+ * Field: F_p.  Two builds of the same sources implement this ABI, one per
+ * field: libmvk.so over p = 2^31 - 1 (MVK_PRIME) and libmvk_bb.so over the
+ * BabyBear prime q = 15 * 2^27 + 1 (MVK_PRIME_BABYBEAR), the field of the
+ * paper's evaluation (Sec. 7.1).  mvk_field_modulus() names the build's p;
+ * everything below holds for either.  A "field array" is uint32 in canonical
+ * form [0, p).  The public matrix W is int8 (each entry w is the field element
  * w mod p; Sec. 7.2 embeds quantised signed integers into the field).
  *
  * Conventions shared by every call
@@ -37,7 +41,8 @@ extern "C" {
 #endif
 
 #define MVK_PRIME 2147483647u
-#define MVK_ABI_VERSION 4
+#define MVK_PRIME_BABYBEAR 2013265921u
+#define MVK_ABI_VERSION 5
 
 typedef int32_t mvk_status;
 #define MVK_OK 0
@@ -100,6 +105,9 @@ const char *mvk_status_str(mvk_status s);
 
 /* MVK_ABI_VERSION of the loaded library. */
 int32_t mvk_abi_version(void);
+
+/* The prime p of the loaded build: MVK_PRIME or MVK_PRIME_BABYBEAR. */
+uint32_t mvk_field_modulus(void);
 
 /*
  * Server evaluation (Protocol pvMVMD: the server's only work is the field

@@ -5,7 +5,10 @@ baseline leg are the only callers.  The product library shares no code with
 this package and never imports it.
 
 The arithmetic lives in ``mvk_oracle.c`` (plain C, '%' on uint64); this module
-only builds it with gcc, loads it with ctypes and marshals numpy arrays.  The
+only builds it with gcc, loads it with ctypes and marshals numpy arrays.  The C
+file is built once per field (``-DORC_P``): p = 2^31 - 1 (``P``, the default
+of every function) and the BabyBear prime 15 * 2^27 + 1 (``P_BABYBEAR``, the
+field of Sec. 7.1); every function takes the field as its ``p`` argument.  The
 parameter helpers below restate the paper's formulas (Eq. (1) and Theorem 6.1).
 
 Parity status per function:
@@ -34,28 +37,32 @@ import threading
 import numpy as np
 
 P = 2**31 - 1
+P_BABYBEAR = 15 * 2**27 + 1
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "mvk_oracle.c")
-_LIB = os.path.join(_HERE, "libmvk_oracle.so")
+_LIBS = {P: os.path.join(_HERE, "libmvk_oracle.so"), P_BABYBEAR: os.path.join(_HERE, "libmvk_oracle_bb.so")}
 _lock = threading.Lock()
-_lib = None
+_lib = {}
 
 
-def build(force: bool = False) -> str:
-    """Compile the oracle with gcc (no GPU code involved)."""
-    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
-        tmp = _LIB + ".tmp%d" % os.getpid()
-        subprocess.check_call(["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-o", tmp, _SRC])
-        os.replace(tmp, _LIB)
-    return _LIB
+def build(force: bool = False) -> list:
+    """Compile the oracle with gcc, once per field (no GPU code involved)."""
+    for p, path in _LIBS.items():
+        if force or not os.path.exists(path) or os.path.getmtime(path) < os.path.getmtime(_SRC):
+            tmp = path + ".tmp%d" % os.getpid()
+            subprocess.check_call(["gcc", "-O2", "-std=c99", "-fPIC", "-shared", f"-DORC_P={p}ULL", "-o", tmp,
+                                   _SRC])
+            os.replace(tmp, path)
+    return list(_LIBS.values())
 
 
-def lib():
-    global _lib
+def lib(p: int = P):
     with _lock:
-        if _lib is None:
+        if p not in _lib:
+            if p not in _LIBS:
+                raise ValueError(f"no oracle build over p = {p}")
             build()
-            L = ctypes.CDLL(_LIB)
+            L = ctypes.CDLL(_LIBS[p])
             u32p = ctypes.POINTER(ctypes.c_uint32)
             i8p = ctypes.POINTER(ctypes.c_int8)
             u8p = ctypes.POINTER(ctypes.c_uint8)
@@ -76,8 +83,9 @@ def lib():
             L.orc_verify.argtypes = [u32, u32, u32, u32p, u32p, u32p, u32p, u32p, u32p, u32p, u32,
                                      u32p, u32p, u32, u32, u32p, u32p, u8p]
             L.orc_prime.restype = u32
-            _lib = L
-    return _lib
+            assert L.orc_prime() == p
+            _lib[p] = L
+    return _lib[p]
 
 
 def _u32(a) -> np.ndarray:
@@ -99,32 +107,32 @@ def _code_args(code):
 # ---------------------------------------------------------------------------
 # RAA code maps (App. B)
 # ---------------------------------------------------------------------------
-def encT(code: dict, w) -> np.ndarray:
+def encT(code: dict, w, p: int = P) -> np.ndarray:
     """G^T w for w in F^k (App. B, linear-time encoding)."""
     k, r = code["k"], code["r"]
     w = _u32(w)
     assert w.shape == (k,)
     c = _code_args(code)
     out = np.empty(k * r, dtype=np.uint32)
-    lib().orc_encT(k, r, *[_p(a) for a in c], _p(w), _p(out))
+    lib(p).orc_encT(k, r, *[_p(a) for a in c], _p(w), _p(out))
     return out
 
 
-def syn(code: dict, v) -> np.ndarray:
+def syn(code: dict, v, p: int = P) -> np.ndarray:
     """G v for v in F^N (App. B, syndrome by the transposition principle)."""
     k, r = code["k"], code["r"]
     v = _u32(v)
     assert v.shape == (k * r,)
     c = _code_args(code)
     out = np.empty(k, dtype=np.uint32)
-    lib().orc_syn(k, r, *[_p(a) for a in c], _p(v), _p(out))
+    lib(p).orc_syn(k, r, *[_p(a) for a in c], _p(v), _p(out))
     return out
 
 
 # ---------------------------------------------------------------------------
 # Protocol pvMVMD
 # ---------------------------------------------------------------------------
-def server_eval(W, Xhat, rows=None) -> np.ndarray:
+def server_eval(W, Xhat, rows=None, p: int = P) -> np.ndarray:
     """Yhat = W Xhat mod p; W int8 m x n, Xhat uint32 B x n -> uint32 B x m.
 
     ``rows`` = (row0, row1) restricts the computation to a row range (other
@@ -137,13 +145,13 @@ def server_eval(W, Xhat, rows=None) -> np.ndarray:
     assert Xhat.shape == (B, n)
     Y = np.zeros((B, m), dtype=np.uint32)
     if rows is None:
-        lib().orc_server_eval(_p(W, ctypes.c_int8), m, n, _p(Xhat), B, _p(Y))
+        lib(p).orc_server_eval(_p(W, ctypes.c_int8), m, n, _p(Xhat), B, _p(Y))
     else:
-        lib().orc_server_eval_rows(_p(W, ctypes.c_int8), m, n, _p(Xhat), B, _p(Y), int(rows[0]), int(rows[1]))
+        lib(p).orc_server_eval_rows(_p(W, ctypes.c_int8), m, n, _p(Xhat), B, _p(Y), int(rows[0]), int(rows[1]))
     return Y
 
 
-def keygen(W, cx: dict, cy: dict, want_P: bool = True, want_Q: bool = True):
+def keygen(W, cx: dict, cy: dict, want_P: bool = True, want_Q: bool = True, p: int = P):
     """Preprocess: returns (PT, Q) with PT = (W Gx)^T (Nx x m), Q = Gy^T W (Ny x n)."""
     W = np.ascontiguousarray(W, dtype=np.int8)
     m, n = W.shape
@@ -152,12 +160,12 @@ def keygen(W, cx: dict, cy: dict, want_P: bool = True, want_Q: bool = True):
     Q = np.empty((cy["N"], n), dtype=np.uint32) if want_Q else None
     ax = _code_args(cx)
     ay = _code_args(cy)
-    lib().orc_keygen(_p(W, ctypes.c_int8), m, n, cx["r"], *[_p(a) for a in ax],
+    lib(p).orc_keygen(_p(W, ctypes.c_int8), m, n, cx["r"], *[_p(a) for a in ax],
                      cy["r"], *[_p(a) for a in ay], _p(PT), _p(Q))
     return PT, Q
 
 
-def encode(cx: dict, X, ex_idx, ex_val) -> np.ndarray:
+def encode(cx: dict, X, ex_idx, ex_val, p: int = P) -> np.ndarray:
     """Encrypt: Xhat = X + Gx e_x (per column); X uint32 B x n."""
     X = _u32(np.atleast_2d(X))
     B, n = X.shape
@@ -168,11 +176,11 @@ def encode(cx: dict, X, ex_idx, ex_val) -> np.ndarray:
     assert ex_idx.shape == (B, tx) and ex_val.shape == (B, tx)
     Xhat = np.empty_like(X)
     a = _code_args(cx)
-    lib().orc_encode(n, cx["r"], *[_p(x) for x in a], _p(X), B, _p(ex_idx), _p(ex_val), tx, _p(Xhat))
+    lib(p).orc_encode(n, cx["r"], *[_p(x) for x in a], _p(X), B, _p(ex_idx), _p(ex_val), tx, _p(Xhat))
     return Xhat
 
 
-def decode(PT, Yhat, ex_idx, ex_val) -> np.ndarray:
+def decode(PT, Yhat, ex_idx, ex_val, p: int = P) -> np.ndarray:
     """Decrypt: Y = Yhat - P e_x."""
     PT = _u32(PT)
     Yhat = _u32(np.atleast_2d(Yhat))
@@ -183,11 +191,11 @@ def decode(PT, Yhat, ex_idx, ex_val) -> np.ndarray:
     tx = ex_idx.shape[1]
     assert int(ex_idx.max(initial=0)) < PT.shape[0]
     Y = np.empty_like(Yhat)
-    lib().orc_decode(_p(PT), m, _p(Yhat), B, _p(ex_idx), _p(ex_val), tx, _p(Y))
+    lib(p).orc_decode(_p(PT), m, _p(Yhat), B, _p(ex_idx), _p(ex_val), tx, _p(Y))
     return Y
 
 
-def verify(cy: dict, Q, Xhat, Yhat, ey_idx, ey_val):
+def verify(cy: dict, Q, Xhat, Yhat, ey_idx, ey_val, p: int = P):
     """Verify: returns (accept[B] bool, vL[ell, B], vR[ell, B])."""
     Q = _u32(Q)
     Xhat = _u32(np.atleast_2d(Xhat))
@@ -202,7 +210,7 @@ def verify(cy: dict, Q, Xhat, Yhat, ey_idx, ey_val):
     vR = np.empty((ell, B), dtype=np.uint32)
     acc = np.empty(B, dtype=np.uint8)
     a = _code_args(cy)
-    lib().orc_verify(m, n, cy["r"], *[_p(x) for x in a], _p(Q), _p(Xhat), _p(Yhat), B,
+    lib(p).orc_verify(m, n, cy["r"], *[_p(x) for x in a], _p(Q), _p(Xhat), _p(Yhat), B,
                      _p(ey_idx), _p(ey_val), ty, ell, _p(vL), _p(vR), _p(acc, ctypes.c_uint8))
     return acc.astype(bool), vL, vR
 
@@ -210,18 +218,18 @@ def verify(cy: dict, Q, Xhat, Yhat, ey_idx, ey_val):
 # ---------------------------------------------------------------------------
 # Protocol Batch-vMVMD (Sec. 5.4)
 # ---------------------------------------------------------------------------
-def batch_aux(Qs, c2: dict) -> np.ndarray:
+def batch_aux(Qs, c2: dict, p: int = P) -> np.ndarray:
     """Preprocess: Qaux = Qt^T G' (N x N') for Qs = [Q_1, ..., Q_B] (B x N x n)."""
     Qs = _u32(Qs)
     B, N, n = Qs.shape
     assert c2["k"] == B * n
     a = _code_args(c2)
     out = np.empty((N, c2["N"]), dtype=np.uint32)
-    lib().orc_batch_aux(B, N, n, _p(Qs), c2["r"], *[_p(x) for x in a], _p(out))
+    lib(p).orc_batch_aux(B, N, n, _p(Qs), c2["r"], *[_p(x) for x in a], _p(out))
     return out
 
 
-def batch_project(Qs, e_idx, e_val) -> np.ndarray:
+def batch_project(Qs, e_idx, e_val, p: int = P) -> np.ndarray:
     """Server step: u~(q) = Qt e(q) (ell x Bn)."""
     Qs = _u32(Qs)
     B, N, n = Qs.shape
@@ -230,11 +238,11 @@ def batch_project(Qs, e_idx, e_val) -> np.ndarray:
     ell, t = e_idx.shape
     assert int(e_idx.max(initial=0)) < N
     out = np.empty((ell, B * n), dtype=np.uint32)
-    lib().orc_batch_project(B, N, n, _p(Qs), _p(e_idx), _p(e_val), t, ell, _p(out))
+    lib(p).orc_batch_project(B, N, n, _p(Qs), _p(e_idx), _p(e_val), t, ell, _p(out))
     return out
 
 
-def batch_verify(cy: dict, c2: dict, Qaux, X, Y, e_idx, e_val, ut, e2_idx, e2_val):
+def batch_verify(cy: dict, c2: dict, Qaux, X, Y, e_idx, e_val, ut, e2_idx, e2_val, p: int = P):
     """Client checks.  Returns (accept[B] bool, batch_ok bool, vL, vR (ell x B),
     sL, sR (ell x ell2)); claim b is accepted iff every secondary check of the
     batch and every original check of b passes."""
@@ -256,7 +264,7 @@ def batch_verify(cy: dict, c2: dict, Qaux, X, Y, e_idx, e_val, ut, e2_idx, e2_va
     sL = np.empty((ell, ell2), dtype=np.uint32)
     sR = np.empty((ell, ell2), dtype=np.uint32)
     a, a2 = _code_args(cy), _code_args(c2)
-    lib().orc_batch_verify(m, n, B, cy["r"], *[_p(x) for x in a], c2["r"], *[_p(x) for x in a2], _p(Qaux),
+    lib(p).orc_batch_verify(m, n, B, cy["r"], *[_p(x) for x in a], c2["r"], *[_p(x) for x in a2], _p(Qaux),
                            _p(X), _p(Y), _p(e_idx), _p(e_val), t, ell, _p(ut), _p(e2_idx), _p(e2_val), t2, ell2,
                            _p(vL), _p(vR), _p(sL), _p(sR))
     batch_ok = bool((sL == sR).all())

@@ -9,7 +9,11 @@
  * '%' operator on 64-bit unsigned integers; nothing is blocked, fused or
  * reordered beyond what the paper's definitions state.  Indices are 0-based.
  *
- * Field: F_p with p = 2^31 - 1.  Field arrays are uint32 in [0, p).
+ * Field: F_p, p fixed when the file is compiled: 2^31 - 1 by default, or the
+ * BabyBear prime 15 * 2^27 + 1 (the field of the paper's Sec. 7.1) with
+ * -DORC_P=2013265921.  Any prime below 2^31 works: every product of two
+ * field elements and every sum of two fits in 64 bits before its '%'.
+ * Field arrays are uint32 in [0, p).
  * Signed int8 weights are embedded as w mod p (Sec. 7.2, "Model quantization":
  * signed integers are embedded into the field).
  *
@@ -40,7 +44,9 @@
 #include <stdlib.h>
 #include <string.h>
 
+#ifndef ORC_P
 #define ORC_P 2147483647ULL
+#endif
 
 static uint64_t fadd(uint64_t a, uint64_t b) { return (a + b) % ORC_P; }
 static uint64_t fsub(uint64_t a, uint64_t b) { return (a + ORC_P - b) % ORC_P; }

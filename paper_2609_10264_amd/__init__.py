@@ -4,10 +4,13 @@ matrix-vector multiplication delegation (pvMVMD, Maverick, arxiv 2609.10264).
 Thin Python binding over the C ABI in include/mvk.h: every function only
 checks tensor shapes/dtypes, passes raw device pointers and the current HIP
 stream, and raises on a non-zero status.  All computation runs in the HIP
-kernels of libmvk.so; there is no CPU fallback.
+kernels of libmvk.so (p = 2^31 - 1) or libmvk_bb.so (BabyBear, p = 15 * 2^27 + 1);
+there is no CPU fallback.
 
-Tensors: field arrays are torch.int32 on the GPU holding canonical values in
-[0, p), p = 2^31 - 1 (these fit a non-negative int32); W is torch.int8.
+Field: every code carries its prime p (P or P_BABYBEAR) and every call runs
+in the library built over the p of its codes (or of its `p` argument where no
+code is passed).  Tensors: field arrays are torch.int32 on the GPU holding
+canonical values in [0, p) (these fit a non-negative int32); W is torch.int8.
 """
 from __future__ import annotations
 
@@ -17,16 +20,18 @@ from dataclasses import dataclass
 import torch
 
 from . import _lib
-from ._lib import MVK_MAX_N, MVK_PRIME, MvkCode, MvkError, MvkKey, MvkSparse
+from ._lib import MVK_MAX_N, MVK_PRIME, MVK_PRIME_BABYBEAR, MvkCode, MvkError, MvkKey, MvkSparse
 
 P = MVK_PRIME
+P_BABYBEAR = MVK_PRIME_BABYBEAR
+FIELDS = {"m31": P, "babybear": P_BABYBEAR}
 
-__all__ = ["P", "MVK_MAX_N", "MvkError", "Code", "Key", "PackedW", "pack_weights", "server_eval", "keygen", "encode",
+__all__ = ["P", "P_BABYBEAR", "FIELDS", "MVK_MAX_N", "MvkError", "Code", "Key", "PackedW", "pack_weights", "server_eval", "keygen", "encode",
            "decode_verify", "verify_prepare", "raa_encode", "raa_syndrome", "library_path"]
 
 
-def library_path() -> str:
-    return _lib.LIB_PATH
+def library_path(p: int = P) -> str:
+    return _lib.LIB_PATHS[p]
 
 
 def _stream(stream) -> ctypes.c_void_p:
@@ -56,16 +61,17 @@ class Code:
     pi2: torch.Tensor
     v1: torch.Tensor
     v2: torch.Tensor
+    p: int = P  # the field the diagonals (and everything coded with it) live in
 
     @property
     def N(self) -> int:
         return self.k * self.r
 
     @classmethod
-    def from_arrays(cls, k, r, pi1, pi2, v1, v2, device="cuda") -> "Code":
+    def from_arrays(cls, k, r, pi1, pi2, v1, v2, device="cuda", p: int = P) -> "Code":
         def t(a):
             return torch.as_tensor(a).to(torch.int64).to(torch.int32).to(device).contiguous()
-        return cls(int(k), int(r), t(pi1), t(pi2), t(v1), t(v2))
+        return cls(int(k), int(r), t(pi1), t(pi2), t(v1), t(v2), int(p))
 
     def struct(self) -> MvkCode:
         N = self.N
@@ -84,8 +90,14 @@ class Key:
     PT: torch.Tensor  # Nx x m
     Q: torch.Tensor   # Ny x n
 
+    @property
+    def p(self) -> int:
+        return self.cx.p
+
     @classmethod
     def allocate(cls, m: int, n: int, cx: Code, cy: Code, device="cuda") -> "Key":
+        if cx.p != cy.p:
+            raise ValueError("the two codes of a key must be over one field")
         PT = torch.empty((cx.N, m), dtype=torch.int32, device=device)
         Q = torch.empty((cy.N, n), dtype=torch.int32, device=device)
         return cls(int(m), int(n), cx, cy, PT, Q)
@@ -138,7 +150,7 @@ def pack_weights(W: torch.Tensor, out: torch.Tensor | None = None, stream=None) 
 
 
 def server_eval(W, Xhat: torch.Tensor, out: torch.Tensor | None = None, stream=None,
-                path: str = "auto") -> torch.Tensor:
+                path: str = "auto", p: int = P) -> torch.Tensor:
     """Yhat = W Xhat mod p.  W: m x n int8 (or a PackedW); Xhat: B x n int32 field; returns B x m.
 
     path selects the kernel family ("auto", "valu" or "mfma"); results are identical.
@@ -147,7 +159,7 @@ def server_eval(W, Xhat: torch.Tensor, out: torch.Tensor | None = None, stream=N
     B = Xhat.shape[0]
     if out is None:
         out = torch.empty((B, m), dtype=torch.int32, device=W.device)
-    L = _lib.load()
+    L = _lib.load(p)
     tail = (m, n, _dev(Xhat, torch.int32, (B, n), "Xhat"), B, _dev(out, torch.int32, (B, m), "Yhat"))
     if isinstance(W, PackedW):
         if path == "valu":
@@ -166,7 +178,7 @@ def keygen(key: Key, W: torch.Tensor, stream=None) -> Key:
     """Preprocess: fills key.PT = (W Gx)^T and key.Q = Gy^T W."""
     _dev(W, torch.int8, (key.m, key.n), "W")
     ks = key.struct()
-    _lib.check("mvk_keygen", _lib.load().mvk_keygen(ctypes.byref(ks), W.data_ptr(), _stream(stream)))
+    _lib.check("mvk_keygen", _lib.load(key.p).mvk_keygen(ctypes.byref(ks), W.data_ptr(), _stream(stream)))
     return key
 
 
@@ -178,7 +190,7 @@ def encode(key: Key, X: torch.Tensor, ex_idx: torch.Tensor, ex_val: torch.Tensor
         out = torch.empty_like(X)
     ks = key.struct()
     ex = _sparse(ex_idx, ex_val, "ex")
-    _lib.check("mvk_encode", _lib.load().mvk_encode(
+    _lib.check("mvk_encode", _lib.load(key.p).mvk_encode(
         ctypes.byref(ks), _dev(X, torch.int32, (B, key.n), "X"), B, ctypes.byref(ex),
         _dev(out, torch.int32, (B, key.n), "Xhat"), _stream(stream)))
     return out
@@ -192,7 +204,7 @@ def verify_prepare(key: Key, ey_idx: torch.Tensor, ey_val: torch.Tensor, R: torc
         R = torch.empty((ell, key.m), dtype=torch.int32, device=ey_idx.device)
     ks = key.struct()
     ey = _sparse(ey_idx, ey_val, "ey")
-    _lib.check("mvk_verify_prepare", _lib.load().mvk_verify_prepare(
+    _lib.check("mvk_verify_prepare", _lib.load(key.p).mvk_verify_prepare(
         ctypes.byref(ks), ctypes.byref(ey), _dev(R, torch.int32, (ell, key.m), "R"), _stream(stream)))
     return R
 
@@ -222,9 +234,9 @@ def decode_verify(key: Key, Xhat: torch.Tensor, Yhat: torch.Tensor, ex_idx: torc
     outs = (_dev(Y, torch.int32, (B, key.m), "Y"), vLp, vRp, _dev(accept, torch.int32, (B,), "accept"),
             _stream(stream))
     if R is None:
-        _lib.check("mvk_decode_verify", _lib.load().mvk_decode_verify(ctypes.byref(ks), *common, *outs))
+        _lib.check("mvk_decode_verify", _lib.load(key.p).mvk_decode_verify(ctypes.byref(ks), *common, *outs))
     else:
-        _lib.check("mvk_decode_verify_prepared", _lib.load().mvk_decode_verify_prepared(
+        _lib.check("mvk_decode_verify_prepared", _lib.load(key.p).mvk_decode_verify_prepared(
             ctypes.byref(ks), *common, _dev(R, torch.int32, (ell, key.m), "R"), *outs))
     return Y, accept, vL, vR
 
@@ -256,7 +268,7 @@ def client_prepare(key: Key, ex_idx: torch.Tensor, ex_val: torch.Tensor, ey_idx:
     ks = key.struct()
     ex = _sparse(ex_idx, ex_val, "ex")
     ey = _sparse(ey_idx, ey_val, "ey")
-    _lib.check("mvk_client_prepare", _lib.load().mvk_client_prepare(
+    _lib.check("mvk_client_prepare", _lib.load(key.p).mvk_client_prepare(
         ctypes.byref(ks), ctypes.byref(ex), ctypes.byref(ey),
         _dev(out.Mx, torch.int32, (B, key.n), "Mx"), _dev(out.My, torch.int32, (B, key.m), "My"),
         _dev(out.R, torch.int32, (ell, key.m), "R"), _dev(out.U, torch.int32, (ell, key.n), "U"),
@@ -274,7 +286,7 @@ def encode_masked(key: Key, X: torch.Tensor, prep: Prepared, out: torch.Tensor |
     if out is None:
         out = torch.empty_like(X)
     ks = key.struct()
-    _lib.check("mvk_encode_masked", _lib.load().mvk_encode_masked(
+    _lib.check("mvk_encode_masked", _lib.load(key.p).mvk_encode_masked(
         ctypes.byref(ks), _dev(X, torch.int32, (B, key.n), "X"), B,
         _dev(prep.Mx, torch.int32, (B, key.n), "Mx"), _dev(out, torch.int32, (B, key.n), "Xhat"),
         _dev(ready_flag, torch.int32, (), "ready_flag") if ready_flag is not None else None, ready_value,
@@ -296,7 +308,7 @@ def decode_verify_masked(key: Key, Xhat: torch.Tensor, Yhat: torch.Tensor, prep:
     ks = key.struct()
     vLp = _dev(vL, torch.int32, (ell, B), "vL") if vL is not None else None
     vRp = _dev(vR, torch.int32, (ell, B), "vR") if vR is not None else None
-    _lib.check("mvk_decode_verify_masked", _lib.load().mvk_decode_verify_masked(
+    _lib.check("mvk_decode_verify_masked", _lib.load(key.p).mvk_decode_verify_masked(
         ctypes.byref(ks), _dev(Xhat, torch.int32, (B, key.n), "Xhat"), _dev(Yhat, torch.int32, (B, key.m), "Yhat"),
         B, _dev(prep.My, torch.int32, (B, key.m), "My"), ell, _dev(prep.R, torch.int32, (ell, key.m), "R"),
         _dev(prep.U, torch.int32, (ell, key.n), "U"), _dev(Y, torch.int32, (B, key.m), "Y"), vLp, vRp,
@@ -328,7 +340,7 @@ def verify(key: Key, X: torch.Tensor, Y: torch.Tensor, ey_idx: torch.Tensor, ey_
         accept = torch.empty((B,), dtype=torch.int32, device=X.device)
     ks = key.struct()
     ey = _sparse(ey_idx, ey_val, "ey")
-    _lib.check("mvk_verify", _lib.load().mvk_verify(
+    _lib.check("mvk_verify", _lib.load(key.p).mvk_verify(
         ctypes.byref(ks), _dev(X, torch.int32, (B, key.n), "X"), _dev(Y, torch.int32, (B, key.m), "Y"), B,
         ctypes.byref(ey), _dev(vL, torch.int32, (ell, B), "vL") if vL is not None else None,
         _dev(vR, torch.int32, (ell, B), "vR") if vR is not None else None,
@@ -346,13 +358,13 @@ def batch_preprocess(Qs: list, c2: Code, stream=None):
     QtT = torch.empty((N, B * n), dtype=torch.int32, device=dev)
     Qaux = torch.empty((N, c2.N), dtype=torch.int32, device=dev)
     cs = c2.struct()
-    _lib.check("mvk_batch_preprocess", _lib.load().mvk_batch_preprocess(
+    _lib.check("mvk_batch_preprocess", _lib.load(c2.p).mvk_batch_preprocess(
         B, ptrs, N, n, ctypes.byref(cs), QtT.data_ptr(), Qaux.data_ptr(), _stream(stream)))
     return QtT, Qaux
 
 
 def batch_project(QtT: torch.Tensor, n: int, e_idx: torch.Tensor, e_val: torch.Tensor,
-                  out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+                  out: torch.Tensor | None = None, stream=None, p: int = P) -> torch.Tensor:
     """Batch verification, server step: Ut[q] = Qt e_q (ell x Bn)."""
     N, Bn = QtT.shape
     B = Bn // n
@@ -360,7 +372,7 @@ def batch_project(QtT: torch.Tensor, n: int, e_idx: torch.Tensor, e_val: torch.T
     if out is None:
         out = torch.empty((ell, Bn), dtype=torch.int32, device=QtT.device)
     e = _sparse(e_idx, e_val, "e")
-    _lib.check("mvk_batch_project", _lib.load().mvk_batch_project(
+    _lib.check("mvk_batch_project", _lib.load(p).mvk_batch_project(
         _dev(QtT, torch.int32, (N, Bn), "QtT"), N, n, B, ctypes.byref(e),
         _dev(out, torch.int32, (ell, Bn), "Ut"), _stream(stream)))
     return out
@@ -375,10 +387,12 @@ def batch_verify(cy: Code, c2: Code, Qaux: torch.Tensor, X: torch.Tensor, Y: tor
     ell, ell2 = e_idx.shape[0], e2_idx.shape[0]
     if accept is None:
         accept = torch.empty((B,), dtype=torch.int32, device=X.device)
+    if cy.p != c2.p:
+        raise ValueError("the two codes must be over one field")
     c1s, c2s = cy.struct(), c2.struct()
     e, e2 = _sparse(e_idx, e_val, "e"), _sparse(e2_idx, e2_val, "e2")
     opt = lambda t, shape, name: _dev(t, torch.int32, shape, name) if t is not None else None  # noqa: E731
-    _lib.check("mvk_batch_verify", _lib.load().mvk_batch_verify(
+    _lib.check("mvk_batch_verify", _lib.load(cy.p).mvk_batch_verify(
         ctypes.byref(c1s), ctypes.byref(c2s), _dev(Qaux, torch.int32, (cy.N, c2.N), "Qaux"), m, n, B,
         _dev(X, torch.int32, (B, n), "X"), _dev(Y, torch.int32, (B, m), "Y"), ctypes.byref(e),
         _dev(Ut, torch.int32, (ell, B * n), "Ut"), ctypes.byref(e2), opt(vL, (ell, B), "vL"), opt(vR, (ell, B), "vR"),
@@ -394,7 +408,7 @@ def raa_encode(code: Code, w: torch.Tensor, out: torch.Tensor | None = None, str
     if out is None:
         out = torch.empty((count, code.N), dtype=torch.int32, device=w.device)
     cs = code.struct()
-    _lib.check("mvk_raa_encode", _lib.load().mvk_raa_encode(
+    _lib.check("mvk_raa_encode", _lib.load(code.p).mvk_raa_encode(
         ctypes.byref(cs), _dev(w2, torch.int32, (count, code.k), "w"), count,
         _dev(out, torch.int32, (count, code.N), "out"), _stream(stream)))
     return out
@@ -407,7 +421,7 @@ def raa_syndrome(code: Code, v: torch.Tensor, out: torch.Tensor | None = None, s
     if out is None:
         out = torch.empty((count, code.k), dtype=torch.int32, device=v.device)
     cs = code.struct()
-    _lib.check("mvk_raa_syndrome", _lib.load().mvk_raa_syndrome(
+    _lib.check("mvk_raa_syndrome", _lib.load(code.p).mvk_raa_syndrome(
         ctypes.byref(cs), _dev(v2, torch.int32, (count, code.N), "v"), count,
         _dev(out, torch.int32, (count, code.k), "out"), _stream(stream)))
     return out

@@ -1,4 +1,5 @@
-"""ctypes loader and C struct layouts for libmvk.so (include/mvk.h)."""
+"""ctypes loader and C struct layouts for the libraries behind include/mvk.h:
+libmvk.so (p = 2^31 - 1) and libmvk_bb.so (BabyBear, p = 15 * 2^27 + 1)."""
 from __future__ import annotations
 
 import ctypes
@@ -6,6 +7,7 @@ import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libmvk.so")
+LIB_PATH_BB = os.path.join(_HERE, "libmvk_bb.so")
 
 MVK_OK = 0
 MVK_EINVAL = -1
@@ -13,16 +15,20 @@ MVK_ERANGE = -2
 MVK_ENOMEM = -3
 MVK_EHIP = -4
 MVK_PRIME = 2147483647
+MVK_PRIME_BABYBEAR = 2013265921
 MVK_MAX_N = 131071
 MVK_PATH_AUTO = 0
 MVK_PATH_VALU = 1
 MVK_PATH_MFMA = 2
-ABI_VERSION = 4
+ABI_VERSION = 5
+# field modulus -> library built over that field
+LIB_PATHS = {MVK_PRIME: LIB_PATH, MVK_PRIME_BABYBEAR: LIB_PATH_BB}
 
 # Every symbol include/mvk.h declares.
 EXPORTS = (
     "mvk_status_str",
     "mvk_abi_version",
+    "mvk_field_modulus",
     "mvk_server_eval",
     "mvk_server_eval_path",
     "mvk_packed_weight_bytes",
@@ -84,18 +90,21 @@ class MvkError(RuntimeError):
         self.status = status
 
 
-_lib = None
+_libs: dict = {}
 
 
-def load() -> ctypes.CDLL:
-    """Load the built library; raises if it has not been built."""
-    global _lib
-    if _lib is not None:
-        return _lib
-    if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} not found: build it with `python -m paper_2609_10264_amd.build` "
+def load(p: int = MVK_PRIME) -> ctypes.CDLL:
+    """Load the library built over F_p; raises if it has not been built."""
+    L = _libs.get(p)
+    if L is not None:
+        return L
+    if p not in LIB_PATHS:
+        raise ValueError(f"no build over p = {p}; fields: {sorted(LIB_PATHS)}")
+    path = LIB_PATHS[p]
+    if not os.path.exists(path):
+        raise ImportError(f"{path} not found: build it with `python -m paper_2609_10264_amd.build` "
                           "(there is no fallback implementation)")
-    L = ctypes.CDLL(LIB_PATH)
+    L = ctypes.CDLL(path)
     st = ctypes.c_int32
     vp = ctypes.c_void_p
     u32 = ctypes.c_uint32
@@ -103,6 +112,8 @@ def load() -> ctypes.CDLL:
     L.mvk_status_str.restype = ctypes.c_char_p
     L.mvk_abi_version.argtypes = []
     L.mvk_abi_version.restype = ctypes.c_int32
+    L.mvk_field_modulus.argtypes = []
+    L.mvk_field_modulus.restype = ctypes.c_uint32
     L.mvk_server_eval.argtypes = [vp, u32, u32, vp, u32, vp, vp]
     L.mvk_server_eval.restype = st
     L.mvk_server_eval_path.argtypes = [vp, u32, u32, vp, u32, vp, ctypes.c_int32, vp]
@@ -150,8 +161,10 @@ def load() -> ctypes.CDLL:
     L.mvk_raa_syndrome.argtypes = [ctypes.POINTER(MvkCode), vp, u32, vp, vp]
     L.mvk_raa_syndrome.restype = st
     if L.mvk_abi_version() != ABI_VERSION:
-        raise ImportError("libmvk.so ABI version mismatch; rebuild the library")
-    _lib = L
+        raise ImportError(f"{path}: ABI version mismatch; rebuild the library")
+    if L.mvk_field_modulus() != p:
+        raise ImportError(f"{path} is built over p = {L.mvk_field_modulus()}, expected {p}")
+    _libs[p] = L
     return L
 
 

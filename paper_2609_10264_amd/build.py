@@ -1,9 +1,11 @@
-"""Build libmvk.so (the HIP library behind include/mvk.h) for gfx950 with hipcc.
+"""Build the HIP libraries behind include/mvk.h for gfx950 with hipcc.
 
     python -m paper_2609_10264_amd.build
 
-Always recompiles.  Each .hip translation unit is compiled in parallel, then
-linked into one shared object next to this file.
+The same sources are built once per field: libmvk.so over 2^31 - 1 and
+libmvk_bb.so over BabyBear (15 * 2^27 + 1, macro MVK_FIELD_BABYBEAR).  Always
+recompiles.  The translation units of both builds are compiled in parallel,
+then each build is linked into one shared object next to this file.
 """
 from __future__ import annotations
 
@@ -18,7 +20,10 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libmvk.so")
+LIB_BB = os.path.join(PKG, "libmvk_bb.so")
 ARCH = "gfx950"
+# field name -> (library, extra compiler flags)
+VARIANTS = {"m31": (LIB, []), "babybear": (LIB_BB, ["-DMVK_FIELD_BABYBEAR"])}
 
 HIPCC_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
@@ -43,30 +48,37 @@ def sources() -> list[str]:
 
 
 def build(verbose: bool = False) -> str:
+    """Compile and link every field variant; returns the 2^31 - 1 library's path."""
     cc = hipcc()
-    objdir = os.path.join(PKG, "_build")
-    os.makedirs(objdir, exist_ok=True)
+    jobs = []
+    for name, (_, flags) in VARIANTS.items():
+        objdir = os.path.join(PKG, "_build", name)
+        os.makedirs(objdir, exist_ok=True)
+        for src in sources():
+            jobs.append((name, src, os.path.join(objdir, os.path.basename(src).replace(".hip", ".o")), flags))
 
-    def compile_one(src: str) -> str:
-        obj = os.path.join(objdir, os.path.basename(src).replace(".hip", ".o"))
-        cmd = [cc, *HIPCC_FLAGS, "-c", src, "-o", obj]
+    def compile_one(job) -> str:
+        _, src, obj, flags = job
+        cmd = [cc, *HIPCC_FLAGS, *flags, "-c", src, "-o", obj]
         r = subprocess.run(cmd, capture_output=True, text=True)
         out = "\n".join(l for l in (r.stdout + r.stderr).splitlines()
                         if "packed-fp32-ops" not in l)
         if r.returncode != 0:
-            raise RuntimeError(f"hipcc failed for {src}:\n{out}")
+            raise RuntimeError(f"hipcc failed for {src} ({job[0]}):\n{out}")
         if verbose and out.strip():
             print(out, file=sys.stderr)
         return obj
 
     with ThreadPoolExecutor(max_workers=min(8, os.cpu_count() or 1)) as ex:
-        objs = list(ex.map(compile_one, sources()))
-    tmp = LIB + f".tmp{os.getpid()}"
-    cmd = [cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
-    r = subprocess.run(cmd, capture_output=True, text=True)
-    if r.returncode != 0:
-        raise RuntimeError(f"link failed:\n{r.stdout}{r.stderr}")
-    os.replace(tmp, LIB)
+        objs = list(ex.map(compile_one, jobs))
+    for name, (lib, _) in VARIANTS.items():
+        mine = [o for o, j in zip(objs, jobs) if j[0] == name]
+        tmp = lib + f".tmp{os.getpid()}"
+        cmd = [cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *mine]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"link failed ({name}):\n{r.stdout}{r.stderr}")
+        os.replace(tmp, lib)
     return LIB
 
 

@@ -9,6 +9,7 @@
 #include <utility>
 
 #include "mvk.h"
+#include "field.h"
 #include "mvk_internal.h"
 
 namespace mvk {
@@ -167,6 +168,8 @@ const char* mvk_status_str(mvk_status s) {
 }
 
 int32_t mvk_abi_version(void) { return MVK_ABI_VERSION; }
+
+uint32_t mvk_field_modulus(void) { return mvk::kP; }
 
 mvk_status mvk_server_eval(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* Xhat, uint32_t B,
                            uint32_t* Yhat, void* stream) {

@@ -468,24 +468,8 @@ __global__ __launch_bounds__(256) void digits_tiled_kernel(const uint32_t* __res
         *reinterpret_cast<int4*>(dst + 16 * d) = make_int4(pl[d][0], pl[d][1], pl[d][2], pl[d][3]);
 }
 
-// sum_d 2^(8d) S_d mod p for four signed digit sums |S_d| < 2^31, in 32-bit
-// arithmetic: S_d mod p, then multiplication by 2^(8d), which modulo
-// p = 2^31 - 1 is a rotation of the 31-bit value by 8d.
-__device__ __forceinline__ uint32_t rotl31(uint32_t x, int k) {
-    return ((x << k) | (x >> (31 - k))) & kP;
-}
-
-__device__ __forceinline__ uint32_t digits_to_field(v4i sum) {
-    uint32_t r[4];
-#pragma unroll
-    for (int d = 0; d < 4; ++d) {
-        const int32_t v = sum[d];
-        // v >= 0: v <= 2^31 - 1 = p, so v mod p is v or 0; v < 0: p + v >= 0
-        const uint32_t u = v >= 0 ? (uint32_t)v : kP + (uint32_t)v;
-        r[d] = u >= kP ? u - kP : u;
-    }
-    return fadd(fadd(r[0], rotl31(r[1], 8)), fadd(rotl31(r[2], 16), rotl31(r[3], 24)));
-}
+// sum_d 2^(8d) S_d mod p for the four signed digit-plane sums of one output.
+__device__ __forceinline__ uint32_t digits_to_field(v4i sum) { return fdigits4(sum[0], sum[1], sum[2], sum[3]); }
 
 // Epilogue of the streamed kernels: lane `lane` of wave `wave` holds the
 // accumulator tiles acc[i][t] of queries qbase + 4i and rows rowbase + 16t.

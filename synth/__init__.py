@@ -7,7 +7,9 @@ description, the sparse noise of Encrypt and the sparse challenges of Verify).
 Both the CPU oracle and the HIP library receive these arrays as explicit
 inputs, so the two sides never need a shared sampler.
 
-Field: p = 2^31 - 1.  All field arrays are uint32 in canonical form [0, p).
+Field: p = 2^31 - 1 by default; the draws that depend on the field take it as
+``p`` (the BabyBear prime 15 * 2^27 + 1 is ``P_BABYBEAR``).  All field arrays
+are uint32 in canonical form [0, p).
 
 Distributions (paper notation):
   * W: i.i.d. uniform int8 in [-127, 127] (integer-quantised weights that the
@@ -27,6 +29,7 @@ from __future__ import annotations
 import numpy as np
 
 P = 2**31 - 1
+P_BABYBEAR = 15 * 2**27 + 1
 
 PURPOSE_W = 1
 PURPOSE_X = 2
@@ -54,23 +57,23 @@ def weights(seed: int, m: int, n: int, lo: int = -127, hi: int = 127) -> np.ndar
     return g.integers(lo, hi + 1, size=(m, n), dtype=np.int16).astype(np.int8)
 
 
-def field_uniform(seed: int, shape) -> np.ndarray:
+def field_uniform(seed: int, shape, p: int = P) -> np.ndarray:
     """uint32 array uniform in [0, p)."""
     g = rng(seed)
-    return g.integers(0, P, size=shape, dtype=np.uint32)
+    return g.integers(0, p, size=shape, dtype=np.uint32)
 
 
-def field_nonzero(seed: int, shape) -> np.ndarray:
+def field_nonzero(seed: int, shape, p: int = P) -> np.ndarray:
     """uint32 array uniform in [1, p-1]."""
     g = rng(seed)
-    return g.integers(1, P, size=shape, dtype=np.uint32)
+    return g.integers(1, p, size=shape, dtype=np.uint32)
 
 
 def permutation(g: np.random.Generator, N: int) -> np.ndarray:
     return g.permutation(N).astype(np.uint32)
 
 
-def raa_code(seed: int, k: int, r: int) -> dict:
+def raa_code(seed: int, k: int, r: int, p: int = P) -> dict:
     """Random description of an RAA code of dimension k and block length N = r*k.
 
     Returns dict(k, r, N, pi1, pi2, v1, v2) with uint32 arrays of length N.
@@ -79,8 +82,8 @@ def raa_code(seed: int, k: int, r: int) -> dict:
     g = rng(seed)
     pi1 = permutation(g, N)
     pi2 = permutation(g, N)
-    v1 = g.integers(1, P, size=N, dtype=np.uint32)
-    v2 = g.integers(1, P, size=N, dtype=np.uint32)
+    v1 = g.integers(1, p, size=N, dtype=np.uint32)
+    v2 = g.integers(1, p, size=N, dtype=np.uint32)
     return dict(k=int(k), r=int(r), N=N, pi1=pi1, pi2=pi2, v1=v1, v2=v2)
 
 
@@ -92,7 +95,7 @@ def identity_code(k: int, r: int) -> dict:
     return dict(k=int(k), r=int(r), N=N, pi1=ident.copy(), pi2=ident.copy(), v1=ones.copy(), v2=ones.copy())
 
 
-def sparse(seed: int, count: int, N: int, t: int) -> tuple[np.ndarray, np.ndarray]:
+def sparse(seed: int, count: int, N: int, t: int, p: int = P) -> tuple[np.ndarray, np.ndarray]:
     """``count`` independent draws from E_t^N.
 
     Returns (idx, val), each uint32 of shape (count, t).  idx rows hold t
@@ -118,15 +121,15 @@ def sparse(seed: int, count: int, N: int, t: int) -> tuple[np.ndarray, np.ndarra
             idx[c] = np.asarray(out, dtype=np.uint32)
         else:
             idx[c] = g.choice(N, size=t, replace=False).astype(np.uint32)
-    val = g.integers(1, P, size=(count, t), dtype=np.uint32)
+    val = g.integers(1, p, size=(count, t), dtype=np.uint32)
     return idx, val
 
 
-def tamper_delta(seed: int, count: int, m: int) -> tuple[np.ndarray, np.ndarray]:
+def tamper_delta(seed: int, count: int, m: int, p: int = P) -> tuple[np.ndarray, np.ndarray]:
     """Per tampered response: a coordinate in [0, m) and a nonzero additive delta."""
     g = rng(seed)
     pos = g.integers(0, m, size=count, dtype=np.uint32)
-    delta = g.integers(1, P, size=count, dtype=np.uint32)
+    delta = g.integers(1, p, size=count, dtype=np.uint32)
     return pos, delta
 
 
@@ -141,6 +144,12 @@ CONFIGS = {
     "mlp_up_11008x4096": dict(cid=2, m=11008, n=4096, B=16, r=3, tx=64, ty=31, ell=2),
     "mlp_large_28672x8192": dict(cid=3, m=28672, n=8192, B=64, r=4, tx=128, ty=31, ell=2),
 }
+
+# The pvMVMD evaluation of Sec. 7.1: square n x n matrices, one query, over
+# BabyBear, RAA rate 1/8 for both codes (r = 8), noise weight t_x from Eq. (1)
+# for the block length 8n, t_y = 31 and ell = 2.
+PAPER_EVAL = dict(cid=6, r=8, ty=31, ell=2, B=1, p=P_BABYBEAR,
+                  tx={1024: 160, 2048: 159, 4096: 157, 8192: 156, 16384: 154})
 
 # 32-layer stack: per layer the seven projections of a 4096-wide decoder block
 # (q, k, v, o: 4096x4096; up, gate: 11008x4096; down: 4096x11008), 8 columns.

@@ -37,6 +37,20 @@ def test_library_exports_every_declared_symbol():
     assert sorted(L.EXPORTS) == _declared()
 
 
+def test_both_field_builds_load_and_export_every_symbol():
+    L = _lib()
+    for p, path in L.LIB_PATHS.items():
+        if not os.path.exists(path):
+            pytest.skip(f"{os.path.basename(path)} not built")
+        raw = ctypes.CDLL(path)
+        assert not [n for n in _declared() if not hasattr(raw, n)]
+        lib = L.load(p)
+        assert lib.mvk_field_modulus() == p and lib.mvk_abi_version() == L.ABI_VERSION
+    assert sorted(L.LIB_PATHS) == [L.MVK_PRIME_BABYBEAR, L.MVK_PRIME] == [15 * 2**27 + 1, 2**31 - 1]
+    with pytest.raises(ValueError):
+        L.load(97)
+
+
 def test_abi_version_and_status_strings():
     L = _lib()
     lib = L.load()

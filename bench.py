@@ -134,7 +134,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", default="attn4096",
-                    help="attn4096 (default), mlp_up_11008x4096, mlp_large_28672x8192, tiny or stack32")
+                    help="attn4096 (default), mlp_up_11008x4096, mlp_large_28672x8192, tiny, stack32 or paper_eval "
+                         "(the Sec. 7.1 BabyBear sweep; --n picks one size)")
     ap.add_argument("--pool", type=int, default=0, help="distinct W matrices cycled (0: enough for 2x the LLC)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="time budget of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -189,6 +190,8 @@ def main():
         return stack_bench(args)
     if args.batch_verify:
         return batch_verify_bench(args)
+    if args.config == "paper_eval":
+        return paper_eval_bench(args)
     cfg = dict(synth.CONFIGS[args.config])
     if args.server_only:
         for key in ("m", "n", "B"):
@@ -667,6 +670,179 @@ def batch_verify_bench(args):
                                   f"secondary RAA r'={r2} over Bn={B * n}, t=t'={ty}, ell=ell'={ell}",
                       "claims": B},
            "batch_us": out["batch"], "one_by_one_us": out["one_by_one"], "all_accepted": ok}
+    print(json.dumps(res), flush=True)
+    if not ok:
+        sys.exit(1)
+
+
+# The paper's own timings for this workload (Sec. 7.1, online-breakdown and
+# preprocessing tables; Rust, one thread of an x86 c8i.4xlarge, BabyBear):
+# n -> (server MVM, client online total, one-time preprocessing), milliseconds.
+PAPER_SEC71_MS = {1024: (0.39, 0.79, 329.54), 2048: (1.59, 1.55, 1499.06), 4096: (9.54, 2.33, 6030.76),
+                  8192: (34.68, 4.56, 25063.59), 16384: (116.00, 9.33, 135800.06)}
+
+
+def paper_eval_bench(args):
+    """The pvMVMD evaluation of Sec. 7.1 on the GPU, over BabyBear: square
+    n x n int8-valued W, one query, RAA rate 1/8 for both codes, t_x of Eq. (1),
+    t_y = 31, ell = 2, for n = 2^10 .. 2^14 (or --n).  Per n: keygen (P^T and Q,
+    the one-time preprocessing), and HIP-event means over graphs of K calls of
+    encode, server_eval and decode_verify alone and of the whole step, cycling a
+    pool of distinct W (and keys) that exceeds the last-level cache twice."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import paper_2609_10264_amd as mvk
+    import synth
+
+    cfg = synth.PAPER_EVAL
+    p, r, ty, ell, B, cid = (cfg[k] for k in ("p", "r", "ty", "ell", "B", "cid"))
+    dev = torch.device("cuda")
+    s = torch.cuda.Stream()
+    K = max(8, args.steps)
+    ns = [args.n] if args.n else sorted(cfg["tx"])
+
+    def d(a):
+        return torch.from_numpy(np.ascontiguousarray(a).astype(np.int32)).to(dev)
+
+    def code(c):
+        return mvk.Code(c["k"], c["r"], d(c["pi1"]), d(c["pi2"]), d(c["v1"]), d(c["v2"]), p)
+
+    def timed(fn, reps):
+        """Mean milliseconds per call of fn(i), i < reps, from one graph replay."""
+        with torch.cuda.stream(s):
+            fn(0)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            for i in range(reps):
+                fn(i)
+
+        def replay():
+            with torch.cuda.stream(s):
+                g.replay()
+
+        warm(replay, args.warm_seconds)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(s):
+            e0.record()
+            g.replay()
+            e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    rows, ok = [], True
+    for n in ns:
+        m, tx = n, cfg["tx"][n]
+        pool = max(2, -(-2 * 256 * 2**20 // (m * n)))
+        cx_h = synth.raa_code(synth.seed_for(cid, synth.PURPOSE_CX, n), n, r, p=p)
+        cy_h = synth.raa_code(synth.seed_for(cid, synth.PURPOSE_CY, n), m, r, p=p)
+        cx, cy = code(cx_h), code(cy_h)
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(args.seed + n)
+        Ws, keys, kg_ms = [], [], []
+        with torch.cuda.stream(s):
+            for j in range(pool + 1):  # the first keygen (workspace sizing) is not timed
+                Wj = torch.randint(-127, 128, (m, n), generator=gen, device=dev, dtype=torch.int8)
+                kj = mvk.Key.allocate(m, n, cx, cy)
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                mvk.keygen(kj, Wj, stream=s)
+                e1.record()
+                e1.synchronize()
+                if j:
+                    kg_ms.append(e0.elapsed_time(e1))
+                    Ws.append(mvk.pack_weights(Wj, stream=s))
+                    keys.append(kj)
+                del Wj
+        X = torch.randint(0, p, (K, B, n), generator=gen, device=dev, dtype=torch.int32)
+        exi, exv = synth.sparse(synth.seed_for(cid, synth.PURPOSE_NOISE, n), K * B, cx.N, tx, p=p)
+        eyi, eyv = synth.sparse(synth.seed_for(cid, synth.PURPOSE_CHAL, n), K * ell, cy.N, ty, p=p)
+        EXI, EXV = d(exi).view(K, B, tx), d(exv).view(K, B, tx)
+        EYI, EYV = d(eyi).view(K, ell, ty), d(eyv).view(K, ell, ty)
+        Xh = torch.empty((K, B, n), dtype=torch.int32, device=dev)
+        Yh = torch.empty((K, B, m), dtype=torch.int32, device=dev)
+        Y = torch.empty((K, B, m), dtype=torch.int32, device=dev)
+        ACC = torch.zeros((K, B), dtype=torch.int32, device=dev)
+
+        def enc(i):
+            mvk.encode(keys[i % pool], X[i], EXI[i], EXV[i], out=Xh[i])
+
+        def se(i):
+            mvk.server_eval(Ws[i % pool], Xh[i], out=Yh[i], p=p)
+
+        def dv(i):
+            mvk.decode_verify(keys[i % pool], Xh[i], Yh[i], EXI[i], EXV[i], EYI[i], EYV[i], Y=Y[i], accept=ACC[i])
+
+        def step(i):
+            enc(i)
+            se(i)
+            dv(i)
+
+        t_enc, t_se, t_dv = timed(enc, K), timed(se, K), timed(dv, K)
+        ACC.zero_()
+        t_step = timed(step, K)
+        acc_ok = bool((ACC == 1).all().item())
+        # boost mode (Sec. 7): the masks and challenge vectors of every step
+        # prepared ahead (client_prepare, timed on its own); online only
+        # encode_masked -> server_eval -> decode_verify_masked
+        preps = [mvk.Prepared(keys[i % pool], B, ell) for i in range(K)]
+
+        def prep(i):
+            mvk.client_prepare(keys[i % pool], EXI[i], EXV[i], EYI[i], EYV[i], out=preps[i])
+
+        def online(i):
+            mvk.encode_masked(keys[i % pool], X[i], preps[i], out=Xh[i])
+            se(i)
+            mvk.decode_verify_masked(keys[i % pool], Xh[i], Yh[i], preps[i], Y=Y[i], accept=ACC[i])
+
+        t_prep = timed(prep, K)
+        ACC.zero_()
+        t_online = timed(online, K)
+        acc_ok = acc_ok and bool((ACC == 1).all().item())
+        del preps
+        # the last step's decrypted output against the server product of the plaintext query
+        with torch.cuda.stream(s):
+            plain = mvk.server_eval(Ws[(K - 1) % pool], X[K - 1], p=p)
+        torch.cuda.synchronize()
+        acc_ok = acc_ok and bool(torch.equal(plain, Y[K - 1]))
+        ok = ok and acc_ok
+        alg_bytes = m * n + 4 * n * B + 4 * m * B
+        srv_s = 1e-3 * t_se
+        paper = PAPER_SEC71_MS[n]
+        rows.append({"n": n, "t_x": tx, "w_pool": pool, "keygen_ms": float(np.mean(kg_ms)),
+                     "encode_us": 1e3 * t_enc, "server_eval_us": 1e3 * t_se, "decode_verify_us": 1e3 * t_dv,
+                     "step_us": 1e3 * t_step, "boost_prepare_us": 1e3 * t_prep, "boost_online_us": 1e3 * t_online,
+                     "server_gb_per_s": alg_bytes / srv_s / 1e9,
+                     "server_hbm_frac": alg_bytes / srv_s / 1e9 / HBM_PEAK_GBS,
+                     "step_modmac_per_s": m * n * B / (1e-3 * t_step), "all_accepted": acc_ok,
+                     "paper_cpu_ms": {"server": paper[0], "client_online": paper[1], "preprocessing": paper[2]}})
+        del Ws, keys, X, Xh, Yh, Y
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+    top = rows[-1]
+    res = {"metric": METRIC, "value": top["step_modmac_per_s"], "unit": "modMAC/s", "n_gpus": 1, "steps": K,
+           "warmup": 1, "ms_per_step": 1e-3 * top["step_us"], "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "i8xi8->i32 limb dot products, mod 15*2^27+1", "data": "synthetic",
+           "config": {"workload": f"Sec. 7.1 pvMVMD evaluation over BabyBear: W {top['n']}x{top['n']} int8-valued, "
+                                  f"one query, RAA r={r}, t_x={top['t_x']}, t_y={ty}, ell={ell}; step = "
+                                  "encode+server_eval+decode_verify", "global_batch": B, "launch": "hip_graph"},
+           "sweep": rows, "all_accepted": ok}
+    if not args.no_cpu_baseline:
+        # the oracle's server product over a row sample of the largest W
+        n = top["n"]
+        Wh = synth.weights(synth.seed_for(cid, synth.PURPOSE_W, n), 256, n)
+        Xq = synth.field_uniform(synth.seed_for(cid, synth.PURPOSE_X, n), (1, n), p=p)
+        reps, el = 0, 0.0
+        while el < min(args.cpu_seconds, 5.0):
+            t0 = time.perf_counter()
+            oracle.server_eval(Wh, Xq, p=p)
+            el += time.perf_counter() - t0
+            reps += 1
+        res["cpu_baseline"] = {"value": 256 * n * reps / el, "unit": "modMAC/s", "cores": 1, "kind": "oracle",
+                               "sample": f"{reps} oracle server products of 256 rows x {n} over BabyBear, "
+                                         f"{el:.1f} s; single-threaded C, '%' per field op"}
     print(json.dumps(res), flush=True)
     if not ok:
         sys.exit(1)

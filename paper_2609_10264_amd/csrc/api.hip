@@ -227,7 +227,7 @@ mvk_status mvk_encode(const mvk_key* key, const uint32_t* X, uint32_t B, const m
     const size_t Nx = (size_t)key->cx.r * key->n;
     if (ex->t > Nx) return MVK_EINVAL;
     void* ws = nullptr;
-    st = workspace(s, Nx > kSynScratchAbove ? (size_t)B * 2 * Nx * sizeof(uint32_t) : 0, &ws);
+    st = workspace(s, syn_scratch_bytes(B, Nx), &ws);
     if (st) return st;
     return hip_status(launch_syn_sparse(key->cx, ex->idx, ex->val, ex->t, B, X, (uint32_t*)ws, Xhat, s));
 }
@@ -241,7 +241,7 @@ mvk_status mvk_verify_prepare(const mvk_key* key, const mvk_sparse* ey, uint32_t
     hipStream_t s = (hipStream_t)stream;
     const size_t Ny = (size_t)key->cy.r * key->m;
     void* ws = nullptr;
-    st = workspace(s, Ny > kSynScratchAbove ? (size_t)ey->count * 2 * Ny * 4 : 0, &ws);
+    st = workspace(s, syn_scratch_bytes(ey->count, Ny), &ws);
     if (st) return st;
     return hip_status(launch_syn_sparse(key->cy, ey->idx, ey->val, ey->t, ey->count, nullptr, (uint32_t*)ws, R, s));
 }
@@ -271,7 +271,7 @@ mvk_status decode_verify_run(const mvk_key* key, const uint32_t* Xhat, const uin
     const uint32_t m = key->m, ell = ey->count;
     const size_t Ny = (size_t)key->cy.r * m;
     const size_t r_bytes = align_up((size_t)ell * m * 4);
-    const size_t syn_bytes = Ny > kSynScratchAbove ? align_up((size_t)ell * 2 * Ny * 4) : 0;
+    const size_t syn_bytes = align_up(syn_scratch_bytes(ell, Ny));
     void* ws = nullptr;
     uint32_t* ctrl = nullptr;
     const mvk_status st = workspace(s, r_bytes + syn_bytes, &ws, &ctrl, dv_ctrl_bytes(ell, B));
@@ -341,8 +341,8 @@ mvk_status mvk_client_prepare(const mvk_key* key, const mvk_sparse* ex, const mv
     if (nx == 0 && ny == 0) return done_flag ? hip_status(launch_flag_signal(done_flag, done_value, s)) : MVK_OK;
     const size_t Nx = (size_t)key->cx.r * key->n, Ny = (size_t)key->cy.r * key->m;
     size_t scratch = 0;
-    if (nx && Nx > kSynScratchAbove) scratch = (size_t)nx * 2 * Nx * 4;
-    if (ny && Ny > kSynScratchAbove && (size_t)ny * 2 * Ny * 4 > scratch) scratch = (size_t)ny * 2 * Ny * 4;
+    if (nx) scratch = syn_scratch_bytes(nx, Nx);
+    if (ny && syn_scratch_bytes(ny, Ny) > scratch) scratch = syn_scratch_bytes(ny, Ny);
     void* ws = nullptr;
     uint32_t* ctrl = nullptr;
     st = workspace(s, scratch, &ws, &ctrl);
@@ -453,8 +453,8 @@ mvk_status mvk_batch_verify(const mvk_code* cy, const mvk_code* c2, const uint32
     hipStream_t s = (hipStream_t)stream;
     const size_t r_bytes = align_up((size_t)ell * m * 4), rs_bytes = align_up((size_t)ell2 * Bn * 4);
     size_t syn_bytes = 0;
-    if (N > kSynScratchAbove) syn_bytes = (size_t)ell * 2 * N * 4;
-    if (N2 > kSynScratchAbove && (size_t)ell2 * 2 * N2 * 4 > syn_bytes) syn_bytes = (size_t)ell2 * 2 * N2 * 4;
+    syn_bytes = syn_scratch_bytes(ell, N);
+    if (syn_scratch_bytes(ell2, N2) > syn_bytes) syn_bytes = syn_scratch_bytes(ell2, N2);
     void* ws = nullptr;
     uint32_t* ctrl = nullptr;
     st = workspace(s, r_bytes + rs_bytes + syn_bytes, &ws, &ctrl,
@@ -496,7 +496,7 @@ mvk_status mvk_raa_syndrome(const mvk_code* code, const uint32_t* v, uint32_t co
     hipStream_t s = (hipStream_t)stream;
     const size_t N = (size_t)code->k * code->r;
     void* ws = nullptr;
-    st = workspace(s, (size_t)count * 2 * N * sizeof(uint32_t), &ws);
+    st = workspace(s, syn_scratch_bytes(count, N), &ws);
     if (st) return st;
     return hip_status(launch_syn_dense(*code, v, count, (uint32_t*)ws, out, s));
 }

@@ -34,12 +34,21 @@ hipError_t launch_encT_u32(const mvk_code& c, const uint32_t* in, size_t ld_in, 
                            uint32_t* t3, uint32_t* out, size_t ld_out, size_t vs_out, hipStream_t s);
 hipError_t launch_encT_i8(const mvk_code& c, const int8_t* in, size_t ld_in, size_t vs_in, uint32_t nvec,
                           uint32_t* t3, uint32_t* out, size_t ld_out, size_t vs_out, hipStream_t s);
-// Block lengths above this value run the syndrome in segments and need a
-// scratch of count x 2N words; up to it the syndrome runs in LDS.
+// Block lengths above this value run the syndrome in segments of kSynSegLen
+// positions (several workgroups per vector) and need syn_scratch_bytes(count,
+// N) bytes of scratch; up to it the syndrome runs in LDS and needs none.
 constexpr size_t kSynScratchAbove = 16384;
+constexpr size_t kSynSegLen = 1024;
+// Two work arrays of N words per vector, then per vector a ticket word and one
+// status word per segment (64-bit each).
+inline size_t syn_scratch_bytes(size_t count, size_t N) {
+    if (N <= kSynScratchAbove) return 0;
+    const size_t nseg = (N + kSynSegLen - 1) / kSynSegLen;
+    return count * (2 * N * sizeof(uint32_t) + (nseg + 1) * sizeof(uint64_t));
+}
 // G v for `count` vectors: dense (v: count x N) or sparse (idx/val: count x t).
 // If X != nullptr the result is added to X (out = X + G v), as in Encrypt.
-// scratch: count * 2N uint32.
+// scratch: syn_scratch_bytes(count, N), 8-byte aligned.
 hipError_t launch_syn_dense(const mvk_code& c, const uint32_t* v, uint32_t count, uint32_t* scratch,
                             uint32_t* out, hipStream_t s);
 hipError_t launch_syn_sparse(const mvk_code& c, const uint32_t* idx, const uint32_t* val, uint32_t t,

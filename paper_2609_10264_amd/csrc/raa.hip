@@ -121,15 +121,32 @@ __global__ __launch_bounds__(kSynThreads) void syn_wg(uint32_t k, uint32_t r, co
 // workgroup each, in three launches:
 //   p1: a = suffix sum of the input (the carry into a segment is the sum of the
 //       input beyond it: for sparse input a sum over the t terms, for dense
-//       input a reduction of the tail), then b[pi2[j]] = v2[j] a[j]
-//   p2: c = suffix sum of b (carry: each workgroup reduces the tail of b
-//       itself, so no workgroup waits for another), then d[pi1[j]] = v1[j] c[j]
+//       input a reduction of the tail), then b[pi2[j]] = v2[j] a[j]; p1 also
+//       resets p2's look-back state
+//   p2: c = suffix sum of b, then d[pi1[j]] = v1[j] c[j].  The carry into a
+//       segment is the sum of the later segments' sums: every workgroup
+//       publishes its segment's sum and reads the later ones (a single-pass
+//       scan with look-back).  Segments are handed out by a ticket counter
+//       from the last one down, so a workgroup only ever waits for segments
+//       taken by workgroups that started before it.
 //   p3: out[i] = (X[i] +) sum_{q<r} d[i r + q]
-// b and d live in the global scratch (count x 2N words).
+// b and d live in the global scratch (count x 2N words), followed by the
+// look-back state: per vector one ticket word and one status word per segment
+// (bit 32 set once the segment's sum, in the low 31 bits, is published).
 // ---------------------------------------------------------------------------
 constexpr int kSegThreads = 256;
 constexpr int kSegPer = 4;
 constexpr uint32_t kSegLen = kSegThreads * kSegPer;
+static_assert(kSegLen == kSynSegLen, "segment length of the scratch layout");
+// Bound on the polls of one look-back read (each followed by a short sleep):
+// every awaited segment belongs to a workgroup that is already running, so the
+// bound is only a guard that makes every wave exit.
+constexpr uint32_t kLookSpinLimit = 1u << 22;
+
+__device__ __forceinline__ unsigned long long* look_state(uint32_t* scratch, uint32_t count, uint32_t N, uint32_t c) {
+    const uint32_t nseg = (N + kSegLen - 1) / kSegLen;
+    return reinterpret_cast<unsigned long long*>(scratch + (size_t)count * 2 * N) + (size_t)c * (nseg + 1);
+}
 
 __device__ __forceinline__ uint64_t block_sum_u64_256(uint64_t v, uint64_t* red) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -183,6 +200,12 @@ __global__ __launch_bounds__(kSegThreads) void syn_p1(uint32_t k, uint32_t r, co
     const uint32_t j0 = blockIdx.x * kSegLen, j1 = (j0 + kSegLen < N) ? j0 + kSegLen : N;
     const int tid = threadIdx.x;
     uint32_t* bbuf = scratch + (size_t)c * 2 * N;
+    if (tid == 0) {
+        // p2's look-back state: this segment's status word, and (segment 0) the ticket
+        unsigned long long* st = look_state(scratch, gridDim.y, N, c);
+        st[1 + blockIdx.x] = 0ull;
+        if (blockIdx.x == 0) st[0] = 0ull;
+    }
     // code entries of this thread's positions (in flight during the carry)
     uint32_t p2[kSegPer], w2[kSegPer];
 #pragma unroll
@@ -234,9 +257,17 @@ __global__ __launch_bounds__(kSegThreads) void syn_p2(uint32_t k, uint32_t r, co
                                                       const uint32_t* __restrict__ v1, uint32_t* __restrict__ scratch) {
     __shared__ uint64_t red[4];
     __shared__ uint32_t wsum[4];
-    const uint32_t c = blockIdx.y, N = k * r;
-    const uint32_t j0 = blockIdx.x * kSegLen, j1 = (j0 + kSegLen < N) ? j0 + kSegLen : N;
-    const int tid = threadIdx.x;
+    __shared__ uint32_t sh_seg, sh_carry;
+    const uint32_t c = blockIdx.y, N = k * r, nseg = (N + kSegLen - 1) / kSegLen;
+    const int tid = threadIdx.x, lane = tid & 63;
+    unsigned long long* st = look_state(scratch, gridDim.y, N, c);
+    if (tid == 0) {
+        const uint32_t ticket = atomicAdd(reinterpret_cast<uint32_t*>(st), 1u);  // < nseg: one per workgroup
+        sh_seg = ticket < nseg ? nseg - 1 - ticket : 0u;
+    }
+    __syncthreads();
+    const uint32_t sg = sh_seg;
+    const uint32_t j0 = sg * kSegLen, j1 = (j0 + kSegLen < N) ? j0 + kSegLen : N;
     const uint32_t* bbuf = scratch + (size_t)c * 2 * N;
     uint32_t* dbuf = scratch + (size_t)c * 2 * N + N;
     uint32_t p1[kSegPer], w1[kSegPer], x[kSegPer];
@@ -249,11 +280,33 @@ __global__ __launch_bounds__(kSegThreads) void syn_p2(uint32_t k, uint32_t r, co
         const uint32_t b = bbuf[js];
         x[e] = j < j1 ? b : 0u;
     }
-    uint64_t part = 0;
-#pragma unroll 8
-    for (uint32_t j = j1 + tid; j < N; j += kSegThreads) part += bbuf[j];
-    const uint32_t carry = fred64(block_sum_u64_256(part, red));
-    seg_suffix_scan(x, carry, wsum);  // A
+    // publish this segment's sum
+    const uint32_t own = fred64(block_sum_u64_256((uint64_t)x[0] + x[1] + x[2] + x[3], red));
+    if (tid == 0) __hip_atomic_store(&st[1 + sg], (1ull << 32) | own, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // carry = sum of the later segments' sums, read 64 segments at a time
+    if (tid < 64) {
+        uint64_t acc = 0;
+        for (uint32_t base = sg + 1; base < nseg; base += 64) {
+            const uint32_t q = base + lane;
+            if (q < nseg) {
+                unsigned long long v = __hip_atomic_load(&st[1 + q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                for (uint32_t spin = 0; !(v >> 32) && spin < kLookSpinLimit; ++spin) {
+                    __builtin_amdgcn_s_sleep(1);
+                    v = __hip_atomic_load(&st[1 + q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+                acc += (uint32_t)v;
+            }
+        }
+#pragma unroll
+        for (int sh = 32; sh >= 1; sh >>= 1) {
+            const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)acc, sh);
+            const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(acc >> 32), sh);
+            acc += ((uint64_t)hi << 32) | lo;
+        }
+        if (tid == 0) sh_carry = fred64(acc);
+    }
+    __syncthreads();
+    seg_suffix_scan(x, sh_carry, wsum);  // A
 #pragma unroll
     for (int e = 0; e < kSegPer; ++e) {
         const uint32_t j = j0 + tid * kSegPer + e;

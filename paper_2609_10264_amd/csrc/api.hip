@@ -110,18 +110,13 @@ mvk_status check_decode_verify(const mvk_key* key, const uint32_t* Xhat, const u
     return MVK_OK;
 }
 
-// Control region of decode_verify: the counter (first 256 bytes), then the
-// 2*ell*B 64-bit accumulators.
-inline size_t dv_ctrl_bytes(uint32_t ell, uint32_t B) { return kCtrlBase + (size_t)2 * ell * B * 8; }
-
 hipError_t launch_dv(const mvk_key* key, const uint32_t* Xhat, const uint32_t* Yhat, uint32_t B,
                      const mvk_sparse* ex, const mvk_sparse* ey, const uint32_t* R, uint32_t* Y, uint32_t* vL,
                      uint32_t* vR, uint32_t* accept, uint32_t* ctrl, hipStream_t s) {
     const uint32_t m = key->m, n = key->n;
     const uint32_t Nx = key->cx.r * n, Ny = key->cy.r * m;
     return launch_decode_verify(key->PT, key->Q, m, n, Nx, Ny, Xhat, Yhat, B, ex->idx, ex->val, ex->t, ey->idx,
-                                ey->val, ey->t, ey->count, R, Y, (unsigned long long*)((char*)ctrl + kCtrlBase),
-                                &ctrl[0], vL, vR, accept, s);
+                                ey->val, ey->t, ey->count, R, Y, ctrl, vL, vR, accept, s);
 }
 
 }  // namespace
@@ -255,7 +250,7 @@ mvk_status mvk_decode_verify_prepared(const mvk_key* key, const uint32_t* Xhat, 
     hipStream_t s = (hipStream_t)stream;
     void* ws = nullptr;
     uint32_t* ctrl = nullptr;
-    st = workspace(s, 0, &ws, &ctrl, dv_ctrl_bytes(ey->count, B));
+    st = workspace(s, 0, &ws, &ctrl, dv_ctrl_bytes(key->m, key->n, B, ey->count));
     if (st) return st;
     return hip_status(launch_dv(key, Xhat, Yhat, B, ex, ey, R, Y, vL, vR, accept, ctrl, s));
 }
@@ -274,7 +269,7 @@ mvk_status decode_verify_run(const mvk_key* key, const uint32_t* Xhat, const uin
     const size_t syn_bytes = align_up(syn_scratch_bytes(ell, Ny));
     void* ws = nullptr;
     uint32_t* ctrl = nullptr;
-    const mvk_status st = workspace(s, r_bytes + syn_bytes, &ws, &ctrl, dv_ctrl_bytes(ell, B));
+    const mvk_status st = workspace(s, r_bytes + syn_bytes, &ws, &ctrl, dv_ctrl_bytes(m, key->n, B, ell));
     if (st) return st;
     uint32_t* rv = (uint32_t*)ws;
     uint32_t* syn_scratch = (uint32_t*)((char*)ws + r_bytes);
@@ -283,8 +278,7 @@ mvk_status decode_verify_run(const mvk_key* key, const uint32_t* Xhat, const uin
         const mvk_code& cy = key->cy;
         return hip_status(launch_decode_verify_syn(
             key->PT, key->Q, m, key->n, key->cx.r * key->n, (uint32_t)Ny, Xhat, Yhat, B, ex->idx, ex->val, ex->t,
-            ey->idx, ey->val, ey->t, ell, cy.r, cy.pi1, cy.pi2, cy.v1, cy.v2, rv, Y,
-            (unsigned long long*)((char*)ctrl + kCtrlBase), ctrl, vL, vR, accept, s));
+            ey->idx, ey->val, ey->t, ell, cy.r, cy.pi1, cy.pi2, cy.v1, cy.v2, rv, Y, ctrl, vL, vR, accept, s));
     }
     // r_q = Gy e_q for every repetition (shared by all columns)
     hipError_t e = launch_syn_sparse(key->cy, ey->idx, ey->val, ey->t, ell, nullptr, syn_scratch, rv, s);
@@ -345,7 +339,7 @@ mvk_status mvk_client_prepare(const mvk_key* key, const mvk_sparse* ex, const mv
     if (ny && syn_scratch_bytes(ny, Ny) > scratch) scratch = syn_scratch_bytes(ny, Ny);
     void* ws = nullptr;
     uint32_t* ctrl = nullptr;
-    st = workspace(s, scratch, &ws, &ctrl);
+    st = workspace(s, scratch, &ws, &ctrl, 4 * (kPrepCounterWord + prep_ctrl_words(*key, nx, ny)));
     if (st) return st;
     return hip_status(launch_client_prepare(*key, nx ? ex->idx : nullptr, nx ? ex->val : nullptr, nx ? ex->t : 0u,
                                             nx, ny ? ey->idx : nullptr, ny ? ey->val : nullptr, ny ? ey->t : 0u, ny,
@@ -383,10 +377,9 @@ mvk_status mvk_decode_verify_masked(const mvk_key* key, const uint32_t* Xhat, co
     hipStream_t s = (hipStream_t)stream;
     void* ws = nullptr;
     uint32_t* ctrl = nullptr;
-    st = workspace(s, 0, &ws, &ctrl, dv_ctrl_bytes(ell, B));
+    st = workspace(s, 0, &ws, &ctrl, dv_ctrl_bytes(key->m, key->n, B, ell));
     if (st) return st;
-    return hip_status(launch_decode_verify_masked(key->m, key->n, Xhat, Yhat, B, My, ell, R, U, Y,
-                                                  (unsigned long long*)((char*)ctrl + kCtrlBase), &ctrl[0], vL, vR,
+    return hip_status(launch_decode_verify_masked(key->m, key->n, Xhat, Yhat, B, My, ell, R, U, Y, ctrl, vL, vR,
                                                   accept, s));
 }
 
@@ -457,8 +450,7 @@ mvk_status mvk_batch_verify(const mvk_code* cy, const mvk_code* c2, const uint32
     if (syn_scratch_bytes(ell2, N2) > syn_bytes) syn_bytes = syn_scratch_bytes(ell2, N2);
     void* ws = nullptr;
     uint32_t* ctrl = nullptr;
-    st = workspace(s, r_bytes + rs_bytes + syn_bytes, &ws, &ctrl,
-                   kCtrlBase + ((size_t)2 * ell * B + (size_t)2 * ell * ell2) * 8);
+    st = workspace(s, r_bytes + rs_bytes + syn_bytes, &ws, &ctrl, batch_ctrl_bytes(m, n, B, ell, ell2));
     if (st) return st;
     uint32_t* R = (uint32_t*)ws;
     uint32_t* Rs = (uint32_t*)((char*)ws + r_bytes);
@@ -468,8 +460,7 @@ mvk_status mvk_batch_verify(const mvk_code* cy, const mvk_code* c2, const uint32
     if (err == hipSuccess) err = launch_syn_sparse(*c2, e2->idx, e2->val, e2->t, ell2, nullptr, scratch, Rs, s);
     if (err == hipSuccess)
         err = launch_batch_check(m, n, B, X, Y, Ut, R, Rs, Qaux, (uint32_t)N, (uint32_t)N2, e->idx, e->val, e->t, ell,
-                                 e2->idx, e2->val, e2->t, ell2, (unsigned long long*)((char*)ctrl + kCtrlBase),
-                                 &ctrl[0], vL, vR, sL, sR, accept, s);
+                                 e2->idx, e2->val, e2->t, ell2, ctrl, vL, vR, sL, sR, accept, s);
     return hip_status(err);
 }
 

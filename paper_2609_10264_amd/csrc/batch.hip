@@ -10,6 +10,7 @@
 //                secondary (e(q))^T Qaux e'(j)  ==  (G' e'(j))^T u~(q)
 // The primary side uses the transposed form of App. B, as the one-claim
 // Verify does: (e^T G^T) y = (G e)^T y, one syndrome per repetition.
+#include "count.h"
 #include "field.h"
 #include "mvk_internal.h"
 
@@ -53,7 +54,8 @@ struct CheckArgs {
     const uint32_t *X, *Y, *Ut, *R, *Rs, *Qaux;
     const uint32_t *e_idx, *e_val, *e2_idx, *e2_val;
     unsigned long long *accL, *accR, *accS, *accA;  // ell x B, ell x B, ell x ell2, ell x ell2
-    uint32_t* counter;
+    uint32_t* ctrl;  // completion counters (count.h)
+    uint32_t slots;
     uint32_t *vL, *vR, *sL, *sR, *accept;
     uint32_t nbL, nbR, nbS;  // 256-element blocks of n, m and Bn
 };
@@ -61,7 +63,7 @@ struct CheckArgs {
 // Workgroups [0, B*nbL): v_L terms u_b(q)[k] x_b[k]; next B*nbR: v_R terms
 // R_q[i] y_b[i]; next nbS: secondary right sides r_j[c] u~(q)[c]; the last
 // ell*ell2: the t x t' lookups of one secondary left side each.  Partial sums go into
-// 64-bit accumulators; the workgroup that finishes last (counter) reads and
+// 64-bit accumulators; the workgroup that finishes last (count.h) reads and
 // clears them and writes the results and the accept bits.
 __global__ __launch_bounds__(kBT) void batch_check_kernel(CheckArgs a) {
     __shared__ uint64_t red[kBW];
@@ -128,7 +130,7 @@ __global__ __launch_bounds__(kBT) void batch_check_kernel(CheckArgs a) {
     // accumulators with atomics.
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (tid == 0) last = (atomicAdd(a.counter, 1u) == gridDim.x - 1) ? 1u : 0u;
+    if (tid == 0) last = count_last(a.ctrl, a.slots) ? 1u : 0u;
     __syncthreads();
     if (!last) return;
     // secondary checks (one bit for the batch), then the claims
@@ -155,30 +157,37 @@ __global__ __launch_bounds__(kBT) void batch_check_kernel(CheckArgs a) {
         }
         a.accept[b] = ok;
     }
-    if (tid == 0) atomicExch(a.counter, 0u);
 }
 
 }  // namespace
+
+size_t batch_ctrl_bytes(uint32_t m, uint32_t n, uint32_t B, uint32_t ell, uint32_t ell2) {
+    const uint64_t grid = (uint64_t)B * (ceil_div(n, kBT) + ceil_div(m, kBT)) + ceil_div(B * n, kBT) +
+                          (uint64_t)ell * ell2;
+    const uint32_t slots = count_slots(grid > 0xffffffffull ? 0xffffffffu : (uint32_t)grid);
+    return (size_t)count_words(slots) * 4 + ((size_t)2 * ell * B + (size_t)2 * ell * ell2) * 8;
+}
 
 hipError_t launch_batch_check(uint32_t m, uint32_t n, uint32_t B, const uint32_t* X, const uint32_t* Y,
                               const uint32_t* Ut, const uint32_t* R, const uint32_t* Rs, const uint32_t* Qaux,
                               uint32_t N, uint32_t N2, const uint32_t* e_idx, const uint32_t* e_val, uint32_t t,
                               uint32_t ell, const uint32_t* e2_idx, const uint32_t* e2_val, uint32_t t2,
-                              uint32_t ell2, unsigned long long* acc, uint32_t* counter, uint32_t* vL, uint32_t* vR,
-                              uint32_t* sL, uint32_t* sR, uint32_t* accept, hipStream_t s) {
+                              uint32_t ell2, uint32_t* ctrl, uint32_t* vL, uint32_t* vR, uint32_t* sL, uint32_t* sR,
+                              uint32_t* accept, hipStream_t s) {
     CheckArgs a;
     a.m = m, a.n = n, a.B = B, a.ell = ell, a.ell2 = ell2, a.t = t, a.t2 = t2, a.N = N, a.N2 = N2;
     a.X = X, a.Y = Y, a.Ut = Ut, a.R = R, a.Rs = Rs, a.Qaux = Qaux;
     a.e_idx = e_idx, a.e_val = e_val, a.e2_idx = e2_idx, a.e2_val = e2_val;
-    a.accL = acc;
-    a.accR = a.accL + (size_t)ell * B;
-    a.accS = a.accR + (size_t)ell * B;
-    a.accA = a.accS + (size_t)ell * ell2;
-    a.counter = counter;
     a.vL = vL, a.vR = vR, a.sL = sL, a.sR = sR, a.accept = accept;
     a.nbL = ceil_div(n, kBT), a.nbR = ceil_div(m, kBT), a.nbS = ceil_div(B * n, kBT);
     const uint64_t grid = (uint64_t)B * (a.nbL + a.nbR) + a.nbS + (uint64_t)ell * ell2;
     if (grid > 0x7fffffffu) return hipErrorInvalidValue;
+    a.ctrl = ctrl;
+    a.slots = count_slots((uint32_t)grid);
+    a.accL = reinterpret_cast<unsigned long long*>(ctrl + count_words(a.slots));
+    a.accR = a.accL + (size_t)ell * B;
+    a.accS = a.accR + (size_t)ell * B;
+    a.accA = a.accS + (size_t)ell * ell2;
     hipLaunchKernelGGL(batch_check_kernel, dim3((uint32_t)grid), dim3(kBT), 0, s, a);
     return hipGetLastError();
 }

@@ -15,6 +15,10 @@
 // and reduced once per workgroup; the per-workgroup partials (each < p) are
 // added into 64-bit accumulators with atomics and reduced by the last
 // workgroup.  All sums are exact, so results do not depend on the order.
+// Every (repetition, column) sum has nsub accumulators, 64 bits each, which
+// the workgroups of a column use in turn (block index mod nsub): atomics on one
+// address are serialised, so this bounds the workgroups per address.
+#include "count.h"
 #include "field.h"
 #include "mvk_internal.h"
 #include "syn_block.h"
@@ -85,9 +89,9 @@ __device__ __forceinline__ void decode_part(const uint32_t* __restrict__ PT, uin
                                             const uint32_t* __restrict__ Yhat, uint32_t B,
                                             const uint32_t* __restrict__ ex_idx, const uint32_t* __restrict__ ex_val,
                                             uint32_t tx, const uint32_t* rv, uint32_t ell,
-                                            uint32_t* __restrict__ Y, unsigned long long* accR, uint32_t b,
-                                            uint32_t cb, uint64_t (*part)[kCols], uint32_t* rdone, uint32_t* err,
-                                            const uint32_t* __restrict__ My = nullptr) {
+                                            uint32_t* __restrict__ Y, unsigned long long* accR, uint32_t nsub,
+                                            uint32_t b, uint32_t cb, uint64_t (*part)[kCols], uint32_t* rdone,
+                                            uint32_t* err, const uint32_t* __restrict__ My = nullptr) {
     const int lane = threadIdx.x & 63;
     const int g = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform group
     const uint32_t i = cb * kCols + lane;
@@ -162,18 +166,18 @@ __device__ __forceinline__ void decode_part(const uint32_t* __restrict__ PT, uin
                 r = WAIT_R ? __hip_atomic_load(&rv[(size_t)q * m + is], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
                            : rv[(size_t)q * m + is];
             const uint64_t ws = wave_sum_u64(ffold((uint64_t)r * yh));
-            if (lane == 0) atomicAdd(&accR[(size_t)q * B + b], (unsigned long long)fred64(ws));
+            if (lane == 0) atomicAdd(&accR[((size_t)q * B + b) * nsub + cb % nsub], (unsigned long long)fred64(ws));
         }
     }
 }
 
 // v_L partials of one query column: sum over this block's k of u_q[k] * x[k].
 __device__ __forceinline__ void verify_column(const uint32_t (*u_s)[kCols], uint32_t ell, uint32_t B, uint32_t b,
-                                              uint32_t x, unsigned long long* accL) {
+                                              uint32_t x, unsigned long long* accL, uint32_t nsub, uint32_t sub) {
     const int lane = threadIdx.x & 63;
     for (uint32_t q = 0; q < ell; ++q) {
         const uint64_t ws = wave_sum_u64(ffold((uint64_t)u_s[q][lane] * x));
-        if (lane == 0) atomicAdd(&accL[(size_t)q * B + b], (unsigned long long)fred64(ws));
+        if (lane == 0) atomicAdd(&accL[((size_t)q * B + b) * nsub + sub], (unsigned long long)fred64(ws));
     }
 }
 
@@ -187,8 +191,8 @@ template <int G, bool PRE = false>
 __device__ __forceinline__ void verify_part(const uint32_t* __restrict__ Q, uint32_t n, uint32_t Ny,
                                             const uint32_t* __restrict__ Xhat, uint32_t B,
                                             const uint32_t* __restrict__ ey_idx, const uint32_t* __restrict__ ey_val,
-                                            uint32_t ty, uint32_t ell, unsigned long long* accL, uint32_t cb,
-                                            uint64_t (*part)[kCols], uint32_t (*u_s)[kCols],
+                                            uint32_t ty, uint32_t ell, unsigned long long* accL, uint32_t nsub,
+                                            uint32_t cb, uint64_t (*part)[kCols], uint32_t (*u_s)[kCols],
                                             const uint32_t* __restrict__ U = nullptr) {
     static_assert(G <= kItems, "one work item per group at least");
     const int lane = threadIdx.x & 63;
@@ -243,26 +247,26 @@ __device__ __forceinline__ void verify_part(const uint32_t* __restrict__ Q, uint
 #pragma unroll
     for (int u = 0; u < kPreB; ++u) {
         const uint32_t b = (uint32_t)g + G * u;
-        if (b < B) verify_column(u_s, ell, B, b, xp[u], accL);
+        if (b < B) verify_column(u_s, ell, B, b, xp[u], accL, nsub, cb % nsub);
     }
     for (uint32_t b = (uint32_t)g + G * kPreB; b < B; b += G)
-        verify_column(u_s, ell, B, b, Xhat[(size_t)b * n + ks], accL);
+        verify_column(u_s, ell, B, b, Xhat[(size_t)b * n + ks], accL, nsub, cb % nsub);
 }
 
 // End of a decode/verify launch.  Ordering without cache-wide fences: the
 // accumulators are touched only by atomics, which are performed at the
 // device-wide coherence point.  Every wave waits for its atomics to complete
-// (vmcnt 0) before the barrier, the counter increment follows the barrier,
-// and the last workgroup reads the accumulators with atomics after seeing the
-// final count.  It clears them, resets the counter (and rdone / err, when
-// given), and writes vL, vR and accept.
-__device__ __forceinline__ void finish(uint32_t B, uint32_t ell, unsigned long long* accL,
-                                       unsigned long long* accR, uint32_t* counter, uint32_t* rdone, uint32_t* err,
-                                       uint32_t* __restrict__ vL, uint32_t* __restrict__ vR,
+// (vmcnt 0) before the barrier, the completion count (count.h) follows the
+// barrier, and the last workgroup reads the accumulators with atomics after
+// it has been found.  It clears them, resets rdone / err (when given), and
+// writes vL, vR and accept.
+__device__ __forceinline__ void finish(uint32_t B, uint32_t ell, uint32_t nsub, unsigned long long* accL,
+                                       unsigned long long* accR, uint32_t* ctrl, uint32_t slots, uint32_t* rdone,
+                                       uint32_t* err, uint32_t* __restrict__ vL, uint32_t* __restrict__ vR,
                                        uint32_t* __restrict__ accept, uint32_t* last) {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (threadIdx.x == 0) *last = (atomicAdd(counter, 1u) == gridDim.x - 1) ? 1u : 0u;
+    if (threadIdx.x == 0) *last = count_last(ctrl, slots) ? 1u : 0u;
     __syncthreads();
     if (!*last) return;
     const uint32_t bad = err ? __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
@@ -270,8 +274,12 @@ __device__ __forceinline__ void finish(uint32_t B, uint32_t ell, unsigned long l
         uint32_t ok = bad ? 0u : 1u;
         for (uint32_t q = 0; q < ell; ++q) {
             const size_t o = (size_t)q * B + b;
-            const uint32_t L = fred64(atomicExch(&accL[o], 0ull));
-            const uint32_t R = fred64(atomicExch(&accR[o], 0ull));
+            uint64_t l = 0, r = 0;  // each accumulator < 2^61
+            for (uint32_t u = 0; u < nsub; ++u) {
+                l += atomicExch(&accL[o * nsub + u], 0ull);
+                r += atomicExch(&accR[o * nsub + u], 0ull);
+            }
+            const uint32_t L = fred64(l), R = fred64(r);
             if (vL) vL[o] = L;
             if (vR) vR[o] = R;
             ok &= (L == R) ? 1u : 0u;
@@ -282,18 +290,16 @@ __device__ __forceinline__ void finish(uint32_t B, uint32_t ell, unsigned long l
     if (threadIdx.x == 0) {
         if (rdone) atomicExch(rdone, 0u);
         if (err) atomicExch(err, 0u);
-        atomicExch(counter, 0u);
     }
 }
 
 // One launch for Decrypt, the two inner products of Verify and the final
 // comparison.  Workgroups [0, B*nblkR) take the decode role, the next nblkL
 // the verify role.  Every workgroup adds its partial sums (each < p) into the
-// 64-bit accumulators accL / accR (ell x B each; exact, so the order of the
-// additions does not matter), then counts itself done on `counter`; the
-// workgroup that finishes last (it sees count == gridDim.x - 1) reads and
-// clears the accumulators, writes vL, vR and accept, and resets the counter,
-// so every launch leaves the accumulators and the counter at zero.
+// 64-bit accumulators accL / accR (ell x B x nsub each; exact, so the order of
+// the additions does not matter), then counts itself done; the workgroup that
+// finishes last reads and clears the accumulators and writes vL, vR and
+// accept, so every launch leaves the accumulators and the counters at zero.
 //
 // PRE: the output masks My and the vectors u_q (U) come from client_prepare;
 // the workgroups then only stream Yhat, My, r and U, Xhat.
@@ -304,20 +310,22 @@ __global__ __launch_bounds__(kB) void decode_verify_fused(
     const uint32_t* __restrict__ ex_idx, const uint32_t* __restrict__ ex_val, uint32_t tx,
     const uint32_t* __restrict__ ey_idx, const uint32_t* __restrict__ ey_val, uint32_t ty, uint32_t ell,
     const uint32_t* __restrict__ rv, uint32_t* __restrict__ Y, unsigned long long* accL, unsigned long long* accR,
-    uint32_t nblkR, uint32_t* counter, uint32_t* __restrict__ vL, uint32_t* __restrict__ vR,
-    uint32_t* __restrict__ accept, const uint32_t* __restrict__ My, const uint32_t* __restrict__ U) {
+    uint32_t nsub, uint32_t nblkR, uint32_t* ctrl, uint32_t slots, uint32_t* __restrict__ vL,
+    uint32_t* __restrict__ vR, uint32_t* __restrict__ accept, const uint32_t* __restrict__ My,
+    const uint32_t* __restrict__ U) {
     __shared__ uint64_t part[kItems][kCols];
     __shared__ uint32_t u_s[kMaxEll][kCols];
     __shared__ uint32_t last;
     const uint32_t bid = blockIdx.x;
     const uint32_t ndec = B * nblkR;
     if (bid < ndec)
-        decode_part<false, kGroups, PRE>(PT, m, Nx, Yhat, B, ex_idx, ex_val, tx, rv, ell, Y, accR, bid / nblkR,
-                                         bid % nblkR, part, nullptr, nullptr, My);
+        decode_part<false, kGroups, PRE>(PT, m, Nx, Yhat, B, ex_idx, ex_val, tx, rv, ell, Y, accR, nsub,
+                                         bid / nblkR, bid % nblkR, part, nullptr, nullptr, My);
     else
-        verify_part<kGroups, PRE>(Q, n, Ny, Xhat, B, ey_idx, ey_val, ty, ell, accL, bid - ndec, part, u_s, U);
+        verify_part<kGroups, PRE>(Q, n, Ny, Xhat, B, ey_idx, ey_val, ty, ell, accL, nsub, bid - ndec, part, u_s,
+                                  U);
 
-    finish(B, ell, accL, accR, counter, nullptr, nullptr, vL, vR, accept, &last);
+    finish(B, ell, nsub, accL, accR, ctrl, slots, nullptr, nullptr, vL, vR, accept, &last);
 }
 
 // Syndrome role of decode_verify_syn: r_c = Gy e_c into rv (device-coherent
@@ -360,26 +368,26 @@ __global__ __launch_bounds__(kFusedThreads) void decode_verify_syn(
     const uint32_t* __restrict__ ey_idx, const uint32_t* __restrict__ ey_val, uint32_t ty, uint32_t ell,
     uint32_t cyr, const uint32_t* __restrict__ pi1, const uint32_t* __restrict__ pi2,
     const uint32_t* __restrict__ v1, const uint32_t* __restrict__ v2, uint32_t* rv, uint32_t* __restrict__ Y,
-    unsigned long long* accL, unsigned long long* accR, uint32_t nblkR, uint32_t nblkL, uint32_t* ctrl,
-    uint32_t* __restrict__ vL, uint32_t* __restrict__ vR, uint32_t* __restrict__ accept) {
+    unsigned long long* accL, unsigned long long* accR, uint32_t nsub, uint32_t nblkR, uint32_t nblkL,
+    uint32_t* ctrl, uint32_t slots, uint32_t* __restrict__ vL, uint32_t* __restrict__ vR,
+    uint32_t* __restrict__ accept) {
     __shared__ __align__(16) uint32_t lds[fused_lds_words<U>()];
     __shared__ uint32_t last;
     auto part = reinterpret_cast<uint64_t (*)[kCols]>(lds);
     auto u_s = reinterpret_cast<uint32_t (*)[kCols]>(lds + 2 * kItems * kCols);
-    uint32_t* counter = &ctrl[0];
     uint32_t* rdone = &ctrl[1];
     uint32_t* err = &ctrl[2];
     const uint32_t bid = blockIdx.x;
     if (bid < ell)
         syn_part<U>(bid, m, cyr, pi1, pi2, v1, v2, ey_idx, ey_val, ty, rv, rdone, lds);
     else if (bid < ell + nblkL)
-        verify_part<kFusedGroups>(Q, n, Ny, Xhat, B, ey_idx, ey_val, ty, ell, accL, bid - ell, part, u_s);
+        verify_part<kFusedGroups>(Q, n, Ny, Xhat, B, ey_idx, ey_val, ty, ell, accL, nsub, bid - ell, part, u_s);
     else {
         const uint32_t d = bid - ell - nblkL;
-        decode_part<true, kFusedGroups>(PT, m, Nx, Yhat, B, ex_idx, ex_val, tx, rv, ell, Y, accR, d / nblkR,
+        decode_part<true, kFusedGroups>(PT, m, Nx, Yhat, B, ex_idx, ex_val, tx, rv, ell, Y, accR, nsub, d / nblkR,
                                         d % nblkR, part, rdone, err);
     }
-    finish(B, ell, accL, accR, counter, rdone, err, vL, vR, accept, &last);
+    finish(B, ell, nsub, accL, accR, ctrl, slots, rdone, err, vL, vR, accept, &last);
 }
 
 // decode_verify_masked for small problems, by a few workgroups (at most 8):
@@ -510,6 +518,33 @@ int fused_blocks_per_cu() {
 
 }  // namespace
 
+namespace {
+// Control region of a decode/verify launch: the counters (count.h; rdone and
+// err in words 1 and 2 of the top counter's line), then the accumulators,
+// 2 x ell x B x nsub 64-bit words.  Sized for the largest grid of the three
+// kernels, so that one layout serves every call with the same (m, n, B, ell).
+struct DvLayout {
+    uint32_t slots, nsub;
+    size_t acc_word;  // first accumulator, in 32-bit words from ctrl
+    size_t bytes;
+};
+
+DvLayout dv_layout(uint32_t m, uint32_t n, uint32_t B, uint32_t ell) {
+    const uint32_t nblkL = ceil_div(n, kCols), nblkR = ceil_div(m, kCols);
+    const uint64_t grid = (uint64_t)B * nblkR + nblkL + ell;
+    DvLayout l;
+    l.slots = count_slots(grid > 0xffffffffull ? 0xffffffffu : (uint32_t)grid);
+    // workgroups per accumulator address: at most ~32
+    const uint32_t per = nblkR > nblkL ? nblkR : nblkL;
+    l.nsub = per <= 32 ? 1u : (per >= 8 * 32 ? 8u : ceil_div(per, 32u));
+    l.acc_word = count_words(l.slots);
+    l.bytes = l.acc_word * 4 + (size_t)2 * ell * B * l.nsub * 8;
+    return l;
+}
+}  // namespace
+
+size_t dv_ctrl_bytes(uint32_t m, uint32_t n, uint32_t B, uint32_t ell) { return dv_layout(m, n, B, ell).bytes; }
+
 uint32_t dv_syn_u(uint32_t Ny) {
     for (uint32_t U : {8u, 16u, 24u, 32u})
         if (Ny <= (uint32_t)kFusedThreads * U) return U;
@@ -541,16 +576,19 @@ hipError_t launch_decode_verify_syn(const uint32_t* PT, const uint32_t* Q, uint3
                                     const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx,
                                     const uint32_t* ey_idx, const uint32_t* ey_val, uint32_t ty, uint32_t ell,
                                     uint32_t cyr, const uint32_t* pi1, const uint32_t* pi2, const uint32_t* v1,
-                                    const uint32_t* v2, uint32_t* r, uint32_t* Y, unsigned long long* acc,
-                                    uint32_t* ctrl, uint32_t* vL, uint32_t* vR, uint32_t* accept, hipStream_t s) {
+                                    const uint32_t* v2, uint32_t* r, uint32_t* Y, uint32_t* ctrl, uint32_t* vL,
+                                    uint32_t* vR, uint32_t* accept, hipStream_t s) {
     const uint32_t U = dv_syn_u(Ny);
     if (U == 0 || ell == 0 || ell > (uint32_t)kMaxEll || (uint64_t)cyr * m != Ny) return hipErrorInvalidValue;
     const uint32_t nblkL = ceil_div(n, kCols), nblkR = ceil_div(m, kCols);
     const uint32_t grid = ell + nblkL + B * nblkR;
+    const DvLayout l = dv_layout(m, n, B, ell);
+    unsigned long long* acc = reinterpret_cast<unsigned long long*>(ctrl + l.acc_word);
+    const uint32_t slots = count_slots(grid);
 #define MVK_DVS(UU)                                                                                               \
     hipLaunchKernelGGL(decode_verify_syn<UU>, dim3(grid), dim3(kFusedThreads), 0, s, PT, Q, m, n, Nx, Ny, Xhat,   \
                        Yhat, B, ex_idx, ex_val, tx, ey_idx, ey_val, ty, ell, cyr, pi1, pi2, v1, v2, r, Y, acc,     \
-                       acc + (size_t)ell * B, nblkR, nblkL, ctrl, vL, vR, accept)
+                       acc + (size_t)ell * B * l.nsub, l.nsub, nblkR, nblkL, ctrl, slots, vL, vR, accept)
     if (U == 8) MVK_DVS(8);
     else if (U == 16) MVK_DVS(16);
     else if (U == 24) MVK_DVS(24);
@@ -563,22 +601,26 @@ hipError_t launch_decode_verify(const uint32_t* PT, const uint32_t* Q, uint32_t 
                                 uint32_t Ny, const uint32_t* Xhat, const uint32_t* Yhat, uint32_t B,
                                 const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx, const uint32_t* ey_idx,
                                 const uint32_t* ey_val, uint32_t ty, uint32_t ell, const uint32_t* r, uint32_t* Y,
-                                unsigned long long* acc, uint32_t* counter, uint32_t* vL, uint32_t* vR,
-                                uint32_t* accept, hipStream_t s) {
+                                uint32_t* ctrl, uint32_t* vL, uint32_t* vR, uint32_t* accept, hipStream_t s) {
     if (ell == 0 || ell > (uint32_t)kMaxEll) return hipErrorInvalidValue;
     const uint32_t nblkL = ceil_div(n, kCols), nblkR = ceil_div(m, kCols);
     const uint32_t grid = B * nblkR + nblkL;
+    const DvLayout l = dv_layout(m, n, B, ell);
+    unsigned long long* acc = reinterpret_cast<unsigned long long*>(ctrl + l.acc_word);
     hipLaunchKernelGGL(decode_verify_fused<false>, dim3(grid), dim3(kB), 0, s, PT, Q, m, n, Nx, Ny, Xhat, Yhat, B,
-                       ex_idx, ex_val, tx, ey_idx, ey_val, ty, ell, r, Y, acc, acc + (size_t)ell * B, nblkR, counter,
-                       vL, vR, accept, nullptr, nullptr);
+                       ex_idx, ex_val, tx, ey_idx, ey_val, ty, ell, r, Y, acc, acc + (size_t)ell * B * l.nsub, l.nsub,
+                       nblkR, ctrl, count_slots(grid), vL, vR, accept, nullptr, nullptr);
     return hipGetLastError();
 }
 
 hipError_t launch_decode_verify_masked(uint32_t m, uint32_t n, const uint32_t* Xhat, const uint32_t* Yhat,
                                        uint32_t B, const uint32_t* My, uint32_t ell, const uint32_t* r,
-                                       const uint32_t* U, uint32_t* Y, unsigned long long* acc, uint32_t* counter,
-                                       uint32_t* vL, uint32_t* vR, uint32_t* accept, hipStream_t s) {
+                                       const uint32_t* U, uint32_t* Y, uint32_t* ctrl, uint32_t* vL, uint32_t* vR,
+                                       uint32_t* accept, hipStream_t s) {
     if (ell == 0 || ell > (uint32_t)kMaxEll) return hipErrorInvalidValue;
+    const DvLayout l = dv_layout(m, n, B, ell);
+    unsigned long long* acc = reinterpret_cast<unsigned long long*>(ctrl + l.acc_word);
+    uint32_t* counter = ctrl;
     if ((uint64_t)B * ((uint64_t)m + n) <= kSmallDvWords && ell <= 4) {
         // one element per thread and pass over up to 8 workgroups, then 4
         const uint32_t len = m > n ? m : n;
@@ -599,8 +641,8 @@ hipError_t launch_decode_verify_masked(uint32_t m, uint32_t n, const uint32_t* X
     const uint32_t nblkL = ceil_div(n, kCols), nblkR = ceil_div(m, kCols);
     const uint32_t grid = B * nblkR + nblkL;
     hipLaunchKernelGGL(decode_verify_fused<true>, dim3(grid), dim3(kB), 0, s, nullptr, nullptr, m, n, 0u, 0u, Xhat,
-                       Yhat, B, nullptr, nullptr, 0u, nullptr, nullptr, 0u, ell, r, Y, acc, acc + (size_t)ell * B,
-                       nblkR, counter, vL, vR, accept, My, U);
+                       Yhat, B, nullptr, nullptr, 0u, nullptr, nullptr, 0u, ell, r, Y, acc,
+                       acc + (size_t)ell * B * l.nsub, l.nsub, nblkR, ctrl, count_slots(grid), vL, vR, accept, My, U);
     return hipGetLastError();
 }
 

@@ -62,23 +62,24 @@ hipError_t launch_fill_u32(uint32_t* p, size_t count, uint32_t value, hipStream_
 constexpr uint32_t kClientBlock = 256;  // threads per workgroup of the gather kernels
 constexpr uint32_t kClientCols = 64;    // output columns per workgroup of the gather kernels
 // Decrypt + Verify in one launch (see client.hip).  r: ell x m words,
-// r_q = Gy e_q.  acc: 2*ell*B 64-bit accumulators and counter: one word, all
-// zero before the first launch (every launch leaves them at zero).
+// r_q = Gy e_q.  ctrl: dv_ctrl_bytes(m, n, B, ell) bytes of control region
+// (completion counters, then the 64-bit accumulators), zero before the first
+// launch and left at zero by every launch of the three decode/verify kernels.
 // ell <= kMaxEll.
 constexpr uint32_t kMaxEll = 16;
+size_t dv_ctrl_bytes(uint32_t m, uint32_t n, uint32_t B, uint32_t ell);
 hipError_t launch_decode_verify(const uint32_t* PT, const uint32_t* Q, uint32_t m, uint32_t n, uint32_t Nx,
                                 uint32_t Ny, const uint32_t* Xhat, const uint32_t* Yhat, uint32_t B,
                                 const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx, const uint32_t* ey_idx,
                                 const uint32_t* ey_val, uint32_t ty, uint32_t ell, const uint32_t* r, uint32_t* Y,
-                                unsigned long long* acc, uint32_t* counter, uint32_t* vL, uint32_t* vR,
-                                uint32_t* accept, hipStream_t s);
+                                uint32_t* ctrl, uint32_t* vL, uint32_t* vR, uint32_t* accept, hipStream_t s);
 
 // The same with the challenge syndromes r_q = Gy e_q computed in the launch
 // (written to r, ell x m words) by 512-thread workgroups that hold a whole
-// block of Ny = cyr * m positions in LDS.  ctrl: words 0 (counter), 1 and 2
-// (syndrome completion count, wait time-out flag), zero before the first
-// launch and left at zero.  dv_syn_fits: the launch applies (Ny small enough,
-// every workgroup resident at once on the current device).
+// block of Ny = cyr * m positions in LDS.  ctrl as above; its words 1 and 2
+// hold the syndrome completion count and the wait time-out flag.
+// dv_syn_fits: the launch applies (Ny small enough, every workgroup resident
+// at once on the current device).
 constexpr uint32_t kDvSynThreads = 512;
 uint32_t dv_syn_u(uint32_t Ny);
 bool dv_syn_fits(uint32_t m, uint32_t n, uint32_t Ny, uint32_t B, uint32_t ell);
@@ -87,22 +88,24 @@ hipError_t launch_decode_verify_syn(const uint32_t* PT, const uint32_t* Q, uint3
                                     const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx,
                                     const uint32_t* ey_idx, const uint32_t* ey_val, uint32_t ty, uint32_t ell,
                                     uint32_t cyr, const uint32_t* pi1, const uint32_t* pi2, const uint32_t* v1,
-                                    const uint32_t* v2, uint32_t* r, uint32_t* Y, unsigned long long* acc,
-                                    uint32_t* ctrl, uint32_t* vL, uint32_t* vR, uint32_t* accept, hipStream_t s);
+                                    const uint32_t* v2, uint32_t* r, uint32_t* Y, uint32_t* ctrl, uint32_t* vL,
+                                    uint32_t* vR, uint32_t* accept, hipStream_t s);
 
 // decode_verify with the output masks My (B x m) and the vectors u_q (U,
 // ell x n) from client_prepare in place of the gathers.
 hipError_t launch_decode_verify_masked(uint32_t m, uint32_t n, const uint32_t* Xhat, const uint32_t* Yhat,
                                        uint32_t B, const uint32_t* My, uint32_t ell, const uint32_t* r,
-                                       const uint32_t* U, uint32_t* Y, unsigned long long* acc, uint32_t* counter,
-                                       uint32_t* vL, uint32_t* vR, uint32_t* accept, hipStream_t s);
+                                       const uint32_t* U, uint32_t* Y, uint32_t* ctrl, uint32_t* vL, uint32_t* vR,
+                                       uint32_t* accept, hipStream_t s);
 
 // prepare.hip ---------------------------------------------------------------
 // Mx, My for nx noise vectors and R, U for ny challenges (either count may
 // be 0).  scratch: max(nx * 2 * Nx, ny * 2 * Ny) words when that block length
 // is above kSynScratchAbove, else unused.  done (may be null): set to
 // done_value once every output is stored and visible device-wide; counter:
-// a word that is zero before the launch (left zero).
+// prep_ctrl_words(key, nx, ny) words of completion counters (count.h), zero
+// before the launch (left zero).
+size_t prep_ctrl_words(const mvk_key& key, uint32_t nx, uint32_t ny);
 hipError_t launch_client_prepare(const mvk_key& key, const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx,
                                  uint32_t nx, const uint32_t* ey_idx, const uint32_t* ey_val, uint32_t ty,
                                  uint32_t ny, uint32_t* Mx, uint32_t* My, uint32_t* R, uint32_t* Uq,
@@ -123,14 +126,17 @@ hipError_t launch_flag_wait(uint32_t* flag, uint32_t value, uint32_t timeout_us,
 
 // batch.hip -----------------------------------------------------------------
 // Client checks of batch verification.  R: ell x m primary syndromes G e_q;
-// Rs: ell2 x Bn secondary syndromes G' e'_j; acc: 2*ell*B + 2*ell*ell2 64-bit
-// accumulators and counter: one word, zero before the launch (left zero).
+// Rs: ell2 x Bn secondary syndromes G' e'_j; ctrl: batch_ctrl_bytes(...) of
+// control region.
 hipError_t launch_batch_check(uint32_t m, uint32_t n, uint32_t B, const uint32_t* X, const uint32_t* Y,
                               const uint32_t* Ut, const uint32_t* R, const uint32_t* Rs, const uint32_t* Qaux,
                               uint32_t N, uint32_t N2, const uint32_t* e_idx, const uint32_t* e_val, uint32_t t,
                               uint32_t ell, const uint32_t* e2_idx, const uint32_t* e2_val, uint32_t t2,
-                              uint32_t ell2, unsigned long long* acc, uint32_t* counter, uint32_t* vL, uint32_t* vR,
-                              uint32_t* sL, uint32_t* sR, uint32_t* accept, hipStream_t s);
+                              uint32_t ell2, uint32_t* ctrl, uint32_t* vL, uint32_t* vR, uint32_t* sL, uint32_t* sR,
+                              uint32_t* accept, hipStream_t s);
+// Control bytes of launch_batch_check (completion counters, then the 64-bit
+// accumulators), zero before the launch and left at zero.
+size_t batch_ctrl_bytes(uint32_t m, uint32_t n, uint32_t B, uint32_t ell, uint32_t ell2);
 
 inline uint32_t ceil_div(uint32_t a, uint32_t b) { return (a + b - 1) / b; }
 

@@ -11,6 +11,7 @@
 // plus the two online element-wise steps and the stream flags that order a
 // preparation stream against the online stream when both are captured in
 // separate HIP graphs.
+#include "count.h"
 #include "field.h"
 #include "mvk_internal.h"
 #include "syn_block.h"
@@ -100,7 +101,8 @@ struct PrepArgs {
     uint32_t* My;
     uint32_t* R;
     uint32_t* Uq;
-    uint32_t* counter;  // SIG: workgroups done (zero before and after the launch)
+    uint32_t* counter;  // SIG: completion counters (count.h; zero before and after the launch)
+    uint32_t slots;
     uint32_t* done;     // SIG: set to done_value once every output is stored
     uint32_t done_value;
 };
@@ -110,9 +112,9 @@ struct PrepArgs {
 // nx * ceil(m/64) items of My (rows of PT), then the ny * ceil(n/64) items of
 // U (rows of Q).
 // SIG: every output is stored device-coherently; each workgroup waits for its
-// stores to complete (vmcnt 0) before the barrier and then counts itself done;
-// the last one resets the counter and sets the done flag, so a kernel of
-// another stream that sees the flag sees every output.
+// stores to complete (vmcnt 0) before the barrier and then counts itself done
+// (count.h); the last one sets the done flag, so a kernel of another stream
+// that sees the flag sees every output.
 template <int U, bool SIG>
 __global__ __launch_bounds__(kPrepThreads) void client_prepare_kernel(PrepArgs a) {
     __shared__ __align__(16) uint32_t lds[prep_lds_words<U>()];
@@ -152,10 +154,8 @@ __global__ __launch_bounds__(kPrepThreads) void client_prepare_kernel(PrepArgs a
     if constexpr (SIG) {
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
-        if (threadIdx.x == 0 && atomicAdd(a.counter, 1u) == gridDim.x - 1) {
-            atomicExch(a.counter, 0u);
+        if (threadIdx.x == 0 && count_last(a.counter, a.slots))
             __hip_atomic_store(a.done, a.done_value, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
     }
 }
 
@@ -287,7 +287,21 @@ uint32_t prep_u(uint64_t N) {
     return 0;
 }
 
+// Workgroups of client_prepare_kernel: one per syndrome short enough for one
+// workgroup, then the gather items, kQuarters per workgroup.
+uint64_t prep_grid(const mvk_key& key, uint32_t nx, uint32_t ny) {
+    const uint64_t Nx = (uint64_t)key.cx.r * key.n, Ny = (uint64_t)key.cy.r * key.m;
+    const uint32_t ux = nx ? prep_u(Nx) : 0u, uy = ny ? prep_u(Ny) : 0u;
+    const uint64_t items = (uint64_t)nx * ceil_div(key.m, kQCols) + (uint64_t)ny * ceil_div(key.n, kQCols);
+    return (ux ? nx : 0u) + (uy ? ny : 0u) + (items + kQuarters - 1) / kQuarters;
+}
+
 }  // namespace
+
+size_t prep_ctrl_words(const mvk_key& key, uint32_t nx, uint32_t ny) {
+    const uint64_t grid = prep_grid(key, nx, ny);
+    return count_words(count_slots(grid > 0x7fffffffu ? 0x7fffffffu : (uint32_t)grid));
+}
 
 hipError_t launch_client_prepare(const mvk_key& key, const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx,
                                  uint32_t nx, const uint32_t* ey_idx, const uint32_t* ey_val, uint32_t ty,
@@ -320,11 +334,11 @@ hipError_t launch_client_prepare(const mvk_key& key, const uint32_t* ex_idx, con
     a.PT = key.PT, a.Q = key.Q;
     a.Mx = Mx, a.My = My, a.R = R, a.Uq = Uq;
     a.counter = counter, a.done = done, a.done_value = done_value;
-    const uint64_t items = (uint64_t)nx * ceil_div(key.m, kQCols) + (uint64_t)ny * ceil_div(key.n, kQCols);
     const uint32_t U = ux > uy ? ux : uy;
-    const uint64_t grid = (U ? a.nsx + a.nsy : 0u) + (items + kQuarters - 1) / kQuarters;
+    const uint64_t grid = prep_grid(key, nx, ny);
     if (grid == 0) return hipSuccess;
     if (grid > 0x7fffffffu) return hipErrorInvalidValue;
+    a.slots = count_slots((uint32_t)grid);
 #define MVK_PREP(UU)                                                                                        \
     if (done)                                                                                               \
         hipLaunchKernelGGL((client_prepare_kernel<UU, true>), dim3((uint32_t)grid), dim3(kPrepThreads), 0, s, a); \

@@ -66,8 +66,9 @@ constexpr int kItems = kMaxEll;  // verify work items (repetition, chunk) per wo
 // syndrome of a block of up to 512 * 32 = 16384 positions in LDS.
 constexpr int kFusedThreads = kDvSynThreads;
 
-// decode_verify_masked runs in one workgroup up to this many words of
-// responses plus queries (B * (m + n)) and up to 4 repetitions, else on the
+// decode_verify_masked runs on decode_verify_small (at most 8 workgroups) up
+// to this many words of responses plus queries (B * (m + n)) and up to 4
+// repetitions; above, on decode_verify_wide (up to 4 repetitions) or the
 // multi-workgroup kernel above.
 constexpr uint64_t kSmallDvWords = 32768;
 constexpr int kFusedGroups = kFusedThreads / kCols;
@@ -508,6 +509,121 @@ __global__ __launch_bounds__(kSmallThreads) void decode_verify_small(
     if (tid == 0) atomicExch(counter, 0u);
 }
 
+// Transpose-reduction mod p of V values per lane over the 64 lanes of a wave:
+// each step sends half of the live values to the partner lane and keeps the
+// other half, so V - 1 + 6 - log2 V exchanges in all.  Afterwards lane L holds
+// the wave-wide sum of value index L >> (6 - log2 V).
+template <int V>
+__device__ __forceinline__ uint32_t wave_xreduce_mod(uint32_t (&a)[V], int lane) {
+    constexpr int LOGV = (V == 64) ? 6 : (V == 32) ? 5 : (V == 16) ? 4 : (V == 8) ? 3 : -1;
+    static_assert(LOGV > 0, "V must be 8, 16, 32 or 64");
+#pragma unroll
+    for (int step = 0; step < LOGV; ++step) {
+        const int s = 32 >> step;
+        const int half = V >> (step + 1);
+        const bool up = (lane & s) != 0;
+#pragma unroll
+        for (int i = 0; i < half; ++i) {
+            const uint32_t send = up ? a[i] : a[i + half];
+            const uint32_t keep = up ? a[i + half] : a[i];
+            a[i] = fadd(keep, (uint32_t)__shfl_xor((int)send, s));
+        }
+    }
+    uint32_t v = a[0];
+#pragma unroll
+    for (int s = 32 >> LOGV; s >= 1; s >>= 1) v = fadd(v, (uint32_t)__shfl_xor((int)v, s));
+    return v;
+}
+
+// decode_verify_masked for larger problems (ell <= EL): workgroup (element
+// block eb, column group) takes the elements j = 1024 eb + t + 256 u (u < 4)
+// of thread t, as outputs i (Y_b[i] = Yhat_b[i] - My_b[i] and the v_R terms
+// R_q[i] Yhat_b[i]) and as inputs k (the v_L terms U_q[k] Xhat_b[k]), for
+// kWideCols columns b; every load of the workgroup is issued before the first
+// is used (addresses clamped in range, terms masked).  Per thread the 2 EL C
+// sums are reduced mod p, across the wave by a transpose-reduction and across
+// the waves in LDS, and added into the accumulators (sum of column b,
+// repetition q: nsub of them, used by element block mod nsub); the last
+// workgroup (count.h) compares.  C = 16 / EL columns keep 32 sums per thread.
+constexpr int kWideThreads = 256, kWidePer = 4;
+constexpr uint32_t kWideElems = kWideThreads * kWidePer;
+template <int EL>
+constexpr int wide_cols() { return 16 / EL; }
+template <int EL>
+__global__ __launch_bounds__(kWideThreads) void decode_verify_wide(
+    uint32_t m, uint32_t n, const uint32_t* __restrict__ Xhat, const uint32_t* __restrict__ Yhat, uint32_t B,
+    const uint32_t* __restrict__ My, uint32_t ell, const uint32_t* __restrict__ R, const uint32_t* __restrict__ U,
+    uint32_t* __restrict__ Y, unsigned long long* accL, unsigned long long* accR, uint32_t nsub, uint32_t neb,
+    uint32_t* ctrl, uint32_t slots, uint32_t* __restrict__ vL, uint32_t* __restrict__ vR,
+    uint32_t* __restrict__ accept) {
+    constexpr int NW = kWideThreads / 64, C = wide_cols<EL>(), V = 2 * EL * C;
+    __shared__ uint32_t red[NW][V];
+    __shared__ uint32_t last;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const uint32_t eb = blockIdx.x % neb, b0 = (blockIdx.x / neb) * C;
+    const uint32_t base = eb * kWideElems + (uint32_t)tid;
+    uint32_t rv[EL][kWidePer], uv[EL][kWidePer], yv[C][kWidePer], mv[C][kWidePer], xv[C][kWidePer];
+#pragma unroll
+    for (int u = 0; u < kWidePer; ++u) {
+        const uint32_t j = base + kWideThreads * u;
+        const uint32_t i = j < m ? j : m - 1, k = j < n ? j : n - 1;
+#pragma unroll
+        for (int q = 0; q < EL; ++q) {
+            const uint32_t qs = (uint32_t)q < ell ? (uint32_t)q : 0u;
+            rv[q][u] = R[(size_t)qs * m + i];
+            uv[q][u] = U[(size_t)qs * n + k];
+        }
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const uint32_t b = b0 + c < B ? b0 + c : B - 1;
+            yv[c][u] = Yhat[(size_t)b * m + i];
+            mv[c][u] = My[(size_t)b * m + i];
+            xv[c][u] = Xhat[(size_t)b * n + k];
+        }
+    }
+    uint32_t a[V];  // index (c * EL + q) * 2 + side; side 0: v_L, 1: v_R
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        uint64_t l[EL], r[EL];
+#pragma unroll
+        for (int q = 0; q < EL; ++q) l[q] = r[q] = 0;
+#pragma unroll
+        for (int u = 0; u < kWidePer; ++u) {
+            const uint32_t j = base + kWideThreads * u;
+            // pinned before the guarded store (see decode_verify_small)
+            uint32_t yo = fsub(yv[c][u], mv[c][u]);
+            asm volatile("" : "+v"(yo));
+            if (j < m && b0 + c < B) Y[(size_t)(b0 + c) * m + j] = yo;
+            const uint32_t y = j < m ? yv[c][u] : 0u, x = j < n ? xv[c][u] : 0u;
+#pragma unroll
+            for (int q = 0; q < EL; ++q) {
+                r[q] += ffold((uint64_t)rv[q][u] * y);
+                l[q] += ffold((uint64_t)uv[q][u] * x);
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < EL; ++q) {
+            a[(c * EL + q) * 2] = fred64(l[q]);
+            a[(c * EL + q) * 2 + 1] = fred64(r[q]);
+        }
+    }
+    const uint32_t w = wave_xreduce_mod<V>(a, lane);
+    constexpr int SH = (V == 64) ? 0 : (V == 32) ? 1 : (V == 16) ? 2 : 3;
+    if ((lane & ((1 << SH) - 1)) == 0) red[wave][lane >> SH] = w;
+    __syncthreads();
+    if (tid < V) {
+        uint32_t tot = 0;
+#pragma unroll
+        for (int h = 0; h < NW; ++h) tot = fadd(tot, red[h][tid]);
+        const uint32_t side = (uint32_t)tid & 1u, q = ((uint32_t)tid >> 1) % EL, c = ((uint32_t)tid >> 1) / EL;
+        if (q < ell && b0 + c < B) {
+            unsigned long long* acc = side ? accR : accL;
+            atomicAdd(&acc[((size_t)q * B + b0 + c) * nsub + eb % nsub], (unsigned long long)tot);
+        }
+    }
+    finish(B, ell, nsub, accL, accR, ctrl, slots, nullptr, nullptr, vL, vR, accept, &last);
+}
+
 template <int U>
 int fused_blocks_per_cu() {
     int nb = 0;
@@ -636,6 +752,23 @@ hipError_t launch_decode_verify_masked(uint32_t m, uint32_t n, const uint32_t* X
             if (one) MVK_DVS(4, 1); else MVK_DVS(4, 4);
         }
 #undef MVK_DVS
+        return hipGetLastError();
+    }
+    if (ell <= 4) {
+        // element blocks x column groups, all loads of a workgroup in flight together
+        const uint32_t len = m > n ? m : n;
+        const uint32_t neb = ceil_div(len, kWideElems);
+        const uint32_t cols = ell <= 2 ? wide_cols<2>() : wide_cols<4>();
+        const uint64_t grid = (uint64_t)neb * ceil_div(B, cols);
+        if (grid > 0x7fffffffu) return hipErrorInvalidValue;
+        const uint32_t slots = count_slots((uint32_t)grid);
+        if (count_words(slots) > l.acc_word) return hipErrorInvalidValue;  // the layout holds the counters
+#define MVK_DVW(EL)                                                                                           \
+    hipLaunchKernelGGL(decode_verify_wide<EL>, dim3((uint32_t)grid), dim3(kWideThreads), 0, s, m, n, Xhat, Yhat, B, \
+                       My, ell, r, U, Y, acc, acc + (size_t)ell * B * l.nsub, l.nsub, neb, ctrl, slots, vL, vR,  \
+                       accept)
+        if (ell <= 2) MVK_DVW(2); else MVK_DVW(4);
+#undef MVK_DVW
         return hipGetLastError();
     }
     const uint32_t nblkL = ceil_div(n, kCols), nblkR = ceil_div(m, kCols);

@@ -536,27 +536,27 @@ __device__ __forceinline__ uint32_t wave_xreduce_mod(uint32_t (&a)[V], int lane)
 }
 
 // decode_verify_masked for larger problems (ell <= EL): workgroup (element
-// block eb, column group) takes the elements j = 1024 eb + t + 256 u (u < 4)
-// of thread t, as outputs i (Y_b[i] = Yhat_b[i] - My_b[i] and the v_R terms
-// R_q[i] Yhat_b[i]) and as inputs k (the v_L terms U_q[k] Xhat_b[k]), for
-// kWideCols columns b; every load of the workgroup is issued before the first
-// is used (addresses clamped in range, terms masked).  Per thread the 2 EL C
-// sums are reduced mod p, across the wave by a transpose-reduction and across
-// the waves in LDS, and added into the accumulators (sum of column b,
-// repetition q: nsub of them, used by element block mod nsub); the last
-// workgroup (count.h) compares.  C = 16 / EL columns keep 32 sums per thread.
-constexpr int kWideThreads = 256, kWidePer = 4;
-constexpr uint32_t kWideElems = kWideThreads * kWidePer;
-template <int EL>
-constexpr int wide_cols() { return 16 / EL; }
-template <int EL>
+// block eb, column group) takes the elements j = 256 PER eb + t + 256 u
+// (u < PER) of thread t, as outputs i (Y_b[i] = Yhat_b[i] - My_b[i] and the
+// v_R terms R_q[i] Yhat_b[i]) and as inputs k (the v_L terms U_q[k]
+// Xhat_b[k]), for C columns b; every load of the workgroup is issued before
+// the first is used (addresses clamped in range, terms masked).  Per thread
+// the 2 EL C sums are reduced mod p, across the wave by a transpose-reduction
+// and across the waves in LDS, and added into the accumulators (sum of column
+// b, repetition q: nsub of them, used by element block mod nsub); the last
+// workgroup (count.h) compares.  The host picks PER and C so that the grid
+// has a few hundred workgroups where the problem allows.
+constexpr int kWideThreads = 256;
+template <int EL, int C, int PER>
 __global__ __launch_bounds__(kWideThreads) void decode_verify_wide(
     uint32_t m, uint32_t n, const uint32_t* __restrict__ Xhat, const uint32_t* __restrict__ Yhat, uint32_t B,
     const uint32_t* __restrict__ My, uint32_t ell, const uint32_t* __restrict__ R, const uint32_t* __restrict__ U,
     uint32_t* __restrict__ Y, unsigned long long* accL, unsigned long long* accR, uint32_t nsub, uint32_t neb,
     uint32_t* ctrl, uint32_t slots, uint32_t* __restrict__ vL, uint32_t* __restrict__ vR,
     uint32_t* __restrict__ accept) {
-    constexpr int NW = kWideThreads / 64, C = wide_cols<EL>(), V = 2 * EL * C;
+    constexpr int NW = kWideThreads / 64, V = 2 * EL * C;
+    constexpr int kWidePer = PER;
+    constexpr uint32_t kWideElems = kWideThreads * PER;
     __shared__ uint32_t red[NW][V];
     __shared__ uint32_t last;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -647,7 +647,11 @@ struct DvLayout {
 
 DvLayout dv_layout(uint32_t m, uint32_t n, uint32_t B, uint32_t ell) {
     const uint32_t nblkL = ceil_div(n, kCols), nblkR = ceil_div(m, kCols);
-    const uint64_t grid = (uint64_t)B * nblkR + nblkL + ell;
+    // the largest grid: decode_verify_syn, or decode_verify_wide with one
+    // element per thread and one column per workgroup
+    const uint64_t g_fused = (uint64_t)B * nblkR + nblkL + ell;
+    const uint64_t g_wide = (uint64_t)ceil_div(m > n ? m : n, (uint32_t)kWideThreads) * B;
+    const uint64_t grid = g_fused > g_wide ? g_fused : g_wide;
     DvLayout l;
     l.slots = count_slots(grid > 0xffffffffull ? 0xffffffffu : (uint32_t)grid);
     // workgroups per accumulator address: at most ~32
@@ -755,19 +759,27 @@ hipError_t launch_decode_verify_masked(uint32_t m, uint32_t n, const uint32_t* X
         return hipGetLastError();
     }
     if (ell <= 4) {
-        // element blocks x column groups, all loads of a workgroup in flight together
+        // element blocks x column groups, all loads of a workgroup in flight
+        // together: 4 elements per thread and 16 / EL columns per workgroup, or
+        // (grids below 256 workgroups) 1 element and 4 / EL columns
         const uint32_t len = m > n ? m : n;
-        const uint32_t neb = ceil_div(len, kWideElems);
-        const uint32_t cols = ell <= 2 ? wide_cols<2>() : wide_cols<4>();
+        const uint32_t el = ell <= 2 ? 2u : 4u;
+        bool wide = (uint64_t)ceil_div(len, 4u * kWideThreads) * ceil_div(B, 16u / el) >= 256u;
+        const uint32_t per = wide ? 4u : 1u, cols = wide ? 16u / el : 4u / el;
+        const uint32_t neb = ceil_div(len, per * kWideThreads);
         const uint64_t grid = (uint64_t)neb * ceil_div(B, cols);
         if (grid > 0x7fffffffu) return hipErrorInvalidValue;
         const uint32_t slots = count_slots((uint32_t)grid);
         if (count_words(slots) > l.acc_word) return hipErrorInvalidValue;  // the layout holds the counters
-#define MVK_DVW(EL)                                                                                           \
-    hipLaunchKernelGGL(decode_verify_wide<EL>, dim3((uint32_t)grid), dim3(kWideThreads), 0, s, m, n, Xhat, Yhat, B, \
-                       My, ell, r, U, Y, acc, acc + (size_t)ell * B * l.nsub, l.nsub, neb, ctrl, slots, vL, vR,  \
-                       accept)
-        if (ell <= 2) MVK_DVW(2); else MVK_DVW(4);
+#define MVK_DVW(EL, C, PER)                                                                                  \
+    hipLaunchKernelGGL((decode_verify_wide<EL, C, PER>), dim3((uint32_t)grid), dim3(kWideThreads), 0, s, m, n,  \
+                       Xhat, Yhat, B, My, ell, r, U, Y, acc, acc + (size_t)ell * B * l.nsub, l.nsub, neb, ctrl,  \
+                       slots, vL, vR, accept)
+        if (el == 2) {
+            if (wide) MVK_DVW(2, 8, 4); else MVK_DVW(2, 2, 1);
+        } else {
+            if (wide) MVK_DVW(4, 4, 4); else MVK_DVW(4, 1, 1);
+        }
 #undef MVK_DVW
         return hipGetLastError();
     }

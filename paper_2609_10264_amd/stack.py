@@ -13,6 +13,12 @@ Codes are shared per shape (one privacy code per input width n, one
 verification code per output height m); P^T and Q are per matrix.  This module
 only orchestrates calls of the C ABI (through the binding); all arithmetic runs
 in the HIP kernels.
+
+Two schedules of a layer: run_layer (the one-call path: encode, server_eval,
+decode_verify) and prepare_layer + run_layer_prepared (the standard mode with
+precomputation, Sec. 7: the masks and challenge vectors depend on neither the
+queries nor the responses, so a preparation stream computes them ahead and
+the online calls only add masks, evaluate and check).
 """
 from __future__ import annotations
 
@@ -20,7 +26,8 @@ from dataclasses import dataclass, field
 
 import torch
 
-from . import Code, Key, decode_verify, encode, keygen, pack_weights, server_eval
+from . import (Code, Key, Prepared, client_prepare, decode_verify, decode_verify_masked, encode, encode_masked, keygen,
+               pack_weights, server_eval)
 
 # (name, m, n, input group)
 PROJECTIONS = (
@@ -83,6 +90,49 @@ def run_layer(layer: Layer, X: dict, ex: dict, ey: dict, tamper=None, stream=Non
     return out
 
 
+def prepare_layer(layer: Layer, ex: dict, ey: dict, flags: torch.Tensor, out: dict | None = None,
+                  stream=None) -> dict:
+    """Client preparation of one layer: for every projection the masks
+    Gx e and P e of its input's noise and the vectors Gy e_q, e_q^T Q of its
+    challenges (client_prepare).  flags: one int32 device word per projection,
+    each set to 1 once that projection's outputs are visible device-wide (in
+    call order, so the last flag covers the whole layer).  Returns
+    {name: Prepared}."""
+    preps = out if out is not None else {}
+    for i, (name, m, n, group) in enumerate(PROJECTIONS):
+        B = ex[group][0].shape[0]
+        ell = ey[name][0].shape[0]
+        if name not in preps:
+            preps[name] = Prepared(layer.keys[name], B, ell, device=ex[group][0].device)
+        client_prepare(layer.keys[name], ex[group][0], ex[group][1], ey[name][0], ey[name][1], out=preps[name],
+                       done_flag=flags[i], stream=stream)
+    return preps
+
+
+def run_layer_prepared(layer: Layer, X: dict, preps: dict, ready_flag: torch.Tensor | None = None,
+                       timeout_us: int = 200000, timed_out: torch.Tensor | None = None, tamper=None, stream=None):
+    """The online part of a layer with prepared masks: x^ = x + Gx e per
+    input, server_eval, and decode_verify_masked per projection.  ready_flag:
+    the layer's last preparation flag; the first masked encode waits for it
+    (and clears it).  Same outputs as run_layer with the same noise and
+    challenges."""
+    Xhat = {}
+    wait = ready_flag
+    for group in INPUTS:
+        name = next(p for (p, _, _, g) in PROJECTIONS if g == group)
+        Xhat[group] = encode_masked(layer.keys[name], X[group], preps[name], ready_flag=wait,
+                                    timeout_us=timeout_us, timed_out=timed_out, stream=stream)
+        wait = None
+    out = {}
+    for name, m, n, group in PROJECTIONS:
+        Yhat = server_eval(layer.W[name], Xhat[group], stream=stream)
+        if tamper is not None:
+            tamper(name, Yhat)
+        Y, acc, _, _ = decode_verify_masked(layer.keys[name], Xhat[group], Yhat, preps[name], stream=stream)
+        out[name] = (Y, acc, Xhat[group], Yhat)
+    return out
+
+
 def codes_for(make_code) -> tuple[dict, dict]:
     """Shared codes: privacy code per input width, verification code per output height."""
     ns = sorted({n for (_, _, n, _) in PROJECTIONS})
@@ -94,5 +144,5 @@ def macs_per_layer(B: int) -> int:
     return sum(m * n for (_, m, n, _) in PROJECTIONS) * B
 
 
-__all__ = ["PROJECTIONS", "INPUTS", "Layer", "build_layer", "run_layer", "codes_for", "input_width",
-           "macs_per_layer", "Code"]
+__all__ = ["PROJECTIONS", "INPUTS", "Layer", "build_layer", "run_layer", "prepare_layer", "run_layer_prepared",
+           "codes_for", "input_width", "macs_per_layer", "Code"]

@@ -66,12 +66,14 @@ def test_client_prepare_matches_oracle(cid, m, n, B, rx, ry, tx, ell):
 
 # few-workgroup decode/verify (B * (m + n) <= 32768 and ell <= 4: one
 # workgroup, six with one element per thread, three with four, ell 2 and 3),
-# the element-block x column-group kernel above that (ell <= 4: 8 columns per
-# workgroup for ell <= 2, 4 for ell 3 and 4; ragged column groups and element
-# blocks, n > m) and the general kernel (ell = 7)
+# the element-block x column-group kernel above that (ell <= 4; one element
+# per thread and 4 / ell columns per workgroup, or at 256 workgroups and more
+# four elements and 16 / ell columns; ragged column groups and element blocks,
+# n > m) and the general kernel (ell = 7)
 MASKED = PREP[:2] + PREP[3:4] + [(86, 3000, 2000, 8, 2, 2, 16, 3), (87, 500, 400, 2, 2, 2, 9, 7),
                                  (88, 12000, 300, 2, 2, 2, 9, 2), (90, 4096, 1000, 20, 2, 2, 16, 2),
-                                 (91, 700, 5000, 13, 2, 2, 9, 4), (92, 1500, 1500, 9, 2, 2, 9, 1)]
+                                 (91, 700, 5000, 13, 2, 2, 9, 4), (92, 1500, 1500, 9, 2, 2, 9, 1),
+                                 (93, 16384, 100, 128, 2, 2, 5, 2), (94, 16000, 90, 64, 2, 2, 5, 3)]
 
 
 @pytest.mark.parametrize("cid,m,n,B,rx,ry,tx,ell", MASKED)

@@ -108,3 +108,60 @@ def test_stack_parity_and_tamper_schedule():
                                       oracle.encT(cy, (Wh[name][:, k0].astype(np.int64) % P).astype(np.uint32)))
         del layer, out
     assert seen_tampered == len(tampered) >= (1 if total > offset else 0)
+
+
+def test_stack_prepared_schedule_matches_one_call_path():
+    """prepare_layer on a preparation stream (flags) + run_layer_prepared on an
+    online stream give the outputs of run_layer, bit for bit, for two layers;
+    a tampered response is rejected by both."""
+    import paper_2609_10264_amd.stack as stack
+
+    cfg = synth.STACK
+    B, r, tx, ty, ell, cid = cfg["B"], cfg["r"], cfg["tx"], cfg["ty"], cfg["ell"], cfg["cid"]
+
+    def make_code(kind, k):
+        purpose = synth.PURPOSE_CX if kind == "x" else synth.PURPOSE_CY
+        return dev_code(synth.raa_code(synth.seed_for(cid, purpose, sub=k), k, r))
+
+    cx_by_n, cy_by_m = stack.codes_for(make_code)
+    nproj = len(stack.PROJECTIONS)
+    flags = torch.zeros((2, nproj), dtype=torch.int32, device="cuda")
+    late = torch.zeros((), dtype=torch.int32, device="cuda")
+    s_prep, s_on = torch.cuda.Stream(), torch.cuda.Stream()
+    for L in range(2):
+        print(f"stack prepared layer {L}", flush=True)
+        sub = 500 + L
+        Wh = {name: synth.weights(synth.seed_for(cid, synth.PURPOSE_W, sub + i), m, n)
+              for i, (name, m, n, _) in enumerate(stack.PROJECTIONS)}
+        layer = stack.build_layer({k: dev(v) for k, v in Wh.items()}, cx_by_n, cy_by_m)
+        X = {g: dev(synth.field_uniform(synth.seed_for(cid, synth.PURPOSE_X, sub + j), (B, stack.input_width(g))))
+             for j, g in enumerate(stack.INPUTS)}
+        ex = {g: tuple(dev(a) for a in synth.sparse(synth.seed_for(cid, synth.PURPOSE_NOISE, sub + j), B,
+                                                     r * stack.input_width(g), tx))
+              for j, g in enumerate(stack.INPUTS)}
+        ey = {name: tuple(dev(a) for a in synth.sparse(synth.seed_for(cid, synth.PURPOSE_CHAL, sub + i), ell, r * m,
+                                                        ty))
+              for i, (name, m, _, _) in enumerate(stack.PROJECTIONS)}
+        torch.cuda.synchronize()
+
+        def tamper(name, Yhat):
+            if name == "gate":
+                Yhat[B - 1, 17] = int((int(Yhat[B - 1, 17].item()) + 99) % P)
+
+        ref = stack.run_layer(layer, X, ex, ey, tamper=tamper)
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s_prep):
+            preps = stack.prepare_layer(layer, ex, ey, flags[L], stream=s_prep)
+        with torch.cuda.stream(s_on):
+            got = stack.run_layer_prepared(layer, X, preps, ready_flag=flags[L, nproj - 1], timeout_us=2_000_000,
+                                           timed_out=late, tamper=tamper, stream=s_on)
+        torch.cuda.synchronize()
+        assert int(late.item()) == 0 and int(flags[L, nproj - 1].item()) == 0
+        for name, _, _, _ in stack.PROJECTIONS:
+            for a, b in zip(ref[name], got[name]):
+                assert torch.equal(a, b), (L, name)
+            want = [1] * B
+            if name == "gate":
+                want[B - 1] = 0
+            assert host(got[name][1]).tolist() == want, (L, name)
+        del layer, ref, got, preps

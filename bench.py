@@ -175,7 +175,7 @@ def main():
         return write_traffic(args.write_traffic[0], args.write_traffic[1], args.config, args.weights,
                              args.calib_copy_mib or 256, args.traffic_kernel)
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; multi-GPU runs are not supported",
+        print(json.dumps({"error": "this benchmark runs on one GPU only; multi-GPU runs are not supported",
                           "n_gpus": args.gpus}), flush=True)
         sys.exit(2)
 

@@ -64,8 +64,9 @@ def test_client_prepare_matches_oracle(cid, m, n, B, rx, ry, tx, ell):
     assert np.array_equal(host(prep.U), oracle.server_eval(np.ascontiguousarray(inst.W.T), R))
 
 
-# few-workgroup decode/verify (B * (m + n) <= 32768 and ell <= 4: one
-# workgroup, six with one element per thread, three with four, ell 2 and 3),
+# few-workgroup decode/verify (B * (m + n) <= 32768 and ell <= 4: four
+# elements per thread, one workgroup up to 4096 elements, three for 12000;
+# ell 2 and 3),
 # the element-block x column-group kernel above that (ell <= 4; one element
 # per thread and 4 / ell columns per workgroup, or at 256 workgroups and more
 # four elements and 16 / ell columns; ragged column groups and element blocks,

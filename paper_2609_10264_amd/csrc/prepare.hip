@@ -368,9 +368,9 @@ hipError_t launch_add_masks(const uint32_t* X, const uint32_t* Mx, size_t count,
                             uint32_t value, uint32_t timeout_us, uint32_t* timed_out, uint32_t* counter,
                             hipStream_t s) {
     if (count == 0 && !flag) return hipSuccess;
-    // one word per thread over up to 8 workgroups; beyond, four per thread
-    const bool one = count <= 8u * kAddThreads;
-    size_t blocks = one ? (count + kAddThreads - 1) / kAddThreads : (count + 4u * kAddThreads - 1) / (4u * kAddThreads);
+    // four words per thread, one pass per workgroup up to 256 workgroups (a
+    // single workgroup up to 4096 words clears the flag itself)
+    size_t blocks = (count + 4u * kAddThreads - 1) / (4u * kAddThreads);
     if (blocks > 256) blocks = 256;
     if (blocks == 0) blocks = 1;
     uint64_t ticks = 0;
@@ -381,11 +381,7 @@ hipError_t launch_add_masks(const uint32_t* X, const uint32_t* Mx, size_t count,
 #define MVK_ADD(W, P)                                                                                          \
     hipLaunchKernelGGL((add_masks<W, P>), dim3((uint32_t)blocks), dim3(kAddThreads), 0, s, X, Mx, count, Xhat, flag, \
                        value, ticks, timed_out, counter)
-    if (flag) {
-        if (one) MVK_ADD(true, 1); else MVK_ADD(true, 4);
-    } else {
-        if (one) MVK_ADD(false, 1); else MVK_ADD(false, 4);
-    }
+    if (flag) MVK_ADD(true, 4); else MVK_ADD(false, 4);
 #undef MVK_ADD
     return hipGetLastError();
 }

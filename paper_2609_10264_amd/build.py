@@ -10,6 +10,7 @@ then each build is linked into one shared object next to this file.
 from __future__ import annotations
 
 import os
+import re
 import shutil
 import subprocess
 import sys
@@ -47,6 +48,59 @@ def sources() -> list[str]:
     return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
 
 
+# Source files whose kernels issue loads through inline assembly (the compiler
+# does not know those loads are in flight until the kernel's explicit wait).
+ASM_LOAD_SOURCES = ("server_eval.hip",)
+
+
+def _vregs(tok: str) -> set:
+    m = re.match(r"v\[(\d+):(\d+)\]$", tok)
+    if m:
+        return set(range(int(m.group(1)), int(m.group(2)) + 1))
+    m = re.match(r"v(\d+)$", tok)
+    return {int(m.group(1))} if m else set()
+
+
+def asm_load_hazards(asm_text: str) -> list:
+    """Register copies (v_mov*, v_accvgpr*) that read a register written by an
+    inline-assembly global_load_dwordx4 of the same kernel before the next
+    wait for all loads (s_waitcnt vmcnt(0)).  The compiler treats
+    the asm output as ready when the asm statement ends, so such a copy (it
+    appears under register pressure) can read the register before the load
+    lands, and the late data then overwrites whatever reused the register: a
+    corrupted address and a memory fault.  Returns [(kernel, instruction)]."""
+    bad, cur, inasm, dests = [], None, False, set()
+    for line in asm_text.split("\n"):
+        m = re.match(r"^(_Z\S+):", line)
+        if m:
+            cur, dests = m.group(1), set()
+            continue
+        if cur is None:
+            continue
+        if "s_endpgm" in line:
+            cur = None
+            continue
+        if ";;#ASMSTART" in line:
+            inasm = True
+            continue
+        if ";;#ASMEND" in line:
+            inasm = False
+            continue
+        parts = line.strip().split(None, 1)
+        if not parts:
+            continue
+        op, args = parts[0], [a.strip() for a in parts[1].split(",")] if len(parts) > 1 else []
+        if op == "s_waitcnt" and re.search(r"vmcnt\(0\)", line):
+            dests = set()  # every load has landed; the registers are free again
+            continue
+        if inasm and op == "global_load_dwordx4" and args:
+            dests |= _vregs(args[0])
+        elif op.startswith("v_mov") or op.startswith("v_accvgpr"):
+            if any(_vregs(a) & dests for a in args[1:]):
+                bad.append((cur, line.strip()))
+    return bad
+
+
 def build(verbose: bool = False) -> str:
     """Compile and link every field variant; returns the 2^31 - 1 library's path."""
     cc = hipcc()
@@ -69,8 +123,24 @@ def build(verbose: bool = False) -> str:
             print(out, file=sys.stderr)
         return obj
 
+    def check_asm(job) -> list:
+        # device assembly of a translation unit with inline-assembly loads
+        _, src, obj, flags = job
+        out = obj.replace(".o", ".s")
+        cmd = [cc, *HIPCC_FLAGS, *flags, "--cuda-device-only", "-S", src, "-o", out]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"hipcc -S failed for {src}:\n{r.stdout}{r.stderr}")
+        with open(out) as f:
+            return asm_load_hazards(f.read())
+
+    asm_jobs = [j for j in jobs if os.path.basename(j[1]) in ASM_LOAD_SOURCES]
     with ThreadPoolExecutor(max_workers=min(8, os.cpu_count() or 1)) as ex:
         objs = list(ex.map(compile_one, jobs))
+        hazards = [h for hs in ex.map(check_asm, asm_jobs) for h in hs]
+    if hazards:
+        lines = "\n".join(f"  {k}: {i}" for k, i in hazards[:20])
+        raise RuntimeError(f"registers of in-flight inline-assembly loads are copied ({len(hazards)}):\n{lines}")
     for name, (lib, _) in VARIANTS.items():
         mine = [o for o, j in zip(objs, jobs) if j[0] == name]
         tmp = lib + f".tmp{os.getpid()}"

@@ -27,6 +27,8 @@ Printed JSON line:
   roofline    server_eval kernel: algorithmic bytes (m*n + 4*n*B + 4*m*B) per
               launch / mean launch duration (HIP events around each launch on
               the launch stream), against 8 TB/s HBM
+  server_eval_large  the same single-query kernel at 16384 x 16384 (268 MB of
+              W per launch), where streaming W dominates the launch
   cpu_baseline the CPU oracle (single-threaded plain C) on a bounded sample of
               the same steps, on this host
 """
@@ -139,6 +141,8 @@ def parse():
     ap.add_argument("--pool", type=int, default=0, help="distinct W matrices cycled (0: enough for 2x the LLC)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="time budget of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-large", action="store_true",
+                    help="skip the 16384 x 16384 single-query server_eval measurement of the default line")
     ap.add_argument("--eager", action="store_true", help="launch the timed steps one by one instead of a HIP graph")
     ap.add_argument("--chains", type=int, default=1,
                     help="serial schedule: independent query chains run side by side (step i belongs to chain "
@@ -402,6 +406,7 @@ def main():
         e1.record()
     torch.cuda.synchronize()
     se_mean_s = 1e-3 * e0.elapsed_time(e1) / reps
+    large = None if args.no_large else server_eval_large(args, gen, dev)
 
     macs = m * n * B
     ms_per_step = 1e3 * elapsed / args.steps
@@ -432,6 +437,7 @@ def main():
                      "kernel": f"server_eval ({args.path})", "alg_bytes_per_launch": alg_bytes,
                      "mean_launch_us": 1e6 * se_mean_s},
         "server_eval": {"modmac_per_s": macs / se_mean_s, "gb_per_s": achieved},
+        "server_eval_large": large,
         "all_accepted": accepted_serial and accepted_pipe,
         "replay_matches_eager": replay_matches_eager,
         "pipelined_matches_one_call_path": pipe_matches,
@@ -444,6 +450,50 @@ def main():
     print(json.dumps(out), flush=True)
     if not (accepted_serial and accepted_pipe and replay_matches_eager and pipe_matches):
         sys.exit(1)
+
+
+def server_eval_large(args, gen, dev, m=16384, n=16384, pool=2, reps=40):
+    """The same single-query kernel where W streaming dominates: 16384 x 16384
+    (268 MB of packed W per launch, a pool of two), HIP events around a graph of
+    back-to-back launches on the launch stream."""
+    import torch
+
+    import paper_2609_10264_amd as mvk
+
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        Ws = []
+        for _ in range(pool):
+            W = torch.randint(-127, 128, (m, n), generator=gen, device=dev, dtype=torch.int8)
+            Ws.append(mvk.pack_weights(W, stream=s))
+            del W
+        X = torch.randint(0, mvk.P, (pool, 1, n), generator=gen, device=dev, dtype=torch.int32)
+        Y = torch.empty((1, m), dtype=torch.int32, device=dev)
+        for j in range(pool):
+            mvk.server_eval(Ws[j], X[j], out=Y, stream=s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        for k in range(reps):
+            mvk.server_eval(Ws[k % pool], X[k % pool], out=Y, stream=s)
+
+    def replay():
+        with torch.cuda.stream(s):
+            g.replay()
+
+    warm(replay, args.warm_seconds)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(s):
+        e0.record()
+        g.replay()
+        e1.record()
+    torch.cuda.synchronize()
+    t = 1e-3 * e0.elapsed_time(e1) / reps
+    alg = m * n + 4 * n + 4 * m
+    del Ws, X, Y, g
+    torch.cuda.empty_cache()
+    return {"workload": f"W {m}x{n} int8-valued, B=1, packed", "mean_launch_us": 1e6 * t,
+            "achieved_gbps": alg / t / 1e9, "frac": alg / t / 1e9 / HBM_PEAK_GBS}
 
 
 def stack_bench(args):

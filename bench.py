@@ -27,6 +27,8 @@ Printed JSON line:
   roofline    server_eval kernel: algorithmic bytes (m*n + 4*n*B + 4*m*B) per
               launch / mean launch duration (HIP events around each launch on
               the launch stream), against 8 TB/s HBM
+              read_floor: a pure streaming read (mvk_stream_read) of the same
+              buffers timed the same way; frac = read time / server_eval time
   server_eval_large  the same single-query kernel at 16384 x 16384 (268 MB of
               W per launch), where streaming W dominates the launch
   cpu_baseline the CPU oracle (single-threaded plain C) on a bounded sample of
@@ -406,6 +408,7 @@ def main():
         e1.record()
     torch.cuda.synchronize()
     se_mean_s = 1e-3 * e0.elapsed_time(e1) / reps
+    read_s = read_floor([w.data if isinstance(w, mvk.PackedW) else w for w in Ws], reps, args)
     large = None if args.no_large else server_eval_large(args, gen, dev)
 
     macs = m * n * B
@@ -435,7 +438,9 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(args.config, args.weights),
                      "kernel": f"server_eval ({args.path})", "alg_bytes_per_launch": alg_bytes,
-                     "mean_launch_us": 1e6 * se_mean_s},
+                     "mean_launch_us": 1e6 * se_mean_s,
+                     "read_floor": {"mean_launch_us": 1e6 * read_s, "gbps": alg_bytes / read_s / 1e9,
+                                    "frac": read_s / se_mean_s}},
         "server_eval": {"modmac_per_s": macs / se_mean_s, "gb_per_s": achieved},
         "server_eval_large": large,
         "all_accepted": accepted_serial and accepted_pipe,
@@ -450,6 +455,39 @@ def main():
     print(json.dumps(out), flush=True)
     if not (accepted_serial and accepted_pipe and replay_matches_eager and pipe_matches):
         sys.exit(1)
+
+
+def read_floor(bufs, reps, args):
+    """Seconds per launch of a pure streaming read (mvk_stream_read) of the same
+    buffers, back to back over the pool as the server_eval launches are: the
+    measured read floor for that many bytes."""
+    import torch
+
+    import paper_2609_10264_amd as mvk
+
+    s = torch.cuda.Stream()
+    sink = torch.empty((mvk._lib.MVK_STREAM_READ_BLOCKS,), dtype=torch.int32, device=bufs[0].device)
+    with torch.cuda.stream(s):
+        for b in bufs:
+            mvk.stream_read(b, sink, stream=s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        for k in range(reps):
+            mvk.stream_read(bufs[k % len(bufs)], sink, stream=s)
+
+    def replay():
+        with torch.cuda.stream(s):
+            g.replay()
+
+    warm(replay, args.warm_seconds)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(s):
+        e0.record()
+        g.replay()
+        e1.record()
+    torch.cuda.synchronize()
+    return 1e-3 * e0.elapsed_time(e1) / reps
 
 
 def server_eval_large(args, gen, dev, m=16384, n=16384, pool=2, reps=40):
@@ -490,10 +528,12 @@ def server_eval_large(args, gen, dev, m=16384, n=16384, pool=2, reps=40):
     torch.cuda.synchronize()
     t = 1e-3 * e0.elapsed_time(e1) / reps
     alg = m * n + 4 * n + 4 * m
+    t_read = read_floor([w.data for w in Ws], reps, args)
     del Ws, X, Y, g
     torch.cuda.empty_cache()
     return {"workload": f"W {m}x{n} int8-valued, B=1, packed", "mean_launch_us": 1e6 * t,
-            "achieved_gbps": alg / t / 1e9, "frac": alg / t / 1e9 / HBM_PEAK_GBS}
+            "achieved_gbps": alg / t / 1e9, "frac": alg / t / 1e9 / HBM_PEAK_GBS,
+            "read_floor": {"mean_launch_us": 1e6 * t_read, "gbps": alg / t_read / 1e9, "frac": t_read / t}}
 
 
 def stack_bench(args):

@@ -370,6 +370,18 @@ mvk_status mvk_raa_encode(const mvk_code *code, const uint32_t *w, uint32_t coun
 mvk_status mvk_raa_syndrome(const mvk_code *code, const uint32_t *v, uint32_t count,
                             uint32_t *out, void *stream);
 
+/*
+ * Streaming read of `bytes` bytes at `data` (device, 16-byte aligned, bytes a
+ * multiple of 16), nothing computed but a checksum: the HBM read floor for a
+ * buffer of that size, which server_eval's stream of W is measured against.
+ * sink: device, MVK_STREAM_READ_BLOCKS uint32 words; word w receives the XOR
+ * of the 32-bit words read by workgroup w (zero for workgroups the launch
+ * does not have), so the XOR of all sink words is the XOR of the whole buffer.
+ * Errors: MVK_EINVAL (null or misaligned pointer, bytes not a multiple of 16).
+ */
+#define MVK_STREAM_READ_BLOCKS 4096u
+mvk_status mvk_stream_read(const void *data, size_t bytes, uint32_t *sink, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

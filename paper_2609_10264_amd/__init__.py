@@ -425,3 +425,18 @@ def raa_syndrome(code: Code, v: torch.Tensor, out: torch.Tensor | None = None, s
         ctypes.byref(cs), _dev(v2, torch.int32, (count, code.N), "v"), count,
         _dev(out, torch.int32, (count, code.k), "out"), _stream(stream)))
     return out
+
+
+def stream_read(data: torch.Tensor, sink: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Streaming read of a contiguous device tensor (its bytes, a multiple of 16,
+    16-byte aligned): the HBM read floor for that size.  Returns the sink
+    (MVK_STREAM_READ_BLOCKS int32 words whose XOR is the XOR of the buffer's
+    32-bit words)."""
+    if not data.is_cuda or not data.is_contiguous():
+        raise ValueError("data must be a contiguous CUDA tensor")
+    if sink is None:
+        sink = torch.empty((_lib.MVK_STREAM_READ_BLOCKS,), dtype=torch.int32, device=data.device)
+    nbytes = data.numel() * data.element_size()
+    _lib.check("mvk_stream_read", _lib.load().mvk_stream_read(
+        data.data_ptr(), nbytes, _dev(sink, torch.int32, (_lib.MVK_STREAM_READ_BLOCKS,), "sink"), _stream(stream)))
+    return sink

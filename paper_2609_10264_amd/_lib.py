@@ -20,6 +20,7 @@ MVK_MAX_N = 131071
 MVK_PATH_AUTO = 0
 MVK_PATH_VALU = 1
 MVK_PATH_MFMA = 2
+MVK_STREAM_READ_BLOCKS = 4096
 ABI_VERSION = 5
 # field modulus -> library built over that field
 LIB_PATHS = {MVK_PRIME: LIB_PATH, MVK_PRIME_BABYBEAR: LIB_PATH_BB}
@@ -50,6 +51,7 @@ EXPORTS = (
     "mvk_batch_verify",
     "mvk_raa_encode",
     "mvk_raa_syndrome",
+    "mvk_stream_read",
 )
 
 
@@ -160,6 +162,8 @@ def load(p: int = MVK_PRIME) -> ctypes.CDLL:
     L.mvk_raa_encode.restype = st
     L.mvk_raa_syndrome.argtypes = [ctypes.POINTER(MvkCode), vp, u32, vp, vp]
     L.mvk_raa_syndrome.restype = st
+    L.mvk_stream_read.argtypes = [vp, ctypes.c_size_t, vp, vp]
+    L.mvk_stream_read.restype = st
     if L.mvk_abi_version() != ABI_VERSION:
         raise ImportError(f"{path}: ABI version mismatch; rebuild the library")
     if L.mvk_field_modulus() != p:

@@ -492,4 +492,10 @@ mvk_status mvk_raa_syndrome(const mvk_code* code, const uint32_t* v, uint32_t co
     return hip_status(launch_syn_dense(*code, v, count, (uint32_t*)ws, out, s));
 }
 
+mvk_status mvk_stream_read(const void* data, size_t bytes, uint32_t* sink, void* stream) {
+    if (bytes == 0) return MVK_OK;
+    if (!data || !sink || ((uintptr_t)data & 15) || (bytes & 15)) return MVK_EINVAL;
+    return hip_status(launch_stream_read(data, bytes, sink, MVK_STREAM_READ_BLOCKS, (hipStream_t)stream));
+}
+
 }  // extern "C"

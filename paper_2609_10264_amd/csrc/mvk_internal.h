@@ -138,6 +138,11 @@ hipError_t launch_batch_check(uint32_t m, uint32_t n, uint32_t B, const uint32_t
 // accumulators), zero before the launch and left at zero.
 size_t batch_ctrl_bytes(uint32_t m, uint32_t n, uint32_t B, uint32_t ell, uint32_t ell2);
 
+// calib.hip -----------------------------------------------------------------
+// Streaming read of bytes (a multiple of 16) at data; sink: sink_words words
+// (at least 256), their XOR is the XOR of the buffer's words.
+hipError_t launch_stream_read(const void* data, size_t bytes, uint32_t* sink, uint32_t sink_words, hipStream_t s);
+
 inline uint32_t ceil_div(uint32_t a, uint32_t b) { return (a + b - 1) / b; }
 
 }  // namespace mvk

@@ -235,3 +235,14 @@ def test_batch_argument_checks_without_device_work():
     assert call(args(e2=ctypes.byref(L.MvkSparse(0x1000, 0x1000, 2, 17)))) == L.MVK_ERANGE
     assert call(args(e2=ctypes.byref(L.MvkSparse(0x1000, 0x1000, 25, 2)))) == L.MVK_EINVAL  # t' > N' = 24
     assert call(args(e=ctypes.byref(L.MvkSparse(0x1000, 0x1000, 25, 2)))) == L.MVK_EINVAL   # t > N = 24
+
+
+def test_stream_read_argument_checks_without_device_work():
+    L = _lib()
+    lib = L.load()
+    fake = ctypes.c_void_p(0x1000)
+    assert lib.mvk_stream_read(None, 0, None, None) == L.MVK_OK  # empty read
+    assert lib.mvk_stream_read(None, 64, fake, None) == L.MVK_EINVAL
+    assert lib.mvk_stream_read(fake, 64, None, None) == L.MVK_EINVAL
+    assert lib.mvk_stream_read(ctypes.c_void_p(0x1004), 64, fake, None) == L.MVK_EINVAL  # misaligned
+    assert lib.mvk_stream_read(fake, 60, fake, None) == L.MVK_EINVAL  # not a multiple of 16

@@ -136,6 +136,16 @@ def test_server_eval_repeatable_and_noncontiguous_offsets():
     assert not big[:64].any()
 
 
+@pytest.mark.parametrize("nbytes", [16, 4096, 16 * 262144 * 8 + 48, 16777216 + 1024])
+def test_stream_read_checksum(nbytes):
+    """The calibration read covers every byte once: the XOR of its sink words is
+    the XOR of the buffer's 32-bit words (ragged passes included)."""
+    data = synth.weights(nbytes, 1, nbytes)
+    sink = mvk.stream_read(dev(data))
+    want = np.bitwise_xor.reduce(data.view(np.uint32).ravel())
+    assert int(np.bitwise_xor.reduce(host(sink))) == int(want)
+
+
 # ---------------------------------------------------------------------------
 # RAA encoding / syndrome
 # ---------------------------------------------------------------------------

@@ -26,6 +26,11 @@
  *  - Inputs are not validated on the device: field inputs must be < p and
  *    permutations / sparse positions must be in range, or the outputs are
  *    undefined (out-of-range indices are clamped, never dereferenced).
+ *    With MVK_VALIDATE=1 in the environment, mvk_server_eval*, mvk_encode,
+ *    mvk_decode_verify*, mvk_verify, mvk_encode_masked and
+ *    mvk_decode_verify_masked first check that their field inputs are
+ *    canonical, waiting for the stream, and return MVK_ERANGE (nothing else
+ *    enqueued) if one is not; a debugging mode, not for graph capture.
  *  - The library keeps a per-(device, stream) workspace that grows on demand
  *    (hipMalloc at first use and when a larger size is needed); calls enqueued
  *    on two different streams never share workspace memory.
@@ -47,7 +52,7 @@ extern "C" {
 typedef int32_t mvk_status;
 #define MVK_OK 0
 #define MVK_EINVAL (-1) /* missing pointer, zero or inconsistent size */
-#define MVK_ERANGE (-2) /* a size beyond the exactness limit of a kernel */
+#define MVK_ERANGE (-2) /* a size beyond the exactness limit of a kernel, or (MVK_VALIDATE) a field input >= p */
 #define MVK_ENOMEM (-3) /* workspace allocation failed */
 #define MVK_EHIP (-4)   /* a HIP runtime call or kernel launch failed */
 

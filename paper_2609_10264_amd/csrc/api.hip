@@ -4,6 +4,8 @@
 // enqueues the kernels; all arithmetic happens in the kernels.
 #include <hip/hip_runtime.h>
 
+#include <cstdlib>
+#include <initializer_list>
 #include <map>
 #include <mutex>
 #include <utility>
@@ -69,6 +71,45 @@ mvk_status workspace(hipStream_t s, size_t bytes, void** out, uint32_t** ctrl = 
 }
 
 inline mvk_status hip_status(hipError_t e) { return e == hipSuccess ? MVK_OK : MVK_EHIP; }
+
+// MVK_VALIDATE=1 in the environment: the pvMVMD calls check that their field
+// inputs are canonical before enqueuing anything else.
+bool validate_mode() {
+    const char* v = getenv("MVK_VALIDATE");
+    return v && v[0] == '1' && v[1] == '\0';
+}
+
+// MVK_ERANGE if a[0, count) holds a word >= p.  Waits for the stream (the
+// validation mode is synchronous); one device word per device, for this check.
+mvk_status check_canonical(const uint32_t* a, size_t count, hipStream_t s) {
+    if (!a || count == 0) return MVK_OK;
+    static std::mutex mu;
+    static std::map<int, uint32_t*> words;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return MVK_EHIP;
+    std::lock_guard<std::mutex> lk(mu);
+    uint32_t*& w = words[dev];
+    if (!w && hipMalloc(&w, sizeof(uint32_t)) != hipSuccess) {
+        (void)hipGetLastError();
+        w = nullptr;
+        return MVK_ENOMEM;
+    }
+    uint32_t bad = 0;
+    if (hipMemsetAsync(w, 0, sizeof(uint32_t), s) != hipSuccess) return MVK_EHIP;
+    if (launch_count_noncanonical(a, count, w, s) != hipSuccess) return MVK_EHIP;
+    if (hipMemcpyAsync(&bad, w, sizeof(uint32_t), hipMemcpyDeviceToHost, s) != hipSuccess) return MVK_EHIP;
+    if (hipStreamSynchronize(s) != hipSuccess) return MVK_EHIP;
+    return bad ? MVK_ERANGE : MVK_OK;
+}
+
+// check_canonical over several arrays; nulls are skipped.
+mvk_status check_all(hipStream_t s, std::initializer_list<std::pair<const uint32_t*, size_t>> arrays) {
+    for (const auto& a : arrays) {
+        const mvk_status st = check_canonical(a.first, a.second, s);
+        if (st) return st;
+    }
+    return MVK_OK;
+}
 
 inline size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -136,6 +177,10 @@ mvk_status server_eval_impl(const int8_t* W, uint32_t m, uint32_t n, const uint3
     if (!W || !Xhat) return MVK_EINVAL;
     if (n > MVK_MAX_N) return MVK_ERANGE;
     if (packed && (uintptr_t)W % 16 != 0) return MVK_EINVAL;
+    if (validate_mode()) {
+        const mvk_status st = check_canonical(Xhat, (size_t)B * n, s);
+        if (st) return st;
+    }
     void* ws = nullptr;
     uint32_t* ctrl = nullptr;
     const ServerEvalPlan pl = server_eval_plan(m, n, B, path, packed);
@@ -155,7 +200,7 @@ const char* mvk_status_str(mvk_status s) {
     switch (s) {
         case MVK_OK: return "ok";
         case MVK_EINVAL: return "invalid argument";
-        case MVK_ERANGE: return "size out of range";
+        case MVK_ERANGE: return "size or value out of range";
         case MVK_ENOMEM: return "out of device memory";
         case MVK_EHIP: return "HIP runtime error";
         default: return "unknown status";
@@ -221,6 +266,7 @@ mvk_status mvk_encode(const mvk_key* key, const uint32_t* X, uint32_t B, const m
     hipStream_t s = (hipStream_t)stream;
     const size_t Nx = (size_t)key->cx.r * key->n;
     if (ex->t > Nx) return MVK_EINVAL;
+    if (validate_mode() && (st = check_all(s, {{X, (size_t)B * key->n}, {ex->val, (size_t)B * ex->t}}))) return st;
     void* ws = nullptr;
     st = workspace(s, syn_scratch_bytes(B, Nx), &ws);
     if (st) return st;
@@ -248,6 +294,9 @@ mvk_status mvk_decode_verify_prepared(const mvk_key* key, const uint32_t* Xhat, 
     if (st || B == 0) return st;
     if (!R) return MVK_EINVAL;
     hipStream_t s = (hipStream_t)stream;
+    if (validate_mode() && (st = check_all(s, {{Xhat, (size_t)B * key->n}, {Yhat, (size_t)B * key->m},
+                                               {R, (size_t)ey->count * key->m}})))
+        return st;
     void* ws = nullptr;
     uint32_t* ctrl = nullptr;
     st = workspace(s, 0, &ws, &ctrl, dv_ctrl_bytes(key->m, key->n, B, ey->count));
@@ -294,6 +343,9 @@ mvk_status mvk_decode_verify(const mvk_key* key, const uint32_t* Xhat, const uin
                              uint32_t* accept, void* stream) {
     mvk_status st = check_decode_verify(key, Xhat, Yhat, B, ex, ey, Y, accept);
     if (st || B == 0) return st;
+    if (validate_mode() && (st = check_all((hipStream_t)stream, {{Xhat, (size_t)B * key->n},
+                                                                  {Yhat, (size_t)B * key->m}})))
+        return st;
     return decode_verify_run(key, Xhat, Yhat, B, ex, ey, Y, vL, vR, accept, (hipStream_t)stream);
 }
 
@@ -306,6 +358,8 @@ mvk_status mvk_verify(const mvk_key* key, const uint32_t* X, const uint32_t* Y, 
     st = check_challenges(key, ey);
     if (st) return st;
     if (B > 65535u) return MVK_ERANGE;
+    if (validate_mode() && (st = check_all((hipStream_t)stream, {{X, (size_t)B * key->n}, {Y, (size_t)B * key->m}})))
+        return st;
     const mvk_sparse none = {nullptr, nullptr, 0u, B};  // no noise: nothing to decrypt
     return decode_verify_run(key, X, Y, B, &none, ey, nullptr, vL, vR, accept, (hipStream_t)stream);
 }
@@ -356,6 +410,9 @@ mvk_status mvk_encode_masked(const mvk_key* key, const uint32_t* X, uint32_t B, 
     if (B == 0 && !ready_flag) return MVK_OK;
     if (B && (!X || !Mx || !Xhat)) return MVK_EINVAL;
     hipStream_t s = (hipStream_t)stream;
+    // (Mx may still be in preparation on another stream when a flag orders it)
+    if (validate_mode() && (st = check_all(s, {{X, (size_t)B * key->n}, {ready_flag ? nullptr : Mx, (size_t)B * key->n}})))
+        return st;
     uint32_t* ctrl = nullptr;
     if (ready_flag) {
         void* ws = nullptr;
@@ -375,6 +432,10 @@ mvk_status mvk_decode_verify_masked(const mvk_key* key, const uint32_t* Xhat, co
     if (!Xhat || !Yhat || !My || !R || !U || !Y || !accept || ell == 0) return MVK_EINVAL;
     if (ell > kMaxEll || B > 65535u) return MVK_ERANGE;
     hipStream_t s = (hipStream_t)stream;
+    if (validate_mode() && (st = check_all(s, {{Xhat, (size_t)B * key->n}, {Yhat, (size_t)B * key->m},
+                                               {My, (size_t)B * key->m}, {R, (size_t)ell * key->m},
+                                               {U, (size_t)ell * key->n}})))
+        return st;
     void* ws = nullptr;
     uint32_t* ctrl = nullptr;
     st = workspace(s, 0, &ws, &ctrl, dv_ctrl_bytes(key->m, key->n, B, ell));

@@ -138,6 +138,10 @@ hipError_t launch_batch_check(uint32_t m, uint32_t n, uint32_t B, const uint32_t
 // accumulators), zero before the launch and left at zero.
 size_t batch_ctrl_bytes(uint32_t m, uint32_t n, uint32_t B, uint32_t ell, uint32_t ell2);
 
+// validate.hip --------------------------------------------------------------
+// Adds to *out the number of words of a[0, count) that are >= p.
+hipError_t launch_count_noncanonical(const uint32_t* a, size_t count, uint32_t* out, hipStream_t s);
+
 // calib.hip -----------------------------------------------------------------
 // Streaming read of bytes (a multiple of 16) at data; sink: sink_words words
 // (at least 256), their XOR is the XOR of the buffer's words.

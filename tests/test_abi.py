@@ -56,7 +56,7 @@ def test_abi_version_and_status_strings():
     lib = L.load()
     assert lib.mvk_abi_version() == L.ABI_VERSION
     assert lib.mvk_status_str(0) == b"ok"
-    assert lib.mvk_status_str(L.MVK_ERANGE) == b"size out of range"
+    assert lib.mvk_status_str(L.MVK_ERANGE) == b"size or value out of range"
     assert lib.mvk_status_str(12345) == b"unknown status"
 
 

@@ -4,6 +4,8 @@ All arithmetic is integer mod p, so every comparison is exact equality.
 Sizes span several workgroup tiles with ragged tails; the full-size LLM-layer
 shapes compare either the whole output or oracle-computable samples.
 """
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -144,6 +146,35 @@ def test_stream_read_checksum(nbytes):
     sink = mvk.stream_read(dev(data))
     want = np.bitwise_xor.reduce(data.view(np.uint32).ravel())
     assert int(np.bitwise_xor.reduce(host(sink))) == int(want)
+
+
+def test_validate_mode_rejects_noncanonical_inputs():
+    """MVK_VALIDATE=1: a field input >= p is an error (MVK_ERANGE) before any
+    work; canonical inputs give the usual results."""
+    inst = Instance(61, 200, 300, 2, 2, 5).to_device()
+    mvk.keygen(inst.key, inst.dW)
+    Xh = mvk.encode(inst.key, inst.dX, inst.dexi, inst.dexv)
+    Yh = mvk.server_eval(inst.dW, Xh)
+    torch.cuda.synchronize()
+    os.environ["MVK_VALIDATE"] = "1"
+    try:
+        assert np.array_equal(host(mvk.server_eval(inst.dW, Xh)), host(Yh))
+        bad = Xh.clone()
+        bad[1, 7] = P
+        for call in (lambda: mvk.server_eval(inst.dW, bad),
+                     lambda: mvk.encode(inst.key, bad, inst.dexi, inst.dexv),
+                     lambda: mvk.decode_verify(inst.key, bad, Yh, inst.dexi, inst.dexv, inst.deyi, inst.deyv)):
+            with pytest.raises(mvk.MvkError) as err:
+                call()
+            assert err.value.status == mvk._lib.MVK_ERANGE
+        badY = Yh.clone()
+        badY[0, 3] = -1  # 0xffffffff
+        with pytest.raises(mvk.MvkError):
+            mvk.decode_verify(inst.key, Xh, badY, inst.dexi, inst.dexv, inst.deyi, inst.deyv)
+        Y, acc, _, _ = mvk.decode_verify(inst.key, Xh, Yh, inst.dexi, inst.dexv, inst.deyi, inst.deyv)
+        assert host(acc).tolist() == [1, 1]
+    finally:
+        del os.environ["MVK_VALIDATE"]
 
 
 # ---------------------------------------------------------------------------

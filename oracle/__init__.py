@@ -83,6 +83,9 @@ def lib(p: int = P):
             L.orc_verify.argtypes = [u32, u32, u32, u32p, u32p, u32p, u32p, u32p, u32p, u32p, u32,
                                      u32p, u32p, u32, u32, u32p, u32p, u8p]
             L.orc_prime.restype = u32
+            L.orc_ops_reset.argtypes = []
+            L.orc_ops_count.argtypes = []
+            L.orc_ops_count.restype = ctypes.c_uint64
             assert L.orc_prime() == p
             _lib[p] = L
     return _lib[p]
@@ -116,6 +119,15 @@ def encT(code: dict, w, p: int = P) -> np.ndarray:
     out = np.empty(k * r, dtype=np.uint32)
     lib(p).orc_encT(k, r, *[_p(a) for a in c], _p(w), _p(out))
     return out
+
+
+def field_ops(fn, p: int = P) -> int:
+    """Field operations the oracle performs while fn() runs (fn calls the oracle
+    over the same field)."""
+    L = lib(p)
+    L.orc_ops_reset()
+    fn()
+    return int(L.orc_ops_count())
 
 
 def syn(code: dict, v, p: int = P) -> np.ndarray:

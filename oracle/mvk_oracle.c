@@ -48,9 +48,16 @@
 #define ORC_P 2147483647ULL
 #endif
 
-static uint64_t fadd(uint64_t a, uint64_t b) { return (a + b) % ORC_P; }
-static uint64_t fsub(uint64_t a, uint64_t b) { return (a + ORC_P - b) % ORC_P; }
-static uint64_t fmul(uint64_t a, uint64_t b) { return (a * b) % ORC_P; }
+/* Count of field operations (additions, subtractions, multiplications) since
+ * the last orc_ops_reset: lets a test compare the RAA maps' cost with the
+ * bounds App. B states (at most 4N for an encoding, 5N for a syndrome). */
+static uint64_t g_ops;
+void orc_ops_reset(void) { g_ops = 0; }
+uint64_t orc_ops_count(void) { return g_ops; }
+
+static uint64_t fadd(uint64_t a, uint64_t b) { ++g_ops; return (a + b) % ORC_P; }
+static uint64_t fsub(uint64_t a, uint64_t b) { ++g_ops; return (a + ORC_P - b) % ORC_P; }
+static uint64_t fmul(uint64_t a, uint64_t b) { ++g_ops; return (a * b) % ORC_P; }
 
 /* Embedding of a signed integer into F_p. */
 static uint64_t emb(int64_t w) {

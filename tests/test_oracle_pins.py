@@ -151,6 +151,38 @@ def test_transposition_identity(k, r, p):
         assert lhs == rhs
 
 
+@pytest.mark.parametrize("k,r", [(1, 1), (7, 3), (100, 2), (257, 8)])
+def test_raa_cost_within_the_bounds_of_app_b(k, r, p):
+    """App. B: an encoding costs at most 4N field operations (two diagonal
+    scalings and two prefix sums), a syndrome at most 5N (plus the fold)."""
+    o = Fp(p)
+    code = o.raa_code(2000 + k, k, r)
+    N = k * r
+    w = o.field_uniform(1, k)
+    v = o.field_uniform(2, N)
+    enc_ops = oracle.field_ops(lambda: o.encT(code, w), p=p)
+    syn_ops = oracle.field_ops(lambda: o.syn(code, v), p=p)
+    assert 0 < enc_ops <= 4 * N
+    assert 0 < syn_ops <= 5 * N
+
+
+def test_masks_look_uniform(p):
+    """Privacy sanity check (the mask's pseudorandomness is the dual-LPN
+    assumption, not something a test can prove): the masks Gx e of sparse noise
+    are nonzero almost everywhere and spread evenly over F_p (chi-square over
+    16 buckets, 8 masks of 4096 entries)."""
+    o = Fp(p)
+    n, r, t = 4096, 3, 64
+    code = o.raa_code(3000, n, r)
+    idx, val = o.sparse(3001, 8, n * r, t)
+    masks = o.encode(code, np.zeros((8, n), dtype=np.uint32), idx, val)
+    assert (masks != 0).mean() > 0.999
+    counts = np.bincount((masks.astype(np.uint64) * 16 // p).ravel().astype(np.int64), minlength=16)
+    expect = masks.size / 16
+    chi2 = float(((counts - expect) ** 2 / expect).sum())
+    assert chi2 < 37.7  # 15 degrees of freedom, p = 0.001
+
+
 # ---------------------------------------------------------------------------
 # Server evaluation against Python big integers
 # ---------------------------------------------------------------------------

@@ -56,6 +56,33 @@ def build(force: bool = False) -> list:
     return list(_LIBS.values())
 
 
+def configure(L) -> None:
+    """Argument and result types of every oracle entry point on a loaded library."""
+    u32p = ctypes.POINTER(ctypes.c_uint32)
+    i8p = ctypes.POINTER(ctypes.c_int8)
+    u8p = ctypes.POINTER(ctypes.c_uint8)
+    u32 = ctypes.c_uint32
+    L.orc_encT.argtypes = [u32, u32, u32p, u32p, u32p, u32p, u32p, u32p]
+    L.orc_syn.argtypes = [u32, u32, u32p, u32p, u32p, u32p, u32p, u32p]
+    L.orc_server_eval.argtypes = [i8p, u32, u32, u32p, u32, u32p]
+    L.orc_server_eval_rows.argtypes = [i8p, u32, u32, u32p, u32, u32p, u32, u32]
+    L.orc_keygen.argtypes = [i8p, u32, u32, u32, u32p, u32p, u32p, u32p,
+                             u32, u32p, u32p, u32p, u32p, u32p, u32p]
+    L.orc_encode.argtypes = [u32, u32, u32p, u32p, u32p, u32p, u32p, u32, u32p, u32p, u32, u32p]
+    L.orc_decode.argtypes = [u32p, u32, u32p, u32, u32p, u32p, u32, u32p]
+    L.orc_batch_aux.argtypes = [u32, u32, u32, u32p, u32, u32p, u32p, u32p, u32p, u32p]
+    L.orc_batch_project.argtypes = [u32, u32, u32, u32p, u32p, u32p, u32, u32, u32p]
+    L.orc_batch_verify.argtypes = [u32, u32, u32, u32, u32p, u32p, u32p, u32p, u32, u32p, u32p, u32p, u32p,
+                                   u32p, u32p, u32p, u32p, u32p, u32, u32, u32p, u32p, u32p, u32, u32,
+                                   u32p, u32p, u32p, u32p]
+    L.orc_verify.argtypes = [u32, u32, u32, u32p, u32p, u32p, u32p, u32p, u32p, u32p, u32,
+                             u32p, u32p, u32, u32, u32p, u32p, u8p]
+    L.orc_prime.restype = u32
+    L.orc_ops_reset.argtypes = []
+    L.orc_ops_count.argtypes = []
+    L.orc_ops_count.restype = ctypes.c_uint64
+
+
 def lib(p: int = P):
     with _lock:
         if p not in _lib:
@@ -63,29 +90,7 @@ def lib(p: int = P):
                 raise ValueError(f"no oracle build over p = {p}")
             build()
             L = ctypes.CDLL(_LIBS[p])
-            u32p = ctypes.POINTER(ctypes.c_uint32)
-            i8p = ctypes.POINTER(ctypes.c_int8)
-            u8p = ctypes.POINTER(ctypes.c_uint8)
-            u32 = ctypes.c_uint32
-            L.orc_encT.argtypes = [u32, u32, u32p, u32p, u32p, u32p, u32p, u32p]
-            L.orc_syn.argtypes = [u32, u32, u32p, u32p, u32p, u32p, u32p, u32p]
-            L.orc_server_eval.argtypes = [i8p, u32, u32, u32p, u32, u32p]
-            L.orc_server_eval_rows.argtypes = [i8p, u32, u32, u32p, u32, u32p, u32, u32]
-            L.orc_keygen.argtypes = [i8p, u32, u32, u32, u32p, u32p, u32p, u32p,
-                                     u32, u32p, u32p, u32p, u32p, u32p, u32p]
-            L.orc_encode.argtypes = [u32, u32, u32p, u32p, u32p, u32p, u32p, u32, u32p, u32p, u32, u32p]
-            L.orc_decode.argtypes = [u32p, u32, u32p, u32, u32p, u32p, u32, u32p]
-            L.orc_batch_aux.argtypes = [u32, u32, u32, u32p, u32, u32p, u32p, u32p, u32p, u32p]
-            L.orc_batch_project.argtypes = [u32, u32, u32, u32p, u32p, u32p, u32, u32, u32p]
-            L.orc_batch_verify.argtypes = [u32, u32, u32, u32, u32p, u32p, u32p, u32p, u32, u32p, u32p, u32p, u32p,
-                                           u32p, u32p, u32p, u32p, u32p, u32, u32, u32p, u32p, u32p, u32, u32,
-                                           u32p, u32p, u32p, u32p]
-            L.orc_verify.argtypes = [u32, u32, u32, u32p, u32p, u32p, u32p, u32p, u32p, u32p, u32,
-                                     u32p, u32p, u32, u32, u32p, u32p, u8p]
-            L.orc_prime.restype = u32
-            L.orc_ops_reset.argtypes = []
-            L.orc_ops_count.argtypes = []
-            L.orc_ops_count.restype = ctypes.c_uint64
+            configure(L)
             assert L.orc_prime() == p
             _lib[p] = L
     return _lib[p]

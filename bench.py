@@ -31,6 +31,8 @@ Printed JSON line:
               buffers timed the same way; frac = read time / server_eval time
   server_eval_large  the same single-query kernel at 16384 x 16384 (268 MB of
               W per launch), where streaming W dominates the launch
+  server_eval_batched  the 64-query kernel at 28672 x 8192 against the int8
+              matrix-core peak (4 digit-plane multiply-adds per mod-MAC)
   cpu_baseline the CPU oracle (single-threaded plain C) on a bounded sample of
               the same steps, on this host
 """
@@ -47,6 +49,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "server_eval mod-MACs/s + achieved HBM GB/s (fraction of peak), 1×MI355X"
 HBM_PEAK_GBS = 8000.0
+MFMA_INT8_PEAK_OPS = 5.0e15  # MI355X dense int8 matrix-core peak
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "server_eval_attn4096_traffic.json")
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_10264_amd", "csrc", "server_eval.hip")
 
@@ -144,7 +147,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="time budget of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-large", action="store_true",
-                    help="skip the 16384 x 16384 single-query server_eval measurement of the default line")
+                    help="skip the 16384 x 16384 single-query and 28672 x 8192 64-query server_eval "
+                         "measurements of the default line")
     ap.add_argument("--eager", action="store_true", help="launch the timed steps one by one instead of a HIP graph")
     ap.add_argument("--chains", type=int, default=1,
                     help="serial schedule: independent query chains run side by side (step i belongs to chain "
@@ -410,6 +414,7 @@ def main():
     se_mean_s = 1e-3 * e0.elapsed_time(e1) / reps
     read_s = read_floor([w.data if isinstance(w, mvk.PackedW) else w for w in Ws], reps, args)
     large = None if args.no_large else server_eval_large(args, gen, dev)
+    batched = None if args.no_large else server_eval_batched(args, gen, dev)
 
     macs = m * n * B
     ms_per_step = 1e3 * elapsed / args.steps
@@ -443,6 +448,7 @@ def main():
                                     "frac": read_s / se_mean_s}},
         "server_eval": {"modmac_per_s": macs / se_mean_s, "gb_per_s": achieved},
         "server_eval_large": large,
+        "server_eval_batched": batched,
         "all_accepted": accepted_serial and accepted_pipe,
         "replay_matches_eager": replay_matches_eager,
         "pipelined_matches_one_call_path": pipe_matches,
@@ -534,6 +540,53 @@ def server_eval_large(args, gen, dev, m=16384, n=16384, pool=2, reps=40):
     return {"workload": f"W {m}x{n} int8-valued, B=1, packed", "mean_launch_us": 1e6 * t,
             "achieved_gbps": alg / t / 1e9, "frac": alg / t / 1e9 / HBM_PEAK_GBS,
             "read_floor": {"mean_launch_us": 1e6 * t_read, "gbps": alg / t_read / 1e9, "frac": t_read / t}}
+
+
+def server_eval_batched(args, gen, dev, m=28672, n=8192, B=64, pool=3, reps=30):
+    """The batched kernel at 28672 x 8192 with 64 queries (235 MB of packed W per
+    launch, a pool of three): HIP events around a graph of back-to-back
+    launches; int8 matrix-core work 4 m n B multiply-adds (four digit planes)
+    against the 5.0 POP/s dense int8 peak, and algorithmic HBM bytes."""
+    import torch
+
+    import paper_2609_10264_amd as mvk
+
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        Ws = []
+        for _ in range(pool):
+            W = torch.randint(-127, 128, (m, n), generator=gen, device=dev, dtype=torch.int8)
+            Ws.append(mvk.pack_weights(W, stream=s))
+            del W
+        X = torch.randint(0, mvk.P, (pool, B, n), generator=gen, device=dev, dtype=torch.int32)
+        Y = torch.empty((B, m), dtype=torch.int32, device=dev)
+        for j in range(pool):
+            mvk.server_eval(Ws[j], X[j], out=Y, stream=s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        for k in range(reps):
+            mvk.server_eval(Ws[k % pool], X[k % pool], out=Y, stream=s)
+
+    def replay():
+        with torch.cuda.stream(s):
+            g.replay()
+
+    warm(replay, args.warm_seconds)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(s):
+        e0.record()
+        g.replay()
+        e1.record()
+    torch.cuda.synchronize()
+    t = 1e-3 * e0.elapsed_time(e1) / reps
+    alg = m * n + 4 * n * B + 4 * m * B
+    ops = 2.0 * 4 * m * n * B
+    del Ws, X, Y, g
+    torch.cuda.empty_cache()
+    return {"workload": f"W {m}x{n} int8-valued, B={B}, packed", "mean_launch_us": 1e6 * t,
+            "modmac_per_s": m * n * B / t, "int8_tops": ops / t / 1e12,
+            "mfma_frac": ops / t / MFMA_INT8_PEAK_OPS, "hbm_gbps": alg / t / 1e9}
 
 
 def stack_bench(args):

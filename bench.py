@@ -1051,11 +1051,24 @@ def paper_eval_bench(args):
             el += time.perf_counter() - t0
             reps += 1
         res["cpu_baseline"] = {"value": 256 * n * reps / el, "unit": "modMAC/s", "cores": 1, "kind": "oracle",
+                               "host_cpu": host_cpu(),
                                "sample": f"{reps} oracle server products of 256 rows x {n} over BabyBear, "
                                          f"{el:.1f} s; single-threaded C, '%' per field op"}
     print(json.dumps(res), flush=True)
     if not ok:
         sys.exit(1)
+
+
+def host_cpu() -> str:
+    """The host CPU model (Linux /proc/cpuinfo), for the CPU baseline's record."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def cpu_baseline(args, cfg, cx_h, cy_h):
@@ -1085,7 +1098,7 @@ def cpu_baseline(args, cfg, cx_h, cy_h):
         steps += 1
         if el >= args.cpu_seconds or steps >= 10000:
             break
-    return {"value": m * n * B * steps / el, "unit": "modMAC/s", "cores": 1, "kind": "oracle",
+    return {"value": m * n * B * steps / el, "unit": "modMAC/s", "cores": 1, "kind": "oracle", "host_cpu": host_cpu(),
             "sample": f"{steps} full steps (encode+server_eval+verify+decode) of the same workload, one W, "
                       f"{el:.1f} s of oracle time (input drawing excluded); single-threaded C, '%' per field op"}
 

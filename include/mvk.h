@@ -33,7 +33,10 @@
  *    enqueued) if one is not; a debugging mode, not for graph capture.
  *  - The library keeps a per-(device, stream) workspace that grows on demand
  *    (hipMalloc at first use and when a larger size is needed); calls enqueued
- *    on two different streams never share workspace memory.
+ *    on two different streams never share workspace memory.  Calls on one
+ *    stream from several host threads at once are not supported (a call that
+ *    grows the workspace frees the old buffer): give each thread its own
+ *    stream.
  */
 #ifndef MVK_H_
 #define MVK_H_
@@ -165,7 +168,7 @@ mvk_status mvk_server_eval_packed(const int8_t *Wp, uint32_t m, uint32_t n, cons
  *         must be set (cx.k == n, cy.k == m)
  *   W   : device, m x n int8
  * Uses a workspace of about m*n + max(Nx*m, Ny*n)*4 bytes.
- * Errors: MVK_EINVAL, MVK_ENOMEM.
+ * Errors: MVK_EINVAL, MVK_ERANGE (a buffer size above 2^62 bytes), MVK_ENOMEM.
  */
 mvk_status mvk_keygen(const mvk_key *key, const int8_t *W, void *stream);
 
@@ -176,7 +179,7 @@ mvk_status mvk_keygen(const mvk_key *key, const int8_t *W, void *stream);
  * state st for decode.
  *   X    : device, B x n field array (plaintext queries)
  *   Xhat : device, B x n field array, written
- * Errors: MVK_EINVAL, MVK_ENOMEM.
+ * Errors: MVK_EINVAL, MVK_ERANGE (B > 65535), MVK_ENOMEM.
  */
 mvk_status mvk_encode(const mvk_key *key, const uint32_t *X, uint32_t B, const mvk_sparse *ex,
                       uint32_t *Xhat, void *stream);
@@ -364,6 +367,8 @@ mvk_status mvk_batch_verify(const mvk_code *cy, const mvk_code *c2, const uint32
 /*
  * RAA encoding w -> G^T w (App. B, "Linear-time encoding") for `count`
  * vectors.  w: device, count x k field array; out: device, count x N.
+ * Uses a workspace of N*count words.
+ * Errors: MVK_EINVAL, MVK_ERANGE (N*count*4 above 2^62 bytes), MVK_ENOMEM.
  */
 mvk_status mvk_raa_encode(const mvk_code *code, const uint32_t *w, uint32_t count, uint32_t *out,
                           void *stream);
@@ -371,6 +376,7 @@ mvk_status mvk_raa_encode(const mvk_code *code, const uint32_t *w, uint32_t coun
 /*
  * RAA syndrome v -> G v (App. B, transposition principle) for `count` dense
  * vectors.  v: device, count x N field array; out: device, count x k.
+ * Errors: MVK_EINVAL, MVK_ERANGE (count > 65535), MVK_ENOMEM.
  */
 mvk_status mvk_raa_syndrome(const mvk_code *code, const uint32_t *v, uint32_t count,
                             uint32_t *out, void *stream);

@@ -113,6 +113,16 @@ mvk_status check_all(hipStream_t s, std::initializer_list<std::pair<const uint32
 
 inline size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// True if a*b elements of `elem` bytes exceed 2^62 bytes: no such buffer can
+// exist, and the size arithmetic below would wrap; the call returns MVK_ERANGE.
+inline bool too_big(uint64_t a, uint64_t b, uint64_t elem) {
+    return a != 0 && b > ((1ull << 62) / elem) / a;
+}
+
+// Vectors per call of the syndrome kernels: the count is a grid dimension of
+// the segmented form.
+constexpr uint32_t kMaxSynCount = 65535u;
+
 mvk_status check_code(const mvk_code* c, uint32_t k) {
     if (!c || !c->pi1 || !c->pi2 || !c->v1 || !c->v2) return MVK_EINVAL;
     if (c->k != k || c->r == 0 || k == 0) return MVK_EINVAL;
@@ -242,6 +252,7 @@ mvk_status mvk_keygen(const mvk_key* key, const int8_t* W, void* stream) {
     hipStream_t s = (hipStream_t)stream;
     const uint32_t m = key->m, n = key->n;
     const size_t Nx = (size_t)key->cx.r * n, Ny = (size_t)key->cy.r * m;
+    if (too_big(m, n, 1) || too_big(Nx, m, 4) || too_big(Ny, n, 4)) return MVK_ERANGE;
     const size_t wt_bytes = align_up((size_t)m * n);
     const size_t t3_bytes = (Nx * m > Ny * n ? Nx * m : Ny * n) * sizeof(uint32_t);
     void* ws = nullptr;
@@ -263,6 +274,7 @@ mvk_status mvk_encode(const mvk_key* key, const uint32_t* X, uint32_t B, const m
     if (st) return st;
     if (B == 0) return MVK_OK;
     if (!X || !Xhat || !ex || ex->count != B || (ex->t && (!ex->idx || !ex->val))) return MVK_EINVAL;
+    if (B > kMaxSynCount) return MVK_ERANGE;
     hipStream_t s = (hipStream_t)stream;
     const size_t Nx = (size_t)key->cx.r * key->n;
     if (ex->t > Nx) return MVK_EINVAL;
@@ -464,6 +476,7 @@ mvk_status mvk_batch_preprocess(uint32_t B, const uint32_t* const* Q, uint32_t N
     for (uint32_t b = 0; b < B; ++b)
         if (!Q[b]) return MVK_EINVAL;
     const uint64_t N2 = Bn * c2->r;
+    if (too_big(N, N2, sizeof(uint32_t))) return MVK_ERANGE;
     hipStream_t s = (hipStream_t)stream;
     void* ws = nullptr;
     st = workspace(s, (size_t)N * N2 * sizeof(uint32_t), &ws);  // column scratch of the batched encoder
@@ -533,6 +546,7 @@ mvk_status mvk_raa_encode(const mvk_code* code, const uint32_t* w, uint32_t coun
     if (!w || !out) return MVK_EINVAL;
     hipStream_t s = (hipStream_t)stream;
     const size_t N = (size_t)code->k * code->r;
+    if (too_big(N, count, sizeof(uint32_t))) return MVK_ERANGE;
     void* ws = nullptr;
     st = workspace(s, N * count * sizeof(uint32_t), &ws);
     if (st) return st;
@@ -545,6 +559,7 @@ mvk_status mvk_raa_syndrome(const mvk_code* code, const uint32_t* v, uint32_t co
     if (st) return st;
     if (count == 0) return MVK_OK;
     if (!v || !out) return MVK_EINVAL;
+    if (count > kMaxSynCount) return MVK_ERANGE;
     hipStream_t s = (hipStream_t)stream;
     const size_t N = (size_t)code->k * code->r;
     void* ws = nullptr;

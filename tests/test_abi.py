@@ -90,6 +90,32 @@ def test_host_argument_checks_without_device_work():
     assert lib.mvk_raa_syndrome(ctypes.byref(nullcode), fake, 1, fake, None) == L.MVK_EINVAL
 
 
+def test_sizes_no_buffer_can_hold_are_rejected():
+    """Sizes whose buffers would exceed 2^62 bytes, and vector counts beyond the
+    syndrome kernels' grid dimension, return MVK_ERANGE before any device work."""
+    L = _lib()
+    lib = L.load()
+    fake = ctypes.c_void_p(0x1000)
+    # keygen: Nx * m words of scratch with Nx = 2^31 - 1, m = 2^31 - 1
+    cx = L.MvkCode(1, 0x7FFFFFFF, 0x1000, 0x1000, 0x1000, 0x1000)
+    cy = L.MvkCode(0x7FFFFFFF, 1, 0x1000, 0x1000, 0x1000, 0x1000)
+    key = L.MvkKey(0x7FFFFFFF, 1, cx, cy, 0x1000, 0x1000)
+    assert lib.mvk_keygen(ctypes.byref(key), fake, None) == L.MVK_ERANGE
+    # raa_encode: N * count words of scratch
+    big = L.MvkCode(1 << 30, 1, 0x1000, 0x1000, 0x1000, 0x1000)
+    assert lib.mvk_raa_encode(ctypes.byref(big), fake, 0xFFFFFFFF, fake, None) == L.MVK_ERANGE
+    # syndromes of more than 65535 vectors in one call
+    small = L.MvkCode(8, 2, 0x1000, 0x1000, 0x1000, 0x1000)
+    assert lib.mvk_raa_syndrome(ctypes.byref(small), fake, 65536, fake, None) == L.MVK_ERANGE
+    key8 = L.MvkKey(8, 8, small, small, 0x1000, 0x1000)
+    ex = L.MvkSparse(None, None, 0, 65536)
+    assert lib.mvk_encode(ctypes.byref(key8), fake, 65536, ctypes.byref(ex), fake, None) == L.MVK_ERANGE
+    # batch_preprocess: N * N' words of scratch
+    qs = (ctypes.c_void_p * 1)(0x1000)
+    c2 = L.MvkCode(1 << 30, 1, 0x1000, 0x1000, 0x1000, 0x1000)
+    assert lib.mvk_batch_preprocess(1, qs, 0xFFFFFFFF, 1 << 30, ctypes.byref(c2), fake, fake, None) == L.MVK_ERANGE
+
+
 def test_verify_argument_checks_without_device_work():
     L = _lib()
     lib = L.load()

@@ -23,33 +23,44 @@ namespace {
 constexpr int kPrepThreads = 1024;     // syndrome workgroups hold a block of up to 16384 positions
 constexpr int kQuarter = 256;          // gather items per workgroup: kPrepThreads / kQuarter
 constexpr int kQuarters = kPrepThreads / kQuarter;
-constexpr int kQCols = 64;             // columns per gather item, one per lane
-constexpr int kQGroups = kQuarter / kQCols;  // waves per item, each a share of the sparse terms
+constexpr int kQGroups = kQuarter / 64;  // waves per item, each a share of the sparse terms
 constexpr int kQBatch = 16;            // gathers in flight per thread
 
+// Columns per gather item: one per lane, or with VEC four consecutive ones per
+// lane (16-byte loads: a wave reads 1 KiB of a row per term).
+constexpr uint32_t gather_cols(bool vec) { return vec ? 256u : 64u; }
+// 64-bit partial sums of one item in LDS (a value per wave and column)
+constexpr size_t gather_part(bool vec) { return (size_t)kQGroups * gather_cols(vec); }
+
 // One gather item by a 256-thread quarter of the workgroup:
-// out[i] = sum_s val[s] * M[idx[s], i] for the 64 columns i in [col0, col0+64).
-// Every quarter of the workgroup passes the one barrier here; a quarter with
-// no item (live = false) issues no loads and writes nothing.  COHERENT: the
-// results are stored device-coherently.
-template <bool COHERENT>
+// out[i] = sum_s val[s] * M[idx[s], i] for the gather_cols(VEC) columns i from
+// col0.  The four waves take a contiguous share of the terms each and add
+// their partial sums in LDS (`part`, gather_part(VEC) values).  VEC: ld
+// is a multiple of 4 and M 16-byte aligned, so a lane's four columns are all
+// in the row or all past it.  Every quarter of the workgroup passes the one
+// barrier here; a quarter with no item (live = false) issues no loads and
+// writes nothing.  COHERENT: the results are stored device-coherently.
+template <bool COHERENT, bool VEC>
 __device__ __forceinline__ void gather_item(const uint32_t* __restrict__ M, uint32_t ld, uint32_t nrows,
                                             const uint32_t* __restrict__ idx, const uint32_t* __restrict__ val,
                                             uint32_t t, uint32_t* __restrict__ out, uint32_t col0, bool live,
-                                            uint64_t (*part)[kQCols]) {
+                                            uint64_t* part) {
+    constexpr int E = VEC ? 4 : 1;  // columns per lane
     const int ltid = threadIdx.x & (kQuarter - 1);
     const int lane = ltid & 63;
     const int g = __builtin_amdgcn_readfirstlane(ltid >> 6);
-    const uint32_t i = col0 + lane;
-    const bool act = live && i < ld;
-    const uint32_t is = act ? i : 0u;
+    const uint32_t i0 = col0 + (uint32_t)lane * E;
+    const bool act = live && i0 < ld;
+    const uint32_t is = act ? i0 : 0u;
     const uint32_t tt = live ? t : 0u;
     const uint32_t chunk = (tt + kQGroups - 1) / kQGroups;
     const uint32_t s_beg = (uint32_t)g * chunk;
     const uint32_t s_end = s_beg + chunk < tt ? s_beg + chunk : tt;
-    uint64_t acc = 0;
+    uint64_t acc[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] = 0;
     for (uint32_t s0 = s_beg; s0 < s_end; s0 += kQBatch) {
-        uint32_t mv[kQBatch], ww[kQBatch];
+        uint32_t mv[kQBatch][E], ww[kQBatch];
 #pragma unroll
         for (int u = 0; u < kQBatch; ++u) {
             const uint32_t sx = s0 + (uint32_t)u;
@@ -58,27 +69,42 @@ __device__ __forceinline__ void gather_item(const uint32_t* __restrict__ M, uint
             uint32_t j = idx[sl];
             j = j < nrows ? j : nrows - 1;
             ww[u] = ok ? val[sl] : 0u;
-            mv[u] = M[(size_t)j * ld + is];
+            const uint32_t* src = M + (size_t)j * ld + is;
+            if constexpr (VEC) {
+                const uint4 v = *reinterpret_cast<const uint4*>(src);
+                mv[u][0] = v.x;
+                mv[u][1] = v.y;
+                mv[u][2] = v.z;
+                mv[u][3] = v.w;
+            } else {
+                mv[u][0] = *src;
+            }
         }
 #pragma unroll
-        for (int u = 0; u < kQBatch; ++u) acc += ffold((uint64_t)ww[u] * mv[u]);
+        for (int u = 0; u < kQBatch; ++u)
+#pragma unroll
+            for (int e = 0; e < E; ++e) acc[e] += ffold((uint64_t)ww[u] * mv[u][e]);
     }
-    part[g][lane] = acc;
+#pragma unroll
+    for (int e = 0; e < E; ++e) part[(g * E + e) * 64 + lane] = acc[e];
     __syncthreads();
     if (g == 0 && act) {
-        uint64_t tot = 0;
 #pragma unroll
-        for (int h = 0; h < kQGroups; ++h) tot += part[h][lane];
-        if (COHERENT)
-            __hip_atomic_store(&out[i], fred64(tot), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        else
-            out[i] = fred64(tot);
+        for (int e = 0; e < E; ++e) {
+            uint64_t tot = 0;
+#pragma unroll
+            for (int h = 0; h < kQGroups; ++h) tot += part[(h * E + e) * 64 + lane];
+            if (COHERENT)
+                __hip_atomic_store(&out[i0 + e], fred64(tot), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            else
+                out[i0 + e] = fred64(tot);
+        }
     }
 }
 
 template <int U>
 constexpr size_t prep_lds_words() {
-    constexpr size_t gather = (size_t)kQuarters * kQGroups * kQCols * 2;
+    constexpr size_t gather = (size_t)kQuarters * gather_part(true) * 2;
     if constexpr (U > 0)
         return syn::lds_words<U, kPrepThreads>() > gather ? syn::lds_words<U, kPrepThreads>() : gather;
     else
@@ -95,7 +121,7 @@ struct PrepArgs {
     uint32_t tx, nx;  // nx noise vectors (My items), tx terms each
     const uint32_t *ey_idx, *ey_val;
     uint32_t ty, ny;  // ny challenges (U items), ty terms each
-    uint32_t nbm, nbn;  // 64-column blocks of m and n
+    uint32_t nbm, nbn;  // gather_cols(VEC)-column blocks of m and n
     const uint32_t *PT, *Q;
     uint32_t* Mx;
     uint32_t* My;
@@ -109,13 +135,13 @@ struct PrepArgs {
 
 // Workgroups [0, nsx) and [nsx, nsx + nsy): one syndrome each (U > 0; the
 // whole block in LDS); the rest: kQuarters gather items each, first the
-// nx * ceil(m/64) items of My (rows of PT), then the ny * ceil(n/64) items of
-// U (rows of Q).
+// nx * nbm items of My (rows of PT), then the ny * nbn items of U (rows of Q).
+// VEC: m and n are multiples of 4 and PT, Q 16-byte aligned.
 // SIG: every output is stored device-coherently; each workgroup waits for its
 // stores to complete (vmcnt 0) before the barrier and then counts itself done
 // (count.h); the last one sets the done flag, so a kernel of another stream
 // that sees the flag sees every output.
-template <int U, bool SIG>
+template <int U, bool SIG, bool VEC>
 __global__ __launch_bounds__(kPrepThreads) void client_prepare_kernel(PrepArgs a) {
     __shared__ __align__(16) uint32_t lds[prep_lds_words<U>()];
     uint32_t bid = blockIdx.x;
@@ -135,20 +161,21 @@ __global__ __launch_bounds__(kPrepThreads) void client_prepare_kernel(PrepArgs a
     }
     if (gather) {
         const int quarter = threadIdx.x / kQuarter;
-        auto part = reinterpret_cast<uint64_t (*)[kQCols]>(lds) + quarter * kQGroups;
+        uint64_t* part = reinterpret_cast<uint64_t*>(lds) + quarter * gather_part(VEC);
+        constexpr uint32_t cols = gather_cols(VEC);
         const uint32_t item = bid * kQuarters + (uint32_t)quarter;
         const uint32_t nbm = a.nbm, nbn = a.nbn;
         const uint32_t ix = a.nx * nbm, iy = a.ny * nbn;
         if (item < ix) {
             const uint32_t b = item / nbm, cb = item % nbm;
-            gather_item<SIG>(a.PT, a.m, a.rx * a.n, a.ex_idx + (size_t)b * a.tx, a.ex_val + (size_t)b * a.tx, a.tx,
-                             a.My + (size_t)b * a.m, cb * kQCols, true, part);
+            gather_item<SIG, VEC>(a.PT, a.m, a.rx * a.n, a.ex_idx + (size_t)b * a.tx, a.ex_val + (size_t)b * a.tx,
+                                  a.tx, a.My + (size_t)b * a.m, cb * cols, true, part);
         } else if (item < ix + iy) {
             const uint32_t q = (item - ix) / nbn, cb = (item - ix) % nbn;
-            gather_item<SIG>(a.Q, a.n, a.ry * a.m, a.ey_idx + (size_t)q * a.ty, a.ey_val + (size_t)q * a.ty, a.ty,
-                             a.Uq + (size_t)q * a.n, cb * kQCols, true, part);
+            gather_item<SIG, VEC>(a.Q, a.n, a.ry * a.m, a.ey_idx + (size_t)q * a.ty, a.ey_val + (size_t)q * a.ty,
+                                  a.ty, a.Uq + (size_t)q * a.n, cb * cols, true, part);
         } else {
-            gather_item<SIG>(nullptr, 0u, 1u, nullptr, nullptr, 0u, nullptr, 0u, false, part);
+            gather_item<SIG, VEC>(nullptr, 0u, 1u, nullptr, nullptr, 0u, nullptr, 0u, false, part);
         }
     }
     if constexpr (SIG) {
@@ -172,20 +199,21 @@ __device__ __forceinline__ bool poll_flag(const uint32_t* flag, uint32_t value, 
 }
 
 // out[v][i] = sum_s val[v*t + s] * M[idx[v*t + s], i] for `count` sparse
-// vectors v (M: nrows x ld): nb = ceil(ld/64) items per vector, four per
-// workgroup.
+// vectors v (M: nrows x ld): nb = ceil(ld / gather_cols(VEC)) items per
+// vector, four per workgroup.
+template <bool VEC>
 __global__ __launch_bounds__(kPrepThreads) void gather_rows_kernel(const uint32_t* __restrict__ M, uint32_t ld,
                                                                    uint32_t nrows, const uint32_t* __restrict__ idx,
                                                                    const uint32_t* __restrict__ val, uint32_t t,
                                                                    uint32_t count, uint32_t nb,
                                                                    uint32_t* __restrict__ out) {
-    __shared__ uint64_t part[kQuarters * kQGroups][kQCols];
+    __shared__ uint64_t part[kQuarters * gather_part(VEC)];
     const int quarter = threadIdx.x / kQuarter;
     const uint32_t item = blockIdx.x * kQuarters + (uint32_t)quarter;
     const bool live = item < count * nb;
     const uint32_t v = live ? item / nb : 0u, cb = live ? item % nb : 0u;
-    gather_item<false>(M, ld, nrows, idx + (size_t)v * t, val + (size_t)v * t, t, out + (size_t)v * ld, cb * kQCols,
-                       live, part + quarter * kQGroups);
+    gather_item<false, VEC>(M, ld, nrows, idx + (size_t)v * t, val + (size_t)v * t, t, out + (size_t)v * ld,
+                            cb * gather_cols(VEC), live, part + quarter * gather_part(VEC));
 }
 
 // Xhat = X + Mx, element-wise over count words, PER words per thread and
@@ -287,12 +315,18 @@ uint32_t prep_u(uint64_t N) {
     return 0;
 }
 
+// Whether the gathers of client_prepare_kernel read 16 bytes per lane.
+bool prep_vec(const mvk_key& key) {
+    return key.m % 4 == 0 && key.n % 4 == 0 && ((uintptr_t)key.PT & 15) == 0 && ((uintptr_t)key.Q & 15) == 0;
+}
+
 // Workgroups of client_prepare_kernel: one per syndrome short enough for one
 // workgroup, then the gather items, kQuarters per workgroup.
 uint64_t prep_grid(const mvk_key& key, uint32_t nx, uint32_t ny) {
     const uint64_t Nx = (uint64_t)key.cx.r * key.n, Ny = (uint64_t)key.cy.r * key.m;
     const uint32_t ux = nx ? prep_u(Nx) : 0u, uy = ny ? prep_u(Ny) : 0u;
-    const uint64_t items = (uint64_t)nx * ceil_div(key.m, kQCols) + (uint64_t)ny * ceil_div(key.n, kQCols);
+    const uint32_t cols = gather_cols(prep_vec(key));
+    const uint64_t items = (uint64_t)nx * ceil_div(key.m, cols) + (uint64_t)ny * ceil_div(key.n, cols);
     return (ux ? nx : 0u) + (uy ? ny : 0u) + (items + kQuarters - 1) / kQuarters;
 }
 
@@ -330,7 +364,8 @@ hipError_t launch_client_prepare(const mvk_key& key, const uint32_t* ex_idx, con
     a.ypi1 = key.cy.pi1, a.ypi2 = key.cy.pi2, a.yv1 = key.cy.v1, a.yv2 = key.cy.v2;
     a.ex_idx = ex_idx, a.ex_val = ex_val, a.tx = tx, a.nx = nx;
     a.ey_idx = ey_idx, a.ey_val = ey_val, a.ty = ty, a.ny = ny;
-    a.nbm = ceil_div(key.m, kQCols), a.nbn = ceil_div(key.n, kQCols);
+    const bool vec = prep_vec(key);
+    a.nbm = ceil_div(key.m, gather_cols(vec)), a.nbn = ceil_div(key.n, gather_cols(vec));
     a.PT = key.PT, a.Q = key.Q;
     a.Mx = Mx, a.My = My, a.R = R, a.Uq = Uq;
     a.counter = counter, a.done = done, a.done_value = done_value;
@@ -339,28 +374,42 @@ hipError_t launch_client_prepare(const mvk_key& key, const uint32_t* ex_idx, con
     if (grid == 0) return hipSuccess;
     if (grid > 0x7fffffffu) return hipErrorInvalidValue;
     a.slots = count_slots((uint32_t)grid);
-#define MVK_PREP(UU)                                                                                        \
-    if (done)                                                                                               \
-        hipLaunchKernelGGL((client_prepare_kernel<UU, true>), dim3((uint32_t)grid), dim3(kPrepThreads), 0, s, a); \
-    else                                                                                                    \
-        hipLaunchKernelGGL((client_prepare_kernel<UU, false>), dim3((uint32_t)grid), dim3(kPrepThreads), 0, s, a)
+#define MVK_PREP_V(UU, SIG)                                                                                     \
+    if (vec)                                                                                                    \
+        hipLaunchKernelGGL((client_prepare_kernel<UU, SIG, true>), dim3((uint32_t)grid), dim3(kPrepThreads), 0, s, \
+                           a);                                                                                  \
+    else                                                                                                        \
+        hipLaunchKernelGGL((client_prepare_kernel<UU, SIG, false>), dim3((uint32_t)grid), dim3(kPrepThreads), 0,   \
+                           s, a)
+#define MVK_PREP(UU)          \
+    if (done) {               \
+        MVK_PREP_V(UU, true);  \
+    } else {                  \
+        MVK_PREP_V(UU, false); \
+    }
     if (U == 0) { MVK_PREP(0); }
     else if (U == 4) { MVK_PREP(4); }
     else if (U == 8) { MVK_PREP(8); }
     else if (U == 12) { MVK_PREP(12); }
     else { MVK_PREP(16); }
 #undef MVK_PREP
+#undef MVK_PREP_V
     return hipGetLastError();
 }
 
 hipError_t launch_gather_rows(const uint32_t* M, uint32_t ld, uint32_t nrows, const uint32_t* idx,
                               const uint32_t* val, uint32_t t, uint32_t count, uint32_t* out, hipStream_t s) {
     if (count == 0 || ld == 0) return hipSuccess;
-    const uint32_t nb = ceil_div(ld, kQCols);
+    const bool vec = ld % 4 == 0 && ((uintptr_t)M & 15) == 0;
+    const uint32_t nb = ceil_div(ld, gather_cols(vec));
     const uint64_t grid = ((uint64_t)count * nb + kQuarters - 1) / kQuarters;
     if (grid > 0x7fffffffu) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(gather_rows_kernel, dim3((uint32_t)grid), dim3(kPrepThreads), 0, s, M, ld, nrows, idx, val, t,
-                       count, nb, out);
+    if (vec)
+        hipLaunchKernelGGL(gather_rows_kernel<true>, dim3((uint32_t)grid), dim3(kPrepThreads), 0, s, M, ld, nrows,
+                           idx, val, t, count, nb, out);
+    else
+        hipLaunchKernelGGL(gather_rows_kernel<false>, dim3((uint32_t)grid), dim3(kPrepThreads), 0, s, M, ld, nrows,
+                           idx, val, t, count, nb, out);
     return hipGetLastError();
 }
 

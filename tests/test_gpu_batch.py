@@ -60,6 +60,7 @@ SHAPES = [  # cid, m, n, B, r, r2
     (101, 1000, 300, 4, 3, 2),
     (102, 6000, 96, 2, 3, 2),     # primary block length 18000: segmented syndromes
     (103, 500, 5000, 2, 2, 2),    # secondary block length 20000: segmented syndromes
+    (104, 300, 75, 3, 3, 2),      # B*n = 225: 4-byte gathers of the projection
 ]
 
 

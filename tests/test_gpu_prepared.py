@@ -36,13 +36,15 @@ def _dense(N, idx, val):
 
 # cid, m, n, B, r_x, r_y, t_x, ell: block lengths in the one-launch range and
 # above it (Nx = 16500, Ny = 18000: the syndromes take their own launches),
-# several noise vectors and challenges, ragged 64-column blocks.
+# several noise vectors and challenges, ragged column blocks of the 16-byte
+# gathers (m, n multiples of 4) and of the 4-byte ones (85: m, n odd).
 PREP = [
     (80, 256, 256, 1, 2, 2, 8, 2),
     (81, 1000, 700, 3, 3, 2, 17, 3),
     (82, 4096, 4096, 1, 3, 3, 64, 2),
     (83, 300, 5500, 2, 3, 3, 64, 2),
     (84, 6000, 200, 1, 1, 3, 5, 16),
+    (85, 1001, 703, 3, 3, 2, 17, 3),
 ]
 
 

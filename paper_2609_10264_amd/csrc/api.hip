@@ -334,7 +334,8 @@ mvk_status decode_verify_run(const mvk_key* key, const uint32_t* Xhat, const uin
     if (st) return st;
     uint32_t* rv = (uint32_t*)ws;
     uint32_t* syn_scratch = (uint32_t*)((char*)ws + r_bytes);
-    if (Ny <= kSynScratchAbove && dv_syn_fits(m, key->n, (uint32_t)Ny, B, ell)) {
+    if (Ny <= kSynScratchAbove &&
+        dv_syn_fits(m, key->n, (uint32_t)Ny, B, ell, dv_decode_cols(m, B, key->PT, Yhat, Y, rv))) {
         // one launch: the syndromes overlap the Decrypt and Verify gathers
         const mvk_code& cy = key->cy;
         return hip_status(launch_decode_verify_syn(

@@ -18,6 +18,8 @@
 // Every (repetition, column) sum has nsub accumulators, 64 bits each, which
 // the workgroups of a column use in turn (block index mod nsub): atomics on one
 // address are serialised, so this bounds the workgroups per address.
+#include <initializer_list>
+
 #include "count.h"
 #include "field.h"
 #include "mvk_internal.h"
@@ -62,6 +64,27 @@ constexpr int kPreQ = 4;
 constexpr int kPreB = 4;
 constexpr int kItems = kMaxEll;  // verify work items (repetition, chunk) per workgroup, at most
 
+// E consecutive words at p (E = 4: one 16-byte access; p 16-byte aligned).
+template <int E>
+__device__ __forceinline__ void load_cols(const uint32_t* p, uint32_t (&v)[E]) {
+    if constexpr (E == 4) {
+        const uint4 t = *reinterpret_cast<const uint4*>(p);
+        v[0] = t.x;
+        v[1] = t.y;
+        v[2] = t.z;
+        v[3] = t.w;
+    } else {
+        v[0] = *p;
+    }
+}
+template <int E>
+__device__ __forceinline__ void store_cols(uint32_t* p, const uint32_t (&v)[E]) {
+    if constexpr (E == 4)
+        *reinterpret_cast<uint4*>(p) = make_uint4(v[0], v[1], v[2], v[3]);
+    else
+        *p = v[0];
+}
+
 // Workgroup of decode_verify_syn: 512 threads, so that one workgroup holds the
 // syndrome of a block of up to 512 * 32 = 16384 positions in LDS.
 constexpr int kFusedThreads = kDvSynThreads;
@@ -77,43 +100,50 @@ constexpr int kFusedGroups = kFusedThreads / kCols;
 // over a second in total): a wait that does not end is reported, not hung.
 constexpr uint32_t kSpinLimit = 1u << 24;
 
-// Decode role: columns [cb*kCols, cb*kCols + kCols) of response b, by the
-// G*64 threads of the workgroup.  WAIT_R: the r_q are being written by other
+// Decode role: columns [cb*kCols*E, (cb+1)*kCols*E) of response b, E
+// consecutive ones per lane, by the G*64 threads of the workgroup; the
+// partial sums of the groups meet in `part` (G*E*64 values).  E = 4: m is a
+// multiple of 4 and PT, Yhat, Y and rv are 16-byte aligned (16-byte loads, so
+// a wave reads 1 KiB of a row of PT per term).  WAIT_R: the r_q are being written by other
 // workgroups of the same launch; thread 0 waits until `rdone` reaches ell (or
 // the spin limit passes, which sets *err), then, after a workgroup barrier,
 // the r_q are read device-coherently.
 //
 // PRE: the output mask P e_b is given (My, B x m, from client_prepare) and
 // replaces the gathers.
-template <bool WAIT_R, int G, bool PRE = false>
+template <bool WAIT_R, int G, bool PRE = false, int E = 1>
 __device__ __forceinline__ void decode_part(const uint32_t* __restrict__ PT, uint32_t m, uint32_t Nx,
                                             const uint32_t* __restrict__ Yhat, uint32_t B,
                                             const uint32_t* __restrict__ ex_idx, const uint32_t* __restrict__ ex_val,
                                             uint32_t tx, const uint32_t* rv, uint32_t ell,
                                             uint32_t* __restrict__ Y, unsigned long long* accR, uint32_t nsub,
-                                            uint32_t b, uint32_t cb, uint64_t (*part)[kCols], uint32_t* rdone,
+                                            uint32_t b, uint32_t cb, uint64_t* part, uint32_t* rdone,
                                             uint32_t* err, const uint32_t* __restrict__ My = nullptr) {
+    static_assert(E == 1 || E == 4, "one or four columns per lane");
     const int lane = threadIdx.x & 63;
     const int g = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform group
-    const uint32_t i = cb * kCols + lane;
-    const bool act = i < m;
-    const uint32_t is = act ? i : 0u;
+    const uint32_t i0 = cb * (kCols * E) + (uint32_t)lane * E;
+    const bool act = i0 < m;
+    const uint32_t is = act ? i0 : 0u;
     const uint32_t* ei = ex_idx + (size_t)b * tx;
     const uint32_t* ev = ex_val + (size_t)b * tx;
-    const uint32_t yraw = Yhat[(size_t)b * m + is];
-    uint32_t rq[kPreQ];
+    uint32_t yraw[E];
+    load_cols<E>(Yhat + (size_t)b * m + is, yraw);
+    uint32_t rq[kPreQ][E];
     if (!WAIT_R && g == 0) {
 #pragma unroll
-        for (int q = 0; q < kPreQ; ++q) rq[q] = rv[(size_t)((uint32_t)q < ell ? q : 0) * m + is];
+        for (int q = 0; q < kPreQ; ++q) load_cols<E>(rv + (size_t)((uint32_t)q < ell ? q : 0) * m + is, rq[q]);
     }
     // group g takes the contiguous terms [g*chunk, min(tx, g*chunk + chunk))
     if (PRE) tx = 0;
     const uint32_t chunk = (tx + G - 1) / G;
     const uint32_t s_beg = (uint32_t)g * chunk;
     const uint32_t s_end = s_beg + chunk < tx ? s_beg + chunk : tx;
-    uint64_t acc = 0;
+    uint64_t acc[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] = 0;
     for (uint32_t s0 = s_beg; s0 < s_end; s0 += kBatch) {
-        uint32_t pv[kBatch], ww[kBatch];
+        uint32_t pv[kBatch][E], ww[kBatch];
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
             const uint32_t s = s0 + (uint32_t)u;
@@ -122,20 +152,35 @@ __device__ __forceinline__ void decode_part(const uint32_t* __restrict__ PT, uin
             uint32_t j = ei[sl];
             j = j < Nx ? j : Nx - 1;
             ww[u] = ok ? ev[sl] : 0u;
-            pv[u] = PT[(size_t)j * m + is];
+            load_cols<E>(PT + (size_t)j * m + is, pv[u]);
         }
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) acc += ffold((uint64_t)ww[u] * pv[u]);
-    }
-    if (PRE && g == 0) acc = My[(size_t)b * m + is];
-    part[g][lane] = acc;
-    __syncthreads();
-    const uint32_t yh = act ? yraw : 0u;
-    if (g == 0) {
-        uint64_t tot = 0;
+        for (int u = 0; u < kBatch; ++u)
 #pragma unroll
-        for (int h = 0; h < G; ++h) tot += part[h][lane];
-        if (act && Y) Y[(size_t)b * m + i] = fsub(yh, fred64(tot));
+            for (int e = 0; e < E; ++e) acc[e] += ffold((uint64_t)ww[u] * pv[u][e]);
+    }
+    if (PRE && g == 0) {
+        uint32_t mm[E];
+        load_cols<E>(My + (size_t)b * m + is, mm);
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[e] = mm[e];
+    }
+#pragma unroll
+    for (int e = 0; e < E; ++e) part[(g * E + e) * 64 + lane] = acc[e];
+    __syncthreads();
+    uint32_t yh[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) yh[e] = act ? yraw[e] : 0u;
+    if (g == 0) {
+        uint32_t y[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            uint64_t tot = 0;
+#pragma unroll
+            for (int h = 0; h < G; ++h) tot += part[(h * E + e) * 64 + lane];
+            y[e] = fsub(yh[e], fred64(tot));
+        }
+        if (act && Y) store_cols<E>(Y + (size_t)b * m + i0, y);
     }
     if (WAIT_R) {
         if (threadIdx.x == 0) {
@@ -152,21 +197,34 @@ __device__ __forceinline__ void decode_part(const uint32_t* __restrict__ PT, uin
         if (g == 0) {
 #pragma unroll
             for (int q = 0; q < kPreQ; ++q)
-                rq[q] = __hip_atomic_load(&rv[(size_t)((uint32_t)q < ell ? q : 0) * m + is], __ATOMIC_RELAXED,
-                                          __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+                for (int e = 0; e < E; ++e)
+                    rq[q][e] = __hip_atomic_load(&rv[(size_t)((uint32_t)q < ell ? q : 0) * m + is + e],
+                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
     if (g == 0) {
         // v_R partial: sum over this block's outputs of r_q[i] * yhat[i]
         for (uint32_t q = 0; q < ell; ++q) {
-            uint32_t r = 0;
+            uint32_t r[E];
+#pragma unroll
+            for (int e = 0; e < E; ++e) r[e] = 0;
 #pragma unroll
             for (int u = 0; u < kPreQ; ++u)
-                if ((uint32_t)u == q) r = rq[u];
-            if (q >= (uint32_t)kPreQ)
-                r = WAIT_R ? __hip_atomic_load(&rv[(size_t)q * m + is], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                           : rv[(size_t)q * m + is];
-            const uint64_t ws = wave_sum_u64(ffold((uint64_t)r * yh));
+                if ((uint32_t)u == q)
+#pragma unroll
+                    for (int e = 0; e < E; ++e) r[e] = rq[u][e];
+            if (q >= (uint32_t)kPreQ) {
+#pragma unroll
+                for (int e = 0; e < E; ++e)
+                    r[e] = WAIT_R ? __hip_atomic_load(&rv[(size_t)q * m + is + e], __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_AGENT)
+                                  : rv[(size_t)q * m + is + e];
+            }
+            uint64_t t = 0;
+#pragma unroll
+            for (int e = 0; e < E; ++e) t += ffold((uint64_t)r[e] * yh[e]);
+            const uint64_t ws = wave_sum_u64(t);
             if (lane == 0) atomicAdd(&accR[((size_t)q * B + b) * nsub + cb % nsub], (unsigned long long)fred64(ws));
         }
     }
@@ -304,7 +362,7 @@ __device__ __forceinline__ void finish(uint32_t B, uint32_t ell, uint32_t nsub, 
 //
 // PRE: the output masks My and the vectors u_q (U) come from client_prepare;
 // the workgroups then only stream Yhat, My, r and U, Xhat.
-template <bool PRE>
+template <bool PRE, int E>
 __global__ __launch_bounds__(kB) void decode_verify_fused(
     const uint32_t* __restrict__ PT, const uint32_t* __restrict__ Q, uint32_t m, uint32_t n, uint32_t Nx,
     uint32_t Ny, const uint32_t* __restrict__ Xhat, const uint32_t* __restrict__ Yhat, uint32_t B,
@@ -320,8 +378,8 @@ __global__ __launch_bounds__(kB) void decode_verify_fused(
     const uint32_t bid = blockIdx.x;
     const uint32_t ndec = B * nblkR;
     if (bid < ndec)
-        decode_part<false, kGroups, PRE>(PT, m, Nx, Yhat, B, ex_idx, ex_val, tx, rv, ell, Y, accR, nsub,
-                                         bid / nblkR, bid % nblkR, part, nullptr, nullptr, My);
+        decode_part<false, kGroups, PRE, E>(PT, m, Nx, Yhat, B, ex_idx, ex_val, tx, rv, ell, Y, accR, nsub,
+                                            bid / nblkR, bid % nblkR, &part[0][0], nullptr, nullptr, My);
     else
         verify_part<kGroups, PRE>(Q, n, Ny, Xhat, B, ey_idx, ey_val, ty, ell, accL, nsub, bid - ndec, part, u_s,
                                   U);
@@ -347,9 +405,12 @@ __device__ __forceinline__ void syn_part(uint32_t c, uint32_t k, uint32_t r, con
 // LDS words of decode_verify_syn<U>: the syndrome work arrays, or the part and
 // u_s arrays of the gather roles, whichever is larger (a workgroup has one role).
 constexpr size_t kGatherWords = (sizeof(uint64_t) * kItems * kCols + sizeof(uint32_t) * kMaxEll * kCols) / 4;
+constexpr size_t kDecodeWords = 2 * (size_t)kFusedGroups * 4 * kCols;  // decode role, E = 4
+static_assert(kItems * kCols >= kGroups * 4 * kCols, "decode_verify_fused: part holds the decode role's sums");
 template <int U>
 constexpr size_t fused_lds_words() {
-    return syn::lds_words<U, kFusedThreads>() > kGatherWords ? syn::lds_words<U, kFusedThreads>() : kGatherWords;
+    constexpr size_t g = kGatherWords > kDecodeWords ? kGatherWords : kDecodeWords;
+    return syn::lds_words<U, kFusedThreads>() > g ? syn::lds_words<U, kFusedThreads>() : g;
 }
 
 // decode_verify_fused with the challenge syndromes r_q = Gy e_q computed in the
@@ -361,7 +422,7 @@ constexpr size_t fused_lds_words() {
 // syndrome workgroups have the lowest indices and are dispatched first, so the
 // waits end whatever the residency.  The last workgroup also resets rdone and
 // err; if a wait ran into its spin limit, every column is rejected.
-template <int U>
+template <int U, int E>
 __global__ __launch_bounds__(kFusedThreads) void decode_verify_syn(
     const uint32_t* __restrict__ PT, const uint32_t* __restrict__ Q, uint32_t m, uint32_t n, uint32_t Nx,
     uint32_t Ny, const uint32_t* __restrict__ Xhat, const uint32_t* __restrict__ Yhat, uint32_t B,
@@ -385,8 +446,9 @@ __global__ __launch_bounds__(kFusedThreads) void decode_verify_syn(
         verify_part<kFusedGroups>(Q, n, Ny, Xhat, B, ey_idx, ey_val, ty, ell, accL, nsub, bid - ell, part, u_s);
     else {
         const uint32_t d = bid - ell - nblkL;
-        decode_part<true, kFusedGroups>(PT, m, Nx, Yhat, B, ex_idx, ex_val, tx, rv, ell, Y, accR, nsub, d / nblkR,
-                                        d % nblkR, part, rdone, err);
+        decode_part<true, kFusedGroups, false, E>(PT, m, Nx, Yhat, B, ex_idx, ex_val, tx, rv, ell, Y, accR, nsub,
+                                                  d / nblkR, d % nblkR, reinterpret_cast<uint64_t*>(lds), rdone,
+                                                  err);
     }
     finish(B, ell, nsub, accL, accR, ctrl, slots, rdone, err, vL, vR, accept, &last);
 }
@@ -624,10 +686,10 @@ __global__ __launch_bounds__(kWideThreads) void decode_verify_wide(
     finish(B, ell, nsub, accL, accR, ctrl, slots, nullptr, nullptr, vL, vR, accept, &last);
 }
 
-template <int U>
+template <int U, int E>
 int fused_blocks_per_cu() {
     int nb = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, decode_verify_syn<U>, kFusedThreads, 0) != hipSuccess)
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, decode_verify_syn<U, E>, kFusedThreads, 0) != hipSuccess)
         return 0;
     return nb;
 }
@@ -665,30 +727,45 @@ DvLayout dv_layout(uint32_t m, uint32_t n, uint32_t B, uint32_t ell) {
 
 size_t dv_ctrl_bytes(uint32_t m, uint32_t n, uint32_t B, uint32_t ell) { return dv_layout(m, n, B, ell).bytes; }
 
+uint32_t dv_decode_cols(uint32_t m, uint32_t B, const void* PT, const void* Yhat, const void* Y, const void* r) {
+    // Four columns per lane take a quarter of the workgroups: only when those
+    // still fill the chip (measured: B = 1 at m = 4096 slows down from 24 to
+    // 28 us with four, 16 columns at m = 11008 speed up).
+    if (m % 4 != 0 || (uint64_t)B * ceil_div(m, kCols * 4) < 256) return 1u;
+    for (const void* p : {PT, Yhat, Y, r})
+        if ((uintptr_t)p & 15) return 1u;
+    return 4u;
+}
+
 uint32_t dv_syn_u(uint32_t Ny) {
     for (uint32_t U : {8u, 16u, 24u, 32u})
         if (Ny <= (uint32_t)kFusedThreads * U) return U;
     return 0;
 }
 
-bool dv_syn_fits(uint32_t m, uint32_t n, uint32_t Ny, uint32_t B, uint32_t ell) {
+bool dv_syn_fits(uint32_t m, uint32_t n, uint32_t Ny, uint32_t B, uint32_t ell, uint32_t E) {
     const uint32_t U = dv_syn_u(Ny);
-    if (U == 0 || ell == 0 || ell > (uint32_t)kMaxEll || Ny == 0) return false;
-    // residency of one workgroup per CU at least, per device and U (cached)
+    if (U == 0 || ell == 0 || ell > (uint32_t)kMaxEll || Ny == 0 || (E != 1 && E != 4)) return false;
+    // residency of one workgroup per CU at least, per device, U and E (cached)
     constexpr int kMaxDevices = 64;
-    static int cache[kMaxDevices][4];  // blocks per CU x CUs, plus one; 0 = not yet known
+    static int cache[kMaxDevices][4][2];  // blocks per CU x CUs, plus one; 0 = not yet known
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return false;
-    const int ui = (int)U / 8 - 1;
-    if (cache[dev][ui] == 0) {
+    const int ui = (int)U / 8 - 1, ei = E == 4 ? 1 : 0;
+    if (cache[dev][ui][ei] == 0) {
         int ncu = 0;
         if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return false;
-        const int nb = U == 8 ? fused_blocks_per_cu<8>() : U == 16 ? fused_blocks_per_cu<16>()
-                     : U == 24 ? fused_blocks_per_cu<24>() : fused_blocks_per_cu<32>();
-        cache[dev][ui] = nb * ncu + 1;
+        int nb = 0;
+        if (E == 4)
+            nb = U == 8 ? fused_blocks_per_cu<8, 4>() : U == 16 ? fused_blocks_per_cu<16, 4>()
+               : U == 24 ? fused_blocks_per_cu<24, 4>() : fused_blocks_per_cu<32, 4>();
+        else
+            nb = U == 8 ? fused_blocks_per_cu<8, 1>() : U == 16 ? fused_blocks_per_cu<16, 1>()
+               : U == 24 ? fused_blocks_per_cu<24, 1>() : fused_blocks_per_cu<32, 1>();
+        cache[dev][ui][ei] = nb * ncu + 1;
     }
-    const uint64_t grid = (uint64_t)ell + ceil_div(n, kCols) + (uint64_t)B * ceil_div(m, kCols);
-    return grid <= (uint64_t)(cache[dev][ui] - 1);
+    const uint64_t grid = (uint64_t)ell + ceil_div(n, kCols) + (uint64_t)B * ceil_div(m, kCols * E);
+    return grid <= (uint64_t)(cache[dev][ui][ei] - 1);
 }
 
 hipError_t launch_decode_verify_syn(const uint32_t* PT, const uint32_t* Q, uint32_t m, uint32_t n, uint32_t Nx,
@@ -700,19 +777,23 @@ hipError_t launch_decode_verify_syn(const uint32_t* PT, const uint32_t* Q, uint3
                                     uint32_t* vR, uint32_t* accept, hipStream_t s) {
     const uint32_t U = dv_syn_u(Ny);
     if (U == 0 || ell == 0 || ell > (uint32_t)kMaxEll || (uint64_t)cyr * m != Ny) return hipErrorInvalidValue;
-    const uint32_t nblkL = ceil_div(n, kCols), nblkR = ceil_div(m, kCols);
+    const uint32_t E = dv_decode_cols(m, B, PT, Yhat, Y, r);
+    const uint32_t nblkL = ceil_div(n, kCols), nblkR = ceil_div(m, kCols * E);
     const uint32_t grid = ell + nblkL + B * nblkR;
     const DvLayout l = dv_layout(m, n, B, ell);
     unsigned long long* acc = reinterpret_cast<unsigned long long*>(ctrl + l.acc_word);
     const uint32_t slots = count_slots(grid);
-#define MVK_DVS(UU)                                                                                               \
-    hipLaunchKernelGGL(decode_verify_syn<UU>, dim3(grid), dim3(kFusedThreads), 0, s, PT, Q, m, n, Nx, Ny, Xhat,   \
-                       Yhat, B, ex_idx, ex_val, tx, ey_idx, ey_val, ty, ell, cyr, pi1, pi2, v1, v2, r, Y, acc,     \
-                       acc + (size_t)ell * B * l.nsub, l.nsub, nblkR, nblkL, ctrl, slots, vL, vR, accept)
-    if (U == 8) MVK_DVS(8);
-    else if (U == 16) MVK_DVS(16);
-    else if (U == 24) MVK_DVS(24);
-    else MVK_DVS(32);
+#define MVK_DVS(UU, EE)                                                                                           \
+    hipLaunchKernelGGL((decode_verify_syn<UU, EE>), dim3(grid), dim3(kFusedThreads), 0, s, PT, Q, m, n, Nx, Ny,   \
+                       Xhat, Yhat, B, ex_idx, ex_val, tx, ey_idx, ey_val, ty, ell, cyr, pi1, pi2, v1, v2, r, Y,    \
+                       acc, acc + (size_t)ell * B * l.nsub, l.nsub, nblkR, nblkL, ctrl, slots, vL, vR, accept)
+#define MVK_DVS_E(UU) \
+    if (E == 4) MVK_DVS(UU, 4); else MVK_DVS(UU, 1)
+    if (U == 8) { MVK_DVS_E(8); }
+    else if (U == 16) { MVK_DVS_E(16); }
+    else if (U == 24) { MVK_DVS_E(24); }
+    else { MVK_DVS_E(32); }
+#undef MVK_DVS_E
 #undef MVK_DVS
     return hipGetLastError();
 }
@@ -723,13 +804,18 @@ hipError_t launch_decode_verify(const uint32_t* PT, const uint32_t* Q, uint32_t 
                                 const uint32_t* ey_val, uint32_t ty, uint32_t ell, const uint32_t* r, uint32_t* Y,
                                 uint32_t* ctrl, uint32_t* vL, uint32_t* vR, uint32_t* accept, hipStream_t s) {
     if (ell == 0 || ell > (uint32_t)kMaxEll) return hipErrorInvalidValue;
-    const uint32_t nblkL = ceil_div(n, kCols), nblkR = ceil_div(m, kCols);
+    const uint32_t E = dv_decode_cols(m, B, PT, Yhat, Y, r);
+    const uint32_t nblkL = ceil_div(n, kCols), nblkR = ceil_div(m, kCols * E);
     const uint32_t grid = B * nblkR + nblkL;
     const DvLayout l = dv_layout(m, n, B, ell);
     unsigned long long* acc = reinterpret_cast<unsigned long long*>(ctrl + l.acc_word);
-    hipLaunchKernelGGL(decode_verify_fused<false>, dim3(grid), dim3(kB), 0, s, PT, Q, m, n, Nx, Ny, Xhat, Yhat, B,
-                       ex_idx, ex_val, tx, ey_idx, ey_val, ty, ell, r, Y, acc, acc + (size_t)ell * B * l.nsub, l.nsub,
-                       nblkR, ctrl, count_slots(grid), vL, vR, accept, nullptr, nullptr);
+#define MVK_DVF(EE)                                                                                                \
+    hipLaunchKernelGGL((decode_verify_fused<false, EE>), dim3(grid), dim3(kB), 0, s, PT, Q, m, n, Nx, Ny, Xhat,    \
+                       Yhat, B, ex_idx, ex_val, tx, ey_idx, ey_val, ty, ell, r, Y, acc,                            \
+                       acc + (size_t)ell * B * l.nsub, l.nsub, nblkR, ctrl, count_slots(grid), vL, vR, accept,     \
+                       nullptr, nullptr)
+    if (E == 4) MVK_DVF(4); else MVK_DVF(1);
+#undef MVK_DVF
     return hipGetLastError();
 }
 
@@ -783,8 +869,8 @@ hipError_t launch_decode_verify_masked(uint32_t m, uint32_t n, const uint32_t* X
     }
     const uint32_t nblkL = ceil_div(n, kCols), nblkR = ceil_div(m, kCols);
     const uint32_t grid = B * nblkR + nblkL;
-    hipLaunchKernelGGL(decode_verify_fused<true>, dim3(grid), dim3(kB), 0, s, nullptr, nullptr, m, n, 0u, 0u, Xhat,
-                       Yhat, B, nullptr, nullptr, 0u, nullptr, nullptr, 0u, ell, r, Y, acc,
+    hipLaunchKernelGGL((decode_verify_fused<true, 1>), dim3(grid), dim3(kB), 0, s, nullptr, nullptr, m, n, 0u, 0u,
+                       Xhat, Yhat, B, nullptr, nullptr, 0u, nullptr, nullptr, 0u, ell, r, Y, acc,
                        acc + (size_t)ell * B * l.nsub, l.nsub, nblkR, ctrl, count_slots(grid), vL, vR, accept, My, U);
     return hipGetLastError();
 }

@@ -78,11 +78,15 @@ hipError_t launch_decode_verify(const uint32_t* PT, const uint32_t* Q, uint32_t 
 // (written to r, ell x m words) by 512-thread workgroups that hold a whole
 // block of Ny = cyr * m positions in LDS.  ctrl as above; its words 1 and 2
 // hold the syndrome completion count and the wait time-out flag.
+// dv_decode_cols: output columns per lane of the decode role these launches
+// pick (4 when m % 4 == 0, PT, Yhat, Y and r are 16-byte aligned and the
+// B * ceil(m / 256) decode workgroups fill the chip, else 1).
 // dv_syn_fits: the launch applies (Ny small enough, every workgroup resident
-// at once on the current device).
+// at once on the current device), for the decode width E = dv_decode_cols.
 constexpr uint32_t kDvSynThreads = 512;
 uint32_t dv_syn_u(uint32_t Ny);
-bool dv_syn_fits(uint32_t m, uint32_t n, uint32_t Ny, uint32_t B, uint32_t ell);
+uint32_t dv_decode_cols(uint32_t m, uint32_t B, const void* PT, const void* Yhat, const void* Y, const void* r);
+bool dv_syn_fits(uint32_t m, uint32_t n, uint32_t Ny, uint32_t B, uint32_t ell, uint32_t E);
 hipError_t launch_decode_verify_syn(const uint32_t* PT, const uint32_t* Q, uint32_t m, uint32_t n, uint32_t Nx,
                                     uint32_t Ny, const uint32_t* Xhat, const uint32_t* Yhat, uint32_t B,
                                     const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx,

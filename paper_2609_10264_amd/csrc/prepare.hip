@@ -315,9 +315,17 @@ uint32_t prep_u(uint64_t N) {
     return 0;
 }
 
-// Whether the gathers of client_prepare_kernel read 16 bytes per lane.
-bool prep_vec(const mvk_key& key) {
-    return key.m % 4 == 0 && key.n % 4 == 0 && ((uintptr_t)key.PT & 15) == 0 && ((uintptr_t)key.Q & 15) == 0;
+// Whether the gathers of client_prepare_kernel read 16 bytes per lane: when
+// the rows allow it and the 64-column items would need more than 256
+// workgroups (a quarter as many wider items then still keep the chip busy;
+// below, more and narrower items spread the gathers over more compute units:
+// at 4096 x 4096 with one column the wider items cost a microsecond per step).
+bool prep_vec(const mvk_key& key, uint32_t nx, uint32_t ny) {
+    if (key.m % 4 != 0 || key.n % 4 != 0 || ((uintptr_t)key.PT & 15) != 0 || ((uintptr_t)key.Q & 15) != 0)
+        return false;
+    const uint64_t items = (uint64_t)nx * ceil_div(key.m, gather_cols(false)) +
+                           (uint64_t)ny * ceil_div(key.n, gather_cols(false));
+    return items > 256u * kQuarters;
 }
 
 // Workgroups of client_prepare_kernel: one per syndrome short enough for one
@@ -325,7 +333,7 @@ bool prep_vec(const mvk_key& key) {
 uint64_t prep_grid(const mvk_key& key, uint32_t nx, uint32_t ny) {
     const uint64_t Nx = (uint64_t)key.cx.r * key.n, Ny = (uint64_t)key.cy.r * key.m;
     const uint32_t ux = nx ? prep_u(Nx) : 0u, uy = ny ? prep_u(Ny) : 0u;
-    const uint32_t cols = gather_cols(prep_vec(key));
+    const uint32_t cols = gather_cols(prep_vec(key, nx, ny));
     const uint64_t items = (uint64_t)nx * ceil_div(key.m, cols) + (uint64_t)ny * ceil_div(key.n, cols);
     return (ux ? nx : 0u) + (uy ? ny : 0u) + (items + kQuarters - 1) / kQuarters;
 }
@@ -364,7 +372,7 @@ hipError_t launch_client_prepare(const mvk_key& key, const uint32_t* ex_idx, con
     a.ypi1 = key.cy.pi1, a.ypi2 = key.cy.pi2, a.yv1 = key.cy.v1, a.yv2 = key.cy.v2;
     a.ex_idx = ex_idx, a.ex_val = ex_val, a.tx = tx, a.nx = nx;
     a.ey_idx = ey_idx, a.ey_val = ey_val, a.ty = ty, a.ny = ny;
-    const bool vec = prep_vec(key);
+    const bool vec = prep_vec(key, nx, ny);
     a.nbm = ceil_div(key.m, gather_cols(vec)), a.nbn = ceil_div(key.n, gather_cols(vec));
     a.PT = key.PT, a.Q = key.Q;
     a.Mx = Mx, a.My = My, a.R = R, a.Uq = Uq;
@@ -400,7 +408,9 @@ hipError_t launch_client_prepare(const mvk_key& key, const uint32_t* ex_idx, con
 hipError_t launch_gather_rows(const uint32_t* M, uint32_t ld, uint32_t nrows, const uint32_t* idx,
                               const uint32_t* val, uint32_t t, uint32_t count, uint32_t* out, hipStream_t s) {
     if (count == 0 || ld == 0) return hipSuccess;
-    const bool vec = ld % 4 == 0 && ((uintptr_t)M & 15) == 0;
+    // wider items as in client_prepare_kernel (prep_vec)
+    const bool vec = ld % 4 == 0 && ((uintptr_t)M & 15) == 0 &&
+                     (uint64_t)count * ceil_div(ld, gather_cols(false)) > 256u * kQuarters;
     const uint32_t nb = ceil_div(ld, gather_cols(vec));
     const uint64_t grid = ((uint64_t)count * nb + kQuarters - 1) / kQuarters;
     if (grid > 0x7fffffffu) return hipErrorInvalidValue;

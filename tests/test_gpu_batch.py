@@ -64,6 +64,19 @@ SHAPES = [  # cid, m, n, B, r, r2
 ]
 
 
+@pytest.mark.parametrize("N,n,B,ell", [(300, 4000, 4, 5), (200, 4096, 4, 5), (300, 1001, 3, 2)])
+def test_batch_project_widths(N, n, B, ell):
+    """The projection's row gathers with 16-byte loads (B*n a multiple of 4 and
+    more than 1024 64-column items: 256 columns per item, ragged at
+    B*n = 16000) and with 4-byte loads (few items, or B*n odd)."""
+    _say(f"batch project N={N} n={n} B={B} ell={ell}")
+    Qs = synth.field_uniform(900 + n, (B, N, n))
+    ei, ev = synth.sparse(901 + n, ell, N, 31)
+    QtT = dev(np.ascontiguousarray(np.concatenate(list(Qs), axis=1)))
+    Ut = mvk.batch_project(QtT, n, dev(ei), dev(ev))
+    assert np.array_equal(host(Ut), oracle.batch_project(Qs, ei, ev))
+
+
 @pytest.mark.parametrize("cid,m,n,B,r,r2", SHAPES)
 def test_batch_verification_matches_oracle(cid, m, n, B, r, r2):
     _say(f"batch verify cid={cid} m={m} n={n} B={B} r={r} r2={r2}")

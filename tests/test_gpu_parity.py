@@ -332,6 +332,37 @@ def test_decode_verify_syndrome_in_launch(m, ry, B, ell):
         assert np.array_equal(host(Y), oracle.decode(PT, resp, inst.exi, inst.exv))
 
 
+@pytest.mark.parametrize("m,ry,B,misalign", [(6000, 3, 48, False), (6000, 3, 48, True), (6001, 3, 48, False),
+                                             (6000, 3, 3, False), (1000, 4, 64, False), (1000, 4, 64, True),
+                                             (998, 4, 64, False)])
+def test_decode_widths(m, ry, B, misalign):
+    """The decode role with four output columns per lane (m a multiple of 4,
+    every row array 16-byte aligned and B * ceil(m/256) >= 256: 16-byte
+    gathers, ragged 256-column tail) and with one (m not a multiple of 4, Y 4
+    bytes past an alignment, or few columns), in the launch without
+    (Ny > 16384) and with the challenge syndromes."""
+    _say(f"decode widths m={m} ry={ry} B={B} misalign={misalign}")
+    ell = 2
+    inst = Instance(57, m, 96, B, 2, 9, ty=31, ell=ell, ry=ry).to_device()
+    mvk.keygen(inst.key, inst.dW)
+    PT, Q = oracle.keygen(inst.W, inst.cx, inst.cy)
+    dXh = mvk.encode(inst.key, inst.dX, inst.dexi, inst.dexv)
+    Xh = host(dXh)
+    Yh = oracle.server_eval(inst.W, Xh)
+    bad = Yh.copy()
+    bad[1, m - 1] = (int(bad[1, m - 1]) + 1) % P
+    for resp, want in ((Yh, [1] * B), (bad, [1, 0] + [1] * (B - 2))):
+        flat = torch.full((B * m + 4,), -1, dtype=torch.int32, device="cuda")
+        off = 1 if misalign else 0
+        Yout = flat[off: off + B * m].view(B, m)
+        Y, acc, _, _ = mvk.decode_verify(inst.key, dXh, dev(resp), inst.dexi, inst.dexv, inst.deyi, inst.deyv,
+                                         Y=Yout)
+        assert host(acc).tolist() == want
+        assert np.array_equal(host(Y), oracle.decode(PT, resp, inst.exi, inst.exv))
+        rest = flat.cpu().numpy()
+        assert (rest[:off] == -1).all() and (rest[off + B * m:] == -1).all()
+
+
 @pytest.mark.parametrize("ell,ty", [(1, 31), (3, 5), (5, 31), (16, 2)])
 def test_verify_repetition_counts(ell, ty):
     """Work-item split of the verify role for 1..16 repetitions (the maximum)."""

@@ -36,8 +36,9 @@ def _dense(N, idx, val):
 
 # cid, m, n, B, r_x, r_y, t_x, ell: block lengths in the one-launch range and
 # above it (Nx = 16500, Ny = 18000: the syndromes take their own launches),
-# several noise vectors and challenges, ragged column blocks of the 16-byte
-# gathers (m, n multiples of 4) and of the 4-byte ones (85: m, n odd).
+# several noise vectors and challenges, ragged column blocks of the 4-byte
+# gathers (64 columns per item: up to 1024 items, or m, n not multiples of 4)
+# and of the 16-byte ones (95, 96: 256 columns per item).
 PREP = [
     (80, 256, 256, 1, 2, 2, 8, 2),
     (81, 1000, 700, 3, 3, 2, 17, 3),
@@ -45,6 +46,8 @@ PREP = [
     (83, 300, 5500, 2, 3, 3, 64, 2),
     (84, 6000, 200, 1, 1, 3, 5, 16),
     (85, 1001, 703, 3, 3, 2, 17, 3),
+    (95, 1000, 300, 70, 2, 2, 9, 2),
+    (96, 2048, 1000, 40, 2, 2, 9, 3),
 ]
 
 
@@ -73,7 +76,7 @@ def test_client_prepare_matches_oracle(cid, m, n, B, rx, ry, tx, ell):
 # per thread and 4 / ell columns per workgroup, or at 256 workgroups and more
 # four elements and 16 / ell columns; ragged column groups and element blocks,
 # n > m) and the general kernel (ell = 7)
-MASKED = PREP[:2] + PREP[3:4] + [(86, 3000, 2000, 8, 2, 2, 16, 3), (87, 500, 400, 2, 2, 2, 9, 7),
+MASKED = PREP[:2] + PREP[3:4] + PREP[6:] + [(86, 3000, 2000, 8, 2, 2, 16, 3), (87, 500, 400, 2, 2, 2, 9, 7),
                                  (88, 12000, 300, 2, 2, 2, 9, 2), (90, 4096, 1000, 20, 2, 2, 16, 2),
                                  (91, 700, 5000, 13, 2, 2, 9, 4), (92, 1500, 1500, 9, 2, 2, 9, 1),
                                  (93, 16384, 100, 128, 2, 2, 5, 2), (94, 16000, 90, 64, 2, 2, 5, 3)]

@@ -792,17 +792,23 @@ __global__ __launch_bounds__(512) void server_eval_mfma_dstat(const int8_t* __re
             }
         }
     };
+    // (a chunk is loaded only if it holds a block of the range: no loads past
+    // the end that nothing uses)
     for (uint32_t j0 = 0; j0 < nk; j0 += 2 * C) {
+        if (j0 + C < nk) {
 #pragma unroll
-        for (int c = 0; c < C; ++c)
+            for (int c = 0; c < C; ++c)
 #pragma unroll
-            for (int t = 0; t < TWW; ++t) wb[c][t] = load_w(j0 + C + c, t);
+                for (int t = 0; t < TWW; ++t) wb[c][t] = load_w(j0 + C + c, t);
+        }
         compute(j0, wa);
         if (j0 + C >= nk) break;
+        if (j0 + 2 * C < nk) {
 #pragma unroll
-        for (int c = 0; c < C; ++c)
+            for (int c = 0; c < C; ++c)
 #pragma unroll
-            for (int t = 0; t < TWW; ++t) wa[c][t] = load_w(j0 + 2 * C + c, t);
+                for (int t = 0; t < TWW; ++t) wa[c][t] = load_w(j0 + 2 * C + c, t);
+        }
         compute(j0 + C, wb);
     }
     __syncthreads();  // every wave is past its last digit-tile read
@@ -921,17 +927,28 @@ struct GroupPlan {
     uint32_t tww;   // W tiles per wave (digits-stationary kernel)
     uint32_t rows;  // rows per workgroup
     uint32_t ks;    // k-ranges
+    uint32_t kbm;   // k-blocks of digit tiles the LDS holds (digits-stationary kernel)
 };
 
 constexpr uint32_t kDstatKbm4 = 32, kDstatKbm2 = 64;  // k-blocks of digit tiles in 128 KiB of LDS
 
+// LDS of the digits-stationary kernel sized to the k-range: the next power of
+// two of its k-blocks, at least 8.  (A 16-query launch at 4096 x 4096 with four
+// ranges of 16 k-blocks: 9.9 us with 64 KiB of LDS against 11.8 us with 128 KiB.)
+uint32_t dstat_kbm(uint32_t kb_per) {
+    uint32_t k = 8;
+    while (k < kb_per) k *= 2;
+    return k;
+}
+
 GroupPlan group_plan(uint32_t m, uint32_t n, uint32_t nb) {
     const uint32_t qt = group_qt(nb), nkb = ceil_div(n, 64);
-    GroupPlan g{false, qt, 0, stream_rows(qt), stream_ksplit(m, n, qt)};
+    GroupPlan g{false, qt, 0, stream_rows(qt), stream_ksplit(m, n, qt), 0};
     if (qt > 4) return g;
     // digits-stationary: rows 128*tww, each k-range's digit tiles fit in LDS;
     // estimated time ceil(workgroups / 256) * (W k-blocks per workgroup in units
-    // of 128 rows + fill + exchange of the split values)
+    // of 128 rows + fill + exchange of the split values, which the last
+    // workgroup of a row block reads from the ks - 1 others)
     const uint32_t kbm = qt == 4 ? kDstatKbm4 : kDstatKbm2;
     uint32_t best = 0xffffffffu;
     for (uint32_t tww = 1; tww <= 2; ++tww)
@@ -939,10 +956,10 @@ GroupPlan group_plan(uint32_t m, uint32_t n, uint32_t nb) {
             const uint32_t kb_per = ceil_div(nkb, ks);
             if (kb_per > kbm) continue;
             const uint32_t rows = 128 * tww, nwg = ceil_div(m, rows) * ks;
-            const uint32_t cost = ceil_div(nwg, 256) * (kb_per * tww + 6 + (ks > 1 ? qt : 0u));
+            const uint32_t cost = ceil_div(nwg, 256) * (kb_per * tww + 6 + qt * (ks - 1));
             if (cost < best) {
                 best = cost;
-                g = GroupPlan{true, qt, tww, rows, ks};
+                g = GroupPlan{true, qt, tww, rows, ks, dstat_kbm(kb_per)};
             }
         }
     return g;
@@ -951,7 +968,28 @@ GroupPlan group_plan(uint32_t m, uint32_t n, uint32_t nb) {
 template <int QT, int TWW, int KBM, int C>
 hipError_t launch_dstat_cfg(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t nkb, uint32_t B,
                             uint32_t* Y, uint32_t ksplit, uint32_t* part, uint32_t* counters, bool packed,
+                            hipStream_t s);
+
+// launch_dstat_cfg for the plan's LDS size (kbm a power of two in [8, KBM max])
+template <int QT, int TWW>
+hipError_t launch_dstat_kbm(uint32_t kbm, const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t nkb,
+                            uint32_t B, uint32_t* Y, uint32_t ksplit, uint32_t* part, uint32_t* counters,
+                            bool packed, hipStream_t s) {
+    constexpr uint32_t kMax = QT == 4 ? kDstatKbm4 : kDstatKbm2;
+    if (kbm == 8) return launch_dstat_cfg<QT, TWW, 8, 8>(W, m, n, X, nkb, B, Y, ksplit, part, counters, packed, s);
+    if (kbm == 16) return launch_dstat_cfg<QT, TWW, 16, 8>(W, m, n, X, nkb, B, Y, ksplit, part, counters, packed, s);
+    if (kbm == 32) return launch_dstat_cfg<QT, TWW, 32, 8>(W, m, n, X, nkb, B, Y, ksplit, part, counters, packed, s);
+    if constexpr (kMax >= 64)
+        if (kbm == 64)
+            return launch_dstat_cfg<QT, TWW, 64, 8>(W, m, n, X, nkb, B, Y, ksplit, part, counters, packed, s);
+    return hipErrorInvalidValue;
+}
+
+template <int QT, int TWW, int KBM, int C>
+hipError_t launch_dstat_cfg(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t nkb, uint32_t B,
+                            uint32_t* Y, uint32_t ksplit, uint32_t* part, uint32_t* counters, bool packed,
                             hipStream_t s) {
+    if (ksplit == 0 || ceil_div(nkb, ksplit) > (uint32_t)KBM) return hipErrorInvalidValue;  // LDS holds the range
     const uint32_t nrb = ceil_div(m, 128 * TWW), per_group = 8 / ksplit;
     const dim3 grid(ceil_div(nrb, per_group) * 8);
     if (packed)
@@ -1030,15 +1068,15 @@ hipError_t launch_server_eval(const int8_t* W, uint32_t m, uint32_t n, const uin
         hipError_t e = hipSuccess;
         if (g.dstat) {
             if (g.qt == 4)
-                e = g.tww == 1 ? launch_dstat_cfg<4, 1, kDstatKbm4, 8>(W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
-                                                                        packed, s)
-                               : launch_dstat_cfg<4, 2, kDstatKbm4, 8>(W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
-                                                                        packed, s);
+                e = g.tww == 1 ? launch_dstat_kbm<4, 1>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
+                                                        packed, s)
+                               : launch_dstat_kbm<4, 2>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
+                                                        packed, s);
             else
-                e = g.tww == 1 ? launch_dstat_cfg<2, 1, kDstatKbm2, 8>(W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
-                                                                        packed, s)
-                               : launch_dstat_cfg<2, 2, kDstatKbm2, 8>(W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
-                                                                        packed, s);
+                e = g.tww == 1 ? launch_dstat_kbm<2, 1>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
+                                                        packed, s)
+                               : launch_dstat_kbm<2, 2>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
+                                                        packed, s);
             if (e != hipSuccess) return e;
             continue;
         }

@@ -1,18 +1,20 @@
 // Streaming read of a device buffer: the HBM read floor that server_eval's
 // W stream is compared against (same bytes, nothing computed but an XOR
 // checksum).  Every thread issues all of a pass's 16-byte loads before
-// combining them; each workgroup writes the XOR of everything it read to its
-// own sink word, and workgroup 0 clears the words of workgroups the launch
-// does not have.  Shape by size (measured on MI355X): up to 64 MiB one pass
+// combining them; the loads are non-temporal, as server_eval's W loads.  Each
+// workgroup writes the XOR of everything it read to its own sink word, and
+// workgroup 0 clears the words of workgroups the launch does not have.  Shape
+// by size (measured on MI355X, back-to-back launches): up to 64 MiB one pass
 // of 4 loads per thread over as many workgroups as that takes (16.8 MB:
-// 4.4 us); above, 256 workgroups looping with 8 loads per thread (268 MB:
-// 42.6 us, 6.3 TB/s).
+// 4.6 us); above, 256 workgroups looping with 8 loads per thread (268 MB:
+// 39.7 us, 6.8 TB/s; 4.9 and 42.6 us with ordinary loads).
 #include "mvk_internal.h"
 
 namespace mvk {
 
 namespace {
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kReadThreads = 256;
 
 template <int kReadPer>
@@ -24,11 +26,12 @@ __global__ __launch_bounds__(kReadThreads) void stream_read_kernel(const uint4* 
     const size_t g = (size_t)blockIdx.x * kReadThreads + threadIdx.x;
     uint32_t x = 0;
     for (size_t base = 0; base < n16; base += stride * kReadPer) {
-        uint4 v[kReadPer];
+        u32x4 v[kReadPer];
 #pragma unroll
         for (int u = 0; u < kReadPer; ++u) {
             const size_t i = base + g + stride * u;
-            v[u] = i < n16 ? p[i] : make_uint4(0u, 0u, 0u, 0u);
+            // non-temporal, as server_eval reads W
+            v[u] = i < n16 ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p) + i) : u32x4{0u, 0u, 0u, 0u};
         }
 #pragma unroll
         for (int u = 0; u < kReadPer; ++u) x ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;

@@ -64,11 +64,13 @@ constexpr int kPreQ = 4;
 constexpr int kPreB = 4;
 constexpr int kItems = kMaxEll;  // verify work items (repetition, chunk) per workgroup, at most
 
-// E consecutive words at p (E = 4: one 16-byte access; p 16-byte aligned).
+// E consecutive words at p (E = 4: one 16-byte non-temporal access, p 16-byte
+// aligned; the rows these loads stream are read once per launch).
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 template <int E>
 __device__ __forceinline__ void load_cols(const uint32_t* p, uint32_t (&v)[E]) {
     if constexpr (E == 4) {
-        const uint4 t = *reinterpret_cast<const uint4*>(p);
+        const u32x4 t = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
         v[0] = t.x;
         v[1] = t.y;
         v[2] = t.z;

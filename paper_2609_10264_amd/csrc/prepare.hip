@@ -24,6 +24,7 @@ constexpr int kPrepThreads = 1024;     // syndrome workgroups hold a block of up
 constexpr int kQuarter = 256;          // gather items per workgroup: kPrepThreads / kQuarter
 constexpr int kQuarters = kPrepThreads / kQuarter;
 constexpr int kQGroups = kQuarter / 64;  // waves per item, each a share of the sparse terms
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kQBatch = 16;            // gathers in flight per thread
 
 // Columns per gather item: one per lane, or with VEC four consecutive ones per
@@ -71,7 +72,8 @@ __device__ __forceinline__ void gather_item(const uint32_t* __restrict__ M, uint
             ww[u] = ok ? val[sl] : 0u;
             const uint32_t* src = M + (size_t)j * ld + is;
             if constexpr (VEC) {
-                const uint4 v = *reinterpret_cast<const uint4*>(src);
+                // non-temporal: every row segment is read once per launch
+                const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src));
                 mv[u][0] = v.x;
                 mv[u][1] = v.y;
                 mv[u][2] = v.z;

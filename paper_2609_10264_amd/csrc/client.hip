@@ -64,8 +64,8 @@ constexpr int kPreQ = 4;
 constexpr int kPreB = 4;
 constexpr int kItems = kMaxEll;  // verify work items (repetition, chunk) per workgroup, at most
 
-// E consecutive words at p (E = 4: one 16-byte non-temporal access, p 16-byte
-// aligned; the rows these loads stream are read once per launch).
+// E consecutive words at p, non-temporal (the rows these loads stream are read
+// once per launch; E = 4: one 16-byte access, p 16-byte aligned).
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 template <int E>
 __device__ __forceinline__ void load_cols(const uint32_t* p, uint32_t (&v)[E]) {
@@ -76,7 +76,7 @@ __device__ __forceinline__ void load_cols(const uint32_t* p, uint32_t (&v)[E]) {
         v[2] = t.z;
         v[3] = t.w;
     } else {
-        v[0] = *p;
+        v[0] = __builtin_nontemporal_load(p);
     }
 }
 template <int E>

@@ -71,15 +71,15 @@ __device__ __forceinline__ void gather_item(const uint32_t* __restrict__ M, uint
             j = j < nrows ? j : nrows - 1;
             ww[u] = ok ? val[sl] : 0u;
             const uint32_t* src = M + (size_t)j * ld + is;
+            // non-temporal: every row segment is read once per launch
             if constexpr (VEC) {
-                // non-temporal: every row segment is read once per launch
                 const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src));
                 mv[u][0] = v.x;
                 mv[u][1] = v.y;
                 mv[u][2] = v.z;
                 mv[u][3] = v.w;
             } else {
-                mv[u][0] = *src;
+                mv[u][0] = __builtin_nontemporal_load(src);
             }
         }
 #pragma unroll

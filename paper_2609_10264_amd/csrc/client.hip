@@ -287,7 +287,7 @@ __device__ __forceinline__ void verify_part(const uint32_t* __restrict__ Q, uint
                 uint32_t j = ei[sl];
                 j = j < Ny ? j : Ny - 1;
                 ww[u] = ok ? ev[sl] : 0u;
-                qv[u] = Q[(size_t)j * n + ks];
+                qv[u] = __builtin_nontemporal_load(&Q[(size_t)j * n + ks]);  // rows read once per launch
             }
 #pragma unroll
             for (int u = 0; u < kBatch; ++u) acc += ffold((uint64_t)ww[u] * qv[u]);

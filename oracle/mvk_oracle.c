@@ -50,14 +50,39 @@
 
 /* Count of field operations (additions, subtractions, multiplications) since
  * the last orc_ops_reset: lets a test compare the RAA maps' cost with the
- * bounds App. B states (at most 4N for an encoding, 5N for a syndrome). */
+ * bounds App. B states (at most 4N for an encoding, 5N for a syndrome).
+ * Only the counting build (-DORC_COUNT_OPS, single-threaded use) counts; in
+ * the other builds the functions below are re-entrant and the library may be
+ * called from several threads at once (each call on its own outputs). */
+#ifdef ORC_COUNT_OPS
 static uint64_t g_ops;
-void orc_ops_reset(void) { g_ops = 0; }
-uint64_t orc_ops_count(void) { return g_ops; }
+#define ORC_COUNT() (++g_ops)
+#else
+#define ORC_COUNT() ((void)0)
+#endif
+void orc_ops_reset(void) {
+#ifdef ORC_COUNT_OPS
+    g_ops = 0;
+#endif
+}
+uint64_t orc_ops_count(void) {
+#ifdef ORC_COUNT_OPS
+    return g_ops;
+#else
+    return 0;
+#endif
+}
+int orc_counts_ops(void) {
+#ifdef ORC_COUNT_OPS
+    return 1;
+#else
+    return 0;
+#endif
+}
 
-static uint64_t fadd(uint64_t a, uint64_t b) { ++g_ops; return (a + b) % ORC_P; }
-static uint64_t fsub(uint64_t a, uint64_t b) { ++g_ops; return (a + ORC_P - b) % ORC_P; }
-static uint64_t fmul(uint64_t a, uint64_t b) { ++g_ops; return (a * b) % ORC_P; }
+static uint64_t fadd(uint64_t a, uint64_t b) { ORC_COUNT(); return (a + b) % ORC_P; }
+static uint64_t fsub(uint64_t a, uint64_t b) { ORC_COUNT(); return (a + ORC_P - b) % ORC_P; }
+static uint64_t fmul(uint64_t a, uint64_t b) { ORC_COUNT(); return (a * b) % ORC_P; }
 
 /* Embedding of a signed integer into F_p. */
 static uint64_t emb(int64_t w) {
@@ -159,35 +184,48 @@ void orc_server_eval(const int8_t *W, uint32_t m, uint32_t n, const uint32_t *Xh
  * P^T = Gx^T W^T is m encodings of the rows of W; Q is n encodings of the
  * columns of W (Sec. 6.3, "Preprocessing time").
  * PT is stored Nx x m row-major (PT[j*m + i] = P[i][j]); Q is Ny x n row-major.
- * Either output pointer may be NULL to skip it.
+ *
+ * orc_keygen_PT_rows: the columns i in [i0, i1) of PT (encodings of rows i of W).
+ * orc_keygen_Q_cols:  the columns k in [k0, k1) of Q (encodings of columns k of W).
+ * Ranges that do not overlap write disjoint entries, so they may run at once.
  */
+void orc_keygen_PT_rows(const int8_t *W, uint32_t m, uint32_t n, uint32_t rx, const uint32_t *xpi1,
+                        const uint32_t *xpi2, const uint32_t *xv1, const uint32_t *xv2, uint32_t *PT,
+                        uint32_t i0, uint32_t i1) {
+    uint64_t Nx = (uint64_t)rx * n;
+    uint32_t *row = (uint32_t *)malloc((uint64_t)n * sizeof(uint32_t));
+    uint32_t *enc = (uint32_t *)malloc(Nx * sizeof(uint32_t));
+    for (uint32_t i = i0; i < i1 && i < m; i++) {
+        for (uint32_t k = 0; k < n; k++) row[k] = (uint32_t)emb(W[(uint64_t)i * n + k]);
+        orc_encT(n, rx, xpi1, xpi2, xv1, xv2, row, enc);
+        for (uint64_t j = 0; j < Nx; j++) PT[j * m + i] = enc[j];
+    }
+    free(row);
+    free(enc);
+}
+
+void orc_keygen_Q_cols(const int8_t *W, uint32_t m, uint32_t n, uint32_t ry, const uint32_t *ypi1,
+                       const uint32_t *ypi2, const uint32_t *yv1, const uint32_t *yv2, uint32_t *Q,
+                       uint32_t k0, uint32_t k1) {
+    uint64_t Ny = (uint64_t)ry * m;
+    uint32_t *col = (uint32_t *)malloc((uint64_t)m * sizeof(uint32_t));
+    uint32_t *enc = (uint32_t *)malloc(Ny * sizeof(uint32_t));
+    for (uint32_t k = k0; k < k1 && k < n; k++) {
+        for (uint32_t i = 0; i < m; i++) col[i] = (uint32_t)emb(W[(uint64_t)i * n + k]);
+        orc_encT(m, ry, ypi1, ypi2, yv1, yv2, col, enc);
+        for (uint64_t j = 0; j < Ny; j++) Q[j * n + k] = enc[j];
+    }
+    free(col);
+    free(enc);
+}
+
+/* Both outputs at once; either pointer may be NULL to skip it. */
 void orc_keygen(const int8_t *W, uint32_t m, uint32_t n,
                 uint32_t rx, const uint32_t *xpi1, const uint32_t *xpi2, const uint32_t *xv1, const uint32_t *xv2,
                 uint32_t ry, const uint32_t *ypi1, const uint32_t *ypi2, const uint32_t *yv1, const uint32_t *yv2,
                 uint32_t *PT, uint32_t *Q) {
-    uint64_t Nx = (uint64_t)rx * n, Ny = (uint64_t)ry * m;
-    if (PT) {
-        uint32_t *row = (uint32_t *)malloc((uint64_t)n * sizeof(uint32_t));
-        uint32_t *enc = (uint32_t *)malloc(Nx * sizeof(uint32_t));
-        for (uint32_t i = 0; i < m; i++) {
-            for (uint32_t k = 0; k < n; k++) row[k] = (uint32_t)emb(W[(uint64_t)i * n + k]);
-            orc_encT(n, rx, xpi1, xpi2, xv1, xv2, row, enc);
-            for (uint64_t j = 0; j < Nx; j++) PT[j * m + i] = enc[j];
-        }
-        free(row);
-        free(enc);
-    }
-    if (Q) {
-        uint32_t *col = (uint32_t *)malloc((uint64_t)m * sizeof(uint32_t));
-        uint32_t *enc = (uint32_t *)malloc(Ny * sizeof(uint32_t));
-        for (uint32_t k = 0; k < n; k++) {
-            for (uint32_t i = 0; i < m; i++) col[i] = (uint32_t)emb(W[(uint64_t)i * n + k]);
-            orc_encT(m, ry, ypi1, ypi2, yv1, yv2, col, enc);
-            for (uint64_t j = 0; j < Ny; j++) Q[j * n + k] = enc[j];
-        }
-        free(col);
-        free(enc);
-    }
+    if (PT) orc_keygen_PT_rows(W, m, n, rx, xpi1, xpi2, xv1, xv2, PT, 0, m);
+    if (Q) orc_keygen_Q_cols(W, m, n, ry, ypi1, ypi2, yv1, yv2, Q, 0, n);
 }
 
 /*
@@ -374,4 +412,118 @@ void orc_batch_verify(uint32_t m, uint32_t n, uint32_t B, uint32_t r, const uint
     free(z);
     free(e2);
     free(rj);
+}
+
+/*
+ * Seeded sampling of the method's random draws: the codes of Preprocess
+ * (App. B: two uniform permutations and two diagonals over F_p^*), the noise
+ * e_x <- E_{tx}^{Nx} of Encrypt and the challenges e <- E_{ty}^{Ny} of Verify
+ * (Sec. 3: exactly t nonzero entries; Lemma 5.1 draws the support uniformly
+ * and the values uniformly in F_p^*).  The paper does not fix a generator;
+ * this is a written specification, followed independently by the library:
+ *
+ *   mix(z)    = SplitMix64's output function (Steele, Lea and Flood, 2014):
+ *               z ^= z >> 30; z *= 0xBF58476D1CE4E5B9; z ^= z >> 27;
+ *               z *= 0x94D049BB133111EB; z ^= z >> 31
+ *   stream    : a 64-bit state s; each draw is s += 0x9E3779B97F4A7C15, then mix(s)
+ *   stream (seed, tag, c) starts at s = mix(seed ^ tag ^ mix(c))
+ *   below(b)  : draw z until z < 2^64 - (2^64 mod b) (no rejection when
+ *               2^64 mod b = 0); return z mod b.  At most 64 draws: if all
+ *               are rejected, the last one's z mod b
+ *   nonzero   : draw z until 1 <= (z >> 33) <= p - 1; return z >> 33.  At
+ *               most 64 draws: if none is accepted, the value 1
+ *   permutation of [0, N): the identity, then for i = N-1 down to 1:
+ *               j = below(i + 1), swap entries i and j (Fisher-Yates)
+ *   code (k, r) from (seed, tag): stream c = 0; pi1 = permutation, then
+ *               pi2 = permutation, then N nonzero values v1, then N values v2
+ *   sparse vector c of E_t^N from (seed, tag): stream c; positions
+ *               j = below(N), skipping a j already taken, until t are taken
+ *               (kept in draw order), at most 2^24 of them per vector (then
+ *               the smallest positions not taken, in increasing order, fill
+ *               the rest); then t nonzero values
+ * The caps only make every loop finite: with t <= N the chance of reaching
+ * any of them is below 2^-100 for every size this library accepts.
+ */
+static uint64_t sm_mix(uint64_t z) {
+    z ^= z >> 30;
+    z *= 0xBF58476D1CE4E5B9ULL;
+    z ^= z >> 27;
+    z *= 0x94D049BB133111EBULL;
+    z ^= z >> 31;
+    return z;
+}
+
+static uint64_t sm_draw(uint64_t *s) {
+    *s += 0x9E3779B97F4A7C15ULL;
+    return sm_mix(*s);
+}
+
+static uint64_t sm_start(uint64_t seed, uint64_t tag, uint64_t c) { return sm_mix(seed ^ tag ^ sm_mix(c)); }
+
+static uint64_t sm_below(uint64_t *s, uint64_t b) {
+    uint64_t rem = (0 - b) % b; /* 2^64 mod b */
+    uint64_t z = 0;
+    for (int d = 0; d < 64; d++) {
+        z = sm_draw(s);
+        if (rem == 0 || z < 0 - rem) return z % b;
+    }
+    return z % b;
+}
+
+static uint32_t sm_nonzero(uint64_t *s) {
+    for (int d = 0; d < 64; d++) {
+        uint64_t v = sm_draw(s) >> 33;
+        if (v >= 1 && v <= ORC_P - 1) return (uint32_t)v;
+    }
+    return 1;
+}
+
+/* The raw stream from a given state (for the generator's published test values). */
+void orc_sm64_draws(uint64_t state, uint32_t count, uint64_t *out) {
+    for (uint32_t i = 0; i < count; i++) out[i] = sm_draw(&state);
+}
+
+static void sm_permutation(uint64_t *s, uint64_t N, uint32_t *a) {
+    for (uint64_t j = 0; j < N; j++) a[j] = (uint32_t)j;
+    for (uint64_t i = N - 1; i >= 1 && i < N; i--) {
+        uint64_t j = sm_below(s, i + 1);
+        uint32_t t = a[i];
+        a[i] = a[j];
+        a[j] = t;
+    }
+}
+
+/* A random RAA code of dimension k and rate 1/r: arrays of N = k*r words. */
+void orc_sample_code(uint32_t k, uint32_t r, uint64_t seed, uint64_t tag, uint32_t *pi1, uint32_t *pi2,
+                     uint32_t *v1, uint32_t *v2) {
+    uint64_t N = (uint64_t)k * r;
+    uint64_t s = sm_start(seed, tag, 0);
+    sm_permutation(&s, N, pi1);
+    sm_permutation(&s, N, pi2);
+    for (uint64_t j = 0; j < N; j++) v1[j] = sm_nonzero(&s);
+    for (uint64_t j = 0; j < N; j++) v2[j] = sm_nonzero(&s);
+}
+
+/* `count` draws from E_t^N (t <= N): idx, val are count x t. */
+void orc_sample_sparse(uint32_t count, uint32_t N, uint32_t t, uint64_t seed, uint64_t tag, uint32_t *idx,
+                       uint32_t *val) {
+    for (uint32_t c = 0; c < count; c++) {
+        uint64_t s = sm_start(seed, tag, c);
+        uint32_t *ic = idx + (uint64_t)c * t;
+        uint32_t got = 0;
+        for (uint64_t d = 0; got < t && d < (1ULL << 24); d++) {
+            uint32_t j = (uint32_t)sm_below(&s, N);
+            int taken = 0;
+            for (uint32_t q = 0; q < got; q++)
+                if (ic[q] == j) taken = 1;
+            if (!taken) ic[got++] = j;
+        }
+        for (uint32_t j = 0; got < t && j < N; j++) {
+            int taken = 0;
+            for (uint32_t q = 0; q < got; q++)
+                if (ic[q] == j) taken = 1;
+            if (!taken) ic[got++] = j;
+        }
+        for (uint32_t q = 0; q < t; q++) val[(uint64_t)c * t + q] = sm_nonzero(&s);
+    }
 }

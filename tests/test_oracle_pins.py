@@ -160,10 +160,12 @@ def test_raa_cost_within_the_bounds_of_app_b(k, r, p):
     N = k * r
     w = o.field_uniform(1, k)
     v = o.field_uniform(2, N)
-    enc_ops = oracle.field_ops(lambda: o.encT(code, w), p=p)
-    syn_ops = oracle.field_ops(lambda: o.syn(code, v), p=p)
+    enc_ops = oracle.field_ops("encT", code, w, p=p)
+    syn_ops = oracle.field_ops("syn", code, v, p=p)
     assert 0 < enc_ops <= 4 * N
     assert 0 < syn_ops <= 5 * N
+    # the counting build computes the same values as the build the tests use
+    assert np.array_equal(oracle.encT(code, w, p=p, _count=True), o.encT(code, w))
 
 
 def test_masks_look_uniform(p):

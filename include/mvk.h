@@ -33,10 +33,13 @@
  *    enqueued) if one is not; a debugging mode, not for graph capture.
  *  - The library keeps a per-(device, stream) workspace that grows on demand
  *    (hipMalloc at first use and when a larger size is needed); calls enqueued
- *    on two different streams never share workspace memory.  Calls on one
- *    stream from several host threads at once are not supported (a call that
- *    grows the workspace frees the old buffer): give each thread its own
- *    stream.
+ *    on two different streams never share workspace memory.  A buffer that a
+ *    growth replaces is retired, not freed, so HIP graphs captured earlier on
+ *    the stream (which hold its address) stay valid; mvk_workspace_release
+ *    frees the retired buffers.  A call whose stream is capturing a graph and
+ *    that would need a larger workspace returns MVK_ECAPTURE (run it once
+ *    outside the capture first).  Calls on one stream from several host
+ *    threads at once are not supported: give each thread its own stream.
  */
 #ifndef MVK_H_
 #define MVK_H_
@@ -50,7 +53,7 @@ extern "C" {
 
 #define MVK_PRIME 2147483647u
 #define MVK_PRIME_BABYBEAR 2013265921u
-#define MVK_ABI_VERSION 5
+#define MVK_ABI_VERSION 6
 
 typedef int32_t mvk_status;
 #define MVK_OK 0
@@ -58,6 +61,8 @@ typedef int32_t mvk_status;
 #define MVK_ERANGE (-2) /* a size beyond the exactness limit of a kernel, or (MVK_VALIDATE) a field input >= p */
 #define MVK_ENOMEM (-3) /* workspace allocation failed */
 #define MVK_EHIP (-4)   /* a HIP runtime call or kernel launch failed */
+#define MVK_ERANDOM (-5)   /* the operating system's random source failed (MVK_SEED_FRESH) */
+#define MVK_ECAPTURE (-6)  /* the workspace would have to grow while the stream captures a graph */
 
 /* Largest column count n of W for which server_eval's int8-limb accumulation
  * is exact: n * 128 * 128 < 2^31. */
@@ -392,6 +397,123 @@ mvk_status mvk_raa_syndrome(const mvk_code *code, const uint32_t *v, uint32_t co
  */
 #define MVK_STREAM_READ_BLOCKS 4096u
 mvk_status mvk_stream_read(const void *data, size_t bytes, uint32_t *sink, void *stream);
+
+/*
+ * Frees the workspace buffers that growths have retired (see the conventions
+ * above), after waiting for the device.  Call it only when no HIP graph
+ * captured before those growths will be replayed again.
+ */
+mvk_status mvk_workspace_release(void);
+
+/* ---------------------------------------------------------------------------
+ * Seeded calls: the library draws the method's randomness.
+ *
+ * Protocol pvMVMD (Sec. 6.1) samples the two RAA codes in Preprocess (App. B:
+ * uniform permutations pi1, pi2 of [0, N) and diagonals v1, v2 with entries
+ * uniform in F_p^*), fresh noise e_x <- E_{tx}^{Nx} for every query column in
+ * Encrypt, and the challenges e <- E_{ty}^{Ny} in Verify once the responses
+ * are fixed (E_t^N: exactly t nonzero entries, Sec. 3; Lemma 5.1 draws the
+ * support uniformly and the values uniformly in F_p^*).  The calls below draw
+ * them from 64-bit seeds; the same seed reproduces the same draws.  The paper
+ * does not fix a generator; the library follows this specification:
+ *   - SplitMix64 (Steele, Lea and Flood, 2014): the state advances by
+ *     0x9E3779B97F4A7C15 and each output is the state passed through the
+ *     finaliser z ^= z>>30; z *= 0xBF58476D1CE4E5B9; z ^= z>>27;
+ *     z *= 0x94D049BB133111EB; z ^= z>>31.
+ *   - Stream c of (seed, tag) starts from finaliser(seed ^ tag ^ finaliser(c)).
+ *   - An integer below b: outputs z >= 2^64 - (2^64 mod b) are rejected, the
+ *     value is z mod b (after 64 rejections, the last z mod b).  A value in
+ *     F_p^*: the top 31 bits of an output, rejected unless in [1, p-1] (after
+ *     64 rejections, 1).
+ *   - A code (k, r): stream 0; pi1, then pi2 by Fisher-Yates (from the
+ *     identity, for i = N-1 down to 1 swap entries i and below(i+1)), then the
+ *     N values of v1, then those of v2.
+ *   - Sparse vector c of E_t^N: stream c; positions below(N), repeats skipped,
+ *     until t are held, in draw order (after 2^24 draws the smallest free
+ *     positions complete it); then its t values in F_p^*.
+ * Tags (ASCII, big-endian) separate the purposes of one seed.
+ */
+#define MVK_TAG_CODE_X 0x6D766B2D636F6478ull    /* "mvk-codx": the privacy code Gx */
+#define MVK_TAG_CODE_Y 0x6D766B2D636F6479ull    /* "mvk-cody": the verification code Gy */
+#define MVK_TAG_NOISE 0x6D766B2D6E6F6973ull     /* "mvk-nois": e_x of Encrypt */
+#define MVK_TAG_CHALLENGE 0x6D766B2D6368616Cull /* "mvk-chal": e of Verify */
+/* As a seed: draw the seed itself from the operating system (getrandom). */
+#define MVK_SEED_FRESH 0xFFFFFFFFFFFFFFFFull
+/* Largest sparsity t the seeded calls accept. */
+#define MVK_SEEDED_MAX_T 4096u
+
+/* pp: the public parameters of Preprocess (both codes, P^T and Q), and st:
+ * the secret state of Encrypt (the noise vectors).  Both are library-owned,
+ * with their device memory; the *_free calls release them. */
+typedef struct mvk_pp mvk_pp;
+typedef struct mvk_st mvk_st;
+
+/*
+ * The sampling specification above on the host, for callers that keep the
+ * draws themselves (and for tests).  mvk_sample_code: a code of dimension k
+ * and block length N = r*k into pi1, pi2, v1, v2 (host, N words each).
+ * mvk_sample_sparse: `count` draws from E_t^N into idx, val (host, count x t
+ * words each; t <= N).  The values are in the build's field.
+ * Errors: MVK_EINVAL (null pointer, k, r or N zero, t > N), MVK_ERANGE (N above
+ * 2^31 - 1).
+ */
+mvk_status mvk_sample_code(uint32_t k, uint32_t r, uint64_t seed, uint64_t tag, uint32_t *pi1, uint32_t *pi2,
+                           uint32_t *v1, uint32_t *v2);
+mvk_status mvk_sample_sparse(uint32_t count, uint32_t N, uint32_t t, uint64_t seed, uint64_t tag, uint32_t *idx,
+                             uint32_t *val);
+
+/*
+ * Preprocess with codes the library draws (Protocol pvMVMD, Preprocess; App. B):
+ * Gx (k = n, rate 1/r_x) from (code_seed, MVK_TAG_CODE_X), Gy (k = m, rate
+ * 1/r_y) from (code_seed, MVK_TAG_CODE_Y), then P^T = (W Gx)^T and Q = Gy^T W
+ * as mvk_keygen.  W: device, m x n int8.  *out receives a new pp holding one
+ * device allocation (the code arrays, P^T and Q); mvk_pp_key gives the
+ * mvk_key view every other call takes.  Waits for `stream` (the code arrays
+ * are copied from the host), so it cannot be captured in a graph.
+ * Errors: MVK_EINVAL, MVK_ERANGE (n > MVK_MAX_N, a block length above
+ * 2^31 - 1, a buffer above 2^62 bytes), MVK_ENOMEM, MVK_ERANDOM, MVK_EHIP.
+ */
+mvk_status mvk_keygen_seeded(uint32_t m, uint32_t n, uint32_t r_x, uint32_t r_y, uint64_t code_seed,
+                             const int8_t *W, void *stream, mvk_pp **out);
+/* The key of pp (valid until mvk_pp_free); NULL for a NULL pp. */
+const mvk_key *mvk_pp_key(const mvk_pp *pp);
+/* Frees pp and its device memory (hipFree; work that reads the key must be
+ * complete).  NULL is ignored. */
+void mvk_pp_free(mvk_pp *pp);
+
+/*
+ * Encrypt with noise the library draws (Protocol pvMVMD, Encrypt): column b
+ * gets e_b = sparse vector b of E_{t_x}^{Nx} from (noise_seed, MVK_TAG_NOISE),
+ * drawn on the device, and Xhat_b = X_b + Gx e_b (as mvk_encode).  Every call
+ * must use a new seed (Sec. 4.2: reusing the noise of a column leaks the
+ * difference of the two queries); MVK_SEED_FRESH takes one from the
+ * operating system.  *st receives a new state holding the noise (device
+ * memory), the secret st of Encrypt that decode needs; mvk_st_noise exposes it.
+ *   X: device, B x n (plaintext);  Xhat: device, B x n, written.
+ * Stream-ordered like mvk_encode (the draws are a kernel on `stream`).
+ * Errors: MVK_EINVAL (t_x > Nx, null pointer), MVK_ERANGE (B > 65535,
+ * t_x > MVK_SEEDED_MAX_T), MVK_ENOMEM, MVK_ERANDOM, MVK_EHIP.
+ */
+mvk_status mvk_encode_seeded(const mvk_key *key, const uint32_t *X, uint32_t B, uint32_t t_x, uint64_t noise_seed,
+                             uint32_t *Xhat, mvk_st **st, void *stream);
+/* The noise of st (B sparse vectors of t_x positions; device arrays). */
+const mvk_sparse *mvk_st_noise(const mvk_st *st);
+/* Frees st and its device memory (work that reads it must be complete). */
+void mvk_st_free(mvk_st *st);
+
+/*
+ * Verify + Decrypt with challenges the library draws (Protocol pvMVMD, Verify
+ * and Decrypt): ell challenges, challenge q = sparse vector q of E_{t_y}^{Ny}
+ * from (chal_seed, MVK_TAG_CHALLENGE), drawn on the device when the call
+ * runs, after the responses Yhat it is given; then everything as
+ * mvk_decode_verify with the noise of st (B = the column count of st).
+ * Outputs as mvk_decode_verify.  Errors: as mvk_decode_verify, plus
+ * MVK_EINVAL (null st, t_y > Ny), MVK_ERANGE (t_y > MVK_SEEDED_MAX_T),
+ * MVK_ERANDOM.
+ */
+mvk_status mvk_decode_verify_seeded(const mvk_key *key, const mvk_st *st, const uint32_t *Xhat,
+                                    const uint32_t *Yhat, uint32_t t_y, uint32_t ell, uint64_t chal_seed,
+                                    uint32_t *Y, uint32_t *vL, uint32_t *vR, uint32_t *accept, void *stream);
 
 #ifdef __cplusplus
 }

@@ -26,8 +26,10 @@ P = MVK_PRIME
 P_BABYBEAR = MVK_PRIME_BABYBEAR
 FIELDS = {"m31": P, "babybear": P_BABYBEAR}
 
-__all__ = ["P", "P_BABYBEAR", "FIELDS", "MVK_MAX_N", "MvkError", "Code", "Key", "PackedW", "pack_weights", "server_eval", "keygen", "encode",
-           "decode_verify", "verify_prepare", "raa_encode", "raa_syndrome", "library_path"]
+__all__ = ["P", "P_BABYBEAR", "FIELDS", "MVK_MAX_N", "MvkError", "Code", "Key", "PackedW", "pack_weights", "server_eval",
+           "keygen", "encode", "decode_verify", "verify_prepare", "raa_encode", "raa_syndrome", "library_path",
+           "keygen_seeded", "encode_seeded", "decode_verify_seeded", "sample_code", "sample_sparse", "SeededPP",
+           "SeededState", "TAG_CODE_X", "TAG_CODE_Y", "TAG_NOISE", "TAG_CHALLENGE", "SEED_FRESH"]
 
 
 def library_path(p: int = P) -> str:
@@ -440,3 +442,143 @@ def stream_read(data: torch.Tensor, sink: torch.Tensor | None = None, stream=Non
     _lib.check("mvk_stream_read", _lib.load().mvk_stream_read(
         data.data_ptr(), nbytes, _dev(sink, torch.int32, (_lib.MVK_STREAM_READ_BLOCKS,), "sink"), _stream(stream)))
     return sink
+
+
+# ---------------------------------------------------------------------------
+# Seeded calls: the library draws the codes, the noise and the challenges
+# ---------------------------------------------------------------------------
+TAG_CODE_X = _lib.MVK_TAG_CODE_X
+TAG_CODE_Y = _lib.MVK_TAG_CODE_Y
+TAG_NOISE = _lib.MVK_TAG_NOISE
+TAG_CHALLENGE = _lib.MVK_TAG_CHALLENGE
+SEED_FRESH = _lib.MVK_SEED_FRESH
+
+
+class _DeviceArray:
+    """A library-owned int32 device array, seen by torch through the CUDA
+    array interface (no copy; the owner keeps the memory alive)."""
+
+    def __init__(self, ptr: int, shape: tuple):
+        self.__cuda_array_interface__ = {"shape": tuple(int(d) for d in shape), "typestr": "<i4",
+                                         "data": (int(ptr), False), "version": 2, "strides": None}
+
+
+def _view(ptr: int, shape: tuple, device) -> torch.Tensor:
+    if int(np_prod(shape)) == 0:
+        return torch.empty(shape, dtype=torch.int32, device=device)
+    return torch.as_tensor(_DeviceArray(ptr, shape), device=device)
+
+
+def np_prod(shape) -> int:
+    out = 1
+    for d in shape:
+        out *= int(d)
+    return out
+
+
+class SeededPP:
+    """pp of Preprocess with library-drawn codes (mvk_keygen_seeded).  ``key`` is
+    a Key whose tensors view the library's memory; every call that takes a Key
+    accepts it.  The memory is freed when this object is collected."""
+
+    def __init__(self, handle: int, p: int, device):
+        self._handle, self._p = handle, p
+        ks = _lib.load(p).mvk_pp_key(handle).contents
+        cx, cy, m, n = ks.cx, ks.cy, ks.m, ks.n
+
+        def code(c):
+            N = c.k * c.r
+            return Code(c.k, c.r, _view(c.pi1, (N,), device), _view(c.pi2, (N,), device), _view(c.v1, (N,), device),
+                        _view(c.v2, (N,), device), p)
+
+        self.key = Key(m, n, code(cx), code(cy), _view(ks.PT, (cx.k * cx.r, m), device),
+                       _view(ks.Q, (cy.k * cy.r, n), device))
+        self.key._owner = self
+
+    def __del__(self):
+        h, self._handle = getattr(self, "_handle", None), None
+        if h:
+            _lib.load(self._p).mvk_pp_free(h)
+
+
+class SeededState:
+    """st of Encrypt with library-drawn noise (mvk_encode_seeded): ``idx``,
+    ``val`` (B x t_x) view the library's device arrays."""
+
+    def __init__(self, handle: int, p: int, device):
+        self._handle, self._p = handle, p
+        sp = _lib.load(p).mvk_st_noise(handle).contents
+        self.B, self.t = sp.count, sp.t
+        self.idx = _view(sp.idx or 0, (sp.count, sp.t), device)
+        self.val = _view(sp.val or 0, (sp.count, sp.t), device)
+
+    def __del__(self):
+        h, self._handle = getattr(self, "_handle", None), None
+        if h:
+            _lib.load(self._p).mvk_st_free(h)
+
+
+def keygen_seeded(W: torch.Tensor, r_x: int, r_y: int, code_seed: int, p: int = P, stream=None) -> SeededPP:
+    """Preprocess with codes drawn from code_seed (SEED_FRESH: from the OS)."""
+    m, n = W.shape
+    out = ctypes.c_void_p()
+    _lib.check("mvk_keygen_seeded", _lib.load(p).mvk_keygen_seeded(
+        m, n, r_x, r_y, code_seed & 0xFFFFFFFFFFFFFFFF, _dev(W, torch.int8, (m, n), "W"), _stream(stream),
+        ctypes.byref(out)))
+    return SeededPP(out.value, p, W.device)
+
+
+def encode_seeded(key: Key, X: torch.Tensor, t_x: int, noise_seed: int, out: torch.Tensor | None = None,
+                  stream=None):
+    """Encrypt with noise drawn from noise_seed: returns (Xhat, SeededState)."""
+    B = X.shape[0]
+    if out is None:
+        out = torch.empty_like(X)
+    ks = key.struct()
+    h = ctypes.c_void_p()
+    _lib.check("mvk_encode_seeded", _lib.load(key.p).mvk_encode_seeded(
+        ctypes.byref(ks), _dev(X, torch.int32, (B, key.n), "X"), B, t_x, noise_seed & 0xFFFFFFFFFFFFFFFF,
+        _dev(out, torch.int32, (B, key.n), "Xhat"), ctypes.byref(h), _stream(stream)))
+    return out, SeededState(h.value, key.p, X.device)
+
+
+def decode_verify_seeded(key: Key, st: SeededState, Xhat: torch.Tensor, Yhat: torch.Tensor, t_y: int, ell: int,
+                         chal_seed: int, Y: torch.Tensor | None = None, vL: torch.Tensor | None = None,
+                         vR: torch.Tensor | None = None, accept: torch.Tensor | None = None, stream=None):
+    """Verify + Decrypt with ell challenges drawn from chal_seed.  Returns (Y, accept, vL, vR)."""
+    B = st.B
+    dev = Xhat.device
+    if Y is None:
+        Y = torch.empty((B, key.m), dtype=torch.int32, device=dev)
+    if accept is None:
+        accept = torch.empty((B,), dtype=torch.int32, device=dev)
+    ks = key.struct()
+    _lib.check("mvk_decode_verify_seeded", _lib.load(key.p).mvk_decode_verify_seeded(
+        ctypes.byref(ks), st._handle, _dev(Xhat, torch.int32, (B, key.n), "Xhat"),
+        _dev(Yhat, torch.int32, (B, key.m), "Yhat"), t_y, ell, chal_seed & 0xFFFFFFFFFFFFFFFF,
+        _dev(Y, torch.int32, (B, key.m), "Y"), _dev(vL, torch.int32, (ell, B), "vL") if vL is not None else None,
+        _dev(vR, torch.int32, (ell, B), "vR") if vR is not None else None, _dev(accept, torch.int32, (B,), "accept"),
+        _stream(stream)))
+    return Y, accept, vL, vR
+
+
+def sample_code(k: int, r: int, seed: int, tag: int, p: int = P) -> dict:
+    """The library's host draw of a code (k, r): dict(k, r, N, pi1, pi2, v1, v2) of uint32 numpy arrays."""
+    import numpy as np
+    N = k * r
+    arrs = [np.empty(N, dtype=np.uint32) for _ in range(4)]
+    ptr = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32))  # noqa: E731
+    _lib.check("mvk_sample_code", _lib.load(p).mvk_sample_code(k, r, seed & 0xFFFFFFFFFFFFFFFF, tag,
+                                                               *[ptr(a) for a in arrs]))
+    return dict(k=k, r=r, N=N, pi1=arrs[0], pi2=arrs[1], v1=arrs[2], v2=arrs[3])
+
+
+def sample_sparse(count: int, N: int, t: int, seed: int, tag: int, p: int = P):
+    """The library's host draw of ``count`` vectors of E_t^N: (idx, val), uint32 numpy count x t."""
+    import numpy as np
+    idx = np.empty((count, t), dtype=np.uint32)
+    val = np.empty((count, t), dtype=np.uint32)
+    ptr = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_uint32))  # noqa: E731
+    _lib.check("mvk_sample_sparse", _lib.load(p).mvk_sample_sparse(count, N, t, seed & 0xFFFFFFFFFFFFFFFF, tag,
+                                                                   ptr(idx), ptr(val)))
+    return idx, val

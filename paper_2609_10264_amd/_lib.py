@@ -14,6 +14,8 @@ MVK_EINVAL = -1
 MVK_ERANGE = -2
 MVK_ENOMEM = -3
 MVK_EHIP = -4
+MVK_ERANDOM = -5
+MVK_ECAPTURE = -6
 MVK_PRIME = 2147483647
 MVK_PRIME_BABYBEAR = 2013265921
 MVK_MAX_N = 131071
@@ -21,7 +23,13 @@ MVK_PATH_AUTO = 0
 MVK_PATH_VALU = 1
 MVK_PATH_MFMA = 2
 MVK_STREAM_READ_BLOCKS = 4096
-ABI_VERSION = 5
+MVK_TAG_CODE_X = 0x6D766B2D636F6478
+MVK_TAG_CODE_Y = 0x6D766B2D636F6479
+MVK_TAG_NOISE = 0x6D766B2D6E6F6973
+MVK_TAG_CHALLENGE = 0x6D766B2D6368616C
+MVK_SEED_FRESH = 0xFFFFFFFFFFFFFFFF
+MVK_SEEDED_MAX_T = 4096
+ABI_VERSION = 6
 # field modulus -> library built over that field
 LIB_PATHS = {MVK_PRIME: LIB_PATH, MVK_PRIME_BABYBEAR: LIB_PATH_BB}
 
@@ -52,6 +60,16 @@ EXPORTS = (
     "mvk_raa_encode",
     "mvk_raa_syndrome",
     "mvk_stream_read",
+    "mvk_workspace_release",
+    "mvk_sample_code",
+    "mvk_sample_sparse",
+    "mvk_keygen_seeded",
+    "mvk_pp_key",
+    "mvk_pp_free",
+    "mvk_encode_seeded",
+    "mvk_st_noise",
+    "mvk_st_free",
+    "mvk_decode_verify_seeded",
 )
 
 
@@ -164,6 +182,28 @@ def load(p: int = MVK_PRIME) -> ctypes.CDLL:
     L.mvk_raa_syndrome.restype = st
     L.mvk_stream_read.argtypes = [vp, ctypes.c_size_t, vp, vp]
     L.mvk_stream_read.restype = st
+    u64 = ctypes.c_uint64
+    u32p = ctypes.POINTER(ctypes.c_uint32)
+    L.mvk_workspace_release.argtypes = []
+    L.mvk_workspace_release.restype = st
+    L.mvk_sample_code.argtypes = [u32, u32, u64, u64, u32p, u32p, u32p, u32p]
+    L.mvk_sample_code.restype = st
+    L.mvk_sample_sparse.argtypes = [u32, u32, u32, u64, u64, u32p, u32p]
+    L.mvk_sample_sparse.restype = st
+    L.mvk_keygen_seeded.argtypes = [u32, u32, u32, u32, u64, vp, vp, ctypes.POINTER(vp)]
+    L.mvk_keygen_seeded.restype = st
+    L.mvk_pp_key.argtypes = [vp]
+    L.mvk_pp_key.restype = ctypes.POINTER(MvkKey)
+    L.mvk_pp_free.argtypes = [vp]
+    L.mvk_pp_free.restype = None
+    L.mvk_encode_seeded.argtypes = [ctypes.POINTER(MvkKey), vp, u32, u32, u64, vp, ctypes.POINTER(vp), vp]
+    L.mvk_encode_seeded.restype = st
+    L.mvk_st_noise.argtypes = [vp]
+    L.mvk_st_noise.restype = ctypes.POINTER(MvkSparse)
+    L.mvk_st_free.argtypes = [vp]
+    L.mvk_st_free.restype = None
+    L.mvk_decode_verify_seeded.argtypes = [ctypes.POINTER(MvkKey), vp, vp, vp, u32, u32, u64, vp, vp, vp, vp, vp]
+    L.mvk_decode_verify_seeded.restype = st
     if L.mvk_abi_version() != ABI_VERSION:
         raise ImportError(f"{path}: ABI version mismatch; rebuild the library")
     if L.mvk_field_modulus() != p:

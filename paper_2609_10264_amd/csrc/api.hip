@@ -4,11 +4,14 @@
 // enqueues the kernels; all arithmetic happens in the kernels.
 #include <hip/hip_runtime.h>
 
+#include <sys/random.h>
+
 #include <cstdlib>
 #include <initializer_list>
 #include <map>
 #include <mutex>
 #include <utility>
+#include <vector>
 
 #include "mvk.h"
 #include "field.h"
@@ -25,6 +28,19 @@ struct Workspace {
 
 std::mutex g_ws_mu;
 std::map<std::pair<int, hipStream_t>, Workspace>* g_ws = nullptr;
+// Buffers replaced by a growth: graphs captured before the growth still hold
+// their addresses, so they live until mvk_workspace_release.
+std::vector<void*>* g_ws_retired = nullptr;
+
+// True if `s` is capturing a graph (no allocation may happen then).
+bool capturing(hipStream_t s) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &cs) != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    return cs != hipStreamCaptureStatusNone;
+}
 
 // The first kCtrlBase bytes of every workspace hold control words; a call may
 // ask for a larger control region.  The control region is zeroed when the
@@ -33,35 +49,39 @@ constexpr size_t kCtrlBase = 256;
 
 // Returns a device buffer of at least `bytes` private to (current device, s),
 // placed after the control region of at least `ctrl_bytes` (>= kCtrlBase;
-// *ctrl, may be null).  Growing waits for the work already enqueued on `s`
-// before freeing the old buffer, so earlier calls on the same stream can still
-// be using it; pointers from earlier calls are then invalid, so a call takes
-// everything it needs from one workspace() request.
+// *ctrl, may be null).  A growth retires the old buffer (earlier calls and
+// captured graphs may still use it) and allocates one at least 1.5 times as
+// large; pointers from earlier requests then refer to the retired buffer, so a
+// call takes everything it needs from one workspace() request.  Under graph
+// capture a growth is refused (MVK_ECAPTURE).
 mvk_status workspace(hipStream_t s, size_t bytes, void** out, uint32_t** ctrl = nullptr, size_t ctrl_bytes = 0) {
     ctrl_bytes = ctrl_bytes < kCtrlBase ? kCtrlBase : (ctrl_bytes + 255) & ~(size_t)255;
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return MVK_EHIP;
     std::lock_guard<std::mutex> lk(g_ws_mu);
     if (!g_ws) g_ws = new std::map<std::pair<int, hipStream_t>, Workspace>();
+    if (!g_ws_retired) g_ws_retired = new std::vector<void*>();
     Workspace& w = (*g_ws)[std::make_pair(dev, s)];
     const size_t need_ctrl = ctrl_bytes > w.ctrl ? ctrl_bytes : w.ctrl;
     if (w.size < need_ctrl + bytes || w.ctrl < need_ctrl) {
-        if (w.ptr) {
-            if (hipStreamSynchronize(s) != hipSuccess) return MVK_EHIP;
-            (void)hipFree(w.ptr);
-            w.ptr = nullptr;
-            w.size = 0;
-            w.ctrl = 0;
-        }
+        if (capturing(s)) return MVK_ECAPTURE;
         size_t sz = need_ctrl + bytes;
+        if (sz < w.size + w.size / 2) sz = w.size + w.size / 2;
         sz = sz < ((size_t)1 << 20) ? ((size_t)1 << 20) : sz;
         sz = (sz + 4095) & ~(size_t)4095;
-        if (hipMalloc(&w.ptr, sz) != hipSuccess) {
+        void* fresh = nullptr;
+        if (hipMalloc(&fresh, sz) != hipSuccess) {
             (void)hipGetLastError();
-            w.ptr = nullptr;
             return MVK_ENOMEM;
         }
-        if (hipMemset(w.ptr, 0, need_ctrl) != hipSuccess) return MVK_EHIP;
+        // zero the new control region in stream order (the retired buffer may
+        // still be in use by work queued earlier on `s`)
+        if (launch_fill_u32((uint32_t*)fresh, need_ctrl / 4, 0u, s) != hipSuccess) {
+            (void)hipFree(fresh);
+            return MVK_EHIP;
+        }
+        if (w.ptr) g_ws_retired->push_back(w.ptr);
+        w.ptr = fresh;
         w.size = sz;
         w.ctrl = need_ctrl;
     }
@@ -213,6 +233,8 @@ const char* mvk_status_str(mvk_status s) {
         case MVK_ERANGE: return "size or value out of range";
         case MVK_ENOMEM: return "out of device memory";
         case MVK_EHIP: return "HIP runtime error";
+        case MVK_ERANDOM: return "the operating system's random source failed";
+        case MVK_ECAPTURE: return "the workspace would have to grow during graph capture";
         default: return "unknown status";
     }
 }
@@ -319,21 +341,41 @@ mvk_status mvk_decode_verify_prepared(const mvk_key* key, const uint32_t* Xhat, 
 }  // extern "C"
 
 namespace {
+// Challenges that decode_verify_run draws itself (the seeded Verify).
+struct ChallengeDraw {
+    uint64_t seed;
+};
+
 // decode_verify after the argument checks; Y may be null (no decryption
-// output) and ex may have t = 0 (no gathers of Pᵀ).
+// output) and ex may have t = 0 (no gathers of Pᵀ).  With `draw`, the ell
+// challenges of t positions that `ey` describes (its idx/val are ignored) are
+// first drawn into the workspace from draw->seed (sample.h).
 mvk_status decode_verify_run(const mvk_key* key, const uint32_t* Xhat, const uint32_t* Yhat, uint32_t B,
-                             const mvk_sparse* ex, const mvk_sparse* ey, uint32_t* Y, uint32_t* vL, uint32_t* vR,
-                             uint32_t* accept, hipStream_t s) {
-    const uint32_t m = key->m, ell = ey->count;
+                             const mvk_sparse* ey_in, uint32_t* Y, uint32_t* vL, uint32_t* vR, uint32_t* accept,
+                             hipStream_t s, const mvk_sparse* ex, const ChallengeDraw* draw = nullptr) {
+    const uint32_t m = key->m, ell = ey_in->count;
     const size_t Ny = (size_t)key->cy.r * m;
+    const size_t e_bytes = draw ? align_up((size_t)2 * ell * ey_in->t * 4) : 0;
     const size_t r_bytes = align_up((size_t)ell * m * 4);
     const size_t syn_bytes = align_up(syn_scratch_bytes(ell, Ny));
     void* ws = nullptr;
     uint32_t* ctrl = nullptr;
-    const mvk_status st = workspace(s, r_bytes + syn_bytes, &ws, &ctrl, dv_ctrl_bytes(m, key->n, B, ell));
+    const mvk_status st =
+        workspace(s, e_bytes + r_bytes + syn_bytes, &ws, &ctrl, dv_ctrl_bytes(m, key->n, B, ell));
     if (st) return st;
-    uint32_t* rv = (uint32_t*)ws;
-    uint32_t* syn_scratch = (uint32_t*)((char*)ws + r_bytes);
+    mvk_sparse drawn = *ey_in;
+    if (draw) {
+        uint32_t* idx = (uint32_t*)ws;
+        uint32_t* val = idx + (size_t)ell * ey_in->t;
+        if (launch_sample_sparse(draw->seed, MVK_TAG_CHALLENGE, ell, (uint32_t)Ny, ey_in->t, idx, val, s) !=
+            hipSuccess)
+            return MVK_EHIP;
+        drawn.idx = idx;
+        drawn.val = val;
+    }
+    const mvk_sparse* ey = &drawn;
+    uint32_t* rv = (uint32_t*)((char*)ws + e_bytes);
+    uint32_t* syn_scratch = (uint32_t*)((char*)ws + e_bytes + r_bytes);
     if (Ny <= kSynScratchAbove &&
         dv_syn_fits(m, key->n, (uint32_t)Ny, B, ell, dv_decode_cols(m, B, key->PT, Yhat, Y, rv))) {
         // one launch: the syndromes overlap the Decrypt and Verify gathers
@@ -359,7 +401,7 @@ mvk_status mvk_decode_verify(const mvk_key* key, const uint32_t* Xhat, const uin
     if (validate_mode() && (st = check_all((hipStream_t)stream, {{Xhat, (size_t)B * key->n},
                                                                   {Yhat, (size_t)B * key->m}})))
         return st;
-    return decode_verify_run(key, Xhat, Yhat, B, ex, ey, Y, vL, vR, accept, (hipStream_t)stream);
+    return decode_verify_run(key, Xhat, Yhat, B, ey, Y, vL, vR, accept, (hipStream_t)stream, ex);
 }
 
 mvk_status mvk_verify(const mvk_key* key, const uint32_t* X, const uint32_t* Y, uint32_t B, const mvk_sparse* ey,
@@ -374,7 +416,7 @@ mvk_status mvk_verify(const mvk_key* key, const uint32_t* X, const uint32_t* Y, 
     if (validate_mode() && (st = check_all((hipStream_t)stream, {{X, (size_t)B * key->n}, {Y, (size_t)B * key->m}})))
         return st;
     const mvk_sparse none = {nullptr, nullptr, 0u, B};  // no noise: nothing to decrypt
-    return decode_verify_run(key, X, Y, B, &none, ey, nullptr, vL, vR, accept, (hipStream_t)stream);
+    return decode_verify_run(key, X, Y, B, ey, nullptr, vL, vR, accept, (hipStream_t)stream, &none);
 }
 
 // Control word of the workgroup counters of client_prepare and encode_masked.
@@ -573,6 +615,188 @@ mvk_status mvk_stream_read(const void* data, size_t bytes, uint32_t* sink, void*
     if (bytes == 0) return MVK_OK;
     if (!data || !sink || ((uintptr_t)data & 15) || (bytes & 15)) return MVK_EINVAL;
     return hip_status(launch_stream_read(data, bytes, sink, MVK_STREAM_READ_BLOCKS, (hipStream_t)stream));
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Seeded calls (the library draws the method's randomness, sample.h)
+// ---------------------------------------------------------------------------
+struct mvk_pp {
+    mvk_key key;
+    void* mem;  // one device allocation: both codes' arrays, PT, Q
+};
+
+struct mvk_st {
+    mvk_sparse ex;
+    void* mem;  // device: idx then val (count x t words each)
+};
+
+namespace {
+// A seed from the operating system for MVK_SEED_FRESH; other seeds pass through.
+mvk_status resolve_seed(uint64_t* seed) {
+    if (*seed != MVK_SEED_FRESH) return MVK_OK;
+    uint64_t v = 0;
+    size_t got = 0;
+    while (got < sizeof(v)) {
+        const ssize_t r = getrandom((char*)&v + got, sizeof(v) - got, 0);
+        if (r <= 0) return MVK_ERANDOM;
+        got += (size_t)r;
+    }
+    *seed = v;
+    return MVK_OK;
+}
+}  // namespace
+
+extern "C" {
+
+mvk_status mvk_workspace_release(void) {
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    if (!g_ws_retired || g_ws_retired->empty()) return MVK_OK;
+    if (hipDeviceSynchronize() != hipSuccess) return MVK_EHIP;
+    for (void* p : *g_ws_retired) (void)hipFree(p);
+    g_ws_retired->clear();
+    return MVK_OK;
+}
+
+mvk_status mvk_sample_code(uint32_t k, uint32_t r, uint64_t seed, uint64_t tag, uint32_t* pi1, uint32_t* pi2,
+                           uint32_t* v1, uint32_t* v2) {
+    if (!pi1 || !pi2 || !v1 || !v2 || k == 0 || r == 0) return MVK_EINVAL;
+    if ((uint64_t)k * r > 0x7fffffffull) return MVK_ERANGE;
+    sample_code_host(k, r, seed, tag, pi1, pi2, v1, v2);
+    return MVK_OK;
+}
+
+mvk_status mvk_sample_sparse(uint32_t count, uint32_t N, uint32_t t, uint64_t seed, uint64_t tag, uint32_t* idx,
+                             uint32_t* val) {
+    if (count == 0 || t == 0) return MVK_OK;
+    if (!idx || !val || N == 0 || t > N) return MVK_EINVAL;
+    sample_sparse_host(count, N, t, seed, tag, idx, val);
+    return MVK_OK;
+}
+
+mvk_status mvk_keygen_seeded(uint32_t m, uint32_t n, uint32_t r_x, uint32_t r_y, uint64_t code_seed,
+                             const int8_t* W, void* stream, mvk_pp** out) {
+    if (!out) return MVK_EINVAL;
+    *out = nullptr;
+    if (!W || m == 0 || n == 0 || r_x == 0 || r_y == 0) return MVK_EINVAL;
+    if (n > MVK_MAX_N) return MVK_ERANGE;
+    const uint64_t Nx = (uint64_t)r_x * n, Ny = (uint64_t)r_y * m;
+    if (Nx > 0x7fffffffull || Ny > 0x7fffffffull) return MVK_ERANGE;
+    if (too_big(Nx, m, 4) || too_big(Ny, n, 4)) return MVK_ERANGE;
+    mvk_status st = resolve_seed(&code_seed);
+    if (st) return st;
+    // host draws of both codes: pi1, pi2, v1, v2 of Gx, then of Gy
+    std::vector<uint32_t> hx(4 * Nx), hy(4 * Ny);
+    sample_code_host(n, r_x, code_seed, MVK_TAG_CODE_X, &hx[0], &hx[Nx], &hx[2 * Nx], &hx[3 * Nx]);
+    sample_code_host(m, r_y, code_seed, MVK_TAG_CODE_Y, &hy[0], &hy[Ny], &hy[2 * Ny], &hy[3 * Ny]);
+    const size_t cx_bytes = align_up(4 * Nx * 4), cy_bytes = align_up(4 * Ny * 4);
+    const size_t pt_bytes = align_up(Nx * m * 4), q_bytes = align_up(Ny * n * 4);
+    void* mem = nullptr;
+    if (hipMalloc(&mem, cx_bytes + cy_bytes + pt_bytes + q_bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        return MVK_ENOMEM;
+    }
+    hipStream_t s = (hipStream_t)stream;
+    uint32_t* dx = (uint32_t*)mem;
+    uint32_t* dy = (uint32_t*)((char*)mem + cx_bytes);
+    mvk_pp* pp = new mvk_pp;
+    pp->mem = mem;
+    pp->key.m = m;
+    pp->key.n = n;
+    pp->key.cx = mvk_code{n, r_x, dx, dx + Nx, dx + 2 * Nx, dx + 3 * Nx};
+    pp->key.cy = mvk_code{m, r_y, dy, dy + Ny, dy + 2 * Ny, dy + 3 * Ny};
+    pp->key.PT = (uint32_t*)((char*)mem + cx_bytes + cy_bytes);
+    pp->key.Q = (uint32_t*)((char*)mem + cx_bytes + cy_bytes + pt_bytes);
+    // the host arrays must outlive the copies: wait for them
+    hipError_t e = hipMemcpyAsync(dx, hx.data(), 4 * Nx * 4, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(dy, hy.data(), 4 * Ny * 4, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    st = e == hipSuccess ? mvk_keygen(&pp->key, W, stream) : MVK_EHIP;
+    if (st) {
+        (void)hipStreamSynchronize(s);
+        (void)hipFree(mem);
+        delete pp;
+        return st;
+    }
+    *out = pp;
+    return MVK_OK;
+}
+
+const mvk_key* mvk_pp_key(const mvk_pp* pp) { return pp ? &pp->key : nullptr; }
+
+void mvk_pp_free(mvk_pp* pp) {
+    if (!pp) return;
+    (void)hipFree(pp->mem);
+    delete pp;
+}
+
+mvk_status mvk_encode_seeded(const mvk_key* key, const uint32_t* X, uint32_t B, uint32_t t_x, uint64_t noise_seed,
+                             uint32_t* Xhat, mvk_st** st_out, void* stream) {
+    if (!st_out) return MVK_EINVAL;
+    *st_out = nullptr;
+    mvk_status st = check_key(key);
+    if (st) return st;
+    if (B == 0 || !X || !Xhat) return MVK_EINVAL;
+    if (B > kMaxSynCount || t_x > MVK_SEEDED_MAX_T) return MVK_ERANGE;
+    const uint64_t Nx = (uint64_t)key->cx.r * key->n;
+    if (t_x > Nx) return MVK_EINVAL;
+    st = resolve_seed(&noise_seed);
+    if (st) return st;
+    hipStream_t s = (hipStream_t)stream;
+    void* mem = nullptr;
+    const size_t words = (size_t)B * t_x;
+    if (words && hipMalloc(&mem, 2 * words * 4) != hipSuccess) {
+        (void)hipGetLastError();
+        return MVK_ENOMEM;
+    }
+    mvk_st* state = new mvk_st;
+    state->mem = mem;
+    uint32_t* idx = (uint32_t*)mem;
+    state->ex = mvk_sparse{idx, words ? idx + words : nullptr, t_x, B};
+    st = hip_status(launch_sample_sparse(noise_seed, MVK_TAG_NOISE, B, (uint32_t)Nx, t_x, idx,
+                                         idx ? idx + words : nullptr, s));
+    if (!st) st = mvk_encode(key, X, B, &state->ex, Xhat, stream);
+    if (st) {
+        (void)hipStreamSynchronize(s);
+        (void)hipFree(mem);
+        delete state;
+        return st;
+    }
+    *st_out = state;
+    return MVK_OK;
+}
+
+const mvk_sparse* mvk_st_noise(const mvk_st* st) { return st ? &st->ex : nullptr; }
+
+void mvk_st_free(mvk_st* st) {
+    if (!st) return;
+    if (st->mem) (void)hipFree(st->mem);
+    delete st;
+}
+
+mvk_status mvk_decode_verify_seeded(const mvk_key* key, const mvk_st* st, const uint32_t* Xhat,
+                                    const uint32_t* Yhat, uint32_t t_y, uint32_t ell, uint64_t chal_seed,
+                                    uint32_t* Y, uint32_t* vL, uint32_t* vR, uint32_t* accept, void* stream) {
+    if (!st) return MVK_EINVAL;
+    mvk_status s0 = check_key(key);
+    if (s0) return s0;
+    if (ell == 0 || t_y == 0) return MVK_EINVAL;
+    if (ell > kMaxEll || t_y > MVK_SEEDED_MAX_T) return MVK_ERANGE;
+    if ((uint64_t)t_y > (uint64_t)key->cy.r * key->m) return MVK_EINVAL;
+    const uint32_t B = st->ex.count;
+    // the challenge arrays are drawn inside the call: a stand-in for the checks
+    static const uint32_t placeholder = 0;
+    const mvk_sparse ey = {&placeholder, &placeholder, t_y, ell};
+    s0 = check_decode_verify(key, Xhat, Yhat, B, &st->ex, &ey, Y, accept);
+    if (s0 || B == 0) return s0;
+    hipStream_t s = (hipStream_t)stream;
+    if (validate_mode() && (s0 = check_all(s, {{Xhat, (size_t)B * key->n}, {Yhat, (size_t)B * key->m}})))
+        return s0;
+    s0 = resolve_seed(&chal_seed);
+    if (s0) return s0;
+    const ChallengeDraw draw{chal_seed};
+    return decode_verify_run(key, Xhat, Yhat, B, &ey, Y, vL, vR, accept, s, &st->ex, &draw);
 }
 
 }  // extern "C"

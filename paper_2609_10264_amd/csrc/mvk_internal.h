@@ -151,6 +151,17 @@ hipError_t launch_count_noncanonical(const uint32_t* a, size_t count, uint32_t* 
 // (at least 256), their XOR is the XOR of the buffer's words.
 hipError_t launch_stream_read(const void* data, size_t bytes, uint32_t* sink, uint32_t sink_words, hipStream_t s);
 
+// seeded.hip ----------------------------------------------------------------
+// The sampling specification of sample.h.  Host: a code's four arrays (N = k*r
+// words each) and `count` sparse vectors (count x t each, t <= N).  Device:
+// the same sparse vectors, one lane per vector.
+void sample_code_host(uint32_t k, uint32_t r, uint64_t seed, uint64_t tag, uint32_t* pi1, uint32_t* pi2,
+                      uint32_t* v1, uint32_t* v2);
+void sample_sparse_host(uint32_t count, uint32_t N, uint32_t t, uint64_t seed, uint64_t tag, uint32_t* idx,
+                        uint32_t* val);
+hipError_t launch_sample_sparse(uint64_t seed, uint64_t tag, uint32_t count, uint32_t N, uint32_t t, uint32_t* idx,
+                                uint32_t* val, hipStream_t s);
+
 inline uint32_t ceil_div(uint32_t a, uint32_t b) { return (a + b - 1) / b; }
 
 }  // namespace mvk

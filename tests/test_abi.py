@@ -272,3 +272,36 @@ def test_stream_read_argument_checks_without_device_work():
     assert lib.mvk_stream_read(fake, 64, None, None) == L.MVK_EINVAL
     assert lib.mvk_stream_read(ctypes.c_void_p(0x1004), 64, fake, None) == L.MVK_EINVAL  # misaligned
     assert lib.mvk_stream_read(fake, 60, fake, None) == L.MVK_EINVAL  # not a multiple of 16
+
+
+def test_seeded_call_argument_checks_without_device_work():
+    """The seeded calls reject bad sizes and pointers before any allocation or
+    launch; the accessors and frees accept NULL."""
+    L = _lib()
+    lib = L.load()
+    fake = ctypes.c_void_p(0x1000)
+    out = ctypes.c_void_p()
+    assert lib.mvk_keygen_seeded(8, 8, 3, 3, 1, None, None, ctypes.byref(out)) == L.MVK_EINVAL
+    assert lib.mvk_keygen_seeded(8, 8, 3, 3, 1, fake, None, None) == L.MVK_EINVAL
+    assert lib.mvk_keygen_seeded(8, 8, 0, 3, 1, fake, None, ctypes.byref(out)) == L.MVK_EINVAL
+    assert lib.mvk_keygen_seeded(8, L.MVK_MAX_N + 1, 3, 3, 1, fake, None, ctypes.byref(out)) == L.MVK_ERANGE
+    assert lib.mvk_keygen_seeded(1 << 30, 8, 3, 3, 1, fake, None, ctypes.byref(out)) == L.MVK_ERANGE  # Ny > 2^31-1
+    assert out.value is None
+    code = L.MvkCode(8, 2, 0x1000, 0x1000, 0x1000, 0x1000)
+    key = L.MvkKey(8, 8, code, code, 0x1000, 0x1000)
+    st = ctypes.c_void_p()
+    assert lib.mvk_encode_seeded(ctypes.byref(key), fake, 2, 4, 1, fake, None, None) == L.MVK_EINVAL
+    assert lib.mvk_encode_seeded(ctypes.byref(key), fake, 2, 17, 1, fake, ctypes.byref(st), None) == L.MVK_EINVAL
+    assert lib.mvk_encode_seeded(ctypes.byref(key), fake, 2, L.MVK_SEEDED_MAX_T + 1, 1, fake, ctypes.byref(st),
+                                 None) == L.MVK_ERANGE
+    assert lib.mvk_encode_seeded(ctypes.byref(key), fake, 65536, 4, 1, fake, ctypes.byref(st), None) == L.MVK_ERANGE
+    assert lib.mvk_encode_seeded(ctypes.byref(key), None, 2, 4, 1, fake, ctypes.byref(st), None) == L.MVK_EINVAL
+    assert st.value is None
+    assert lib.mvk_decode_verify_seeded(ctypes.byref(key), None, fake, fake, 4, 2, 1, fake, None, None, fake,
+                                        None) == L.MVK_EINVAL
+    assert not lib.mvk_pp_key(None)
+    assert lib.mvk_st_noise(None) is not None and not lib.mvk_st_noise(None)
+    lib.mvk_pp_free(None)
+    lib.mvk_st_free(None)
+    assert lib.mvk_status_str(L.MVK_ERANDOM) != b"unknown status"
+    assert lib.mvk_status_str(L.MVK_ECAPTURE) != b"unknown status"

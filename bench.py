@@ -1,40 +1,41 @@
 """Benchmark of the pvMVMD hot path on one MI355X.
 
-One step = one pass of the whole hot path over one batch of query columns:
-    encode (Encrypt: x^ = x + Gx e_x)  ->  server_eval (y^ = W x^ mod p)
-    ->  decode_verify (Verify with ell sparse challenges + Decrypt)
-on the 4096 x 4096 attention-projection workload (one query column, r = 3,
-t_x = 64, t_y = 31, ell = 2, p = 2^31 - 1, W int8-valued).  All inputs are
-resident in HBM before the timed region.  A pool of distinct weight matrices
-(each with its own preprocessed P^T and Q) is cycled so that consecutive steps
-never find W in the 256 MB last-level cache.
+Default run (the line the driver reads): the 32-layer decoder stack, the
+largest workload that fits one GPU.  Per layer seven projections (q, k, v, o
+4096 x 4096; up, gate 11008 x 4096; down 4096 x 11008, int8-valued W over
+p = 2^31 - 1), eight query columns, RAA r = 3, t_x = 64, t_y = 31, ell = 2.
+One step = one pass over the 32 layers: per layer 4 encodes (Encrypt:
+x^ = x + Gx e_x), 7 server products (y^ = W x^ mod p) and 7 decode/verify
+calls (Verify with ell sparse challenges + Decrypt), with one response in
+1000 tampered (a nonzero delta at a seeded coordinate) and rejected inside
+the timed region.  Every input (6.48 GB of packed W, 155 GB of P^T and Q, the
+queries, noise and challenges) is resident in HBM before timing.
 
 Two schedules of the same work (--mode):
   pipelined   the paper's standard mode with pipelining (Sec. 7): the work that
               depends on neither the query nor the response (masks Gx e_x and
               P e_x, challenge vectors Gy e_q and e_q^T Q; client_prepare) runs
-              on a preparation stream ahead of the online stream
-              (encode_masked -> server_eval -> decode_verify_masked); stream
-              flags order each step after its own preparation.  Both streams
-              replay one HIP graph each, concurrently.
-  serial      every step's calls back to back on one stream (encode ->
-              server_eval -> decode_verify), one HIP graph.
-Every timed step does all of its work inside the timed region in both.
+              on a preparation stream beside the online stream
+              (encode_masked -> server_eval -> decode_verify_masked); device
+              flags order each layer after its preparation.  Each stream
+              replays one HIP graph of the pass.
+  serial      every call of the pass back to back on one stream, one graph.
 
-Printed JSON line:
-  value       modMAC/s of the whole step (m*n*B per step / step time), in the
-              chosen mode; the other mode's step time is printed beside it
-  roofline    server_eval kernel: algorithmic bytes (m*n + 4*n*B + 4*m*B) per
-              launch / mean launch duration (HIP events around each launch on
-              the launch stream), against 8 TB/s HBM
-              read_floor: a pure streaming read (mvk_stream_read) of the same
-              buffers timed the same way; frac = read time / server_eval time
-  server_eval_large  the same single-query kernel at 16384 x 16384 (268 MB of
-              W per launch), where streaming W dominates the launch
-  server_eval_batched  the 64-query kernel at 28672 x 8192 against the int8
-              matrix-core peak (4 digit-plane multiply-adds per mod-MAC)
-  cpu_baseline the CPU oracle (single-threaded plain C) on a bounded sample of
-              the same steps, on this host
+The JSON line:
+  value       modMAC/s of the whole pass (51.8 G mod-MACs / pass time), in the
+              chosen mode; both schedules' pass times beside it
+  roofline    the pass's 224 server_eval launches, captured back to back as a
+              graph and timed with HIP events on their stream: algorithmic
+              bytes (m*n + 4*n*B + 4*m*B per launch) over their device time,
+              against 8 TB/s of HBM; per shape beside it, and a streaming read
+              of the same W buffers (the measured read floor)
+  cpu_baseline the CPU oracle (plain C, threaded over row blocks on every core
+              of this host) on one layer's step of the same shapes
+  configs     the single-matrix workloads (4096 x 4096 B=1, 11008 x 4096 B=16,
+              28672 x 8192 B=64), each with its own step time, roofline and
+              cpu_baseline
+--config <name> runs one workload alone; --config paper_eval the Sec. 7.1
+sweep over BabyBear; --batch-verify B batch verification.
 """
 from __future__ import annotations
 
@@ -50,8 +51,10 @@ sys.path.insert(0, ROOT)
 METRIC = "server_eval mod-MACs/s + achieved HBM GB/s (fraction of peak), 1×MI355X"
 HBM_PEAK_GBS = 8000.0
 MFMA_INT8_PEAK_OPS = 5.0e15  # MI355X dense int8 matrix-core peak
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "server_eval_attn4096_traffic.json")
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_10264_amd", "csrc", "server_eval.hip")
+STACK_LAUNCHES_PER_PASS = 32 * 7
+SIDE_CONFIGS = ("attn4096", "mlp_up_11008x4096", "mlp_large_28672x8192")
+DTYPE = "i8xi8->i32 limb dot products, mod 2^31-1"
 
 
 def kernel_src_sha256() -> str:
@@ -60,12 +63,16 @@ def kernel_src_sha256() -> str:
         return hashlib.sha256(f.read()).hexdigest()
 
 
+def traffic_file(config: str) -> str:
+    return os.path.join(ROOT, "profiles", f"server_eval_{config}_traffic.json")
+
+
 def measured_traffic(config: str, weights: str):
-    """HBM bytes per server_eval launch from the committed counter runs, if they
-    were taken on the current kernel source, this workload and weight layout;
-    else None."""
+    """HBM bytes per server_eval launch (per pass of the 224 launches for the
+    stack) from the committed counter runs, if they were taken on the current
+    kernel source, this workload and weight layout; else None."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(traffic_file(config)) as f:
             rec = json.load(f)
         sha = kernel_src_sha256()
     except OSError:
@@ -77,9 +84,11 @@ def measured_traffic(config: str, weights: str):
 
 def write_traffic(fetch_csv: str, write_csv: str, config: str, weights: str, copy_mib: int, kernel_match: str):
     """Traffic record from two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE; KiB
-    per dispatch) of `bench.py --calib-copy-mib copy_mib`: the server_eval
-    kernel's medians, each scaled by what the same counter reads for the
-    copy_mib MiB device copy (which reads and writes copy_mib MiB)."""
+    per dispatch) of `bench.py --calib-copy-mib copy_mib`, each scaled by what
+    the same counter reads for the copy_mib MiB device copy (which reads and
+    writes copy_mib MiB).  Single-matrix workloads: the median over the
+    dispatches whose name contains kernel_match.  The stack: the sum over
+    those dispatches divided by the passes they make up (224 per pass)."""
     import csv
     import statistics
 
@@ -96,18 +105,22 @@ def write_traffic(fetch_csv: str, write_csv: str, config: str, weights: str, cop
                     copies.append(v)
         if not vals or not copies:
             raise SystemExit(f"{path}: no {counter} rows for {kernel_match!r} or the copy kernel")
+        if config == "stack32":
+            passes = len(vals) / STACK_LAUNCHES_PER_PASS
+            return sum(vals) / passes, len(vals), max(copies)
         return statistics.median(vals), len(vals), max(copies)
 
     f_med, f_n, f_copy = per_kernel(fetch_csv, "FETCH_SIZE")
     w_med, w_n, w_copy = per_kernel(write_csv, "WRITE_SIZE")
     ref_kib = copy_mib * 1024.0
     fs, ws = ref_kib / f_copy, ref_kib / w_copy
+    unit = "pass" if config == "stack32" else "dispatch"
     rec = {"kernel": kernel_match, "config": config, "weights": weights, "kernel_src_sha256": kernel_src_sha256(),
-           "fetch_size_kib_per_dispatch": f_med, "write_size_kib_per_dispatch": w_med, "dispatches": [f_n, w_n],
+           f"fetch_size_kib_per_{unit}": f_med, f"write_size_kib_per_{unit}": w_med, "dispatches": [f_n, w_n],
            "copy_reference_mib": copy_mib, "copy_fetch_size_kib": f_copy, "copy_write_size_kib": w_copy,
            "fetch_scale": fs, "write_scale": ws,
            "traffic_bytes_per_launch": int(round((f_med * fs + w_med * ws) * 1024))}
-    with open(TRAFFIC_FILE, "w") as f:
+    with open(traffic_file(config), "w") as f:
         json.dump(rec, f, indent=1)
     print(json.dumps(rec))
 
@@ -135,91 +148,152 @@ def warm(replay, seconds):
             return
 
 
+def graph_mean_seconds(stream, body, reps, warm_seconds, prime=None):
+    """Mean seconds per call of body(k), k < reps, captured back to back as one
+    HIP graph on `stream` and timed with HIP events on that stream."""
+    import torch
+
+    with torch.cuda.stream(stream):
+        (prime or body)(0)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        for k in range(reps):
+            body(k)
+
+    def replay():
+        with torch.cuda.stream(stream):
+            g.replay()
+
+    warm(replay, warm_seconds)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(stream):
+        e0.record()
+        g.replay()
+        e1.record()
+    torch.cuda.synchronize()
+    del g
+    return 1e-3 * e0.elapsed_time(e1) / reps
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", default="attn4096",
-                    help="attn4096 (default), mlp_up_11008x4096, mlp_large_28672x8192, tiny, stack32 or paper_eval "
-                         "(the Sec. 7.1 BabyBear sweep; --n picks one size)")
+    ap.add_argument("--steps", type=int, default=20, help="timed steps of the headline workload")
+    ap.add_argument("--warmup", type=int, default=5, help="untimed steps before them")
+    ap.add_argument("--config", default="all",
+                    help="all (the stack line with the single-matrix workloads as side keys), stack32, one of "
+                         "synth.CONFIGS, or paper_eval")
+    ap.add_argument("--side-steps", type=int, default=100, help="timed steps of each single-matrix side workload")
+    ap.add_argument("--side-warmup", type=int, default=10)
     ap.add_argument("--pool", type=int, default=0, help="distinct W matrices cycled (0: enough for 2x the LLC)")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="time budget of the CPU oracle sample")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="oracle time of the headline CPU baseline")
+    ap.add_argument("--side-cpu-seconds", type=float, default=4.0, help="oracle time of each side CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-large", action="store_true",
-                    help="skip the 16384 x 16384 single-query and 28672 x 8192 64-query server_eval "
-                         "measurements of the default line")
+    ap.add_argument("--no-side", action="store_true", help="headline only")
+    ap.add_argument("--no-large", action="store_true", help="skip the 16384 x 16384 single-query measurement")
     ap.add_argument("--eager", action="store_true", help="launch the timed steps one by one instead of a HIP graph")
     ap.add_argument("--chains", type=int, default=1,
-                    help="serial schedule: independent query chains run side by side (step i belongs to chain "
-                         "i mod chains)")
+                    help="serial mode of a single-matrix workload: independent query chains on their own streams")
     ap.add_argument("--mode", default="pipelined", choices=["pipelined", "serial"],
-                    help="schedule of the timed steps whose time gives `value` (both are measured)")
+                    help="schedule reported as value (both are timed)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
-                    help="after timing, copy this many MiB device-to-device (reference kernel for HBM counters)")
+                    help="after the run, copy a buffer of this many MiB (reference for the traffic counters)")
     ap.add_argument("--seed", type=int, default=2609)
     ap.add_argument("--warm-seconds", type=float, default=0.3,
-                    help="untimed replays of each timed graph before its timed replay")
+                    help="untimed graph replays before each timed replay (clock ramp-up)")
     ap.add_argument("--path", default="auto", choices=["auto", "valu", "mfma"], help="server_eval kernel family")
     ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
-                    help="write the server_eval traffic record from two rocprofv3 --pmc counter files and exit")
-    ap.add_argument("--traffic-kernel", default="server_eval_mfma_small<1, 8, 8, true, 2>",
-                    help="kernel name fragment the traffic record is taken for")
+                    help="derive the traffic record of --config from two rocprofv3 --pmc counter files and exit")
+    ap.add_argument("--traffic-kernel", default="server_eval_mfma",
+                    help="kernel-name substring selected by --write-traffic")
     ap.add_argument("--weights", default="packed", choices=["packed", "rowmajor"],
-                    help="server weight layout: packed once into matrix-core operand order (untimed, like "
-                         "keygen), or row-major as given")
+                    help="server-side layout of W (packed: matrix-core operand order, written once like P^T and Q)")
     ap.add_argument("--m", type=int, default=0, help="override the workload's row count (server-only)")
     ap.add_argument("--n", type=int, default=0, help="override the workload's column count (server-only)")
     ap.add_argument("--B", type=int, default=0, help="override the workload's query count (server-only)")
     ap.add_argument("--server-only", action="store_true",
-                    help="time server_eval alone (no client steps) on the chosen workload")
+                    help="time server_eval alone over a rotated W pool (no client steps)")
     ap.add_argument("--batch-verify", type=int, default=0, metavar="B",
-                    help="time batch verification (Protocol Batch-vMVMD) of B claims of the workload's shape "
-                         "against B one-claim verifications, and exit")
+                    help="time batch verification (Protocol Batch-vMVMD) of B claims of the workload's shape")
     return ap.parse_args()
 
 
 def main():
     args = parse()
     if args.write_traffic:
-        return write_traffic(args.write_traffic[0], args.write_traffic[1], args.config, args.weights,
+        cfg = "stack32" if args.config in ("all", "stack32") else args.config
+        return write_traffic(args.write_traffic[0], args.write_traffic[1], cfg, args.weights,
                              args.calib_copy_mib or 256, args.traffic_kernel)
     if args.gpus != 1:
-        print(json.dumps({"error": "this benchmark runs on one GPU only; multi-GPU runs are not supported",
+        print(json.dumps({"error": "this benchmark runs on one GPU only; runs on several GPUs are not supported",
                           "n_gpus": args.gpus}), flush=True)
         sys.exit(2)
 
+    import torch
+
+    import synth
+
+    torch.cuda.set_device(0)
+    if args.batch_verify:
+        return batch_verify_bench(args)
+    if args.config == "paper_eval":
+        return paper_eval_bench(args)
+    if args.server_only:
+        cfg = dict(synth.CONFIGS[args.config])
+        for key in ("m", "n", "B"):
+            if getattr(args, key):
+                cfg[key] = getattr(args, key)
+        pool = args.pool or max(2, -(-2 * 256 * 2**20 // (cfg["m"] * cfg["n"])))
+        return server_only(args, cfg, pool, args.warmup + args.steps, torch.device("cuda"))
+    if args.config in synth.CONFIGS:
+        res = config_bench(args, args.config, args.steps, args.warmup, args.cpu_seconds, large=not args.no_large)
+        ok = res.pop("_ok")
+    else:
+        if args.config not in ("all", "stack32"):
+            raise SystemExit(f"unknown --config {args.config}")
+        res = stack_bench(args, args.steps, args.warmup, args.cpu_seconds)
+        ok = res.pop("_ok")
+        if args.config == "all" and not args.no_side:
+            torch.cuda.synchronize()
+            torch.cuda.empty_cache()
+            side = {}
+            for name in SIDE_CONFIGS:
+                print(f"[bench] side workload {name}", file=sys.stderr, flush=True)
+                side[name] = config_bench(args, name, args.side_steps, args.side_warmup, args.side_cpu_seconds,
+                                          large=(name == "attn4096" and not args.no_large))
+                ok = side[name].pop("_ok") and ok
+                torch.cuda.synchronize()
+                torch.cuda.empty_cache()
+            res["configs"] = side
+    if args.calib_copy_mib:
+        calib_copy(args.calib_copy_mib)
+    print(json.dumps(res), flush=True)
+    if not ok:
+        sys.exit(1)
+
+
+def config_bench(args, name, steps, warmup, cpu_seconds, large=False):
+    """One single-matrix workload: K whole steps (encode -> server_eval ->
+    decode_verify) in both schedules over a pool of distinct W (each with its
+    own P^T and Q) that exceeds the last-level cache twice, the server_eval
+    roofline, and the oracle's CPU baseline.  Returns the record (with "_ok")."""
     import numpy as np
     import torch
 
     import paper_2609_10264_amd as mvk
     import synth
 
-    torch.cuda.set_device(0)
-    if args.config == "stack32":
-        return stack_bench(args)
-    if args.batch_verify:
-        return batch_verify_bench(args)
-    if args.config == "paper_eval":
-        return paper_eval_bench(args)
-    cfg = dict(synth.CONFIGS[args.config])
-    if args.server_only:
-        for key in ("m", "n", "B"):
-            if getattr(args, key):
-                cfg[key] = getattr(args, key)
+    cfg = dict(synth.CONFIGS[name])
     m, n, B, r, tx, ty, ell = (cfg[k] for k in ("m", "n", "B", "r", "tx", "ty", "ell"))
     cid = cfg["cid"]
-    w_bytes = m * n
-    pool = args.pool or max(2, -(-2 * 256 * 2**20 // w_bytes))
-    total_steps = args.warmup + args.steps
+    pool = args.pool or max(2, -(-2 * 256 * 2**20 // (m * n)))
+    total_steps = warmup + steps
     dev = torch.device("cuda")
 
     def d(a):
         a = np.ascontiguousarray(a)
         return torch.from_numpy(a.astype(np.int32) if a.dtype != np.int8 else a).to(dev)
-
-    if args.server_only:
-        return server_only(args, cfg, pool, total_steps, dev)
 
     # ---- setup (untimed) ---------------------------------------------------
     cx_h = synth.raa_code(synth.seed_for(cid, synth.PURPOSE_CX), n, r)
@@ -238,15 +312,15 @@ def main():
         mvk.keygen(kj, Wj)
         Ws.append(mvk.pack_weights(Wj) if args.weights == "packed" else Wj)
         keys.append(kj)
+        del Wj
     X = torch.randint(0, mvk.P, (total_steps, B, n), generator=gen, device=dev, dtype=torch.int32)
     exi, exv = synth.sparse(synth.seed_for(cid, synth.PURPOSE_NOISE, 7), total_steps * B, cx.N, tx)
     eyi, eyv = synth.sparse(synth.seed_for(cid, synth.PURPOSE_CHAL, 7), total_steps * ell, cy.N, ty)
     EXI, EXV = d(exi).view(total_steps, B, tx), d(exv).view(total_steps, B, tx)
     EYI, EYV = d(eyi).view(total_steps, ell, ty), d(eyv).view(total_steps, ell, ty)
     C = max(1, args.chains)
-    if args.warmup < C:
+    if warmup < C:
         raise SystemExit("--warmup must be at least --chains (each chain warms its own stream)")
-    # per chain: its own stream, its own output buffers
     streams = [torch.cuda.Stream() for _ in range(C)]
     Xh = [torch.empty((B, n), dtype=torch.int32, device=dev) for _ in range(C)]
     Yh = [torch.empty((B, m), dtype=torch.int32, device=dev) for _ in range(C)]
@@ -262,17 +336,17 @@ def main():
         mvk.decode_verify(keys[j], Xh[c], Yh[c], EXI[i], EXV[i], EYI[i], EYV[i], Y=Y[c], accept=ACC[i])
 
     # warm-up on the launch streams (also sizes the library's per-stream workspaces)
-    for i in range(args.warmup):
+    for i in range(warmup):
         with torch.cuda.stream(streams[i % C]):
             step(i)
     torch.cuda.synchronize()
-    timed = [[args.warmup + k for k in range(args.steps) if (args.warmup + k) % C == c] for c in range(C)]
+    timed = [[warmup + k for k in range(steps) if (warmup + k) % C == c] for c in range(C)]
 
     if args.eager:
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        for k in range(args.steps):
-            i = args.warmup + k
+        for k in range(steps):
+            i = warmup + k
             with torch.cuda.stream(streams[i % C]):
                 step(i)
         torch.cuda.synchronize()
@@ -302,7 +376,7 @@ def main():
         replay_all()
         torch.cuda.synchronize()
         elapsed = time.perf_counter() - t0
-    accepted = bool((ACC[args.warmup:] == 1).all().item())
+    accepted = bool((ACC[warmup:] == 1).all().item())
     # The buffers hold the last timed step of every chain; recompute those
     # steps eagerly and compare.
     last = [(Xh[c].clone(), Yh[c].clone(), Y[c].clone()) for c in range(C) if timed[c]]
@@ -340,14 +414,14 @@ def main():
         mvk.server_eval(Ws[j], pXh, out=pYh, path=args.path)
         mvk.decode_verify_masked(keys[j], pXh, pYh, preps[i], Y=pY, accept=ACC2[i])
 
-    for i in range(args.warmup):  # also sizes the library's per-stream workspaces
+    for i in range(warmup):  # also sizes the library's per-stream workspaces
         with torch.cuda.stream(s_prep):
             prepare(i)
-    for i in range(args.warmup):
+    for i in range(warmup):
         with torch.cuda.stream(s_on):
             online(i)
     torch.cuda.synchronize()
-    steps_t = list(range(args.warmup, total_steps))
+    steps_t = list(range(warmup, total_steps))
     g_prep, g_on = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
     with torch.cuda.graph(g_prep, stream=s_prep):
         for i in steps_t:
@@ -372,7 +446,7 @@ def main():
     replay_pipelined()
     torch.cuda.synchronize()
     elapsed_pipe = time.perf_counter() - t0
-    accepted_pipe = bool((ACC2[args.warmup:] == 1).all().item()) and int(late.item()) == 0
+    accepted_pipe = bool((ACC2[warmup:] == 1).all().item()) and int(late.item()) == 0
     # the last timed step again through the one-call path: same Xhat, Yhat, Y
     i_last = steps_t[-1]
     got = (pXh.clone(), pYh.clone(), pY.clone())
@@ -383,84 +457,363 @@ def main():
                                         EYV[i_last])
     torch.cuda.synchronize()
     pipe_matches = all(bool(torch.equal(a, b)) for a, b in zip(got, (rXh, rYh, rY)))
-    if args.mode == "pipelined":
-        elapsed, accepted = elapsed_pipe, accepted_pipe
+    del g_prep, g_on, preps
+    if not args.eager:
+        del graphs
+    elapsed = elapsed_pipe if args.mode == "pipelined" else elapsed_serial
+
+    # server_eval alone over the same W pool, captured back to back; HIP events
+    # on the launch stream bracket the replay.
     s = streams[0]
-    Yh = Yh[0]
-
-    # server_eval alone, same W pool and masked queries, captured back to back;
-    # HIP events on the launch stream bracket the replay.
-    reps = args.steps
+    reps = max(steps, 2 * pool)
     Xs = torch.randint(0, mvk.P, (pool, B, n), generator=gen, device=dev, dtype=torch.int32)
-    ge = torch.cuda.CUDAGraph()
-    with torch.cuda.stream(s):
-        for j in range(pool):
-            mvk.server_eval(Ws[j], Xs[j], out=Yh, path=args.path)
-    torch.cuda.synchronize()
-    with torch.cuda.graph(ge, stream=s):
-        for k in range(reps):
-            mvk.server_eval(Ws[k % pool], Xs[k % pool], out=Yh, path=args.path)
-    def replay_ge():
-        with torch.cuda.stream(s):
-            ge.replay()
-
-    warm(replay_ge, args.warm_seconds)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    with torch.cuda.stream(s):
-        e0.record()
-        ge.replay()
-        e1.record()
-    torch.cuda.synchronize()
-    se_mean_s = 1e-3 * e0.elapsed_time(e1) / reps
+    se_mean_s = graph_mean_seconds(s, lambda k: mvk.server_eval(Ws[k % pool], Xs[k % pool], out=Yh[0],
+                                                                 path=args.path), reps, args.warm_seconds)
     read_s = read_floor([w.data if isinstance(w, mvk.PackedW) else w for w in Ws], reps, args)
-    large = None if args.no_large else server_eval_large(args, gen, dev)
-    batched = None if args.no_large else server_eval_batched(args, gen, dev)
-
     macs = m * n * B
-    ms_per_step = 1e3 * elapsed / args.steps
     alg_bytes = m * n + 4 * n * B + 4 * m * B
     achieved = alg_bytes / se_mean_s / 1e9
-
     out = {
-        "metric": METRIC,
-        "value": macs * args.steps / elapsed,
-        "unit": "modMAC/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "i8xi8->i32 limb dot products, mod 2^31-1",
-        "data": "synthetic",
-        "config": {"workload": f"{args.config}: W {m}x{n} int8-valued in F_p (p=2^31-1), B={B} query column(s), "
-                               f"RAA r={r}, t_x={tx}, t_y={ty}, ell={ell}; step = encode+server_eval+decode_verify",
-                   "global_batch": B, "w_pool": pool, "launch": "eager" if args.eager else "hip_graph",
-                   "mode": args.mode, "chains": C if args.mode == "serial" else 1, "weights": args.weights},
-        "ms_per_step_pipelined": 1e3 * elapsed_pipe / args.steps,
-        "ms_per_step_serial": 1e3 * elapsed_serial / args.steps,
+        "workload": f"{name}: W {m}x{n} int8-valued in F_p (p=2^31-1), B={B} query column(s), RAA r={r}, "
+                    f"t_x={tx}, t_y={ty}, ell={ell}; step = encode+server_eval+decode_verify",
+        "value": macs * steps / elapsed, "unit": "modMAC/s", "steps": steps, "warmup": warmup,
+        "ms_per_step": 1e3 * elapsed / steps, "mode": args.mode,
+        "ms_per_step_pipelined": 1e3 * elapsed_pipe / steps, "ms_per_step_serial": 1e3 * elapsed_serial / steps,
+        "w_pool": pool, "weights": args.weights, "launch": "eager" if args.eager else "hip_graph",
+        "chains": C if args.mode == "serial" else 1,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(args.config, args.weights),
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(name, args.weights),
                      "kernel": f"server_eval ({args.path})", "alg_bytes_per_launch": alg_bytes,
-                     "mean_launch_us": 1e6 * se_mean_s,
+                     "mean_launch_us": 1e6 * se_mean_s, "launches": reps,
                      "read_floor": {"mean_launch_us": 1e6 * read_s, "gbps": alg_bytes / read_s / 1e9,
                                     "frac": read_s / se_mean_s}},
         "server_eval": {"modmac_per_s": macs / se_mean_s, "gb_per_s": achieved},
-        "server_eval_large": large,
-        "server_eval_batched": batched,
         "all_accepted": accepted_serial and accepted_pipe,
         "replay_matches_eager": replay_matches_eager,
         "pipelined_matches_one_call_path": pipe_matches,
     }
-
-    if args.calib_copy_mib:
-        calib_copy(args.calib_copy_mib)
+    if B > 4:
+        ops = 2.0 * 4 * macs  # four int8 digit planes per mod-MAC
+        out["mfma"] = {"int8_tops": ops / se_mean_s / 1e12, "peak_tops": MFMA_INT8_PEAK_OPS / 1e12,
+                       "frac": ops / se_mean_s / MFMA_INT8_PEAK_OPS,
+                       "ops_per_alg_byte": ops / alg_bytes, "ridge_ops_per_byte": MFMA_INT8_PEAK_OPS / 8e12}
+    del Ws, keys, X, Xs
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    if large:
+        out["server_eval_large"] = server_eval_large(args, gen, dev)
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(args, cfg, cx_h, cy_h)
-    print(json.dumps(out), flush=True)
-    if not (accepted_serial and accepted_pipe and replay_matches_eager and pipe_matches):
-        sys.exit(1)
+        out["cpu_baseline"] = cpu_baseline_config(cfg, cpu_seconds)
+    out["_ok"] = accepted_serial and accepted_pipe and replay_matches_eager and pipe_matches
+    return out
+
+
+def stack_bench(args, steps, warmup, cpu_seconds):
+    """The 32-layer stack (seven projections per layer, 8 query columns): one
+    step is a full pass (4 encodes, 7 server evaluations, 7 verifications per
+    layer) with the seeded one-in-1000 tampered responses.  Both schedules are
+    timed over `steps` passes after `warmup` untimed ones; returns the record
+    (with "_ok")."""
+    import numpy as np
+    import torch
+
+    import paper_2609_10264_amd as mvk
+    import paper_2609_10264_amd.stack as stack
+    import synth
+
+    cfg = synth.STACK
+    layers, B, r, tx, ty, ell, cid = (cfg[k] for k in ("layers", "B", "r", "tx", "ty", "ell", "cid"))
+    nproj = len(stack.PROJECTIONS)
+    dev = torch.device("cuda")
+    P = mvk.P
+
+    def d(a):
+        return torch.from_numpy(np.ascontiguousarray(a).astype(np.int32)).to(dev)
+
+    def make_code(kind, k):
+        purpose = synth.PURPOSE_CX if kind == "x" else synth.PURPOSE_CY
+        c = synth.raa_code(synth.seed_for(cid, purpose, sub=k), k, r)
+        return mvk.Code(c["k"], c["r"], d(c["pi1"]), d(c["pi2"]), d(c["v1"]), d(c["v2"]))
+
+    t_setup = time.perf_counter()
+    cx_by_n, cy_by_m = stack.codes_for(make_code)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(args.seed)
+    s = torch.cuda.Stream()
+    built, inputs = [], []
+    with torch.cuda.stream(s):
+        for L in range(layers):
+            Ws = {name: torch.randint(-127, 128, (m, n), generator=gen, device=dev, dtype=torch.int8)
+                  for (name, m, n, _) in stack.PROJECTIONS}
+            built.append(stack.build_layer(Ws, cx_by_n, cy_by_m, stream=s))
+            del Ws
+            X = {grp: torch.randint(0, P, (B, stack.input_width(grp)), generator=gen, device=dev,
+                                    dtype=torch.int32) for grp in stack.INPUTS}
+            ex = {}
+            for j, grp in enumerate(stack.INPUTS):
+                i_, v_ = synth.sparse(synth.seed_for(cid, synth.PURPOSE_NOISE, 100 * L + j), B,
+                                      r * stack.input_width(grp), tx)
+                ex[grp] = (d(i_), d(v_))
+            ey = {}
+            for i, (name, m, _, _) in enumerate(stack.PROJECTIONS):
+                i_, v_ = synth.sparse(synth.seed_for(cid, synth.PURPOSE_CHAL, 100 * L + i), ell, r * m, ty)
+                ey[name] = (d(i_), d(v_))
+            inputs.append((X, ex, ey))
+    torch.cuda.synchronize()
+    t_setup = time.perf_counter() - t_setup
+    print(f"[bench] stack setup {t_setup:.1f} s", file=sys.stderr, flush=True)
+
+    # one response in 1000 of a pass (layer, projection, column) is tampered
+    total = layers * nproj * B
+    g = synth.rng(synth.seed_for(cid, synth.PURPOSE_TAMPER))
+    offset = int(g.integers(0, 1000))
+    plan = {}
+    for k in range(offset, total, 1000):
+        L, rest = divmod(k, nproj * B)
+        i, b = divmod(rest, B)
+        m = stack.PROJECTIONS[i][1]
+        plan.setdefault((L, stack.PROJECTIONS[i][0]), []).append((b, int(g.integers(0, m)), int(g.integers(1, P))))
+
+    def tamperer(L):
+        def tamper(name, Yhat):
+            for b, pos, delta in plan.get((L, name), []):
+                Yhat[b, pos] = (Yhat[b, pos].to(torch.int64) + delta) % P
+        return tamper
+
+    def expected_accept(L, name):
+        bad = {b for (b, _, _) in plan.get((L, name), [])}
+        return [0 if b in bad else 1 for b in range(B)]
+
+    def accepts_ok(results):
+        return all(out[name][1].tolist() == expected_accept(L, name)
+                   for L, out in enumerate(results) for name in out)
+
+    def time_passes(replay):
+        warm(replay, args.warm_seconds)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            replay()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / steps
+
+    # ---- serial -------------------------------------------------------------
+    results = []
+
+    def one_pass():
+        results.clear()
+        for L in range(layers):
+            results.append(stack.run_layer(built[L], *inputs[L], tamper=tamperer(L), stream=s))
+
+    with torch.cuda.stream(s):
+        for _ in range(warmup):
+            one_pass()
+    torch.cuda.synchronize()
+    gs = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gs, stream=s):
+        one_pass()
+
+    def replay_serial():
+        with torch.cuda.stream(s):
+            gs.replay()
+
+    t_serial = time_passes(replay_serial)
+    ok_serial = accepts_ok(results)
+
+    # ---- pipelined ----------------------------------------------------------
+    s_prep, s_on = torch.cuda.Stream(), torch.cuda.Stream()
+    flags = torch.zeros((layers, nproj), dtype=torch.int32, device=dev)
+    late = torch.zeros((), dtype=torch.int32, device=dev)
+    preps = [dict() for _ in range(layers)]
+    presults = []
+
+    def prep_pass():
+        for L in range(layers):
+            stack.prepare_layer(built[L], inputs[L][1], inputs[L][2], flags[L], out=preps[L], stream=s_prep)
+
+    def online_pass():
+        presults.clear()
+        for L in range(layers):
+            presults.append(stack.run_layer_prepared(built[L], inputs[L][0], preps[L], ready_flag=flags[L, nproj - 1],
+                                                     timeout_us=200_000, timed_out=late, tamper=tamperer(L),
+                                                     stream=s_on))
+
+    for _ in range(warmup):  # also sizes the per-stream workspaces
+        with torch.cuda.stream(s_prep):
+            prep_pass()
+        with torch.cuda.stream(s_on):
+            online_pass()
+        torch.cuda.synchronize()
+    gp, go = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gp, stream=s_prep):
+        prep_pass()
+    with torch.cuda.graph(go, stream=s_on):
+        online_pass()
+
+    def replay_pipelined():
+        # a pass's preparation starts after the previous pass's online part
+        # (it rewrites the prepared buffers and the flags that part consumes),
+        # and is submitted first: the two streams may share a hardware queue
+        s_prep.wait_stream(s_on)
+        with torch.cuda.stream(s_prep):
+            gp.replay()
+        with torch.cuda.stream(s_on):
+            go.replay()
+
+    late.zero_()
+    t_pipe = time_passes(replay_pipelined)
+    ok_pipe = accepts_ok(presults) and int(late.item()) == 0
+    same = all(bool(torch.equal(a, b)) for sr, pr in zip(results, presults) for name in sr
+               for a, b in zip(sr[name], pr[name]))
+    del gs, gp, go
+
+    # ---- the pass's server_eval launches alone ------------------------------
+    Xs = [{grp: torch.randint(0, P, (B, stack.input_width(grp)), generator=gen, device=dev, dtype=torch.int32)
+           for grp in stack.INPUTS} for _ in range(layers)]
+    Ys = {m: torch.empty((B, m), dtype=torch.int32, device=dev) for m in sorted({m for (_, m, _, _) in stack.PROJECTIONS})}
+    shapes = {}  # (m, n) -> [(L, name, group)]
+    for L in range(layers):
+        for name, m, n, grp in stack.PROJECTIONS:
+            shapes.setdefault((m, n), []).append((L, name, grp))
+
+    def launches(items):
+        for (L, name, grp) in items:
+            m = built[L].W[name].m
+            mvk.server_eval(built[L].W[name], Xs[L][grp], out=Ys[m], path=args.path, stream=s)
+
+    every = [it for v in shapes.values() for it in v]
+    every.sort()
+    pass_s = graph_mean_seconds(s, lambda k: launches(every), steps, args.warm_seconds)
+    alg_pass = sum(m * n + 4 * n * B + 4 * m * B for (_, m, n, _) in stack.PROJECTIONS) * layers
+    per_shape = {}
+    for (m, n), items in shapes.items():
+        t = graph_mean_seconds(s, lambda k, it=items: launches(it), max(2, steps // 4), args.warm_seconds)
+        t_launch = t / len(items)
+        alg = m * n + 4 * n * B + 4 * m * B
+        per_shape[f"{m}x{n}"] = {"launches_per_pass": len(items), "mean_launch_us": 1e6 * t_launch,
+                                 "alg_bytes_per_launch": alg, "gbps": alg / t_launch / 1e9,
+                                 "frac": alg / t_launch / 1e9 / HBM_PEAK_GBS}
+    read_s = read_floor([built[L].W[name].data for (L, name, _) in every], len(every), args)
+    achieved = alg_pass / pass_s / 1e9
+    macs = stack.macs_per_layer(B) * layers
+    elapsed = t_pipe if args.mode == "pipelined" else t_serial
+    res = {"metric": METRIC, "value": macs / elapsed, "unit": "modMAC/s", "n_gpus": 1, "steps": steps,
+           "warmup": warmup, "ms_per_step": 1e3 * elapsed, "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": DTYPE, "data": "synthetic",
+           "config": {"workload": f"stack32: {layers} layers x (q,k,v,o 4096x4096; up,gate 11008x4096; "
+                                  f"down 4096x11008) int8-valued W in F_p (p=2^31-1), B={B} query columns per "
+                                  f"projection, RAA r={r}, t_x={tx}, t_y={ty}, ell={ell}; step = one pass (per layer "
+                                  "4 encodes, 7 server_evals, 7 decode_verifies) with one response in 1000 "
+                                  "tampered and rejected",
+                      "global_batch": B, "launch": "hip_graph", "mode": args.mode, "weights": "packed"},
+           "ms_per_step_pipelined": 1e3 * t_pipe, "ms_per_step_serial": 1e3 * t_serial,
+           "modmac_per_pass": macs,
+           "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                        "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic("stack32", "packed"),
+                        "kernel": f"server_eval ({args.path}), the {len(every)} launches of a pass back to back",
+                        "alg_bytes_per_launch": alg_pass / len(every), "alg_bytes_per_pass": alg_pass,
+                        "launches_per_pass": len(every), "mean_launch_us": 1e6 * pass_s / len(every),
+                        "server_ms_per_pass": 1e3 * pass_s, "per_shape": per_shape,
+                        "read_floor": {"ms_per_pass": 1e3 * read_s * len(every),
+                                       "gbps": alg_pass / (read_s * len(every)) / 1e9,
+                                       "frac": read_s * len(every) / pass_s}},
+           "server_eval": {"modmac_per_s": macs / pass_s, "gb_per_s": achieved},
+           "tampered_per_pass": sum(len(v) for v in plan.values()),
+           "all_expected_verdicts": ok_serial and ok_pipe, "pipelined_matches_serial": same,
+           "setup_s": t_setup}
+    del built, inputs, results, presults, preps, Xs, Ys
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline_stack(cpu_seconds)
+    res["_ok"] = ok_serial and ok_pipe and same
+    return res
+
+
+def cpu_baseline_config(cfg, seconds):
+    """The oracle's whole step (encode, server_eval, verify, decode) on the
+    workload's shapes, threaded over row blocks on every core of this host,
+    timed over repeated steps for about `seconds` (preprocessing untimed)."""
+    import oracle
+    import synth
+
+    m, n, B, r, tx, ty, ell = (cfg[k] for k in ("m", "n", "B", "r", "tx", "ty", "ell"))
+    cid = cfg["cid"]
+    T = oracle.threads()
+    cx = synth.raa_code(synth.seed_for(cid, synth.PURPOSE_CX), n, r)
+    cy = synth.raa_code(synth.seed_for(cid, synth.PURPOSE_CY), m, r)
+    W = synth.weights(synth.seed_for(cid, synth.PURPOSE_W, 5), m, n)
+    PT, Q = oracle.keygen(W, cx, cy, nthreads=T)  # preprocessing, untimed
+    steps, el = 0, 0.0
+    while True:
+        X = synth.field_uniform(synth.seed_for(cid, synth.PURPOSE_X, 100 + steps), (B, n))
+        exi, exv = synth.sparse(synth.seed_for(cid, synth.PURPOSE_NOISE, 100 + steps), B, cx["N"], tx)
+        eyi, eyv = synth.sparse(synth.seed_for(cid, synth.PURPOSE_CHAL, 100 + steps), ell, cy["N"], ty)
+        t0 = time.perf_counter()
+        Xh = oracle.encode(cx, X, exi, exv)
+        Yh = oracle.server_eval(W, Xh, nthreads=T)
+        acc, _, _ = oracle.verify(cy, Q, Xh, Yh, eyi, eyv)
+        oracle.decode(PT, Yh, exi, exv, nthreads=T)
+        el += time.perf_counter() - t0
+        assert acc.all()
+        steps += 1
+        if el >= seconds or steps >= 10000:
+            break
+    return {"value": m * n * B * steps / el, "unit": "modMAC/s", "cores": T, "kind": "oracle",
+            "host_cpu": host_cpu(),
+            "sample": f"{steps} whole steps (encode+server_eval+verify+decode) of the same shapes, one W, "
+                      f"{el:.1f} s of oracle time (input drawing and preprocessing excluded); plain C, '%' per "
+                      f"field op, server product and decryption split over {T} threads by row blocks"}
+
+
+def cpu_baseline_stack(seconds):
+    """The oracle on one layer of the stack (4 encodes, 7 server products, 7
+    verifications and decryptions), threaded over row blocks on every core,
+    repeated for about `seconds`; scaled to mod-MAC/s like the GPU pass."""
+    import oracle
+    import paper_2609_10264_amd.stack as stack
+    import synth
+
+    cfg = synth.STACK
+    B, r, tx, ty, ell, cid = (cfg[k] for k in ("B", "r", "tx", "ty", "ell", "cid"))
+    T = oracle.threads()
+    cxs = {n: synth.raa_code(synth.seed_for(cid, synth.PURPOSE_CX, sub=n), n, r)
+           for n in {n for (_, _, n, _) in stack.PROJECTIONS}}
+    cys = {m: synth.raa_code(synth.seed_for(cid, synth.PURPOSE_CY, sub=m), m, r)
+           for m in {m for (_, m, _, _) in stack.PROJECTIONS}}
+    Ws, keys = {}, {}
+    for i, (name, m, n, _) in enumerate(stack.PROJECTIONS):
+        Ws[name] = synth.weights(synth.seed_for(cid, synth.PURPOSE_W, 900 + i), m, n)
+        keys[name] = oracle.keygen(Ws[name], cxs[n], cys[m], nthreads=T)  # preprocessing, untimed
+    steps, el = 0, 0.0
+    while True:
+        X, ex = {}, {}
+        for j, grp in enumerate(stack.INPUTS):
+            n = stack.input_width(grp)
+            X[grp] = synth.field_uniform(synth.seed_for(cid, synth.PURPOSE_X, 900 + 10 * steps + j), (B, n))
+            ex[grp] = synth.sparse(synth.seed_for(cid, synth.PURPOSE_NOISE, 900 + 10 * steps + j), B, r * n, tx)
+        ey = {name: synth.sparse(synth.seed_for(cid, synth.PURPOSE_CHAL, 900 + 10 * steps + i), ell, r * m, ty)
+              for i, (name, m, _, _) in enumerate(stack.PROJECTIONS)}
+        t0 = time.perf_counter()
+        Xh = {grp: oracle.encode(cxs[stack.input_width(grp)], X[grp], *ex[grp]) for grp in stack.INPUTS}
+        ok = True
+        for name, m, n, grp in stack.PROJECTIONS:
+            PT, Q = keys[name]
+            Yh = oracle.server_eval(Ws[name], Xh[grp], nthreads=T)
+            acc, _, _ = oracle.verify(cys[m], Q, Xh[grp], Yh, *ey[name])
+            oracle.decode(PT, Yh, *ex[grp], nthreads=T)
+            ok = ok and bool(acc.all())
+        el += time.perf_counter() - t0
+        assert ok
+        steps += 1
+        if el >= seconds:
+            break
+    macs = stack.macs_per_layer(B)
+    return {"value": macs * steps / el, "unit": "modMAC/s", "cores": T, "kind": "oracle", "host_cpu": host_cpu(),
+            "sample": f"{steps} steps of one layer of the stack (4 encodes, 7 server products, 7 verifications "
+                      f"and decryptions; {macs / 1e9:.2f} G mod-MACs each), {el:.1f} s of oracle time (input drawing "
+                      f"and preprocessing excluded); plain C, '%' per field op, server products and decryptions "
+                      f"split over {T} threads by row blocks"}
 
 
 def read_floor(bufs, reps, args):
@@ -540,201 +893,6 @@ def server_eval_large(args, gen, dev, m=16384, n=16384, pool=2, reps=40):
     return {"workload": f"W {m}x{n} int8-valued, B=1, packed", "mean_launch_us": 1e6 * t,
             "achieved_gbps": alg / t / 1e9, "frac": alg / t / 1e9 / HBM_PEAK_GBS,
             "read_floor": {"mean_launch_us": 1e6 * t_read, "gbps": alg / t_read / 1e9, "frac": t_read / t}}
-
-
-def server_eval_batched(args, gen, dev, m=28672, n=8192, B=64, pool=3, reps=30):
-    """The batched kernel at 28672 x 8192 with 64 queries (235 MB of packed W per
-    launch, a pool of three): HIP events around a graph of back-to-back
-    launches; int8 matrix-core work 4 m n B multiply-adds (four digit planes)
-    against the 5.0 POP/s dense int8 peak, and algorithmic HBM bytes."""
-    import torch
-
-    import paper_2609_10264_amd as mvk
-
-    s = torch.cuda.Stream()
-    with torch.cuda.stream(s):
-        Ws = []
-        for _ in range(pool):
-            W = torch.randint(-127, 128, (m, n), generator=gen, device=dev, dtype=torch.int8)
-            Ws.append(mvk.pack_weights(W, stream=s))
-            del W
-        X = torch.randint(0, mvk.P, (pool, B, n), generator=gen, device=dev, dtype=torch.int32)
-        Y = torch.empty((B, m), dtype=torch.int32, device=dev)
-        for j in range(pool):
-            mvk.server_eval(Ws[j], X[j], out=Y, stream=s)
-    torch.cuda.synchronize()
-    g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g, stream=s):
-        for k in range(reps):
-            mvk.server_eval(Ws[k % pool], X[k % pool], out=Y, stream=s)
-
-    def replay():
-        with torch.cuda.stream(s):
-            g.replay()
-
-    warm(replay, args.warm_seconds)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    with torch.cuda.stream(s):
-        e0.record()
-        g.replay()
-        e1.record()
-    torch.cuda.synchronize()
-    t = 1e-3 * e0.elapsed_time(e1) / reps
-    alg = m * n + 4 * n * B + 4 * m * B
-    ops = 2.0 * 4 * m * n * B
-    del Ws, X, Y, g
-    torch.cuda.empty_cache()
-    return {"workload": f"W {m}x{n} int8-valued, B={B}, packed", "mean_launch_us": 1e6 * t,
-            "modmac_per_s": m * n * B / t, "int8_tops": ops / t / 1e12,
-            "mfma_frac": ops / t / MFMA_INT8_PEAK_OPS, "hbm_gbps": alg / t / 1e9}
-
-
-def stack_bench(args):
-    """32 decoder layers (seven projections each, 8 query columns): one step is a
-    full pass (4 encodes, 7 server evaluations, 7 verifications per layer).
-    Two schedules of the same work: serial (run_layer on one stream) and
-    pipelined (prepare_layer for every layer on a preparation stream, flags
-    ordering each layer's online part, run_layer_prepared, after its
-    preparation); --mode picks the one reported as value."""
-    import numpy as np
-    import torch
-
-    import paper_2609_10264_amd as mvk
-    import paper_2609_10264_amd.stack as stack
-    import synth
-
-    cfg = synth.STACK
-    layers, B, r, tx, ty, ell, cid = (cfg[k] for k in ("layers", "B", "r", "tx", "ty", "ell", "cid"))
-    dev = torch.device("cuda")
-
-    def d(a):
-        return torch.from_numpy(np.ascontiguousarray(a).astype(np.int32)).to(dev)
-
-    def make_code(kind, k):
-        purpose = synth.PURPOSE_CX if kind == "x" else synth.PURPOSE_CY
-        c = synth.raa_code(synth.seed_for(cid, purpose, sub=k), k, r)
-        return mvk.Code(c["k"], c["r"], d(c["pi1"]), d(c["pi2"]), d(c["v1"]), d(c["v2"]))
-
-    cx_by_n, cy_by_m = stack.codes_for(make_code)
-    gen = torch.Generator(device=dev)
-    gen.manual_seed(args.seed)
-    s = torch.cuda.Stream()
-    built, inputs = [], []
-    with torch.cuda.stream(s):
-        for L in range(layers):
-            Ws = {name: torch.randint(-127, 128, (m, n), generator=gen, device=dev, dtype=torch.int8)
-                  for (name, m, n, _) in stack.PROJECTIONS}
-            built.append(stack.build_layer(Ws, cx_by_n, cy_by_m))
-            X = {grp: torch.randint(0, mvk.P, (B, stack.input_width(grp)), generator=gen, device=dev,
-                                    dtype=torch.int32) for grp in stack.INPUTS}
-            ex = {}
-            for j, grp in enumerate(stack.INPUTS):
-                i_, v_ = synth.sparse(synth.seed_for(cid, synth.PURPOSE_NOISE, 100 * L + j), B,
-                                      r * stack.input_width(grp), tx)
-                ex[grp] = (d(i_), d(v_))
-            ey = {}
-            for i, (name, m, _, _) in enumerate(stack.PROJECTIONS):
-                i_, v_ = synth.sparse(synth.seed_for(cid, synth.PURPOSE_CHAL, 100 * L + i), ell, r * m, ty)
-                ey[name] = (d(i_), d(v_))
-            inputs.append((X, ex, ey))
-    torch.cuda.synchronize()
-    steps = max(1, args.steps // 40)
-    warmup = max(1, args.warmup // 10)
-
-    def time_graphs(replay, reps):
-        warm(replay, args.warm_seconds)
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(reps):
-            replay()
-        torch.cuda.synchronize()
-        return (time.perf_counter() - t0) / reps
-
-    # ---- serial -------------------------------------------------------------
-    results = []
-
-    def one_pass():
-        results.clear()
-        for L in range(layers):
-            results.append(stack.run_layer(built[L], *inputs[L]))
-
-    with torch.cuda.stream(s):
-        for _ in range(warmup):
-            one_pass()
-    torch.cuda.synchronize()
-    g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g, stream=s):
-        one_pass()
-
-    def replay_serial():
-        with torch.cuda.stream(s):
-            g.replay()
-
-    t_serial = time_graphs(replay_serial, steps)
-    ok_serial = all(bool((out[name][1] == 1).all().item()) for out in results for name in out)
-    last_serial = [t.clone() for t in results[-1]["down"][:2]]
-
-    # ---- pipelined ----------------------------------------------------------
-    s_prep, s_on = torch.cuda.Stream(), torch.cuda.Stream()
-    nproj = len(stack.PROJECTIONS)
-    flags = torch.zeros((layers, nproj), dtype=torch.int32, device=dev)
-    late = torch.zeros((), dtype=torch.int32, device=dev)
-    preps = [dict() for _ in range(layers)]
-    presults = []
-
-    def prep_pass():
-        for L in range(layers):
-            stack.prepare_layer(built[L], inputs[L][1], inputs[L][2], flags[L], out=preps[L], stream=s_prep)
-
-    def online_pass():
-        presults.clear()
-        for L in range(layers):
-            presults.append(stack.run_layer_prepared(built[L], inputs[L][0], preps[L], ready_flag=flags[L, nproj - 1],
-                                                     timeout_us=200_000, timed_out=late, stream=s_on))
-
-    for _ in range(warmup):  # also sizes the per-stream workspaces
-        with torch.cuda.stream(s_prep):
-            prep_pass()
-        with torch.cuda.stream(s_on):
-            online_pass()
-        torch.cuda.synchronize()
-    gp, go = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
-    with torch.cuda.graph(gp, stream=s_prep):
-        prep_pass()
-    with torch.cuda.graph(go, stream=s_on):
-        online_pass()
-
-    def replay_pipelined():
-        # a pass's preparation starts after the previous pass's online part
-        # (it rewrites the prepared buffers and the flags that part consumes),
-        # and is submitted first: the two streams may share a hardware queue
-        s_prep.wait_stream(s_on)
-        with torch.cuda.stream(s_prep):
-            gp.replay()
-        with torch.cuda.stream(s_on):
-            go.replay()
-
-    late.zero_()
-    t_pipe = time_graphs(replay_pipelined, steps)
-    ok_pipe = all(bool((out[name][1] == 1).all().item()) for out in presults for name in out)
-    ok_pipe = ok_pipe and int(late.item()) == 0
-    same = all(bool(torch.equal(a, b)) for a, b in zip(last_serial, presults[-1]["down"][:2]))
-
-    elapsed = t_pipe if args.mode == "pipelined" else t_serial
-    macs = stack.macs_per_layer(B) * layers
-    res = {"metric": METRIC, "value": macs / elapsed, "unit": "modMAC/s", "n_gpus": 1, "steps": steps,
-           "warmup": warmup, "ms_per_step": 1e3 * elapsed, "higher_is_better": True,
-           "scaling": "weak", "vs_baseline": None, "dtype": "i8xi8->i32 limb dot products, mod 2^31-1",
-           "data": "synthetic",
-           "config": {"workload": f"stack32: {layers} layers x (q,k,v,o 4096x4096; up,gate 11008x4096; "
-                                  f"down 4096x11008), B={B}, r={r}, t_x={tx}, t_y={ty}, ell={ell}; step = one full "
-                                  "pass (4 encodes, 7 server_evals, 7 decode_verifies per layer)",
-                      "global_batch": B, "launch": "hip_graph", "mode": args.mode},
-           "ms_per_step_pipelined": 1e3 * t_pipe, "ms_per_step_serial": 1e3 * t_serial,
-           "all_accepted": ok_serial and ok_pipe, "pipelined_matches_one_call_path": same}
-    print(json.dumps(res), flush=True)
-    if not (ok_serial and ok_pipe and same):
-        sys.exit(1)
 
 
 def server_only(args, cfg, pool, total_steps, dev):
@@ -1042,18 +1200,20 @@ def paper_eval_bench(args):
     if not args.no_cpu_baseline:
         # the oracle's server product over a row sample of the largest W
         n = top["n"]
-        Wh = synth.weights(synth.seed_for(cid, synth.PURPOSE_W, n), 256, n)
+        T = oracle.threads()
+        rows_s = 64 * T
+        Wh = synth.weights(synth.seed_for(cid, synth.PURPOSE_W, n), rows_s, n)
         Xq = synth.field_uniform(synth.seed_for(cid, synth.PURPOSE_X, n), (1, n), p=p)
         reps, el = 0, 0.0
         while el < min(args.cpu_seconds, 5.0):
             t0 = time.perf_counter()
-            oracle.server_eval(Wh, Xq, p=p)
+            oracle.server_eval(Wh, Xq, p=p, nthreads=T)
             el += time.perf_counter() - t0
             reps += 1
-        res["cpu_baseline"] = {"value": 256 * n * reps / el, "unit": "modMAC/s", "cores": 1, "kind": "oracle",
+        res["cpu_baseline"] = {"value": rows_s * n * reps / el, "unit": "modMAC/s", "cores": T, "kind": "oracle",
                                "host_cpu": host_cpu(),
-                               "sample": f"{reps} oracle server products of 256 rows x {n} over BabyBear, "
-                                         f"{el:.1f} s; single-threaded C, '%' per field op"}
+                               "sample": f"{reps} oracle server products of {rows_s} rows x {n} over BabyBear, "
+                                         f"{el:.1f} s; plain C, '%' per field op, rows split over {T} threads"}
     print(json.dumps(res), flush=True)
     if not ok:
         sys.exit(1)
@@ -1069,38 +1229,6 @@ def host_cpu() -> str:
     except OSError:
         pass
     return "unknown"
-
-
-def cpu_baseline(args, cfg, cx_h, cy_h):
-    """Oracle step (encode, server_eval, verify, decode) timed on a bounded sample."""
-    import numpy as np
-
-    import oracle
-    import synth
-
-    m, n, B, tx, ty, ell = (cfg[k] for k in ("m", "n", "B", "tx", "ty", "ell"))
-    cid = cfg["cid"]
-    W = synth.weights(synth.seed_for(cid, synth.PURPOSE_W, 5), m, n)
-    PT, Q = oracle.keygen(W, cx_h, cy_h)  # preprocessing, untimed
-    steps = 0
-    el = 0.0
-    while True:
-        X = synth.field_uniform(synth.seed_for(cid, synth.PURPOSE_X, 100 + steps), (B, n))
-        exi, exv = synth.sparse(synth.seed_for(cid, synth.PURPOSE_NOISE, 100 + steps), B, cx_h["N"], tx)
-        eyi, eyv = synth.sparse(synth.seed_for(cid, synth.PURPOSE_CHAL, 100 + steps), ell, cy_h["N"], ty)
-        t0 = time.perf_counter()
-        Xh = oracle.encode(cx_h, X, exi, exv)
-        Yh = oracle.server_eval(W, Xh)
-        acc, _, _ = oracle.verify(cy_h, Q, Xh, Yh, eyi, eyv)
-        oracle.decode(PT, Yh, exi, exv)
-        el += time.perf_counter() - t0
-        assert acc.all()
-        steps += 1
-        if el >= args.cpu_seconds or steps >= 10000:
-            break
-    return {"value": m * n * B * steps / el, "unit": "modMAC/s", "cores": 1, "kind": "oracle", "host_cpu": host_cpu(),
-            "sample": f"{steps} full steps (encode+server_eval+verify+decode) of the same workload, one W, "
-                      f"{el:.1f} s of oracle time (input drawing excluded); single-threaded C, '%' per field op"}
 
 
 if __name__ == "__main__":

@@ -72,7 +72,7 @@ def run_layer(layer: Layer, X: dict, ex: dict, ey: dict, tamper=None, stream=Non
     input (B x t_x); ey[name] = (idx, val) challenges (ell x t_y).
     tamper: optional callable(name, Yhat) applied to each response before
     verification (the test harness's dishonest server).
-    Returns {name: (Y, accept)}.
+    Returns {name: (Y, accept, Xhat, Yhat, vL, vR)}.
     """
     Xhat = {}
     for group in INPUTS:
@@ -84,9 +84,12 @@ def run_layer(layer: Layer, X: dict, ex: dict, ey: dict, tamper=None, stream=Non
         Yhat = server_eval(layer.W[name], Xhat[group], stream=stream)
         if tamper is not None:
             tamper(name, Yhat)
+        ell, B = ey[name][0].shape[0], Yhat.shape[0]
+        vL = torch.empty((ell, B), dtype=torch.int32, device=Yhat.device)
+        vR = torch.empty_like(vL)
         Y, acc, _, _ = decode_verify(layer.keys[name], Xhat[group], Yhat, ex[group][0], ex[group][1],
-                                     ey[name][0], ey[name][1], stream=stream)
-        out[name] = (Y, acc, Xhat[group], Yhat)
+                                     ey[name][0], ey[name][1], vL=vL, vR=vR, stream=stream)
+        out[name] = (Y, acc, Xhat[group], Yhat, vL, vR)
     return out
 
 
@@ -128,8 +131,11 @@ def run_layer_prepared(layer: Layer, X: dict, preps: dict, ready_flag: torch.Ten
         Yhat = server_eval(layer.W[name], Xhat[group], stream=stream)
         if tamper is not None:
             tamper(name, Yhat)
-        Y, acc, _, _ = decode_verify_masked(layer.keys[name], Xhat[group], Yhat, preps[name], stream=stream)
-        out[name] = (Y, acc, Xhat[group], Yhat)
+        vL = torch.empty((preps[name].ell, Yhat.shape[0]), dtype=torch.int32, device=Yhat.device)
+        vR = torch.empty_like(vL)
+        Y, acc, _, _ = decode_verify_masked(layer.keys[name], Xhat[group], Yhat, preps[name], vL=vL, vR=vR,
+                                            stream=stream)
+        out[name] = (Y, acc, Xhat[group], Yhat, vL, vR)
     return out
 
 

@@ -1,8 +1,8 @@
 """GPU parity: every call of the C ABI against the CPU oracle, bit-exact.
 
 All arithmetic is integer mod p, so every comparison is exact equality.
-Sizes span several workgroup tiles with ragged tails; the full-size LLM-layer
-shapes compare either the whole output or oracle-computable samples.
+Sizes span several workgroup tiles with ragged tails; the 4096 x 4096 layer
+is compared whole here, the larger LLM-layer shapes in test_gpu_fullsize.py.
 """
 import os
 
@@ -414,47 +414,3 @@ def test_attn4096_full():
     oacc, ovL, ovR = oracle.verify(inst.cy, Q, Xh, Yh, inst.eyi, inst.eyv)
     assert np.array_equal(host(vL), ovL) and np.array_equal(host(vR), ovR) and host(acc).tolist() == [1]
     assert np.array_equal(host(Y), oracle.decode(PT, Yh, inst.exi, inst.exv))
-
-
-def _sampled_layer_check(name, sample_rows=96, sample_cols=24):
-    cfg = synth.CONFIGS[name]
-    m, n, B = cfg["m"], cfg["n"], cfg["B"]
-    _say(f"{name} sampled compare m={m} n={n} B={B}")
-    inst = Instance(cfg["cid"], m, n, B, cfg["r"], cfg["tx"], cfg["ty"], cfg["ell"]).to_device()
-    mvk.keygen(inst.key, inst.dW)
-    g = synth.rng(synth.seed_for(cfg["cid"], 99))
-    rows = np.unique(np.concatenate([[0, m - 1], g.integers(0, m, sample_rows)]))
-    cols = np.unique(np.concatenate([[0, n - 1], g.integers(0, n, sample_cols)]))
-    # P^T column i = Gx^T W[i, :]; Q column k = Gy^T W[:, k]
-    PTd = inst.key.PT
-    Qd = inst.key.Q
-    for i in rows[:24]:
-        want = oracle.encT(inst.cx, (inst.W[i].astype(np.int64) % P).astype(np.uint32))
-        assert np.array_equal(host(PTd[:, int(i)]), want)
-    for k in cols:
-        want = oracle.encT(inst.cy, (inst.W[:, k].astype(np.int64) % P).astype(np.uint32))
-        assert np.array_equal(host(Qd[:, int(k)]), want)
-    dXh = mvk.encode(inst.key, inst.dX, inst.dexi, inst.dexv)
-    Xh = oracle.encode(inst.cx, inst.X, inst.exi, inst.exv)
-    assert np.array_equal(host(dXh), Xh)
-    dYh = mvk.server_eval(inst.dW, dXh)
-    Yh_s = oracle.server_eval(inst.W[rows], Xh)
-    assert np.array_equal(host(dYh)[:, rows], Yh_s)
-    Y, acc, _, _ = mvk.decode_verify(inst.key, dXh, dYh, inst.dexi, inst.dexv, inst.deyi, inst.deyv)
-    assert host(acc).tolist() == [1] * B
-    assert np.array_equal(host(Y)[:, rows], oracle.server_eval(inst.W[rows], inst.X))
-    bad = dYh.clone()
-    b = B // 2
-    bad[b, int(rows[1])] = (int(bad[b, int(rows[1])]) + 12345) % P
-    _, acc2, _, _ = mvk.decode_verify(inst.key, dXh, bad, inst.dexi, inst.dexv, inst.deyi, inst.deyv)
-    want = [1] * B
-    want[b] = 0
-    assert host(acc2).tolist() == want
-
-
-def test_mlp_up_11008x4096_sampled():
-    _sampled_layer_check("mlp_up_11008x4096")
-
-
-def test_mlp_large_28672x8192_sampled():
-    _sampled_layer_check("mlp_large_28672x8192", sample_rows=48)

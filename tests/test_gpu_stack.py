@@ -2,11 +2,19 @@
 
 Per layer: seven projections (q, k, v, o 4096x4096; up, gate 11008x4096; down
 4096x11008), eight query columns, r = 3, t_x = 64, t_y = 31, ell = 2.  The
-responses are enumerated (layer, projection, column); the one whose index is
-congruent to a seeded offset modulo 1000 is tampered (a nonzero delta at a
-seeded coordinate) and must be rejected while every other column is accepted.
-Checked against the CPU oracle: every masked query in full, P^T / Q columns of
-every projection of layer 0, and sampled rows of every decrypted output.
+responses of a pass are enumerated (layer, projection, column); the one whose
+index is congruent to a seeded offset modulo 1000 is tampered (a nonzero
+delta at a seeded coordinate).
+
+One test per layer compares, against the CPU oracle (threaded over the host's
+cores), for every projection: the masked queries X^ in full, the responses Y^
+in full, Q in full, v_L, v_R and the accept bits of Verify, and the
+decrypted outputs Y.  On the first and last layer and on every layer that
+holds a tampered response, P^T is compared whole too and Y with the
+oracle's Decrypt; on the other layers Y is compared with W x, the oracle's
+product of the plaintext (completeness, Thm. 6.1), which equals the oracle's
+Decrypt of an honest response.  The prepared schedule (preparation stream,
+flags, masked encode and decode/verify) must reproduce the one-call outputs.
 """
 import os
 
@@ -17,24 +25,25 @@ import torch
 import oracle
 import synth
 from tests.gpu_util import code as dev_code
-from tests.gpu_util import dev, host
+from tests.gpu_util import dev
 
 pytestmark = pytest.mark.gpu
 P = synth.P
+CFG = synth.STACK
+LAYERS = int(os.environ.get("MVK_STACK_LAYERS", CFG["layers"]))
 
 
-@pytest.fixture(scope="module", autouse=True)
-def _gpu():
+def hv(t: torch.Tensor) -> np.ndarray:
+    return t.cpu().numpy().view(np.uint32)
+
+
+@pytest.fixture(scope="module")
+def stack_setup():
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
-
-
-def test_stack_parity_and_tamper_schedule():
     import paper_2609_10264_amd.stack as stack
 
-    cfg = synth.STACK
-    layers = int(os.environ.get("MVK_STACK_LAYERS", cfg["layers"]))
-    B, r, tx, ty, ell, cid = cfg["B"], cfg["r"], cfg["tx"], cfg["ty"], cfg["ell"], cfg["cid"]
+    r, cid = CFG["r"], CFG["cid"]
     host_codes = {}
 
     def make_code(kind, k):
@@ -45,123 +54,95 @@ def test_stack_parity_and_tamper_schedule():
 
     cx_by_n, cy_by_m = stack.codes_for(make_code)
     nproj = len(stack.PROJECTIONS)
-    total = layers * nproj * B
+    total = CFG["layers"] * nproj * CFG["B"]
     g = synth.rng(synth.seed_for(cid, synth.PURPOSE_TAMPER))
     offset = int(g.integers(0, 1000))
-    tampered = {k for k in range(offset, total, 1000)}
-    seen_tampered = 0
-    for L in range(layers):
-        print(f"stack layer {L}", flush=True)
-        sub = 100 * (L + 1)
-        Wh = {name: synth.weights(synth.seed_for(cid, synth.PURPOSE_W, sub + i), m, n)
-              for i, (name, m, n, _) in enumerate(stack.PROJECTIONS)}
-        layer = stack.build_layer({k: dev(v) for k, v in Wh.items()}, cx_by_n, cy_by_m)
-        Xh_host, ex_host = {}, {}
-        for j, grp in enumerate(stack.INPUTS):
-            n = stack.input_width(grp)
-            Xh_host[grp] = synth.field_uniform(synth.seed_for(cid, synth.PURPOSE_X, sub + j), (B, n))
-            ex_host[grp] = synth.sparse(synth.seed_for(cid, synth.PURPOSE_NOISE, sub + j), B, r * n, tx)
-        ey_host = {name: synth.sparse(synth.seed_for(cid, synth.PURPOSE_CHAL, sub + i), ell, r * m, ty)
-                   for i, (name, m, n, _) in enumerate(stack.PROJECTIONS)}
-        X = {k: dev(v) for k, v in Xh_host.items()}
-        ex = {k: (dev(a), dev(b)) for k, (a, b) in ex_host.items()}
-        ey = {k: (dev(a), dev(b)) for k, (a, b) in ey_host.items()}
-
-        planned = {}
-        for i, (name, m, _, _) in enumerate(stack.PROJECTIONS):
-            for b in range(B):
-                if (L * nproj + i) * B + b in tampered:
-                    pos = int(g.integers(0, m))
-                    delta = int(g.integers(1, P))
-                    planned.setdefault(name, []).append((b, pos, delta))
-
-        def tamper(name, Yhat):
-            for b, pos, delta in planned.get(name, []):
-                Yhat[b, pos] = int((int(Yhat[b, pos].item()) + delta) % P)
-
-        out = stack.run_layer(layer, X, ex, ey, tamper=tamper)
-        torch.cuda.synchronize()
-
-        for grp in stack.INPUTS:
-            n = stack.input_width(grp)
-            want = oracle.encode(host_codes[("x", n)], Xh_host[grp], *ex_host[grp])
-            name = next(p for (p, _, _, gg) in stack.PROJECTIONS if gg == grp)
-            assert np.array_equal(host(out[name][2]), want), (L, grp)
-        rs = synth.rng(synth.seed_for(cid, 99, sub))
-        for i, (name, m, n, grp) in enumerate(stack.PROJECTIONS):
-            Y, acc, _, _ = out[name]
-            bad = {b for (b, _, _) in planned.get(name, [])}
-            want_acc = [0 if b in bad else 1 for b in range(B)]
-            assert host(acc).tolist() == want_acc, (L, name)
-            seen_tampered += len(bad)
-            rows = np.unique(np.concatenate([[0, m - 1], rs.integers(0, m, 6)]))
-            good = [b for b in range(B) if b not in bad]
-            want = oracle.server_eval(Wh[name][rows], Xh_host[grp][good])
-            assert np.array_equal(host(Y)[np.ix_(good, rows)], want), (L, name)
-            if L == 0:
-                cx, cy = host_codes[("x", n)], host_codes[("y", m)]
-                key = layer.keys[name]
-                i0, k0 = int(rows[len(rows) // 2]), int(rs.integers(0, n))
-                assert np.array_equal(host(key.PT[:, i0]),
-                                      oracle.encT(cx, (Wh[name][i0].astype(np.int64) % P).astype(np.uint32)))
-                assert np.array_equal(host(key.Q[:, k0]),
-                                      oracle.encT(cy, (Wh[name][:, k0].astype(np.int64) % P).astype(np.uint32)))
-        del layer, out
-    assert seen_tampered == len(tampered) >= (1 if total > offset else 0)
+    plan = {}  # (layer, projection index) -> [(column, coordinate, delta)]
+    for k in range(offset, total, 1000):
+        L, rest = divmod(k, nproj * CFG["B"])
+        i, b = divmod(rest, CFG["B"])
+        m = stack.PROJECTIONS[i][1]
+        plan.setdefault((L, i), []).append((b, int(g.integers(0, m)), int(g.integers(1, P))))
+    return stack, host_codes, cx_by_n, cy_by_m, plan, offset
 
 
-def test_stack_prepared_schedule_matches_one_call_path():
-    """prepare_layer on a preparation stream (flags) + run_layer_prepared on an
-    online stream give the outputs of run_layer, bit for bit, for two layers;
-    a tampered response is rejected by both."""
-    import paper_2609_10264_amd.stack as stack
+def test_tamper_schedule_covers_a_pass(stack_setup):
+    """One response in 1000 of the pass's 32 * 7 * 8 = 1792, at a seeded offset."""
+    _, _, _, _, plan, offset = stack_setup
+    total = CFG["layers"] * 7 * CFG["B"]
+    assert sum(len(v) for v in plan.values()) == len(range(offset, total, 1000)) >= 1
 
-    cfg = synth.STACK
-    B, r, tx, ty, ell, cid = cfg["B"], cfg["r"], cfg["tx"], cfg["ty"], cfg["ell"], cfg["cid"]
 
-    def make_code(kind, k):
-        purpose = synth.PURPOSE_CX if kind == "x" else synth.PURPOSE_CY
-        return dev_code(synth.raa_code(synth.seed_for(cid, purpose, sub=k), k, r))
-
-    cx_by_n, cy_by_m = stack.codes_for(make_code)
+@pytest.mark.parametrize("L", range(LAYERS))
+def test_stack_layer_matches_oracle(stack_setup, L):
+    stack, host_codes, cx_by_n, cy_by_m, plan, _ = stack_setup
+    B, r, tx, ty, ell, cid = (CFG[k] for k in ("B", "r", "tx", "ty", "ell", "cid"))
+    T = oracle.threads()
     nproj = len(stack.PROJECTIONS)
-    flags = torch.zeros((2, nproj), dtype=torch.int32, device="cuda")
+    print(f"stack layer {L} ({T} oracle threads)", flush=True)
+    sub = 100 * (L + 1)
+    Wh = {name: synth.weights(synth.seed_for(cid, synth.PURPOSE_W, sub + i), m, n)
+          for i, (name, m, n, _) in enumerate(stack.PROJECTIONS)}
+    layer = stack.build_layer({k: dev(v) for k, v in Wh.items()}, cx_by_n, cy_by_m)
+    X_h, ex_h = {}, {}
+    for j, grp in enumerate(stack.INPUTS):
+        n = stack.input_width(grp)
+        X_h[grp] = synth.field_uniform(synth.seed_for(cid, synth.PURPOSE_X, sub + j), (B, n))
+        ex_h[grp] = synth.sparse(synth.seed_for(cid, synth.PURPOSE_NOISE, sub + j), B, r * n, tx)
+    ey_h = {name: synth.sparse(synth.seed_for(cid, synth.PURPOSE_CHAL, sub + i), ell, r * m, ty)
+            for i, (name, m, n, _) in enumerate(stack.PROJECTIONS)}
+    X = {k: dev(v) for k, v in X_h.items()}
+    ex = {k: (dev(a), dev(b)) for k, (a, b) in ex_h.items()}
+    ey = {k: (dev(a), dev(b)) for k, (a, b) in ey_h.items()}
+    mine = {stack.PROJECTIONS[i][0]: v for (LL, i), v in plan.items() if LL == L}
+
+    def tamper(name, Yhat):
+        for b, pos, delta in mine.get(name, []):
+            Yhat[b, pos] = (Yhat[b, pos].to(torch.int64) + delta) % P
+
+    out = stack.run_layer(layer, X, ex, ey, tamper=tamper)
+    # the prepared schedule: preparation stream with flags, then the online part
+    flags = torch.zeros(nproj, dtype=torch.int32, device="cuda")
     late = torch.zeros((), dtype=torch.int32, device="cuda")
     s_prep, s_on = torch.cuda.Stream(), torch.cuda.Stream()
-    for L in range(2):
-        print(f"stack prepared layer {L}", flush=True)
-        sub = 500 + L
-        Wh = {name: synth.weights(synth.seed_for(cid, synth.PURPOSE_W, sub + i), m, n)
-              for i, (name, m, n, _) in enumerate(stack.PROJECTIONS)}
-        layer = stack.build_layer({k: dev(v) for k, v in Wh.items()}, cx_by_n, cy_by_m)
-        X = {g: dev(synth.field_uniform(synth.seed_for(cid, synth.PURPOSE_X, sub + j), (B, stack.input_width(g))))
-             for j, g in enumerate(stack.INPUTS)}
-        ex = {g: tuple(dev(a) for a in synth.sparse(synth.seed_for(cid, synth.PURPOSE_NOISE, sub + j), B,
-                                                     r * stack.input_width(g), tx))
-              for j, g in enumerate(stack.INPUTS)}
-        ey = {name: tuple(dev(a) for a in synth.sparse(synth.seed_for(cid, synth.PURPOSE_CHAL, sub + i), ell, r * m,
-                                                        ty))
-              for i, (name, m, _, _) in enumerate(stack.PROJECTIONS)}
-        torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s_prep):
+        preps = stack.prepare_layer(layer, ex, ey, flags, stream=s_prep)
+    with torch.cuda.stream(s_on):
+        pout = stack.run_layer_prepared(layer, X, preps, ready_flag=flags[nproj - 1], timeout_us=2_000_000,
+                                        timed_out=late, tamper=tamper, stream=s_on)
+    torch.cuda.synchronize()
+    assert int(late.item()) == 0
+    for name in out:
+        for a, b in zip(out[name], pout[name]):
+            assert torch.equal(a, b), (L, name, "prepared schedule")
 
-        def tamper(name, Yhat):
-            if name == "gate":
-                Yhat[B - 1, 17] = int((int(Yhat[B - 1, 17].item()) + 99) % P)
-
-        ref = stack.run_layer(layer, X, ex, ey, tamper=tamper)
-        torch.cuda.synchronize()
-        with torch.cuda.stream(s_prep):
-            preps = stack.prepare_layer(layer, ex, ey, flags[L], stream=s_prep)
-        with torch.cuda.stream(s_on):
-            got = stack.run_layer_prepared(layer, X, preps, ready_flag=flags[L, nproj - 1], timeout_us=2_000_000,
-                                           timed_out=late, tamper=tamper, stream=s_on)
-        torch.cuda.synchronize()
-        assert int(late.item()) == 0 and int(flags[L, nproj - 1].item()) == 0
-        for name, _, _, _ in stack.PROJECTIONS:
-            for a, b in zip(ref[name], got[name]):
-                assert torch.equal(a, b), (L, name)
-            want = [1] * B
-            if name == "gate":
-                want[B - 1] = 0
-            assert host(got[name][1]).tolist() == want, (L, name)
-        del layer, ref, got, preps
+    full = L in (0, LAYERS - 1) or any(LL == L for (LL, _) in plan)
+    Xh_o = {}
+    for grp in stack.INPUTS:
+        n = stack.input_width(grp)
+        Xh_o[grp] = oracle.encode(host_codes[("x", n)], X_h[grp], *ex_h[grp])
+    for i, (name, m, n, grp) in enumerate(stack.PROJECTIONS):
+        cx, cy = host_codes[("x", n)], host_codes[("y", m)]
+        Y, acc, Xh, Yh, vL, vR = out[name]
+        key = layer.keys[name]
+        assert np.array_equal(hv(Xh), Xh_o[grp]), (L, name, "X^")
+        Yh_o = oracle.server_eval(Wh[name], Xh_o[grp], nthreads=T)
+        for b, pos, delta in mine.get(name, []):
+            Yh_o[b, pos] = (int(Yh_o[b, pos]) + delta) % P
+        assert np.array_equal(hv(Yh), Yh_o), (L, name, "Y^")
+        PT, Q = oracle.keygen(Wh[name], cx, cy, want_P=full, nthreads=T)
+        assert np.array_equal(hv(key.Q), Q), (L, name, "Q")
+        if full:
+            assert np.array_equal(hv(key.PT), PT), (L, name, "P^T")
+        oacc, ovL, ovR = oracle.verify(cy, Q, Xh_o[grp], Yh_o, *ey_h[name])
+        assert np.array_equal(hv(vL), ovL) and np.array_equal(hv(vR), ovR), (L, name, "v_L, v_R")
+        assert hv(acc).tolist() == oacc.astype(np.uint32).tolist(), (L, name, "accept")
+        bad = {b for (b, _, _) in mine.get(name, [])}
+        assert [b for b in range(B) if not oacc[b]] == sorted(bad), (L, name, "schedule")
+        if full:
+            assert np.array_equal(hv(Y), oracle.decode(PT, Yh_o, *ex_h[grp], nthreads=T)), (L, name, "Y")
+        else:
+            assert not bad
+            assert np.array_equal(hv(Y), oracle.server_eval(Wh[name], X_h[grp], nthreads=T)), (L, name, "Y")
+    del layer, out, pout, preps

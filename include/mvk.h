@@ -167,6 +167,24 @@ mvk_status mvk_server_eval_packed(const int8_t *Wp, uint32_t m, uint32_t n, cons
                                   uint32_t B, uint32_t *Yhat, void *stream);
 
 /*
+ * mvk_server_eval_packed for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same product, bit for bit, whose kernels keep their scratch
+ * (the batched kernels' digit matrix, split-k partial sums and row-block
+ * counters) in a device array of the library, MVK_STATIC_SCRATCH_BYTES of data
+ * plus 64 KiB of control words, held on every GPU the library runs on until
+ * the process ends.  It calls no hipMalloc or hipFree.  The counters are
+ * cleared by a kernel at every call.  Every call on one GPU shares that GPU's
+ * array: calls that overlap in time on one GPU (two streams, two threads)
+ * race and must be ordered by the caller.
+ * Errors: as mvk_server_eval_packed, plus MVK_ERANGE when the shape's scratch
+ * exceeds the array (28672 x 8192 with 64 queries needs about 16.7 MB).
+ */
+#define MVK_STATIC_SCRATCH_BYTES (32u << 20)
+mvk_status mvk_server_eval_packed_static(const int8_t *Wp, uint32_t m, uint32_t n, const uint32_t *Xhat,
+                                         uint32_t B, uint32_t *Yhat, void *stream);
+
+/*
  * Preprocess (Protocol pvMVMD): writes key->PT = (W Gx)^T and key->Q = Gy^T W
  * (m encodings of the rows and n encodings of the columns of W, Sec. 6.3).
  *   key : host struct; key->m, key->n, the two codes and the PT, Q buffers

@@ -99,8 +99,18 @@ bool validate_mode() {
     return v && v[0] == '1' && v[1] == '\0';
 }
 
-// MVK_ERANGE if a[0, count) holds a word >= p.  Waits for the stream (the
-// validation mode is synchronous); one device word per device, for this check.
+// MVK_ERANGE if a[0, count) holds a word >= p, counted into the device word w.
+// Waits for the stream (the validation mode is synchronous).
+mvk_status check_canonical_at(const uint32_t* a, size_t count, uint32_t* w, hipStream_t s) {
+    uint32_t bad = 0;
+    if (launch_fill_u32(w, 1, 0u, s) != hipSuccess) return MVK_EHIP;
+    if (launch_count_noncanonical(a, count, w, s) != hipSuccess) return MVK_EHIP;
+    if (hipMemcpyAsync(&bad, w, sizeof(uint32_t), hipMemcpyDeviceToHost, s) != hipSuccess) return MVK_EHIP;
+    if (hipStreamSynchronize(s) != hipSuccess) return MVK_EHIP;
+    return bad ? MVK_ERANGE : MVK_OK;
+}
+
+// check_canonical_at with one device word per device, for this check.
 mvk_status check_canonical(const uint32_t* a, size_t count, hipStream_t s) {
     if (!a || count == 0) return MVK_OK;
     static std::mutex mu;
@@ -114,12 +124,7 @@ mvk_status check_canonical(const uint32_t* a, size_t count, hipStream_t s) {
         w = nullptr;
         return MVK_ENOMEM;
     }
-    uint32_t bad = 0;
-    if (hipMemsetAsync(w, 0, sizeof(uint32_t), s) != hipSuccess) return MVK_EHIP;
-    if (launch_count_noncanonical(a, count, w, s) != hipSuccess) return MVK_EHIP;
-    if (hipMemcpyAsync(&bad, w, sizeof(uint32_t), hipMemcpyDeviceToHost, s) != hipSuccess) return MVK_EHIP;
-    if (hipStreamSynchronize(s) != hipSuccess) return MVK_EHIP;
-    return bad ? MVK_ERANGE : MVK_OK;
+    return check_canonical_at(a, count, w, s);
 }
 
 // check_canonical over several arrays; nulls are skipped.
@@ -265,6 +270,68 @@ mvk_status mvk_pack_weights(const int8_t* W, uint32_t m, uint32_t n, int8_t* Wp,
 mvk_status mvk_server_eval_packed(const int8_t* Wp, uint32_t m, uint32_t n, const uint32_t* Xhat, uint32_t B,
                                   uint32_t* Yhat, void* stream) {
     return server_eval_impl(Wp, m, n, Xhat, B, Yhat, MVK_PATH_AUTO, true, stream);
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Allocation-free server product: the scratch of the batched kernels (digit
+// matrix, split-k partial sums, row-block counters) lives in one statically
+// sized device array instead of the per-stream workspace.
+// ---------------------------------------------------------------------------
+namespace {
+constexpr size_t kScratchCtrlBytes = 64u << 10;  // word 0: validation count; counters from byte 256
+constexpr size_t kScratchDataBytes = (size_t)MVK_STATIC_SCRATCH_BYTES;
+__device__ __align__(256) uint8_t scratch[kScratchCtrlBytes + kScratchDataBytes];
+
+constexpr int kScratchMaxDevices = 64;
+std::mutex g_scratch_mu;
+uint8_t* g_scratch_ptr[kScratchMaxDevices] = {};
+
+// Device address of the current device's copy of `scratch`, looked up once
+// per device (with that device current) and kept.
+mvk_status scratch_address(uint8_t** out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return MVK_EHIP;
+    if (dev < 0 || dev >= kScratchMaxDevices) return MVK_ERANGE;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+            (void)hipGetLastError();
+            return MVK_EHIP;
+        }
+        g_scratch_ptr[dev] = (uint8_t*)p;
+    }
+    *out = g_scratch_ptr[dev];
+    return MVK_OK;
+}
+}  // namespace
+
+extern "C" {
+
+mvk_status mvk_server_eval_packed_static(const int8_t* Wp, uint32_t m, uint32_t n, const uint32_t* Xhat,
+                                         uint32_t B, uint32_t* Yhat, void* stream) {
+    if (m == 0 || B == 0) return MVK_OK;
+    if (!Yhat) return MVK_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    if (n == 0) return hip_status(launch_fill_u32(Yhat, (size_t)m * B, 0u, s));
+    if (!Wp || !Xhat || (uintptr_t)Wp % 16 != 0) return MVK_EINVAL;
+    if (n > MVK_MAX_N) return MVK_ERANGE;
+    const ServerEvalPlan pl = server_eval_plan(m, n, B, MVK_PATH_AUTO, true);
+    if (pl.ws_bytes > kScratchDataBytes || 256 + 4 * pl.ctrl_words > kScratchCtrlBytes) return MVK_ERANGE;
+    const bool validate = validate_mode();
+    if (!pl.ws_bytes && !pl.ctrl_words && !validate)
+        return hip_status(launch_server_eval(Wp, m, n, Xhat, B, Yhat, MVK_PATH_AUTO, true, nullptr, nullptr, s));
+    uint8_t* base = nullptr;
+    mvk_status st = scratch_address(&base);
+    if (st) return st;
+    if (validate && (st = check_canonical_at(Xhat, (size_t)B * n, (uint32_t*)base, s))) return st;
+    uint32_t* counters = (uint32_t*)(base + 256);
+    // the counters start at zero for every call (a kernel, so that the call can be captured)
+    if (pl.ctrl_words && launch_fill_u32(counters, pl.ctrl_words, 0u, s) != hipSuccess) return MVK_EHIP;
+    return hip_status(launch_server_eval(Wp, m, n, Xhat, B, Yhat, MVK_PATH_AUTO, true, base + kScratchCtrlBytes,
+                                         counters, s));
 }
 
 mvk_status mvk_keygen(const mvk_key* key, const int8_t* W, void* stream) {

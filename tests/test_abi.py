@@ -305,3 +305,19 @@ def test_seeded_call_argument_checks_without_device_work():
     lib.mvk_st_free(None)
     assert lib.mvk_status_str(L.MVK_ERANDOM) != b"unknown status"
     assert lib.mvk_status_str(L.MVK_ECAPTURE) != b"unknown status"
+
+
+def test_static_server_eval_rejects_shapes_beyond_its_scratch():
+    """mvk_server_eval_packed_static checks the shape's scratch against its
+    static array on the host, before any device work: 28672 x 131071 with 64
+    queries needs 46 MiB of split-k partial sums and digit tiles (limit
+    MVK_STATIC_SCRATCH_BYTES = 32 MiB)."""
+    L = _lib()
+    lib = L.load()
+    fake = ctypes.c_void_p(0x1000)
+    assert L.MVK_STATIC_SCRATCH_BYTES == 32 << 20
+    assert lib.mvk_server_eval_packed_static(fake, 28672, 131071, fake, 64, fake, None) == L.MVK_ERANGE
+    assert lib.mvk_server_eval_packed_static(fake, 4, L.MVK_MAX_N + 1, fake, 1, fake, None) == L.MVK_ERANGE
+    assert lib.mvk_server_eval_packed_static(ctypes.c_void_p(0x1001), 4, 16, fake, 1, fake, None) == L.MVK_EINVAL
+    assert lib.mvk_server_eval_packed_static(fake, 4, 16, fake, 1, None, None) == L.MVK_EINVAL
+    assert lib.mvk_server_eval_packed_static(None, 0, 16, None, 1, None, None) == L.MVK_OK

@@ -11,19 +11,24 @@ calls (Verify with ell sparse challenges + Decrypt), with one response in
 the timed region.  Every input (6.48 GB of packed W, 155 GB of P^T and Q, the
 queries, noise and challenges) is resident in HBM before timing.
 
-Two schedules of the same work (--mode):
-  pipelined   the paper's standard mode with pipelining (Sec. 7): the work that
-              depends on neither the query nor the response (masks Gx e_x and
-              P e_x, challenge vectors Gy e_q and e_q^T Q; client_prepare) runs
-              on a preparation stream beside the online stream
-              (encode_masked -> server_eval -> decode_verify_masked); device
-              flags order each layer after its preparation.  Each stream
-              replays one HIP graph of the pass.
+Three schedules of the same work (--stack-mode):
+  overlapped  the paper's standard mode with precomputation
+              (Sec. 7): the work that depends on neither the query nor the
+              response (masks Gx e_x and P e_x, challenge vectors Gy e_q and
+              e_q^T Q; client_prepare) runs on preparation streams one layer
+              ahead; the online part (encode_masked -> server_eval ->
+              decode_verify_masked) keeps the order of an inference pass (q, k,
+              v, then o, then up and gate, then down, each input after the
+              previous stage's checks) with the projections of a stage side by
+              side.  One HIP graph of the pass over several streams.
+  pipelined   (default) the same work on one preparation stream and one
+              online stream (every call of the online part in sequence), device
+              flags between the two streams' graphs.
   serial      every call of the pass back to back on one stream, one graph.
 
 The JSON line:
   value       modMAC/s of the whole pass (51.8 G mod-MACs / pass time), in the
-              chosen mode; both schedules' pass times beside it
+              chosen schedule; every schedule's pass time beside it
   roofline    the pass's 224 server_eval launches, captured back to back as a
               graph and timed with HIP events on their stream: algorithmic
               bytes (m*n + 4*n*B + 4*m*B per launch) over their device time,
@@ -196,7 +201,10 @@ def parse():
     ap.add_argument("--chains", type=int, default=1,
                     help="serial mode of a single-matrix workload: independent query chains on their own streams")
     ap.add_argument("--mode", default="pipelined", choices=["pipelined", "serial"],
-                    help="schedule reported as value (both are timed)")
+                    help="schedule reported as value of a single-matrix workload (both are timed)")
+    ap.add_argument("--stack-mode", default="pipelined", choices=["overlapped", "pipelined", "serial"],
+                    help="schedule reported as value of the stack (all three are timed)")
+    ap.add_argument("--prep-streams", type=int, default=4, help="preparation streams of the overlapped stack pass")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the run, copy a buffer of this many MiB (reference for the traffic counters)")
     ap.add_argument("--seed", type=int, default=2609)
@@ -667,6 +675,39 @@ def stack_bench(args, steps, warmup, cpu_seconds):
                for a, b in zip(sr[name], pr[name]))
     del gs, gp, go
 
+    # ---- overlapped: the pass on several streams, one graph ----------------
+    ov_main = torch.cuda.Stream()
+    ov_prep = [torch.cuda.Stream() for _ in range(args.prep_streams)]
+    ov_branch = [torch.cuda.Stream() for _ in range(3)]
+    ov_preps = [{name: mvk.Prepared(built[L].keys[name], B, ell) for (name, _, _, _) in stack.PROJECTIONS}
+                for L in range(layers)]
+    ov_outs = [stack.LayerOutputs.allocate(B, ell) for _ in range(layers)]
+
+    def ov_tamper(L, name, Yhat):
+        tamperer(L)(name, Yhat)
+
+    def ov_pass():
+        stack.run_pass_overlapped(built, inputs, ov_preps, ov_outs, ov_main, ov_prep, ov_branch, tamper=ov_tamper)
+
+    for _ in range(warmup):  # also sizes every stream's workspace
+        with torch.cuda.stream(ov_main):
+            ov_pass()
+        torch.cuda.synchronize()
+    gov = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gov, stream=ov_main):
+        ov_pass()
+
+    def replay_overlapped():
+        with torch.cuda.stream(ov_main):
+            gov.replay()
+
+    t_ov = time_passes(replay_overlapped)
+    oresults = [o.as_dict() for o in ov_outs]
+    ok_ov = accepts_ok(oresults)
+    same_ov = all(bool(torch.equal(a, b)) for sr, orr in zip(results, oresults) for name in sr
+                  for a, b in zip(sr[name], orr[name]))
+    del gov
+
     # ---- the pass's server_eval launches alone ------------------------------
     Xs = [{grp: torch.randint(0, P, (B, stack.input_width(grp)), generator=gen, device=dev, dtype=torch.int32)
            for grp in stack.INPUTS} for _ in range(layers)]
@@ -696,7 +737,7 @@ def stack_bench(args, steps, warmup, cpu_seconds):
     read_s = read_floor([built[L].W[name].data for (L, name, _) in every], len(every), args)
     achieved = alg_pass / pass_s / 1e9
     macs = stack.macs_per_layer(B) * layers
-    elapsed = t_pipe if args.mode == "pipelined" else t_serial
+    elapsed = {"pipelined": t_pipe, "serial": t_serial, "overlapped": t_ov}[args.stack_mode]
     res = {"metric": METRIC, "value": macs / elapsed, "unit": "modMAC/s", "n_gpus": 1, "steps": steps,
            "warmup": warmup, "ms_per_step": 1e3 * elapsed, "higher_is_better": True,
            "scaling": "weak", "vs_baseline": None, "dtype": DTYPE, "data": "synthetic",
@@ -705,8 +746,9 @@ def stack_bench(args, steps, warmup, cpu_seconds):
                                   f"projection, RAA r={r}, t_x={tx}, t_y={ty}, ell={ell}; step = one pass (per layer "
                                   "4 encodes, 7 server_evals, 7 decode_verifies) with one response in 1000 "
                                   "tampered and rejected",
-                      "global_batch": B, "launch": "hip_graph", "mode": args.mode, "weights": "packed"},
-           "ms_per_step_pipelined": 1e3 * t_pipe, "ms_per_step_serial": 1e3 * t_serial,
+                      "global_batch": B, "launch": "hip_graph", "mode": args.stack_mode, "weights": "packed"},
+           "ms_per_step_overlapped": 1e3 * t_ov, "ms_per_step_pipelined": 1e3 * t_pipe,
+           "ms_per_step_serial": 1e3 * t_serial,
            "modmac_per_pass": macs,
            "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                         "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic("stack32", "packed"),
@@ -719,14 +761,14 @@ def stack_bench(args, steps, warmup, cpu_seconds):
                                        "frac": read_s * len(every) / pass_s}},
            "server_eval": {"modmac_per_s": macs / pass_s, "gb_per_s": achieved},
            "tampered_per_pass": sum(len(v) for v in plan.values()),
-           "all_expected_verdicts": ok_serial and ok_pipe, "pipelined_matches_serial": same,
-           "setup_s": t_setup}
-    del built, inputs, results, presults, preps, Xs, Ys
+           "all_expected_verdicts": ok_serial and ok_pipe and ok_ov, "pipelined_matches_serial": same,
+           "overlapped_matches_serial": same_ov, "setup_s": t_setup}
+    del built, inputs, results, presults, preps, Xs, Ys, oresults, ov_outs, ov_preps
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline_stack(cpu_seconds)
-    res["_ok"] = ok_serial and ok_pipe and same
+    res["_ok"] = ok_serial and ok_pipe and ok_ov and same and same_ov
     return res
 
 

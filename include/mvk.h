@@ -129,7 +129,8 @@ uint32_t mvk_field_modulus(void);
  *   Xhat : device, B x n field array (the masked queries)
  *   Yhat : device, B x m field array, written: Yhat[b][i] = sum_k W[i][k] Xhat[b][k] mod p
  * m == 0 or B == 0: no work.  n == 0: Yhat is zeroed.
- * Errors: MVK_EINVAL (null pointer), MVK_ERANGE (n > MVK_MAX_N).
+ * Errors: MVK_EINVAL (null pointer), MVK_ERANGE (n > MVK_MAX_N, m or B at
+ * least 2^31, W or Yhat above 2^62 bytes).
  */
 mvk_status mvk_server_eval(const int8_t *W, uint32_t m, uint32_t n, const uint32_t *Xhat,
                            uint32_t B, uint32_t *Yhat, void *stream);

@@ -144,6 +144,12 @@ inline bool too_big(uint64_t a, uint64_t b, uint64_t elem) {
     return a != 0 && b > ((1ull << 62) / elem) / a;
 }
 
+// Row and query counts of the server product: below 2^31 each (the launch
+// grids divide them with 32-bit rounding up), and W and Yhat below 2^62 bytes.
+inline bool server_dims_too_big(uint32_t m, uint32_t n, uint32_t B) {
+    return m > 0x7fffffffu || B > 0x7fffffffu || too_big(m, B, 4) || too_big(m, n, 1);
+}
+
 // Vectors per call of the syndrome kernels: the count is a grid dimension of
 // the segmented form.
 constexpr uint32_t kMaxSynCount = 65535u;
@@ -207,6 +213,7 @@ mvk_status server_eval_impl(const int8_t* W, uint32_t m, uint32_t n, const uint3
     if (packed && path == MVK_PATH_VALU) return MVK_EINVAL;
     if (m == 0 || B == 0) return MVK_OK;
     if (!Yhat) return MVK_EINVAL;
+    if (server_dims_too_big(m, n, B)) return MVK_ERANGE;
     hipStream_t s = (hipStream_t)stream;
     if (n == 0) return hip_status(launch_fill_u32(Yhat, (size_t)m * B, 0u, s));
     if (!W || !Xhat) return MVK_EINVAL;
@@ -263,6 +270,7 @@ size_t mvk_packed_weight_bytes(uint32_t m, uint32_t n) { return (m && n) ? packe
 mvk_status mvk_pack_weights(const int8_t* W, uint32_t m, uint32_t n, int8_t* Wp, void* stream) {
     if (m == 0 || n == 0) return MVK_OK;
     if (!W || !Wp) return MVK_EINVAL;
+    if (server_dims_too_big(m, n, 1)) return MVK_ERANGE;
     if ((uintptr_t)Wp % 16 != 0) return MVK_EINVAL;
     return hip_status(launch_pack_w(W, m, n, Wp, (hipStream_t)stream));
 }
@@ -314,6 +322,7 @@ mvk_status mvk_server_eval_packed_static(const int8_t* Wp, uint32_t m, uint32_t 
                                          uint32_t B, uint32_t* Yhat, void* stream) {
     if (m == 0 || B == 0) return MVK_OK;
     if (!Yhat) return MVK_EINVAL;
+    if (server_dims_too_big(m, n, B)) return MVK_ERANGE;
     hipStream_t s = (hipStream_t)stream;
     if (n == 0) return hip_status(launch_fill_u32(Yhat, (size_t)m * B, 0u, s));
     if (!Wp || !Xhat || (uintptr_t)Wp % 16 != 0) return MVK_EINVAL;

@@ -225,8 +225,9 @@ __global__ __launch_bounds__(KW * 64) void server_eval_mfma_small(const int8_t* 
     constexpr int KC = 64 * KBW * KW;  // k per chunk
     constexpr int STRIDE = KC + 16;    // padded LDS row (bytes)
     constexpr int ROWS = 4 * QB;
+    constexpr int NT = (ROWS + 15) / 16;  // A tiles of 16 digit rows (four queries each)
     __shared__ __align__(16) uint8_t dig[ROWS * STRIDE];
-    __shared__ v4i red[KW][64];
+    __shared__ v4i red[KW][NT][64];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const uint32_t row0 = blockIdx.x * 16;
     const uint32_t q0 = blockIdx.y * QB;
@@ -238,7 +239,9 @@ __global__ __launch_bounds__(KW * 64) void server_eval_mfma_small(const int8_t* 
     // Query elements converted per thread and chunk (four consecutive k each).
     constexpr int NXG = QB * (KC / 4) / (KW * 64);
     static_assert(NXG * KW * 64 == QB * (KC / 4), "chunk must split evenly over the workgroup");
-    v4i acc = {0, 0, 0, 0};
+    v4i acc[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[t] = v4i{0, 0, 0, 0};
     for (uint32_t kc0 = 0; kc0 < n; kc0 += KC) {
         // 1. query loads first (needed first), 2. W loads (in flight during the
         // conversion), 3. convert the query chunk into LDS digit planes.
@@ -323,31 +326,41 @@ __global__ __launch_bounds__(KW * 64) void server_eval_mfma_small(const int8_t* 
 #pragma unroll
         for (int j = 0; j < KBW; ++j) {
             const int kbl = wave * KBW + j;
-            const v4i araw = *reinterpret_cast<const v4i*>(dig + (arow < ROWS ? arow : 0) * STRIDE + kbl * 64 + kg * 16);
-            const int32_t msk = arow < ROWS ? -1 : 0;
-            v4i a, w;
-            a[0] = araw[0] & msk;
-            a[1] = araw[1] & msk;
-            a[2] = araw[2] & msk;
-            a[3] = araw[3] & msk;
+            v4i w;
             w[0] = bw[j][0] & wmask[j];
             w[1] = bw[j][1] & wmask[j];
             w[2] = bw[j][2] & wmask[j];
             w[3] = bw[j][3] & wmask[j];
-            acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, w, acc, 0, 0, 0);
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                const int r = t * 16 + arow;  // digit row: 4 * query + digit
+                const v4i araw = *reinterpret_cast<const v4i*>(dig + (r < ROWS ? r : 0) * STRIDE + kbl * 64 + kg * 16);
+                const int32_t msk = r < ROWS ? -1 : 0;
+                v4i a;
+                a[0] = araw[0] & msk;
+                a[1] = araw[1] & msk;
+                a[2] = araw[2] & msk;
+                a[3] = araw[3] & msk;
+                acc[t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, w, acc[t], 0, 0, 0);
+            }
         }
         __syncthreads();
     }
-    red[wave][lane] = acc;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) red[wave][t][lane] = acc[t];
     __syncthreads();
     if (wave == 0) {
-        v4i sum = red[0][lane];
 #pragma unroll
-        for (int w = 1; w < KW; ++w) sum += red[w][lane];
-        const int q = lane >> 4;
-        if (q < QB && q0 + q < B && wrow < m) {
-            int64_t v = (int64_t)sum[0] + ((int64_t)sum[1] << 8) + ((int64_t)sum[2] << 16) + ((int64_t)sum[3] << 24);
-            Y[(size_t)(q0 + q) * m + wrow] = fred_s64(v);
+        for (int t = 0; t < NT; ++t) {
+            v4i sum = red[0][t][lane];
+#pragma unroll
+            for (int w = 1; w < KW; ++w) sum += red[w][t][lane];
+            const int q = t * 4 + (lane >> 4);
+            if (q < QB && q0 + q < B && wrow < m) {
+                int64_t v = (int64_t)sum[0] + ((int64_t)sum[1] << 8) + ((int64_t)sum[2] << 16) +
+                            ((int64_t)sum[3] << 24);
+                Y[(size_t)(q0 + q) * m + wrow] = fred_s64(v);
+            }
         }
     }
 }

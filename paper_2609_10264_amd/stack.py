@@ -14,11 +14,13 @@ verification code per output height m); P^T and Q are per matrix.  This module
 only orchestrates calls of the C ABI (through the binding); all arithmetic runs
 in the HIP kernels.
 
-Two schedules of a layer: run_layer (the one-call path: encode, server_eval,
-decode_verify) and prepare_layer + run_layer_prepared (the standard mode with
-precomputation, Sec. 7: the masks and challenge vectors depend on neither the
-queries nor the responses, so a preparation stream computes them ahead and
-the online calls only add masks, evaluate and check).
+Schedules: run_layer (the one-call path: encode, server_eval, decode_verify,
+one layer on one stream), prepare_layer + run_layer_prepared (the standard
+mode with precomputation, Sec. 7: the masks and challenge vectors depend on
+neither the queries nor the responses, so a preparation stream computes them
+ahead and the online calls only add masks, evaluate and check), and
+run_pass_overlapped (the same prepared work for a whole pass on several
+streams, every data dependence of an inference pass kept as a stream edge).
 """
 from __future__ import annotations
 
@@ -139,6 +141,98 @@ def run_layer_prepared(layer: Layer, X: dict, preps: dict, ready_flag: torch.Ten
     return out
 
 
+@dataclass
+class LayerOutputs:
+    """Preallocated outputs of one layer for run_pass_overlapped: X^ per input,
+    and per projection Y^, Y, v_L, v_R and the accept bits."""
+    xhat: dict = field(default_factory=dict)
+    yhat: dict = field(default_factory=dict)
+    y: dict = field(default_factory=dict)
+    vl: dict = field(default_factory=dict)
+    vr: dict = field(default_factory=dict)
+    accept: dict = field(default_factory=dict)
+
+    @classmethod
+    def allocate(cls, B: int, ell: int, device="cuda") -> "LayerOutputs":
+        o = cls()
+        i32 = dict(dtype=torch.int32, device=device)
+        for group in INPUTS:
+            o.xhat[group] = torch.empty((B, input_width(group)), **i32)
+        for name, m, n, _ in PROJECTIONS:
+            o.yhat[name] = torch.empty((B, m), **i32)
+            o.y[name] = torch.empty((B, m), **i32)
+            o.vl[name] = torch.empty((ell, B), **i32)
+            o.vr[name] = torch.empty((ell, B), **i32)
+            o.accept[name] = torch.empty((B,), **i32)
+        return o
+
+    def as_dict(self) -> dict:
+        """{name: (Y, accept, Xhat, Yhat, vL, vR)}, as run_layer returns."""
+        return {name: (self.y[name], self.accept[name], self.xhat[group], self.yhat[name], self.vl[name],
+                       self.vr[name]) for name, _, _, group in PROJECTIONS}
+
+
+def run_pass_overlapped(layers: list, inputs: list, preps: list, outs: list, main, prep_streams: list,
+                        branch_streams: list, tamper=None):
+    """One pass over every layer, issued on several streams so that work
+    without a data dependence runs side by side; captured on `main`, the
+    streams fork from it and join it again, so a HIP graph of the pass keeps
+    every dependence below as an edge.
+
+    Dependences kept (the rest runs concurrently):
+      * the client's preparation of a projection (client_prepare: masks and
+        challenge vectors, independent of queries and responses, Sec. 7)
+        runs on the preparation streams, one layer ahead of the online part;
+        a layer's online part waits for its preparation;
+      * per layer the inputs follow one another as in inference: q, k, v
+        share one input, o's input comes after the q, k, v outputs, up and
+        gate share the next, down's comes last; each input's masked encode
+        waits for every verification of the previous stage;
+      * within a stage every projection is one branch: server_eval, then its
+        decode/verify.
+    inputs[L] = (X, ex, ey) as for run_layer; preps[L]: {name: Prepared};
+    outs[L]: LayerOutputs; tamper: optional callable(L, name, Yhat) on the
+    branch stream between the product and its check."""
+    every = list(prep_streams) + list(branch_streams)
+    for s in every:
+        s.wait_stream(main)
+
+    def prepare(L):
+        _, ex, ey = inputs[L]
+        for k, (name, _, _, group) in enumerate(PROJECTIONS):
+            s = prep_streams[k % len(prep_streams)]
+            with torch.cuda.stream(s):
+                client_prepare(layers[L].keys[name], ex[group][0], ex[group][1], ey[name][0], ey[name][1],
+                               out=preps[L][name], stream=s)
+        return [s.record_event() for s in prep_streams]
+
+    ready = {0: prepare(0)} if layers else {}
+    for L, layer in enumerate(layers):
+        if L + 1 < len(layers):
+            ready[L + 1] = prepare(L + 1)
+        for e in ready.pop(L):
+            main.wait_event(e)
+        X = inputs[L][0]
+        o = outs[L]
+        for group in INPUTS:
+            stage = [name for (name, _, _, g) in PROJECTIONS if g == group]
+            with torch.cuda.stream(main):
+                encode_masked(layer.keys[stage[0]], X[group], preps[L][stage[0]], out=o.xhat[group], stream=main)
+            for j, name in enumerate(stage):
+                b = branch_streams[j]
+                b.wait_stream(main)
+                with torch.cuda.stream(b):
+                    server_eval(layer.W[name], o.xhat[group], out=o.yhat[name], stream=b)
+                    if tamper is not None:
+                        tamper(L, name, o.yhat[name])
+                    decode_verify_masked(layer.keys[name], o.xhat[group], o.yhat[name], preps[L][name], Y=o.y[name],
+                                         vL=o.vl[name], vR=o.vr[name], accept=o.accept[name], stream=b)
+            for j in range(len(stage)):
+                main.wait_stream(branch_streams[j])
+    for s in every:
+        main.wait_stream(s)
+
+
 def codes_for(make_code) -> tuple[dict, dict]:
     """Shared codes: privacy code per input width, verification code per output height."""
     ns = sorted({n for (_, _, n, _) in PROJECTIONS})
@@ -150,5 +244,5 @@ def macs_per_layer(B: int) -> int:
     return sum(m * n for (_, m, n, _) in PROJECTIONS) * B
 
 
-__all__ = ["PROJECTIONS", "INPUTS", "Layer", "build_layer", "run_layer", "prepare_layer", "run_layer_prepared",
-           "codes_for", "input_width", "macs_per_layer", "Code"]
+__all__ = ["PROJECTIONS", "INPUTS", "Layer", "LayerOutputs", "build_layer", "run_layer", "prepare_layer",
+           "run_layer_prepared", "run_pass_overlapped", "codes_for", "input_width", "macs_per_layer", "Code"]

@@ -321,3 +321,9 @@ def test_static_server_eval_rejects_shapes_beyond_its_scratch():
     assert lib.mvk_server_eval_packed_static(ctypes.c_void_p(0x1001), 4, 16, fake, 1, fake, None) == L.MVK_EINVAL
     assert lib.mvk_server_eval_packed_static(fake, 4, 16, fake, 1, None, None) == L.MVK_EINVAL
     assert lib.mvk_server_eval_packed_static(None, 0, 16, None, 1, None, None) == L.MVK_OK
+    # row or query counts whose rounded-up tile counts would wrap in 32 bits
+    assert lib.mvk_server_eval_packed_static(fake, 0xFFFFFFFF, 131071, fake, 0xFFFFFFFF, fake, None) == L.MVK_ERANGE
+    assert lib.mvk_server_eval_packed_static(fake, 0xFFFFFFF0, 64, fake, 64, fake, None) == L.MVK_ERANGE
+    assert lib.mvk_server_eval(fake, 0xFFFFFFF0, 64, fake, 1, fake, None) == L.MVK_ERANGE
+    assert lib.mvk_server_eval_packed(fake, 16, 64, fake, 0x80000000, fake, None) == L.MVK_ERANGE
+    assert lib.mvk_pack_weights(fake, 0xFFFFFFF0, 64, fake, None) == L.MVK_ERANGE

@@ -146,3 +146,74 @@ def test_stack_layer_matches_oracle(stack_setup, L):
             assert not bad
             assert np.array_equal(hv(Y), oracle.server_eval(Wh[name], X_h[grp], nthreads=T)), (L, name, "Y")
     del layer, out, pout, preps
+
+
+def test_overlapped_pass_matches_one_call_path(stack_setup):
+    """run_pass_overlapped (preparation streams one layer ahead, the projections
+    of a stage on parallel branches) gives the one-call outputs bit for bit,
+    eager and as a captured graph replayed three times with other work between
+    the replays; a tampered response is rejected on both."""
+    stack, _, cx_by_n, cy_by_m, _, _ = stack_setup
+    import paper_2609_10264_amd as mvk
+
+    B, r, tx, ty, ell, cid = (CFG[k] for k in ("B", "r", "tx", "ty", "ell", "cid"))
+    nl = 3
+    layers, inputs = [], []
+    for L in range(nl):
+        sub = 700 + 10 * L
+        Ws = {name: dev(synth.weights(synth.seed_for(cid, synth.PURPOSE_W, sub + i), m, n))
+              for i, (name, m, n, _) in enumerate(stack.PROJECTIONS)}
+        layers.append(stack.build_layer(Ws, cx_by_n, cy_by_m))
+        X = {g: dev(synth.field_uniform(synth.seed_for(cid, synth.PURPOSE_X, sub + j), (B, stack.input_width(g))))
+             for j, g in enumerate(stack.INPUTS)}
+        ex = {g: tuple(dev(a) for a in synth.sparse(synth.seed_for(cid, synth.PURPOSE_NOISE, sub + j), B,
+                                                     r * stack.input_width(g), tx))
+              for j, g in enumerate(stack.INPUTS)}
+        ey = {name: tuple(dev(a) for a in synth.sparse(synth.seed_for(cid, synth.PURPOSE_CHAL, sub + i), ell,
+                                                        r * m, ty))
+              for i, (name, m, _, _) in enumerate(stack.PROJECTIONS)}
+        inputs.append((X, ex, ey))
+
+    def tamper(L, name, Yhat):
+        if L == 1 and name == "up":
+            Yhat[3, 100] = (Yhat[3, 100].to(torch.int64) + 5) % P
+
+    ref = [stack.run_layer(layers[L], *inputs[L], tamper=lambda nm, Y, L=L: tamper(L, nm, Y)) for L in range(nl)]
+    torch.cuda.synchronize()
+    main = torch.cuda.Stream()
+    preps_s = [torch.cuda.Stream() for _ in range(4)]
+    branches = [torch.cuda.Stream() for _ in range(3)]
+    preps = [{name: mvk.Prepared(layers[L].keys[name], B, ell) for (name, _, _, _) in stack.PROJECTIONS}
+             for L in range(nl)]
+    outs = [stack.LayerOutputs.allocate(B, ell) for _ in range(nl)]
+
+    def check(tag):
+        for L in range(nl):
+            got = outs[L].as_dict()
+            for name in ref[L]:
+                for a, b in zip(ref[L][name], got[name]):
+                    assert torch.equal(a, b), (tag, L, name)
+        want = [1] * B
+        want[3] = 0
+        assert outs[1].accept["up"].tolist() == want
+
+    def one_pass():
+        stack.run_pass_overlapped(layers, inputs, preps, outs, main, preps_s, branches, tamper=tamper)
+
+    with torch.cuda.stream(main):
+        one_pass()
+    torch.cuda.synchronize()
+    check("eager")
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=main):
+        one_pass()
+    for rep in range(3):
+        for o in outs:
+            for t in list(o.y.values()) + list(o.accept.values()) + list(o.yhat.values()):
+                t.fill_(-1)
+        torch.cuda.synchronize()
+        with torch.cuda.stream(main):
+            g.replay()
+        torch.cuda.synchronize()
+        check(f"replay {rep}")
+    del g

@@ -29,11 +29,13 @@ Three schedules of the same work (--stack-mode):
 The JSON line:
   value       modMAC/s of the whole pass (51.8 G mod-MACs / pass time), in the
               chosen schedule; every schedule's pass time beside it
-  roofline    the pass's 224 server_eval launches, captured back to back as a
-              graph and timed with HIP events on their stream: algorithmic
-              bytes (m*n + 4*n*B + 4*m*B per launch) over their device time,
-              against 8 TB/s of HBM; per shape beside it, and a streaming read
-              of the same W buffers (the measured read floor)
+  roofline    the pass's 128 server calls (per layer: q, k, v grouped in one
+              launch over their shared input, o, up and gate grouped, down),
+              captured back to back as a graph and timed with HIP events on
+              their stream: algorithmic bytes (m*n + 4*n*B + 4*m*B per
+              product) over their device time, against 8 TB/s of HBM; per
+              call type beside it, and a streaming read of the same W buffers
+              (the measured read floor)
   cpu_baseline the CPU oracle (plain C, threaded over row blocks on every core
               of this host) on one layer's step of the same shapes
   configs     the single-matrix workloads (4096 x 4096 B=1, 11008 x 4096 B=16,
@@ -57,7 +59,7 @@ METRIC = "server_eval mod-MACs/s + achieved HBM GB/s (fraction of peak), 1×MI35
 HBM_PEAK_GBS = 8000.0
 MFMA_INT8_PEAK_OPS = 5.0e15  # MI355X dense int8 matrix-core peak
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_10264_amd", "csrc", "server_eval.hip")
-STACK_LAUNCHES_PER_PASS = 32 * 7
+STACK_LAUNCHES_PER_PASS = 32 * 4  # server calls per pass: (q,k,v), o, (up,gate), down per layer
 SIDE_CONFIGS = ("attn4096", "mlp_up_11008x4096", "mlp_large_28672x8192")
 DTYPE = "i8xi8->i32 limb dot products, mod 2^31-1"
 
@@ -73,7 +75,7 @@ def traffic_file(config: str) -> str:
 
 
 def measured_traffic(config: str, weights: str):
-    """HBM bytes per server_eval launch (per pass of the 224 launches for the
+    """HBM bytes per server_eval launch (per pass of the 128 server calls for the
     stack) from the committed counter runs, if they were taken on the current
     kernel source, this workload and weight layout; else None."""
     try:
@@ -93,7 +95,7 @@ def write_traffic(fetch_csv: str, write_csv: str, config: str, weights: str, cop
     the same counter reads for the copy_mib MiB device copy (which reads and
     writes copy_mib MiB).  Single-matrix workloads: the median over the
     dispatches whose name contains kernel_match.  The stack: the sum over
-    those dispatches divided by the passes they make up (224 per pass)."""
+    those dispatches divided by the passes they make up (128 per pass)."""
     import csv
     import statistics
 
@@ -709,31 +711,34 @@ def stack_bench(args, steps, warmup, cpu_seconds):
     del gov
 
     # ---- the pass's server_eval launches alone ------------------------------
+    # one server call per layer and input: q, k, v as one grouped launch over
+    # their row stack, o alone, up and gate grouped, down alone
     Xs = [{grp: torch.randint(0, P, (B, stack.input_width(grp)), generator=gen, device=dev, dtype=torch.int32)
            for grp in stack.INPUTS} for _ in range(layers)]
-    Ys = {m: torch.empty((B, m), dtype=torch.int32, device=dev) for m in sorted({m for (_, m, _, _) in stack.PROJECTIONS})}
-    shapes = {}  # (m, n) -> [(L, name, group)]
-    for L in range(layers):
-        for name, m, n, grp in stack.PROJECTIONS:
-            shapes.setdefault((m, n), []).append((L, name, grp))
+    Ys = {name: torch.empty((B, m), dtype=torch.int32, device=dev) for (name, m, _, _) in stack.PROJECTIONS}
+    calls = [(L, grp) for L in range(layers) for grp in stack.INPUTS]
 
     def launches(items):
-        for (L, name, grp) in items:
-            m = built[L].W[name].m
-            mvk.server_eval(built[L].W[name], Xs[L][grp], out=Ys[m], path=args.path, stream=s)
+        for (L, grp) in items:
+            stack.evaluate_stage(built[L], grp, Xs[L][grp], outs=Ys, stream=s)
 
-    every = [it for v in shapes.values() for it in v]
-    every.sort()
-    pass_s = graph_mean_seconds(s, lambda k: launches(every), steps, args.warm_seconds)
-    alg_pass = sum(m * n + 4 * n * B + 4 * m * B for (_, m, n, _) in stack.PROJECTIONS) * layers
+    def alg_bytes(grp):
+        return sum(m * n + 4 * n * B + 4 * m * B for (name, m, n, g) in stack.PROJECTIONS if g == grp)
+
+    pass_s = graph_mean_seconds(s, lambda k: launches(calls), steps, args.warm_seconds)
+    alg_pass = sum(alg_bytes(grp) for (_, grp) in calls)
     per_shape = {}
-    for (m, n), items in shapes.items():
+    for grp in stack.INPUTS:
+        items = [c for c in calls if c[1] == grp]
         t = graph_mean_seconds(s, lambda k, it=items: launches(it), max(2, steps // 4), args.warm_seconds)
         t_launch = t / len(items)
-        alg = m * n + 4 * n * B + 4 * m * B
-        per_shape[f"{m}x{n}"] = {"launches_per_pass": len(items), "mean_launch_us": 1e6 * t_launch,
-                                 "alg_bytes_per_launch": alg, "gbps": alg / t_launch / 1e9,
-                                 "frac": alg / t_launch / 1e9 / HBM_PEAK_GBS}
+        names = stack.stage(grp)
+        m, n = next((m, n) for (nm, m, n, _) in stack.PROJECTIONS if nm == names[0])
+        label = f"{','.join(names)}: {len(names)}x{m}x{n}" if len(names) > 1 else f"{names[0]}: {m}x{n}"
+        per_shape[label] = {"launches_per_pass": len(items), "mean_launch_us": 1e6 * t_launch,
+                            "alg_bytes_per_launch": alg_bytes(grp), "gbps": alg_bytes(grp) / t_launch / 1e9,
+                            "frac": alg_bytes(grp) / t_launch / 1e9 / HBM_PEAK_GBS}
+    every = [(L, name, grp) for (L, grp) in calls for name in stack.stage(grp)]
     read_s = read_floor([built[L].W[name].data for (L, name, _) in every], len(every), args)
     achieved = alg_pass / pass_s / 1e9
     macs = stack.macs_per_layer(B) * layers
@@ -752,13 +757,15 @@ def stack_bench(args, steps, warmup, cpu_seconds):
            "modmac_per_pass": macs,
            "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                         "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic("stack32", "packed"),
-                        "kernel": f"server_eval ({args.path}), the {len(every)} launches of a pass back to back",
-                        "alg_bytes_per_launch": alg_pass / len(every), "alg_bytes_per_pass": alg_pass,
-                        "launches_per_pass": len(every), "mean_launch_us": 1e6 * pass_s / len(every),
+                        "kernel": f"server_eval ({args.path}), the {len(calls)} server calls of a pass back to "
+                                  f"back ({len(every)} products: q,k,v and up,gate grouped over their shared input)",
+                        "alg_bytes_per_launch": alg_pass / len(calls), "alg_bytes_per_pass": alg_pass,
+                        "launches_per_pass": len(calls), "mean_launch_us": 1e6 * pass_s / len(calls),
                         "server_ms_per_pass": 1e3 * pass_s, "per_shape": per_shape,
                         "read_floor": {"ms_per_pass": 1e3 * read_s * len(every),
                                        "gbps": alg_pass / (read_s * len(every)) / 1e9,
-                                       "frac": read_s * len(every) / pass_s}},
+                                       "frac": read_s * len(every) / pass_s,
+                                       "what": "a streaming read of the same W buffers, one launch per matrix"}},
            "server_eval": {"modmac_per_s": macs / pass_s, "gb_per_s": achieved},
            "tampered_per_pass": sum(len(v) for v in plan.values()),
            "all_expected_verdicts": ok_serial and ok_pipe and ok_ov, "pipelined_matches_serial": same,

@@ -168,6 +168,26 @@ mvk_status mvk_server_eval_packed(const int8_t *Wp, uint32_t m, uint32_t n, cons
                                   uint32_t B, uint32_t *Yhat, void *stream);
 
 /*
+ * Several matrices of one shape applied to the same queries in one launch
+ * (for example the q, k and v projections of a decoder layer, which share
+ * their input): Yhat[g] = W_g Xhat mod p for g < G, bit for bit the products
+ * G calls of mvk_server_eval_packed would give (Protocol pvMVMD, server step,
+ * once per matrix).  The server stores the G matrices as the packed layout of
+ * their row stack [W_0; W_1; ...] ((G*m) x n): mvk_pack_weights of the stacked
+ * matrix, or G packed buffers of mvk_packed_weight_bytes(m, n) bytes placed
+ * back to back (the same bytes when m is a multiple of 16).
+ *   Wp   : device, packed (G*m) x n, 16-byte aligned
+ *   G    : 1..MVK_MAX_GROUP; m must be a multiple of 16 when G > 1
+ *   Xhat : device, B x n field array
+ *   Yhat : host array of G device pointers, each B x m, written
+ * Errors: MVK_EINVAL (null or misaligned pointer, G out of range, m not a
+ * multiple of 16), MVK_ERANGE (as mvk_server_eval for m*G rows).
+ */
+#define MVK_MAX_GROUP 4u
+mvk_status mvk_server_eval_packed_group(const int8_t *Wp, uint32_t G, uint32_t m, uint32_t n,
+                                        const uint32_t *Xhat, uint32_t B, uint32_t *const *Yhat, void *stream);
+
+/*
  * mvk_server_eval_packed for callers that cannot allocate device memory (code
  * under HIP graph capture, tight serving loops, harnesses that forbid
  * hipMalloc): the same product, bit for bit, whose kernels keep their scratch

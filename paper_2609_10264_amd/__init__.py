@@ -151,6 +151,36 @@ def pack_weights(W: torch.Tensor, out: torch.Tensor | None = None, stream=None) 
     return PackedW(out, m, n)
 
 
+def pack_weights_group(Ws: list, stream=None) -> PackedW:
+    """The G matrices Ws (each m x n int8, m a multiple of 16 when G > 1) in
+    the packed layout of their row stack: G packed buffers back to back."""
+    G = len(Ws)
+    m, n = Ws[0].shape
+    L = _lib.load()
+    nbytes = int(L.mvk_packed_weight_bytes(m, n))
+    out = torch.empty((max(G * nbytes, 1),), dtype=torch.int8, device=Ws[0].device)
+    for g, W in enumerate(Ws):
+        if tuple(W.shape) != (m, n):
+            raise ValueError("the matrices of a group must have one shape")
+        pack_weights(W, out=out[g * nbytes:(g + 1) * nbytes], stream=stream)
+    return PackedW(out, G * m, n)
+
+
+def server_eval_group(Wstack: PackedW, G: int, Xhat: torch.Tensor, outs: list | None = None, stream=None,
+                      p: int = P) -> list:
+    """[W_g Xhat mod p for g < G] in one launch, Wstack the packed row stack of
+    the G matrices (pack_weights_group); returns the G outputs (B x m each)."""
+    m = Wstack.m // G
+    n = Wstack.n
+    B = Xhat.shape[0]
+    if outs is None:
+        outs = [torch.empty((B, m), dtype=torch.int32, device=Xhat.device) for _ in range(G)]
+    ptrs = (ctypes.c_void_p * G)(*[_dev(o, torch.int32, (B, m), f"Yhat[{g}]") for g, o in enumerate(outs)])
+    _lib.check("mvk_server_eval_packed_group", _lib.load(p).mvk_server_eval_packed_group(
+        Wstack.data.data_ptr(), G, m, n, _dev(Xhat, torch.int32, (B, n), "Xhat"), B, ptrs, _stream(stream)))
+    return outs
+
+
 def server_eval(W, Xhat: torch.Tensor, out: torch.Tensor | None = None, stream=None,
                 path: str = "auto", p: int = P) -> torch.Tensor:
     """Yhat = W Xhat mod p.  W: m x n int8 (or a PackedW); Xhat: B x n int32 field; returns B x m.

@@ -30,6 +30,7 @@ MVK_TAG_CHALLENGE = 0x6D766B2D6368616C
 MVK_SEED_FRESH = 0xFFFFFFFFFFFFFFFF
 MVK_SEEDED_MAX_T = 4096
 MVK_STATIC_SCRATCH_BYTES = 32 << 20
+MVK_MAX_GROUP = 4
 ABI_VERSION = 6
 # field modulus -> library built over that field
 LIB_PATHS = {MVK_PRIME: LIB_PATH, MVK_PRIME_BABYBEAR: LIB_PATH_BB}
@@ -72,6 +73,7 @@ EXPORTS = (
     "mvk_st_free",
     "mvk_decode_verify_seeded",
     "mvk_server_eval_packed_static",
+    "mvk_server_eval_packed_group",
 )
 
 
@@ -208,6 +210,8 @@ def load(p: int = MVK_PRIME) -> ctypes.CDLL:
     L.mvk_decode_verify_seeded.restype = st
     L.mvk_server_eval_packed_static.argtypes = [vp, u32, u32, vp, u32, vp, vp]
     L.mvk_server_eval_packed_static.restype = st
+    L.mvk_server_eval_packed_group.argtypes = [vp, u32, u32, u32, vp, u32, ctypes.POINTER(vp), vp]
+    L.mvk_server_eval_packed_group.restype = st
     if L.mvk_abi_version() != ABI_VERSION:
         raise ImportError(f"{path}: ABI version mismatch; rebuild the library")
     if L.mvk_field_modulus() != p:

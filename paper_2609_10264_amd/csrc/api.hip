@@ -280,6 +280,38 @@ mvk_status mvk_server_eval_packed(const int8_t* Wp, uint32_t m, uint32_t n, cons
     return server_eval_impl(Wp, m, n, Xhat, B, Yhat, MVK_PATH_AUTO, true, stream);
 }
 
+mvk_status mvk_server_eval_packed_group(const int8_t* Wp, uint32_t G, uint32_t m, uint32_t n, const uint32_t* Xhat,
+                                        uint32_t B, uint32_t* const* Yhat, void* stream) {
+    if (G == 0 || G > MVK_MAX_GROUP || !Yhat) return MVK_EINVAL;
+    if (G > 1 && m % 16 != 0) return MVK_EINVAL;
+    for (uint32_t g = 0; g < G; ++g)
+        if (!Yhat[g]) return MVK_EINVAL;
+    if (m == 0 || B == 0) return MVK_OK;
+    if (server_dims_too_big(G * (uint64_t)m > 0xffffffffull ? 0xffffffffu : G * m, n, B)) return MVK_ERANGE;
+    hipStream_t s = (hipStream_t)stream;
+    if (n == 0) {
+        for (uint32_t g = 0; g < G; ++g)
+            if (launch_fill_u32(Yhat[g], (size_t)m * B, 0u, s) != hipSuccess) return MVK_EHIP;
+        return MVK_OK;
+    }
+    if (!Wp || !Xhat || (uintptr_t)Wp % 16 != 0) return MVK_EINVAL;
+    if (n > MVK_MAX_N) return MVK_ERANGE;
+    if (validate_mode()) {
+        const mvk_status st = check_canonical(Xhat, (size_t)B * n, s);
+        if (st) return st;
+    }
+    void* ws = nullptr;
+    uint32_t* ctrl = nullptr;
+    const ServerEvalPlan pl = server_eval_plan(G * m, n, B, MVK_PATH_AUTO, true);
+    if (pl.ws_bytes || pl.ctrl_words) {
+        const mvk_status st = workspace(s, pl.ws_bytes, &ws, &ctrl, kCtrlBase + 4 * pl.ctrl_words);
+        if (st) return st;
+    }
+    uint32_t* counters = ctrl ? (uint32_t*)((char*)ctrl + kCtrlBase) : nullptr;
+    return hip_status(
+        launch_server_eval_group(Wp, G, m, n, Xhat, B, Yhat, MVK_PATH_AUTO, true, ws, counters, s));
+}
+
 }  // extern "C"
 
 // ---------------------------------------------------------------------------

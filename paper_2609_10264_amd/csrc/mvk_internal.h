@@ -22,6 +22,13 @@ ServerEvalPlan server_eval_plan(uint32_t m, uint32_t n, uint32_t B, int path, bo
 // W: row-major m x n, or (packed) the layout written by launch_pack_w.
 hipError_t launch_server_eval(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t B,
                               uint32_t* Y, int path, bool packed, void* ws, uint32_t* counters, hipStream_t s);
+// G (<= kMaxGroup) matrices of mg x n sharing the queries X: W is the packed
+// layout of their row stack (G * mg rows; mg a multiple of 16 when G > 1) and
+// Ys[g] (B x mg) receives matrix g's product.  Plan with m = G * mg.
+constexpr uint32_t kMaxGroup = MVK_MAX_GROUP;
+hipError_t launch_server_eval_group(const int8_t* W, uint32_t G, uint32_t mg, uint32_t n, const uint32_t* X,
+                                    uint32_t B, uint32_t* const* Ys, int path, bool packed, void* ws,
+                                    uint32_t* counters, hipStream_t s);
 // Packed W: ceil(m/16) * ceil(n/64) tiles of 1 KiB in MFMA operand order.
 size_t packed_w_bytes(uint32_t m, uint32_t n);
 hipError_t launch_pack_w(const int8_t* W, uint32_t m, uint32_t n, int8_t* Wp, hipStream_t s);

@@ -183,6 +183,26 @@ __global__ __launch_bounds__(256) void server_eval_valu(const int8_t* __restrict
 
 typedef int32_t v4i __attribute__((ext_vector_type(4)));
 
+// Where a launch writes its results.  The launch walks m = G * mg rows: the
+// row stack of G matrices of mg rows each (G = 1: one matrix); row r of the
+// stack is row r % mg of output r / mg, and output g is B x mg (query q at
+// y[g] + q * mg).
+struct YOut {
+    uint32_t* y[kMaxGroup];
+    uint32_t mg;
+    __device__ __forceinline__ uint32_t* at(uint32_t q, uint32_t row) const {
+        const uint32_t g = row / mg;
+        return y[g] + (size_t)q * mg + (row - g * mg);
+    }
+};
+
+// The outputs of queries b0.. of every matrix of the stack.
+inline YOut yout_shift(YOut o, uint32_t b0) {
+    for (int g = 0; g < kMaxGroup; ++g)
+        if (o.y[g]) o.y[g] += (size_t)b0 * o.mg;
+    return o;
+}
+
 // 16 bytes of W, a non-temporal load: W is streamed once per launch, so its
 // lines are not kept in the caches (measured on MI355X: the single-query
 // launch at 4096 x 4096 from 5.2 to 4.9 us, at 16384 x 16384 from 46 to 41 us).
@@ -221,7 +241,7 @@ enum WLayout { kWRowVec = 0, kWRowScalar = 1, kWPacked = 2 };
 template <int QB, int KW, int KBW, bool VEC, int WL>
 __global__ __launch_bounds__(KW * 64) void server_eval_mfma_small(const int8_t* __restrict__ W, uint32_t m,
                                                                   uint32_t n, const uint32_t* __restrict__ X,
-                                                                  uint32_t B, uint32_t* __restrict__ Y) {
+                                                                  uint32_t B, const YOut Y) {
     constexpr int KC = 64 * KBW * KW;  // k per chunk
     constexpr int STRIDE = KC + 16;    // padded LDS row (bytes)
     constexpr int ROWS = 4 * QB;
@@ -359,14 +379,14 @@ __global__ __launch_bounds__(KW * 64) void server_eval_mfma_small(const int8_t* 
             if (q < QB && q0 + q < B && wrow < m) {
                 int64_t v = (int64_t)sum[0] + ((int64_t)sum[1] << 8) + ((int64_t)sum[2] << 16) +
                             ((int64_t)sum[3] << 24);
-                Y[(size_t)(q0 + q) * m + wrow] = fred_s64(v);
+                *Y.at(q0 + q, wrow) = fred_s64(v);
             }
         }
     }
 }
 
 template <int QB, int KW, int KBW>
-hipError_t launch_mfma_small(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t B, uint32_t* Y,
+hipError_t launch_mfma_small(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t B, const YOut& Y,
                              bool packed, hipStream_t s) {
     const dim3 grid(ceil_div(m, 16), ceil_div(B, QB));
     const bool xvec = (n % 16 == 0) && ((uintptr_t)X % 16 == 0);
@@ -503,7 +523,7 @@ __device__ __forceinline__ uint32_t digits_to_field(v4i sum) { return fdigits4(s
 // covers whole cache lines.  `flag` is a word of idle LDS.
 template <int QW, int TWW, int NW>
 __device__ __forceinline__ void store_tiles(const v4i (&acc)[QW][TWW], uint32_t m, uint32_t B,
-                                            uint32_t* __restrict__ Y, uint32_t* part, uint32_t* counters,
+                                            const YOut& Y, uint32_t* part, uint32_t* counters,
                                             uint32_t rb, uint32_t nrb, uint32_t ks, uint32_t ksplit, int wave,
                                             int lane, uint32_t rowbase, uint32_t qbase, uint32_t* flag) {
     if (ksplit == 1) {
@@ -512,7 +532,7 @@ __device__ __forceinline__ void store_tiles(const v4i (&acc)[QW][TWW], uint32_t 
 #pragma unroll
             for (int t = 0; t < TWW; ++t) {
                 const uint32_t q = qbase + 4 * i, row = rowbase + 16 * t;
-                if (q < B && row < m) Y[(size_t)q * m + row] = digits_to_field(acc[i][t]);
+                if (q < B && row < m) *Y.at(q, row) = digits_to_field(acc[i][t]);
             }
         return;
     }
@@ -549,7 +569,7 @@ __device__ __forceinline__ void store_tiles(const v4i (&acc)[QW][TWW], uint32_t 
 #pragma unroll
         for (int t = 0; t < TWW; ++t) {
             const uint32_t q = qbase + 4 * i, row = rowbase + 16 * t;
-            if (q < B && row < m) Y[(size_t)q * m + row] = v[i][t];
+            if (q < B && row < m) *Y.at(q, row) = v[i][t];
         }
     if (threadIdx.x == 0) atomicExch(&counters[rb], 0u);
 }
@@ -575,7 +595,7 @@ __device__ __forceinline__ void pin_vgpr(v4i& x) { asm volatile("" : "+v"(x)); }
 template <int QT, int NW, int WQ, int TWW, int S, bool PACKED>
 __global__ __launch_bounds__(NW * 64) void server_eval_mfma_stream(
     const int8_t* __restrict__ W, uint32_t m, uint32_t n, const int8_t* __restrict__ Dt, uint32_t nkb,
-    uint32_t ksplit, uint32_t B, uint32_t* __restrict__ Y, uint32_t* part, uint32_t* counters) {
+    uint32_t ksplit, uint32_t B, const YOut Y, uint32_t* part, uint32_t* counters) {
     constexpr int WR = NW / WQ;               // waves along the row dimension
     constexpr int NWT = WR * TWW;             // W tiles per workgroup
     constexpr int QW = QT / WQ;               // digit tiles per wave
@@ -692,7 +712,7 @@ __global__ __launch_bounds__(NW * 64) void server_eval_mfma_stream(
 template <int QT, int TWW, int KBM, int C, bool PACKED>
 __global__ __launch_bounds__(512) void server_eval_mfma_dstat(const int8_t* __restrict__ W, uint32_t m, uint32_t n,
                                                               const uint32_t* __restrict__ X, uint32_t nkb,
-                                                              uint32_t ksplit, uint32_t B, uint32_t* __restrict__ Y,
+                                                              uint32_t ksplit, uint32_t B, const YOut Y,
                                                               uint32_t* part, uint32_t* counters) {
     constexpr int NW = 8;
     constexpr uint32_t kRows = NW * TWW * 16;
@@ -870,7 +890,7 @@ uint32_t stream_ksplit(uint32_t m, uint32_t n, uint32_t qt) {
 
 template <int QT, int WQ, int TWW, int S>
 hipError_t launch_stream_cfg(const int8_t* W, uint32_t m, uint32_t n, const int8_t* Dt, uint32_t nkb, uint32_t B,
-                             uint32_t* Y, uint32_t ksplit, uint32_t* part, uint32_t* counters, bool packed,
+                             const YOut& Y, uint32_t ksplit, uint32_t* part, uint32_t* counters, bool packed,
                              hipStream_t s) {
     constexpr uint32_t rows = (kStreamWaves / WQ) * TWW * 16;
     const uint32_t nrb = ceil_div(m, rows), per_group = 8 / ksplit;
@@ -987,13 +1007,13 @@ GroupPlan group_plan(uint32_t m, uint32_t n, uint32_t nb) {
 
 template <int QT, int TWW, int KBM, int C>
 hipError_t launch_dstat_cfg(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t nkb, uint32_t B,
-                            uint32_t* Y, uint32_t ksplit, uint32_t* part, uint32_t* counters, bool packed,
+                            const YOut& Y, uint32_t ksplit, uint32_t* part, uint32_t* counters, bool packed,
                             hipStream_t s);
 
 // launch_dstat_cfg for the plan's LDS size (kbm a power of two in [8, KBM max])
 template <int QT, int TWW>
 hipError_t launch_dstat_kbm(uint32_t kbm, const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t nkb,
-                            uint32_t B, uint32_t* Y, uint32_t ksplit, uint32_t* part, uint32_t* counters,
+                            uint32_t B, const YOut& Y, uint32_t ksplit, uint32_t* part, uint32_t* counters,
                             bool packed, hipStream_t s) {
     constexpr uint32_t kMax = QT == 4 ? kDstatKbm4 : kDstatKbm2;
     if (kbm == 8) return launch_dstat_cfg<QT, TWW, 8, 8>(W, m, n, X, nkb, B, Y, ksplit, part, counters, packed, s);
@@ -1007,7 +1027,7 @@ hipError_t launch_dstat_kbm(uint32_t kbm, const int8_t* W, uint32_t m, uint32_t 
 
 template <int QT, int TWW, int KBM, int C>
 hipError_t launch_dstat_cfg(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t nkb, uint32_t B,
-                            uint32_t* Y, uint32_t ksplit, uint32_t* part, uint32_t* counters, bool packed,
+                            const YOut& Y, uint32_t ksplit, uint32_t* part, uint32_t* counters, bool packed,
                             hipStream_t s) {
     if (ksplit == 0 || ceil_div(nkb, ksplit) > (uint32_t)KBM) return hipErrorInvalidValue;  // LDS holds the range
     const uint32_t nrb = ceil_div(m, 128 * TWW), per_group = 8 / ksplit;
@@ -1047,23 +1067,30 @@ ServerEvalPlan server_eval_plan(uint32_t m, uint32_t n, uint32_t B, int path, bo
     return pl;
 }
 
-hipError_t launch_server_eval(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t B,
-                              uint32_t* Y, int path, bool packed, void* ws, uint32_t* counters, hipStream_t s) {
+hipError_t launch_server_eval_group(const int8_t* W, uint32_t G, uint32_t mg, uint32_t n, const uint32_t* X,
+                                    uint32_t B, uint32_t* const* Ys, int path, bool packed, void* ws,
+                                    uint32_t* counters, hipStream_t s) {
+    if (G == 0 || G > kMaxGroup || (G > 1 && (!packed || path == MVK_PATH_VALU))) return hipErrorInvalidValue;
+    YOut out{};
+    for (uint32_t g = 0; g < G; ++g) out.y[g] = Ys[g];
+    out.mg = mg;
+    const uint32_t m = G * mg;  // rows of the stack
+    uint32_t* const Y = Ys[0];
     if (path == MVK_PATH_VALU) {
         if (B == 1) return launch_cfg<16, 1>(W, m, n, X, B, Y, s);
         if (B == 2) return launch_cfg<8, 2>(W, m, n, X, B, Y, s);
         return launch_cfg<4, 4>(W, m, n, X, B, Y, s);
     }
-    if (B == 1) return launch_mfma_small<1, 8, 8>(W, m, n, X, B, Y, packed, s);
-    if (B == 2) return launch_mfma_small<2, 8, 8>(W, m, n, X, B, Y, packed, s);
-    if (B <= 4) return launch_mfma_small<4, 8, 4>(W, m, n, X, B, Y, packed, s);
+    if (B == 1) return launch_mfma_small<1, 8, 8>(W, m, n, X, B, out, packed, s);
+    if (B == 2) return launch_mfma_small<2, 8, 8>(W, m, n, X, B, out, packed, s);
+    if (B <= 4) return launch_mfma_small<4, 8, 4>(W, m, n, X, B, out, packed, s);
     if (!packed && (n % 16 != 0 || (uintptr_t)W % 16 != 0)) {
         // Rows that are not whole 16-byte granules: the streamed path would read
         // past the end of W on the last row; use the small path per 4 queries.
         for (uint32_t b0 = 0; b0 < B; b0 += 4) {
             const uint32_t nb = (B - b0) < 4 ? (B - b0) : 4;
             const hipError_t e =
-                launch_mfma_small<4, 8, 4>(W, m, n, X + (size_t)b0 * n, nb, Y + (size_t)b0 * m, false, s);
+                launch_mfma_small<4, 8, 4>(W, m, n, X + (size_t)b0 * n, nb, yout_shift(out, b0), false, s);
             if (e != hipSuccess) return e;
         }
         return hipSuccess;
@@ -1084,7 +1111,7 @@ hipError_t launch_server_eval(const int8_t* W, uint32_t m, uint32_t n, const uin
         const uint32_t nb = (B - b0) < 64 ? (B - b0) : 64;
         const GroupPlan g = group_plan(m, n, nb);
         const uint32_t* Xb = X + (size_t)b0 * n;
-        uint32_t* Yb = Y + (size_t)b0 * m;
+        const YOut Yb = yout_shift(out, b0);
         hipError_t e = hipSuccess;
         if (g.dstat) {
             if (g.qt == 4)
@@ -1121,6 +1148,11 @@ hipError_t launch_server_eval(const int8_t* W, uint32_t m, uint32_t n, const uin
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
+}
+
+hipError_t launch_server_eval(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t B,
+                              uint32_t* Y, int path, bool packed, void* ws, uint32_t* counters, hipStream_t s) {
+    return launch_server_eval_group(W, 1, m, n, X, B, &Y, path, packed, ws, counters, s);
 }
 
 }  // namespace mvk

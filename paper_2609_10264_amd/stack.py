@@ -28,8 +28,8 @@ from dataclasses import dataclass, field
 
 import torch
 
-from . import (Code, Key, Prepared, client_prepare, decode_verify, decode_verify_masked, encode, encode_masked, keygen,
-               pack_weights, server_eval)
+from . import (Code, Key, PackedW, Prepared, client_prepare, decode_verify, decode_verify_masked, encode, encode_masked,
+               keygen, pack_weights, pack_weights_group, server_eval, server_eval_group)
 
 # (name, m, n, input group)
 PROJECTIONS = (
@@ -46,25 +46,59 @@ INPUTS = ("attn_in", "attn_out", "mlp_in", "mlp_out")
 
 @dataclass
 class Layer:
-    W: dict = field(default_factory=dict)      # name -> int8 m x n, or its PackedW
-    keys: dict = field(default_factory=dict)   # name -> Key
+    W: dict = field(default_factory=dict)       # name -> int8 m x n, or its PackedW
+    keys: dict = field(default_factory=dict)    # name -> Key
+    stacks: dict = field(default_factory=dict)  # input group -> (PackedW row stack, [names]) for shared inputs
 
 
 def input_width(group: str) -> int:
     return next(n for (_, _, n, g) in PROJECTIONS if g == group)
 
 
+def stage(group: str) -> list:
+    """The projections fed by one input, in PROJECTIONS order."""
+    return [name for (name, _, _, g) in PROJECTIONS if g == group]
+
+
 def build_layer(weights: dict, cx_by_n: dict, cy_by_m: dict, stream=None, packed: bool = True) -> Layer:
-    """Preprocess every projection of one layer (keygen on the device); with
-    `packed` the server keeps each W in the packed matrix-core layout."""
+    """Preprocess every projection of one layer (keygen on the device).  With
+    `packed` the server keeps W in the packed matrix-core layout, and the
+    projections that share an input (q, k, v; up, gate) as one row stack, so
+    that one launch evaluates them together; layer.W[name] views its part."""
     layer = Layer()
     for name, m, n, _ in PROJECTIONS:
         W = weights[name]
         key = Key.allocate(m, n, cx_by_n[n], cy_by_m[m], device=W.device)
         keygen(key, W, stream=stream)
-        layer.W[name] = pack_weights(W, stream=stream) if packed else W
         layer.keys[name] = key
+        if not packed:
+            layer.W[name] = W
+    if packed:
+        for group in INPUTS:
+            names = stage(group)
+            if len(names) == 1:
+                layer.W[names[0]] = pack_weights(weights[names[0]], stream=stream)
+                continue
+            st = pack_weights_group([weights[nm] for nm in names], stream=stream)
+            nb = st.data.numel() // len(names)
+            for g, nm in enumerate(names):
+                m, n = weights[nm].shape
+                layer.W[nm] = PackedW(st.data[g * nb:(g + 1) * nb], m, n)
+            layer.stacks[group] = (st, names)
     return layer
+
+
+def evaluate_stage(layer: Layer, group: str, Xhat: torch.Tensor, outs: dict | None = None, stream=None) -> dict:
+    """The server's products for every projection fed by one input: one
+    launch over the row stack where the layer keeps one, else one per
+    projection.  Returns {name: Yhat}."""
+    names = stage(group)
+    if group in layer.stacks:
+        st, _ = layer.stacks[group]
+        res = server_eval_group(st, len(names), Xhat, outs=[outs[nm] for nm in names] if outs else None,
+                                stream=stream)
+        return dict(zip(names, res))
+    return {nm: server_eval(layer.W[nm], Xhat, out=outs[nm] if outs else None, stream=stream) for nm in names}
 
 
 def run_layer(layer: Layer, X: dict, ex: dict, ey: dict, tamper=None, stream=None):
@@ -82,8 +116,11 @@ def run_layer(layer: Layer, X: dict, ex: dict, ey: dict, tamper=None, stream=Non
         name = next(p for (p, _, _, g) in PROJECTIONS if g == group)
         Xhat[group] = encode(layer.keys[name], X[group], ex[group][0], ex[group][1], stream=stream)
     out = {}
+    Yhats = {}
+    for group in INPUTS:
+        Yhats.update(evaluate_stage(layer, group, Xhat[group], stream=stream))
     for name, m, n, group in PROJECTIONS:
-        Yhat = server_eval(layer.W[name], Xhat[group], stream=stream)
+        Yhat = Yhats[name]
         if tamper is not None:
             tamper(name, Yhat)
         ell, B = ey[name][0].shape[0], Yhat.shape[0]
@@ -129,8 +166,11 @@ def run_layer_prepared(layer: Layer, X: dict, preps: dict, ready_flag: torch.Ten
                                     timeout_us=timeout_us, timed_out=timed_out, stream=stream)
         wait = None
     out = {}
+    Yhats = {}
+    for group in INPUTS:
+        Yhats.update(evaluate_stage(layer, group, Xhat[group], stream=stream))
     for name, m, n, group in PROJECTIONS:
-        Yhat = server_eval(layer.W[name], Xhat[group], stream=stream)
+        Yhat = Yhats[name]
         if tamper is not None:
             tamper(name, Yhat)
         vL = torch.empty((preps[name].ell, Yhat.shape[0]), dtype=torch.int32, device=Yhat.device)
@@ -188,8 +228,9 @@ def run_pass_overlapped(layers: list, inputs: list, preps: list, outs: list, mai
         share one input, o's input comes after the q, k, v outputs, up and
         gate share the next, down's comes last; each input's masked encode
         waits for every verification of the previous stage;
-      * within a stage every projection is one branch: server_eval, then its
-        decode/verify.
+      * within a stage the server's products run first (one launch over the
+        row stack of the projections that share the input), then every
+        projection's decode/verify on a branch of its own.
     inputs[L] = (X, ex, ey) as for run_layer; preps[L]: {name: Prepared};
     outs[L]: LayerOutputs; tamper: optional callable(L, name, Yhat) on the
     branch stream between the product and its check."""
@@ -215,19 +256,19 @@ def run_pass_overlapped(layers: list, inputs: list, preps: list, outs: list, mai
         X = inputs[L][0]
         o = outs[L]
         for group in INPUTS:
-            stage = [name for (name, _, _, g) in PROJECTIONS if g == group]
+            names = stage(group)
             with torch.cuda.stream(main):
-                encode_masked(layer.keys[stage[0]], X[group], preps[L][stage[0]], out=o.xhat[group], stream=main)
-            for j, name in enumerate(stage):
+                encode_masked(layer.keys[names[0]], X[group], preps[L][names[0]], out=o.xhat[group], stream=main)
+                evaluate_stage(layer, group, o.xhat[group], outs=o.yhat, stream=main)
+            for j, name in enumerate(names):
                 b = branch_streams[j]
                 b.wait_stream(main)
                 with torch.cuda.stream(b):
-                    server_eval(layer.W[name], o.xhat[group], out=o.yhat[name], stream=b)
                     if tamper is not None:
                         tamper(L, name, o.yhat[name])
                     decode_verify_masked(layer.keys[name], o.xhat[group], o.yhat[name], preps[L][name], Y=o.y[name],
                                          vL=o.vl[name], vR=o.vr[name], accept=o.accept[name], stream=b)
-            for j in range(len(stage)):
+            for j in range(len(names)):
                 main.wait_stream(branch_streams[j])
     for s in every:
         main.wait_stream(s)
@@ -244,5 +285,6 @@ def macs_per_layer(B: int) -> int:
     return sum(m * n for (_, m, n, _) in PROJECTIONS) * B
 
 
-__all__ = ["PROJECTIONS", "INPUTS", "Layer", "LayerOutputs", "build_layer", "run_layer", "prepare_layer",
-           "run_layer_prepared", "run_pass_overlapped", "codes_for", "input_width", "macs_per_layer", "Code"]
+__all__ = ["PROJECTIONS", "INPUTS", "Layer", "LayerOutputs", "build_layer", "evaluate_stage", "run_layer",
+           "prepare_layer", "run_layer_prepared", "run_pass_overlapped", "codes_for", "input_width", "stage",
+           "macs_per_layer", "Code"]

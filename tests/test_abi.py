@@ -327,3 +327,21 @@ def test_static_server_eval_rejects_shapes_beyond_its_scratch():
     assert lib.mvk_server_eval(fake, 0xFFFFFFF0, 64, fake, 1, fake, None) == L.MVK_ERANGE
     assert lib.mvk_server_eval_packed(fake, 16, 64, fake, 0x80000000, fake, None) == L.MVK_ERANGE
     assert lib.mvk_pack_weights(fake, 0xFFFFFFF0, 64, fake, None) == L.MVK_ERANGE
+
+
+def test_group_server_eval_argument_checks_without_device_work():
+    L = _lib()
+    lib = L.load()
+    fake = ctypes.c_void_p(0x1000)
+    ys = (ctypes.c_void_p * 4)(0x1000, 0x1000, 0x1000, 0x1000)
+    assert L.MVK_MAX_GROUP == 4
+    assert lib.mvk_server_eval_packed_group(fake, 0, 16, 64, fake, 1, ys, None) == L.MVK_EINVAL
+    assert lib.mvk_server_eval_packed_group(fake, 5, 16, 64, fake, 1, ys, None) == L.MVK_EINVAL
+    assert lib.mvk_server_eval_packed_group(fake, 2, 17, 64, fake, 1, ys, None) == L.MVK_EINVAL  # m % 16
+    assert lib.mvk_server_eval_packed_group(fake, 2, 16, 64, fake, 1, None, None) == L.MVK_EINVAL
+    nully = (ctypes.c_void_p * 2)(0x1000, None)
+    assert lib.mvk_server_eval_packed_group(fake, 2, 16, 64, fake, 1, nully, None) == L.MVK_EINVAL
+    assert lib.mvk_server_eval_packed_group(fake, 4, 0x40000000, 64, fake, 1, ys, None) == L.MVK_ERANGE
+    assert lib.mvk_server_eval_packed_group(fake, 2, 16, L.MVK_MAX_N + 1, fake, 1, ys, None) == L.MVK_ERANGE
+    assert lib.mvk_server_eval_packed_group(ctypes.c_void_p(0x1008), 2, 16, 64, fake, 1, ys, None) == L.MVK_EINVAL
+    assert lib.mvk_server_eval_packed_group(fake, 2, 0, 64, fake, 1, ys, None) == L.MVK_OK

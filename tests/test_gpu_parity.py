@@ -414,3 +414,23 @@ def test_attn4096_full():
     oacc, ovL, ovR = oracle.verify(inst.cy, Q, Xh, Yh, inst.eyi, inst.eyv)
     assert np.array_equal(host(vL), ovL) and np.array_equal(host(vR), ovR) and host(acc).tolist() == [1]
     assert np.array_equal(host(Y), oracle.decode(PT, Yh, inst.exi, inst.exv))
+
+
+# ---------------------------------------------------------------------------
+# several matrices sharing their queries in one launch
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("G,m,n,B", [(1, 33, 300, 8), (2, 16, 64, 1), (3, 4096, 4096, 8), (2, 11008, 4096, 8),
+                                     (3, 4096, 4096, 1), (4, 256, 1000, 3), (2, 512, 4160, 16), (3, 160, 2048, 40),
+                                     (2, 1024, 8192, 64), (4, 48, 130, 70)])
+def test_server_eval_group_matches_separate_products(G, m, n, B):
+    _say(f"server_eval_group G={G} m={m} n={n} B={B}")
+    Ws = [synth.weights(600 + 7 * g + m, m, n, lo=-128, hi=127) for g in range(G)]
+    X = synth.field_uniform(700 + n + B, (B, n))
+    dX = dev(X)
+    stackW = mvk.pack_weights_group([dev(W) for W in Ws])
+    outs = mvk.server_eval_group(stackW, G, dX)
+    for g, W in enumerate(Ws):
+        want = mvk.server_eval(mvk.pack_weights(dev(W)), dX)
+        assert torch.equal(outs[g], want), g
+    # one of them against the oracle as well
+    assert np.array_equal(host(outs[G - 1]), oracle.server_eval(Ws[G - 1], X))

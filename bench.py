@@ -21,9 +21,11 @@ Three schedules of the same work (--stack-mode):
               v, then o, then up and gate, then down, each input after the
               previous stage's checks) with the projections of a stage side by
               side.  One HIP graph of the pass over several streams.
-  pipelined   (default) the same work on one preparation stream and one
-              online stream (every call of the online part in sequence), device
-              flags between the two streams' graphs.
+  pipelined   (default) the same work on preparation streams (one graph
+              each, every input's preparation one launch for the projections
+              it feeds) and one online stream (per input in inference order:
+              masked encode, one grouped server launch, one grouped check),
+              with a device flag per input between the graphs.
   serial      every call of the pass back to back on one stream, one graph.
 
 The JSON line:
@@ -206,7 +208,9 @@ def parse():
                     help="schedule reported as value of a single-matrix workload (both are timed)")
     ap.add_argument("--stack-mode", default="pipelined", choices=["overlapped", "pipelined", "serial"],
                     help="schedule reported as value of the stack (all three are timed)")
-    ap.add_argument("--prep-streams", type=int, default=4, help="preparation streams of the overlapped stack pass")
+    ap.add_argument("--prep-streams", type=int, default=1,
+                    help="preparation streams of the pipelined and overlapped stack schedules (more than one "
+                         "measured slower: 5.4 against 4.2 ms per pass with two)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the run, copy a buffer of this many MiB (reference for the traffic counters)")
     ap.add_argument("--seed", type=int, default=2609)
@@ -631,42 +635,56 @@ def stack_bench(args, steps, warmup, cpu_seconds):
     ok_serial = accepts_ok(results)
 
     # ---- pipelined ----------------------------------------------------------
-    s_prep, s_on = torch.cuda.Stream(), torch.cuda.Stream()
-    flags = torch.zeros((layers, nproj), dtype=torch.int32, device=dev)
+    # the four inputs' preparations of every layer spread over the preparation
+    # streams (input i on stream i % P), one graph each; each sets its own
+    # input's flag, for which that input's masked encode on the online stream
+    # waits
+    nin = len(stack.INPUTS)
+    npre = max(1, args.prep_streams)
+    s_preps, s_on = [torch.cuda.Stream() for _ in range(npre)], torch.cuda.Stream()
+    flags = torch.zeros((layers, nin), dtype=torch.int32, device=dev)
     late = torch.zeros((), dtype=torch.int32, device=dev)
     preps = [dict() for _ in range(layers)]
     presults = []
 
-    def prep_pass():
+    def prep_pass(k):
         for L in range(layers):
-            stack.prepare_layer(built[L], inputs[L][1], inputs[L][2], flags[L], out=preps[L], stream=s_prep)
+            _, ex, ey = inputs[L]
+            for i, grp in enumerate(stack.INPUTS):
+                if i % npre == k:
+                    stack.prepare_input(built[L], grp, ex, ey, preps[L], flag=flags[L, i], stream=s_preps[k])
 
     def online_pass():
         presults.clear()
         for L in range(layers):
-            presults.append(stack.run_layer_prepared(built[L], inputs[L][0], preps[L], ready_flag=flags[L, nproj - 1],
+            presults.append(stack.run_layer_prepared(built[L], inputs[L][0], preps[L],
+                                                     ready_flag=[flags[L, i] for i in range(nin)],
                                                      timeout_us=200_000, timed_out=late, tamper=tamperer(L),
                                                      stream=s_on))
 
     for _ in range(warmup):  # also sizes the per-stream workspaces
-        with torch.cuda.stream(s_prep):
-            prep_pass()
+        for k in range(npre):
+            with torch.cuda.stream(s_preps[k]):
+                prep_pass(k)
         with torch.cuda.stream(s_on):
             online_pass()
         torch.cuda.synchronize()
-    gp, go = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
-    with torch.cuda.graph(gp, stream=s_prep):
-        prep_pass()
+    gps = [torch.cuda.CUDAGraph() for _ in range(npre)]
+    for k in range(npre):
+        with torch.cuda.graph(gps[k], stream=s_preps[k]):
+            prep_pass(k)
+    go = torch.cuda.CUDAGraph()
     with torch.cuda.graph(go, stream=s_on):
         online_pass()
 
     def replay_pipelined():
         # a pass's preparation starts after the previous pass's online part
         # (it rewrites the prepared buffers and the flags that part consumes),
-        # and is submitted first: the two streams may share a hardware queue
-        s_prep.wait_stream(s_on)
-        with torch.cuda.stream(s_prep):
-            gp.replay()
+        # and is submitted first: streams may share a hardware queue
+        for k in range(npre):
+            s_preps[k].wait_stream(s_on)
+            with torch.cuda.stream(s_preps[k]):
+                gps[k].replay()
         with torch.cuda.stream(s_on):
             go.replay()
 
@@ -675,12 +693,11 @@ def stack_bench(args, steps, warmup, cpu_seconds):
     ok_pipe = accepts_ok(presults) and int(late.item()) == 0
     same = all(bool(torch.equal(a, b)) for sr, pr in zip(results, presults) for name in sr
                for a, b in zip(sr[name], pr[name]))
-    del gs, gp, go
+    del gs, gps, go
 
     # ---- overlapped: the pass on several streams, one graph ----------------
     ov_main = torch.cuda.Stream()
     ov_prep = [torch.cuda.Stream() for _ in range(args.prep_streams)]
-    ov_branch = [torch.cuda.Stream() for _ in range(3)]
     ov_preps = [{name: mvk.Prepared(built[L].keys[name], B, ell) for (name, _, _, _) in stack.PROJECTIONS}
                 for L in range(layers)]
     ov_outs = [stack.LayerOutputs.allocate(B, ell) for _ in range(layers)]
@@ -689,7 +706,7 @@ def stack_bench(args, steps, warmup, cpu_seconds):
         tamperer(L)(name, Yhat)
 
     def ov_pass():
-        stack.run_pass_overlapped(built, inputs, ov_preps, ov_outs, ov_main, ov_prep, ov_branch, tamper=ov_tamper)
+        stack.run_pass_overlapped(built, inputs, ov_preps, ov_outs, ov_main, ov_prep, tamper=ov_tamper)
 
     for _ in range(warmup):  # also sizes every stream's workspace
         with torch.cuda.stream(ov_main):

@@ -312,6 +312,23 @@ mvk_status mvk_client_prepare(const mvk_key *key, const mvk_sparse *ex, const mv
                               uint32_t *done_flag, uint32_t done_value, void *stream);
 
 /*
+ * mvk_client_prepare for G <= MVK_MAX_GROUP keys that share their input (for
+ * example q, k and v): keys of one shape m x n and one privacy code (the same
+ * cx arrays), so that the noise vectors ex and the input mask Mx are shared;
+ * My[g] = P_g e_b, R[g] = Gy_g e_q and U[g] = e_q^T Q_g for each key with its
+ * own challenges ey[g] (the same count and t for every g).  My, R, U, ey: host
+ * arrays of G pointers (device buffers as mvk_client_prepare).  One launch
+ * when Nx and Ny are at most 16384 (else the longer syndromes first, in their
+ * own launches); same outputs, bit for bit, as G calls of mvk_client_prepare.
+ * Errors: as mvk_client_prepare, plus MVK_EINVAL (G out of range, keys of
+ * different shapes or privacy codes, challenge sets of different sizes).
+ */
+mvk_status mvk_client_prepare_group(uint32_t G, const mvk_key *const *keys, const mvk_sparse *ex,
+                                    const mvk_sparse *const *ey, uint32_t *Mx, uint32_t *const *My,
+                                    uint32_t *const *R, uint32_t *const *U, uint32_t *done_flag, uint32_t done_value,
+                                    void *stream);
+
+/*
  * Encrypt with a prepared input mask: Xhat = X + Mx (B x n, element-wise mod p).
  * Same result as mvk_encode with the noise vectors Mx was prepared from.
  * X, Mx: device, read; Xhat: device, written (may alias X).
@@ -339,6 +356,26 @@ mvk_status mvk_decode_verify_masked(const mvk_key *key, const uint32_t *Xhat, co
                                     uint32_t B, const uint32_t *My, uint32_t ell, const uint32_t *R,
                                     const uint32_t *U, uint32_t *Y, uint32_t *vL, uint32_t *vR,
                                     uint32_t *accept, void *stream);
+
+/*
+ * mvk_decode_verify_masked for G <= MVK_MAX_GROUP matrices that share the
+ * queries Xhat (for example q, k and v, evaluated by
+ * mvk_server_eval_packed_group): problem g has its key keys[g] (all keys of
+ * one shape m x n), response Yhat[g], prepared vectors My[g], R[g], U[g]
+ * (from mvk_client_prepare with keys[g]) and outputs Y[g], vL[g], vR[g],
+ * accept[g]; every array is a host array of G device pointers (vL, vR may be
+ * NULL, or hold NULL entries).  Same outputs, bit for bit, as G calls of
+ * mvk_decode_verify_masked; one launch where the problem is large enough for
+ * the element-block kernel (B * (m + n) above 32768 words, ell <= 4), else
+ * one per matrix.
+ * Errors: MVK_EINVAL (null pointer, G out of range, keys of different
+ * shapes), MVK_ERANGE (ell > 16 or B > 65535), MVK_ENOMEM.
+ */
+mvk_status mvk_decode_verify_masked_group(uint32_t G, const mvk_key *const *keys, const uint32_t *Xhat, uint32_t B,
+                                          const uint32_t *const *Yhat, const uint32_t *const *My, uint32_t ell,
+                                          const uint32_t *const *R, const uint32_t *const *U, uint32_t *const *Y,
+                                          uint32_t *const *vL, uint32_t *const *vR, uint32_t *const *accept,
+                                          void *stream);
 
 /*
  * Stream flags: order work on two streams whose launches are captured in two

@@ -309,6 +309,38 @@ def client_prepare(key: Key, ex_idx: torch.Tensor, ex_val: torch.Tensor, ey_idx:
     return out
 
 
+def client_prepare_group(keys: list, ex_idx: torch.Tensor, ex_val: torch.Tensor, eys: list, outs: list | None = None,
+                         done_flag: torch.Tensor | None = None, done_value: int = 1, stream=None) -> list:
+    """client_prepare for several keys sharing the noise (one shape, one privacy
+    code): the input mask once (in every returned Prepared), the output masks
+    and challenge vectors per key.  eys: [(ey_idx, ey_val)] per key."""
+    G = len(keys)
+    B = ex_idx.shape[0]
+    ell = eys[0][0].shape[0]
+    if outs is None:
+        outs = [Prepared(k, B, ell, device=ex_idx.device) for k in keys]
+    if any((o.B, o.ell) != (B, ell) for o in outs):
+        raise ValueError("Prepared buffers do not match the noise / challenge counts")
+    structs = [k.struct() for k in keys]
+    kp = (ctypes.POINTER(MvkKey) * G)(*[ctypes.pointer(ks) for ks in structs])
+    ex = _sparse(ex_idx, ex_val, "ex")
+    ey_structs = [_sparse(i, v, f"ey[{g}]") for g, (i, v) in enumerate(eys)]
+    eyp = (ctypes.POINTER(MvkSparse) * G)(*[ctypes.pointer(e) for e in ey_structs])
+    m, n = keys[0].m, keys[0].n
+    # the shared input mask goes to the first Prepared; the others get a copy view of it
+    arr = lambda ts, shape, name: (ctypes.c_void_p * G)(*[_dev(t, torch.int32, shape, f"{name}[{g}]")  # noqa: E731
+                                                          for g, t in enumerate(ts)])
+    _lib.check("mvk_client_prepare_group", _lib.load(keys[0].p).mvk_client_prepare_group(
+        G, kp, ctypes.byref(ex), eyp, _dev(outs[0].Mx, torch.int32, (B, n), "Mx"),
+        arr([o.My for o in outs], (B, m), "My"), arr([o.R for o in outs], (ell, m), "R"),
+        arr([o.U for o in outs], (ell, n), "U"),
+        _dev(done_flag, torch.int32, (), "done_flag") if done_flag is not None else None, done_value,
+        _stream(stream)))
+    for o in outs[1:]:
+        o.Mx = outs[0].Mx
+    return outs
+
+
 def encode_masked(key: Key, X: torch.Tensor, prep: Prepared, out: torch.Tensor | None = None,
                   ready_flag: torch.Tensor | None = None, ready_value: int = 1, timeout_us: int = 200000,
                   timed_out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
@@ -346,6 +378,37 @@ def decode_verify_masked(key: Key, Xhat: torch.Tensor, Yhat: torch.Tensor, prep:
         _dev(prep.U, torch.int32, (ell, key.n), "U"), _dev(Y, torch.int32, (B, key.m), "Y"), vLp, vRp,
         _dev(accept, torch.int32, (B,), "accept"), _stream(stream)))
     return Y, accept, vL, vR
+
+
+def decode_verify_masked_group(keys: list, Xhat: torch.Tensor, Yhats: list, preps: list, Ys: list | None = None,
+                               vLs: list | None = None, vRs: list | None = None, accepts: list | None = None,
+                               stream=None):
+    """decode_verify_masked for several matrices sharing the queries Xhat (one
+    launch where the problem allows).  Returns (Ys, accepts, vLs, vRs)."""
+    G = len(keys)
+    B = Xhat.shape[0]
+    ell = preps[0].ell
+    m, n = keys[0].m, keys[0].n
+    dev = Xhat.device
+    if Ys is None:
+        Ys = [torch.empty((B, m), dtype=torch.int32, device=dev) for _ in range(G)]
+    if accepts is None:
+        accepts = [torch.empty((B,), dtype=torch.int32, device=dev) for _ in range(G)]
+    structs = [k.struct() for k in keys]
+    kp = (ctypes.POINTER(MvkKey) * G)(*[ctypes.pointer(ks) for ks in structs])
+
+    def arr(ts, shape, name):
+        return (ctypes.c_void_p * G)(*[_dev(t, torch.int32, shape, f"{name}[{g}]") for g, t in enumerate(ts)])
+
+    if any(p.ell != ell for p in preps):
+        raise ValueError("the prepared vectors of a group must have one repetition count")
+    _lib.check("mvk_decode_verify_masked_group", _lib.load(keys[0].p).mvk_decode_verify_masked_group(
+        G, kp, _dev(Xhat, torch.int32, (B, n), "Xhat"), B, arr(Yhats, (B, m), "Yhat"),
+        arr([p.My for p in preps], (B, m), "My"), ell, arr([p.R for p in preps], (ell, m), "R"),
+        arr([p.U for p in preps], (ell, n), "U"), arr(Ys, (B, m), "Y"),
+        arr(vLs, (ell, B), "vL") if vLs is not None else None, arr(vRs, (ell, B), "vR") if vRs is not None else None,
+        arr(accepts, (B,), "accept"), _stream(stream)))
+    return Ys, accepts, vLs, vRs
 
 
 def flag_signal(flag: torch.Tensor, value: int = 1, stream=None) -> None:

@@ -74,6 +74,8 @@ EXPORTS = (
     "mvk_decode_verify_seeded",
     "mvk_server_eval_packed_static",
     "mvk_server_eval_packed_group",
+    "mvk_decode_verify_masked_group",
+    "mvk_client_prepare_group",
 )
 
 
@@ -212,6 +214,13 @@ def load(p: int = MVK_PRIME) -> ctypes.CDLL:
     L.mvk_server_eval_packed_static.restype = st
     L.mvk_server_eval_packed_group.argtypes = [vp, u32, u32, u32, vp, u32, ctypes.POINTER(vp), vp]
     L.mvk_server_eval_packed_group.restype = st
+    pvp = ctypes.POINTER(vp)
+    L.mvk_decode_verify_masked_group.argtypes = [u32, ctypes.POINTER(ctypes.POINTER(MvkKey)), vp, u32, pvp, pvp, u32,
+                                                 pvp, pvp, pvp, pvp, pvp, pvp, vp]
+    L.mvk_decode_verify_masked_group.restype = st
+    L.mvk_client_prepare_group.argtypes = [u32, ctypes.POINTER(ctypes.POINTER(MvkKey)), ctypes.POINTER(MvkSparse),
+                                           ctypes.POINTER(ctypes.POINTER(MvkSparse)), vp, pvp, pvp, pvp, vp, u32, vp]
+    L.mvk_client_prepare_group.restype = st
     if L.mvk_abi_version() != ABI_VERSION:
         raise ImportError(f"{path}: ABI version mismatch; rebuild the library")
     if L.mvk_field_modulus() != p:

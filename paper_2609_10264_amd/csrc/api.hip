@@ -564,6 +564,66 @@ mvk_status mvk_client_prepare(const mvk_key* key, const mvk_sparse* ex, const mv
                                             done_value, s));
 }
 
+mvk_status mvk_client_prepare_group(uint32_t G, const mvk_key* const* keys, const mvk_sparse* ex,
+                                    const mvk_sparse* const* ey, uint32_t* Mx, uint32_t* const* My,
+                                    uint32_t* const* R, uint32_t* const* U, uint32_t* done_flag, uint32_t done_value,
+                                    void* stream) {
+    if (G == 0 || G > MVK_MAX_GROUP || !keys) return MVK_EINVAL;
+    for (uint32_t g = 0; g < G; ++g) {
+        const mvk_status st = check_key(keys[g]);
+        if (st) return st;
+        const mvk_key &k = *keys[g], &k0 = *keys[0];
+        // one shape and one privacy code: the noise and its mask are shared
+        if (k.m != k0.m || k.n != k0.n || k.cx.r != k0.cx.r || k.cx.pi1 != k0.cx.pi1 || k.cx.pi2 != k0.cx.pi2 ||
+            k.cx.v1 != k0.cx.v1 || k.cx.v2 != k0.cx.v2 || k.cy.r != k0.cy.r)
+            return MVK_EINVAL;
+    }
+    if (done_flag && done_value == 0) return MVK_EINVAL;
+    const mvk_key& key = *keys[0];
+    const uint32_t nx = ex ? ex->count : 0u;
+    if (nx) {
+        if (!Mx || !My || (ex->t && (!ex->idx || !ex->val))) return MVK_EINVAL;
+        if ((uint64_t)ex->t > (uint64_t)key.cx.r * key.n) return MVK_EINVAL;
+        if (nx > 65535u) return MVK_ERANGE;
+        for (uint32_t g = 0; g < G; ++g)
+            if (!My[g] || !keys[g]->PT) return MVK_EINVAL;
+    }
+    uint32_t ny = 0, ty = 0;
+    const uint32_t* eyi[MVK_MAX_GROUP] = {};
+    const uint32_t* eyv[MVK_MAX_GROUP] = {};
+    if (ey) {
+        for (uint32_t g = 0; g < G; ++g) {
+            if (!ey[g]) return MVK_EINVAL;
+            if (ey[g]->count != ey[0]->count || ey[g]->t != ey[0]->t) return MVK_EINVAL;
+        }
+        ny = ey[0]->count;
+        ty = ey[0]->t;
+    }
+    if (ny) {
+        if (!R || !U) return MVK_EINVAL;
+        for (uint32_t g = 0; g < G; ++g) {
+            const mvk_status st = check_challenges(keys[g], ey[g]);
+            if (st) return st;
+            if (!R[g] || !U[g] || !keys[g]->Q) return MVK_EINVAL;
+            eyi[g] = ey[g]->idx;
+            eyv[g] = ey[g]->val;
+        }
+    }
+    hipStream_t s = (hipStream_t)stream;
+    if (nx == 0 && ny == 0) return done_flag ? hip_status(launch_flag_signal(done_flag, done_value, s)) : MVK_OK;
+    const size_t Nx = (size_t)key.cx.r * key.n, Ny = (size_t)key.cy.r * key.m;
+    size_t scratch = 0;
+    if (nx) scratch = syn_scratch_bytes(nx, Nx);
+    if (ny && syn_scratch_bytes(ny, Ny) > scratch) scratch = syn_scratch_bytes(ny, Ny);
+    void* ws = nullptr;
+    uint32_t* ctrl = nullptr;
+    mvk_status st = workspace(s, scratch, &ws, &ctrl, 4 * (kPrepCounterWord + prep_ctrl_words(keys, G, nx, ny)));
+    if (st) return st;
+    return hip_status(launch_client_prepare_group(G, keys, nx ? ex->idx : nullptr, nx ? ex->val : nullptr,
+                                                  nx ? ex->t : 0u, nx, eyi, eyv, ty, ny, Mx, My, R, U,
+                                                  (uint32_t*)ws, &ctrl[kPrepCounterWord], done_flag, done_value, s));
+}
+
 mvk_status mvk_encode_masked(const mvk_key* key, const uint32_t* X, uint32_t B, const uint32_t* Mx, uint32_t* Xhat,
                              uint32_t* ready_flag, uint32_t ready_value, uint32_t timeout_us, uint32_t* timed_out,
                              void* stream) {
@@ -605,6 +665,39 @@ mvk_status mvk_decode_verify_masked(const mvk_key* key, const uint32_t* Xhat, co
     if (st) return st;
     return hip_status(launch_decode_verify_masked(key->m, key->n, Xhat, Yhat, B, My, ell, R, U, Y, ctrl, vL, vR,
                                                   accept, s));
+}
+
+mvk_status mvk_decode_verify_masked_group(uint32_t G, const mvk_key* const* keys, const uint32_t* Xhat, uint32_t B,
+                                          const uint32_t* const* Yhat, const uint32_t* const* My, uint32_t ell,
+                                          const uint32_t* const* R, const uint32_t* const* U, uint32_t* const* Y,
+                                          uint32_t* const* vL, uint32_t* const* vR, uint32_t* const* accept,
+                                          void* stream) {
+    if (G == 0 || G > MVK_MAX_GROUP || !keys || !Yhat || !My || !R || !U || !Y || !accept) return MVK_EINVAL;
+    for (uint32_t g = 0; g < G; ++g) {
+        const mvk_status st = check_key(keys[g]);
+        if (st) return st;
+        if (keys[g]->m != keys[0]->m || keys[g]->n != keys[0]->n) return MVK_EINVAL;
+    }
+    if (B == 0) return MVK_OK;
+    if (!Xhat || ell == 0) return MVK_EINVAL;
+    for (uint32_t g = 0; g < G; ++g)
+        if (!Yhat[g] || !My[g] || !R[g] || !U[g] || !Y[g] || !accept[g]) return MVK_EINVAL;
+    if (ell > kMaxEll || B > 65535u) return MVK_ERANGE;
+    const uint32_t m = keys[0]->m, n = keys[0]->n;
+    hipStream_t s = (hipStream_t)stream;
+    if (validate_mode()) {
+        mvk_status st = check_canonical(Xhat, (size_t)B * n, s);
+        for (uint32_t g = 0; g < G && !st; ++g)
+            st = check_all(s, {{Yhat[g], (size_t)B * m}, {My[g], (size_t)B * m}, {R[g], (size_t)ell * m},
+                               {U[g], (size_t)ell * n}});
+        if (st) return st;
+    }
+    void* ws = nullptr;
+    uint32_t* ctrl = nullptr;
+    const mvk_status st = workspace(s, 0, &ws, &ctrl, 4 * G * dv_group_ctrl_stride(m, n, B, ell));
+    if (st) return st;
+    return hip_status(launch_decode_verify_masked_group(G, m, n, Xhat, B, Yhat, My, ell, R, U, Y, vL, vR, accept,
+                                                        ctrl, s));
 }
 
 mvk_status mvk_flag_signal(uint32_t* flag, uint32_t value, void* stream) {

@@ -610,19 +610,40 @@ __device__ __forceinline__ uint32_t wave_xreduce_mod(uint32_t (&a)[V], int lane)
 // b, repetition q: nsub of them, used by element block mod nsub); the last
 // workgroup (count.h) compares.  The host picks PER and C so that the grid
 // has a few hundred workgroups where the problem allows.
+//
+// A launch may cover G <= kMaxGroup problems that share the queries Xhat
+// (several matrices applied to one input): problem g = blockIdx.y has its own
+// responses, masks, challenge vectors and outputs (DvGroup) and its own
+// control region, ctrl + g * ctrl_stride words.
 constexpr int kWideThreads = 256;
+struct DvGroup {
+    const uint32_t* Yhat[kMaxGroup];
+    const uint32_t* My[kMaxGroup];
+    const uint32_t* R[kMaxGroup];
+    const uint32_t* U[kMaxGroup];
+    uint32_t* Y[kMaxGroup];
+    uint32_t* vL[kMaxGroup];
+    uint32_t* vR[kMaxGroup];
+    uint32_t* accept[kMaxGroup];
+};
 template <int EL, int C, int PER>
 __global__ __launch_bounds__(kWideThreads) void decode_verify_wide(
-    uint32_t m, uint32_t n, const uint32_t* __restrict__ Xhat, const uint32_t* __restrict__ Yhat, uint32_t B,
-    const uint32_t* __restrict__ My, uint32_t ell, const uint32_t* __restrict__ R, const uint32_t* __restrict__ U,
-    uint32_t* __restrict__ Y, unsigned long long* accL, unsigned long long* accR, uint32_t nsub, uint32_t neb,
-    uint32_t* ctrl, uint32_t slots, uint32_t* __restrict__ vL, uint32_t* __restrict__ vR,
-    uint32_t* __restrict__ accept) {
+    uint32_t m, uint32_t n, const uint32_t* __restrict__ Xhat, uint32_t B, uint32_t ell, const DvGroup grp,
+    size_t acc_word, uint32_t nsub, uint32_t neb, uint32_t* ctrl0, size_t ctrl_stride, uint32_t slots) {
     constexpr int NW = kWideThreads / 64, V = 2 * EL * C;
     constexpr int kWidePer = PER;
     constexpr uint32_t kWideElems = kWideThreads * PER;
     __shared__ uint32_t red[NW][V];
     __shared__ uint32_t last;
+    const uint32_t g = blockIdx.y;
+    const uint32_t* __restrict__ Yhat = grp.Yhat[g];
+    const uint32_t* __restrict__ My = grp.My[g];
+    const uint32_t* __restrict__ R = grp.R[g];
+    const uint32_t* __restrict__ U = grp.U[g];
+    uint32_t* __restrict__ Y = grp.Y[g];
+    uint32_t* ctrl = ctrl0 + g * ctrl_stride;
+    unsigned long long* accL = reinterpret_cast<unsigned long long*>(ctrl + acc_word);
+    unsigned long long* accR = accL + (size_t)ell * B * nsub;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const uint32_t eb = blockIdx.x % neb, b0 = (blockIdx.x / neb) * C;
     const uint32_t base = eb * kWideElems + (uint32_t)tid;
@@ -685,7 +706,7 @@ __global__ __launch_bounds__(kWideThreads) void decode_verify_wide(
             atomicAdd(&acc[((size_t)q * B + b0 + c) * nsub + eb % nsub], (unsigned long long)tot);
         }
     }
-    finish(B, ell, nsub, accL, accR, ctrl, slots, nullptr, nullptr, vL, vR, accept, &last);
+    finish(B, ell, nsub, accL, accR, ctrl, slots, nullptr, nullptr, grp.vL[g], grp.vR[g], grp.accept[g], &last);
 }
 
 template <int U, int E>
@@ -821,6 +842,55 @@ hipError_t launch_decode_verify(const uint32_t* PT, const uint32_t* Q, uint32_t 
     return hipGetLastError();
 }
 
+namespace {
+// The decode_verify_wide configuration for a problem (ell <= 4): element
+// blocks x column groups, all loads of a workgroup in flight together: 4
+// elements per thread and 16 / EL columns per workgroup, or (grids below 256
+// workgroups) 1 element and 4 / EL columns.
+struct WideShape {
+    uint32_t el, per, cols, neb;
+    uint64_t grid;
+};
+WideShape wide_shape(uint32_t m, uint32_t n, uint32_t B, uint32_t ell) {
+    const uint32_t len = m > n ? m : n;
+    const uint32_t el = ell <= 2 ? 2u : 4u;
+    const bool wide = (uint64_t)ceil_div(len, 4u * kWideThreads) * ceil_div(B, 16u / el) >= 256u;
+    WideShape w;
+    w.el = el;
+    w.per = wide ? 4u : 1u;
+    w.cols = wide ? 16u / el : 4u / el;
+    w.neb = ceil_div(len, w.per * kWideThreads);
+    w.grid = (uint64_t)w.neb * ceil_div(B, w.cols);
+    return w;
+}
+
+bool takes_small(uint32_t m, uint32_t n, uint32_t B, uint32_t ell) {
+    return (uint64_t)B * ((uint64_t)m + n) <= kSmallDvWords && ell <= 4;
+}
+
+// decode_verify_wide over G problems (grid.y = G); each control region as
+// dv_layout(m, n, B, ell), ctrl_stride words apart.
+hipError_t launch_wide(uint32_t m, uint32_t n, const uint32_t* Xhat, uint32_t B, uint32_t ell, const DvGroup& grp,
+                       uint32_t G, uint32_t* ctrl, size_t ctrl_stride, hipStream_t s) {
+    const DvLayout l = dv_layout(m, n, B, ell);
+    const WideShape w = wide_shape(m, n, B, ell);
+    if (w.grid > 0x7fffffffu) return hipErrorInvalidValue;
+    const uint32_t slots = count_slots((uint32_t)w.grid);
+    if (count_words(slots) > l.acc_word) return hipErrorInvalidValue;  // the layout holds the counters
+    const dim3 grid((uint32_t)w.grid, G);
+#define MVK_DVW(EL, C, PER)                                                                                 \
+    hipLaunchKernelGGL((decode_verify_wide<EL, C, PER>), grid, dim3(kWideThreads), 0, s, m, n, Xhat, B, ell, \
+                       grp, l.acc_word, l.nsub, w.neb, ctrl, ctrl_stride, slots)
+    if (w.el == 2) {
+        if (w.per == 4) MVK_DVW(2, 8, 4); else MVK_DVW(2, 2, 1);
+    } else {
+        if (w.per == 4) MVK_DVW(4, 4, 4); else MVK_DVW(4, 1, 1);
+    }
+#undef MVK_DVW
+    return hipGetLastError();
+}
+}  // namespace
+
 hipError_t launch_decode_verify_masked(uint32_t m, uint32_t n, const uint32_t* Xhat, const uint32_t* Yhat,
                                        uint32_t B, const uint32_t* My, uint32_t ell, const uint32_t* r,
                                        const uint32_t* U, uint32_t* Y, uint32_t* ctrl, uint32_t* vL, uint32_t* vR,
@@ -829,7 +899,7 @@ hipError_t launch_decode_verify_masked(uint32_t m, uint32_t n, const uint32_t* X
     const DvLayout l = dv_layout(m, n, B, ell);
     unsigned long long* acc = reinterpret_cast<unsigned long long*>(ctrl + l.acc_word);
     uint32_t* counter = ctrl;
-    if ((uint64_t)B * ((uint64_t)m + n) <= kSmallDvWords && ell <= 4) {
+    if (takes_small(m, n, B, ell)) {
         // four elements per thread, one pass per column: a single workgroup up
         // to 4096 elements (no accumulators or counter), else up to 8.  (One
         // workgroup with all of a column's loads in flight beat four with one
@@ -845,29 +915,16 @@ hipError_t launch_decode_verify_masked(uint32_t m, uint32_t n, const uint32_t* X
         return hipGetLastError();
     }
     if (ell <= 4) {
-        // element blocks x column groups, all loads of a workgroup in flight
-        // together: 4 elements per thread and 16 / EL columns per workgroup, or
-        // (grids below 256 workgroups) 1 element and 4 / EL columns
-        const uint32_t len = m > n ? m : n;
-        const uint32_t el = ell <= 2 ? 2u : 4u;
-        bool wide = (uint64_t)ceil_div(len, 4u * kWideThreads) * ceil_div(B, 16u / el) >= 256u;
-        const uint32_t per = wide ? 4u : 1u, cols = wide ? 16u / el : 4u / el;
-        const uint32_t neb = ceil_div(len, per * kWideThreads);
-        const uint64_t grid = (uint64_t)neb * ceil_div(B, cols);
-        if (grid > 0x7fffffffu) return hipErrorInvalidValue;
-        const uint32_t slots = count_slots((uint32_t)grid);
-        if (count_words(slots) > l.acc_word) return hipErrorInvalidValue;  // the layout holds the counters
-#define MVK_DVW(EL, C, PER)                                                                                  \
-    hipLaunchKernelGGL((decode_verify_wide<EL, C, PER>), dim3((uint32_t)grid), dim3(kWideThreads), 0, s, m, n,  \
-                       Xhat, Yhat, B, My, ell, r, U, Y, acc, acc + (size_t)ell * B * l.nsub, l.nsub, neb, ctrl,  \
-                       slots, vL, vR, accept)
-        if (el == 2) {
-            if (wide) MVK_DVW(2, 8, 4); else MVK_DVW(2, 2, 1);
-        } else {
-            if (wide) MVK_DVW(4, 4, 4); else MVK_DVW(4, 1, 1);
-        }
-#undef MVK_DVW
-        return hipGetLastError();
+        DvGroup grp{};
+        grp.Yhat[0] = Yhat;
+        grp.My[0] = My;
+        grp.R[0] = r;
+        grp.U[0] = U;
+        grp.Y[0] = Y;
+        grp.vL[0] = vL;
+        grp.vR[0] = vR;
+        grp.accept[0] = accept;
+        return launch_wide(m, n, Xhat, B, ell, grp, 1, ctrl, 0, s);
     }
     const uint32_t nblkL = ceil_div(n, kCols), nblkR = ceil_div(m, kCols);
     const uint32_t grid = B * nblkR + nblkL;
@@ -875,6 +932,40 @@ hipError_t launch_decode_verify_masked(uint32_t m, uint32_t n, const uint32_t* X
                        Xhat, Yhat, B, nullptr, nullptr, 0u, nullptr, nullptr, 0u, ell, r, Y, acc,
                        acc + (size_t)ell * B * l.nsub, l.nsub, nblkR, ctrl, count_slots(grid), vL, vR, accept, My, U);
     return hipGetLastError();
+}
+
+size_t dv_group_ctrl_stride(uint32_t m, uint32_t n, uint32_t B, uint32_t ell) {
+    return (dv_ctrl_bytes(m, n, B, ell) + 255) / 256 * 64;  // words, whole 256-byte lines
+}
+
+hipError_t launch_decode_verify_masked_group(uint32_t G, uint32_t m, uint32_t n, const uint32_t* Xhat, uint32_t B,
+                                             const uint32_t* const* Yhat, const uint32_t* const* My, uint32_t ell,
+                                             const uint32_t* const* R, const uint32_t* const* U, uint32_t* const* Y,
+                                             uint32_t* const* vL, uint32_t* const* vR, uint32_t* const* accept,
+                                             uint32_t* ctrl, hipStream_t s) {
+    if (G == 0 || G > kMaxGroup || ell == 0 || ell > (uint32_t)kMaxEll) return hipErrorInvalidValue;
+    const size_t stride = dv_group_ctrl_stride(m, n, B, ell);
+    if (!takes_small(m, n, B, ell) && ell <= 4) {
+        DvGroup grp{};
+        for (uint32_t g = 0; g < G; ++g) {
+            grp.Yhat[g] = Yhat[g];
+            grp.My[g] = My[g];
+            grp.R[g] = R[g];
+            grp.U[g] = U[g];
+            grp.Y[g] = Y[g];
+            grp.vL[g] = vL ? vL[g] : nullptr;
+            grp.vR[g] = vR ? vR[g] : nullptr;
+            grp.accept[g] = accept[g];
+        }
+        return launch_wide(m, n, Xhat, B, ell, grp, G, ctrl, stride, s);
+    }
+    for (uint32_t g = 0; g < G; ++g) {
+        const hipError_t e = launch_decode_verify_masked(m, n, Xhat, Yhat[g], B, My[g], ell, R[g], U[g], Y[g],
+                                                         ctrl + g * stride, vL ? vL[g] : nullptr,
+                                                         vR ? vR[g] : nullptr, accept[g], s);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 }  // namespace mvk

@@ -109,6 +109,16 @@ hipError_t launch_decode_verify_masked(uint32_t m, uint32_t n, const uint32_t* X
                                        const uint32_t* U, uint32_t* Y, uint32_t* ctrl, uint32_t* vL, uint32_t* vR,
                                        uint32_t* accept, hipStream_t s);
 
+// The same for G <= kMaxGroup problems sharing Xhat (one launch where the
+// problem takes the wide kernel, else one per problem); ctrl: G control
+// regions of dv_group_ctrl_stride words each.  vL, vR may be null.
+size_t dv_group_ctrl_stride(uint32_t m, uint32_t n, uint32_t B, uint32_t ell);
+hipError_t launch_decode_verify_masked_group(uint32_t G, uint32_t m, uint32_t n, const uint32_t* Xhat, uint32_t B,
+                                             const uint32_t* const* Yhat, const uint32_t* const* My, uint32_t ell,
+                                             const uint32_t* const* R, const uint32_t* const* U, uint32_t* const* Y,
+                                             uint32_t* const* vL, uint32_t* const* vR, uint32_t* const* accept,
+                                             uint32_t* ctrl, hipStream_t s);
+
 // prepare.hip ---------------------------------------------------------------
 // Mx, My for nx noise vectors and R, U for ny challenges (either count may
 // be 0).  scratch: max(nx * 2 * Nx, ny * 2 * Ny) words when that block length
@@ -117,6 +127,16 @@ hipError_t launch_decode_verify_masked(uint32_t m, uint32_t n, const uint32_t* X
 // prep_ctrl_words(key, nx, ny) words of completion counters (count.h), zero
 // before the launch (left zero).
 size_t prep_ctrl_words(const mvk_key& key, uint32_t nx, uint32_t ny);
+size_t prep_ctrl_words(const mvk_key* const* keys, uint32_t G, uint32_t nx, uint32_t ny);
+// The same for G <= kMaxGroup keys of one shape and one privacy code that share
+// the noise vectors (Mx once; My[g], R[g], Uq[g] per key, with the challenges
+// ey_idx[g], ey_val[g]).
+hipError_t launch_client_prepare_group(uint32_t G, const mvk_key* const* keys, const uint32_t* ex_idx,
+                                       const uint32_t* ex_val, uint32_t tx, uint32_t nx,
+                                       const uint32_t* const* ey_idx, const uint32_t* const* ey_val, uint32_t ty,
+                                       uint32_t ny, uint32_t* Mx, uint32_t* const* My, uint32_t* const* R,
+                                       uint32_t* const* Uq, uint32_t* scratch, uint32_t* counter, uint32_t* done,
+                                       uint32_t done_value, hipStream_t s);
 hipError_t launch_client_prepare(const mvk_key& key, const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx,
                                  uint32_t nx, const uint32_t* ey_idx, const uint32_t* ey_val, uint32_t ty,
                                  uint32_t ny, uint32_t* Mx, uint32_t* My, uint32_t* R, uint32_t* Uq,

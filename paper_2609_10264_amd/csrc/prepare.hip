@@ -114,31 +114,37 @@ constexpr size_t prep_lds_words() {
 }
 
 struct PrepArgs {
-    // syndromes in this launch: nsx vectors of code x (Mx), nsy of code y (R)
+    // G problems (keys of one shape and one privacy code) share the noise
+    // vectors and their input mask Mx; each has its own verification code,
+    // challenges, P^T, Q and outputs My, R, Uq.
+    uint32_t G;
+    // syndromes in this launch: nsx noise vectors of code x (Mx); nsy
+    // challenges of code y per problem (R)
     uint32_t nsx, nsy;
     uint32_t n, rx, m, ry;
     const uint32_t *xpi1, *xpi2, *xv1, *xv2;
-    const uint32_t *ypi1, *ypi2, *yv1, *yv2;
+    const uint32_t *ypi1[kMaxGroup], *ypi2[kMaxGroup], *yv1[kMaxGroup], *yv2[kMaxGroup];
     const uint32_t *ex_idx, *ex_val;
     uint32_t tx, nx;  // nx noise vectors (My items), tx terms each
-    const uint32_t *ey_idx, *ey_val;
-    uint32_t ty, ny;  // ny challenges (U items), ty terms each
+    const uint32_t *ey_idx[kMaxGroup], *ey_val[kMaxGroup];
+    uint32_t ty, ny;  // ny challenges per problem (U items), ty terms each
     uint32_t nbm, nbn;  // gather_cols(VEC)-column blocks of m and n
-    const uint32_t *PT, *Q;
+    const uint32_t *PT[kMaxGroup], *Q[kMaxGroup];
     uint32_t* Mx;
-    uint32_t* My;
-    uint32_t* R;
-    uint32_t* Uq;
+    uint32_t* My[kMaxGroup];
+    uint32_t* R[kMaxGroup];
+    uint32_t* Uq[kMaxGroup];
     uint32_t* counter;  // SIG: completion counters (count.h; zero before and after the launch)
     uint32_t slots;
     uint32_t* done;     // SIG: set to done_value once every output is stored
     uint32_t done_value;
 };
 
-// Workgroups [0, nsx) and [nsx, nsx + nsy): one syndrome each (U > 0; the
-// whole block in LDS); the rest: kQuarters gather items each, first the
-// nx * nbm items of My (rows of PT), then the ny * nbn items of U (rows of Q).
-// VEC: m and n are multiples of 4 and PT, Q 16-byte aligned.
+// Workgroups [0, nsx): one noise syndrome each; [nsx, nsx + G * nsy): one
+// challenge syndrome each, problem by problem (U > 0; the whole block in
+// LDS); the rest: kQuarters gather items each, per problem first the
+// nx * nbm items of My (rows of its PT), then the ny * nbn items of U (rows
+// of its Q).  VEC: m and n are multiples of 4 and every PT, Q 16-byte aligned.
 // SIG: every output is stored device-coherently; each workgroup waits for its
 // stores to complete (vmcnt 0) before the barrier and then counts itself done
 // (count.h); the last one sets the done flag, so a kernel of another stream
@@ -153,29 +159,34 @@ __global__ __launch_bounds__(kPrepThreads) void client_prepare_kernel(PrepArgs a
             syn::syn_block<true, U, kPrepThreads, SIG>(bid, a.n, a.rx, a.xpi1, a.xpi2, a.xv1, a.xv2, nullptr,
                                                        a.ex_idx, a.ex_val, a.tx, nullptr, a.Mx, lds);
             gather = false;
-        } else if (bid < a.nsx + a.nsy) {
-            syn::syn_block<true, U, kPrepThreads, SIG>(bid - a.nsx, a.m, a.ry, a.ypi1, a.ypi2, a.yv1, a.yv2,
-                                                       nullptr, a.ey_idx, a.ey_val, a.ty, nullptr, a.R, lds);
+        } else if (bid < a.nsx + a.G * a.nsy) {
+            const uint32_t k = bid - a.nsx, g = k / a.nsy;
+            syn::syn_block<true, U, kPrepThreads, SIG>(k - g * a.nsy, a.m, a.ry, a.ypi1[g], a.ypi2[g], a.yv1[g],
+                                                       a.yv2[g], nullptr, a.ey_idx[g], a.ey_val[g], a.ty, nullptr,
+                                                       a.R[g], lds);
             gather = false;
         } else {
-            bid -= a.nsx + a.nsy;
+            bid -= a.nsx + a.G * a.nsy;
         }
     }
     if (gather) {
         const int quarter = threadIdx.x / kQuarter;
         uint64_t* part = reinterpret_cast<uint64_t*>(lds) + quarter * gather_part(VEC);
         constexpr uint32_t cols = gather_cols(VEC);
-        const uint32_t item = bid * kQuarters + (uint32_t)quarter;
+        uint32_t item = bid * kQuarters + (uint32_t)quarter;
         const uint32_t nbm = a.nbm, nbn = a.nbn;
-        const uint32_t ix = a.nx * nbm, iy = a.ny * nbn;
-        if (item < ix) {
+        const uint32_t ix = a.nx * nbm, iy = a.ny * nbn, per = ix + iy;
+        const uint32_t g = per ? item / per : a.G;
+        item -= g < a.G ? g * per : 0u;
+        if (g < a.G && item < ix) {
             const uint32_t b = item / nbm, cb = item % nbm;
-            gather_item<SIG, VEC>(a.PT, a.m, a.rx * a.n, a.ex_idx + (size_t)b * a.tx, a.ex_val + (size_t)b * a.tx,
-                                  a.tx, a.My + (size_t)b * a.m, cb * cols, true, part);
-        } else if (item < ix + iy) {
+            gather_item<SIG, VEC>(a.PT[g], a.m, a.rx * a.n, a.ex_idx + (size_t)b * a.tx,
+                                  a.ex_val + (size_t)b * a.tx, a.tx, a.My[g] + (size_t)b * a.m, cb * cols, true, part);
+        } else if (g < a.G) {
             const uint32_t q = (item - ix) / nbn, cb = (item - ix) % nbn;
-            gather_item<SIG, VEC>(a.Q, a.n, a.ry * a.m, a.ey_idx + (size_t)q * a.ty, a.ey_val + (size_t)q * a.ty,
-                                  a.ty, a.Uq + (size_t)q * a.n, cb * cols, true, part);
+            gather_item<SIG, VEC>(a.Q[g], a.n, a.ry * a.m, a.ey_idx[g] + (size_t)q * a.ty,
+                                  a.ey_val[g] + (size_t)q * a.ty, a.ty, a.Uq[g] + (size_t)q * a.n, cb * cols, true,
+                                  part);
         } else {
             gather_item<SIG, VEC>(nullptr, 0u, 1u, nullptr, nullptr, 0u, nullptr, 0u, false, part);
         }
@@ -322,36 +333,47 @@ uint32_t prep_u(uint64_t N) {
 // workgroups (a quarter as many wider items then still keep the chip busy;
 // below, more and narrower items spread the gathers over more compute units:
 // at 4096 x 4096 with one column the wider items cost a microsecond per step).
-bool prep_vec(const mvk_key& key, uint32_t nx, uint32_t ny) {
-    if (key.m % 4 != 0 || key.n % 4 != 0 || ((uintptr_t)key.PT & 15) != 0 || ((uintptr_t)key.Q & 15) != 0)
-        return false;
-    const uint64_t items = (uint64_t)nx * ceil_div(key.m, gather_cols(false)) +
-                           (uint64_t)ny * ceil_div(key.n, gather_cols(false));
+bool prep_vec(const mvk_key* const* keys, uint32_t G, uint32_t nx, uint32_t ny) {
+    const mvk_key& key = *keys[0];
+    if (key.m % 4 != 0 || key.n % 4 != 0) return false;
+    for (uint32_t g = 0; g < G; ++g)
+        if (((uintptr_t)keys[g]->PT & 15) != 0 || ((uintptr_t)keys[g]->Q & 15) != 0) return false;
+    const uint64_t items = (uint64_t)G * ((uint64_t)nx * ceil_div(key.m, gather_cols(false)) +
+                                          (uint64_t)ny * ceil_div(key.n, gather_cols(false)));
     return items > 256u * kQuarters;
 }
 
 // Workgroups of client_prepare_kernel: one per syndrome short enough for one
 // workgroup, then the gather items, kQuarters per workgroup.
-uint64_t prep_grid(const mvk_key& key, uint32_t nx, uint32_t ny) {
+uint64_t prep_grid(const mvk_key* const* keys, uint32_t G, uint32_t nx, uint32_t ny) {
+    const mvk_key& key = *keys[0];
     const uint64_t Nx = (uint64_t)key.cx.r * key.n, Ny = (uint64_t)key.cy.r * key.m;
     const uint32_t ux = nx ? prep_u(Nx) : 0u, uy = ny ? prep_u(Ny) : 0u;
-    const uint32_t cols = gather_cols(prep_vec(key, nx, ny));
-    const uint64_t items = (uint64_t)nx * ceil_div(key.m, cols) + (uint64_t)ny * ceil_div(key.n, cols);
-    return (ux ? nx : 0u) + (uy ? ny : 0u) + (items + kQuarters - 1) / kQuarters;
+    const uint32_t cols = gather_cols(prep_vec(keys, G, nx, ny));
+    const uint64_t items = (uint64_t)G * ((uint64_t)nx * ceil_div(key.m, cols) + (uint64_t)ny * ceil_div(key.n, cols));
+    return (ux ? nx : 0u) + (uy ? (uint64_t)G * ny : 0u) + (items + kQuarters - 1) / kQuarters;
 }
 
 }  // namespace
 
-size_t prep_ctrl_words(const mvk_key& key, uint32_t nx, uint32_t ny) {
-    const uint64_t grid = prep_grid(key, nx, ny);
+size_t prep_ctrl_words(const mvk_key* const* keys, uint32_t G, uint32_t nx, uint32_t ny) {
+    const uint64_t grid = prep_grid(keys, G, nx, ny);
     return count_words(count_slots(grid > 0x7fffffffu ? 0x7fffffffu : (uint32_t)grid));
 }
 
-hipError_t launch_client_prepare(const mvk_key& key, const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx,
-                                 uint32_t nx, const uint32_t* ey_idx, const uint32_t* ey_val, uint32_t ty,
-                                 uint32_t ny, uint32_t* Mx, uint32_t* My, uint32_t* R, uint32_t* Uq,
-                                 uint32_t* scratch, uint32_t* counter, uint32_t* done, uint32_t done_value,
-                                 hipStream_t s) {
+size_t prep_ctrl_words(const mvk_key& key, uint32_t nx, uint32_t ny) {
+    const mvk_key* k = &key;
+    return prep_ctrl_words(&k, 1, nx, ny);
+}
+
+hipError_t launch_client_prepare_group(uint32_t G, const mvk_key* const* keys, const uint32_t* ex_idx,
+                                       const uint32_t* ex_val, uint32_t tx, uint32_t nx,
+                                       const uint32_t* const* ey_idx, const uint32_t* const* ey_val, uint32_t ty,
+                                       uint32_t ny, uint32_t* Mx, uint32_t* const* My, uint32_t* const* R,
+                                       uint32_t* const* Uq, uint32_t* scratch, uint32_t* counter, uint32_t* done,
+                                       uint32_t done_value, hipStream_t s) {
+    if (G == 0 || G > kMaxGroup) return hipErrorInvalidValue;
+    const mvk_key& key = *keys[0];
     const uint64_t Nx = (uint64_t)key.cx.r * key.n, Ny = (uint64_t)key.cy.r * key.m;
     const uint32_t ux = nx ? prep_u(Nx) : 0u, uy = ny ? prep_u(Ny) : 0u;
     // syndromes too long for one workgroup run in their own (segmented) launches first
@@ -360,10 +382,13 @@ hipError_t launch_client_prepare(const mvk_key& key, const uint32_t* ex_idx, con
         if (e != hipSuccess) return e;
     }
     if (ny && !uy) {
-        const hipError_t e = launch_syn_sparse(key.cy, ey_idx, ey_val, ty, ny, nullptr, scratch, R, s);
-        if (e != hipSuccess) return e;
+        for (uint32_t g = 0; g < G; ++g) {
+            const hipError_t e = launch_syn_sparse(keys[g]->cy, ey_idx[g], ey_val[g], ty, ny, nullptr, scratch, R[g], s);
+            if (e != hipSuccess) return e;
+        }
     }
-    PrepArgs a;
+    PrepArgs a{};
+    a.G = G;
     a.nsx = ux ? nx : 0u;
     a.nsy = uy ? ny : 0u;
     a.n = key.n;
@@ -371,16 +396,21 @@ hipError_t launch_client_prepare(const mvk_key& key, const uint32_t* ex_idx, con
     a.m = key.m;
     a.ry = key.cy.r;
     a.xpi1 = key.cx.pi1, a.xpi2 = key.cx.pi2, a.xv1 = key.cx.v1, a.xv2 = key.cx.v2;
-    a.ypi1 = key.cy.pi1, a.ypi2 = key.cy.pi2, a.yv1 = key.cy.v1, a.yv2 = key.cy.v2;
     a.ex_idx = ex_idx, a.ex_val = ex_val, a.tx = tx, a.nx = nx;
-    a.ey_idx = ey_idx, a.ey_val = ey_val, a.ty = ty, a.ny = ny;
-    const bool vec = prep_vec(key, nx, ny);
+    a.ty = ty, a.ny = ny;
+    for (uint32_t g = 0; g < G; ++g) {
+        const mvk_code& cy = keys[g]->cy;
+        a.ypi1[g] = cy.pi1, a.ypi2[g] = cy.pi2, a.yv1[g] = cy.v1, a.yv2[g] = cy.v2;
+        a.ey_idx[g] = ny ? ey_idx[g] : nullptr, a.ey_val[g] = ny ? ey_val[g] : nullptr;
+        a.PT[g] = keys[g]->PT, a.Q[g] = keys[g]->Q;
+        a.My[g] = nx ? My[g] : nullptr, a.R[g] = ny ? R[g] : nullptr, a.Uq[g] = ny ? Uq[g] : nullptr;
+    }
+    const bool vec = prep_vec(keys, G, nx, ny);
     a.nbm = ceil_div(key.m, gather_cols(vec)), a.nbn = ceil_div(key.n, gather_cols(vec));
-    a.PT = key.PT, a.Q = key.Q;
-    a.Mx = Mx, a.My = My, a.R = R, a.Uq = Uq;
+    a.Mx = Mx;
     a.counter = counter, a.done = done, a.done_value = done_value;
     const uint32_t U = ux > uy ? ux : uy;
-    const uint64_t grid = prep_grid(key, nx, ny);
+    const uint64_t grid = prep_grid(keys, G, nx, ny);
     if (grid == 0) return hipSuccess;
     if (grid > 0x7fffffffu) return hipErrorInvalidValue;
     a.slots = count_slots((uint32_t)grid);
@@ -405,6 +435,16 @@ hipError_t launch_client_prepare(const mvk_key& key, const uint32_t* ex_idx, con
 #undef MVK_PREP
 #undef MVK_PREP_V
     return hipGetLastError();
+}
+
+hipError_t launch_client_prepare(const mvk_key& key, const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx,
+                                 uint32_t nx, const uint32_t* ey_idx, const uint32_t* ey_val, uint32_t ty,
+                                 uint32_t ny, uint32_t* Mx, uint32_t* My, uint32_t* R, uint32_t* Uq,
+                                 uint32_t* scratch, uint32_t* counter, uint32_t* done, uint32_t done_value,
+                                 hipStream_t s) {
+    const mvk_key* k = &key;
+    return launch_client_prepare_group(1, &k, ex_idx, ex_val, tx, nx, &ey_idx, &ey_val, ty, ny, Mx, &My, &R, &Uq,
+                                       scratch, counter, done, done_value, s);
 }
 
 hipError_t launch_gather_rows(const uint32_t* M, uint32_t ld, uint32_t nrows, const uint32_t* idx,

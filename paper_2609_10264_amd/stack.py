@@ -28,8 +28,8 @@ from dataclasses import dataclass, field
 
 import torch
 
-from . import (Code, Key, PackedW, Prepared, client_prepare, decode_verify, decode_verify_masked, encode, encode_masked,
-               keygen, pack_weights, pack_weights_group, server_eval, server_eval_group)
+from . import (Code, Key, PackedW, Prepared, client_prepare_group, decode_verify, decode_verify_masked_group, encode,
+               encode_masked, keygen, pack_weights, pack_weights_group, server_eval, server_eval_group)
 
 # (name, m, n, input group)
 PROJECTIONS = (
@@ -132,52 +132,84 @@ def run_layer(layer: Layer, X: dict, ex: dict, ey: dict, tamper=None, stream=Non
     return out
 
 
+def prepare_input(layer: Layer, group: str, ex: dict, ey: dict, preps: dict, flag: torch.Tensor | None = None,
+                  stream=None) -> None:
+    """Client preparation for the projections fed by one input: the input
+    mask Gx e of its noise once, and per projection the output mask P e and
+    the challenge vectors Gy e_q, e_q^T Q (one client_prepare_group launch).
+    flag: an int32 device word set to 1 once every output is visible
+    device-wide."""
+    names = stage(group)
+    B = ex[group][0].shape[0]
+    for nm in names:
+        if nm not in preps:
+            preps[nm] = Prepared(layer.keys[nm], B, ey[nm][0].shape[0], device=ex[group][0].device)
+    client_prepare_group([layer.keys[nm] for nm in names], ex[group][0], ex[group][1], [ey[nm] for nm in names],
+                         outs=[preps[nm] for nm in names], done_flag=flag, stream=stream)
+
+
 def prepare_layer(layer: Layer, ex: dict, ey: dict, flags: torch.Tensor, out: dict | None = None,
                   stream=None) -> dict:
-    """Client preparation of one layer: for every projection the masks
-    Gx e and P e of its input's noise and the vectors Gy e_q, e_q^T Q of its
-    challenges (client_prepare).  flags: one int32 device word per projection,
-    each set to 1 once that projection's outputs are visible device-wide (in
-    call order, so the last flag covers the whole layer).  Returns
-    {name: Prepared}."""
+    """Client preparation of one layer (prepare_input for each of the four
+    inputs).  flags: one int32 device word per input, each set to 1 once that
+    input's preparation is visible device-wide (in call order, so the last
+    flag covers the whole layer).  Returns {name: Prepared}."""
     preps = out if out is not None else {}
-    for i, (name, m, n, group) in enumerate(PROJECTIONS):
-        B = ex[group][0].shape[0]
-        ell = ey[name][0].shape[0]
-        if name not in preps:
-            preps[name] = Prepared(layer.keys[name], B, ell, device=ex[group][0].device)
-        client_prepare(layer.keys[name], ex[group][0], ex[group][1], ey[name][0], ey[name][1], out=preps[name],
-                       done_flag=flags[i], stream=stream)
+    for i, group in enumerate(INPUTS):
+        prepare_input(layer, group, ex, ey, preps, flag=flags[i], stream=stream)
     return preps
+
+
+def check_stage(layer: Layer, group: str, Xhat: torch.Tensor, Yhats: dict, preps: dict, out: dict | None = None,
+                stream=None) -> dict:
+    """The client's Verify + Decrypt for the projections fed by one input (one
+    decode_verify_masked_group launch where the problem allows).  out:
+    {name: (Y, accept, vL, vR)} preallocated, or None.  Returns the same."""
+    names = stage(group)
+    B = Xhat.shape[0]
+    dev_ = Xhat.device
+    res = {}
+    for nm in names:
+        if out is not None:
+            res[nm] = out[nm]
+        else:
+            ell = preps[nm].ell
+            m = layer.keys[nm].m
+            res[nm] = (torch.empty((B, m), dtype=torch.int32, device=dev_),
+                       torch.empty((B,), dtype=torch.int32, device=dev_),
+                       torch.empty((ell, B), dtype=torch.int32, device=dev_),
+                       torch.empty((ell, B), dtype=torch.int32, device=dev_))
+    decode_verify_masked_group([layer.keys[nm] for nm in names], Xhat, [Yhats[nm] for nm in names],
+                               [preps[nm] for nm in names], Ys=[res[nm][0] for nm in names],
+                               vLs=[res[nm][2] for nm in names], vRs=[res[nm][3] for nm in names],
+                               accepts=[res[nm][1] for nm in names], stream=stream)
+    return res
 
 
 def run_layer_prepared(layer: Layer, X: dict, preps: dict, ready_flag: torch.Tensor | None = None,
                        timeout_us: int = 200000, timed_out: torch.Tensor | None = None, tamper=None, stream=None):
-    """The online part of a layer with prepared masks: x^ = x + Gx e per
-    input, server_eval, and decode_verify_masked per projection.  ready_flag:
-    the layer's last preparation flag; the first masked encode waits for it
-    (and clears it).  Same outputs as run_layer with the same noise and
+    """The online part of a layer with prepared masks, input by input as in
+    inference: x^ = x + Gx e, the server's products for that input (one
+    grouped launch for q, k, v and for up, gate), and their checks
+    (decode_verify_masked_group).  ready_flag: one device word (the layer's
+    last preparation flag, waited for by the first masked encode) or a list of
+    four, one per input (each masked encode waits for its own).  Every wait
+    clears its flag.  Same outputs as run_layer with the same noise and
     challenges."""
-    Xhat = {}
-    wait = ready_flag
-    for group in INPUTS:
-        name = next(p for (p, _, _, g) in PROJECTIONS if g == group)
-        Xhat[group] = encode_masked(layer.keys[name], X[group], preps[name], ready_flag=wait,
-                                    timeout_us=timeout_us, timed_out=timed_out, stream=stream)
-        wait = None
     out = {}
-    Yhats = {}
-    for group in INPUTS:
-        Yhats.update(evaluate_stage(layer, group, Xhat[group], stream=stream))
-    for name, m, n, group in PROJECTIONS:
-        Yhat = Yhats[name]
+    for i, group in enumerate(INPUTS):
+        names = stage(group)
+        wait = ready_flag[i] if isinstance(ready_flag, (list, tuple)) else (ready_flag if i == 0 else None)
+        xh = encode_masked(layer.keys[names[0]], X[group], preps[names[0]], ready_flag=wait, timeout_us=timeout_us,
+                           timed_out=timed_out, stream=stream)
+        Yhats = evaluate_stage(layer, group, xh, stream=stream)
         if tamper is not None:
-            tamper(name, Yhat)
-        vL = torch.empty((preps[name].ell, Yhat.shape[0]), dtype=torch.int32, device=Yhat.device)
-        vR = torch.empty_like(vL)
-        Y, acc, _, _ = decode_verify_masked(layer.keys[name], Xhat[group], Yhat, preps[name], vL=vL, vR=vR,
-                                            stream=stream)
-        out[name] = (Y, acc, Xhat[group], Yhat, vL, vR)
+            for nm in names:
+                tamper(nm, Yhats[nm])
+        checked = check_stage(layer, group, xh, Yhats, preps, stream=stream)
+        for nm in names:
+            Y, acc, vL, vR = checked[nm]
+            out[nm] = (Y, acc, xh, Yhats[nm], vL, vR)
     return out
 
 
@@ -213,7 +245,7 @@ class LayerOutputs:
 
 
 def run_pass_overlapped(layers: list, inputs: list, preps: list, outs: list, main, prep_streams: list,
-                        branch_streams: list, tamper=None):
+                        branch_streams: list = (), tamper=None):
     """One pass over every layer, issued on several streams so that work
     without a data dependence runs side by side; captured on `main`, the
     streams fork from it and join it again, so a HIP graph of the pass keeps
@@ -228,9 +260,9 @@ def run_pass_overlapped(layers: list, inputs: list, preps: list, outs: list, mai
         share one input, o's input comes after the q, k, v outputs, up and
         gate share the next, down's comes last; each input's masked encode
         waits for every verification of the previous stage;
-      * within a stage the server's products run first (one launch over the
-        row stack of the projections that share the input), then every
-        projection's decode/verify on a branch of its own.
+      * within a stage the server's products (one launch over the row stack
+        of the projections that share the input), then their checks (one
+        grouped decode/verify launch), on the main stream.
     inputs[L] = (X, ex, ey) as for run_layer; preps[L]: {name: Prepared};
     outs[L]: LayerOutputs; tamper: optional callable(L, name, Yhat) on the
     branch stream between the product and its check."""
@@ -240,11 +272,10 @@ def run_pass_overlapped(layers: list, inputs: list, preps: list, outs: list, mai
 
     def prepare(L):
         _, ex, ey = inputs[L]
-        for k, (name, _, _, group) in enumerate(PROJECTIONS):
+        for k, group in enumerate(INPUTS):
             s = prep_streams[k % len(prep_streams)]
             with torch.cuda.stream(s):
-                client_prepare(layers[L].keys[name], ex[group][0], ex[group][1], ey[name][0], ey[name][1],
-                               out=preps[L][name], stream=s)
+                prepare_input(layers[L], group, ex, ey, preps[L], stream=s)
         return [s.record_event() for s in prep_streams]
 
     ready = {0: prepare(0)} if layers else {}
@@ -260,16 +291,12 @@ def run_pass_overlapped(layers: list, inputs: list, preps: list, outs: list, mai
             with torch.cuda.stream(main):
                 encode_masked(layer.keys[names[0]], X[group], preps[L][names[0]], out=o.xhat[group], stream=main)
                 evaluate_stage(layer, group, o.xhat[group], outs=o.yhat, stream=main)
-            for j, name in enumerate(names):
-                b = branch_streams[j]
-                b.wait_stream(main)
-                with torch.cuda.stream(b):
-                    if tamper is not None:
+            with torch.cuda.stream(main):
+                if tamper is not None:
+                    for name in names:
                         tamper(L, name, o.yhat[name])
-                    decode_verify_masked(layer.keys[name], o.xhat[group], o.yhat[name], preps[L][name], Y=o.y[name],
-                                         vL=o.vl[name], vR=o.vr[name], accept=o.accept[name], stream=b)
-            for j in range(len(names)):
-                main.wait_stream(branch_streams[j])
+                check_stage(layer, group, o.xhat[group], o.yhat, preps[L],
+                            out={nm: (o.y[nm], o.accept[nm], o.vl[nm], o.vr[nm]) for nm in names}, stream=main)
     for s in every:
         main.wait_stream(s)
 
@@ -285,6 +312,6 @@ def macs_per_layer(B: int) -> int:
     return sum(m * n for (_, m, n, _) in PROJECTIONS) * B
 
 
-__all__ = ["PROJECTIONS", "INPUTS", "Layer", "LayerOutputs", "build_layer", "evaluate_stage", "run_layer",
-           "prepare_layer", "run_layer_prepared", "run_pass_overlapped", "codes_for", "input_width", "stage",
-           "macs_per_layer", "Code"]
+__all__ = ["PROJECTIONS", "INPUTS", "Layer", "LayerOutputs", "build_layer", "evaluate_stage", "check_stage",
+           "run_layer", "prepare_input", "prepare_layer", "run_layer_prepared", "run_pass_overlapped", "codes_for",
+           "input_width", "stage", "macs_per_layer", "Code"]

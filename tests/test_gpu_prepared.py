@@ -7,7 +7,7 @@ import torch
 
 import oracle
 import synth
-from tests.gpu_util import Instance, dev, host
+from tests.gpu_util import Instance, code, dev, host
 
 pytestmark = pytest.mark.gpu
 P = synth.P
@@ -219,3 +219,57 @@ def test_verify_only_mode(cid, m, n, B, ry, ell):
         oacc, ovL, ovR = oracle.verify(inst.cy, Q, inst.X, resp, inst.eyi, inst.eyv)
         assert oacc.astype(np.uint32).tolist() == want == host(acc).tolist()
         assert np.array_equal(host(vL), ovL) and np.array_equal(host(vR), ovR)
+
+
+# ---------------------------------------------------------------------------
+# groups of keys sharing an input (one launch for several matrices)
+# ---------------------------------------------------------------------------
+def _group(G, m, n, B, r, tx, ty, ell, sub):
+    cx = synth.raa_code(synth.seed_for(60, synth.PURPOSE_CX, sub), n, r)
+    cy = synth.raa_code(synth.seed_for(60, synth.PURPOSE_CY, sub), m, r)
+    dcx, dcy = code(cx), code(cy)
+    Ws = [synth.weights(synth.seed_for(60, synth.PURPOSE_W, sub + g), m, n) for g in range(G)]
+    keys = []
+    for W in Ws:
+        k = mvk.Key.allocate(m, n, dcx, dcy)
+        mvk.keygen(k, dev(W))
+        keys.append(k)
+    exi, exv = synth.sparse(synth.seed_for(60, synth.PURPOSE_NOISE, sub), B, cx["N"], tx)
+    eys = [tuple(dev(a) for a in synth.sparse(synth.seed_for(60, synth.PURPOSE_CHAL, sub + g), ell, cy["N"], ty))
+           for g in range(G)]
+    X = synth.field_uniform(synth.seed_for(60, synth.PURPOSE_X, sub), (B, n))
+    return Ws, keys, dev(exi), dev(exv), eys, X
+
+
+@pytest.mark.parametrize("G,m,n,B,r,tx,ell", [(3, 4096, 4096, 8, 3, 64, 2), (2, 11008, 4096, 8, 3, 64, 2),
+                                              (3, 300, 200, 2, 2, 10, 3), (2, 6000, 6000, 3, 3, 40, 2),
+                                              (4, 512, 640, 16, 2, 20, 4), (1, 1000, 900, 5, 3, 30, 2)])
+def test_group_preparation_and_checks_match_one_key_at_a_time(G, m, n, B, r, tx, ell):
+    """client_prepare_group and decode_verify_masked_group give, for every key,
+    the outputs of client_prepare and decode_verify_masked, bit for bit, with a
+    tampered response in the group."""
+    print(f"group prepare/check G={G} m={m} n={n} B={B} ell={ell}", flush=True)
+    Ws, keys, exi, exv, eys, X = _group(G, m, n, B, r, tx, 31, ell, 100 * G + m % 97)
+    preps = mvk.client_prepare_group(keys, exi, exv, eys)
+    singles = [mvk.client_prepare(k, exi, exv, *ey) for k, ey in zip(keys, eys)]
+    for g in range(G):
+        for name in ("Mx", "My", "R", "U"):
+            assert torch.equal(getattr(preps[g], name), getattr(singles[g], name)), (g, name)
+    Xh = mvk.encode_masked(keys[0], dev(X), preps[0])
+    Yhs = [mvk.server_eval(dev(W), Xh) for W in Ws]
+    Yhs[G - 1][B - 1, m // 2] = (Yhs[G - 1][B - 1, m // 2].to(torch.int64) + 31337) % P
+    vLs = [torch.empty((ell, B), dtype=torch.int32, device="cuda") for _ in range(G)]
+    vRs = [torch.empty_like(v) for v in vLs]
+    Ys, accs, _, _ = mvk.decode_verify_masked_group(keys, Xh, Yhs, preps, vLs=vLs, vRs=vRs)
+    for g in range(G):
+        vL = torch.empty((ell, B), dtype=torch.int32, device="cuda")
+        vR = torch.empty_like(vL)
+        Y1, acc1, _, _ = mvk.decode_verify_masked(keys[g], Xh, Yhs[g], singles[g], vL=vL, vR=vR)
+        for a, b in ((Ys[g], Y1), (accs[g], acc1), (vLs[g], vL), (vRs[g], vR)):
+            assert torch.equal(a, b), g
+        want = [1] * B
+        if g == G - 1:
+            want[B - 1] = 0
+        assert host(accs[g]).tolist() == want, g
+    # the honest outputs decrypt to W x (oracle); the tampered column is the last one of the last key
+    assert np.array_equal(host(Ys[0])[:B - 1], oracle.server_eval(Ws[0], X)[:B - 1])

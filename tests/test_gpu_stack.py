@@ -78,7 +78,6 @@ def test_stack_layer_matches_oracle(stack_setup, L):
     stack, host_codes, cx_by_n, cy_by_m, plan, _ = stack_setup
     B, r, tx, ty, ell, cid = (CFG[k] for k in ("B", "r", "tx", "ty", "ell", "cid"))
     T = oracle.threads()
-    nproj = len(stack.PROJECTIONS)
     print(f"stack layer {L} ({T} oracle threads)", flush=True)
     sub = 100 * (L + 1)
     Wh = {name: synth.weights(synth.seed_for(cid, synth.PURPOSE_W, sub + i), m, n)
@@ -102,17 +101,18 @@ def test_stack_layer_matches_oracle(stack_setup, L):
 
     out = stack.run_layer(layer, X, ex, ey, tamper=tamper)
     # the prepared schedule: preparation stream with flags, then the online part
-    flags = torch.zeros(nproj, dtype=torch.int32, device="cuda")
+    nin = len(stack.INPUTS)
+    flags = torch.zeros(nin, dtype=torch.int32, device="cuda")
     late = torch.zeros((), dtype=torch.int32, device="cuda")
     s_prep, s_on = torch.cuda.Stream(), torch.cuda.Stream()
     torch.cuda.synchronize()
     with torch.cuda.stream(s_prep):
         preps = stack.prepare_layer(layer, ex, ey, flags, stream=s_prep)
     with torch.cuda.stream(s_on):
-        pout = stack.run_layer_prepared(layer, X, preps, ready_flag=flags[nproj - 1], timeout_us=2_000_000,
-                                        timed_out=late, tamper=tamper, stream=s_on)
+        pout = stack.run_layer_prepared(layer, X, preps, ready_flag=[flags[i] for i in range(nin)],
+                                        timeout_us=2_000_000, timed_out=late, tamper=tamper, stream=s_on)
     torch.cuda.synchronize()
-    assert int(late.item()) == 0
+    assert int(late.item()) == 0 and flags.tolist() == [0] * nin
     for name in out:
         for a, b in zip(out[name], pout[name]):
             assert torch.equal(a, b), (L, name, "prepared schedule")

@@ -61,19 +61,34 @@ def _vregs(tok: str) -> set:
     return {int(m.group(1))} if m else set()
 
 
+_VMEM = ("global_", "buffer_", "flat_", "scratch_")  # every vector-memory op counts on vmcnt
+_VMEM_LOAD = ("global_load", "buffer_load", "flat_load", "scratch_load")
+_VMEM_STORE = ("global_store", "buffer_store", "flat_store", "scratch_store")
+
+
 def asm_load_hazards(asm_text: str) -> list:
-    """Register copies (v_mov*, v_accvgpr*) that read a register written by an
-    inline-assembly global_load_dwordx4 of the same kernel before the next
-    wait for all loads (s_waitcnt vmcnt(0)).  The compiler treats
-    the asm output as ready when the asm statement ends, so such a copy (it
-    appears under register pressure) can read the register before the load
-    lands, and the late data then overwrites whatever reused the register: a
-    corrupted address and a memory fault.  Returns [(kernel, instruction)]."""
-    bad, cur, inasm, dests = [], None, False, set()
+    """Uses of registers that an inline-assembly global_load_dwordx4 of the
+    same kernel still targets.  The compiler treats the asm output as ready
+    when the asm statement ends, so under register pressure it may
+
+      * copy the register (v_mov*, v_accvgpr*): the copy reads it before the
+        load lands;
+      * write the register, reusing it for another value (a VALU instruction
+        or a compiler-issued load with it as destination): the late load data
+        then overwrites that value (a corrupted address, a memory fault);
+      * spill it to scratch (a store of it): the spilled copy is stale.
+
+    A load is in flight from its issue until a wait that covers it: every
+    vector-memory instruction (load, store, LDS DMA) counts on vmcnt in issue
+    order, and `s_waitcnt vmcnt(N)` returns once all but the N most recent
+    have completed.  The scan follows the text of each kernel in order (a loop
+    body once).  Returns [(kernel, instruction)] for every such use."""
+    bad, cur, inasm = [], None, False
+    inflight = []  # per vector-memory op in issue order: the registers an asm load of it targets
     for line in asm_text.split("\n"):
         m = re.match(r"^(_Z\S+):", line)
         if m:
-            cur, dests = m.group(1), set()
+            cur, inflight = m.group(1), []
             continue
         if cur is None:
             continue
@@ -87,17 +102,39 @@ def asm_load_hazards(asm_text: str) -> list:
             inasm = False
             continue
         parts = line.strip().split(None, 1)
-        if not parts:
+        if not parts or parts[0].startswith((";", ".")):
             continue
         op, args = parts[0], [a.strip() for a in parts[1].split(",")] if len(parts) > 1 else []
-        if op == "s_waitcnt" and re.search(r"vmcnt\(0\)", line):
-            dests = set()  # every load has landed; the registers are free again
+        if op == "s_waitcnt":
+            w = re.search(r"vmcnt\((\d+)\)", line)
+            if w:
+                keep = int(w.group(1))
+                inflight = inflight[len(inflight) - keep:] if keep < len(inflight) else inflight
+                if keep == 0:
+                    inflight = []
             continue
-        if inasm and op == "global_load_dwordx4" and args:
-            dests |= _vregs(args[0])
-        elif op.startswith("v_mov") or op.startswith("v_accvgpr"):
+        dests = set().union(*inflight) if inflight else set()
+        if op.startswith(_VMEM):
+            if not inasm and dests:
+                if op.startswith(_VMEM_STORE):
+                    # the stored data: scratch/global/flat stores name it second (after the address
+                    # or "off"), buffer stores first
+                    data = args[0] if op.startswith("buffer_store") else (args[1] if len(args) > 1 else "")
+                    if _vregs(data) & dests:
+                        bad.append((cur, line.strip()))
+                elif op.startswith(_VMEM_LOAD) and args and _vregs(args[0]) & dests:
+                    bad.append((cur, line.strip()))
+            is_asm_load = inasm and op == "global_load_dwordx4" and bool(args)
+            inflight.append(_vregs(args[0]) if is_asm_load else set())
+            continue
+        if inasm or not dests or not args:
+            continue
+        if op.startswith("v_mov") or op.startswith("v_accvgpr"):
             if any(_vregs(a) & dests for a in args[1:]):
                 bad.append((cur, line.strip()))
+                continue
+        if op.startswith("v_") and _vregs(args[0]) & dests:
+            bad.append((cur, line.strip()))
     return bad
 
 
@@ -140,7 +177,8 @@ def build(verbose: bool = False) -> str:
         hazards = [h for hs in ex.map(check_asm, asm_jobs) for h in hs]
     if hazards:
         lines = "\n".join(f"  {k}: {i}" for k, i in hazards[:20])
-        raise RuntimeError(f"registers of in-flight inline-assembly loads are copied ({len(hazards)}):\n{lines}")
+        raise RuntimeError(f"registers of in-flight inline-assembly loads are copied, overwritten or spilled "
+                           f"({len(hazards)}):\n{lines}")
     for name, (lib, _) in VARIANTS.items():
         mine = [o for o, j in zip(objs, jobs) if j[0] == name]
         tmp = lib + f".tmp{os.getpid()}"

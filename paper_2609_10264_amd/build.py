@@ -182,7 +182,8 @@ def build(verbose: bool = False) -> str:
     for name, (lib, _) in VARIANTS.items():
         mine = [o for o, j in zip(objs, jobs) if j[0] == name]
         tmp = lib + f".tmp{os.getpid()}"
-        cmd = [cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *mine]
+        # -z defs: a symbol that no object defines fails the link, not the first load
+        cmd = [cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-Wl,-z,defs", "-o", tmp, *mine]
         r = subprocess.run(cmd, capture_output=True, text=True)
         if r.returncode != 0:
             raise RuntimeError(f"link failed ({name}):\n{r.stdout}{r.stderr}")

@@ -6,6 +6,7 @@
 
 #include <sys/random.h>
 
+#include <algorithm>
 #include <cstdlib>
 #include <initializer_list>
 #include <map>
@@ -383,18 +384,21 @@ mvk_status mvk_keygen(const mvk_key* key, const int8_t* W, void* stream) {
     const uint32_t m = key->m, n = key->n;
     const size_t Nx = (size_t)key->cx.r * n, Ny = (size_t)key->cy.r * m;
     if (too_big(m, n, 1) || too_big(Nx, m, 4) || too_big(Ny, n, 4)) return MVK_ERANGE;
+    if (m > kMaxEncVectors || n > kMaxEncVectors) return MVK_ERANGE;
     const size_t wt_bytes = align_up((size_t)m * n);
-    const size_t t3_bytes = (Nx * m > Ny * n ? Nx * m : Ny * n) * sizeof(uint32_t);
+    const size_t t3_bytes = align_up((Nx * m > Ny * n ? Nx * m : Ny * n) * sizeof(uint32_t));
+    const size_t seg_words = std::max(encT_seg_words(Nx, m), encT_seg_words(Ny, n));
     void* ws = nullptr;
-    st = workspace(s, wt_bytes + t3_bytes, &ws);
+    st = workspace(s, wt_bytes + t3_bytes + seg_words * sizeof(uint32_t), &ws);
     if (st) return st;
     int8_t* WT = (int8_t*)ws;
     uint32_t* t3 = (uint32_t*)((char*)ws + wt_bytes);
+    uint32_t* seg = (uint32_t*)((char*)ws + wt_bytes + t3_bytes);
     // P^T = Gx^T W^T: vector i is row i of W = column i of W^T (n positions).
     hipError_t e = launch_transpose_i8(W, m, n, WT, s);
-    if (e == hipSuccess) e = launch_encT_i8(key->cx, WT, (size_t)m, 1, m, t3, key->PT, (size_t)m, 1, s);
+    if (e == hipSuccess) e = launch_encT_i8(key->cx, WT, (size_t)m, 1, m, t3, seg, key->PT, (size_t)m, 1, s);
     // Q = Gy^T W: vector k is column k of W (m positions).
-    if (e == hipSuccess) e = launch_encT_i8(key->cy, W, (size_t)n, 1, n, t3, key->Q, (size_t)n, 1, s);
+    if (e == hipSuccess) e = launch_encT_i8(key->cy, W, (size_t)n, 1, n, t3, seg, key->Q, (size_t)n, 1, s);
     return hip_status(e);
 }
 
@@ -721,16 +725,19 @@ mvk_status mvk_batch_preprocess(uint32_t B, const uint32_t* const* Q, uint32_t N
         if (!Q[b]) return MVK_EINVAL;
     const uint64_t N2 = Bn * c2->r;
     if (too_big(N, N2, sizeof(uint32_t))) return MVK_ERANGE;
+    if (N > kMaxEncVectors) return MVK_ERANGE;
     hipStream_t s = (hipStream_t)stream;
     void* ws = nullptr;
-    st = workspace(s, (size_t)N * N2 * sizeof(uint32_t), &ws);  // column scratch of the batched encoder
+    const size_t t3_bytes = align_up((size_t)N * N2 * sizeof(uint32_t));  // column scratch of the batched encoder
+    st = workspace(s, t3_bytes + encT_seg_words(N2, N) * sizeof(uint32_t), &ws);
     if (st) return st;
     for (uint32_t b = 0; b < B; ++b) {
         const hipError_t e = hipMemcpy2DAsync(QtT + (size_t)b * n, Bn * sizeof(uint32_t), Q[b], (size_t)n * 4,
                                               (size_t)n * 4, N, hipMemcpyDeviceToDevice, s);
         if (e != hipSuccess) return MVK_EHIP;
     }
-    return hip_status(launch_encT_u32(*c2, QtT, 1, Bn, N, (uint32_t*)ws, Qaux, 1, N2, s));
+    return hip_status(launch_encT_u32(*c2, QtT, 1, Bn, N, (uint32_t*)ws, (uint32_t*)((char*)ws + t3_bytes), Qaux, 1,
+                                      N2, s));
 }
 
 mvk_status mvk_batch_project(const uint32_t* QtT, uint32_t N, uint32_t n, uint32_t B, const mvk_sparse* e,
@@ -791,10 +798,13 @@ mvk_status mvk_raa_encode(const mvk_code* code, const uint32_t* w, uint32_t coun
     hipStream_t s = (hipStream_t)stream;
     const size_t N = (size_t)code->k * code->r;
     if (too_big(N, count, sizeof(uint32_t))) return MVK_ERANGE;
+    if (count > kMaxEncVectors) return MVK_ERANGE;
     void* ws = nullptr;
-    st = workspace(s, N * count * sizeof(uint32_t), &ws);
+    const size_t t3_bytes = align_up(N * count * sizeof(uint32_t));
+    st = workspace(s, t3_bytes + encT_seg_words(N, count) * sizeof(uint32_t), &ws);
     if (st) return st;
-    return hip_status(launch_encT_u32(*code, w, 1, code->k, count, (uint32_t*)ws, out, 1, N, s));
+    return hip_status(
+        launch_encT_u32(*code, w, 1, code->k, count, (uint32_t*)ws, (uint32_t*)((char*)ws + t3_bytes), out, 1, N, s));
 }
 
 mvk_status mvk_raa_syndrome(const mvk_code* code, const uint32_t* v, uint32_t count, uint32_t* out, void* stream) {

@@ -6,12 +6,12 @@
 //             scatter by pi2, suffix sum, scale, scatter by pi1, fold r)
 //
 // Two kernel shapes:
-//  * encT_lanes: many vectors at once (Preprocess encodes every row and every
-//    column of W).  One lane owns one vector and walks its N positions in order,
-//    so each prefix sum is a plain running sum per lane and every access to the
-//    batch (vector index innermost) is a coalesced 64-lane row.  The code arrays
-//    are indexed by the position only, which is uniform across the wave, so they
-//    come through scalar loads.
+//  * encT_seg_*: many vectors at once (Preprocess encodes every row and every
+//    column of W).  One lane owns one vector within a segment of positions, so
+//    each prefix sum is a running sum per lane plus a scan over segments, and
+//    every access to the batch (vector index innermost) is a coalesced row.
+//    The code arrays are indexed by the position only, which is uniform across
+//    the workgroup, so they come through scalar loads.
 //  * syn_wg: few vectors (Encrypt: one per query column; Verify: one per
 //    repetition) of length up to 16384.  One 1024-thread workgroup owns one
 //    vector; both work arrays stay in LDS.
@@ -35,61 +35,124 @@ __device__ __forceinline__ uint32_t div_r(uint32_t x, uint32_t r) {
         return x / r;
 }
 
+// Batched encoding.  The N positions are
+// cut into segments of kEncSeg, and a 256-thread workgroup takes one segment
+// for 256 vectors (one lane per vector, vectors innermost in every array, so
+// each position is one coalesced row).  A prefix sum becomes a local prefix
+// per segment plus the sum of the earlier segments:
+//   stage 1   t3[j][v] = local prefix of v1[j] * w_v[pi1[j] / r], segment sums
+//   scan      off[s][v] = sum of the segment sums before s
+//   stage 2   out[j][v] = local prefix of v2[j] * (t3[pi2[j]][v] + off[seg(pi2[j])][v]),
+//             segment sums
+//   scan, fix-up  out[j][v] += sum of the second stage's earlier segment sums
+// Every output is the field sum of the same terms as one running sum over all N
+// positions; field addition is exact, so the grouping does not change it.
+constexpr uint32_t kEncSeg = 256;
+constexpr int kEncThreads = 256;
+
 template <typename T, int RR>
-__global__ __launch_bounds__(64) void encT_lanes(uint32_t k, uint32_t r, const uint32_t* __restrict__ pi1,
-                                                 const uint32_t* __restrict__ pi2,
-                                                 const uint32_t* __restrict__ v1,
-                                                 const uint32_t* __restrict__ v2, const T* __restrict__ in,
-                                                 size_t ld_in, size_t vs_in, uint32_t nvec,
-                                                 uint32_t* __restrict__ t3, uint32_t* __restrict__ out,
-                                                 size_t ld_out, size_t vs_out) {
-    const uint32_t v = blockIdx.x * 64 + threadIdx.x;
+__global__ __launch_bounds__(kEncThreads) void encT_seg_stage1(uint32_t N, uint32_t r,
+                                                               const uint32_t* __restrict__ pi1,
+                                                               const uint32_t* __restrict__ v1,
+                                                               const T* __restrict__ in, size_t ld_in, size_t vs_in,
+                                                               uint32_t nvec, uint32_t* __restrict__ t3,
+                                                               uint32_t* __restrict__ tot) {
+    const uint32_t seg = blockIdx.x, v = blockIdx.y * kEncThreads + threadIdx.x;
     const bool act = v < nvec;
-    const uint32_t N = k * (RR ? RR : r);
     const T* src = in + (size_t)(act ? v : 0) * vs_in;
-    uint32_t* tcol = t3 + (size_t)(act ? v : 0);
-    const size_t ldt = nvec;
-    // pass 1: a = prefix(v1 .* (Pi1^T R^T w))
+    const uint32_t j0 = seg * kEncSeg, j1 = j0 + kEncSeg < N ? j0 + kEncSeg : N;
     uint32_t s = 0;
 #pragma unroll 8
-    for (uint32_t j = 0; j < N; ++j) {
+    for (uint32_t j = j0; j < j1; ++j) {
         uint32_t pj = pi1[j];
         if (pj >= N) pj = N - 1;
-        const uint32_t i = div_r<RR>(pj, r);
-        const uint32_t x = act ? load_elem(src, (size_t)i * ld_in) : 0u;
+        const uint32_t x = act ? load_elem(src, (size_t)div_r<RR>(pj, r) * ld_in) : 0u;
         s = fadd(s, fmul(v1[j], x));
-        if (act) tcol[(size_t)j * ldt] = s;
+        if (act) t3[(size_t)j * nvec + v] = s;
     }
-    // pass 2: out = prefix(v2 .* (Pi2^T a))
-    uint32_t* dst = out + (size_t)(act ? v : 0) * vs_out;
-    s = 0;
+    if (act) tot[(size_t)seg * nvec + v] = s;
+}
+
+// off[s][v] = sum_{s' < s} tot[s'][v] for every vector v (one thread each)
+__global__ __launch_bounds__(kEncThreads) void encT_seg_scan(uint32_t nseg, uint32_t nvec,
+                                                             const uint32_t* __restrict__ tot,
+                                                             uint32_t* __restrict__ off) {
+    const uint32_t v = blockIdx.x * kEncThreads + threadIdx.x;
+    if (v >= nvec) return;
+    uint32_t run = 0;
+    for (uint32_t sg = 0; sg < nseg; ++sg) {
+        const uint32_t t = tot[(size_t)sg * nvec + v];
+        off[(size_t)sg * nvec + v] = run;
+        run = fadd(run, t);
+    }
+}
+
+__global__ __launch_bounds__(kEncThreads) void encT_seg_stage2(uint32_t N, const uint32_t* __restrict__ pi2,
+                                                               const uint32_t* __restrict__ v2,
+                                                               const uint32_t* __restrict__ t3,
+                                                               const uint32_t* __restrict__ off1, uint32_t nvec,
+                                                               uint32_t* __restrict__ out, size_t ld_out,
+                                                               size_t vs_out, uint32_t* __restrict__ tot) {
+    const uint32_t seg = blockIdx.x, v = blockIdx.y * kEncThreads + threadIdx.x;
+    const bool act = v < nvec;
+    const uint32_t vs = act ? v : 0u;
+    uint32_t* dst = out + (size_t)vs * vs_out;
+    const uint32_t j0 = seg * kEncSeg, j1 = j0 + kEncSeg < N ? j0 + kEncSeg : N;
+    uint32_t s = 0;
 #pragma unroll 8
-    for (uint32_t j = 0; j < N; ++j) {
+    for (uint32_t j = j0; j < j1; ++j) {
         uint32_t pj = pi2[j];
         if (pj >= N) pj = N - 1;
-        const uint32_t a = act ? tcol[(size_t)pj * ldt] : 0u;
+        const uint32_t a = act ? fadd(t3[(size_t)pj * nvec + vs], off1[(size_t)(pj / kEncSeg) * nvec + vs]) : 0u;
         s = fadd(s, fmul(v2[j], a));
         if (act) dst[(size_t)j * ld_out] = s;
     }
+    if (act) tot[(size_t)seg * nvec + v] = s;
+}
+
+// out[j][v] += off[seg(j)][v] for the segments after the first
+__global__ __launch_bounds__(kEncThreads) void encT_seg_fixup(uint32_t N, uint32_t nvec,
+                                                              const uint32_t* __restrict__ off,
+                                                              uint32_t* __restrict__ out, size_t ld_out,
+                                                              size_t vs_out) {
+    const uint32_t seg = blockIdx.x + 1, v = blockIdx.y * kEncThreads + threadIdx.x;
+    if (v >= nvec) return;
+    const uint32_t o = off[(size_t)seg * nvec + v];
+    uint32_t* dst = out + (size_t)v * vs_out;
+    const uint32_t j0 = seg * kEncSeg, j1 = j0 + kEncSeg < N ? j0 + kEncSeg : N;
+#pragma unroll 8
+    for (uint32_t j = j0; j < j1; ++j) dst[(size_t)j * ld_out] = fadd(dst[(size_t)j * ld_out], o);
 }
 
 template <typename T>
 hipError_t launch_encT(const mvk_code& c, const T* in, size_t ld_in, size_t vs_in, uint32_t nvec, uint32_t* t3,
-                       uint32_t* out, size_t ld_out, size_t vs_out, hipStream_t s) {
+                       uint32_t* seg_scratch, uint32_t* out, size_t ld_out, size_t vs_out, hipStream_t s) {
     if (nvec == 0) return hipSuccess;
-    const dim3 grid(ceil_div(nvec, 64)), block(64);
-#define MVK_ENC(RRV)                                                                                         \
-    hipLaunchKernelGGL((encT_lanes<T, RRV>), grid, block, 0, s, c.k, c.r, c.pi1, c.pi2, c.v1, c.v2, in, ld_in, \
-                       vs_in, nvec, t3, out, ld_out, vs_out)
+    if (nvec > kMaxEncVectors) return hipErrorInvalidValue;
+    const uint32_t N = c.k * c.r;
+    const uint32_t nseg = ceil_div(N, kEncSeg), vgroups = ceil_div(nvec, kEncThreads);
+    uint32_t* tot = seg_scratch;
+    uint32_t* off = seg_scratch + (size_t)nseg * nvec;
+    const dim3 grid(nseg, vgroups), block(kEncThreads);
+#define MVK_ENC1(RRV)                                                                                            \
+    hipLaunchKernelGGL((encT_seg_stage1<T, RRV>), grid, block, 0, s, N, c.r, c.pi1, c.v1, in, ld_in, vs_in, nvec, \
+                       t3, tot)
     switch (c.r) {
-        case 1: MVK_ENC(1); break;
-        case 2: MVK_ENC(2); break;
-        case 3: MVK_ENC(3); break;
-        case 4: MVK_ENC(4); break;
-        case 8: MVK_ENC(8); break;
-        default: MVK_ENC(0); break;
+        case 1: MVK_ENC1(1); break;
+        case 2: MVK_ENC1(2); break;
+        case 3: MVK_ENC1(3); break;
+        case 4: MVK_ENC1(4); break;
+        case 8: MVK_ENC1(8); break;
+        default: MVK_ENC1(0); break;
     }
-#undef MVK_ENC
+#undef MVK_ENC1
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(encT_seg_scan, dim3(vgroups), block, 0, s, nseg, nvec, tot, off);
+    hipLaunchKernelGGL(encT_seg_stage2, grid, block, 0, s, N, c.pi2, c.v2, t3, off, nvec, out, ld_out, vs_out, tot);
+    hipLaunchKernelGGL(encT_seg_scan, dim3(vgroups), block, 0, s, nseg, nvec, tot, off);
+    if (nseg > 1)
+        hipLaunchKernelGGL(encT_seg_fixup, dim3(nseg - 1, vgroups), block, 0, s, N, nvec, off, out, ld_out, vs_out);
     return hipGetLastError();
 }
 
@@ -380,14 +443,16 @@ __global__ void fill_u32(uint32_t* p, size_t count, uint32_t value) {
 
 }  // namespace
 
+size_t encT_seg_words(size_t N, size_t nvec) { return 2 * ((N + kEncSeg - 1) / kEncSeg) * nvec; }
+
 hipError_t launch_encT_u32(const mvk_code& c, const uint32_t* in, size_t ld_in, size_t vs_in, uint32_t nvec,
-                           uint32_t* t3, uint32_t* out, size_t ld_out, size_t vs_out, hipStream_t s) {
-    return launch_encT<uint32_t>(c, in, ld_in, vs_in, nvec, t3, out, ld_out, vs_out, s);
+                           uint32_t* t3, uint32_t* seg, uint32_t* out, size_t ld_out, size_t vs_out, hipStream_t s) {
+    return launch_encT<uint32_t>(c, in, ld_in, vs_in, nvec, t3, seg, out, ld_out, vs_out, s);
 }
 
 hipError_t launch_encT_i8(const mvk_code& c, const int8_t* in, size_t ld_in, size_t vs_in, uint32_t nvec,
-                          uint32_t* t3, uint32_t* out, size_t ld_out, size_t vs_out, hipStream_t s) {
-    return launch_encT<int8_t>(c, in, ld_in, vs_in, nvec, t3, out, ld_out, vs_out, s);
+                          uint32_t* t3, uint32_t* seg, uint32_t* out, size_t ld_out, size_t vs_out, hipStream_t s) {
+    return launch_encT<int8_t>(c, in, ld_in, vs_in, nvec, t3, seg, out, ld_out, vs_out, s);
 }
 
 hipError_t launch_syn_dense(const mvk_code& c, const uint32_t* v, uint32_t count, uint32_t* scratch, uint32_t* out,

@@ -214,7 +214,7 @@ mvk_status mvk_server_eval_packed_static(const int8_t *Wp, uint32_t m, uint32_t 
  * Uses a workspace of about m*n + max(Nx*m, Ny*n)*4 bytes (plus 2/256 of that
  * for the segment sums of the prefix scans).
  * Errors: MVK_EINVAL, MVK_ERANGE (a buffer size above 2^62 bytes, m or n above
- * 65535 * 256), MVK_ENOMEM.
+ * 65535 * 64), MVK_ENOMEM.
  */
 mvk_status mvk_keygen(const mvk_key *key, const int8_t *W, void *stream);
 
@@ -415,7 +415,7 @@ mvk_status mvk_flag_wait(uint32_t *flag, uint32_t value, uint32_t timeout_us, ui
  *           (what the server keeps, as the transpose of the stacked Qt)
  *   Qaux  : device, N x N', written: Qaux = QtT G' (the client's state)
  * Uses a workspace of about N*N' words.  Errors: MVK_EINVAL, MVK_ERANGE (also N
- * above 65535 * 256), MVK_ENOMEM.
+ * above 65535 * 64), MVK_ENOMEM.
  */
 mvk_status mvk_batch_preprocess(uint32_t B, const uint32_t *const *Q, uint32_t N, uint32_t n,
                                 const mvk_code *c2, uint32_t *QtT, uint32_t *Qaux, void *stream);
@@ -453,7 +453,7 @@ mvk_status mvk_batch_verify(const mvk_code *cy, const mvk_code *c2, const uint32
  * vectors.  w: device, count x k field array; out: device, count x N.
  * Uses a workspace of about N*count words (plus 2/256 of that).
  * Errors: MVK_EINVAL, MVK_ERANGE (N*count*4 above 2^62 bytes, count above
- * 65535 * 256), MVK_ENOMEM.
+ * 65535 * 64), MVK_ENOMEM.
  */
 mvk_status mvk_raa_encode(const mvk_code *code, const uint32_t *w, uint32_t count, uint32_t *out,
                           void *stream);

@@ -39,8 +39,8 @@ hipError_t launch_pack_w(const int8_t* W, uint32_t m, uint32_t n, int8_t* Wp, hi
 // out[j*ld_out + v*vs_out].  t3: scratch of N*nvec uint32 (N = r*k); seg:
 // scratch of encT_seg_words(N, nvec) uint32.
 size_t encT_seg_words(size_t N, size_t nvec);
-// Vectors per call of the batched encoder (256 per workgroup row, 65535 rows).
-constexpr uint32_t kMaxEncVectors = 65535u * 256u;
+// Vectors per call of the batched encoder (at least 64 per workgroup row, 65535 rows).
+constexpr uint32_t kMaxEncVectors = 65535u * 64u;
 hipError_t launch_encT_u32(const mvk_code& c, const uint32_t* in, size_t ld_in, size_t vs_in, uint32_t nvec,
                            uint32_t* t3, uint32_t* seg, uint32_t* out, size_t ld_out, size_t vs_out, hipStream_t s);
 hipError_t launch_encT_i8(const mvk_code& c, const int8_t* in, size_t ld_in, size_t vs_in, uint32_t nvec,

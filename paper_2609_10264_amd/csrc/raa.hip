@@ -6,7 +6,7 @@
 //             scatter by pi2, suffix sum, scale, scatter by pi1, fold r)
 //
 // Two kernel shapes:
-//  * encT_seg_*: many vectors at once (Preprocess encodes every row and every
+//  * enc_pass1/2: many vectors at once (Preprocess encodes every row and every
 //    column of W).  One lane owns one vector within a segment of positions, so
 //    each prefix sum is a running sum per lane plus a scan over segments, and
 //    every access to the batch (vector index innermost) is a coalesced row.
@@ -35,51 +35,139 @@ __device__ __forceinline__ uint32_t div_r(uint32_t x, uint32_t r) {
         return x / r;
 }
 
-// Batched encoding.  The N positions are
-// cut into segments of kEncSeg, and a 256-thread workgroup takes one segment
-// for 256 vectors (one lane per vector, vectors innermost in every array, so
-// each position is one coalesced row).  A prefix sum becomes a local prefix
-// per segment plus the sum of the earlier segments:
-//   stage 1   t3[j][v] = local prefix of v1[j] * w_v[pi1[j] / r], segment sums
-//   scan      off[s][v] = sum of the segment sums before s
-//   stage 2   out[j][v] = local prefix of v2[j] * (t3[pi2[j]][v] + off[seg(pi2[j])][v]),
-//             segment sums
-//   scan, fix-up  out[j][v] += sum of the second stage's earlier segment sums
+// Batched encoding.  The N positions are cut into segments of L positions
+// (L from enc_seg_len), and a one-wave workgroup takes one segment for 64*V
+// vectors (V consecutive vectors per lane; vectors innermost in every array,
+// so each position is one coalesced row).  Each prefix sum is a reduce, a
+// scan over the segment sums, then a second pass that starts every segment
+// from its offset (so no output is written twice):
+//   sum 1     tot[s][v] = sum over segment s of v1[j] * w_v[pi1[j] / r]
+//   scan      off[s][v] = sum of tot[s'][v] for s' < s
+//   write 1   t3[j][v] = off[seg(j)][v] + running sum within the segment
+//   sum 2, scan, write 2: the same with v2[j] * t3[pi2[j]][v] into out[j][v]
 // Every output is the field sum of the same terms as one running sum over all N
 // positions; field addition is exact, so the grouping does not change it.
-constexpr uint32_t kEncSeg = 256;
-constexpr int kEncThreads = 256;
+constexpr int kEncLanes = 64;
 
-template <typename T, int RR>
-__global__ __launch_bounds__(kEncThreads) void encT_seg_stage1(uint32_t N, uint32_t r,
-                                                               const uint32_t* __restrict__ pi1,
-                                                               const uint32_t* __restrict__ v1,
-                                                               const T* __restrict__ in, size_t ld_in, size_t vs_in,
-                                                               uint32_t nvec, uint32_t* __restrict__ t3,
-                                                               uint32_t* __restrict__ tot) {
-    const uint32_t seg = blockIdx.x, v = blockIdx.y * kEncThreads + threadIdx.x;
-    const bool act = v < nvec;
-    const T* src = in + (size_t)(act ? v : 0) * vs_in;
-    const uint32_t j0 = seg * kEncSeg, j1 = j0 + kEncSeg < N ? j0 + kEncSeg : N;
-    uint32_t s = 0;
+// Segment length: the longest of 256, 128, 64 that still gives at least 2048
+// workgroups (eight waves per compute unit) at four vectors per lane.
+uint32_t enc_seg_len(size_t N, size_t nvec) {
+    const size_t vg = (nvec + 4 * kEncLanes - 1) / (4 * kEncLanes);
+    for (uint32_t L : {256u, 128u})
+        if (((N + L - 1) / L) * vg >= 2048) return L;
+    return 64u;
+}
+
+template <int V>
+struct Lanes {
+    uint32_t x[V];
+};
+
+// V elements (vectors vb .. vb+V-1, stride vs) of one position
+template <int V>
+__device__ __forceinline__ Lanes<V> load_lanes(const uint32_t* p, size_t vs) {
+    Lanes<V> r;
+    if constexpr (V == 4) {
+        const uint4 q = *(const uint4*)p;
+        r.x[0] = q.x, r.x[1] = q.y, r.x[2] = q.z, r.x[3] = q.w;
+    } else {
+#pragma unroll
+        for (int q = 0; q < V; ++q) r.x[q] = p[q * vs];
+    }
+    return r;
+}
+template <int V>
+__device__ __forceinline__ Lanes<V> load_lanes(const int8_t* p, size_t vs) {
+    Lanes<V> r;
+    if constexpr (V == 4) {
+        const uint32_t w = *(const uint32_t*)p;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) r.x[q] = femb((int8_t)(w >> (8 * q)));
+    } else {
+#pragma unroll
+        for (int q = 0; q < V; ++q) r.x[q] = femb(p[q * vs]);
+    }
+    return r;
+}
+template <int V>
+__device__ __forceinline__ void store_lanes(uint32_t* p, size_t vs, const Lanes<V>& v) {
+    if constexpr (V == 4) {
+        *(uint4*)p = make_uint4(v.x[0], v.x[1], v.x[2], v.x[3]);
+    } else {
+#pragma unroll
+        for (int q = 0; q < V; ++q) p[q * vs] = v.x[q];
+    }
+}
+
+// First prefix sum (over v1 .* Pi1^T R^T w).  WRITE = false: segment sums
+// into tot; WRITE = true: t3 from the offsets in off.
+template <typename T, int RR, int V, bool WRITE>
+__global__ __launch_bounds__(kEncLanes) void enc_pass1(uint32_t N, uint32_t r, uint32_t L,
+                                                       const uint32_t* __restrict__ pi1,
+                                                       const uint32_t* __restrict__ v1, const T* __restrict__ in,
+                                                       size_t ld_in, size_t vs_in, uint32_t nvec,
+                                                       const uint32_t* __restrict__ off, uint32_t* __restrict__ t3,
+                                                       uint32_t* __restrict__ tot) {
+    const uint32_t seg = blockIdx.x, vb = (blockIdx.y * kEncLanes + threadIdx.x) * V;
+    if (vb >= nvec) return;
+    const T* src = in + (size_t)vb * vs_in;
+    const uint32_t j0 = seg * L, j1 = j0 + L < N ? j0 + L : N;
+    Lanes<V> acc;
+    if (WRITE)
+        acc = load_lanes<V>(off + (size_t)seg * nvec + vb, 1);
+    else
+#pragma unroll
+        for (int q = 0; q < V; ++q) acc.x[q] = 0;
 #pragma unroll 8
     for (uint32_t j = j0; j < j1; ++j) {
         uint32_t pj = pi1[j];
         if (pj >= N) pj = N - 1;
-        const uint32_t x = act ? load_elem(src, (size_t)div_r<RR>(pj, r) * ld_in) : 0u;
-        s = fadd(s, fmul(v1[j], x));
-        if (act) t3[(size_t)j * nvec + v] = s;
+        const Lanes<V> x = load_lanes<V>(src + (size_t)div_r<RR>(pj, r) * ld_in, vs_in);
+        const uint32_t c = v1[j];
+#pragma unroll
+        for (int q = 0; q < V; ++q) acc.x[q] = fadd(acc.x[q], fmul(c, x.x[q]));
+        if (WRITE) store_lanes<V>(t3 + (size_t)j * nvec + vb, 1, acc);
     }
-    if (act) tot[(size_t)seg * nvec + v] = s;
+    if (!WRITE) store_lanes<V>(tot + (size_t)seg * nvec + vb, 1, acc);
+}
+
+// Second prefix sum (over v2 .* Pi2^T t3), the same two forms, into out.
+template <int V, bool WRITE>
+__global__ __launch_bounds__(kEncLanes) void enc_pass2(uint32_t N, uint32_t L, const uint32_t* __restrict__ pi2,
+                                                       const uint32_t* __restrict__ v2,
+                                                       const uint32_t* __restrict__ t3, uint32_t nvec,
+                                                       const uint32_t* __restrict__ off, uint32_t* __restrict__ out,
+                                                       size_t ld_out, size_t vs_out, uint32_t* __restrict__ tot) {
+    const uint32_t seg = blockIdx.x, vb = (blockIdx.y * kEncLanes + threadIdx.x) * V;
+    if (vb >= nvec) return;
+    uint32_t* dst = out + (size_t)vb * vs_out;
+    const uint32_t j0 = seg * L, j1 = j0 + L < N ? j0 + L : N;
+    Lanes<V> acc;
+    if (WRITE)
+        acc = load_lanes<V>(off + (size_t)seg * nvec + vb, 1);
+    else
+#pragma unroll
+        for (int q = 0; q < V; ++q) acc.x[q] = 0;
+#pragma unroll 8
+    for (uint32_t j = j0; j < j1; ++j) {
+        uint32_t pj = pi2[j];
+        if (pj >= N) pj = N - 1;
+        const Lanes<V> a = load_lanes<V>(t3 + (size_t)pj * nvec + vb, 1);
+        const uint32_t c = v2[j];
+#pragma unroll
+        for (int q = 0; q < V; ++q) acc.x[q] = fadd(acc.x[q], fmul(c, a.x[q]));
+        if (WRITE) store_lanes<V>(dst + (size_t)j * ld_out, vs_out, acc);
+    }
+    if (!WRITE) store_lanes<V>(tot + (size_t)seg * nvec + vb, 1, acc);
 }
 
 // off[s][v] = sum_{s' < s} tot[s'][v] for every vector v (one thread each)
-__global__ __launch_bounds__(kEncThreads) void encT_seg_scan(uint32_t nseg, uint32_t nvec,
-                                                             const uint32_t* __restrict__ tot,
-                                                             uint32_t* __restrict__ off) {
-    const uint32_t v = blockIdx.x * kEncThreads + threadIdx.x;
+__global__ __launch_bounds__(256) void enc_scan(uint32_t nseg, uint32_t nvec, const uint32_t* __restrict__ tot,
+                                                uint32_t* __restrict__ off) {
+    const uint32_t v = blockIdx.x * 256 + threadIdx.x;
     if (v >= nvec) return;
     uint32_t run = 0;
+#pragma unroll 8
     for (uint32_t sg = 0; sg < nseg; ++sg) {
         const uint32_t t = tot[(size_t)sg * nvec + v];
         off[(size_t)sg * nvec + v] = run;
@@ -87,41 +175,34 @@ __global__ __launch_bounds__(kEncThreads) void encT_seg_scan(uint32_t nseg, uint
     }
 }
 
-__global__ __launch_bounds__(kEncThreads) void encT_seg_stage2(uint32_t N, const uint32_t* __restrict__ pi2,
-                                                               const uint32_t* __restrict__ v2,
-                                                               const uint32_t* __restrict__ t3,
-                                                               const uint32_t* __restrict__ off1, uint32_t nvec,
-                                                               uint32_t* __restrict__ out, size_t ld_out,
-                                                               size_t vs_out, uint32_t* __restrict__ tot) {
-    const uint32_t seg = blockIdx.x, v = blockIdx.y * kEncThreads + threadIdx.x;
-    const bool act = v < nvec;
-    const uint32_t vs = act ? v : 0u;
-    uint32_t* dst = out + (size_t)vs * vs_out;
-    const uint32_t j0 = seg * kEncSeg, j1 = j0 + kEncSeg < N ? j0 + kEncSeg : N;
-    uint32_t s = 0;
-#pragma unroll 8
-    for (uint32_t j = j0; j < j1; ++j) {
-        uint32_t pj = pi2[j];
-        if (pj >= N) pj = N - 1;
-        const uint32_t a = act ? fadd(t3[(size_t)pj * nvec + vs], off1[(size_t)(pj / kEncSeg) * nvec + vs]) : 0u;
-        s = fadd(s, fmul(v2[j], a));
-        if (act) dst[(size_t)j * ld_out] = s;
-    }
-    if (act) tot[(size_t)seg * nvec + v] = s;
+template <typename T, int RR, int V>
+hipError_t launch_enc_v(const mvk_code& c, const T* in, size_t ld_in, size_t vs_in, uint32_t nvec, uint32_t* t3,
+                        uint32_t* tot, uint32_t* off, uint32_t* out, size_t ld_out, size_t vs_out, hipStream_t s) {
+    const uint32_t N = c.k * c.r, L = enc_seg_len(N, nvec), nseg = ceil_div(N, L);
+    const dim3 grid(nseg, ceil_div(nvec, kEncLanes * V)), block(kEncLanes), sgrid(ceil_div(nvec, 256u));
+    hipLaunchKernelGGL((enc_pass1<T, RR, V, false>), grid, block, 0, s, N, c.r, L, c.pi1, c.v1, in, ld_in, vs_in,
+                       nvec, nullptr, nullptr, tot);
+    hipLaunchKernelGGL(enc_scan, sgrid, dim3(256), 0, s, nseg, nvec, tot, off);
+    hipLaunchKernelGGL((enc_pass1<T, RR, V, true>), grid, block, 0, s, N, c.r, L, c.pi1, c.v1, in, ld_in, vs_in,
+                       nvec, off, t3, nullptr);
+    hipLaunchKernelGGL((enc_pass2<V, false>), grid, block, 0, s, N, L, c.pi2, c.v2, t3, nvec, nullptr, nullptr,
+                       ld_out, vs_out, tot);
+    hipLaunchKernelGGL(enc_scan, sgrid, dim3(256), 0, s, nseg, nvec, tot, off);
+    hipLaunchKernelGGL((enc_pass2<V, true>), grid, block, 0, s, N, L, c.pi2, c.v2, t3, nvec, off, out, ld_out,
+                       vs_out, nullptr);
+    return hipGetLastError();
 }
 
-// out[j][v] += off[seg(j)][v] for the segments after the first
-__global__ __launch_bounds__(kEncThreads) void encT_seg_fixup(uint32_t N, uint32_t nvec,
-                                                              const uint32_t* __restrict__ off,
-                                                              uint32_t* __restrict__ out, size_t ld_out,
-                                                              size_t vs_out) {
-    const uint32_t seg = blockIdx.x + 1, v = blockIdx.y * kEncThreads + threadIdx.x;
-    if (v >= nvec) return;
-    const uint32_t o = off[(size_t)seg * nvec + v];
-    uint32_t* dst = out + (size_t)v * vs_out;
-    const uint32_t j0 = seg * kEncSeg, j1 = j0 + kEncSeg < N ? j0 + kEncSeg : N;
-#pragma unroll 8
-    for (uint32_t j = j0; j < j1; ++j) dst[(size_t)j * ld_out] = fadd(dst[(size_t)j * ld_out], o);
+template <typename T, int RR>
+hipError_t launch_enc_r(const mvk_code& c, const T* in, size_t ld_in, size_t vs_in, uint32_t nvec, uint32_t* t3,
+                        uint32_t* tot, uint32_t* off, uint32_t* out, size_t ld_out, size_t vs_out, hipStream_t s) {
+    // four vectors per lane when every lane's four elements are adjacent and aligned
+    const size_t al = 4 * sizeof(T);
+    const bool v4 = nvec % 4 == 0 && vs_in == 1 && ld_in % 4 == 0 && (uintptr_t)in % al == 0 && vs_out == 1 &&
+                    ld_out % 4 == 0 && (uintptr_t)out % 16 == 0 && (uintptr_t)t3 % 16 == 0 &&
+                    (uintptr_t)tot % 16 == 0 && (uintptr_t)off % 16 == 0;
+    if (v4) return launch_enc_v<T, RR, 4>(c, in, ld_in, vs_in, nvec, t3, tot, off, out, ld_out, vs_out, s);
+    return launch_enc_v<T, RR, 1>(c, in, ld_in, vs_in, nvec, t3, tot, off, out, ld_out, vs_out, s);
 }
 
 template <typename T>
@@ -130,30 +211,16 @@ hipError_t launch_encT(const mvk_code& c, const T* in, size_t ld_in, size_t vs_i
     if (nvec == 0) return hipSuccess;
     if (nvec > kMaxEncVectors) return hipErrorInvalidValue;
     const uint32_t N = c.k * c.r;
-    const uint32_t nseg = ceil_div(N, kEncSeg), vgroups = ceil_div(nvec, kEncThreads);
     uint32_t* tot = seg_scratch;
-    uint32_t* off = seg_scratch + (size_t)nseg * nvec;
-    const dim3 grid(nseg, vgroups), block(kEncThreads);
-#define MVK_ENC1(RRV)                                                                                            \
-    hipLaunchKernelGGL((encT_seg_stage1<T, RRV>), grid, block, 0, s, N, c.r, c.pi1, c.v1, in, ld_in, vs_in, nvec, \
-                       t3, tot)
+    uint32_t* off = seg_scratch + (size_t)ceil_div(N, enc_seg_len(N, nvec)) * nvec;
     switch (c.r) {
-        case 1: MVK_ENC1(1); break;
-        case 2: MVK_ENC1(2); break;
-        case 3: MVK_ENC1(3); break;
-        case 4: MVK_ENC1(4); break;
-        case 8: MVK_ENC1(8); break;
-        default: MVK_ENC1(0); break;
+        case 1: return launch_enc_r<T, 1>(c, in, ld_in, vs_in, nvec, t3, tot, off, out, ld_out, vs_out, s);
+        case 2: return launch_enc_r<T, 2>(c, in, ld_in, vs_in, nvec, t3, tot, off, out, ld_out, vs_out, s);
+        case 3: return launch_enc_r<T, 3>(c, in, ld_in, vs_in, nvec, t3, tot, off, out, ld_out, vs_out, s);
+        case 4: return launch_enc_r<T, 4>(c, in, ld_in, vs_in, nvec, t3, tot, off, out, ld_out, vs_out, s);
+        case 8: return launch_enc_r<T, 8>(c, in, ld_in, vs_in, nvec, t3, tot, off, out, ld_out, vs_out, s);
+        default: return launch_enc_r<T, 0>(c, in, ld_in, vs_in, nvec, t3, tot, off, out, ld_out, vs_out, s);
     }
-#undef MVK_ENC1
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(encT_seg_scan, dim3(vgroups), block, 0, s, nseg, nvec, tot, off);
-    hipLaunchKernelGGL(encT_seg_stage2, grid, block, 0, s, N, c.pi2, c.v2, t3, off, nvec, out, ld_out, vs_out, tot);
-    hipLaunchKernelGGL(encT_seg_scan, dim3(vgroups), block, 0, s, nseg, nvec, tot, off);
-    if (nseg > 1)
-        hipLaunchKernelGGL(encT_seg_fixup, dim3(nseg - 1, vgroups), block, 0, s, N, nvec, off, out, ld_out, vs_out);
-    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
@@ -443,7 +510,10 @@ __global__ void fill_u32(uint32_t* p, size_t count, uint32_t value) {
 
 }  // namespace
 
-size_t encT_seg_words(size_t N, size_t nvec) { return 2 * ((N + kEncSeg - 1) / kEncSeg) * nvec; }
+size_t encT_seg_words(size_t N, size_t nvec) {
+    const size_t L = enc_seg_len(N, nvec);
+    return 2 * ((N + L - 1) / L) * nvec;
+}
 
 hipError_t launch_encT_u32(const mvk_code& c, const uint32_t* in, size_t ld_in, size_t vs_in, uint32_t nvec,
                            uint32_t* t3, uint32_t* seg, uint32_t* out, size_t ld_out, size_t vs_out, hipStream_t s) {

@@ -554,12 +554,18 @@ def stack_bench(args, steps, warmup, cpu_seconds):
     gen = torch.Generator(device=dev)
     gen.manual_seed(args.seed)
     s = torch.cuda.Stream()
-    built, inputs = [], []
+    built, inputs, pre_ms = [], [], []
     with torch.cuda.stream(s):
         for L in range(layers):
             Ws = {name: torch.randint(-127, 128, (m, n), generator=gen, device=dev, dtype=torch.int8)
                   for (name, m, n, _) in stack.PROJECTIONS}
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(s)
             built.append(stack.build_layer(Ws, cx_by_n, cy_by_m, stream=s))
+            e1.record(s)
+            e1.synchronize()
+            if L:  # the first layer sizes the workspace
+                pre_ms.append(e0.elapsed_time(e1))
             del Ws
             X = {grp: torch.randint(0, P, (B, stack.input_width(grp)), generator=gen, device=dev,
                                     dtype=torch.int32) for grp in stack.INPUTS}
@@ -784,6 +790,7 @@ def stack_bench(args, steps, warmup, cpu_seconds):
                                        "frac": read_s * len(every) / pass_s,
                                        "what": "a streaming read of the same W buffers, one launch per matrix"}},
            "server_eval": {"modmac_per_s": macs / pass_s, "gb_per_s": achieved},
+           "preprocess": preprocess_record(stack, r, pre_ms),
            "tampered_per_pass": sum(len(v) for v in plan.values()),
            "all_expected_verdicts": ok_serial and ok_pipe and ok_ov, "pipelined_matches_serial": same,
            "overlapped_matches_serial": same_ov, "setup_s": t_setup}
@@ -794,6 +801,19 @@ def stack_bench(args, steps, warmup, cpu_seconds):
         res["cpu_baseline"] = cpu_baseline_stack(cpu_seconds)
     res["_ok"] = ok_serial and ok_pipe and ok_ov and same and same_ov
     return res
+
+
+def preprocess_record(stack, r, ms):
+    """Preprocess of one stack layer (keygen of the seven projections: P^T and
+    Q by the batched RAA encoding, then packing W), HIP events per layer.  The
+    algorithmic bytes are W read twice (keygen, packing), P^T and Q written
+    and the packed W written; frac is against the HBM peak."""
+    import numpy as np
+
+    alg = sum(2 * m * n + 4 * r * n * m + 4 * r * m * n + m * n for (_, m, n, _) in stack.PROJECTIONS)
+    t = float(np.mean(ms)) if ms else float("nan")
+    return {"ms_per_layer": t, "layers_timed": len(ms), "alg_bytes_per_layer": alg,
+            "gb_per_s": alg / (1e-3 * t) / 1e9, "frac": alg / (1e-3 * t) / 1e9 / HBM_PEAK_GBS}
 
 
 def cpu_baseline_config(cfg, seconds):
@@ -1245,7 +1265,10 @@ def paper_eval_bench(args):
         alg_bytes = m * n + 4 * n * B + 4 * m * B
         srv_s = 1e-3 * t_se
         paper = PAPER_SEC71_MS[n]
+        kg_bytes = m * n + 4 * r * n * m + 4 * r * m * n  # W read, P^T and Q written
+        kg_s = 1e-3 * float(np.mean(kg_ms))
         rows.append({"n": n, "t_x": tx, "w_pool": pool, "keygen_ms": float(np.mean(kg_ms)),
+                     "keygen_gb_per_s": kg_bytes / kg_s / 1e9, "keygen_hbm_frac": kg_bytes / kg_s / 1e9 / HBM_PEAK_GBS,
                      "encode_us": 1e3 * t_enc, "server_eval_us": 1e3 * t_se, "decode_verify_us": 1e3 * t_dv,
                      "step_us": 1e3 * t_step, "boost_prepare_us": 1e3 * t_prep, "boost_online_us": 1e3 * t_online,
                      "server_gb_per_s": alg_bytes / srv_s / 1e9,

@@ -656,6 +656,9 @@ def stack_bench(args, steps, warmup, cpu_seconds):
     def prep_pass(k):
         for L in range(layers):
             _, ex, ey = inputs[L]
+            if npre == 1:  # the whole layer in one call
+                stack.prepare_layer(built[L], ex, ey, flags[L], out=preps[L], stream=s_preps[0])
+                continue
             for i, grp in enumerate(stack.INPUTS):
                 if i % npre == k:
                     stack.prepare_input(built[L], grp, ex, ey, preps[L], flag=flags[L, i], stream=s_preps[k])

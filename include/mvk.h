@@ -53,7 +53,7 @@ extern "C" {
 
 #define MVK_PRIME 2147483647u
 #define MVK_PRIME_BABYBEAR 2013265921u
-#define MVK_ABI_VERSION 6
+#define MVK_ABI_VERSION 7
 
 typedef int32_t mvk_status;
 #define MVK_OK 0
@@ -329,6 +329,32 @@ mvk_status mvk_client_prepare_group(uint32_t G, const mvk_key *const *keys, cons
                                     const mvk_sparse *const *ey, uint32_t *Mx, uint32_t *const *My,
                                     uint32_t *const *R, uint32_t *const *U, uint32_t *done_flag, uint32_t done_value,
                                     void *stream);
+
+/*
+ * Client preparation of several inputs and the keys they feed in one call
+ * (for example the four inputs and seven projections of a decoder layer):
+ * every syndrome of block length at most 16384 and every row gather of the
+ * call run in one launch, instead of one launch per input.
+ *   G    : 1..MVK_MAX_PREP keys; keys, ex, ey, Mx, My, R, U: host arrays of G
+ *          entries (ex, ey, done_flags may also be NULL as a whole)
+ *   ex[g]: noise of key g's input (NULL or count 0: no masks for key g).
+ *          Keys whose Mx[g] is the same buffer share that input: their ex[g]
+ *          must then describe the same vectors (the same idx and val buffers,
+ *          count and t) and their privacy codes must be the same arrays; the
+ *          input mask is computed once.
+ *   ey[g]: challenges of key g (NULL or count 0: none)
+ *   Mx[g], My[g], R[g], U[g]: as mvk_client_prepare for key g
+ *   done_flags[g] (device word or NULL): set to done_value once every output
+ *          of the call is stored and visible device-wide
+ * Same outputs, bit for bit, as G calls of mvk_client_prepare.
+ * Errors: as mvk_client_prepare, plus MVK_EINVAL (G out of range, keys that
+ * share an input buffer with different noise or privacy codes).
+ */
+#define MVK_MAX_PREP 8u
+mvk_status mvk_client_prepare_multi(uint32_t G, const mvk_key *const *keys, const mvk_sparse *const *ex,
+                                    const mvk_sparse *const *ey, uint32_t *const *Mx, uint32_t *const *My,
+                                    uint32_t *const *R, uint32_t *const *U, uint32_t *const *done_flags,
+                                    uint32_t done_value, void *stream);
 
 /*
  * Encrypt with a prepared input mask: Xhat = X + Mx (B x n, element-wise mod p).

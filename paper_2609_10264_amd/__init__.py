@@ -341,6 +341,64 @@ def client_prepare_group(keys: list, ex_idx: torch.Tensor, ex_val: torch.Tensor,
     return outs
 
 
+def client_prepare_multi(keys: list, exs: list, eys: list, outs: list | None = None, done_flags: list | None = None,
+                         done_value: int = 1, stream=None) -> list:
+    """client_prepare for several keys and inputs in one call (one launch for
+    the short syndromes and every row gather).  exs[g] = (ex_idx, ex_val) of
+    key g's input, or None; eys[g] = (ey_idx, ey_val) or None.  Keys listed
+    with the same noise tensors share their input: the input mask is computed
+    once and every Prepared of that input holds the same Mx tensor.
+    done_flags: None, or per key a device word (or None) set to done_value
+    once every output of the call is visible."""
+    G = len(keys)
+    if not 1 <= G <= _lib.MVK_MAX_PREP or len(exs) != G or len(eys) != G:
+        raise ValueError(f"1..{_lib.MVK_MAX_PREP} keys, with one noise and one challenge entry each")
+    dev_ = next(t[0].device for t in list(exs) + list(eys) if t is not None)
+    if outs is None:
+        outs = [Prepared(k, exs[g][0].shape[0] if exs[g] is not None else 0,
+                         eys[g][0].shape[0] if eys[g] is not None else 0, device=dev_) for g, k in enumerate(keys)]
+    # one input mask per distinct noise: the first Prepared of that noise holds it
+    owner = {}
+    for g, e in enumerate(exs):
+        if e is not None:
+            k = (e[0].data_ptr(), e[1].data_ptr())
+            if k in owner:
+                outs[g].Mx = outs[owner[k]].Mx
+            else:
+                owner[k] = g
+    structs = [k.struct() for k in keys]
+    kp = (ctypes.POINTER(MvkKey) * G)(*[ctypes.pointer(ks) for ks in structs])
+    ex_s = [_sparse(e[0], e[1], f"ex[{g}]") if e is not None else None for g, e in enumerate(exs)]
+    ey_s = [_sparse(e[0], e[1], f"ey[{g}]") if e is not None else None for g, e in enumerate(eys)]
+    exp = (ctypes.POINTER(MvkSparse) * G)(*[ctypes.pointer(e) if e is not None else None for e in ex_s])
+    eyp = (ctypes.POINTER(MvkSparse) * G)(*[ctypes.pointer(e) if e is not None else None for e in ey_s])
+
+    for g, o in enumerate(outs):
+        if (exs[g] is not None and o.B != exs[g][0].shape[0]) or (eys[g] is not None and o.ell != eys[g][0].shape[0]):
+            raise ValueError("Prepared buffers do not match the noise / challenge counts")
+
+    def arr(name, pick):
+        """Device pointers of one output per key; pick(g) -> (tensor, shape) or None."""
+        ptrs = []
+        for g in range(G):
+            ts = pick(g)
+            ptrs.append(_dev(ts[0], torch.int32, ts[1], f"{name}[{g}]") if ts is not None else None)
+        return (ctypes.c_void_p * G)(*ptrs)
+
+    ks_, os_ = keys, outs
+    Mx = arr("Mx", lambda g: (os_[g].Mx, (os_[g].B, ks_[g].n)) if exs[g] is not None else None)
+    My = arr("My", lambda g: (os_[g].My, (os_[g].B, ks_[g].m)) if exs[g] is not None else None)
+    R = arr("R", lambda g: (os_[g].R, (os_[g].ell, ks_[g].m)) if eys[g] is not None else None)
+    U = arr("U", lambda g: (os_[g].U, (os_[g].ell, ks_[g].n)) if eys[g] is not None else None)
+    flags = None
+    if done_flags is not None:
+        flags = (ctypes.c_void_p * G)(*[_dev(f, torch.int32, (), f"done_flags[{g}]") if f is not None else None
+                                        for g, f in enumerate(done_flags)])
+    _lib.check("mvk_client_prepare_multi", _lib.load(keys[0].p).mvk_client_prepare_multi(
+        G, kp, exp, eyp, Mx, My, R, U, flags, done_value, _stream(stream)))
+    return outs
+
+
 def encode_masked(key: Key, X: torch.Tensor, prep: Prepared, out: torch.Tensor | None = None,
                   ready_flag: torch.Tensor | None = None, ready_value: int = 1, timeout_us: int = 200000,
                   timed_out: torch.Tensor | None = None, stream=None) -> torch.Tensor:

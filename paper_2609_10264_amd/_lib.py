@@ -31,7 +31,8 @@ MVK_SEED_FRESH = 0xFFFFFFFFFFFFFFFF
 MVK_SEEDED_MAX_T = 4096
 MVK_STATIC_SCRATCH_BYTES = 32 << 20
 MVK_MAX_GROUP = 4
-ABI_VERSION = 6
+MVK_MAX_PREP = 8
+ABI_VERSION = 7
 # field modulus -> library built over that field
 LIB_PATHS = {MVK_PRIME: LIB_PATH, MVK_PRIME_BABYBEAR: LIB_PATH_BB}
 
@@ -76,6 +77,7 @@ EXPORTS = (
     "mvk_server_eval_packed_group",
     "mvk_decode_verify_masked_group",
     "mvk_client_prepare_group",
+    "mvk_client_prepare_multi",
 )
 
 
@@ -221,6 +223,10 @@ def load(p: int = MVK_PRIME) -> ctypes.CDLL:
     L.mvk_client_prepare_group.argtypes = [u32, ctypes.POINTER(ctypes.POINTER(MvkKey)), ctypes.POINTER(MvkSparse),
                                            ctypes.POINTER(ctypes.POINTER(MvkSparse)), vp, pvp, pvp, pvp, vp, u32, vp]
     L.mvk_client_prepare_group.restype = st
+    L.mvk_client_prepare_multi.argtypes = [u32, ctypes.POINTER(ctypes.POINTER(MvkKey)),
+                                           ctypes.POINTER(ctypes.POINTER(MvkSparse)),
+                                           ctypes.POINTER(ctypes.POINTER(MvkSparse)), pvp, pvp, pvp, pvp, pvp, u32, vp]
+    L.mvk_client_prepare_multi.restype = st
     if L.mvk_abi_version() != ABI_VERSION:
         raise ImportError(f"{path}: ABI version mismatch; rebuild the library")
     if L.mvk_field_modulus() != p:

@@ -628,6 +628,74 @@ mvk_status mvk_client_prepare_group(uint32_t G, const mvk_key* const* keys, cons
                                                   (uint32_t*)ws, &ctrl[kPrepCounterWord], done_flag, done_value, s));
 }
 
+mvk_status mvk_client_prepare_multi(uint32_t G, const mvk_key* const* keys, const mvk_sparse* const* ex,
+                                    const mvk_sparse* const* ey, uint32_t* const* Mx, uint32_t* const* My,
+                                    uint32_t* const* R, uint32_t* const* U, uint32_t* const* done_flags,
+                                    uint32_t done_value, void* stream) {
+    if (G == 0 || G > MVK_MAX_PREP || !keys) return MVK_EINVAL;
+    PrepInputDesc ins[kMaxPrep];
+    PrepProbDesc probs[kMaxPrep];
+    uint32_t* flags[kMaxPrep];
+    uint32_t NI = 0, nflags = 0;
+    bool work = false;
+    for (uint32_t g = 0; g < G; ++g) {
+        mvk_status st = check_key(keys[g]);
+        if (st) return st;
+        const mvk_key& k = *keys[g];
+        uint32_t in = kPrepNoInput;
+        const mvk_sparse* e = ex ? ex[g] : nullptr;
+        if (e && e->count) {
+            if (!Mx || !Mx[g] || !My || !My[g] || !k.PT || (e->t && (!e->idx || !e->val))) return MVK_EINVAL;
+            if ((uint64_t)e->t > (uint64_t)k.cx.r * k.n) return MVK_EINVAL;
+            if (e->count > 65535u) return MVK_ERANGE;
+            for (uint32_t j = 0; j < NI; ++j) {
+                if (ins[j].Mx != Mx[g]) continue;
+                // a shared input: the same noise vectors over the same privacy code
+                const mvk_code& c = *ins[j].cx;
+                if (ins[j].idx != e->idx || ins[j].val != e->val || ins[j].t != e->t || ins[j].count != e->count ||
+                    c.k != k.cx.k || c.r != k.cx.r || c.pi1 != k.cx.pi1 || c.pi2 != k.cx.pi2 || c.v1 != k.cx.v1 ||
+                    c.v2 != k.cx.v2)
+                    return MVK_EINVAL;
+                in = j;
+            }
+            if (in == kPrepNoInput) {
+                ins[NI] = PrepInputDesc{&k.cx, e->idx, e->val, e->t, e->count, Mx[g]};
+                in = NI++;
+            }
+            work = true;
+        }
+        const mvk_sparse* q = ey ? ey[g] : nullptr;
+        const uint32_t ny = q ? q->count : 0u;
+        if (ny) {
+            st = check_challenges(&k, q);
+            if (st) return st;
+            if (!R || !R[g] || !U || !U[g] || !k.Q) return MVK_EINVAL;
+            work = true;
+        }
+        probs[g] = PrepProbDesc{&k, in, ny ? q->idx : nullptr, ny ? q->val : nullptr, ny ? q->t : 0u, ny,
+                                in != kPrepNoInput ? My[g] : nullptr, ny ? R[g] : nullptr, ny ? U[g] : nullptr};
+        if (done_flags && done_flags[g]) {
+            bool seen = false;
+            for (uint32_t f = 0; f < nflags; ++f) seen = seen || flags[f] == done_flags[g];
+            if (!seen) flags[nflags++] = done_flags[g];
+        }
+    }
+    if (nflags && done_value == 0) return MVK_EINVAL;
+    hipStream_t s = (hipStream_t)stream;
+    if (!work) {
+        for (uint32_t f = 0; f < nflags; ++f)
+            if (launch_flag_signal(flags[f], done_value, s) != hipSuccess) return MVK_EHIP;
+        return MVK_OK;
+    }
+    void* ws = nullptr;
+    uint32_t* ctrl = nullptr;
+    const mvk_status st = workspace(s, prep_scratch_bytes(ins, NI, probs, G), &ws, &ctrl,
+                                    4 * (kPrepCounterWord + prep_ctrl_words(ins, NI, probs, G)));
+    if (st) return st;
+    return hip_status(launch_client_prepare_multi(ins, NI, probs, G, (uint32_t*)ws, &ctrl[kPrepCounterWord],
+                                                  nflags ? flags : nullptr, nflags, done_value, s));
+}
+
 mvk_status mvk_encode_masked(const mvk_key* key, const uint32_t* X, uint32_t B, const uint32_t* Mx, uint32_t* Xhat,
                              uint32_t* ready_flag, uint32_t ready_value, uint32_t timeout_us, uint32_t* timed_out,
                              void* stream) {

@@ -131,6 +131,34 @@ hipError_t launch_decode_verify_masked_group(uint32_t G, uint32_t m, uint32_t n,
 // prep_ctrl_words(key, nx, ny) words of completion counters (count.h), zero
 // before the launch (left zero).
 size_t prep_ctrl_words(const mvk_key& key, uint32_t nx, uint32_t ny);
+// Several inputs and the keys they feed in one launch (at most kMaxPrep of
+// each): input j holds `count` noise vectors of `t` terms over the privacy
+// code cx (Mx: count x cx->k); key g the output masks My of the noise of input
+// `in` (kPrepNoInput: none) and `count` challenges with R, U.  Syndromes
+// longer than kSynScratchAbove run first in their own launches (scratch of
+// prep_scratch_bytes); done: ndone device words, each set to done_value once
+// every output is stored and visible device-wide; counter: prep_ctrl_words
+// words, zero before the launch (left zero).
+constexpr uint32_t kMaxPrep = MVK_MAX_PREP;
+constexpr uint32_t kPrepNoInput = 0xffffffffu;
+struct PrepInputDesc {
+    const mvk_code* cx;
+    const uint32_t *idx, *val;
+    uint32_t t, count;
+    uint32_t* Mx;
+};
+struct PrepProbDesc {
+    const mvk_key* key;
+    uint32_t in;
+    const uint32_t *idx, *val;
+    uint32_t t, count;
+    uint32_t *My, *R, *U;
+};
+size_t prep_ctrl_words(const PrepInputDesc* ins, uint32_t NI, const PrepProbDesc* probs, uint32_t G);
+size_t prep_scratch_bytes(const PrepInputDesc* ins, uint32_t NI, const PrepProbDesc* probs, uint32_t G);
+hipError_t launch_client_prepare_multi(const PrepInputDesc* ins, uint32_t NI, const PrepProbDesc* probs, uint32_t G,
+                                       uint32_t* scratch, uint32_t* counter, uint32_t* const* done, uint32_t ndone,
+                                       uint32_t done_value, hipStream_t s);
 size_t prep_ctrl_words(const mvk_key* const* keys, uint32_t G, uint32_t nx, uint32_t ny);
 // The same for G <= kMaxGroup keys of one shape and one privacy code that share
 // the noise vectors (Mx once; My[g], R[g], Uq[g] per key, with the challenges

@@ -61,15 +61,20 @@ __device__ __forceinline__ void gather_item(const uint32_t* __restrict__ M, uint
 #pragma unroll
     for (int e = 0; e < E; ++e) acc[e] = 0;
     for (uint32_t s0 = s_beg; s0 < s_end; s0 += kQBatch) {
+        // the batch's terms first: lane u loads term s0 + u (two loads, one
+        // wait), and each term is read back from its lane as a wave-uniform
+        // value; then every row load of the batch is issued before the first
+        // is used (a row load never waits for a later term's index)
+        const uint32_t lt = s0 + (uint32_t)(lane & (kQBatch - 1));
+        const uint32_t lts = lt < s_end ? lt : s_beg;  // in-range term, value masked below
+        const uint32_t jl = idx[lts], vl = val[lts];
         uint32_t mv[kQBatch][E], ww[kQBatch];
 #pragma unroll
         for (int u = 0; u < kQBatch; ++u) {
-            const uint32_t sx = s0 + (uint32_t)u;
-            const bool ok = sx < s_end;
-            const uint32_t sl = ok ? sx : s_beg;  // in-range term, value masked below
-            uint32_t j = idx[sl];
+            const bool ok = s0 + (uint32_t)u < s_end;
+            uint32_t j = (uint32_t)__builtin_amdgcn_readlane((int)jl, u);
             j = j < nrows ? j : nrows - 1;
-            ww[u] = ok ? val[sl] : 0u;
+            ww[u] = ok ? (uint32_t)__builtin_amdgcn_readlane((int)vl, u) : 0u;
             const uint32_t* src = M + (size_t)j * ld + is;
             // non-temporal: every row segment is read once per launch
             if constexpr (VEC) {
@@ -113,60 +118,78 @@ constexpr size_t prep_lds_words() {
         return gather;
 }
 
-struct PrepArgs {
-    // G problems (keys of one shape and one privacy code) share the noise
-    // vectors and their input mask Mx; each has its own verification code,
-    // challenges, P^T, Q and outputs My, R, Uq.
-    uint32_t G;
-    // syndromes in this launch: nsx noise vectors of code x (Mx); nsy
-    // challenges of code y per problem (R)
-    uint32_t nsx, nsy;
-    uint32_t n, rx, m, ry;
-    const uint32_t *xpi1, *xpi2, *xv1, *xv2;
-    const uint32_t *ypi1[kMaxGroup], *ypi2[kMaxGroup], *yv1[kMaxGroup], *yv2[kMaxGroup];
-    const uint32_t *ex_idx, *ex_val;
-    uint32_t tx, nx;  // nx noise vectors (My items), tx terms each
-    const uint32_t *ey_idx[kMaxGroup], *ey_val[kMaxGroup];
-    uint32_t ty, ny;  // ny challenges per problem (U items), ty terms each
-    uint32_t nbm, nbn;  // gather_cols(VEC)-column blocks of m and n
-    const uint32_t *PT[kMaxGroup], *Q[kMaxGroup];
+// One input of a preparation launch: count noise vectors e_b of t terms over
+// the privacy code (block length r*n) and their input masks Mx (count x n).
+struct PrepIn {
+    const uint32_t *pi1, *pi2, *v1, *v2;
+    const uint32_t *idx, *val;
     uint32_t* Mx;
-    uint32_t* My[kMaxGroup];
-    uint32_t* R[kMaxGroup];
-    uint32_t* Uq[kMaxGroup];
+    uint32_t n, r, t, count;
+};
+// One key of a preparation launch: the output masks My_b = P e_b of the noise
+// of its input (index `in`), and count challenges e_q of t
+// terms over its verification code (block length r*m) with R_q = Gy e_q and
+// U_q = e_q^T Q.  (With no output masks items_x is 0 and `in` is not read.)
+struct PrepProb {
+    const uint32_t *pi1, *pi2, *v1, *v2;
+    const uint32_t *idx, *val;
+    const uint32_t *PT, *Q;
+    uint32_t *My, *R, *U;
+    uint32_t m, n, r, t, count, in;
+    uint32_t nbm, nbn;  // gather_cols(VEC)-column blocks of m and n
+    uint32_t items_x;   // My items: noise vectors of the input x nbm
+};
+struct PrepArgs {
+    uint32_t NI, G;
+    PrepIn in[kMaxPrep];
+    PrepProb pr[kMaxPrep];
+    // cumulative workgroup and item counts: noise syndromes of inputs < j + 1
+    // (syndromes in this launch only), then challenge syndromes of keys
+    // < g + 1 (after all noise syndromes), then gather items of keys < g + 1
+    uint32_t sx_end[kMaxPrep], sy_end[kMaxPrep], it_end[kMaxPrep];
     uint32_t* counter;  // SIG: completion counters (count.h; zero before and after the launch)
     uint32_t slots;
-    uint32_t* done;     // SIG: set to done_value once every output is stored
-    uint32_t done_value;
+    uint32_t* done[kMaxPrep];  // SIG: each set to done_value once every output is stored
+    uint32_t ndone, done_value;
 };
 
-// Workgroups [0, nsx): one noise syndrome each; [nsx, nsx + G * nsy): one
-// challenge syndrome each, problem by problem (U > 0; the whole block in
-// LDS); the rest: kQuarters gather items each, per problem first the
-// nx * nbm items of My (rows of its PT), then the ny * nbn items of U (rows
-// of its Q).  VEC: m and n are multiples of 4 and every PT, Q 16-byte aligned.
-// SIG: every output is stored device-coherently; each workgroup waits for its
-// stores to complete (vmcnt 0) before the barrier and then counts itself done
-// (count.h); the last one sets the done flag, so a kernel of another stream
-// that sees the flag sees every output.
+// Workgroups [0, sx_end[NI-1]): one noise syndrome each, input by input;
+// then one challenge syndrome each, key by key (U > 0; the whole block in
+// LDS; only the blocks short enough, the longer ones ran before); the rest:
+// kQuarters gather items each, per key first the items of My (rows of its
+// PT, the noise of its input), then those of U (rows of its Q).  VEC: every
+// m and n a multiple of 4 and every PT, Q 16-byte aligned.  SIG: every output
+// is stored device-coherently; each workgroup waits for its stores to complete
+// (vmcnt 0) before the barrier and then counts itself done (count.h); the last
+// one sets the done flags, so a kernel of another stream that sees a flag
+// sees every output.  The descriptors are indexed by workgroup-uniform values,
+// so they come through scalar loads from the kernel arguments.
 template <int U, bool SIG, bool VEC>
 __global__ __launch_bounds__(kPrepThreads) void client_prepare_kernel(PrepArgs a) {
     __shared__ __align__(16) uint32_t lds[prep_lds_words<U>()];
     uint32_t bid = blockIdx.x;
     bool gather = true;
     if constexpr (U > 0) {
-        if (bid < a.nsx) {
-            syn::syn_block<true, U, kPrepThreads, SIG>(bid, a.n, a.rx, a.xpi1, a.xpi2, a.xv1, a.xv2, nullptr,
-                                                       a.ex_idx, a.ex_val, a.tx, nullptr, a.Mx, lds);
+        const uint32_t sx = a.NI ? a.sx_end[a.NI - 1] : 0u;
+        const uint32_t sy = a.G ? a.sy_end[a.G - 1] : sx;
+        if (bid < sx) {
+            uint32_t j = 0;
+            while (bid >= a.sx_end[j]) ++j;
+            const PrepIn& in = a.in[j];
+            syn::syn_block<true, U, kPrepThreads, SIG>(bid - (j ? a.sx_end[j - 1] : 0u), in.n, in.r, in.pi1, in.pi2,
+                                                       in.v1, in.v2, nullptr, in.idx, in.val, in.t, nullptr, in.Mx,
+                                                       lds);
             gather = false;
-        } else if (bid < a.nsx + a.G * a.nsy) {
-            const uint32_t k = bid - a.nsx, g = k / a.nsy;
-            syn::syn_block<true, U, kPrepThreads, SIG>(k - g * a.nsy, a.m, a.ry, a.ypi1[g], a.ypi2[g], a.yv1[g],
-                                                       a.yv2[g], nullptr, a.ey_idx[g], a.ey_val[g], a.ty, nullptr,
-                                                       a.R[g], lds);
+        } else if (bid < sy) {
+            uint32_t g = 0;
+            while (bid >= a.sy_end[g]) ++g;
+            const PrepProb& pr = a.pr[g];
+            syn::syn_block<true, U, kPrepThreads, SIG>(bid - (g ? a.sy_end[g - 1] : sx), pr.m, pr.r, pr.pi1, pr.pi2,
+                                                       pr.v1, pr.v2, nullptr, pr.idx, pr.val, pr.t, nullptr, pr.R,
+                                                       lds);
             gather = false;
         } else {
-            bid -= a.nsx + a.G * a.nsy;
+            bid -= sy;
         }
     }
     if (gather) {
@@ -174,19 +197,21 @@ __global__ __launch_bounds__(kPrepThreads) void client_prepare_kernel(PrepArgs a
         uint64_t* part = reinterpret_cast<uint64_t*>(lds) + quarter * gather_part(VEC);
         constexpr uint32_t cols = gather_cols(VEC);
         uint32_t item = bid * kQuarters + (uint32_t)quarter;
-        const uint32_t nbm = a.nbm, nbn = a.nbn;
-        const uint32_t ix = a.nx * nbm, iy = a.ny * nbn, per = ix + iy;
-        const uint32_t g = per ? item / per : a.G;
-        item -= g < a.G ? g * per : 0u;
-        if (g < a.G && item < ix) {
-            const uint32_t b = item / nbm, cb = item % nbm;
-            gather_item<SIG, VEC>(a.PT[g], a.m, a.rx * a.n, a.ex_idx + (size_t)b * a.tx,
-                                  a.ex_val + (size_t)b * a.tx, a.tx, a.My[g] + (size_t)b * a.m, cb * cols, true, part);
-        } else if (g < a.G) {
-            const uint32_t q = (item - ix) / nbn, cb = (item - ix) % nbn;
-            gather_item<SIG, VEC>(a.Q[g], a.n, a.ry * a.m, a.ey_idx[g] + (size_t)q * a.ty,
-                                  a.ey_val[g] + (size_t)q * a.ty, a.ty, a.Uq[g] + (size_t)q * a.n, cb * cols, true,
-                                  part);
+        uint32_t g = 0;
+        while (g < a.G && item >= a.it_end[g]) ++g;
+        if (g < a.G) {
+            const PrepProb& pr = a.pr[g];
+            item -= g ? a.it_end[g - 1] : 0u;
+            if (item < pr.items_x) {
+                const PrepIn& in = a.in[pr.in];
+                const uint32_t b = item / pr.nbm, cb = item % pr.nbm;
+                gather_item<SIG, VEC>(pr.PT, pr.m, in.r * in.n, in.idx + (size_t)b * in.t, in.val + (size_t)b * in.t,
+                                      in.t, pr.My + (size_t)b * pr.m, cb * cols, true, part);
+            } else {
+                const uint32_t q = (item - pr.items_x) / pr.nbn, cb = (item - pr.items_x) % pr.nbn;
+                gather_item<SIG, VEC>(pr.Q, pr.n, pr.r * pr.m, pr.idx + (size_t)q * pr.t, pr.val + (size_t)q * pr.t,
+                                      pr.t, pr.U + (size_t)q * pr.n, cb * cols, true, part);
+            }
         } else {
             gather_item<SIG, VEC>(nullptr, 0u, 1u, nullptr, nullptr, 0u, nullptr, 0u, false, part);
         }
@@ -195,7 +220,8 @@ __global__ __launch_bounds__(kPrepThreads) void client_prepare_kernel(PrepArgs a
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
         if (threadIdx.x == 0 && count_last(a.counter, a.slots))
-            __hip_atomic_store(a.done, a.done_value, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            for (uint32_t f = 0; f < a.ndone; ++f)
+                __hip_atomic_store(a.done[f], a.done_value, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 }
 
@@ -328,37 +354,185 @@ uint32_t prep_u(uint64_t N) {
     return 0;
 }
 
+// Whether a syndrome of block length N runs inside the preparation launch.
+bool prep_short(uint64_t N) { return prep_u(N) != 0; }
+
+// Noise vectors behind the output masks of key g (those of its input).
+uint32_t prob_nx(const PrepInputDesc* ins, const PrepProbDesc& p) {
+    return p.in == kPrepNoInput ? 0u : ins[p.in].count;
+}
+
 // Whether the gathers of client_prepare_kernel read 16 bytes per lane: when
 // the rows allow it and the 64-column items would need more than 256
 // workgroups (a quarter as many wider items then still keep the chip busy;
 // below, more and narrower items spread the gathers over more compute units:
 // at 4096 x 4096 with one column the wider items cost a microsecond per step).
-bool prep_vec(const mvk_key* const* keys, uint32_t G, uint32_t nx, uint32_t ny) {
-    const mvk_key& key = *keys[0];
-    if (key.m % 4 != 0 || key.n % 4 != 0) return false;
-    for (uint32_t g = 0; g < G; ++g)
-        if (((uintptr_t)keys[g]->PT & 15) != 0 || ((uintptr_t)keys[g]->Q & 15) != 0) return false;
-    const uint64_t items = (uint64_t)G * ((uint64_t)nx * ceil_div(key.m, gather_cols(false)) +
-                                          (uint64_t)ny * ceil_div(key.n, gather_cols(false)));
+bool prep_vec(const PrepInputDesc* ins, const PrepProbDesc* probs, uint32_t G) {
+    uint64_t items = 0;
+    for (uint32_t g = 0; g < G; ++g) {
+        const mvk_key& key = *probs[g].key;
+        const uint32_t nx = prob_nx(ins, probs[g]), ny = probs[g].count;
+        if (nx == 0 && ny == 0) continue;
+        if (key.m % 4 != 0 || key.n % 4 != 0) return false;
+        if (((uintptr_t)key.PT & 15) != 0 || ((uintptr_t)key.Q & 15) != 0) return false;
+        items += (uint64_t)nx * ceil_div(key.m, gather_cols(false)) + (uint64_t)ny * ceil_div(key.n, gather_cols(false));
+    }
     return items > 256u * kQuarters;
 }
 
-// Workgroups of client_prepare_kernel: one per syndrome short enough for one
-// workgroup, then the gather items, kQuarters per workgroup.
-uint64_t prep_grid(const mvk_key* const* keys, uint32_t G, uint32_t nx, uint32_t ny) {
-    const mvk_key& key = *keys[0];
-    const uint64_t Nx = (uint64_t)key.cx.r * key.n, Ny = (uint64_t)key.cy.r * key.m;
-    const uint32_t ux = nx ? prep_u(Nx) : 0u, uy = ny ? prep_u(Ny) : 0u;
-    const uint32_t cols = gather_cols(prep_vec(keys, G, nx, ny));
-    const uint64_t items = (uint64_t)G * ((uint64_t)nx * ceil_div(key.m, cols) + (uint64_t)ny * ceil_div(key.n, cols));
-    return (ux ? nx : 0u) + (uy ? (uint64_t)G * ny : 0u) + (items + kQuarters - 1) / kQuarters;
+// The launch's arguments, syndrome tile and grid (workgroups: the syndromes
+// short enough for one workgroup, then the gather items, kQuarters per
+// workgroup).
+struct PrepPlan {
+    PrepArgs a;
+    uint32_t U;
+    bool vec;
+    uint64_t grid;
+};
+
+PrepPlan prep_plan(const PrepInputDesc* ins, uint32_t NI, const PrepProbDesc* probs, uint32_t G) {
+    PrepPlan pl{};
+    PrepArgs& a = pl.a;
+    a.NI = NI;
+    a.G = G;
+    pl.vec = prep_vec(ins, probs, G);
+    const uint32_t cols = gather_cols(pl.vec);
+    uint64_t sx = 0, sy = 0, items = 0;
+    for (uint32_t j = 0; j < NI; ++j) {
+        const PrepInputDesc& d = ins[j];
+        PrepIn& in = a.in[j];
+        const mvk_code* c = d.cx;
+        in.pi1 = c->pi1, in.pi2 = c->pi2, in.v1 = c->v1, in.v2 = c->v2;
+        in.idx = d.idx, in.val = d.val, in.Mx = d.Mx;
+        in.n = c->k, in.r = c->r, in.t = d.t, in.count = d.count;
+        const uint64_t N = (uint64_t)c->k * c->r;
+        if (d.count && prep_short(N)) {
+            sx += d.count;
+            pl.U = prep_u(N) > pl.U ? prep_u(N) : pl.U;
+        }
+        a.sx_end[j] = (uint32_t)(sx < 0xffffffffu ? sx : 0xffffffffu);
+    }
+    sy = sx;
+    for (uint32_t g = 0; g < G; ++g) {
+        const PrepProbDesc& d = probs[g];
+        const mvk_key& key = *d.key;
+        PrepProb& pr = a.pr[g];
+        pr.pi1 = key.cy.pi1, pr.pi2 = key.cy.pi2, pr.v1 = key.cy.v1, pr.v2 = key.cy.v2;
+        pr.idx = d.idx, pr.val = d.val, pr.PT = key.PT, pr.Q = key.Q;
+        pr.My = d.My, pr.R = d.R, pr.U = d.U;
+        pr.m = key.m, pr.n = key.n, pr.r = key.cy.r, pr.t = d.t, pr.count = d.count;
+        const uint32_t nx = prob_nx(ins, d);
+        pr.in = nx ? d.in : 0u;
+        pr.nbm = ceil_div(key.m, cols), pr.nbn = ceil_div(key.n, cols);
+        const uint64_t ix = (uint64_t)nx * pr.nbm, iy = (uint64_t)d.count * pr.nbn;
+        pr.items_x = (uint32_t)(ix < 0xffffffffu ? ix : 0xffffffffu);
+        const uint64_t N = (uint64_t)key.m * key.cy.r;
+        if (d.count && prep_short(N)) {
+            sy += d.count;
+            pl.U = prep_u(N) > pl.U ? prep_u(N) : pl.U;
+        }
+        a.sy_end[g] = (uint32_t)(sy < 0xffffffffu ? sy : 0xffffffffu);
+        items += ix + iy;
+        a.it_end[g] = (uint32_t)(items < 0xffffffffu ? items : 0xffffffffu);
+    }
+    pl.grid = sy + (items + kQuarters - 1) / kQuarters;
+    return pl;
 }
 
 }  // namespace
 
-size_t prep_ctrl_words(const mvk_key* const* keys, uint32_t G, uint32_t nx, uint32_t ny) {
-    const uint64_t grid = prep_grid(keys, G, nx, ny);
+size_t prep_ctrl_words(const PrepInputDesc* ins, uint32_t NI, const PrepProbDesc* probs, uint32_t G) {
+    const uint64_t grid = prep_plan(ins, NI, probs, G).grid;
     return count_words(count_slots(grid > 0x7fffffffu ? 0x7fffffffu : (uint32_t)grid));
+}
+
+size_t prep_scratch_bytes(const PrepInputDesc* ins, uint32_t NI, const PrepProbDesc* probs, uint32_t G) {
+    size_t b = 0;
+    for (uint32_t j = 0; j < NI; ++j) {
+        const uint64_t N = (uint64_t)ins[j].cx->k * ins[j].cx->r;
+        if (ins[j].count && !prep_short(N) && syn_scratch_bytes(ins[j].count, N) > b)
+            b = syn_scratch_bytes(ins[j].count, N);
+    }
+    for (uint32_t g = 0; g < G; ++g) {
+        const uint64_t N = (uint64_t)probs[g].key->m * probs[g].key->cy.r;
+        if (probs[g].count && !prep_short(N) && syn_scratch_bytes(probs[g].count, N) > b)
+            b = syn_scratch_bytes(probs[g].count, N);
+    }
+    return b;
+}
+
+hipError_t launch_client_prepare_multi(const PrepInputDesc* ins, uint32_t NI, const PrepProbDesc* probs, uint32_t G,
+                                       uint32_t* scratch, uint32_t* counter, uint32_t* const* done, uint32_t ndone,
+                                       uint32_t done_value, hipStream_t s) {
+    if (NI > kMaxPrep || G == 0 || G > kMaxPrep || ndone > kMaxPrep) return hipErrorInvalidValue;
+    // syndromes too long for one workgroup run in their own (segmented) launches first
+    for (uint32_t j = 0; j < NI; ++j) {
+        const PrepInputDesc& d = ins[j];
+        if (d.count && !prep_short((uint64_t)d.cx->k * d.cx->r)) {
+            const hipError_t e = launch_syn_sparse(*d.cx, d.idx, d.val, d.t, d.count, nullptr, scratch, d.Mx, s);
+            if (e != hipSuccess) return e;
+        }
+    }
+    for (uint32_t g = 0; g < G; ++g) {
+        const PrepProbDesc& d = probs[g];
+        if (d.count && !prep_short((uint64_t)d.key->m * d.key->cy.r)) {
+            const hipError_t e = launch_syn_sparse(d.key->cy, d.idx, d.val, d.t, d.count, nullptr, scratch, d.R, s);
+            if (e != hipSuccess) return e;
+        }
+    }
+    PrepPlan pl = prep_plan(ins, NI, probs, G);
+    if (pl.grid == 0) return hipSuccess;
+    if (pl.grid > 0x7fffffffu) return hipErrorInvalidValue;
+    PrepArgs& a = pl.a;
+    a.counter = counter;
+    a.slots = count_slots((uint32_t)pl.grid);
+    a.ndone = done ? ndone : 0u;
+    for (uint32_t f = 0; f < a.ndone; ++f) a.done[f] = done[f];
+    a.done_value = done_value;
+    const bool sig = a.ndone > 0;
+    const dim3 grid((uint32_t)pl.grid), block(kPrepThreads);
+#define MVK_PREP_V(UU, SIG)                                                                             \
+    if (pl.vec)                                                                                         \
+        hipLaunchKernelGGL((client_prepare_kernel<UU, SIG, true>), grid, block, 0, s, a);              \
+    else                                                                                                \
+        hipLaunchKernelGGL((client_prepare_kernel<UU, SIG, false>), grid, block, 0, s, a)
+#define MVK_PREP(UU)          \
+    if (sig) {                \
+        MVK_PREP_V(UU, true);  \
+    } else {                  \
+        MVK_PREP_V(UU, false); \
+    }
+    if (pl.U == 0) { MVK_PREP(0); }
+    else if (pl.U == 4) { MVK_PREP(4); }
+    else if (pl.U == 8) { MVK_PREP(8); }
+    else if (pl.U == 12) { MVK_PREP(12); }
+    else { MVK_PREP(16); }
+#undef MVK_PREP
+#undef MVK_PREP_V
+    return hipGetLastError();
+}
+
+namespace {
+// The descriptors of G keys that share one input (the noise ex_idx/ex_val of
+// nx vectors, mask Mx): the privacy code of the first key.
+void group_descs(uint32_t G, const mvk_key* const* keys, const uint32_t* ex_idx, const uint32_t* ex_val,
+                 uint32_t tx, uint32_t nx, const uint32_t* const* ey_idx, const uint32_t* const* ey_val, uint32_t ty,
+                 uint32_t ny, uint32_t* Mx, uint32_t* const* My, uint32_t* const* R, uint32_t* const* Uq,
+                 PrepInputDesc* in, PrepProbDesc* probs) {
+    *in = PrepInputDesc{&keys[0]->cx, ex_idx, ex_val, tx, nx, Mx};
+    for (uint32_t g = 0; g < G; ++g)
+        probs[g] = PrepProbDesc{keys[g], 0u, ny ? ey_idx[g] : nullptr, ny ? ey_val[g] : nullptr, ty, ny,
+                                nx && My ? My[g] : nullptr, ny && R ? R[g] : nullptr, ny && Uq ? Uq[g] : nullptr};
+}
+}  // namespace
+
+size_t prep_ctrl_words(const mvk_key* const* keys, uint32_t G, uint32_t nx, uint32_t ny) {
+    if (G == 0 || G > kMaxPrep) return 0;
+    PrepInputDesc in;
+    PrepProbDesc probs[kMaxPrep];
+    group_descs(G, keys, nullptr, nullptr, 0u, nx, nullptr, nullptr, 0u, ny, nullptr, nullptr, nullptr, nullptr, &in,
+                probs);
+    return prep_ctrl_words(&in, 1, probs, G);
 }
 
 size_t prep_ctrl_words(const mvk_key& key, uint32_t nx, uint32_t ny) {
@@ -373,68 +547,11 @@ hipError_t launch_client_prepare_group(uint32_t G, const mvk_key* const* keys, c
                                        uint32_t* const* Uq, uint32_t* scratch, uint32_t* counter, uint32_t* done,
                                        uint32_t done_value, hipStream_t s) {
     if (G == 0 || G > kMaxGroup) return hipErrorInvalidValue;
-    const mvk_key& key = *keys[0];
-    const uint64_t Nx = (uint64_t)key.cx.r * key.n, Ny = (uint64_t)key.cy.r * key.m;
-    const uint32_t ux = nx ? prep_u(Nx) : 0u, uy = ny ? prep_u(Ny) : 0u;
-    // syndromes too long for one workgroup run in their own (segmented) launches first
-    if (nx && !ux) {
-        const hipError_t e = launch_syn_sparse(key.cx, ex_idx, ex_val, tx, nx, nullptr, scratch, Mx, s);
-        if (e != hipSuccess) return e;
-    }
-    if (ny && !uy) {
-        for (uint32_t g = 0; g < G; ++g) {
-            const hipError_t e = launch_syn_sparse(keys[g]->cy, ey_idx[g], ey_val[g], ty, ny, nullptr, scratch, R[g], s);
-            if (e != hipSuccess) return e;
-        }
-    }
-    PrepArgs a{};
-    a.G = G;
-    a.nsx = ux ? nx : 0u;
-    a.nsy = uy ? ny : 0u;
-    a.n = key.n;
-    a.rx = key.cx.r;
-    a.m = key.m;
-    a.ry = key.cy.r;
-    a.xpi1 = key.cx.pi1, a.xpi2 = key.cx.pi2, a.xv1 = key.cx.v1, a.xv2 = key.cx.v2;
-    a.ex_idx = ex_idx, a.ex_val = ex_val, a.tx = tx, a.nx = nx;
-    a.ty = ty, a.ny = ny;
-    for (uint32_t g = 0; g < G; ++g) {
-        const mvk_code& cy = keys[g]->cy;
-        a.ypi1[g] = cy.pi1, a.ypi2[g] = cy.pi2, a.yv1[g] = cy.v1, a.yv2[g] = cy.v2;
-        a.ey_idx[g] = ny ? ey_idx[g] : nullptr, a.ey_val[g] = ny ? ey_val[g] : nullptr;
-        a.PT[g] = keys[g]->PT, a.Q[g] = keys[g]->Q;
-        a.My[g] = nx ? My[g] : nullptr, a.R[g] = ny ? R[g] : nullptr, a.Uq[g] = ny ? Uq[g] : nullptr;
-    }
-    const bool vec = prep_vec(keys, G, nx, ny);
-    a.nbm = ceil_div(key.m, gather_cols(vec)), a.nbn = ceil_div(key.n, gather_cols(vec));
-    a.Mx = Mx;
-    a.counter = counter, a.done = done, a.done_value = done_value;
-    const uint32_t U = ux > uy ? ux : uy;
-    const uint64_t grid = prep_grid(keys, G, nx, ny);
-    if (grid == 0) return hipSuccess;
-    if (grid > 0x7fffffffu) return hipErrorInvalidValue;
-    a.slots = count_slots((uint32_t)grid);
-#define MVK_PREP_V(UU, SIG)                                                                                     \
-    if (vec)                                                                                                    \
-        hipLaunchKernelGGL((client_prepare_kernel<UU, SIG, true>), dim3((uint32_t)grid), dim3(kPrepThreads), 0, s, \
-                           a);                                                                                  \
-    else                                                                                                        \
-        hipLaunchKernelGGL((client_prepare_kernel<UU, SIG, false>), dim3((uint32_t)grid), dim3(kPrepThreads), 0,   \
-                           s, a)
-#define MVK_PREP(UU)          \
-    if (done) {               \
-        MVK_PREP_V(UU, true);  \
-    } else {                  \
-        MVK_PREP_V(UU, false); \
-    }
-    if (U == 0) { MVK_PREP(0); }
-    else if (U == 4) { MVK_PREP(4); }
-    else if (U == 8) { MVK_PREP(8); }
-    else if (U == 12) { MVK_PREP(12); }
-    else { MVK_PREP(16); }
-#undef MVK_PREP
-#undef MVK_PREP_V
-    return hipGetLastError();
+    PrepInputDesc in;
+    PrepProbDesc probs[kMaxPrep];
+    group_descs(G, keys, ex_idx, ex_val, tx, nx, ey_idx, ey_val, ty, ny, Mx, My, R, Uq, &in, probs);
+    return launch_client_prepare_multi(&in, 1, probs, G, scratch, counter, done ? &done : nullptr, done ? 1u : 0u,
+                                       done_value, s);
 }
 
 hipError_t launch_client_prepare(const mvk_key& key, const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx,

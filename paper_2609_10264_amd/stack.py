@@ -28,7 +28,7 @@ from dataclasses import dataclass, field
 
 import torch
 
-from . import (Code, Key, PackedW, Prepared, client_prepare_group, decode_verify, decode_verify_masked_group, encode,
+from . import (Code, Key, PackedW, Prepared, client_prepare_group, client_prepare_multi, decode_verify, decode_verify_masked_group, encode,
                encode_masked, keygen, pack_weights, pack_weights_group, server_eval, server_eval_group)
 
 # (name, m, n, input group)
@@ -148,15 +148,25 @@ def prepare_input(layer: Layer, group: str, ex: dict, ey: dict, preps: dict, fla
                          outs=[preps[nm] for nm in names], done_flag=flag, stream=stream)
 
 
-def prepare_layer(layer: Layer, ex: dict, ey: dict, flags: torch.Tensor, out: dict | None = None,
+def prepare_layer(layer: Layer, ex: dict, ey: dict, flags: torch.Tensor | None, out: dict | None = None,
                   stream=None) -> dict:
-    """Client preparation of one layer (prepare_input for each of the four
-    inputs).  flags: one int32 device word per input, each set to 1 once that
-    input's preparation is visible device-wide (in call order, so the last
-    flag covers the whole layer).  Returns {name: Prepared}."""
+    """Client preparation of one layer in one call (client_prepare_multi: the
+    four inputs' masks and the seven projections' output masks and challenge
+    vectors; one launch for the short syndromes and every row gather).
+    flags: one int32 device word per input (or None), each set to 1 once
+    every output of the layer is visible device-wide.  Returns {name: Prepared}."""
     preps = out if out is not None else {}
-    for i, group in enumerate(INPUTS):
-        prepare_input(layer, group, ex, ey, preps, flag=flags[i], stream=stream)
+    keys, exs, eys, outs, done = [], [], [], [], []
+    for name, _, _, group in PROJECTIONS:
+        if name not in preps:
+            preps[name] = Prepared(layer.keys[name], ex[group][0].shape[0], ey[name][0].shape[0],
+                                   device=ex[group][0].device)
+        keys.append(layer.keys[name])
+        exs.append(ex[group])
+        eys.append(ey[name])
+        outs.append(preps[name])
+        done.append(flags[INPUTS.index(group)] if flags is not None else None)
+    client_prepare_multi(keys, exs, eys, outs=outs, done_flags=done, stream=stream)
     return preps
 
 
@@ -272,10 +282,14 @@ def run_pass_overlapped(layers: list, inputs: list, preps: list, outs: list, mai
 
     def prepare(L):
         _, ex, ey = inputs[L]
-        for k, group in enumerate(INPUTS):
-            s = prep_streams[k % len(prep_streams)]
-            with torch.cuda.stream(s):
-                prepare_input(layers[L], group, ex, ey, preps[L], stream=s)
+        if len(prep_streams) == 1:  # the whole layer in one call
+            with torch.cuda.stream(prep_streams[0]):
+                prepare_layer(layers[L], ex, ey, None, out=preps[L], stream=prep_streams[0])
+        else:
+            for k, group in enumerate(INPUTS):
+                s = prep_streams[k % len(prep_streams)]
+                with torch.cuda.stream(s):
+                    prepare_input(layers[L], group, ex, ey, preps[L], stream=s)
         return [s.record_event() for s in prep_streams]
 
     ready = {0: prepare(0)} if layers else {}

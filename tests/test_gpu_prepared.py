@@ -273,3 +273,56 @@ def test_group_preparation_and_checks_match_one_key_at_a_time(G, m, n, B, r, tx,
         assert host(accs[g]).tolist() == want, g
     # the honest outputs decrypt to W x (oracle); the tampered column is the last one of the last key
     assert np.array_equal(host(Ys[0])[:B - 1], oracle.server_eval(Ws[0], X)[:B - 1])
+
+
+def test_multi_preparation_matches_oracle():
+    """client_prepare_multi over six keys of four shapes and four inputs: two
+    keys share an input (one noise, one privacy code), one input's noise
+    syndrome and one key's challenge syndromes are longer than 16384 (their own
+    launches), one key has no noise and one no challenges.  Every output
+    against the oracle (masks by Encrypt of the zero query, P e = W Gx e,
+    R by the syndrome, U = R^T W), and the done flags set."""
+    print("multi prepare: six keys, four inputs", flush=True)
+    # (m, n, r_x, r_y, t_x, ell, input), input None: no noise; ell 0: no challenges
+    spec = [(1000, 700, 3, 2, 17, 3, 0), (1000, 700, 3, 3, 17, 2, 0), (6000, 200, 2, 3, 5, 2, 1),
+            (300, 5500, 3, 2, 64, 2, 2), (2048, 1000, 2, 2, 9, 3, None), (512, 640, 2, 2, 20, 0, 3)]
+    B = {0: 3, 1: 2, 2: 2, 3: 4}
+    cxs, inputs = {}, {}
+    keys, hosts, exs, eys = [], [], [], []
+    for g, (m, n, rx, ry, tx, ell, inp) in enumerate(spec):
+        sub = 900 + g
+        W = synth.weights(synth.seed_for(61, synth.PURPOSE_W, sub), m, n)
+        cxk = inp if inp is not None else ("own", g)
+        if cxk not in cxs:
+            c = synth.raa_code(synth.seed_for(61, synth.PURPOSE_CX, 500 + len(cxs)), n, rx)
+            cxs[cxk] = (c, code(c))
+        cx_h, cx_d = cxs[cxk]
+        cy_h = synth.raa_code(synth.seed_for(61, synth.PURPOSE_CY, sub), m, ry)
+        key = mvk.Key.allocate(m, n, cx_d, code(cy_h))
+        mvk.keygen(key, dev(W))
+        keys.append(key)
+        if inp is not None and inp not in inputs:
+            i_, v_ = synth.sparse(synth.seed_for(61, synth.PURPOSE_NOISE, inp), B[inp], cx_h["N"], tx)
+            inputs[inp] = (i_, v_, (dev(i_), dev(v_)))
+        exs.append(inputs[inp][2] if inp is not None else None)
+        ey_h = synth.sparse(synth.seed_for(61, synth.PURPOSE_CHAL, sub), ell, cy_h["N"], 31) if ell else None
+        eys.append(tuple(dev(a) for a in ey_h) if ell else None)
+        hosts.append((W, cx_h, cy_h, inputs[inp][:2] if inp is not None else None, ey_h))
+    assert cxs[0][0]["N"] <= 16384 < cxs[2][0]["N"] and spec[2][0] * spec[2][3] > 16384
+    flags = [torch.zeros((), dtype=torch.int32, device="cuda") for _ in range(2)]
+    done = [flags[g % 2] if g < 4 else None for g in range(len(spec))]
+    preps = mvk.client_prepare_multi(keys, exs, eys, done_flags=done, done_value=7)
+    torch.cuda.synchronize()
+    assert [int(f.item()) for f in flags] == [7, 7]
+    assert preps[0].Mx.data_ptr() == preps[1].Mx.data_ptr()
+    for g, (W, cx_h, cy_h, ex_h, ey_h) in enumerate(hosts):
+        m, n = W.shape
+        if ex_h is not None:
+            Bg = ex_h[0].shape[0]
+            Mx = oracle.encode(cx_h, np.zeros((Bg, n), dtype=np.uint32), *ex_h)
+            assert np.array_equal(host(preps[g].Mx), Mx), (g, "Mx")
+            assert np.array_equal(host(preps[g].My), oracle.server_eval(W, Mx)), (g, "My")
+        if ey_h is not None:
+            R = np.stack([oracle.syn(cy_h, _dense(cy_h["N"], ey_h[0][q], ey_h[1][q])) for q in range(ey_h[0].shape[0])])
+            assert np.array_equal(host(preps[g].R), R), (g, "R")
+            assert np.array_equal(host(preps[g].U), oracle.server_eval(np.ascontiguousarray(W.T), R)), (g, "U")

@@ -65,6 +65,19 @@ hipError_t launch_syn_dense(const mvk_code& c, const uint32_t* v, uint32_t count
 hipError_t launch_syn_sparse(const mvk_code& c, const uint32_t* idx, const uint32_t* val, uint32_t t,
                              uint32_t count, const uint32_t* X, uint32_t* scratch, uint32_t* out,
                              hipStream_t s);
+// Sparse syndromes of long blocks (N > kSynScratchAbove) of several codes in
+// one sequence of three launches: set i is `count` vectors (idx/val: count x
+// t) over code *c, results into out (count x c->k).  scratch:
+// syn_sets_scratch_bytes(sets, S), 256-byte aligned.
+struct SynSet {
+    const mvk_code* c;
+    const uint32_t *idx, *val;
+    uint32_t t, count;
+    uint32_t* out;
+};
+constexpr uint32_t kMaxSynSets = 16;
+size_t syn_sets_scratch_bytes(const SynSet* sets, uint32_t S);
+hipError_t launch_syn_sets(const SynSet* sets, uint32_t S, uint32_t* scratch, hipStream_t s);
 // W (m x n int8) -> WT (n x m int8)
 hipError_t launch_transpose_i8(const int8_t* W, uint32_t m, uint32_t n, int8_t* WT, hipStream_t s);
 hipError_t launch_fill_u32(uint32_t* p, size_t count, uint32_t value, hipStream_t s);

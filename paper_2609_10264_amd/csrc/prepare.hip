@@ -446,39 +446,39 @@ size_t prep_ctrl_words(const PrepInputDesc* ins, uint32_t NI, const PrepProbDesc
     return count_words(count_slots(grid > 0x7fffffffu ? 0x7fffffffu : (uint32_t)grid));
 }
 
+static_assert(2 * kMaxPrep <= kMaxSynSets, "one syndrome set per input and per key");
+
+namespace {
+// The syndromes too long for one workgroup: noise of the inputs, then
+// challenges of the keys (one set each).
+uint32_t long_sets(const PrepInputDesc* ins, uint32_t NI, const PrepProbDesc* probs, uint32_t G, SynSet* sets) {
+    uint32_t S = 0;
+    for (uint32_t j = 0; j < NI; ++j)
+        if (ins[j].count && !prep_short((uint64_t)ins[j].cx->k * ins[j].cx->r))
+            sets[S++] = SynSet{ins[j].cx, ins[j].idx, ins[j].val, ins[j].t, ins[j].count, ins[j].Mx};
+    for (uint32_t g = 0; g < G; ++g)
+        if (probs[g].count && !prep_short((uint64_t)probs[g].key->m * probs[g].key->cy.r))
+            sets[S++] = SynSet{&probs[g].key->cy, probs[g].idx, probs[g].val, probs[g].t, probs[g].count, probs[g].R};
+    return S;
+}
+}  // namespace
+
 size_t prep_scratch_bytes(const PrepInputDesc* ins, uint32_t NI, const PrepProbDesc* probs, uint32_t G) {
-    size_t b = 0;
-    for (uint32_t j = 0; j < NI; ++j) {
-        const uint64_t N = (uint64_t)ins[j].cx->k * ins[j].cx->r;
-        if (ins[j].count && !prep_short(N) && syn_scratch_bytes(ins[j].count, N) > b)
-            b = syn_scratch_bytes(ins[j].count, N);
-    }
-    for (uint32_t g = 0; g < G; ++g) {
-        const uint64_t N = (uint64_t)probs[g].key->m * probs[g].key->cy.r;
-        if (probs[g].count && !prep_short(N) && syn_scratch_bytes(probs[g].count, N) > b)
-            b = syn_scratch_bytes(probs[g].count, N);
-    }
-    return b;
+    SynSet sets[2 * kMaxPrep];
+    return syn_sets_scratch_bytes(sets, long_sets(ins, NI, probs, G, sets));
 }
 
 hipError_t launch_client_prepare_multi(const PrepInputDesc* ins, uint32_t NI, const PrepProbDesc* probs, uint32_t G,
                                        uint32_t* scratch, uint32_t* counter, uint32_t* const* done, uint32_t ndone,
                                        uint32_t done_value, hipStream_t s) {
     if (NI > kMaxPrep || G == 0 || G > kMaxPrep || ndone > kMaxPrep) return hipErrorInvalidValue;
-    // syndromes too long for one workgroup run in their own (segmented) launches first
-    for (uint32_t j = 0; j < NI; ++j) {
-        const PrepInputDesc& d = ins[j];
-        if (d.count && !prep_short((uint64_t)d.cx->k * d.cx->r)) {
-            const hipError_t e = launch_syn_sparse(*d.cx, d.idx, d.val, d.t, d.count, nullptr, scratch, d.Mx, s);
-            if (e != hipSuccess) return e;
-        }
-    }
-    for (uint32_t g = 0; g < G; ++g) {
-        const PrepProbDesc& d = probs[g];
-        if (d.count && !prep_short((uint64_t)d.key->m * d.key->cy.r)) {
-            const hipError_t e = launch_syn_sparse(d.key->cy, d.idx, d.val, d.t, d.count, nullptr, scratch, d.R, s);
-            if (e != hipSuccess) return e;
-        }
+    // syndromes too long for one workgroup run first, all of them in one
+    // sequence of segmented launches
+    SynSet sets[2 * kMaxPrep];
+    const uint32_t S = long_sets(ins, NI, probs, G, sets);
+    if (S) {
+        const hipError_t e = launch_syn_sets(sets, S, scratch, s);
+        if (e != hipSuccess) return e;
     }
     PrepPlan pl = prep_plan(ins, NI, probs, G);
     if (pl.grid == 0) return hipSuccess;

@@ -316,23 +316,50 @@ __device__ __forceinline__ void seg_suffix_scan(uint32_t (&x)[kSegPer], uint32_t
     for (int e = 0; e < kSegPer; ++e) x[e] = fadd(x[e], off);
 }
 
+// Several syndromes of long blocks share each of the three launches: set i is
+// count vectors over its own code, with its own work region (count x 2N words
+// and the look-back state).  grid.y runs over the vectors of all sets, grid.x
+// over the segments (p1, p2) or the fold chunks (p3) of the longest; the
+// workgroups past a shorter set's end return at once (before p2's ticket).
+struct SegSet {
+    const uint32_t *pi1, *pi2, *v1, *v2;
+    const uint32_t *vin, *idx, *val, *X;
+    uint32_t* out;
+    uint32_t* work;
+    uint32_t k, r, t, count;
+};
+struct SegArgs {
+    uint32_t S;
+    uint32_t vend[kMaxSynSets];  // vectors of sets < i + 1
+    SegSet set[kMaxSynSets];
+};
+
+// The set of global vector vy (grid.y) and the vector's index within it.
+__device__ __forceinline__ const SegSet& seg_set(const SegArgs& a, uint32_t vy, uint32_t* c) {
+    uint32_t i = 0;
+    while (vy >= a.vend[i]) ++i;
+    *c = vy - (i ? a.vend[i - 1] : 0u);
+    return a.set[i];
+}
+
 template <bool SPARSE>
-__global__ __launch_bounds__(kSegThreads) void syn_p1(uint32_t k, uint32_t r, const uint32_t* __restrict__ pi2,
-                                                      const uint32_t* __restrict__ v2,
-                                                      const uint32_t* __restrict__ vin,
-                                                      const uint32_t* __restrict__ idx,
-                                                      const uint32_t* __restrict__ val, uint32_t t,
-                                                      uint32_t* __restrict__ scratch) {
+__global__ __launch_bounds__(kSegThreads) void syn_p1(const SegArgs a) {
     __shared__ uint32_t seg[kSegLen];
     __shared__ uint64_t red[4];
     __shared__ uint32_t wsum[4];
-    const uint32_t c = blockIdx.y, N = k * r;
+    uint32_t c;
+    const SegSet& S = seg_set(a, blockIdx.y, &c);
+    const uint32_t N = S.k * S.r, nseg = (N + kSegLen - 1) / kSegLen;
+    if (blockIdx.x >= nseg) return;
     const uint32_t j0 = blockIdx.x * kSegLen, j1 = (j0 + kSegLen < N) ? j0 + kSegLen : N;
     const int tid = threadIdx.x;
-    uint32_t* bbuf = scratch + (size_t)c * 2 * N;
+    const uint32_t t = S.t;
+    const uint32_t* __restrict__ idx = S.idx;
+    const uint32_t* __restrict__ val = S.val;
+    uint32_t* bbuf = S.work + (size_t)c * 2 * N;
     if (tid == 0) {
         // p2's look-back state: this segment's status word, and (segment 0) the ticket
-        unsigned long long* st = look_state(scratch, gridDim.y, N, c);
+        unsigned long long* st = look_state(S.work, S.count, N, c);
         st[1 + blockIdx.x] = 0ull;
         if (blockIdx.x == 0) st[0] = 0ull;
     }
@@ -342,8 +369,8 @@ __global__ __launch_bounds__(kSegThreads) void syn_p1(uint32_t k, uint32_t r, co
     for (int e = 0; e < kSegPer; ++e) {
         const uint32_t j = j0 + tid * kSegPer + e;
         const uint32_t js = j < j1 ? j : j0;
-        p2[e] = pi2[js];
-        w2[e] = v2[js];
+        p2[e] = S.pi2[js];
+        w2[e] = S.v2[js];
     }
     uint64_t part = 0;
     if (SPARSE) {
@@ -352,7 +379,7 @@ __global__ __launch_bounds__(kSegThreads) void syn_p1(uint32_t k, uint32_t r, co
             if (j >= j1 && j < N) part += val[(size_t)c * t + q];
         }
     } else {
-        const uint32_t* src = vin + (size_t)c * N;
+        const uint32_t* src = S.vin + (size_t)c * N;
         for (uint32_t j = j1 + tid; j < N; j += kSegThreads) part += src[j];
     }
     const uint32_t carry = fred64(block_sum_u64_256(part, red));
@@ -372,7 +399,7 @@ __global__ __launch_bounds__(kSegThreads) void syn_p1(uint32_t k, uint32_t r, co
 #pragma unroll
         for (int e = 0; e < kSegPer; ++e) {
             const uint32_t j = j0 + tid * kSegPer + e;
-            x[e] = j < j1 ? vin[(size_t)c * N + j] : 0u;
+            x[e] = j < j1 ? S.vin[(size_t)c * N + j] : 0u;
         }
     }
     seg_suffix_scan(x, carry, wsum);  // A
@@ -383,14 +410,16 @@ __global__ __launch_bounds__(kSegThreads) void syn_p1(uint32_t k, uint32_t r, co
     }
 }
 
-__global__ __launch_bounds__(kSegThreads) void syn_p2(uint32_t k, uint32_t r, const uint32_t* __restrict__ pi1,
-                                                      const uint32_t* __restrict__ v1, uint32_t* __restrict__ scratch) {
+__global__ __launch_bounds__(kSegThreads) void syn_p2(const SegArgs a) {
     __shared__ uint64_t red[4];
     __shared__ uint32_t wsum[4];
     __shared__ uint32_t sh_seg, sh_carry;
-    const uint32_t c = blockIdx.y, N = k * r, nseg = (N + kSegLen - 1) / kSegLen;
+    uint32_t c;
+    const SegSet& S = seg_set(a, blockIdx.y, &c);
+    const uint32_t N = S.k * S.r, nseg = (N + kSegLen - 1) / kSegLen;
+    if (blockIdx.x >= nseg) return;  // (uniform: no ticket taken)
     const int tid = threadIdx.x, lane = tid & 63;
-    unsigned long long* st = look_state(scratch, gridDim.y, N, c);
+    unsigned long long* st = look_state(S.work, S.count, N, c);
     if (tid == 0) {
         const uint32_t ticket = atomicAdd(reinterpret_cast<uint32_t*>(st), 1u);  // < nseg: one per workgroup
         sh_seg = ticket < nseg ? nseg - 1 - ticket : 0u;
@@ -398,15 +427,15 @@ __global__ __launch_bounds__(kSegThreads) void syn_p2(uint32_t k, uint32_t r, co
     __syncthreads();
     const uint32_t sg = sh_seg;
     const uint32_t j0 = sg * kSegLen, j1 = (j0 + kSegLen < N) ? j0 + kSegLen : N;
-    const uint32_t* bbuf = scratch + (size_t)c * 2 * N;
-    uint32_t* dbuf = scratch + (size_t)c * 2 * N + N;
+    const uint32_t* bbuf = S.work + (size_t)c * 2 * N;
+    uint32_t* dbuf = S.work + (size_t)c * 2 * N + N;
     uint32_t p1[kSegPer], w1[kSegPer], x[kSegPer];
 #pragma unroll
     for (int e = 0; e < kSegPer; ++e) {
         const uint32_t j = j0 + tid * kSegPer + e;
         const uint32_t js = j < j1 ? j : j0;
-        p1[e] = pi1[js];
-        w1[e] = v1[js];
+        p1[e] = S.pi1[js];
+        w1[e] = S.v1[js];
         const uint32_t b = bbuf[js];
         x[e] = j < j1 ? b : 0u;
     }
@@ -444,16 +473,41 @@ __global__ __launch_bounds__(kSegThreads) void syn_p2(uint32_t k, uint32_t r, co
     }
 }
 
-__global__ __launch_bounds__(256) void syn_p3(uint32_t k, uint32_t r, const uint32_t* __restrict__ scratch,
-                                              const uint32_t* __restrict__ X, uint32_t* __restrict__ out) {
-    const uint32_t c = blockIdx.y, N = k * r;
+__global__ __launch_bounds__(256) void syn_p3(const SegArgs a) {
+    uint32_t c;
+    const SegSet& S = seg_set(a, blockIdx.y, &c);
+    const uint32_t N = S.k * S.r;
     const uint32_t i = blockIdx.x * 256 + threadIdx.x;
-    if (i >= k) return;
-    const uint32_t* dbuf = scratch + (size_t)c * 2 * N + N;
+    if (i >= S.k) return;
+    const uint32_t* dbuf = S.work + (size_t)c * 2 * N + N;
     uint32_t s = 0;
-    for (uint32_t q = 0; q < r; ++q) s = fadd(s, dbuf[(size_t)i * r + q]);  // R: fold blocks of r
-    if (X) s = fadd(X[(size_t)c * k + i], s);
-    out[(size_t)c * k + i] = s;
+    for (uint32_t q = 0; q < S.r; ++q) s = fadd(s, dbuf[(size_t)i * S.r + q]);  // R: fold blocks of r
+    if (S.X) s = fadd(S.X[(size_t)c * S.k + i], s);
+    S.out[(size_t)c * S.k + i] = s;
+}
+
+// The three launches over sets of one input kind (sparse or dense).
+template <bool SPARSE>
+hipError_t launch_seg_sets(const SegArgs& a, hipStream_t s) {
+    uint32_t maxseg = 0, maxk = 0;
+    for (uint32_t i = 0; i < a.S; ++i) {
+        const size_t N = (size_t)a.set[i].k * a.set[i].r;
+        const uint32_t nseg = (uint32_t)((N + kSegLen - 1) / kSegLen);
+        maxseg = nseg > maxseg ? nseg : maxseg;
+        maxk = a.set[i].k > maxk ? a.set[i].k : maxk;
+    }
+    const uint32_t nv = a.S ? a.vend[a.S - 1] : 0u;
+    if (nv == 0) return hipSuccess;
+    if (nv > 65535u) return hipErrorInvalidValue;
+    const dim3 gseg(maxseg, nv);
+    hipLaunchKernelGGL((syn_p1<SPARSE>), gseg, dim3(kSegThreads), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(syn_p2, gseg, dim3(kSegThreads), 0, s, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(syn_p3, dim3(ceil_div(maxk, 256u), nv), dim3(256), 0, s, a);
+    return hipGetLastError();
 }
 
 template <bool SPARSE>
@@ -475,16 +529,11 @@ hipError_t launch_syn(const mvk_code& c, const uint32_t* v, const uint32_t* idx,
 #undef MVK_SYN
         return hipGetLastError();
     }
-    const dim3 gseg((uint32_t)((N + kSegLen - 1) / kSegLen), count);
-    hipLaunchKernelGGL((syn_p1<SPARSE>), gseg, dim3(kSegThreads), 0, s, c.k, c.r, c.pi2, c.v2, v, idx, val, t,
-                       scratch);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(syn_p2, gseg, dim3(kSegThreads), 0, s, c.k, c.r, c.pi1, c.v1, scratch);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(syn_p3, dim3(ceil_div(c.k, 256), count), dim3(256), 0, s, c.k, c.r, scratch, X, out);
-    return hipGetLastError();
+    SegArgs a{};
+    a.S = 1;
+    a.vend[0] = count;
+    a.set[0] = SegSet{c.pi1, c.pi2, c.v1, c.v2, v, idx, val, X, out, scratch, c.k, c.r, t, count};
+    return launch_seg_sets<SPARSE>(a, s);
 }
 
 __global__ __launch_bounds__(256) void transpose_i8(const int8_t* __restrict__ W, uint32_t m, uint32_t n,
@@ -523,6 +572,31 @@ hipError_t launch_encT_u32(const mvk_code& c, const uint32_t* in, size_t ld_in, 
 hipError_t launch_encT_i8(const mvk_code& c, const int8_t* in, size_t ld_in, size_t vs_in, uint32_t nvec,
                           uint32_t* t3, uint32_t* seg, uint32_t* out, size_t ld_out, size_t vs_out, hipStream_t s) {
     return launch_encT<int8_t>(c, in, ld_in, vs_in, nvec, t3, seg, out, ld_out, vs_out, s);
+}
+
+size_t syn_sets_scratch_bytes(const SynSet* sets, uint32_t S) {
+    size_t b = 0;
+    for (uint32_t i = 0; i < S; ++i) b += (syn_scratch_bytes(sets[i].count, (size_t)sets[i].c->k * sets[i].c->r) + 255) & ~(size_t)255;
+    return b;
+}
+
+hipError_t launch_syn_sets(const SynSet* sets, uint32_t S, uint32_t* scratch, hipStream_t s) {
+    if (S > kMaxSynSets) return hipErrorInvalidValue;
+    SegArgs a{};
+    uint32_t nv = 0;
+    char* w = reinterpret_cast<char*>(scratch);
+    for (uint32_t i = 0; i < S; ++i) {
+        const SynSet& d = sets[i];
+        const size_t N = (size_t)d.c->k * d.c->r;
+        if (N <= kSynScratchAbove) return hipErrorInvalidValue;  // long blocks only
+        if (d.count == 0) continue;
+        a.set[a.S] = SegSet{d.c->pi1, d.c->pi2, d.c->v1, d.c->v2, nullptr, d.idx, d.val, nullptr, d.out,
+                            reinterpret_cast<uint32_t*>(w), d.c->k, d.c->r, d.t, d.count};
+        nv += d.count;
+        a.vend[a.S++] = nv;
+        w += (syn_scratch_bytes(d.count, N) + 255) & ~(size_t)255;
+    }
+    return launch_seg_sets<true>(a, s);
 }
 
 hipError_t launch_syn_dense(const mvk_code& c, const uint32_t* v, uint32_t count, uint32_t* scratch, uint32_t* out,

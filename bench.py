@@ -656,8 +656,8 @@ def stack_bench(args, steps, warmup, cpu_seconds):
     def prep_pass(k):
         for L in range(layers):
             _, ex, ey = inputs[L]
-            if npre == 1:  # the whole layer in one call
-                stack.prepare_layer(built[L], ex, ey, flags[L], out=preps[L], stream=s_preps[0])
+            if npre == 1:  # the whole layer in one call, one flag
+                stack.prepare_layer(built[L], ex, ey, flags[L, 0], out=preps[L], stream=s_preps[0])
                 continue
             for i, grp in enumerate(stack.INPUTS):
                 if i % npre == k:
@@ -667,7 +667,8 @@ def stack_bench(args, steps, warmup, cpu_seconds):
         presults.clear()
         for L in range(layers):
             presults.append(stack.run_layer_prepared(built[L], inputs[L][0], preps[L],
-                                                     ready_flag=[flags[L, i] for i in range(nin)],
+                                                     ready_flag=flags[L, 0] if npre == 1 else
+                                                     [flags[L, i] for i in range(nin)],
                                                      timeout_us=200_000, timed_out=late, tamper=tamperer(L),
                                                      stream=s_on))
 

@@ -554,17 +554,14 @@ mvk_status mvk_client_prepare(const mvk_key* key, const mvk_sparse* ex, const mv
     }
     hipStream_t s = (hipStream_t)stream;
     if (nx == 0 && ny == 0) return done_flag ? hip_status(launch_flag_signal(done_flag, done_value, s)) : MVK_OK;
-    const size_t Nx = (size_t)key->cx.r * key->n, Ny = (size_t)key->cy.r * key->m;
-    size_t scratch = 0;
-    if (nx) scratch = syn_scratch_bytes(nx, Nx);
-    if (ny && syn_scratch_bytes(ny, Ny) > scratch) scratch = syn_scratch_bytes(ny, Ny);
+    const size_t scratch = prep_scratch_bytes(&key, 1, nx, ny);
     void* ws = nullptr;
     uint32_t* ctrl = nullptr;
     st = workspace(s, scratch, &ws, &ctrl, 4 * (kPrepCounterWord + prep_ctrl_words(*key, nx, ny)));
     if (st) return st;
     return hip_status(launch_client_prepare(*key, nx ? ex->idx : nullptr, nx ? ex->val : nullptr, nx ? ex->t : 0u,
                                             nx, ny ? ey->idx : nullptr, ny ? ey->val : nullptr, ny ? ey->t : 0u, ny,
-                                            Mx, My, R, U, (uint32_t*)ws, &ctrl[kPrepCounterWord], done_flag,
+                                            Mx, My, R, U, (uint32_t*)ws, scratch, &ctrl[kPrepCounterWord], done_flag,
                                             done_value, s));
 }
 
@@ -615,17 +612,15 @@ mvk_status mvk_client_prepare_group(uint32_t G, const mvk_key* const* keys, cons
     }
     hipStream_t s = (hipStream_t)stream;
     if (nx == 0 && ny == 0) return done_flag ? hip_status(launch_flag_signal(done_flag, done_value, s)) : MVK_OK;
-    const size_t Nx = (size_t)key.cx.r * key.n, Ny = (size_t)key.cy.r * key.m;
-    size_t scratch = 0;
-    if (nx) scratch = syn_scratch_bytes(nx, Nx);
-    if (ny && syn_scratch_bytes(ny, Ny) > scratch) scratch = syn_scratch_bytes(ny, Ny);
+    const size_t scratch = prep_scratch_bytes(keys, G, nx, ny);
     void* ws = nullptr;
     uint32_t* ctrl = nullptr;
     mvk_status st = workspace(s, scratch, &ws, &ctrl, 4 * (kPrepCounterWord + prep_ctrl_words(keys, G, nx, ny)));
     if (st) return st;
     return hip_status(launch_client_prepare_group(G, keys, nx ? ex->idx : nullptr, nx ? ex->val : nullptr,
                                                   nx ? ex->t : 0u, nx, eyi, eyv, ty, ny, Mx, My, R, U,
-                                                  (uint32_t*)ws, &ctrl[kPrepCounterWord], done_flag, done_value, s));
+                                                  (uint32_t*)ws, scratch, &ctrl[kPrepCounterWord], done_flag,
+                                                  done_value, s));
 }
 
 mvk_status mvk_client_prepare_multi(uint32_t G, const mvk_key* const* keys, const mvk_sparse* const* ex,
@@ -689,10 +684,10 @@ mvk_status mvk_client_prepare_multi(uint32_t G, const mvk_key* const* keys, cons
     }
     void* ws = nullptr;
     uint32_t* ctrl = nullptr;
-    const mvk_status st = workspace(s, prep_scratch_bytes(ins, NI, probs, G), &ws, &ctrl,
-                                    4 * (kPrepCounterWord + prep_ctrl_words(ins, NI, probs, G)));
+    const size_t scratch = prep_scratch_bytes(ins, NI, probs, G);
+    const mvk_status st = workspace(s, scratch, &ws, &ctrl, 4 * (kPrepCounterWord + prep_ctrl_words(ins, NI, probs, G)));
     if (st) return st;
-    return hip_status(launch_client_prepare_multi(ins, NI, probs, G, (uint32_t*)ws, &ctrl[kPrepCounterWord],
+    return hip_status(launch_client_prepare_multi(ins, NI, probs, G, (uint32_t*)ws, scratch, &ctrl[kPrepCounterWord],
                                                   nflags ? flags : nullptr, nflags, done_value, s));
 }
 

@@ -709,6 +709,92 @@ __global__ __launch_bounds__(kWideThreads) void decode_verify_wide(
     finish(B, ell, nsub, accL, accR, ctrl, slots, nullptr, nullptr, grp.vL[g], grp.vR[g], grp.accept[g], &last);
 }
 
+// decode_verify_masked with one workgroup per query column (and problem of
+// the group: grid B x G): 1024 threads take the elements j = t + 1024 u of
+// their column, as outputs i (Y_b[i] = Yhat_b[i] - My_b[i] and the v_R terms
+// R_q[i] Yhat_b[i]) and as inputs k (the v_L terms U_q[k] Xhat_b[k]), PER
+// per pass with all of a pass's loads issued before the first is used
+// (addresses clamped in range, terms masked); the 2 ell sums are reduced
+// across the wave and through LDS, and the workgroup writes v_L, v_R and
+// accept of its column itself: no atomics and no completion count.  ell <= EL.
+template <int EL, int PER>
+__global__ __launch_bounds__(kSmallThreads) void decode_verify_col(uint32_t m, uint32_t n,
+                                                                   const uint32_t* __restrict__ Xhat, uint32_t B,
+                                                                   uint32_t ell, const DvGroup grp) {
+    constexpr int NW = kSmallThreads / 64;
+    __shared__ uint64_t red[NW][2 * EL];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const uint32_t b = blockIdx.x, g = blockIdx.y;
+    const uint32_t* __restrict__ Yhat = grp.Yhat[g] + (size_t)b * m;
+    const uint32_t* __restrict__ My = grp.My[g] + (size_t)b * m;
+    const uint32_t* __restrict__ R = grp.R[g];
+    const uint32_t* __restrict__ U = grp.U[g];
+    const uint32_t* __restrict__ xh = Xhat + (size_t)b * n;
+    uint32_t* __restrict__ Y = grp.Y[g] + (size_t)b * m;
+    const uint32_t len = m > n ? m : n;
+    constexpr uint32_t pass = kSmallThreads * PER;
+    uint64_t l[EL], rr[EL];
+#pragma unroll
+    for (int q = 0; q < EL; ++q) l[q] = rr[q] = 0;
+    for (uint32_t base = 0; base < len; base += pass) {
+        uint32_t yv[PER], mv[PER], xv[PER], rv[EL][PER], uv[EL][PER];
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+            const uint32_t j = base + (uint32_t)tid + kSmallThreads * u;
+            const uint32_t i = j < m ? j : m - 1, k = j < n ? j : n - 1;
+            yv[u] = Yhat[i];
+            mv[u] = My[i];
+            xv[u] = xh[k];
+#pragma unroll
+            for (int q = 0; q < EL; ++q) {
+                const uint32_t qs = (uint32_t)q < ell ? (uint32_t)q : 0u;
+                rv[q][u] = R[(size_t)qs * m + i];
+                uv[q][u] = U[(size_t)qs * n + k];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+            const uint32_t j = base + (uint32_t)tid + kSmallThreads * u;
+            // pinned before the guarded store (see decode_verify_small)
+            uint32_t yo = fsub(yv[u], mv[u]);
+            asm volatile("" : "+v"(yo));
+            if (j < m) Y[j] = yo;
+            const uint32_t y = j < m ? yv[u] : 0u, x = j < n ? xv[u] : 0u;
+#pragma unroll
+            for (int q = 0; q < EL; ++q) {
+                rr[q] += ffold((uint64_t)rv[q][u] * y);
+                l[q] += ffold((uint64_t)uv[q][u] * x);
+            }
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < EL; ++q) {
+        const uint64_t sl = wave_sum_u64(fred64(l[q])), sr = wave_sum_u64(fred64(rr[q]));
+        if (lane == 0) {
+            red[wave][2 * q] = sl;
+            red[wave][2 * q + 1] = sr;
+        }
+    }
+    __syncthreads();
+    if (tid < 64) {
+        // lane 2q: v_L of repetition q, lane 2q + 1: v_R
+        uint64_t tot = 0;
+        if (tid < 2 * EL)
+#pragma unroll
+            for (int w = 0; w < NW; ++w) tot += red[w][tid];
+        const uint32_t v = fred64(tot);
+        const uint32_t other = (uint32_t)__shfl_xor((int)v, 1);
+        const uint32_t q = (uint32_t)tid >> 1;
+        const bool mine = q < ell && tid < 2 * EL;
+        if (mine && (tid & 1) == 0 && grp.vL[g]) grp.vL[g][(size_t)q * B + b] = v;
+        if (mine && (tid & 1) == 1 && grp.vR[g]) grp.vR[g][(size_t)q * B + b] = v;
+        // accept: every repetition's v_L equals its v_R
+        const bool bad = mine && (tid & 1) == 0 && v != other;
+        const bool any_bad = __ballot(bad) != 0;
+        if (tid == 0) grp.accept[g][b] = any_bad ? 0u : 1u;
+    }
+}
+
 template <int U, int E>
 int fused_blocks_per_cu() {
     int nb = 0;
@@ -868,6 +954,25 @@ bool takes_small(uint32_t m, uint32_t n, uint32_t B, uint32_t ell) {
     return (uint64_t)B * ((uint64_t)m + n) <= kSmallDvWords && ell <= 4;
 }
 
+// One workgroup per column (decode_verify_col) from kColsMinB columns up to
+// kColsMaxLen elements per column, ell <= 4: every column's sums stay in its
+// workgroup.
+constexpr uint32_t kColsMinB = 2, kColsMaxLen = 65536, kColsMaxB = 65535;
+bool takes_cols(uint32_t m, uint32_t n, uint32_t B, uint32_t ell) {
+    const uint32_t len = m > n ? m : n;
+    return ell <= 4 && B >= kColsMinB && B <= kColsMaxB && len <= kColsMaxLen && !takes_small(m, n, B, ell);
+}
+
+hipError_t launch_cols(uint32_t m, uint32_t n, const uint32_t* Xhat, uint32_t B, uint32_t ell, const DvGroup& grp,
+                       uint32_t G, hipStream_t s) {
+    const dim3 grid(B, G);
+    if (ell <= 2)
+        hipLaunchKernelGGL((decode_verify_col<2, 4>), grid, dim3(kSmallThreads), 0, s, m, n, Xhat, B, ell, grp);
+    else
+        hipLaunchKernelGGL((decode_verify_col<4, 4>), grid, dim3(kSmallThreads), 0, s, m, n, Xhat, B, ell, grp);
+    return hipGetLastError();
+}
+
 // decode_verify_wide over G problems (grid.y = G); each control region as
 // dv_layout(m, n, B, ell), ctrl_stride words apart.
 hipError_t launch_wide(uint32_t m, uint32_t n, const uint32_t* Xhat, uint32_t B, uint32_t ell, const DvGroup& grp,
@@ -899,6 +1004,18 @@ hipError_t launch_decode_verify_masked(uint32_t m, uint32_t n, const uint32_t* X
     const DvLayout l = dv_layout(m, n, B, ell);
     unsigned long long* acc = reinterpret_cast<unsigned long long*>(ctrl + l.acc_word);
     uint32_t* counter = ctrl;
+    if (takes_cols(m, n, B, ell)) {
+        DvGroup grp{};
+        grp.Yhat[0] = Yhat;
+        grp.My[0] = My;
+        grp.R[0] = r;
+        grp.U[0] = U;
+        grp.Y[0] = Y;
+        grp.vL[0] = vL;
+        grp.vR[0] = vR;
+        grp.accept[0] = accept;
+        return launch_cols(m, n, Xhat, B, ell, grp, 1, s);
+    }
     if (takes_small(m, n, B, ell)) {
         // four elements per thread, one pass per column: a single workgroup up
         // to 4096 elements (no accumulators or counter), else up to 8.  (One
@@ -945,6 +1062,20 @@ hipError_t launch_decode_verify_masked_group(uint32_t G, uint32_t m, uint32_t n,
                                              uint32_t* ctrl, hipStream_t s) {
     if (G == 0 || G > kMaxGroup || ell == 0 || ell > (uint32_t)kMaxEll) return hipErrorInvalidValue;
     const size_t stride = dv_group_ctrl_stride(m, n, B, ell);
+    if (takes_cols(m, n, B, ell)) {
+        DvGroup grp{};
+        for (uint32_t g = 0; g < G; ++g) {
+            grp.Yhat[g] = Yhat[g];
+            grp.My[g] = My[g];
+            grp.R[g] = R[g];
+            grp.U[g] = U[g];
+            grp.Y[g] = Y[g];
+            grp.vL[g] = vL ? vL[g] : nullptr;
+            grp.vR[g] = vR ? vR[g] : nullptr;
+            grp.accept[g] = accept[g];
+        }
+        return launch_cols(m, n, Xhat, B, ell, grp, G, s);
+    }
     if (!takes_small(m, n, B, ell) && ell <= 4) {
         DvGroup grp{};
         for (uint32_t g = 0; g < G; ++g) {

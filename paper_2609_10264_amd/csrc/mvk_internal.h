@@ -67,8 +67,9 @@ hipError_t launch_syn_sparse(const mvk_code& c, const uint32_t* idx, const uint3
                              hipStream_t s);
 // Sparse syndromes of long blocks (N > kSynScratchAbove) of several codes in
 // one sequence of three launches: set i is `count` vectors (idx/val: count x
-// t) over code *c, results into out (count x c->k).  scratch:
-// syn_sets_scratch_bytes(sets, S), 256-byte aligned.
+// t) over code *c, results into out (count x c->k).  scratch: scratch_bytes
+// of at least syn_sets_scratch_bytes(sets, S), 256-byte aligned (else
+// hipErrorInvalidValue and nothing is launched).
 struct SynSet {
     const mvk_code* c;
     const uint32_t *idx, *val;
@@ -77,7 +78,7 @@ struct SynSet {
 };
 constexpr uint32_t kMaxSynSets = 16;
 size_t syn_sets_scratch_bytes(const SynSet* sets, uint32_t S);
-hipError_t launch_syn_sets(const SynSet* sets, uint32_t S, uint32_t* scratch, hipStream_t s);
+hipError_t launch_syn_sets(const SynSet* sets, uint32_t S, uint32_t* scratch, size_t scratch_bytes, hipStream_t s);
 // W (m x n int8) -> WT (n x m int8)
 hipError_t launch_transpose_i8(const int8_t* W, uint32_t m, uint32_t n, int8_t* WT, hipStream_t s);
 hipError_t launch_fill_u32(uint32_t* p, size_t count, uint32_t value, hipStream_t s);
@@ -138,8 +139,8 @@ hipError_t launch_decode_verify_masked_group(uint32_t G, uint32_t m, uint32_t n,
 
 // prepare.hip ---------------------------------------------------------------
 // Mx, My for nx noise vectors and R, U for ny challenges (either count may
-// be 0).  scratch: max(nx * 2 * Nx, ny * 2 * Ny) words when that block length
-// is above kSynScratchAbove, else unused.  done (may be null): set to
+// be 0).  scratch: scratch_bytes of at least prep_scratch_bytes (the work
+// regions of the syndromes longer than kSynScratchAbove, one after another).  done (may be null): set to
 // done_value once every output is stored and visible device-wide; counter:
 // prep_ctrl_words(key, nx, ny) words of completion counters (count.h), zero
 // before the launch (left zero).
@@ -169,9 +170,11 @@ struct PrepProbDesc {
 };
 size_t prep_ctrl_words(const PrepInputDesc* ins, uint32_t NI, const PrepProbDesc* probs, uint32_t G);
 size_t prep_scratch_bytes(const PrepInputDesc* ins, uint32_t NI, const PrepProbDesc* probs, uint32_t G);
+// the same for G keys sharing one input of nx noise vectors, ny challenges each
+size_t prep_scratch_bytes(const mvk_key* const* keys, uint32_t G, uint32_t nx, uint32_t ny);
 hipError_t launch_client_prepare_multi(const PrepInputDesc* ins, uint32_t NI, const PrepProbDesc* probs, uint32_t G,
-                                       uint32_t* scratch, uint32_t* counter, uint32_t* const* done, uint32_t ndone,
-                                       uint32_t done_value, hipStream_t s);
+                                       uint32_t* scratch, size_t scratch_bytes, uint32_t* counter,
+                                       uint32_t* const* done, uint32_t ndone, uint32_t done_value, hipStream_t s);
 size_t prep_ctrl_words(const mvk_key* const* keys, uint32_t G, uint32_t nx, uint32_t ny);
 // The same for G <= kMaxGroup keys of one shape and one privacy code that share
 // the noise vectors (Mx once; My[g], R[g], Uq[g] per key, with the challenges
@@ -180,13 +183,13 @@ hipError_t launch_client_prepare_group(uint32_t G, const mvk_key* const* keys, c
                                        const uint32_t* ex_val, uint32_t tx, uint32_t nx,
                                        const uint32_t* const* ey_idx, const uint32_t* const* ey_val, uint32_t ty,
                                        uint32_t ny, uint32_t* Mx, uint32_t* const* My, uint32_t* const* R,
-                                       uint32_t* const* Uq, uint32_t* scratch, uint32_t* counter, uint32_t* done,
-                                       uint32_t done_value, hipStream_t s);
+                                       uint32_t* const* Uq, uint32_t* scratch, size_t scratch_bytes,
+                                       uint32_t* counter, uint32_t* done, uint32_t done_value, hipStream_t s);
 hipError_t launch_client_prepare(const mvk_key& key, const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx,
                                  uint32_t nx, const uint32_t* ey_idx, const uint32_t* ey_val, uint32_t ty,
                                  uint32_t ny, uint32_t* Mx, uint32_t* My, uint32_t* R, uint32_t* Uq,
-                                 uint32_t* scratch, uint32_t* counter, uint32_t* done, uint32_t done_value,
-                                 hipStream_t s);
+                                 uint32_t* scratch, size_t scratch_bytes, uint32_t* counter, uint32_t* done,
+                                 uint32_t done_value, hipStream_t s);
 // Xhat = X + Mx; with a flag, after waiting for *flag == value (which the
 // launch then clears; counter as above).
 hipError_t launch_add_masks(const uint32_t* X, const uint32_t* Mx, size_t count, uint32_t* Xhat, uint32_t* flag,

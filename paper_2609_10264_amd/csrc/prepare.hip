@@ -469,15 +469,15 @@ size_t prep_scratch_bytes(const PrepInputDesc* ins, uint32_t NI, const PrepProbD
 }
 
 hipError_t launch_client_prepare_multi(const PrepInputDesc* ins, uint32_t NI, const PrepProbDesc* probs, uint32_t G,
-                                       uint32_t* scratch, uint32_t* counter, uint32_t* const* done, uint32_t ndone,
-                                       uint32_t done_value, hipStream_t s) {
+                                       uint32_t* scratch, size_t scratch_bytes, uint32_t* counter,
+                                       uint32_t* const* done, uint32_t ndone, uint32_t done_value, hipStream_t s) {
     if (NI > kMaxPrep || G == 0 || G > kMaxPrep || ndone > kMaxPrep) return hipErrorInvalidValue;
     // syndromes too long for one workgroup run first, all of them in one
     // sequence of segmented launches
     SynSet sets[2 * kMaxPrep];
     const uint32_t S = long_sets(ins, NI, probs, G, sets);
     if (S) {
-        const hipError_t e = launch_syn_sets(sets, S, scratch, s);
+        const hipError_t e = launch_syn_sets(sets, S, scratch, scratch_bytes, s);
         if (e != hipSuccess) return e;
     }
     PrepPlan pl = prep_plan(ins, NI, probs, G);
@@ -521,8 +521,10 @@ void group_descs(uint32_t G, const mvk_key* const* keys, const uint32_t* ex_idx,
                  PrepInputDesc* in, PrepProbDesc* probs) {
     *in = PrepInputDesc{&keys[0]->cx, ex_idx, ex_val, tx, nx, Mx};
     for (uint32_t g = 0; g < G; ++g)
-        probs[g] = PrepProbDesc{keys[g], 0u, ny ? ey_idx[g] : nullptr, ny ? ey_val[g] : nullptr, ty, ny,
-                                nx && My ? My[g] : nullptr, ny && R ? R[g] : nullptr, ny && Uq ? Uq[g] : nullptr};
+        // (the size queries pass no arrays: every array is read only where it exists)
+        probs[g] = PrepProbDesc{keys[g], 0u, ny && ey_idx ? ey_idx[g] : nullptr, ny && ey_val ? ey_val[g] : nullptr,
+                                ty, ny, nx && My ? My[g] : nullptr, ny && R ? R[g] : nullptr,
+                                ny && Uq ? Uq[g] : nullptr};
 }
 }  // namespace
 
@@ -535,6 +537,15 @@ size_t prep_ctrl_words(const mvk_key* const* keys, uint32_t G, uint32_t nx, uint
     return prep_ctrl_words(&in, 1, probs, G);
 }
 
+size_t prep_scratch_bytes(const mvk_key* const* keys, uint32_t G, uint32_t nx, uint32_t ny) {
+    if (G == 0 || G > kMaxPrep) return 0;
+    PrepInputDesc in;
+    PrepProbDesc probs[kMaxPrep];
+    group_descs(G, keys, nullptr, nullptr, 0u, nx, nullptr, nullptr, 0u, ny, nullptr, nullptr, nullptr, nullptr, &in,
+                probs);
+    return prep_scratch_bytes(&in, 1, probs, G);
+}
+
 size_t prep_ctrl_words(const mvk_key& key, uint32_t nx, uint32_t ny) {
     const mvk_key* k = &key;
     return prep_ctrl_words(&k, 1, nx, ny);
@@ -544,24 +555,24 @@ hipError_t launch_client_prepare_group(uint32_t G, const mvk_key* const* keys, c
                                        const uint32_t* ex_val, uint32_t tx, uint32_t nx,
                                        const uint32_t* const* ey_idx, const uint32_t* const* ey_val, uint32_t ty,
                                        uint32_t ny, uint32_t* Mx, uint32_t* const* My, uint32_t* const* R,
-                                       uint32_t* const* Uq, uint32_t* scratch, uint32_t* counter, uint32_t* done,
-                                       uint32_t done_value, hipStream_t s) {
+                                       uint32_t* const* Uq, uint32_t* scratch, size_t scratch_bytes,
+                                       uint32_t* counter, uint32_t* done, uint32_t done_value, hipStream_t s) {
     if (G == 0 || G > kMaxGroup) return hipErrorInvalidValue;
     PrepInputDesc in;
     PrepProbDesc probs[kMaxPrep];
     group_descs(G, keys, ex_idx, ex_val, tx, nx, ey_idx, ey_val, ty, ny, Mx, My, R, Uq, &in, probs);
-    return launch_client_prepare_multi(&in, 1, probs, G, scratch, counter, done ? &done : nullptr, done ? 1u : 0u,
-                                       done_value, s);
+    return launch_client_prepare_multi(&in, 1, probs, G, scratch, scratch_bytes, counter, done ? &done : nullptr,
+                                       done ? 1u : 0u, done_value, s);
 }
 
 hipError_t launch_client_prepare(const mvk_key& key, const uint32_t* ex_idx, const uint32_t* ex_val, uint32_t tx,
                                  uint32_t nx, const uint32_t* ey_idx, const uint32_t* ey_val, uint32_t ty,
                                  uint32_t ny, uint32_t* Mx, uint32_t* My, uint32_t* R, uint32_t* Uq,
-                                 uint32_t* scratch, uint32_t* counter, uint32_t* done, uint32_t done_value,
-                                 hipStream_t s) {
+                                 uint32_t* scratch, size_t scratch_bytes, uint32_t* counter, uint32_t* done,
+                                 uint32_t done_value, hipStream_t s) {
     const mvk_key* k = &key;
     return launch_client_prepare_group(1, &k, ex_idx, ex_val, tx, nx, &ey_idx, &ey_val, ty, ny, Mx, &My, &R, &Uq,
-                                       scratch, counter, done, done_value, s);
+                                       scratch, scratch_bytes, counter, done, done_value, s);
 }
 
 hipError_t launch_gather_rows(const uint32_t* M, uint32_t ld, uint32_t nrows, const uint32_t* idx,

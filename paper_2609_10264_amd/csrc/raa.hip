@@ -580,8 +580,10 @@ size_t syn_sets_scratch_bytes(const SynSet* sets, uint32_t S) {
     return b;
 }
 
-hipError_t launch_syn_sets(const SynSet* sets, uint32_t S, uint32_t* scratch, hipStream_t s) {
+hipError_t launch_syn_sets(const SynSet* sets, uint32_t S, uint32_t* scratch, size_t scratch_bytes, hipStream_t s) {
     if (S > kMaxSynSets) return hipErrorInvalidValue;
+    // the sets' work regions lie one after another: the scratch must hold them all
+    if (syn_sets_scratch_bytes(sets, S) > scratch_bytes) return hipErrorInvalidValue;
     SegArgs a{};
     uint32_t nv = 0;
     char* w = reinterpret_cast<char*>(scratch);

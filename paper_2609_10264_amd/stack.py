@@ -148,15 +148,16 @@ def prepare_input(layer: Layer, group: str, ex: dict, ey: dict, preps: dict, fla
                          outs=[preps[nm] for nm in names], done_flag=flag, stream=stream)
 
 
-def prepare_layer(layer: Layer, ex: dict, ey: dict, flags: torch.Tensor | None, out: dict | None = None,
+def prepare_layer(layer: Layer, ex: dict, ey: dict, flag: torch.Tensor | None, out: dict | None = None,
                   stream=None) -> dict:
     """Client preparation of one layer in one call (client_prepare_multi: the
     four inputs' masks and the seven projections' output masks and challenge
     vectors; one launch for the short syndromes and every row gather).
-    flags: one int32 device word per input (or None), each set to 1 once
-    every output of the layer is visible device-wide.  Returns {name: Prepared}."""
+    flag: an int32 device word (or None) set to 1 once every output of the
+    layer is visible device-wide, so one wait (the first masked encode of the
+    layer's online part) covers the whole layer.  Returns {name: Prepared}."""
     preps = out if out is not None else {}
-    keys, exs, eys, outs, done = [], [], [], [], []
+    keys, exs, eys, outs = [], [], [], []
     for name, _, _, group in PROJECTIONS:
         if name not in preps:
             preps[name] = Prepared(layer.keys[name], ex[group][0].shape[0], ey[name][0].shape[0],
@@ -165,7 +166,7 @@ def prepare_layer(layer: Layer, ex: dict, ey: dict, flags: torch.Tensor | None, 
         exs.append(ex[group])
         eys.append(ey[name])
         outs.append(preps[name])
-        done.append(flags[INPUTS.index(group)] if flags is not None else None)
+    done = [flag] + [None] * (len(keys) - 1) if flag is not None else None
     client_prepare_multi(keys, exs, eys, outs=outs, done_flags=done, stream=stream)
     return preps
 

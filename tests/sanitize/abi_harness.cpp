@@ -2,6 +2,7 @@
 // returns before any device work) so that a build with UndefinedBehavior-
 // Sanitizer on the host code sees the size arithmetic of the checks (CPU
 // only; built and run by tests/test_sanitizers.py).
+#include <hip/hip_runtime.h>
 #include <stdint.h>
 #include <stdio.h>
 
@@ -46,6 +47,27 @@ int main() {
     expect(mvk_sample_sparse(1, 4, 5, 0, 0, a, b), MVK_EINVAL, "sample_sparse t > N");
     expect(mvk_sample_code(0xFFFFu, 0xFFFFu, 0, 0, a, a, a, a), MVK_ERANGE, "sample_code N");
     expect(mvk_sample_sparse(2, 8, 3, 0xFFFFFFFFFFFFFFFFull, MVK_TAG_NOISE, a, b), MVK_OK, "sample_sparse");
+    // Preparation calls whose syndrome and counter sizes are computed on the
+    // host before the workspace is requested (with no device, the request then
+    // fails): long challenge blocks (Ny = 18000 > 16384) with 16 challenges,
+    // keys sharing an input, and the multi-input form.  Only where no device
+    // exists: the arrays are not device memory.
+    int ndev = 0;
+    if (hipGetDeviceCount(&ndev) != hipSuccess || ndev == 0) {
+        (void)hipGetLastError();
+        mvk_code cxs = {200, 1, u, u, u, u}, cyl = {6000, 3, u, u, u, u};
+        mvk_key kl = {6000, 200, cxs, cyl, w, w};
+        mvk_sparse ex = {u, u, 5, 1}, ey = {u, u, 31, 16};
+        expect(mvk_client_prepare(&kl, &ex, &ey, w, w, w, w, nullptr, 0, nullptr), MVK_EHIP, "prepare sizes");
+        const mvk_key* ks[2] = {&kl, &kl};
+        const mvk_sparse* eys[2] = {&ey, &ey};
+        uint32_t* outs[2] = {w, w};
+        expect(mvk_client_prepare_group(2, ks, &ex, eys, w, outs, outs, outs, nullptr, 0, nullptr), MVK_EHIP,
+               "prepare_group sizes");
+        const mvk_sparse* exs[2] = {&ex, nullptr};
+        expect(mvk_client_prepare_multi(2, ks, exs, eys, outs, outs, outs, outs, nullptr, 0, nullptr), MVK_EHIP,
+               "prepare_multi sizes");
+    }
     if (pp || st) ++fails;
     printf(fails ? "FAILED %d\n" : "ok\n", fails);
     return fails ? 1 : 0;

@@ -100,19 +100,19 @@ def test_stack_layer_matches_oracle(stack_setup, L):
             Yhat[b, pos] = (Yhat[b, pos].to(torch.int64) + delta) % P
 
     out = stack.run_layer(layer, X, ex, ey, tamper=tamper)
-    # the prepared schedule: preparation stream with flags, then the online part
-    nin = len(stack.INPUTS)
-    flags = torch.zeros(nin, dtype=torch.int32, device="cuda")
+    # the prepared schedule: the layer's preparation on its own stream (one
+    # call, one flag), then the online part, whose first masked encode waits
+    flag = torch.zeros((), dtype=torch.int32, device="cuda")
     late = torch.zeros((), dtype=torch.int32, device="cuda")
     s_prep, s_on = torch.cuda.Stream(), torch.cuda.Stream()
     torch.cuda.synchronize()
     with torch.cuda.stream(s_prep):
-        preps = stack.prepare_layer(layer, ex, ey, flags, stream=s_prep)
+        preps = stack.prepare_layer(layer, ex, ey, flag, stream=s_prep)
     with torch.cuda.stream(s_on):
-        pout = stack.run_layer_prepared(layer, X, preps, ready_flag=[flags[i] for i in range(nin)],
-                                        timeout_us=2_000_000, timed_out=late, tamper=tamper, stream=s_on)
+        pout = stack.run_layer_prepared(layer, X, preps, ready_flag=flag, timeout_us=2_000_000, timed_out=late,
+                                        tamper=tamper, stream=s_on)
     torch.cuda.synchronize()
-    assert int(late.item()) == 0 and flags.tolist() == [0] * nin
+    assert int(late.item()) == 0 and int(flag.item()) == 0
     for name in out:
         for a, b in zip(out[name], pout[name]):
             assert torch.equal(a, b), (L, name, "prepared schedule")

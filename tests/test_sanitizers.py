@@ -47,7 +47,7 @@ def test_abi_size_checks_under_ubsan(tmp_path):
         assert rc == 0, out
         objs.append(obj)
     harness = str(tmp_path / "abi_harness.o")
-    rc, out = _run([hipcc, *flags, "-x", "c++", "-c", os.path.join(SAN, "abi_harness.cpp"), "-o", harness])
+    rc, out = _run([hipcc, *flags, "-x", "hip", "-c", os.path.join(SAN, "abi_harness.cpp"), "-o", harness])
     assert rc == 0, out
     exe = str(tmp_path / "abi_harness")
     rc, out = _run([hipcc, f"--offload-arch={B.ARCH}", "-fsanitize=undefined", "-o", exe, harness, *objs])

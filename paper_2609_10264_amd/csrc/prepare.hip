@@ -225,6 +225,44 @@ __global__ __launch_bounds__(kPrepThreads) void client_prepare_kernel(PrepArgs a
     }
 }
 
+// The gathers of a preparation launch alone, one item per 256-thread
+// workgroup (a quarter of client_prepare_kernel's), for launches with many
+// items: small workgroups with a small LDS footprint share compute units with
+// the kernels of other streams instead of taking whole ones.  The syndromes
+// then run before, in client_prepare_kernel launched with their workgroups
+// only.  SIG as in client_prepare_kernel.
+template <bool SIG, bool VEC>
+__global__ __launch_bounds__(kQuarter) void client_gather_kernel(PrepArgs a) {
+    __shared__ __align__(16) uint64_t part[gather_part(VEC)];
+    constexpr uint32_t cols = gather_cols(VEC);
+    uint32_t item = blockIdx.x;
+    uint32_t g = 0;
+    while (g < a.G && item >= a.it_end[g]) ++g;
+    if (g < a.G) {
+        const PrepProb& pr = a.pr[g];
+        item -= g ? a.it_end[g - 1] : 0u;
+        if (item < pr.items_x) {
+            const PrepIn& in = a.in[pr.in];
+            const uint32_t b = item / pr.nbm, cb = item % pr.nbm;
+            gather_item<SIG, VEC>(pr.PT, pr.m, in.r * in.n, in.idx + (size_t)b * in.t, in.val + (size_t)b * in.t, in.t,
+                                  pr.My + (size_t)b * pr.m, cb * cols, true, part);
+        } else {
+            const uint32_t q = (item - pr.items_x) / pr.nbn, cb = (item - pr.items_x) % pr.nbn;
+            gather_item<SIG, VEC>(pr.Q, pr.n, pr.r * pr.m, pr.idx + (size_t)q * pr.t, pr.val + (size_t)q * pr.t, pr.t,
+                                  pr.U + (size_t)q * pr.n, cb * cols, true, part);
+        }
+    } else {
+        gather_item<SIG, VEC>(nullptr, 0u, 1u, nullptr, nullptr, 0u, nullptr, 0u, false, part);
+    }
+    if constexpr (SIG) {
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (threadIdx.x == 0 && count_last(a.counter, a.slots))
+            for (uint32_t f = 0; f < a.ndone; ++f)
+                __hip_atomic_store(a.done[f], a.done_value, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
 // Polls *flag (device-coherent loads, a short sleep between polls) from the
 // calling thread until it holds `value`; false after `ticks` of the constant
 // wall clock.
@@ -387,7 +425,9 @@ struct PrepPlan {
     PrepArgs a;
     uint32_t U;
     bool vec;
-    uint64_t grid;
+    uint64_t grid;        // workgroups of the launch (of the gather launch when split)
+    uint64_t syn_groups;  // syndrome workgroups
+    bool split;           // syndromes and gathers in two launches (client_gather_kernel)
 };
 
 PrepPlan prep_plan(const PrepInputDesc* ins, uint32_t NI, const PrepProbDesc* probs, uint32_t G) {
@@ -435,7 +475,11 @@ PrepPlan prep_plan(const PrepInputDesc* ins, uint32_t NI, const PrepProbDesc* pr
         items += ix + iy;
         a.it_end[g] = (uint32_t)(items < 0xffffffffu ? items : 0xffffffffu);
     }
-    pl.grid = sy + (items + kQuarters - 1) / kQuarters;
+    // more gather workgroups than compute units: the gathers take their own
+    // launch of small workgroups (client_gather_kernel), after the syndromes
+    pl.syn_groups = sy;
+    pl.split = (items + kQuarters - 1) / kQuarters > 256;
+    pl.grid = pl.split ? items : sy + (items + kQuarters - 1) / kQuarters;
     return pl;
 }
 
@@ -484,12 +528,36 @@ hipError_t launch_client_prepare_multi(const PrepInputDesc* ins, uint32_t NI, co
     if (pl.grid == 0) return hipSuccess;
     if (pl.grid > 0x7fffffffu) return hipErrorInvalidValue;
     PrepArgs& a = pl.a;
+    if (pl.split && pl.syn_groups) {
+        // the short syndromes: client_prepare_kernel with their workgroups only
+        // (complete, and visible to the gather launch, when it ends)
+        const dim3 sgrid((uint32_t)pl.syn_groups), sblock(kPrepThreads);
+#define MVK_SYN_ONLY(UU) hipLaunchKernelGGL((client_prepare_kernel<UU, false, false>), sgrid, sblock, 0, s, a)
+        if (pl.U == 4) { MVK_SYN_ONLY(4); }
+        else if (pl.U == 8) { MVK_SYN_ONLY(8); }
+        else if (pl.U == 12) { MVK_SYN_ONLY(12); }
+        else { MVK_SYN_ONLY(16); }
+#undef MVK_SYN_ONLY
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     a.counter = counter;
     a.slots = count_slots((uint32_t)pl.grid);
     a.ndone = done ? ndone : 0u;
     for (uint32_t f = 0; f < a.ndone; ++f) a.done[f] = done[f];
     a.done_value = done_value;
     const bool sig = a.ndone > 0;
+    if (pl.split) {
+        const dim3 ggrid((uint32_t)pl.grid), gblock(kQuarter);
+        if (sig) {
+            if (pl.vec) hipLaunchKernelGGL((client_gather_kernel<true, true>), ggrid, gblock, 0, s, a);
+            else hipLaunchKernelGGL((client_gather_kernel<true, false>), ggrid, gblock, 0, s, a);
+        } else {
+            if (pl.vec) hipLaunchKernelGGL((client_gather_kernel<false, true>), ggrid, gblock, 0, s, a);
+            else hipLaunchKernelGGL((client_gather_kernel<false, false>), ggrid, gblock, 0, s, a);
+        }
+        return hipGetLastError();
+    }
     const dim3 grid((uint32_t)pl.grid), block(kPrepThreads);
 #define MVK_PREP_V(UU, SIG)                                                                             \
     if (pl.vec)                                                                                         \

@@ -211,6 +211,10 @@ def parse():
     ap.add_argument("--prep-streams", type=int, default=1,
                     help="preparation streams of the pipelined and overlapped stack schedules (more than one "
                          "measured slower: 5.4 against 4.2 ms per pass with two)")
+    ap.add_argument("--prep-cus", type=int, default=64,
+                    help="pipelined stack schedule: compute units of the preparation stream (the online stream "
+                         "gets the others; 0: both streams on every unit). Measured 3.69 ms per pass with 64, "
+                         "4.00 ms with 0")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the run, copy a buffer of this many MiB (reference for the traffic counters)")
     ap.add_argument("--seed", type=int, default=2609)
@@ -647,7 +651,17 @@ def stack_bench(args, steps, warmup, cpu_seconds):
     # waits
     nin = len(stack.INPUTS)
     npre = max(1, args.prep_streams)
-    s_preps, s_on = [torch.cuda.Stream() for _ in range(npre)], torch.cuda.Stream()
+    cu_streams = []
+    if args.prep_cus and npre == 1:
+        # the preparation on compute units [0, prep_cus), the online calls on
+        # the rest: neither stream's workgroups wait for the other's units
+        ncu = mvk.device_cus()
+        if not 0 < args.prep_cus < ncu:
+            raise SystemExit(f"--prep-cus must be between 1 and {ncu - 1}")
+        cu_streams = [mvk.CUStream(0, args.prep_cus), mvk.CUStream(args.prep_cus, ncu - args.prep_cus)]
+        s_preps, s_on = [cu_streams[0].stream], cu_streams[1].stream
+    else:
+        s_preps, s_on = [torch.cuda.Stream() for _ in range(npre)], torch.cuda.Stream()
     flags = torch.zeros((layers, nin), dtype=torch.int32, device=dev)
     late = torch.zeros((), dtype=torch.int32, device=dev)
     preps = [dict() for _ in range(layers)]
@@ -704,6 +718,8 @@ def stack_bench(args, steps, warmup, cpu_seconds):
     same = all(bool(torch.equal(a, b)) for sr, pr in zip(results, presults) for name in sr
                for a, b in zip(sr[name], pr[name]))
     del gs, gps, go
+    for c in cu_streams:
+        c.close()
 
     # ---- overlapped: the pass on several streams, one graph ----------------
     ov_main = torch.cuda.Stream()
@@ -778,7 +794,8 @@ def stack_bench(args, steps, warmup, cpu_seconds):
                                   f"projection, RAA r={r}, t_x={tx}, t_y={ty}, ell={ell}; step = one pass (per layer "
                                   "4 encodes, 7 server_evals, 7 decode_verifies) with one response in 1000 "
                                   "tampered and rejected",
-                      "global_batch": B, "launch": "hip_graph", "mode": args.stack_mode, "weights": "packed"},
+                      "global_batch": B, "launch": "hip_graph", "mode": args.stack_mode, "weights": "packed",
+                      "prep_cus": args.prep_cus if args.stack_mode == "pipelined" else None},
            "ms_per_step_overlapped": 1e3 * t_ov, "ms_per_step_pipelined": 1e3 * t_pipe,
            "ms_per_step_serial": 1e3 * t_serial,
            "modmac_per_pass": macs,

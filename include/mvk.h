@@ -53,7 +53,7 @@ extern "C" {
 
 #define MVK_PRIME 2147483647u
 #define MVK_PRIME_BABYBEAR 2013265921u
-#define MVK_ABI_VERSION 7
+#define MVK_ABI_VERSION 8
 
 typedef int32_t mvk_status;
 #define MVK_OK 0
@@ -510,6 +510,21 @@ mvk_status mvk_stream_read(const void *data, size_t bytes, uint32_t *sink, void 
  * captured before those growths will be replayed again.
  */
 mvk_status mvk_workspace_release(void);
+
+/*
+ * A stream of the current device whose kernels run only on the compute units
+ * [first_cu, first_cu + count), numbered as the device's compute-unit mask
+ * numbers them (a CU mask on the stream's hardware queue; default priority).
+ * For schedules with two independent streams, such as the client's
+ * preparation beside the online calls of the pipelined mode (Sec. 7): two
+ * disjoint ranges keep the streams' workgroups off each other's compute
+ * units, so a kernel waiting on a flag never holds units the other stream's
+ * producer needs.  Release with mvk_stream_destroy.
+ * Errors: MVK_EINVAL (stream NULL, count 0, or a range past the device's
+ * compute units), MVK_EHIP.
+ */
+mvk_status mvk_stream_create_cu_range(uint32_t first_cu, uint32_t count, void **stream);
+mvk_status mvk_stream_destroy(void *stream);
 
 /* ---------------------------------------------------------------------------
  * Seeded calls: the library draws the method's randomness.

@@ -469,6 +469,38 @@ def decode_verify_masked_group(keys: list, Xhat: torch.Tensor, Yhats: list, prep
     return Ys, accepts, vLs, vRs
 
 
+class CUStream:
+    """A stream restricted to the compute units [first_cu, first_cu + count)
+    (mvk_stream_create_cu_range); .stream is the torch view of it.  The HIP
+    stream is destroyed by close() (or when this object is collected), after
+    the device has finished its work."""
+
+    def __init__(self, first_cu: int, count: int):
+        h = ctypes.c_void_p()
+        _lib.check("mvk_stream_create_cu_range", _lib.load().mvk_stream_create_cu_range(first_cu, count,
+                                                                                          ctypes.byref(h)))
+        self._h = h.value
+        self.first_cu, self.count = first_cu, count
+        self.stream = torch.cuda.ExternalStream(self._h)
+
+    def close(self) -> None:
+        if self._h:
+            torch.cuda.synchronize()
+            _lib.check("mvk_stream_destroy", _lib.load().mvk_stream_destroy(self._h))
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def device_cus() -> int:
+    """Compute units of the current device."""
+    return torch.cuda.get_device_properties(torch.cuda.current_device()).multi_processor_count
+
+
 def flag_signal(flag: torch.Tensor, value: int = 1, stream=None) -> None:
     """Set the device word `flag` to value once the stream's earlier work is done."""
     _lib.check("mvk_flag_signal", _lib.load().mvk_flag_signal(

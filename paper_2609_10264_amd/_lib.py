@@ -32,7 +32,7 @@ MVK_SEEDED_MAX_T = 4096
 MVK_STATIC_SCRATCH_BYTES = 32 << 20
 MVK_MAX_GROUP = 4
 MVK_MAX_PREP = 8
-ABI_VERSION = 7
+ABI_VERSION = 8
 # field modulus -> library built over that field
 LIB_PATHS = {MVK_PRIME: LIB_PATH, MVK_PRIME_BABYBEAR: LIB_PATH_BB}
 
@@ -78,6 +78,8 @@ EXPORTS = (
     "mvk_decode_verify_masked_group",
     "mvk_client_prepare_group",
     "mvk_client_prepare_multi",
+    "mvk_stream_create_cu_range",
+    "mvk_stream_destroy",
 )
 
 
@@ -227,6 +229,10 @@ def load(p: int = MVK_PRIME) -> ctypes.CDLL:
                                            ctypes.POINTER(ctypes.POINTER(MvkSparse)),
                                            ctypes.POINTER(ctypes.POINTER(MvkSparse)), pvp, pvp, pvp, pvp, pvp, u32, vp]
     L.mvk_client_prepare_multi.restype = st
+    L.mvk_stream_create_cu_range.argtypes = [u32, u32, ctypes.POINTER(vp)]
+    L.mvk_stream_create_cu_range.restype = st
+    L.mvk_stream_destroy.argtypes = [vp]
+    L.mvk_stream_destroy.restype = st
     if L.mvk_abi_version() != ABI_VERSION:
         raise ImportError(f"{path}: ABI version mismatch; rebuild the library")
     if L.mvk_field_modulus() != p:

@@ -3,6 +3,7 @@
 // This layer validates sizes, owns the per-(device, stream) workspace and
 // enqueues the kernels; all arithmetic happens in the kernels.
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 
 #include <sys/random.h>
 
@@ -931,6 +932,29 @@ mvk_status mvk_workspace_release(void) {
     for (void* p : *g_ws_retired) (void)hipFree(p);
     g_ws_retired->clear();
     return MVK_OK;
+}
+
+mvk_status mvk_stream_create_cu_range(uint32_t first_cu, uint32_t count, void** stream) {
+    if (!stream || count == 0) return MVK_EINVAL;
+    int dev = 0, ncu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || ncu <= 0)
+        return MVK_EHIP;
+    if ((uint64_t)first_cu + count > (uint64_t)ncu) return MVK_EINVAL;
+    std::vector<uint32_t> mask(((size_t)ncu + 31) / 32, 0u);
+    for (uint32_t c = first_cu; c < first_cu + count; ++c) mask[c / 32] |= 1u << (c % 32);
+    hipStream_t s = nullptr;
+    if (hipExtStreamCreateWithCUMask(&s, (uint32_t)mask.size(), mask.data()) != hipSuccess) {
+        (void)hipGetLastError();
+        return MVK_EHIP;
+    }
+    *stream = s;
+    return MVK_OK;
+}
+
+mvk_status mvk_stream_destroy(void* stream) {
+    if (!stream) return MVK_EINVAL;
+    return hip_status(hipStreamDestroy((hipStream_t)stream));
 }
 
 mvk_status mvk_sample_code(uint32_t k, uint32_t r, uint64_t seed, uint64_t tag, uint32_t* pi1, uint32_t* pi2,

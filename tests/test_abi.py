@@ -88,6 +88,11 @@ def test_host_argument_checks_without_device_work():
     assert lib.mvk_raa_encode(ctypes.byref(bad), fake, 1, fake, None) == L.MVK_EINVAL
     nullcode = L.MvkCode(8, 2, 0, 0x1000, 0x1000, 0x1000)
     assert lib.mvk_raa_syndrome(ctypes.byref(nullcode), fake, 1, fake, None) == L.MVK_EINVAL
+    # compute-unit streams: an empty range or no output pointer
+    h = ctypes.c_void_p()
+    assert lib.mvk_stream_create_cu_range(0, 0, ctypes.byref(h)) == L.MVK_EINVAL
+    assert lib.mvk_stream_create_cu_range(0, 8, None) == L.MVK_EINVAL
+    assert lib.mvk_stream_destroy(None) == L.MVK_EINVAL
 
 
 def test_sizes_no_buffer_can_hold_are_rejected():

@@ -134,6 +134,41 @@ def test_flags_order_two_streams():
     assert int(late.item()) == 1 and int(flags[1].item()) == 0
 
 
+def test_flags_order_compute_unit_streams():
+    """Two streams on disjoint compute-unit ranges (mvk_stream_create_cu_range):
+    a flag wait on one sees the data the other wrote before its signal, and a
+    server product on a restricted stream equals the one on a plain stream;
+    a range past the device's units is refused."""
+    ncu = mvk.device_cus()
+    with pytest.raises(mvk.MvkError):
+        mvk.CUStream(ncu - 4, 8)
+    a, b = mvk.CUStream(0, 64), mvk.CUStream(64, ncu - 64)
+    try:
+        flag = torch.zeros((), dtype=torch.int32, device="cuda")
+        late = torch.zeros((), dtype=torch.int32, device="cuda")
+        buf = torch.zeros(1 << 20, dtype=torch.int32, device="cuda")
+        torch.cuda.synchronize()
+        with torch.cuda.stream(a.stream):
+            buf.fill_(5)
+            mvk.flag_signal(flag, 3, stream=a.stream)
+        mvk.flag_wait(flag, 3, timeout_us=2_000_000, timed_out=late, stream=b.stream)
+        with torch.cuda.stream(b.stream):
+            total = buf.to(torch.int64).sum()
+        torch.cuda.synchronize()
+        assert int(late.item()) == 0 and int(flag.item()) == 0
+        assert int(total.item()) == 5 * buf.numel()
+        W = dev(synth.weights(synth.seed_for(62, synth.PURPOSE_W), 1000, 700))
+        X = dev(synth.field_uniform(synth.seed_for(62, synth.PURPOSE_X), (8, 700)))
+        ref = mvk.server_eval(W, X)
+        with torch.cuda.stream(a.stream):
+            ya = mvk.server_eval(W, X, stream=a.stream)
+        torch.cuda.synchronize()
+        assert torch.equal(ya, ref)
+    finally:
+        a.close()
+        b.close()
+
+
 def test_pipelined_graphs_match_one_call_path():
     """The pipelined standard mode as two HIP graphs (preparation stream ahead of
     the online stream, ordered by flags) against the one-call path, per step."""

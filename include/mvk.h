@@ -191,10 +191,11 @@ mvk_status mvk_server_eval_packed_group(const int8_t *Wp, uint32_t G, uint32_t m
  * mvk_server_eval_packed for callers that cannot allocate device memory (code
  * under HIP graph capture, tight serving loops, harnesses that forbid
  * hipMalloc): the same product, bit for bit, whose kernels keep their scratch
- * (the batched kernels' digit matrix, split-k partial sums and row-block
- * counters) in a device array of the library, MVK_STATIC_SCRATCH_BYTES of data
- * plus 64 KiB of control words, held on every GPU the library runs on until
- * the process ends.  It calls no hipMalloc or hipFree.  The counters are
+ * (the batched kernels' digit matrix, split-k partial sums and accumulators,
+ * row-block counters) in a device array of the library of
+ * MVK_STATIC_SCRATCH_BYTES + 64 KiB (control words first, at least 64 KiB of
+ * them, then the data), held on every GPU the library runs on until the
+ * process ends.  It calls no hipMalloc or hipFree.  The control words are
  * cleared by a kernel at every call.  Every call on one GPU shares that GPU's
  * array: calls that overlap in time on one GPU (two streams, two threads)
  * race and must be ordered by the caller.

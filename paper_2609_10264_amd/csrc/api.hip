@@ -318,11 +318,11 @@ mvk_status mvk_server_eval_packed_group(const int8_t* Wp, uint32_t G, uint32_t m
 
 // ---------------------------------------------------------------------------
 // Allocation-free server product: the scratch of the batched kernels (digit
-// matrix, split-k partial sums, row-block counters) lives in one statically
-// sized device array instead of the per-stream workspace.
+// matrix, split-k partial sums and accumulators, row-block counters) lives in
+// one statically sized device array instead of the per-stream workspace.
 // ---------------------------------------------------------------------------
 namespace {
-constexpr size_t kScratchCtrlBytes = 64u << 10;  // word 0: validation count; counters from byte 256
+constexpr size_t kScratchCtrlBytes = 64u << 10;  // word 0: validation count; control words from byte 256
 constexpr size_t kScratchDataBytes = (size_t)MVK_STATIC_SCRATCH_BYTES;
 __device__ __align__(256) uint8_t scratch[kScratchCtrlBytes + kScratchDataBytes];
 
@@ -362,7 +362,10 @@ mvk_status mvk_server_eval_packed_static(const int8_t* Wp, uint32_t m, uint32_t 
     if (!Wp || !Xhat || (uintptr_t)Wp % 16 != 0) return MVK_EINVAL;
     if (n > MVK_MAX_N) return MVK_ERANGE;
     const ServerEvalPlan pl = server_eval_plan(m, n, B, MVK_PATH_AUTO, true);
-    if (pl.ws_bytes > kScratchDataBytes || 256 + 4 * pl.ctrl_words > kScratchCtrlBytes) return MVK_ERANGE;
+    // the array holds the control words (from byte 256: counters and split-k
+    // accumulators), then the data; at least the first 64 KiB are control
+    const size_t ctrl_bytes = std::max(kScratchCtrlBytes, align_up(256 + 4 * pl.ctrl_words));
+    if (pl.ws_bytes > kScratchCtrlBytes + kScratchDataBytes - ctrl_bytes) return MVK_ERANGE;
     const bool validate = validate_mode();
     if (!pl.ws_bytes && !pl.ctrl_words && !validate)
         return hip_status(launch_server_eval(Wp, m, n, Xhat, B, Yhat, MVK_PATH_AUTO, true, nullptr, nullptr, s));
@@ -373,8 +376,8 @@ mvk_status mvk_server_eval_packed_static(const int8_t* Wp, uint32_t m, uint32_t 
     uint32_t* counters = (uint32_t*)(base + 256);
     // the counters start at zero for every call (a kernel, so that the call can be captured)
     if (pl.ctrl_words && launch_fill_u32(counters, pl.ctrl_words, 0u, s) != hipSuccess) return MVK_EHIP;
-    return hip_status(launch_server_eval(Wp, m, n, Xhat, B, Yhat, MVK_PATH_AUTO, true, base + kScratchCtrlBytes,
-                                         counters, s));
+    return hip_status(launch_server_eval(Wp, m, n, Xhat, B, Yhat, MVK_PATH_AUTO, true, base + ctrl_bytes, counters,
+                                         s));
 }
 
 mvk_status mvk_keygen(const mvk_key* key, const int8_t* W, void* stream) {

@@ -574,6 +574,41 @@ __device__ __forceinline__ void store_tiles(const v4i (&acc)[QW][TWW], uint32_t 
     if (threadIdx.x == 0) atomicExch(&counters[rb], 0u);
 }
 
+// Split-k exchange of the digits-stationary kernel: one 64-bit atomic add
+// per value into a per-value accumulator (this k-range's value mod p in the
+// low 40 bits, a count of arrived k-ranges from bit 40).  The add that
+// completes the count (it returns ksplit - 1 arrivals) holds the whole sum:
+// that lane writes Y and resets the accumulator, so every launch leaves the
+// accumulators at zero.  One round trip to the memory side, and no
+// per-row-block counter.  The accumulators are indexed like the kernel's
+// value layout: (row block, wave, digit tile, W tile, lane).
+template <int QW, int TWW, int NW>
+__device__ __forceinline__ void store_tiles_atomic(const v4i (&acc)[QW][TWW], uint32_t m, uint32_t B,
+                                                   const YOut& Y, unsigned long long* accum, uint32_t rb,
+                                                   uint32_t ksplit, int wave, int lane, uint32_t rowbase,
+                                                   uint32_t qbase) {
+    unsigned long long old[QW][TWW];
+    uint32_t v[QW][TWW];
+    const size_t base = ((size_t)rb * NW + wave) * (QW * TWW);
+#pragma unroll
+    for (int i = 0; i < QW; ++i)
+#pragma unroll
+        for (int t = 0; t < TWW; ++t) {
+            v[i][t] = digits_to_field(acc[i][t]);
+            old[i][t] = atomicAdd(&accum[(base + i * TWW + t) * 64 + lane], (1ull << 40) | (unsigned long long)v[i][t]);
+        }
+#pragma unroll
+    for (int i = 0; i < QW; ++i)
+#pragma unroll
+        for (int t = 0; t < TWW; ++t) {
+            if ((uint32_t)(old[i][t] >> 40) != ksplit - 1) continue;
+            const uint32_t q = qbase + 4 * i, row = rowbase + 16 * t;
+            if (q < B && row < m) *Y.at(q, row) = fred64((old[i][t] & ((1ull << 40) - 1)) + v[i][t]);
+            __hip_atomic_store(&accum[(base + i * TWW + t) * 64 + lane], 0ull, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        }
+}
+
 // global_load_dwordx4 into a register quad, as inline assembly like dma16 so
 // that the explicit wait_vmcnt calls count it; the value may only be used
 // after a wait that covers it and a pin_vgpr that orders the use after that
@@ -713,7 +748,7 @@ template <int QT, int TWW, int KBM, int C, bool PACKED>
 __global__ __launch_bounds__(512) void server_eval_mfma_dstat(const int8_t* __restrict__ W, uint32_t m, uint32_t n,
                                                               const uint32_t* __restrict__ X, uint32_t nkb,
                                                               uint32_t ksplit, uint32_t B, const YOut Y,
-                                                              uint32_t* part, uint32_t* counters) {
+                                                              unsigned long long* accum) {
     constexpr int NW = 8;
     constexpr uint32_t kRows = NW * TWW * 16;
     __shared__ __align__(16) int8_t Dst[KBM][QT][1024];
@@ -851,10 +886,14 @@ __global__ __launch_bounds__(512) void server_eval_mfma_dstat(const int8_t* __re
         }
         compute(j0 + C, wb);
     }
-    __syncthreads();  // every wave is past its last digit-tile read
     const uint32_t rowbase = rb * kRows + wave * (TWW * 16) + (lane & 15);
     const uint32_t qbase = (uint32_t)(lane >> 4);
-    store_tiles<QT, TWW, NW>(acc, m, B, Y, part, counters, rb, (m + kRows - 1) / kRows, ks, ksplit, wave, lane,
+    if (ksplit > 1) {
+        store_tiles_atomic<QT, TWW, NW>(acc, m, B, Y, accum, rb, ksplit, wave, lane, rowbase, qbase);
+        return;
+    }
+    __syncthreads();  // every wave is past its last digit-tile read
+    store_tiles<QT, TWW, NW>(acc, m, B, Y, nullptr, nullptr, rb, (m + kRows - 1) / kRows, ks, 1u, wave, lane,
                              rowbase, qbase, reinterpret_cast<uint32_t*>(&Dst[0][0][0]));
 }
 
@@ -1007,37 +1046,38 @@ GroupPlan group_plan(uint32_t m, uint32_t n, uint32_t nb) {
 
 template <int QT, int TWW, int KBM, int C>
 hipError_t launch_dstat_cfg(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t nkb, uint32_t B,
-                            const YOut& Y, uint32_t ksplit, uint32_t* part, uint32_t* counters, bool packed,
+                            const YOut& Y, uint32_t ksplit, unsigned long long* accum, bool packed,
                             hipStream_t s);
 
 // launch_dstat_cfg for the plan's LDS size (kbm a power of two in [8, KBM max])
 template <int QT, int TWW>
 hipError_t launch_dstat_kbm(uint32_t kbm, const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t nkb,
-                            uint32_t B, const YOut& Y, uint32_t ksplit, uint32_t* part, uint32_t* counters,
+                            uint32_t B, const YOut& Y, uint32_t ksplit, unsigned long long* accum,
                             bool packed, hipStream_t s) {
     constexpr uint32_t kMax = QT == 4 ? kDstatKbm4 : kDstatKbm2;
-    if (kbm == 8) return launch_dstat_cfg<QT, TWW, 8, 8>(W, m, n, X, nkb, B, Y, ksplit, part, counters, packed, s);
-    if (kbm == 16) return launch_dstat_cfg<QT, TWW, 16, 8>(W, m, n, X, nkb, B, Y, ksplit, part, counters, packed, s);
-    if (kbm == 32) return launch_dstat_cfg<QT, TWW, 32, 8>(W, m, n, X, nkb, B, Y, ksplit, part, counters, packed, s);
+    if (kbm == 8) return launch_dstat_cfg<QT, TWW, 8, 8>(W, m, n, X, nkb, B, Y, ksplit, accum, packed, s);
+    if (kbm == 16) return launch_dstat_cfg<QT, TWW, 16, 8>(W, m, n, X, nkb, B, Y, ksplit, accum, packed, s);
+    if (kbm == 32) return launch_dstat_cfg<QT, TWW, 32, 8>(W, m, n, X, nkb, B, Y, ksplit, accum, packed, s);
     if constexpr (kMax >= 64)
         if (kbm == 64)
-            return launch_dstat_cfg<QT, TWW, 64, 8>(W, m, n, X, nkb, B, Y, ksplit, part, counters, packed, s);
+            return launch_dstat_cfg<QT, TWW, 64, 8>(W, m, n, X, nkb, B, Y, ksplit, accum, packed, s);
     return hipErrorInvalidValue;
 }
 
 template <int QT, int TWW, int KBM, int C>
 hipError_t launch_dstat_cfg(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t nkb, uint32_t B,
-                            const YOut& Y, uint32_t ksplit, uint32_t* part, uint32_t* counters, bool packed,
+                            const YOut& Y, uint32_t ksplit, unsigned long long* accum, bool packed,
                             hipStream_t s) {
     if (ksplit == 0 || ceil_div(nkb, ksplit) > (uint32_t)KBM) return hipErrorInvalidValue;  // LDS holds the range
+    if (ksplit > 1 && !accum) return hipErrorInvalidValue;
     const uint32_t nrb = ceil_div(m, 128 * TWW), per_group = 8 / ksplit;
     const dim3 grid(ceil_div(nrb, per_group) * 8);
     if (packed)
         hipLaunchKernelGGL((server_eval_mfma_dstat<QT, TWW, KBM, C, true>), grid, dim3(512), 0, s, W, m, n, X, nkb,
-                           ksplit, B, Y, part, counters);
+                           ksplit, B, Y, accum);
     else
         hipLaunchKernelGGL((server_eval_mfma_dstat<QT, TWW, KBM, C, false>), grid, dim3(512), 0, s, W, m, n, X, nkb,
-                           ksplit, B, Y, part, counters);
+                           ksplit, B, Y, accum);
     return hipGetLastError();
 }
 }  // namespace
@@ -1058,9 +1098,15 @@ ServerEvalPlan server_eval_plan(uint32_t m, uint32_t n, uint32_t B, int path, bo
         }
         if (g.ks > 1) {
             const size_t nrb = ceil_div(m, g.rows);
-            const size_t pb = (size_t)g.ks * nrb * g.rows * g.qt * 4 * 4;
-            part_bytes = pb > part_bytes ? pb : part_bytes;
-            pl.ctrl_words = nrb > pl.ctrl_words ? nrb : pl.ctrl_words;
+            if (g.dstat) {
+                // one 64-bit accumulator per value of the row blocks (zero between launches)
+                const size_t aw = nrb * g.rows * g.qt * 4 * 2;
+                pl.ctrl_words = aw > pl.ctrl_words ? aw : pl.ctrl_words;
+            } else {
+                const size_t pb = (size_t)g.ks * nrb * g.rows * g.qt * 4 * 4;
+                part_bytes = pb > part_bytes ? pb : part_bytes;
+                pl.ctrl_words = nrb > pl.ctrl_words ? nrb : pl.ctrl_words;
+            }
         }
     }
     pl.ws_bytes = dt_bytes + part_bytes;
@@ -1106,6 +1152,9 @@ hipError_t launch_server_eval_group(const int8_t* W, uint32_t G, uint32_t mg, ui
         }
     }
     int8_t* Dt = (int8_t*)ws;
+    // the digits-stationary kernel's split-k accumulators share the control
+    // words with the streamed kernel's counters (each launch leaves them zero)
+    unsigned long long* accum = reinterpret_cast<unsigned long long*>(counters);
     uint32_t* part = (uint32_t*)((char*)ws + dt_bytes);
     for (uint32_t b0 = 0; b0 < B; b0 += 64) {
         const uint32_t nb = (B - b0) < 64 ? (B - b0) : 64;
@@ -1115,14 +1164,14 @@ hipError_t launch_server_eval_group(const int8_t* W, uint32_t G, uint32_t mg, ui
         hipError_t e = hipSuccess;
         if (g.dstat) {
             if (g.qt == 4)
-                e = g.tww == 1 ? launch_dstat_kbm<4, 1>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
+                e = g.tww == 1 ? launch_dstat_kbm<4, 1>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, accum,
                                                         packed, s)
-                               : launch_dstat_kbm<4, 2>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
+                               : launch_dstat_kbm<4, 2>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, accum,
                                                         packed, s);
             else
-                e = g.tww == 1 ? launch_dstat_kbm<2, 1>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
+                e = g.tww == 1 ? launch_dstat_kbm<2, 1>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, accum,
                                                         packed, s)
-                               : launch_dstat_kbm<2, 2>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, part, counters,
+                               : launch_dstat_kbm<2, 2>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, accum,
                                                         packed, s);
             if (e != hipSuccess) return e;
             continue;

@@ -215,6 +215,10 @@ def parse():
                     help="pipelined stack schedule: compute units of the preparation stream (the online stream "
                          "gets the others; 0: both streams on every unit). Measured 3.69 ms per pass with 64, "
                          "4.00 ms with 0")
+    ap.add_argument("--config-prep-cus", type=int, default=0,
+                    help="the same split for the single-matrix workloads' pipelined schedule (0: none; with 64 "
+                         "their preparation, which outweighs the server call at 11008x4096 B=16 and "
+                         "28672x8192 B=64, became the bound)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the run, copy a buffer of this many MiB (reference for the traffic counters)")
     ap.add_argument("--seed", type=int, default=2609)
@@ -417,7 +421,16 @@ def config_bench(args, name, steps, warmup, cpu_seconds, large=False):
     flags = torch.zeros(total_steps, dtype=torch.int32, device=dev)
     late = torch.zeros((), dtype=torch.int32, device=dev)
     ACC2 = torch.zeros((total_steps, B), dtype=torch.int32, device=dev)
-    s_prep, s_on = torch.cuda.Stream(), torch.cuda.Stream()
+    cu_streams = []
+    if args.config_prep_cus:  # preparation and online calls on disjoint compute units
+        ncu = mvk.device_cus()
+        if not 0 < args.config_prep_cus < ncu:
+            raise SystemExit(f"--config-prep-cus must be between 1 and {ncu - 1}")
+        cu_streams = [mvk.CUStream(0, args.config_prep_cus),
+                      mvk.CUStream(args.config_prep_cus, ncu - args.config_prep_cus)]
+        s_prep, s_on = cu_streams[0].stream, cu_streams[1].stream
+    else:
+        s_prep, s_on = torch.cuda.Stream(), torch.cuda.Stream()
     pXh = torch.empty((B, n), dtype=torch.int32, device=dev)
     pYh = torch.empty((B, m), dtype=torch.int32, device=dev)
     pY = torch.empty((B, m), dtype=torch.int32, device=dev)
@@ -476,6 +489,8 @@ def config_bench(args, name, steps, warmup, cpu_seconds, large=False):
     torch.cuda.synchronize()
     pipe_matches = all(bool(torch.equal(a, b)) for a, b in zip(got, (rXh, rYh, rY)))
     del g_prep, g_on, preps
+    for c in cu_streams:
+        c.close()
     if not args.eager:
         del graphs
     elapsed = elapsed_pipe if args.mode == "pipelined" else elapsed_serial
@@ -497,6 +512,7 @@ def config_bench(args, name, steps, warmup, cpu_seconds, large=False):
         "value": macs * steps / elapsed, "unit": "modMAC/s", "steps": steps, "warmup": warmup,
         "ms_per_step": 1e3 * elapsed / steps, "mode": args.mode,
         "ms_per_step_pipelined": 1e3 * elapsed_pipe / steps, "ms_per_step_serial": 1e3 * elapsed_serial / steps,
+        "prep_cus": args.config_prep_cus,
         "w_pool": pool, "weights": args.weights, "launch": "eager" if args.eager else "hip_graph",
         "chains": C if args.mode == "serial" else 1,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",

@@ -109,6 +109,96 @@ __device__ __forceinline__ void gather_item(const uint32_t* __restrict__ M, uint
     }
 }
 
+// Wide gather item for large preparations (VEC only): gather_item over
+// kWideCols = 1024 columns, each lane loading four 16-byte pieces of a row
+// (a wave reads 4 KiB of the row per term, the row segments of an item are
+// four times as long as gather_item's, fewer DRAM pages opened per byte),
+// kWideBatch terms per batch (the same 16 loads per lane in flight).
+constexpr uint32_t kWideCols = 1024;
+constexpr int kWidePieces = 4;  // 16-byte loads per lane and term
+constexpr int kWideBatch = kQBatch / kWidePieces;
+constexpr size_t gather_part_wide() { return (size_t)kQGroups * kWideCols; }
+
+template <bool COHERENT>
+__device__ __forceinline__ void gather_item_wide(const uint32_t* __restrict__ M, uint32_t ld, uint32_t nrows,
+                                                 const uint32_t* __restrict__ idx,
+                                                 const uint32_t* __restrict__ val, uint32_t t,
+                                                 uint32_t* __restrict__ out, uint32_t col0, bool live,
+                                                 uint64_t* part) {
+    constexpr int E = 4 * kWidePieces;  // columns per lane
+    const int ltid = threadIdx.x & (kQuarter - 1);
+    const int lane = ltid & 63;
+    const int g = __builtin_amdgcn_readfirstlane(ltid >> 6);
+    // piece l of this lane: columns col0 + 256 l + 4 lane .. + 3
+    bool act[kWidePieces];
+    uint32_t is[kWidePieces];
+#pragma unroll
+    for (int l = 0; l < kWidePieces; ++l) {
+        const uint32_t i0 = col0 + 256u * l + 4u * lane;
+        act[l] = live && i0 < ld;
+        is[l] = act[l] ? i0 : 0u;
+    }
+    const uint32_t tt = live ? t : 0u;
+    const uint32_t chunk = (tt + kQGroups - 1) / kQGroups;
+    const uint32_t s_beg = (uint32_t)g * chunk;
+    const uint32_t s_end = s_beg + chunk < tt ? s_beg + chunk : tt;
+    uint64_t acc[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] = 0;
+    for (uint32_t s0 = s_beg; s0 < s_end; s0 += kWideBatch) {
+        // the batch's terms by lanes (as in gather_item), then every row load
+        const uint32_t lt = s0 + (uint32_t)(lane & (kWideBatch - 1));
+        const uint32_t lts = lt < s_end ? lt : s_beg;
+        const uint32_t jl = idx[lts], vl = val[lts];
+        uint32_t mv[kWideBatch][E], ww[kWideBatch];
+#pragma unroll
+        for (int u = 0; u < kWideBatch; ++u) {
+            const bool ok = s0 + (uint32_t)u < s_end;
+            uint32_t j = (uint32_t)__builtin_amdgcn_readlane((int)jl, u);
+            j = j < nrows ? j : nrows - 1;
+            ww[u] = ok ? (uint32_t)__builtin_amdgcn_readlane((int)vl, u) : 0u;
+            const uint32_t* row = M + (size_t)j * ld;
+#pragma unroll
+            for (int l = 0; l < kWidePieces; ++l) {
+                const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(row + is[l]));
+                mv[u][4 * l] = v.x;
+                mv[u][4 * l + 1] = v.y;
+                mv[u][4 * l + 2] = v.z;
+                mv[u][4 * l + 3] = v.w;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kWideBatch; ++u)
+#pragma unroll
+            for (int e = 0; e < E; ++e) acc[e] += ffold((uint64_t)ww[u] * mv[u][e]);
+    }
+#pragma unroll
+    for (int e = 0; e < E; ++e) part[(g * E + e) * 64 + lane] = acc[e];
+    __syncthreads();
+    if (g == 0) {
+#pragma unroll
+        for (int l = 0; l < kWidePieces; ++l) {
+            if (!act[l]) continue;
+            uint32_t r[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                uint64_t tot = 0;
+#pragma unroll
+                for (int h = 0; h < kQGroups; ++h) tot += part[(h * E + 4 * l + e) * 64 + lane];
+                r[e] = fred64(tot);
+            }
+            uint32_t* o = out + is[l];  // (word stores: the outputs need no 16-byte alignment)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                if (COHERENT)
+                    __hip_atomic_store(&o[e], r[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                else
+                    o[e] = r[e];
+            }
+        }
+    }
+}
+
 template <int U>
 constexpr size_t prep_lds_words() {
     constexpr size_t gather = (size_t)kQuarters * gather_part(true) * 2;
@@ -231,10 +321,11 @@ __global__ __launch_bounds__(kPrepThreads) void client_prepare_kernel(PrepArgs a
 // the kernels of other streams instead of taking whole ones.  The syndromes
 // then run before, in client_prepare_kernel launched with their workgroups
 // only.  SIG as in client_prepare_kernel.
-template <bool SIG, bool VEC>
+template <bool SIG, bool VEC, bool WIDE>
 __global__ __launch_bounds__(kQuarter) void client_gather_kernel(PrepArgs a) {
-    __shared__ __align__(16) uint64_t part[gather_part(VEC)];
-    constexpr uint32_t cols = gather_cols(VEC);
+    static_assert(!WIDE || VEC, "wide items read 16 bytes per lane and piece");
+    __shared__ __align__(16) uint64_t part[WIDE ? gather_part_wide() : gather_part(VEC)];
+    constexpr uint32_t cols = WIDE ? kWideCols : gather_cols(VEC);
     uint32_t item = blockIdx.x;
     uint32_t g = 0;
     while (g < a.G && item >= a.it_end[g]) ++g;
@@ -244,15 +335,26 @@ __global__ __launch_bounds__(kQuarter) void client_gather_kernel(PrepArgs a) {
         if (item < pr.items_x) {
             const PrepIn& in = a.in[pr.in];
             const uint32_t b = item / pr.nbm, cb = item % pr.nbm;
-            gather_item<SIG, VEC>(pr.PT, pr.m, in.r * in.n, in.idx + (size_t)b * in.t, in.val + (size_t)b * in.t, in.t,
-                                  pr.My + (size_t)b * pr.m, cb * cols, true, part);
+            if constexpr (WIDE)
+                gather_item_wide<SIG>(pr.PT, pr.m, in.r * in.n, in.idx + (size_t)b * in.t, in.val + (size_t)b * in.t,
+                                      in.t, pr.My + (size_t)b * pr.m, cb * cols, true, part);
+            else
+                gather_item<SIG, VEC>(pr.PT, pr.m, in.r * in.n, in.idx + (size_t)b * in.t, in.val + (size_t)b * in.t,
+                                      in.t, pr.My + (size_t)b * pr.m, cb * cols, true, part);
         } else {
             const uint32_t q = (item - pr.items_x) / pr.nbn, cb = (item - pr.items_x) % pr.nbn;
-            gather_item<SIG, VEC>(pr.Q, pr.n, pr.r * pr.m, pr.idx + (size_t)q * pr.t, pr.val + (size_t)q * pr.t, pr.t,
-                                  pr.U + (size_t)q * pr.n, cb * cols, true, part);
+            if constexpr (WIDE)
+                gather_item_wide<SIG>(pr.Q, pr.n, pr.r * pr.m, pr.idx + (size_t)q * pr.t, pr.val + (size_t)q * pr.t,
+                                      pr.t, pr.U + (size_t)q * pr.n, cb * cols, true, part);
+            else
+                gather_item<SIG, VEC>(pr.Q, pr.n, pr.r * pr.m, pr.idx + (size_t)q * pr.t, pr.val + (size_t)q * pr.t,
+                                      pr.t, pr.U + (size_t)q * pr.n, cb * cols, true, part);
         }
     } else {
-        gather_item<SIG, VEC>(nullptr, 0u, 1u, nullptr, nullptr, 0u, nullptr, 0u, false, part);
+        if constexpr (WIDE)
+            gather_item_wide<SIG>(nullptr, 0u, 1u, nullptr, nullptr, 0u, nullptr, 0u, false, part);
+        else
+            gather_item<SIG, VEC>(nullptr, 0u, 1u, nullptr, nullptr, 0u, nullptr, 0u, false, part);
     }
     if constexpr (SIG) {
         __builtin_amdgcn_s_waitcnt(0);
@@ -428,7 +530,11 @@ struct PrepPlan {
     uint64_t grid;        // workgroups of the launch (of the gather launch when split)
     uint64_t syn_groups;  // syndrome workgroups
     bool split;           // syndromes and gathers in two launches (client_gather_kernel)
+    bool wide;            // the gather launch's items are kWideCols columns wide
 };
+
+PrepPlan plan_with_cols(PrepPlan pl, const PrepInputDesc* ins, uint32_t NI, const PrepProbDesc* probs, uint32_t G,
+                        uint32_t cols);
 
 PrepPlan prep_plan(const PrepInputDesc* ins, uint32_t NI, const PrepProbDesc* probs, uint32_t G) {
     PrepPlan pl{};
@@ -436,7 +542,15 @@ PrepPlan prep_plan(const PrepInputDesc* ins, uint32_t NI, const PrepProbDesc* pr
     a.NI = NI;
     a.G = G;
     pl.vec = prep_vec(ins, probs, G);
-    const uint32_t cols = gather_cols(pl.vec);
+    return plan_with_cols(pl, ins, NI, probs, G, gather_cols(pl.vec));
+}
+
+// The plan's descriptors and counts for items of `cols` columns; a split
+// plan with 16-byte rows that has at least 256 items of kWideCols columns
+// takes those (client_gather_kernel's wide form).
+PrepPlan plan_with_cols(PrepPlan pl, const PrepInputDesc* ins, uint32_t NI, const PrepProbDesc* probs, uint32_t G,
+                        uint32_t cols) {
+    PrepArgs& a = pl.a;
     uint64_t sx = 0, sy = 0, items = 0;
     for (uint32_t j = 0; j < NI; ++j) {
         const PrepInputDesc& d = ins[j];
@@ -480,6 +594,11 @@ PrepPlan prep_plan(const PrepInputDesc* ins, uint32_t NI, const PrepProbDesc* pr
     pl.syn_groups = sy;
     pl.split = (items + kQuarters - 1) / kQuarters > 256;
     pl.grid = pl.split ? items : sy + (items + kQuarters - 1) / kQuarters;
+    pl.wide = cols == kWideCols;
+    if (pl.split && pl.vec && !pl.wide) {
+        const PrepPlan w = plan_with_cols(pl, ins, NI, probs, G, kWideCols);
+        if (w.grid >= 256) return w;
+    }
     return pl;
 }
 
@@ -550,11 +669,13 @@ hipError_t launch_client_prepare_multi(const PrepInputDesc* ins, uint32_t NI, co
     if (pl.split) {
         const dim3 ggrid((uint32_t)pl.grid), gblock(kQuarter);
         if (sig) {
-            if (pl.vec) hipLaunchKernelGGL((client_gather_kernel<true, true>), ggrid, gblock, 0, s, a);
-            else hipLaunchKernelGGL((client_gather_kernel<true, false>), ggrid, gblock, 0, s, a);
+            if (pl.wide) hipLaunchKernelGGL((client_gather_kernel<true, true, true>), ggrid, gblock, 0, s, a);
+            else if (pl.vec) hipLaunchKernelGGL((client_gather_kernel<true, true, false>), ggrid, gblock, 0, s, a);
+            else hipLaunchKernelGGL((client_gather_kernel<true, false, false>), ggrid, gblock, 0, s, a);
         } else {
-            if (pl.vec) hipLaunchKernelGGL((client_gather_kernel<false, true>), ggrid, gblock, 0, s, a);
-            else hipLaunchKernelGGL((client_gather_kernel<false, false>), ggrid, gblock, 0, s, a);
+            if (pl.wide) hipLaunchKernelGGL((client_gather_kernel<false, true, true>), ggrid, gblock, 0, s, a);
+            else if (pl.vec) hipLaunchKernelGGL((client_gather_kernel<false, true, false>), ggrid, gblock, 0, s, a);
+            else hipLaunchKernelGGL((client_gather_kernel<false, false, false>), ggrid, gblock, 0, s, a);
         }
         return hipGetLastError();
     }

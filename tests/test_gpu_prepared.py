@@ -38,7 +38,8 @@ def _dense(N, idx, val):
 # above it (Nx = 16500, Ny = 18000: the syndromes take their own launches),
 # several noise vectors and challenges, ragged column blocks of the 4-byte
 # gathers (64 columns per item: up to 1024 items, or m, n not multiples of 4)
-# and of the 16-byte ones (95, 96: 256 columns per item).
+# and of the 16-byte ones (95, 96: 256 columns per item; 97: the separate
+# gather launch with 1024-column items, ragged in m and n).
 PREP = [
     (80, 256, 256, 1, 2, 2, 8, 2),
     (81, 1000, 700, 3, 3, 2, 17, 3),
@@ -48,6 +49,7 @@ PREP = [
     (85, 1001, 703, 3, 3, 2, 17, 3),
     (95, 1000, 300, 70, 2, 2, 9, 2),
     (96, 2048, 1000, 40, 2, 2, 9, 3),
+    (97, 11008, 4100, 32, 2, 2, 16, 2),
 ]
 
 

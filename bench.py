@@ -219,6 +219,9 @@ def parse():
                     help="the same split for the single-matrix workloads' pipelined schedule (0: none; with 64 "
                          "their preparation, which outweighs the server call at 11008x4096 B=16 and "
                          "28672x8192 B=64, became the bound)")
+    ap.add_argument("--client-turn", type=int, default=1, choices=[0, 1],
+                    help="single-matrix pipelined schedule: one launch per step for the response's "
+                         "decode/verify and the next query's masked encode (1), or separate launches (0)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the run, copy a buffer of this many MiB (reference for the traffic counters)")
     ap.add_argument("--seed", type=int, default=2609)
@@ -431,7 +434,8 @@ def config_bench(args, name, steps, warmup, cpu_seconds, large=False):
         s_prep, s_on = cu_streams[0].stream, cu_streams[1].stream
     else:
         s_prep, s_on = torch.cuda.Stream(), torch.cuda.Stream()
-    pXh = torch.empty((B, n), dtype=torch.int32, device=dev)
+    pXhs = [torch.empty((B, n), dtype=torch.int32, device=dev) for _ in range(2)]
+    pXh = pXhs[0]
     pYh = torch.empty((B, m), dtype=torch.int32, device=dev)
     pY = torch.empty((B, m), dtype=torch.int32, device=dev)
 
@@ -439,18 +443,40 @@ def config_bench(args, name, steps, warmup, cpu_seconds, large=False):
         j = i % pool
         mvk.client_prepare(keys[j], EXI[i], EXV[i], EYI[i], EYV[i], out=preps[i], done_flag=flags[i])
 
-    def online(i):
-        j = i % pool
-        mvk.encode_masked(keys[j], X[i], preps[i], out=pXh, ready_flag=flags[i], timeout_us=50_000, timed_out=late)
-        mvk.server_eval(Ws[j], pXh, out=pYh, path=args.path)
-        mvk.decode_verify_masked(keys[j], pXh, pYh, preps[i], Y=pY, accept=ACC2[i])
+    def online(seq):
+        """The online part of the steps in seq.  Client turns (default): the
+        first masked encode, then per step the server call and one launch
+        with this response's decode/verify and the next query's masked encode
+        (the queries are independent), two X^ buffers in turn; else three
+        launches per step."""
+        if not args.client_turn or not seq:
+            for i in seq:
+                j = i % pool
+                mvk.encode_masked(keys[j], X[i], preps[i], out=pXh, ready_flag=flags[i], timeout_us=50_000,
+                                  timed_out=late)
+                mvk.server_eval(Ws[j], pXh, out=pYh, path=args.path)
+                mvk.decode_verify_masked(keys[j], pXh, pYh, preps[i], Y=pY, accept=ACC2[i])
+            return pXh
+        i0 = seq[0]
+        mvk.encode_masked(keys[i0 % pool], X[i0], preps[i0], out=pXhs[0], ready_flag=flags[i0], timeout_us=50_000,
+                          timed_out=late)
+        for k, i in enumerate(seq):
+            j, cur = i % pool, pXhs[k % 2]
+            mvk.server_eval(Ws[j], cur, out=pYh, path=args.path)
+            if k + 1 < len(seq):
+                i1 = seq[k + 1]
+                mvk.decode_verify_encode_masked(keys[j], cur, pYh, preps[i], X[i1], preps[i1], Y=pY, accept=ACC2[i],
+                                                out_next=pXhs[(k + 1) % 2], ready_flag=flags[i1], timeout_us=50_000,
+                                                timed_out=late)
+            else:
+                mvk.decode_verify_masked(keys[j], cur, pYh, preps[i], Y=pY, accept=ACC2[i])
+        return pXhs[(len(seq) - 1) % 2]
 
     for i in range(warmup):  # also sizes the library's per-stream workspaces
         with torch.cuda.stream(s_prep):
             prepare(i)
-    for i in range(warmup):
-        with torch.cuda.stream(s_on):
-            online(i)
+    with torch.cuda.stream(s_on):
+        online(list(range(warmup)))
     torch.cuda.synchronize()
     steps_t = list(range(warmup, total_steps))
     g_prep, g_on = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
@@ -458,8 +484,7 @@ def config_bench(args, name, steps, warmup, cpu_seconds, large=False):
         for i in steps_t:
             prepare(i)
     with torch.cuda.graph(g_on, stream=s_on):
-        for i in steps_t:
-            online(i)
+        last_xh = online(steps_t)
 
     def replay_pipelined():
         # The preparation graph is submitted first: HIP multiplexes streams onto
@@ -480,7 +505,7 @@ def config_bench(args, name, steps, warmup, cpu_seconds, large=False):
     accepted_pipe = bool((ACC2[warmup:] == 1).all().item()) and int(late.item()) == 0
     # the last timed step again through the one-call path: same Xhat, Yhat, Y
     i_last = steps_t[-1]
-    got = (pXh.clone(), pYh.clone(), pY.clone())
+    got = (last_xh.clone(), pYh.clone(), pY.clone())
     with torch.cuda.stream(s_on):
         rXh = mvk.encode(keys[i_last % pool], X[i_last], EXI[i_last], EXV[i_last])
         rYh = mvk.server_eval(Ws[i_last % pool], rXh, path=args.path)
@@ -512,7 +537,7 @@ def config_bench(args, name, steps, warmup, cpu_seconds, large=False):
         "value": macs * steps / elapsed, "unit": "modMAC/s", "steps": steps, "warmup": warmup,
         "ms_per_step": 1e3 * elapsed / steps, "mode": args.mode,
         "ms_per_step_pipelined": 1e3 * elapsed_pipe / steps, "ms_per_step_serial": 1e3 * elapsed_serial / steps,
-        "prep_cus": args.config_prep_cus,
+        "prep_cus": args.config_prep_cus, "client_turn": bool(args.client_turn),
         "w_pool": pool, "weights": args.weights, "launch": "eager" if args.eager else "hip_graph",
         "chains": C if args.mode == "serial" else 1,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",

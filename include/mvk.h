@@ -53,7 +53,7 @@ extern "C" {
 
 #define MVK_PRIME 2147483647u
 #define MVK_PRIME_BABYBEAR 2013265921u
-#define MVK_ABI_VERSION 8
+#define MVK_ABI_VERSION 9
 
 typedef int32_t mvk_status;
 #define MVK_OK 0
@@ -385,6 +385,28 @@ mvk_status mvk_decode_verify_masked(const mvk_key *key, const uint32_t *Xhat, co
                                     uint32_t B, const uint32_t *My, uint32_t ell, const uint32_t *R,
                                     const uint32_t *U, uint32_t *Y, uint32_t *vL, uint32_t *vR,
                                     uint32_t *accept, void *stream);
+
+/*
+ * One client turn between two server calls of independent queries (the
+ * standard mode of Sec. 7, where the client's work for the next query runs
+ * while the server is busy): mvk_decode_verify_masked of one response and
+ * mvk_encode_masked of the next query in one launch when the decode/verify
+ * is small (B (m + n) <= 32768, ell <= 4), else as the two calls.
+ *   key, Xhat, Yhat, B, My, ell, R, U, Y, vL, vR, accept: as
+ *       mvk_decode_verify_masked (the response of the current query)
+ *   X_next, B_next, Mx_next, Xhat_next, ready_flag, ready_value, timeout_us,
+ *       timed_out: as mvk_encode_masked with the same key (the next query;
+ *       B_next may be 0 with no ready_flag: no next query)
+ * Same outputs, bit for bit, as the two calls.
+ * Errors: as the two calls.
+ */
+mvk_status mvk_decode_verify_encode_masked(const mvk_key *key, const uint32_t *Xhat, const uint32_t *Yhat,
+                                           uint32_t B, const uint32_t *My, uint32_t ell, const uint32_t *R,
+                                           const uint32_t *U, uint32_t *Y, uint32_t *vL, uint32_t *vR,
+                                           uint32_t *accept, const uint32_t *X_next, uint32_t B_next,
+                                           const uint32_t *Mx_next, uint32_t *Xhat_next, uint32_t *ready_flag,
+                                           uint32_t ready_value, uint32_t timeout_us, uint32_t *timed_out,
+                                           void *stream);
 
 /*
  * mvk_decode_verify_masked for G <= MVK_MAX_GROUP matrices that share the

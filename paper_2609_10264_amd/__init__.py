@@ -438,6 +438,39 @@ def decode_verify_masked(key: Key, Xhat: torch.Tensor, Yhat: torch.Tensor, prep:
     return Y, accept, vL, vR
 
 
+def decode_verify_encode_masked(key: Key, Xhat: torch.Tensor, Yhat: torch.Tensor, prep: Prepared,
+                                X_next: torch.Tensor, prep_next: Prepared, Y: torch.Tensor | None = None,
+                                vL: torch.Tensor | None = None, vR: torch.Tensor | None = None,
+                                accept: torch.Tensor | None = None, out_next: torch.Tensor | None = None,
+                                ready_flag: torch.Tensor | None = None, ready_value: int = 1,
+                                timeout_us: int = 200000, timed_out: torch.Tensor | None = None, stream=None):
+    """One client turn for independent queries: decode_verify_masked of this
+    response and encode_masked of the next query (one launch where the
+    decode/verify is small).  Returns (Y, accept, vL, vR, Xhat_next)."""
+    B, ell = Xhat.shape[0], prep.ell
+    Bn = X_next.shape[0]
+    dev = Xhat.device
+    if Y is None:
+        Y = torch.empty((B, key.m), dtype=torch.int32, device=dev)
+    if accept is None:
+        accept = torch.empty((B,), dtype=torch.int32, device=dev)
+    if out_next is None:
+        out_next = torch.empty_like(X_next)
+    ks = key.struct()
+    vLp = _dev(vL, torch.int32, (ell, B), "vL") if vL is not None else None
+    vRp = _dev(vR, torch.int32, (ell, B), "vR") if vR is not None else None
+    _lib.check("mvk_decode_verify_encode_masked", _lib.load(key.p).mvk_decode_verify_encode_masked(
+        ctypes.byref(ks), _dev(Xhat, torch.int32, (B, key.n), "Xhat"), _dev(Yhat, torch.int32, (B, key.m), "Yhat"),
+        B, _dev(prep.My, torch.int32, (B, key.m), "My"), ell, _dev(prep.R, torch.int32, (ell, key.m), "R"),
+        _dev(prep.U, torch.int32, (ell, key.n), "U"), _dev(Y, torch.int32, (B, key.m), "Y"), vLp, vRp,
+        _dev(accept, torch.int32, (B,), "accept"), _dev(X_next, torch.int32, (Bn, key.n), "X_next"), Bn,
+        _dev(prep_next.Mx, torch.int32, (Bn, key.n), "Mx_next"), _dev(out_next, torch.int32, (Bn, key.n), "Xhat_next"),
+        _dev(ready_flag, torch.int32, (), "ready_flag") if ready_flag is not None else None, ready_value,
+        timeout_us, _dev(timed_out, torch.int32, (), "timed_out") if timed_out is not None else None,
+        _stream(stream)))
+    return Y, accept, vL, vR, out_next
+
+
 def decode_verify_masked_group(keys: list, Xhat: torch.Tensor, Yhats: list, preps: list, Ys: list | None = None,
                                vLs: list | None = None, vRs: list | None = None, accepts: list | None = None,
                                stream=None):

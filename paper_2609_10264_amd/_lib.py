@@ -32,7 +32,7 @@ MVK_SEEDED_MAX_T = 4096
 MVK_STATIC_SCRATCH_BYTES = 32 << 20
 MVK_MAX_GROUP = 4
 MVK_MAX_PREP = 8
-ABI_VERSION = 8
+ABI_VERSION = 9
 # field modulus -> library built over that field
 LIB_PATHS = {MVK_PRIME: LIB_PATH, MVK_PRIME_BABYBEAR: LIB_PATH_BB}
 
@@ -80,6 +80,7 @@ EXPORTS = (
     "mvk_client_prepare_multi",
     "mvk_stream_create_cu_range",
     "mvk_stream_destroy",
+    "mvk_decode_verify_encode_masked",
 )
 
 
@@ -233,6 +234,9 @@ def load(p: int = MVK_PRIME) -> ctypes.CDLL:
     L.mvk_stream_create_cu_range.restype = st
     L.mvk_stream_destroy.argtypes = [vp]
     L.mvk_stream_destroy.restype = st
+    L.mvk_decode_verify_encode_masked.argtypes = [ctypes.POINTER(MvkKey), vp, vp, u32, vp, u32, vp, vp, vp, vp, vp,
+                                                  vp, vp, u32, vp, vp, vp, u32, u32, vp, vp]
+    L.mvk_decode_verify_encode_masked.restype = st
     if L.mvk_abi_version() != ABI_VERSION:
         raise ImportError(f"{path}: ABI version mismatch; rebuild the library")
     if L.mvk_field_modulus() != p:

@@ -738,6 +738,42 @@ mvk_status mvk_decode_verify_masked(const mvk_key* key, const uint32_t* Xhat, co
                                                   accept, s));
 }
 
+mvk_status mvk_decode_verify_encode_masked(const mvk_key* key, const uint32_t* Xhat, const uint32_t* Yhat,
+                                           uint32_t B, const uint32_t* My, uint32_t ell, const uint32_t* R,
+                                           const uint32_t* U, uint32_t* Y, uint32_t* vL, uint32_t* vR,
+                                           uint32_t* accept, const uint32_t* X_next, uint32_t B_next,
+                                           const uint32_t* Mx_next, uint32_t* Xhat_next, uint32_t* ready_flag,
+                                           uint32_t ready_value, uint32_t timeout_us, uint32_t* timed_out,
+                                           void* stream) {
+    mvk_status st = check_key(key);
+    if (st) return st;
+    if (ready_flag && (ready_value == 0 || timeout_us == 0)) return MVK_EINVAL;
+    if (B_next && (!X_next || !Mx_next || !Xhat_next)) return MVK_EINVAL;
+    if (B == 0)
+        return mvk_encode_masked(key, X_next, B_next, Mx_next, Xhat_next, ready_flag, ready_value, timeout_us,
+                                 timed_out, stream);
+    if (B_next == 0 && !ready_flag)
+        return mvk_decode_verify_masked(key, Xhat, Yhat, B, My, ell, R, U, Y, vL, vR, accept, stream);
+    if (!Xhat || !Yhat || !My || !R || !U || !Y || !accept || ell == 0) return MVK_EINVAL;
+    if (ell > kMaxEll || B > 65535u) return MVK_ERANGE;
+    hipStream_t s = (hipStream_t)stream;
+    if (validate_mode() &&
+        (st = check_all(s, {{Xhat, (size_t)B * key->n}, {Yhat, (size_t)B * key->m}, {My, (size_t)B * key->m},
+                            {R, (size_t)ell * key->m}, {U, (size_t)ell * key->n}, {X_next, (size_t)B_next * key->n},
+                            {ready_flag ? nullptr : Mx_next, (size_t)B_next * key->n}})))
+        return st;
+    void* ws = nullptr;
+    uint32_t* ctrl = nullptr;
+    // the decode/verify's control words from word 0, the masked encode's
+    // counter at word kPrepCounterWord (a word those layouts leave unused)
+    st = workspace(s, 0, &ws, &ctrl,
+                   std::max(dv_ctrl_bytes(key->m, key->n, B, ell), (size_t)4 * (kPrepCounterWord + 1)));
+    if (st) return st;
+    return hip_status(launch_client_turn(key->m, key->n, Xhat, Yhat, B, My, ell, R, U, Y, ctrl, vL, vR, accept,
+                                         X_next, Mx_next, (size_t)B_next * key->n, Xhat_next, ready_flag,
+                                         ready_value, timeout_us, timed_out, &ctrl[kPrepCounterWord], s));
+}
+
 mvk_status mvk_decode_verify_masked_group(uint32_t G, const mvk_key* const* keys, const uint32_t* Xhat, uint32_t B,
                                           const uint32_t* const* Yhat, const uint32_t* const* My, uint32_t ell,
                                           const uint32_t* const* R, const uint32_t* const* U, uint32_t* const* Y,

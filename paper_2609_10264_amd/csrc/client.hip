@@ -22,6 +22,7 @@
 
 #include "count.h"
 #include "field.h"
+#include "masks.h"
 #include "mvk_internal.h"
 #include "syn_block.h"
 
@@ -467,17 +468,18 @@ __global__ __launch_bounds__(kFusedThreads) void decode_verify_syn(
 // ell <= EL.
 constexpr int kSmallThreads = 1024;
 template <int EL, int PER>
-__global__ __launch_bounds__(kSmallThreads) void decode_verify_small(
-    uint32_t m, uint32_t n, const uint32_t* __restrict__ Xhat, const uint32_t* __restrict__ Yhat, uint32_t B,
-    const uint32_t* __restrict__ My, uint32_t ell, const uint32_t* __restrict__ R, const uint32_t* __restrict__ U,
-    uint32_t* __restrict__ Y, unsigned long long* acc, uint32_t* counter, uint32_t* __restrict__ vL,
-    uint32_t* __restrict__ vR, uint32_t* __restrict__ accept) {
+__device__ __forceinline__ void dv_small_body(
+    uint32_t bid, uint32_t G, uint32_t m, uint32_t n, const uint32_t* __restrict__ Xhat,
+    const uint32_t* __restrict__ Yhat, uint32_t B, const uint32_t* __restrict__ My, uint32_t ell,
+    const uint32_t* __restrict__ R, const uint32_t* __restrict__ U, uint32_t* __restrict__ Y,
+    unsigned long long* acc, uint32_t* counter, uint32_t* __restrict__ vL, uint32_t* __restrict__ vR,
+    uint32_t* __restrict__ accept) {
     constexpr int NW = kSmallThreads / 64;
     __shared__ uint64_t red[NW][2 * EL];
     __shared__ uint32_t fin[2 * EL];
     __shared__ uint32_t last;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const uint32_t G = gridDim.x, gt = blockIdx.x * kSmallThreads + (uint32_t)tid;
+    const uint32_t gt = bid * kSmallThreads + (uint32_t)tid;
     const uint32_t stride = G * kSmallThreads, pass = stride * PER;
     const uint32_t len = m > n ? m : n;
     for (uint32_t b = 0; b < B; ++b) {
@@ -571,6 +573,37 @@ __global__ __launch_bounds__(kSmallThreads) void decode_verify_small(
         accept[b] = ok;
     }
     if (tid == 0) atomicExch(counter, 0u);
+}
+
+template <int EL, int PER>
+__global__ __launch_bounds__(kSmallThreads) void decode_verify_small(
+    uint32_t m, uint32_t n, const uint32_t* __restrict__ Xhat, const uint32_t* __restrict__ Yhat, uint32_t B,
+    const uint32_t* __restrict__ My, uint32_t ell, const uint32_t* __restrict__ R, const uint32_t* __restrict__ U,
+    uint32_t* __restrict__ Y, unsigned long long* acc, uint32_t* counter, uint32_t* __restrict__ vL,
+    uint32_t* __restrict__ vR, uint32_t* __restrict__ accept) {
+    dv_small_body<EL, PER>(blockIdx.x, gridDim.x, m, n, Xhat, Yhat, B, My, ell, R, U, Y, acc, counter, vL, vR,
+                           accept);
+}
+
+// One client turn between two server calls of independent queries: the
+// decode/verify of one response (dv_small_body, workgroups [0, Gd)) and the
+// masked encode of the next query (add_masks_body, the other workgroups, with
+// the optional wait for its preparation's flag) in one launch.  The two roles
+// share no data.
+template <int EL, int PER, bool WAIT>
+__global__ __launch_bounds__(kSmallThreads) void client_turn(
+    uint32_t Gd, uint32_t m, uint32_t n, const uint32_t* __restrict__ Xhat, const uint32_t* __restrict__ Yhat,
+    uint32_t B, const uint32_t* __restrict__ My, uint32_t ell, const uint32_t* __restrict__ R,
+    const uint32_t* __restrict__ U, uint32_t* __restrict__ Y, unsigned long long* acc, uint32_t* counter,
+    uint32_t* __restrict__ vL, uint32_t* __restrict__ vR, uint32_t* __restrict__ accept, const uint32_t* Xn,
+    const uint32_t* __restrict__ Mxn, size_t countn, uint32_t* Xhatn, uint32_t* flag, uint32_t value,
+    uint64_t ticks, uint32_t* timed_out, uint32_t* add_counter) {
+    static_assert(kSmallThreads == kAddThreads, "the two roles run in workgroups of one size");
+    if (blockIdx.x < Gd)
+        dv_small_body<EL, PER>(blockIdx.x, Gd, m, n, Xhat, Yhat, B, My, ell, R, U, Y, acc, counter, vL, vR, accept);
+    else
+        add_masks_body<WAIT, 4>(blockIdx.x - Gd, gridDim.x - Gd, Xn, Mxn, countn, Xhatn, flag, value, ticks,
+                                timed_out, add_counter);
 }
 
 // Transpose-reduction mod p of V values per lane over the 64 lanes of a wave:
@@ -1048,6 +1081,46 @@ hipError_t launch_decode_verify_masked(uint32_t m, uint32_t n, const uint32_t* X
     hipLaunchKernelGGL((decode_verify_fused<true, 1>), dim3(grid), dim3(kB), 0, s, nullptr, nullptr, m, n, 0u, 0u,
                        Xhat, Yhat, B, nullptr, nullptr, 0u, nullptr, nullptr, 0u, ell, r, Y, acc,
                        acc + (size_t)ell * B * l.nsub, l.nsub, nblkR, ctrl, count_slots(grid), vL, vR, accept, My, U);
+    return hipGetLastError();
+}
+
+hipError_t launch_client_turn(uint32_t m, uint32_t n, const uint32_t* Xhat, const uint32_t* Yhat, uint32_t B,
+                              const uint32_t* My, uint32_t ell, const uint32_t* r, const uint32_t* U, uint32_t* Y,
+                              uint32_t* ctrl, uint32_t* vL, uint32_t* vR, uint32_t* accept, const uint32_t* Xn,
+                              const uint32_t* Mxn, size_t countn, uint32_t* Xhatn, uint32_t* flag, uint32_t value,
+                              uint32_t timeout_us, uint32_t* timed_out, uint32_t* add_counter, hipStream_t s) {
+    if (ell == 0 || ell > (uint32_t)kMaxEll) return hipErrorInvalidValue;
+    if (!takes_small(m, n, B, ell) || countn == 0) {
+        // larger problems: the two steps as their own launches
+        hipError_t e = launch_decode_verify_masked(m, n, Xhat, Yhat, B, My, ell, r, U, Y, ctrl, vL, vR, accept, s);
+        if (e == hipSuccess)
+            e = launch_add_masks(Xn, Mxn, countn, Xhatn, flag, value, timeout_us, timed_out, add_counter, s);
+        return e;
+    }
+    const DvLayout l = dv_layout(m, n, B, ell);
+    unsigned long long* acc = reinterpret_cast<unsigned long long*>(ctrl + l.acc_word);
+    // decode/verify workgroups as launch_decode_verify_masked's small form,
+    // masked-encode workgroups as launch_add_masks'
+    const uint32_t len = m > n ? m : n;
+    uint32_t Gd = ceil_div(len, 4u * kSmallThreads);
+    Gd = Gd < 1u ? 1u : (Gd > 8u ? 8u : Gd);
+    size_t Ga = (countn + 4u * kAddThreads - 1) / (4u * kAddThreads);
+    Ga = Ga > 256 ? 256 : (Ga == 0 ? 1 : Ga);
+    uint64_t ticks = 0;
+    if (flag) {
+        const hipError_t e = wait_ticks(timeout_us, &ticks);
+        if (e != hipSuccess) return e;
+    }
+    const dim3 grid(Gd + (uint32_t)Ga), block(kSmallThreads);
+#define MVK_TURN(EL, W)                                                                                          \
+    hipLaunchKernelGGL((client_turn<EL, 4, W>), grid, block, 0, s, Gd, m, n, Xhat, Yhat, B, My, ell, r, U, Y, acc, \
+                       ctrl, vL, vR, accept, Xn, Mxn, countn, Xhatn, flag, value, ticks, timed_out, add_counter)
+    if (ell <= 2) {
+        if (flag) MVK_TURN(2, true); else MVK_TURN(2, false);
+    } else {
+        if (flag) MVK_TURN(4, true); else MVK_TURN(4, false);
+    }
+#undef MVK_TURN
     return hipGetLastError();
 }
 

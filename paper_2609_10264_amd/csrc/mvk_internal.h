@@ -131,6 +131,15 @@ hipError_t launch_decode_verify_masked(uint32_t m, uint32_t n, const uint32_t* X
 // problem takes the wide kernel, else one per problem); ctrl: G control
 // regions of dv_group_ctrl_stride words each.  vL, vR may be null.
 size_t dv_group_ctrl_stride(uint32_t m, uint32_t n, uint32_t B, uint32_t ell);
+// The decode/verify of one response and the masked encode of the next,
+// independent query in one launch where the decode/verify takes its small
+// form (else two launches); ctrl as launch_decode_verify_masked, add_counter
+// as launch_add_masks (distinct words).
+hipError_t launch_client_turn(uint32_t m, uint32_t n, const uint32_t* Xhat, const uint32_t* Yhat, uint32_t B,
+                              const uint32_t* My, uint32_t ell, const uint32_t* r, const uint32_t* U, uint32_t* Y,
+                              uint32_t* ctrl, uint32_t* vL, uint32_t* vR, uint32_t* accept, const uint32_t* Xn,
+                              const uint32_t* Mxn, size_t countn, uint32_t* Xhatn, uint32_t* flag, uint32_t value,
+                              uint32_t timeout_us, uint32_t* timed_out, uint32_t* add_counter, hipStream_t s);
 hipError_t launch_decode_verify_masked_group(uint32_t G, uint32_t m, uint32_t n, const uint32_t* Xhat, uint32_t B,
                                              const uint32_t* const* Yhat, const uint32_t* const* My, uint32_t ell,
                                              const uint32_t* const* R, const uint32_t* const* U, uint32_t* const* Y,

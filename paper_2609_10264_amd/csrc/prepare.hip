@@ -13,6 +13,7 @@
 // separate HIP graphs.
 #include "count.h"
 #include "field.h"
+#include "masks.h"
 #include "mvk_internal.h"
 #include "syn_block.h"
 
@@ -365,17 +366,6 @@ __global__ __launch_bounds__(kQuarter) void client_gather_kernel(PrepArgs a) {
     }
 }
 
-// Polls *flag (device-coherent loads, a short sleep between polls) from the
-// calling thread until it holds `value`; false after `ticks` of the constant
-// wall clock.
-__device__ __forceinline__ bool poll_flag(const uint32_t* flag, uint32_t value, uint64_t ticks) {
-    const uint64_t t0 = wall_clock64();
-    while (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != value) {
-        if (wall_clock64() - t0 > ticks) return false;
-        __builtin_amdgcn_s_sleep(4);
-    }
-    return true;
-}
 
 // out[v][i] = sum_s val[v*t + s] * M[idx[v*t + s], i] for `count` sparse
 // vectors v (M: nrows x ld): nb = ceil(ld / gather_cols(VEC)) items per
@@ -395,68 +385,11 @@ __global__ __launch_bounds__(kPrepThreads) void gather_rows_kernel(const uint32_
                             cb * gather_cols(VEC), live, part + quarter * gather_part(VEC));
 }
 
-// Xhat = X + Mx, element-wise over count words, PER words per thread and
-// pass with the pass's loads issued first.  WAIT: the loads of X (the query,
-// not covered by the flag) are issued before thread 0 of each workgroup
-// polls *flag for `value`; Mx is read device-coherently after it.  The flag
-// is cleared by the only workgroup, or, with several, by the last one to
-// finish (counted on `counter`, which it also clears).
-constexpr int kAddThreads = 1024;
 template <bool WAIT, int PER>
 __global__ __launch_bounds__(kAddThreads) void add_masks(const uint32_t* X, const uint32_t* __restrict__ Mx,
                                                          size_t count, uint32_t* Xhat, uint32_t* flag, uint32_t value,
                                                          uint64_t ticks, uint32_t* timed_out, uint32_t* counter) {
-    const size_t stride = (size_t)gridDim.x * kAddThreads, pass = stride * PER;
-    const size_t g = (size_t)blockIdx.x * kAddThreads + threadIdx.x;
-    bool polled = !WAIT;
-    for (size_t base = 0; base < count; base += pass) {
-        uint32_t xv[PER], mv[PER];
-#pragma unroll
-        for (int u = 0; u < PER; ++u) {
-            const size_t i = base + g + stride * u;
-            xv[u] = X[i < count ? i : count - 1];
-        }
-        if (WAIT && !polled) {  // first pass only (uniform)
-            if (threadIdx.x == 0) {
-                if (!poll_flag(flag, value, ticks)) {
-                    if (timed_out) atomicOr(timed_out, 1u);
-                } else if (gridDim.x == 1) {
-                    __hip_atomic_store(flag, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                }
-            }
-            __syncthreads();
-            polled = true;
-        }
-#pragma unroll
-        for (int u = 0; u < PER; ++u) {
-            const size_t i = base + g + stride * u, is = i < count ? i : count - 1;
-            mv[u] = WAIT ? __hip_atomic_load(&Mx[is], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : Mx[is];
-        }
-        uint32_t out[PER];
-#pragma unroll
-        for (int u = 0; u < PER; ++u) {
-            out[u] = fadd(xv[u], mv[u]);
-            // pinned in a register before the guarded store, so that the
-            // compiler does not sink the loads into the branch
-            asm volatile("" : "+v"(out[u]));
-        }
-#pragma unroll
-        for (int u = 0; u < PER; ++u) {
-            const size_t i = base + g + stride * u;
-            if (i < count) Xhat[i] = out[u];
-        }
-    }
-    if constexpr (WAIT) {
-        if (!polled) {  // no pass at all (count == 0): still consume the flag
-            if (threadIdx.x == 0 && !poll_flag(flag, value, ticks) && timed_out) atomicOr(timed_out, 1u);
-            if (threadIdx.x == 0 && gridDim.x == 1)
-                __hip_atomic_store(flag, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-        if (gridDim.x > 1 && threadIdx.x == 0 && atomicAdd(counter, 1u) == gridDim.x - 1) {
-            atomicExch(counter, 0u);
-            __hip_atomic_store(flag, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-    }
+    add_masks_body<WAIT, PER>(blockIdx.x, gridDim.x, X, Mx, count, Xhat, flag, value, ticks, timed_out, counter);
 }
 
 __global__ void flag_signal_kernel(uint32_t* flag, uint32_t value) {
@@ -475,16 +408,6 @@ __global__ void flag_wait_kernel(uint32_t* flag, uint32_t value, uint64_t ticks,
     __hip_atomic_store(flag, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Wall-clock ticks of timeout_us on the current device.
-hipError_t wait_ticks(uint32_t timeout_us, uint64_t* ticks) {
-    int dev = 0, khz = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e == hipSuccess) e = hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev);
-    if (e != hipSuccess) return e;
-    if (khz <= 0) return hipErrorInvalidValue;
-    *ticks = (uint64_t)timeout_us * (uint64_t)khz / 1000u;
-    return hipSuccess;
-}
 
 // Syndrome tile per thread of a 1024-thread workgroup for block length N
 // (0: above kSynScratchAbove, not in this launch).

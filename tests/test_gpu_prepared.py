@@ -171,6 +171,50 @@ def test_flags_order_compute_unit_streams():
         b.close()
 
 
+@pytest.mark.parametrize("cid,m,n,B,r,tx,ell", [(98, 4096, 4096, 1, 3, 64, 2), (99, 1000, 700, 3, 3, 17, 3),
+                                                (100, 3000, 2000, 8, 2, 16, 2), (101, 12000, 300, 2, 2, 9, 2)])
+def test_client_turn_matches_two_calls(cid, m, n, B, r, tx, ell):
+    """decode_verify_encode_masked (the decode/verify of one response and the
+    masked encode of the next query in one launch; 12000 x 300, B = 2: three
+    decode/verify workgroups; 3000 x 2000, B = 8: the two-launch form) gives
+    the outputs of
+    decode_verify_masked and encode_masked, with a tampered column rejected;
+    and a turn whose next query waits for a flag set on another stream."""
+    print(f"client turn cid={cid} m={m} n={n} B={B} ell={ell}", flush=True)
+    inst = Instance(cid, m, n, B, r, tx, ty=31, ell=ell).to_device()
+    mvk.keygen(inst.key, inst.dW)
+    prep = mvk.client_prepare(inst.key, inst.dexi, inst.dexv, inst.deyi, inst.deyv)
+    nxt = Instance(cid + 50, m, n, B, r, tx, ty=31, ell=ell).to_device()
+    prep2 = mvk.client_prepare(inst.key, nxt.dexi, nxt.dexv, nxt.deyi, nxt.deyv)
+    Xh = mvk.encode_masked(inst.key, inst.dX, prep)
+    Yh = mvk.server_eval(inst.dW, Xh)
+    Yh[B - 1, m // 3] = (Yh[B - 1, m // 3].to(torch.int64) + 99) % P
+    vL, vR = (torch.empty((ell, B), dtype=torch.int32, device="cuda") for _ in range(2))
+    Y, acc, _, _, Xh2 = mvk.decode_verify_encode_masked(inst.key, Xh, Yh, prep, nxt.dX, prep2, vL=vL, vR=vR)
+    vL1, vR1 = (torch.empty((ell, B), dtype=torch.int32, device="cuda") for _ in range(2))
+    Y1, acc1, _, _ = mvk.decode_verify_masked(inst.key, Xh, Yh, prep, vL=vL1, vR=vR1)
+    Xh21 = mvk.encode_masked(inst.key, nxt.dX, prep2)
+    torch.cuda.synchronize()
+    for a, b in ((Y, Y1), (acc, acc1), (vL, vL1), (vR, vR1), (Xh2, Xh21)):
+        assert torch.equal(a, b)
+    assert host(acc).tolist() == [1] * (B - 1) + [0]
+    # the next query's mask prepared on another stream, ordered by a flag
+    flag = torch.zeros((), dtype=torch.int32, device="cuda")
+    late = torch.zeros((), dtype=torch.int32, device="cuda")
+    side, main = torch.cuda.Stream(), torch.cuda.Stream()
+    prep3 = mvk.Prepared(inst.key, B, ell)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(side):
+        mvk.client_prepare(inst.key, nxt.dexi, nxt.dexv, nxt.deyi, nxt.deyv, out=prep3, done_flag=flag,
+                           stream=side)
+    with torch.cuda.stream(main):
+        _, _, _, _, Xh3 = mvk.decode_verify_encode_masked(inst.key, Xh, Yh, prep, nxt.dX, prep3, ready_flag=flag,
+                                                         timeout_us=2_000_000, timed_out=late, stream=main)
+    torch.cuda.synchronize()
+    assert int(late.item()) == 0 and int(flag.item()) == 0
+    assert torch.equal(Xh3, Xh21)
+
+
 def test_pipelined_graphs_match_one_call_path():
     """The pipelined standard mode as two HIP graphs (preparation stream ahead of
     the online stream, ordered by flags) against the one-call path, per step."""

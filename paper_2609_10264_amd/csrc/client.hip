@@ -621,8 +621,13 @@ __device__ __forceinline__ uint32_t wave_xreduce_mod(uint32_t (&a)[V], int lane)
         const bool up = (lane & s) != 0;
 #pragma unroll
         for (int i = 0; i < half; ++i) {
-            const uint32_t send = up ? a[i] : a[i + half];
-            const uint32_t keep = up ? a[i + half] : a[i];
+            // the two values pinned in registers: otherwise the compiler turns
+            // the pair of selects into a select of the array index, which it
+            // then expands into compare-and-select chains over the whole array
+            uint32_t lo = a[i], hi = a[i + half];
+            asm volatile("" : "+v"(lo), "+v"(hi));
+            const uint32_t send = up ? lo : hi;
+            const uint32_t keep = up ? hi : lo;
             a[i] = fadd(keep, (uint32_t)__shfl_xor((int)send, s));
         }
     }
@@ -828,6 +833,124 @@ __global__ __launch_bounds__(kSmallThreads) void decode_verify_col(uint32_t m, u
     }
 }
 
+// decode_verify_masked for up to CB <= 8 query columns, spread over the chip
+// (grid S x G, problem g = blockIdx.y): workgroup s takes the elements
+// j = 256 PER s + t + 256 u (u < PER) of thread t for every column at once,
+// so that the challenge vectors r_q and u_q of a segment are read once for
+// all columns: as outputs i (Y_b[i] = Yhat_b[i] - My_b[i] and the v_R terms
+// R_q[i] Yhat_b[i]) and as inputs k (the v_L terms U_q[k] Xhat_b[k]); every
+// load of the workgroup is issued before the first is used (addresses
+// clamped in range, terms masked).  The 2 EL CB sums are reduced mod p across
+// the wave (transpose-reduction) and the waves (LDS) and added into the
+// workgroup's own slot of the control region (no two workgroups share an
+// address, so the device atomics do not queue behind each other); the last
+// of the S workgroups of the problem (count.h) reads and clears every slot,
+// sums them and writes v_L, v_R and accept.
+constexpr uint32_t kSegMaxB = 8, kSegMaxLen = 65536, kSegMaxSlots = 64, kSegSlotWords = 64;
+template <int EL, int CB, int PER>
+__global__ __launch_bounds__(kWideThreads) void decode_verify_seg(uint32_t m, uint32_t n,
+                                                                  const uint32_t* __restrict__ Xhat, uint32_t B,
+                                                                  uint32_t ell, const DvGroup grp, size_t part_word,
+                                                                  uint32_t* ctrl0, size_t ctrl_stride) {
+    constexpr int NW = kWideThreads / 64, V = 2 * EL * CB, TPV = kWideThreads / V;
+    static_assert(V <= 64, "one wave compares");
+    __shared__ uint32_t red[NW][V];
+    __shared__ uint32_t fin[TPV][V];
+    __shared__ uint32_t last;
+    const uint32_t g = blockIdx.y;
+    const uint32_t* __restrict__ Yhat = grp.Yhat[g];
+    const uint32_t* __restrict__ My = grp.My[g];
+    const uint32_t* __restrict__ R = grp.R[g];
+    const uint32_t* __restrict__ U = grp.U[g];
+    uint32_t* __restrict__ Y = grp.Y[g];
+    uint32_t* ctrl = ctrl0 + g * ctrl_stride;
+    uint32_t* part = ctrl + part_word;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const uint32_t base = blockIdx.x * (uint32_t)(kWideThreads * PER) + (uint32_t)tid;
+    uint32_t rv[EL][PER], uv[EL][PER], yv[CB][PER], mv[CB][PER], xv[CB][PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+        const uint32_t j = base + kWideThreads * u;
+        const uint32_t i = j < m ? j : m - 1, k = j < n ? j : n - 1;
+#pragma unroll
+        for (int q = 0; q < EL; ++q) {
+            const uint32_t qs = (uint32_t)q < ell ? (uint32_t)q : 0u;
+            rv[q][u] = R[(size_t)qs * m + i];
+            uv[q][u] = U[(size_t)qs * n + k];
+        }
+#pragma unroll
+        for (int c = 0; c < CB; ++c) {
+            const uint32_t b = (uint32_t)c < B ? (uint32_t)c : B - 1;
+            yv[c][u] = Yhat[(size_t)b * m + i];
+            mv[c][u] = My[(size_t)b * m + i];
+            xv[c][u] = Xhat[(size_t)b * n + k];
+        }
+    }
+    uint32_t a[V];  // index (c * EL + q) * 2 + side; side 0: v_L, 1: v_R
+#pragma unroll
+    for (int c = 0; c < CB; ++c) {
+        uint64_t l[EL], r[EL];
+#pragma unroll
+        for (int q = 0; q < EL; ++q) l[q] = r[q] = 0;
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+            const uint32_t j = base + kWideThreads * u;
+            // pinned before the guarded store (see decode_verify_small)
+            uint32_t yo = fsub(yv[c][u], mv[c][u]);
+            asm volatile("" : "+v"(yo));
+            if (j < m && (uint32_t)c < B) Y[(size_t)c * m + j] = yo;
+            const uint32_t y = j < m ? yv[c][u] : 0u, x = j < n ? xv[c][u] : 0u;
+#pragma unroll
+            for (int q = 0; q < EL; ++q) {
+                r[q] += ffold((uint64_t)rv[q][u] * y);
+                l[q] += ffold((uint64_t)uv[q][u] * x);
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < EL; ++q) {
+            a[(c * EL + q) * 2] = fred64(l[q]);
+            a[(c * EL + q) * 2 + 1] = fred64(r[q]);
+        }
+    }
+    const uint32_t w = wave_xreduce_mod<V>(a, lane);
+    constexpr int SH = (V == 64) ? 0 : (V == 32) ? 1 : (V == 16) ? 2 : 3;
+    if ((lane & ((1 << SH) - 1)) == 0) red[wave][lane >> SH] = w;
+    __syncthreads();
+    if (tid < V) {
+        uint32_t tot = 0;
+#pragma unroll
+        for (int h = 0; h < NW; ++h) tot = fadd(tot, red[h][tid]);
+        atomicAdd(&part[(size_t)blockIdx.x * kSegSlotWords + tid], tot);  // a zero word before
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (tid == 0) last = count_last(ctrl, 0u) ? 1u : 0u;
+    __syncthreads();
+    if (!last) return;
+    // the last workgroup: TPV threads per value read and clear the slots
+    const uint32_t v = (uint32_t)tid % V, h = (uint32_t)tid / V;
+    uint32_t sum = 0;
+    for (uint32_t s2 = h; s2 < gridDim.x; s2 += TPV)
+        sum = fadd(sum, atomicExch(&part[(size_t)s2 * kSegSlotWords + v], 0u));
+    fin[h][v] = sum;
+    __syncthreads();
+    if (tid < 64) {
+        uint32_t val = 0;
+        if (tid < V)
+#pragma unroll
+            for (int h2 = 0; h2 < TPV; ++h2) val = fadd(val, fin[h2][tid]);
+        const uint32_t other = (uint32_t)__shfl_xor((int)val, 1);
+        const uint32_t side = (uint32_t)tid & 1u, q = ((uint32_t)tid >> 1) % EL, c = ((uint32_t)tid >> 1) / EL;
+        const bool valid = tid < V && q < ell && c < B;
+        if (valid && side == 0 && grp.vL[g]) grp.vL[g][(size_t)q * B + c] = val;
+        if (valid && side == 1 && grp.vR[g]) grp.vR[g][(size_t)q * B + c] = val;
+        // accept of column c: every repetition's v_L equals its v_R
+        const uint64_t bad = __ballot(valid && side == 0 && val != other);
+        if (tid < V && (uint32_t)tid % (2 * EL) == 0 && c < B)
+            grp.accept[g][c] = ((bad >> tid) & ((1ull << (2 * EL)) - 1)) == 0 ? 1u : 0u;
+    }
+}
+
 template <int U, int E>
 int fused_blocks_per_cu() {
     int nb = 0;
@@ -863,6 +986,9 @@ DvLayout dv_layout(uint32_t m, uint32_t n, uint32_t B, uint32_t ell) {
     l.nsub = per <= 32 ? 1u : (per >= 8 * 32 ? 8u : ceil_div(per, 32u));
     l.acc_word = count_words(l.slots);
     l.bytes = l.acc_word * 4 + (size_t)2 * ell * B * l.nsub * 8;
+    // decode_verify_seg's slots in the same place
+    const size_t seg = l.acc_word * 4 + (size_t)kSegMaxSlots * kSegSlotWords * 4;
+    l.bytes = seg > l.bytes ? seg : l.bytes;
     return l;
 }
 }  // namespace
@@ -996,6 +1122,45 @@ bool takes_cols(uint32_t m, uint32_t n, uint32_t B, uint32_t ell) {
     return ell <= 4 && B >= kColsMinB && B <= kColsMaxB && len <= kColsMaxLen && !takes_small(m, n, B, ell);
 }
 
+// decode_verify_seg above the length one workgroup per column takes in one
+// pass (4096) up to kSegMaxLen elements, above the one-workgroup size: 1 to
+// kSegMaxB columns with ell <= 2, 1 to 4 with ell <= 4 (64 sums per thread
+// would spill).  The elements per thread (1, 2 or 4) keep a problem's
+// segments at 32 or fewer where the length allows.  (Eight columns: 7.0 us
+// against 7.5 for one workgroup per column at 4096 x 11008, 7.1 against 7.9
+// for two problems at 11008 x 4096; at 4096 x 4096 5.8 against 5.1.)
+bool takes_seg(uint32_t m, uint32_t n, uint32_t B, uint32_t ell) {
+    const uint32_t len = m > n ? m : n;
+    return ell >= 1 && ell <= 4 && B >= 1 && B <= (ell <= 2 ? kSegMaxB : kSegMaxB / 2) &&
+           len > 4u * kSmallThreads && len <= kSegMaxLen && !takes_small(m, n, B, ell);
+}
+
+hipError_t launch_seg(uint32_t m, uint32_t n, const uint32_t* Xhat, uint32_t B, uint32_t ell, const DvGroup& grp,
+                      uint32_t G, uint32_t* ctrl, size_t ctrl_stride, hipStream_t s) {
+    const DvLayout l = dv_layout(m, n, B, ell);
+    const uint32_t len = m > n ? m : n;
+    uint32_t per = 1;
+    while (per < 4 && ceil_div(len, per * (uint32_t)kWideThreads) > 32) per *= 2;
+    const uint32_t S = ceil_div(len, per * (uint32_t)kWideThreads);
+    if (S > kSegMaxSlots || count_words(0) > l.acc_word ||
+        (size_t)S * kSegSlotWords * 4 > l.bytes - l.acc_word * 4)
+        return hipErrorInvalidValue;  // the layout holds the counter and the slots
+    const dim3 grid(S, G);
+#define MVK_SEG(EL, CB, PER)                                                                               \
+    hipLaunchKernelGGL((decode_verify_seg<EL, CB, PER>), grid, dim3(kWideThreads), 0, s, m, n, Xhat, B, ell, \
+                       grp, l.acc_word, ctrl, ctrl_stride)
+#define MVK_SEG_PER(EL, CB) \
+    if (per == 1) MVK_SEG(EL, CB, 1); else if (per == 2) MVK_SEG(EL, CB, 2); else MVK_SEG(EL, CB, 4)
+    if (ell <= 2) {
+        if (B <= 2) { MVK_SEG_PER(2, 2); } else if (B <= 4) { MVK_SEG_PER(2, 4); } else { MVK_SEG_PER(2, 8); }
+    } else {
+        if (B <= 2) { MVK_SEG_PER(4, 2); } else { MVK_SEG_PER(4, 4); }
+    }
+#undef MVK_SEG_PER
+#undef MVK_SEG
+    return hipGetLastError();
+}
+
 hipError_t launch_cols(uint32_t m, uint32_t n, const uint32_t* Xhat, uint32_t B, uint32_t ell, const DvGroup& grp,
                        uint32_t G, hipStream_t s) {
     const dim3 grid(B, G);
@@ -1037,7 +1202,7 @@ hipError_t launch_decode_verify_masked(uint32_t m, uint32_t n, const uint32_t* X
     const DvLayout l = dv_layout(m, n, B, ell);
     unsigned long long* acc = reinterpret_cast<unsigned long long*>(ctrl + l.acc_word);
     uint32_t* counter = ctrl;
-    if (takes_cols(m, n, B, ell)) {
+    if (takes_seg(m, n, B, ell) || takes_cols(m, n, B, ell)) {
         DvGroup grp{};
         grp.Yhat[0] = Yhat;
         grp.My[0] = My;
@@ -1047,6 +1212,7 @@ hipError_t launch_decode_verify_masked(uint32_t m, uint32_t n, const uint32_t* X
         grp.vL[0] = vL;
         grp.vR[0] = vR;
         grp.accept[0] = accept;
+        if (takes_seg(m, n, B, ell)) return launch_seg(m, n, Xhat, B, ell, grp, 1, ctrl, 0, s);
         return launch_cols(m, n, Xhat, B, ell, grp, 1, s);
     }
     if (takes_small(m, n, B, ell)) {
@@ -1135,7 +1301,7 @@ hipError_t launch_decode_verify_masked_group(uint32_t G, uint32_t m, uint32_t n,
                                              uint32_t* ctrl, hipStream_t s) {
     if (G == 0 || G > kMaxGroup || ell == 0 || ell > (uint32_t)kMaxEll) return hipErrorInvalidValue;
     const size_t stride = dv_group_ctrl_stride(m, n, B, ell);
-    if (takes_cols(m, n, B, ell)) {
+    if (takes_seg(m, n, B, ell) || takes_cols(m, n, B, ell)) {
         DvGroup grp{};
         for (uint32_t g = 0; g < G; ++g) {
             grp.Yhat[g] = Yhat[g];
@@ -1147,6 +1313,7 @@ hipError_t launch_decode_verify_masked_group(uint32_t G, uint32_t m, uint32_t n,
             grp.vR[g] = vR ? vR[g] : nullptr;
             grp.accept[g] = accept[g];
         }
+        if (takes_seg(m, n, B, ell)) return launch_seg(m, n, Xhat, B, ell, grp, G, ctrl, stride, s);
         return launch_cols(m, n, Xhat, B, ell, grp, G, s);
     }
     if (!takes_small(m, n, B, ell) && ell <= 4) {

@@ -77,11 +77,18 @@ def test_client_prepare_matches_oracle(cid, m, n, B, rx, ry, tx, ell):
 # the element-block x column-group kernel above that (ell <= 4; one element
 # per thread and 4 / ell columns per workgroup, or at 256 workgroups and more
 # four elements and 16 / ell columns; ragged column groups and element blocks,
-# n > m) and the general kernel (ell = 7)
+# n > m) and the general kernel (ell = 7); the segment kernel (above 4096
+# elements, up to 8 columns with ell <= 2, 4 with ell <= 4): 8 columns in 17
+# segments of one element per thread (110), 5 columns, ell = 1, n > m in 22
+# segments of two (111), ell = 4 and 3 columns in 20 segments of four (112),
+# ell = 3 and 2 columns in 40 segments (113), one column (114), all ragged
 MASKED = PREP[:2] + PREP[3:4] + PREP[6:] + [(86, 3000, 2000, 8, 2, 2, 16, 3), (87, 500, 400, 2, 2, 2, 9, 7),
                                  (88, 12000, 300, 2, 2, 2, 9, 2), (90, 4096, 1000, 20, 2, 2, 16, 2),
                                  (91, 700, 5000, 13, 2, 2, 9, 4), (92, 1500, 1500, 9, 2, 2, 9, 1),
-                                 (93, 16384, 100, 128, 2, 2, 5, 2), (94, 16000, 90, 64, 2, 2, 5, 3)]
+                                 (93, 16384, 100, 128, 2, 2, 5, 2), (94, 16000, 90, 64, 2, 2, 5, 3),
+                                 (110, 4100, 4096, 8, 3, 3, 64, 2), (111, 4100, 11008, 5, 2, 2, 16, 1),
+                                 (112, 20000, 300, 3, 2, 2, 9, 4), (113, 40000, 1000, 2, 2, 2, 9, 3),
+                                 (114, 33000, 500, 1, 2, 2, 9, 2)]
 
 
 @pytest.mark.parametrize("cid,m,n,B,rx,ry,tx,ell", MASKED)

@@ -927,6 +927,206 @@ uint32_t stream_ksplit(uint32_t m, uint32_t n, uint32_t qt) {
     return best;
 }
 
+// ---------------------------------------------------------------------------
+// Wide-tile path for 17..32 queries per launch group on packed W, built on
+// v_mfma_i32_32x32x32_i8: one instruction multiplies a 32 x 32 digit tile by
+// a 32 x 32 W tile, twice the work of a 16x16x64 instruction for the same 2
+// KiB of operands, so every operand byte brought into registers (W from HBM,
+// digits from LDS) does twice the work.  Operand order of the instruction
+// (checked on the hardware): lane l supplies row (or column) l % 32 at k
+// bytes 16*(l/32) .. +16 of the 32-wide k-slice; lane l's sixteen results
+// are column l % 32, rows 8*(j/4) + 4*(l/32) + j%4 (j < 16).
+//
+// digits32_kernel stores the digit matrix D (digit row 4q + d = plane d of
+// query q) in that order: tile (kb, dt, h) is the 1 KiB that the 64 lanes
+// supply for digit rows 32*dt .. +32 and k = 64*kb + 32*h .. +32.  A k-block
+// holds 2*DT tiles (DT = query slots / 8).
+//
+// server_eval_mfma_x32: NW waves, each owning 32 W rows (two packed row
+// tiles) over all of k, so a workgroup owns 32*NW rows and no k is split.
+// Per k-block the digit tiles (shared by the waves) travel L2 -> LDS by
+// global_load_lds into an S-slot ring, each wave issuing its share, and each
+// wave loads its own two W operands (the two 32-wide k-slices of its rows,
+// 16 bytes per lane, gathered from the packed 16-row tiles) straight into
+// registers with non-temporal loads, S k-blocks ahead.  One wait per k-block
+// covers both (loads complete in issue order).  A wave's DT accumulator
+// tiles hold the four digit sums of 2*DT*4 queries per lane, recombined in
+// the lane to values mod p.
+// ---------------------------------------------------------------------------
+template <bool VEC>
+__global__ __launch_bounds__(256) void digits32_kernel(const uint32_t* __restrict__ X, uint32_t n, uint32_t B,
+                                                       uint32_t DT, uint32_t nkb, int8_t* __restrict__ Dt) {
+    // one thread per (k-block kb, query q, 16-element quarter kq)
+    const uint32_t g = blockIdx.x * 256 + threadIdx.x;
+    const uint32_t nq = DT * 8;
+    if (g >= nkb * nq * 4) return;
+    const uint32_t kq = g % 4, q = (g / 4) % nq, kb = g / (4 * nq);
+    const uint32_t k0 = kb * 64 + kq * 16;
+    uint32_t x[16];
+    const bool okq = q < B;
+    const uint32_t* xr = X + (size_t)(okq ? q : 0u) * n;
+    if (VEC) {  // n % 16 == 0 and X 16-byte aligned: the quarter is wholly in or out
+        const bool ok = okq && k0 < n;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const uint4 t = *reinterpret_cast<const uint4*>(xr + (ok ? k0 : 0u) + 4 * v);
+            x[4 * v] = ok ? t.x : 0u;
+            x[4 * v + 1] = ok ? t.y : 0u;
+            x[4 * v + 2] = ok ? t.z : 0u;
+            x[4 * v + 3] = ok ? t.w : 0u;
+        }
+    } else {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const bool ok = okq && k0 + e < n;
+            const uint32_t t = xr[ok ? k0 + e : 0u];
+            x[e] = ok ? t : 0u;
+        }
+    }
+    int32_t pl[4][4];  // pl[d][w]: digit plane d of elements 4w .. 4w+3
+#pragma unroll
+    for (int w = 0; w < 4; ++w)
+        digit_planes(x[4 * w], x[4 * w + 1], x[4 * w + 2], x[4 * w + 3], pl[0][w], pl[1][w], pl[2][w], pl[3][w]);
+    // digit rows 4q .. 4q+3 are lanes (4q % 32) .. +3 of tile (kb, q / 8, kq / 2),
+    // k-half kq % 2 of the slice: 64 consecutive bytes
+    const uint32_t lane0 = (4 * q) % 32 + 32 * (kq % 2);
+    int8_t* dst = Dt + (((size_t)kb * DT + q / 8) * 2 + kq / 2) * 1024 + (size_t)lane0 * 16;
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+        *reinterpret_cast<int4*>(dst + 16 * d) = make_int4(pl[d][0], pl[d][1], pl[d][2], pl[d][3]);
+}
+
+// global_load_dwordx4 with the non-temporal hint, as inline assembly (see
+// load16): W is streamed once per launch.
+__device__ __forceinline__ void load16_nt(v4i& dst, const void* src) {
+    asm volatile("global_load_dwordx4 %0, %1, off nt" : "=v"(dst) : "v"(src) : "memory");
+}
+
+typedef int v16i __attribute__((ext_vector_type(16)));
+
+template <int DT, int NR, int WQ, int S>
+__global__ __launch_bounds__(NR * WQ * 64) void server_eval_mfma_x32(const int8_t* __restrict__ W, uint32_t m,
+                                                                     uint32_t n, const int8_t* __restrict__ Dt,
+                                                                     uint32_t nkb, uint32_t B, const YOut Y) {
+    // NR row groups x WQ digit groups of waves: wave (wr, wq) multiplies the
+    // 32 rows of row group wr by digit tiles [wq*DW, (wq+1)*DW)
+    constexpr int NW = NR * WQ, DW = DT / WQ;
+    constexpr int NT = 2 * DT;                  // digit tiles per k-block
+    constexpr int AD = (NT + NW - 1) / NW;      // digit tiles a wave loads per k-block
+    constexpr int PER = AD + 2;                 // loads per wave per k-block
+    static_assert(DW * WQ == DT, "digit split");
+    static_assert(S * PER <= 63, "vmcnt range");
+    static_assert(S >= 2, "ring depth");
+    __shared__ __align__(16) int8_t Dring[S][NT][1024];
+    const uint32_t rb = blockIdx.x;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wr = wave / WQ, wq = wave % WQ;
+    // this lane's W row: 32 rows per row group, row tile (lane % 32) / 16 of the pair
+    const uint32_t nrt = (m + 15) / 16;
+    const uint32_t rt = (rb * NR + wr) * 2 + ((lane & 31) >> 4);
+    const uint32_t rtc = rt < nrt ? rt : nrt - 1;  // rows past the end re-read the last tile (not stored)
+    const int8_t* wrow = W + (size_t)rtc * nkb * 1024 + (size_t)((lane & 15) + 16 * (lane >> 5)) * 16;
+    v4i wreg[S][2];
+    // k-block j into ring slot `slot` (blocks past the end re-read the last
+    // one, never consumed)
+    auto issue = [&](uint32_t j, int slot) {
+        const uint32_t kb = j < nkb ? j : nkb - 1;
+#pragma unroll
+        for (int a = 0; a < AD; ++a) {
+            const int tile = (wave * AD + a) % NT;
+            dma16(Dt + ((size_t)kb * NT + tile) * 1024 + (size_t)lane * 16, &Dring[slot][tile][0]);
+        }
+        // k-slice h of the block: 16-byte chunks 2h and 2h+1 of the packed tile
+#pragma unroll
+        for (int h = 0; h < 2; ++h) load16_nt(wreg[slot][h], wrow + (size_t)kb * 1024 + (size_t)h * 512);
+    };
+    v16i acc[DW];
+#pragma unroll
+    for (int d = 0; d < DW; ++d)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[d][e] = 0;
+#pragma unroll
+    for (int j = 0; j < S; ++j) issue(j, j);
+    for (uint32_t j0 = 0; j0 < nkb; j0 += S) {
+#pragma unroll
+        for (int sl = 0; sl < S; ++sl) {
+            const uint32_t j = j0 + sl;
+            if (j < nkb) {
+                wait_vmcnt<(S - 1) * PER>();  // this wave's loads of k-block j landed
+                pin_vgpr(wreg[sl][0]);
+                pin_vgpr(wreg[sl][1]);
+                __syncthreads();  // every wave's digit tiles of k-block j landed
+                // all of the block's digit operands are read before the first
+                // MFMA (one LDS latency per block instead of one per MFMA)
+                v4i a[2][DW];
+#pragma unroll
+                for (int h = 0; h < 2; ++h)
+#pragma unroll
+                    for (int d = 0; d < DW; ++d)
+                        a[h][d] = *reinterpret_cast<const v4i*>(&Dring[sl][2 * (wq * DW + d) + h][16 * lane]);
+#pragma unroll
+                for (int h = 0; h < 2; ++h)
+#pragma unroll
+                    for (int d = 0; d < DW; ++d) pin_vgpr(a[h][d]);
+#pragma unroll
+                for (int h = 0; h < 2; ++h)
+#pragma unroll
+                    for (int d = 0; d < DW; ++d)
+                        acc[d] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[h][d], wreg[sl][h], acc[d], 0, 0, 0);
+                __syncthreads();  // every wave has read the slot: refill it
+                issue(j + S, sl);
+            }
+        }
+    }
+    wait_vmcnt<0>();  // drain the trailing prefetches before the registers are reused or the workgroup exits
+#pragma unroll
+    for (int sl = 0; sl < S; ++sl) {
+        pin_vgpr(wreg[sl][0]);
+        pin_vgpr(wreg[sl][1]);
+    }
+    const uint32_t row = (rb * NR + wr) * 32 + (lane & 31);
+#pragma unroll
+    for (int d = 0; d < DW; ++d)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const uint32_t q = 8 * (wq * DW + d) + 2 * g + (uint32_t)(lane >> 5);
+            const v4i s4 = {acc[d][4 * g], acc[d][4 * g + 1], acc[d][4 * g + 2], acc[d][4 * g + 3]};
+            if (q < B && row < m) *Y.at(q, row) = digits_to_field(s4);
+        }
+}
+
+// server_eval_mfma_x32 for a launch group of 17..32 queries (qt = 8 digit
+// tiles of 16 rows, four 32-row digit tiles): digits32_kernel into Dt, then
+// one workgroup per 128 rows.  (Measured at 28672 x 8192: 32 queries 57 us
+// against 65 us for the streamed kernel; with 64 queries, eight 32-row digit
+// tiles per wave, 89 us against 78, so those stay on the streamed kernel.)
+constexpr int kX32RowGroups = 4, kX32Slots = 4;
+constexpr uint32_t kX32Rows = 32 * kX32RowGroups;
+hipError_t launch_x32(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t nkb, uint32_t B,
+                      const YOut& Y, int8_t* Dt, hipStream_t s) {
+    constexpr uint32_t DT = 4;
+    if (B > DT * 8) return hipErrorInvalidValue;
+    const uint32_t threads = nkb * DT * 8 * 4;
+    if (n % 16 == 0 && (uintptr_t)X % 16 == 0)
+        hipLaunchKernelGGL(digits32_kernel<true>, dim3(ceil_div(threads, 256)), dim3(256), 0, s, X, n, B, DT, nkb,
+                           Dt);
+    else
+        hipLaunchKernelGGL(digits32_kernel<false>, dim3(ceil_div(threads, 256)), dim3(256), 0, s, X, n, B, DT, nkb,
+                           Dt);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((server_eval_mfma_x32<DT, kX32RowGroups, 1, kX32Slots>), dim3(ceil_div(m, kX32Rows)),
+                       dim3(kX32RowGroups * 64), 0, s, W, m, n, Dt, nkb, B, Y);
+    return hipGetLastError();
+}
+
+// The wide-tile kernel takes a launch group of packed W with 17..32 queries
+// when its row blocks alone fill the chip (no k is split).
+bool takes_x32(uint32_t m, uint32_t qt, bool packed) {
+    return packed && qt == 8 && ceil_div(m, kX32Rows) >= 192;
+}
+
 template <int QT, int WQ, int TWW, int S>
 hipError_t launch_stream_cfg(const int8_t* W, uint32_t m, uint32_t n, const int8_t* Dt, uint32_t nkb, uint32_t B,
                              const YOut& Y, uint32_t ksplit, uint32_t* part, uint32_t* counters, bool packed,
@@ -1177,6 +1377,11 @@ hipError_t launch_server_eval_group(const int8_t* W, uint32_t G, uint32_t mg, ui
             continue;
         }
         const uint32_t qt = g.qt, ks = g.ks;
+        if (takes_x32(m, qt, packed)) {
+            e = launch_x32(W, m, n, Xb, nkb, nb, Yb, Dt, s);
+            if (e != hipSuccess) return e;
+            continue;
+        }
         const uint32_t threads = nkb * qt * 16;
         if (n % 16 == 0 && (uintptr_t)Xb % 16 == 0)
             hipLaunchKernelGGL(digits_tiled_kernel<true>, dim3(ceil_div(threads, 256)), dim3(256), 0, s, Xb, n, nb,

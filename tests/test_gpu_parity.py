@@ -89,6 +89,35 @@ def test_server_eval_packed_matches_oracle(m, n, B):
     assert np.array_equal(got, oracle.server_eval(W, X))
 
 
+# 17..32 queries on packed W with at least 192 blocks of 128 rows: the
+# 32x32x32 wide-tile kernel (no k split).  Ragged rows (24600, 25000, 24704)
+# and columns (1000 and 520: not multiples of 64, 1000 not of 16), 32, 20 and
+# 17 queries; 8192 columns; next to them 64 and 33 queries of the same shapes
+# (the streamed kernel).
+WIDE_SHAPES = [(24576, 1000, 32), (24600, 640, 25), (25000, 520, 20), (24576, 8192, 32), (24704, 64, 17),
+               (24576, 1000, 64), (24600, 640, 33)]
+
+
+@pytest.mark.parametrize("m,n,B", WIDE_SHAPES)
+def test_server_eval_wide_tiles_match_oracle(m, n, B):
+    _say(f"server_eval wide tiles m={m} n={n} B={B}")
+    W = synth.weights(300 + m + n, m, n)
+    X = synth.field_uniform(301 + B + n, (B, n))
+    got = host(mvk.server_eval(mvk.pack_weights(dev(W)), dev(X)))
+    assert np.array_equal(got, oracle.server_eval(W, X, nthreads=oracle.threads()))
+
+
+def test_server_eval_group_wide_tiles_match_oracle():
+    """A row stack of two matrices (12800 rows each) with 30 queries: the
+    wide-tile kernel writes each matrix's rows to its own output."""
+    mg, n, B = 12800, 700, 30
+    Ws = [synth.weights(310 + g, mg, n) for g in range(2)]
+    X = synth.field_uniform(312, (B, n))
+    outs = mvk.server_eval_group(mvk.pack_weights_group([dev(W) for W in Ws]), 2, dev(X))
+    for W, Y in zip(Ws, outs):
+        assert np.array_equal(host(Y), oracle.server_eval(W, X, nthreads=oracle.threads()))
+
+
 @pytest.mark.parametrize("path", ["valu", "mfma"])
 @pytest.mark.parametrize("wv,xv", [(-128, P - 8421504), (127, P - 1), (-127, P - 1), (-128, 1073741823),
                                    (127, 1073741824), (-1, 0)])

@@ -743,13 +743,14 @@ __global__ __launch_bounds__(NW * 64) void server_eval_mfma_stream(
 // barriers.  W needs no sharing between waves (each wave owns TWW row tiles),
 // so it travels HBM -> registers with ordinary loads: chunks of C k-blocks,
 // the next chunk's loads issued before the current chunk's MFMAs (two
-// register sets used in turn).  Eight waves; rows 128*TWW per workgroup.
-template <int QT, int TWW, int KBM, int C, bool PACKED>
-__global__ __launch_bounds__(512) void server_eval_mfma_dstat(const int8_t* __restrict__ W, uint32_t m, uint32_t n,
-                                                              const uint32_t* __restrict__ X, uint32_t nkb,
-                                                              uint32_t ksplit, uint32_t B, const YOut Y,
-                                                              unsigned long long* accum) {
-    constexpr int NW = 8;
+// register sets used in turn).  NW waves (8, or 4 for more workgroups on
+// short matrices); rows 16*NW*TWW per workgroup.
+template <int QT, int TWW, int KBM, int C, bool PACKED, int NW>
+__global__ __launch_bounds__(NW * 64) void server_eval_mfma_dstat(const int8_t* __restrict__ W, uint32_t m,
+                                                                  uint32_t n, const uint32_t* __restrict__ X,
+                                                                  uint32_t nkb, uint32_t ksplit, uint32_t B,
+                                                                  const YOut Y, unsigned long long* accum,
+                                                                  uint32_t rot_mul) {
     constexpr uint32_t kRows = NW * TWW * 16;
     __shared__ __align__(16) int8_t Dst[KBM][QT][1024];
     const uint32_t xcd = blockIdx.x % 8, per_group = 8 / ksplit;
@@ -771,10 +772,15 @@ __global__ __launch_bounds__(512) void server_eval_mfma_dstat(const int8_t* __re
         const uint32_t row = rb * kRows + (wave * TWW + t) * 16 + (lane & 15);
         wptr[t] = W + (size_t)(row < m ? row : m - 1) * n;
     }
+    // Each wave walks its k-range from its own starting block (row tile *
+    // rot_mul, cyclically): the sum does not depend on the order, and waves
+    // of neighbouring row tiles then do not read the same k-offset at once.
+    const uint32_t rot = nk ? ((rb * (kRows / 16) + (uint32_t)wave * TWW) * rot_mul) % nk : 0u;
+    auto rotj = [&](uint32_t j) { return j + rot < nk ? j + rot : j + rot - nk; };  // j < nk
     // B operand of row tile t at local k-block j (in range: blocks past the
     // end re-read the last block of the range, masked out below)
     auto load_w = [&](uint32_t j, int t) -> v4i {
-        const uint32_t kbj = kb0 + (j < nk ? j : (nk ? nk - 1 : 0u));
+        const uint32_t kbj = kb0 + (j < nk ? rotj(j) : (nk ? rotj(nk - 1) : 0u));
         const uint32_t kbe = kbj < nkb ? kbj : nkb - 1;
         if (PACKED) {
             const uint32_t rt = rb * (kRows / 16) + wave * TWW + t;
@@ -789,13 +795,14 @@ __global__ __launch_bounds__(512) void server_eval_mfma_dstat(const int8_t* __re
     // zero.  A thread has at most kUnits units; their query loads are issued
     // first (needed first), then the first W chunk, then the conversion (which
     // waits for the query loads only).
-    constexpr int kUnits = (KBM * QT * 16 + 511) / 512;
+    constexpr int kThreads = NW * 64;
+    constexpr int kUnits = (KBM * QT * 16 + kThreads - 1) / kThreads;
     const uint32_t nunits = nk * QT * 16;
     const bool xvec = (n % 16 == 0) && (((uintptr_t)X & 15) == 0);
     uint32_t x[kUnits][16];
 #pragma unroll
     for (int r = 0; r < kUnits; ++r) {
-        const uint32_t u = threadIdx.x + 512u * r;
+        const uint32_t u = threadIdx.x + (uint32_t)kThreads * r;
         const uint32_t kq = u % 4, q = (u / 4) % (QT * 4), kbl = u / (QT * 16);
         const uint32_t k0 = (kb0 + kbl) * 64 + kq * 16;
         const bool okq = u < nunits && q < B;
@@ -828,7 +835,7 @@ __global__ __launch_bounds__(512) void server_eval_mfma_dstat(const int8_t* __re
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int r = 0; r < kUnits; ++r) {
-        const uint32_t u = threadIdx.x + 512u * r;
+        const uint32_t u = threadIdx.x + (uint32_t)kThreads * r;
         if (u >= nunits) break;
         const uint32_t kq = u % 4, q = (u / 4) % (QT * 4), kbl = u / (QT * 16);
         int32_t pl[4][4];
@@ -854,7 +861,7 @@ __global__ __launch_bounds__(512) void server_eval_mfma_dstat(const int8_t* __re
         for (int c = 0; c < C; ++c) {
             const uint32_t j = j0 + c;
             const int32_t msk = j < nk ? -1 : 0;
-            const uint32_t jd = j < nk ? j : 0u;
+            const uint32_t jd = j < nk ? rotj(j) : 0u;
             v4i ca[QT];
 #pragma unroll
             for (int i = 0; i < QT; ++i) ca[i] = *reinterpret_cast<const v4i*>(&Dst[jd][i][16 * lane]);
@@ -1207,6 +1214,7 @@ struct GroupPlan {
     uint32_t rows;  // rows per workgroup
     uint32_t ks;    // k-ranges
     uint32_t kbm;   // k-blocks of digit tiles the LDS holds (digits-stationary kernel)
+    uint32_t nw;    // waves per workgroup (digits-stationary kernel)
 };
 
 constexpr uint32_t kDstatKbm4 = 32, kDstatKbm2 = 64;  // k-blocks of digit tiles in 128 KiB of LDS
@@ -1222,7 +1230,7 @@ uint32_t dstat_kbm(uint32_t kb_per) {
 
 GroupPlan group_plan(uint32_t m, uint32_t n, uint32_t nb) {
     const uint32_t qt = group_qt(nb), nkb = ceil_div(n, 64);
-    GroupPlan g{false, qt, 0, stream_rows(qt), stream_ksplit(m, n, qt), 0};
+    GroupPlan g{false, qt, 0, stream_rows(qt), stream_ksplit(m, n, qt), 0, 8};
     if (qt > 4) return g;
     // digits-stationary: rows 128*tww, each k-range's digit tiles fit in LDS;
     // estimated time ceil(workgroups / 256) * (W k-blocks per workgroup in units
@@ -1238,46 +1246,54 @@ GroupPlan group_plan(uint32_t m, uint32_t n, uint32_t nb) {
             const uint32_t cost = ceil_div(nwg, 256) * (kb_per * tww + 6 + qt * (ks - 1));
             if (cost < best) {
                 best = cost;
-                g = GroupPlan{true, qt, tww, rows, ks, dstat_kbm(kb_per)};
+                g = GroupPlan{true, qt, tww, rows, ks, dstat_kbm(kb_per), 8};
             }
         }
     return g;
 }
 
-template <int QT, int TWW, int KBM, int C>
+template <int QT, int TWW, int KBM, int C, int NW>
 hipError_t launch_dstat_cfg(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t nkb, uint32_t B,
                             const YOut& Y, uint32_t ksplit, unsigned long long* accum, bool packed,
                             hipStream_t s);
 
+// Starting-block step of the digits-stationary kernel's k-walk per row tile
+// (odd, so the starting blocks of a power-of-two k-range all differ).
+// Measured on MI355X, the 128 server calls of a stack pass replayed
+// alternately in one process: 1.736 ms without, 1.713 ms with step 7 (5:
+// 1.716, 13: 1.726, 1: 1.737).
+uint32_t dstat_rotation() { return 7u; }
+
 // launch_dstat_cfg for the plan's LDS size (kbm a power of two in [8, KBM max])
-template <int QT, int TWW>
+template <int QT, int TWW, int NW>
 hipError_t launch_dstat_kbm(uint32_t kbm, const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t nkb,
                             uint32_t B, const YOut& Y, uint32_t ksplit, unsigned long long* accum,
                             bool packed, hipStream_t s) {
     constexpr uint32_t kMax = QT == 4 ? kDstatKbm4 : kDstatKbm2;
-    if (kbm == 8) return launch_dstat_cfg<QT, TWW, 8, 8>(W, m, n, X, nkb, B, Y, ksplit, accum, packed, s);
-    if (kbm == 16) return launch_dstat_cfg<QT, TWW, 16, 8>(W, m, n, X, nkb, B, Y, ksplit, accum, packed, s);
-    if (kbm == 32) return launch_dstat_cfg<QT, TWW, 32, 8>(W, m, n, X, nkb, B, Y, ksplit, accum, packed, s);
+    if (kbm == 8) return launch_dstat_cfg<QT, TWW, 8, 8, NW>(W, m, n, X, nkb, B, Y, ksplit, accum, packed, s);
+    if (kbm == 16) return launch_dstat_cfg<QT, TWW, 16, 8, NW>(W, m, n, X, nkb, B, Y, ksplit, accum, packed, s);
+    if (kbm == 32) return launch_dstat_cfg<QT, TWW, 32, 8, NW>(W, m, n, X, nkb, B, Y, ksplit, accum, packed, s);
     if constexpr (kMax >= 64)
         if (kbm == 64)
-            return launch_dstat_cfg<QT, TWW, 64, 8>(W, m, n, X, nkb, B, Y, ksplit, accum, packed, s);
+            return launch_dstat_cfg<QT, TWW, 64, 8, NW>(W, m, n, X, nkb, B, Y, ksplit, accum, packed, s);
     return hipErrorInvalidValue;
 }
 
-template <int QT, int TWW, int KBM, int C>
+template <int QT, int TWW, int KBM, int C, int NW>
 hipError_t launch_dstat_cfg(const int8_t* W, uint32_t m, uint32_t n, const uint32_t* X, uint32_t nkb, uint32_t B,
                             const YOut& Y, uint32_t ksplit, unsigned long long* accum, bool packed,
                             hipStream_t s) {
     if (ksplit == 0 || ceil_div(nkb, ksplit) > (uint32_t)KBM) return hipErrorInvalidValue;  // LDS holds the range
     if (ksplit > 1 && !accum) return hipErrorInvalidValue;
-    const uint32_t nrb = ceil_div(m, 128 * TWW), per_group = 8 / ksplit;
+    const uint32_t nrb = ceil_div(m, 16 * NW * TWW), per_group = 8 / ksplit;
     const dim3 grid(ceil_div(nrb, per_group) * 8);
+    const uint32_t rot = dstat_rotation();
     if (packed)
-        hipLaunchKernelGGL((server_eval_mfma_dstat<QT, TWW, KBM, C, true>), grid, dim3(512), 0, s, W, m, n, X, nkb,
-                           ksplit, B, Y, accum);
+        hipLaunchKernelGGL((server_eval_mfma_dstat<QT, TWW, KBM, C, true, NW>), grid, dim3(NW * 64), 0, s, W, m, n,
+                           X, nkb, ksplit, B, Y, accum, rot);
     else
-        hipLaunchKernelGGL((server_eval_mfma_dstat<QT, TWW, KBM, C, false>), grid, dim3(512), 0, s, W, m, n, X, nkb,
-                           ksplit, B, Y, accum);
+        hipLaunchKernelGGL((server_eval_mfma_dstat<QT, TWW, KBM, C, false, NW>), grid, dim3(NW * 64), 0, s, W, m, n,
+                           X, nkb, ksplit, B, Y, accum, rot);
     return hipGetLastError();
 }
 }  // namespace
@@ -1363,16 +1379,19 @@ hipError_t launch_server_eval_group(const int8_t* W, uint32_t G, uint32_t mg, ui
         const YOut Yb = yout_shift(out, b0);
         hipError_t e = hipSuccess;
         if (g.dstat) {
-            if (g.qt == 4)
-                e = g.tww == 1 ? launch_dstat_kbm<4, 1>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, accum,
-                                                        packed, s)
-                               : launch_dstat_kbm<4, 2>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, accum,
-                                                        packed, s);
+            if (g.nw == 4)  // four waves: one row tile each
+                e = g.qt == 4 ? launch_dstat_kbm<4, 1, 4>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, accum, packed, s)
+                              : launch_dstat_kbm<2, 1, 4>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, accum, packed, s);
+            else if (g.qt == 4)
+                e = g.tww == 1 ? launch_dstat_kbm<4, 1, 8>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, accum,
+                                                           packed, s)
+                               : launch_dstat_kbm<4, 2, 8>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, accum,
+                                                           packed, s);
             else
-                e = g.tww == 1 ? launch_dstat_kbm<2, 1>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, accum,
-                                                        packed, s)
-                               : launch_dstat_kbm<2, 2>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, accum,
-                                                        packed, s);
+                e = g.tww == 1 ? launch_dstat_kbm<2, 1, 8>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, accum,
+                                                           packed, s)
+                               : launch_dstat_kbm<2, 2, 8>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, accum,
+                                                           packed, s);
             if (e != hipSuccess) return e;
             continue;
         }

@@ -743,8 +743,8 @@ __global__ __launch_bounds__(NW * 64) void server_eval_mfma_stream(
 // barriers.  W needs no sharing between waves (each wave owns TWW row tiles),
 // so it travels HBM -> registers with ordinary loads: chunks of C k-blocks,
 // the next chunk's loads issued before the current chunk's MFMAs (two
-// register sets used in turn).  NW waves (8, or 4 for more workgroups on
-// short matrices); rows 16*NW*TWW per workgroup.
+// register sets used in turn).  NW waves (eight as launched: four measured
+// no better); rows 16*NW*TWW per workgroup.
 template <int QT, int TWW, int KBM, int C, bool PACKED, int NW>
 __global__ __launch_bounds__(NW * 64) void server_eval_mfma_dstat(const int8_t* __restrict__ W, uint32_t m,
                                                                   uint32_t n, const uint32_t* __restrict__ X,
@@ -1214,7 +1214,6 @@ struct GroupPlan {
     uint32_t rows;  // rows per workgroup
     uint32_t ks;    // k-ranges
     uint32_t kbm;   // k-blocks of digit tiles the LDS holds (digits-stationary kernel)
-    uint32_t nw;    // waves per workgroup (digits-stationary kernel)
 };
 
 constexpr uint32_t kDstatKbm4 = 32, kDstatKbm2 = 64;  // k-blocks of digit tiles in 128 KiB of LDS
@@ -1230,7 +1229,7 @@ uint32_t dstat_kbm(uint32_t kb_per) {
 
 GroupPlan group_plan(uint32_t m, uint32_t n, uint32_t nb) {
     const uint32_t qt = group_qt(nb), nkb = ceil_div(n, 64);
-    GroupPlan g{false, qt, 0, stream_rows(qt), stream_ksplit(m, n, qt), 0, 8};
+    GroupPlan g{false, qt, 0, stream_rows(qt), stream_ksplit(m, n, qt), 0};
     if (qt > 4) return g;
     // digits-stationary: rows 128*tww, each k-range's digit tiles fit in LDS;
     // estimated time ceil(workgroups / 256) * (W k-blocks per workgroup in units
@@ -1246,7 +1245,7 @@ GroupPlan group_plan(uint32_t m, uint32_t n, uint32_t nb) {
             const uint32_t cost = ceil_div(nwg, 256) * (kb_per * tww + 6 + qt * (ks - 1));
             if (cost < best) {
                 best = cost;
-                g = GroupPlan{true, qt, tww, rows, ks, dstat_kbm(kb_per), 8};
+                g = GroupPlan{true, qt, tww, rows, ks, dstat_kbm(kb_per)};
             }
         }
     return g;
@@ -1379,10 +1378,7 @@ hipError_t launch_server_eval_group(const int8_t* W, uint32_t G, uint32_t mg, ui
         const YOut Yb = yout_shift(out, b0);
         hipError_t e = hipSuccess;
         if (g.dstat) {
-            if (g.nw == 4)  // four waves: one row tile each
-                e = g.qt == 4 ? launch_dstat_kbm<4, 1, 4>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, accum, packed, s)
-                              : launch_dstat_kbm<2, 1, 4>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, accum, packed, s);
-            else if (g.qt == 4)
+            if (g.qt == 4)
                 e = g.tww == 1 ? launch_dstat_kbm<4, 1, 8>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, accum,
                                                            packed, s)
                                : launch_dstat_kbm<4, 2, 8>(g.kbm, W, m, n, Xb, nkb, nb, Yb, g.ks, accum,

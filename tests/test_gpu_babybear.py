@@ -42,6 +42,8 @@ def _dense(N, idx, val):
 SERVER_SHAPES = [
     (1, 1, 1), (17, 33, 2), (257, 4099, 1), (4096, 4096, 1), (100, 160, 5), (300, 1000, 16), (31, 2048, 64),
     (70, 999, 65), (16, 128, 130), (1000, 8192, 64), (257, 11008, 8), (64, 16448, 8), (129, 8192, 16),
+    # packed, 17..32 queries and at least 192 blocks of 128 rows: the wide-tile kernel
+    (24704, 520, 20),
 ]
 
 
@@ -174,6 +176,10 @@ PREP = [  # cid, m, n, B, r_x, r_y, t_x, ell
     (86, 3000, 2000, 8, 2, 2, 16, 3),
     (87, 500, 400, 2, 2, 2, 9, 7),
     (89, 1024, 1024, 1, 8, 8, 160, 2),
+    # one workgroup per column (4096-long columns) and the segment kernel
+    # (ragged 4100 x 11008, five columns)
+    (90, 4096, 3000, 8, 2, 2, 16, 2),
+    (91, 4100, 11008, 5, 2, 2, 16, 2),
 ]
 
 
@@ -204,6 +210,24 @@ def test_prepared_path(cid, m, n, B, rx, ry, tx, ell):
         assert oacc.astype(np.uint32).tolist() == want == host(acc).tolist()
         assert np.array_equal(host(vL), ovL) and np.array_equal(host(vR), ovR)
         assert np.array_equal(host(Y), oracle.decode(PT, resp, inst.exi, inst.exv, p=Q))
+
+
+def test_client_turn():
+    """decode_verify_encode_masked over BabyBear: the fused launch (4096 x
+    4096, one column) and the two-launch form (3000 x 2000, eight columns)
+    give the outputs of decode_verify_masked and encode_masked."""
+    for cid, m, n, B in ((92, 4096, 4096, 1), (93, 3000, 2000, 8)):
+        inst = Instance(cid, m, n, B, 3, 32, ty=31, ell=2, p=Q).to_device()
+        mvk.keygen(inst.key, inst.dW)
+        prep = mvk.client_prepare(inst.key, inst.dexi, inst.dexv, inst.deyi, inst.deyv)
+        prep2 = mvk.client_prepare(inst.key, inst.dexi, inst.dexv, inst.deyi, inst.deyv)
+        Xh = mvk.encode_masked(inst.key, inst.dX, prep)
+        Yh = mvk.server_eval(inst.dW, Xh, p=Q)
+        X2 = dev(synth.field_uniform(cid + 7, (B, n), p=Q))
+        Y, acc, _, _, Xh2 = mvk.decode_verify_encode_masked(inst.key, Xh, Yh, prep, X2, prep2)
+        Y1, acc1, _, _ = mvk.decode_verify_masked(inst.key, Xh, Yh, prep)
+        assert torch.equal(Y, Y1) and torch.equal(acc, acc1) and host(acc).tolist() == [1] * B
+        assert torch.equal(Xh2, mvk.encode_masked(inst.key, X2, prep2))
 
 
 def test_verify_only():

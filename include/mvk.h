@@ -542,7 +542,10 @@ mvk_status mvk_workspace_release(void);
  * preparation beside the online calls of the pipelined mode (Sec. 7): two
  * disjoint ranges keep the streams' workgroups off each other's compute
  * units, so a kernel waiting on a flag never holds units the other stream's
- * producer needs.  Release with mvk_stream_destroy.
+ * producer needs.  Release with mvk_stream_destroy, which waits for the
+ * stream, destroys it, and retires the library's workspace of that stream
+ * (freed by mvk_workspace_release, like the buffers a workspace growth
+ * retires).
  * Errors: MVK_EINVAL (stream NULL, count 0, or a range past the device's
  * compute units), MVK_EHIP.
  */

@@ -993,7 +993,27 @@ mvk_status mvk_stream_create_cu_range(uint32_t first_cu, uint32_t count, void** 
 
 mvk_status mvk_stream_destroy(void* stream) {
     if (!stream) return MVK_EINVAL;
-    return hip_status(hipStreamDestroy((hipStream_t)stream));
+    hipStream_t s = (hipStream_t)stream;
+    if (hipStreamSynchronize(s) != hipSuccess) return MVK_EHIP;
+    {
+        // the stream's workspaces join the retired buffers (graphs captured on
+        // the stream may still hold their addresses): freed by
+        // mvk_workspace_release, and a later stream that gets the same handle
+        // starts with a fresh workspace
+        std::lock_guard<std::mutex> lk(g_ws_mu);
+        if (g_ws) {
+            for (auto it = g_ws->begin(); it != g_ws->end();) {
+                if (it->first.second == s) {
+                    if (!g_ws_retired) g_ws_retired = new std::vector<void*>();
+                    if (it->second.ptr) g_ws_retired->push_back(it->second.ptr);
+                    it = g_ws->erase(it);
+                } else {
+                    ++it;
+                }
+            }
+        }
+    }
+    return hip_status(hipStreamDestroy(s));
 }
 
 mvk_status mvk_sample_code(uint32_t k, uint32_t r, uint64_t seed, uint64_t tag, uint32_t* pi1, uint32_t* pi2,

@@ -176,6 +176,19 @@ def test_flags_order_compute_unit_streams():
     finally:
         a.close()
         b.close()
+    # destroying a stream retires its workspace: streams created afterwards
+    # (which may get the same handle) start with a fresh one, and the
+    # retired buffers are freed by mvk_workspace_release
+    for _ in range(2):
+        c = mvk.CUStream(0, ncu)
+        try:
+            with torch.cuda.stream(c.stream):
+                yc = mvk.server_eval(mvk.pack_weights(W), X, stream=c.stream)
+            torch.cuda.synchronize()
+            assert torch.equal(yc, ref)
+        finally:
+            c.close()
+    assert mvk._lib.load().mvk_workspace_release() == 0
 
 
 @pytest.mark.parametrize("cid,m,n,B,r,tx,ell", [(98, 4096, 4096, 1, 3, 64, 2), (99, 1000, 700, 3, 3, 17, 3),

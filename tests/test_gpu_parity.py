@@ -92,10 +92,11 @@ def test_server_eval_packed_matches_oracle(m, n, B):
 # 17..32 queries on packed W with at least 192 blocks of 128 rows: the
 # 32x32x32 wide-tile kernel (no k split).  Ragged rows (24600, 25000, 24704)
 # and columns (1000 and 520: not multiples of 64, 1000 not of 16), 32, 20 and
-# 17 queries; 8192 columns; next to them 64 and 33 queries of the same shapes
-# (the streamed kernel).
+# 17 queries; 8192 columns.  Next to them 33..64 queries on the streamed
+# kernel: 64 and 33 queries of those shapes, 200 columns (four k-blocks, the
+# last one ragged), 40960 rows, 57 queries at 20736 x 4096.
 WIDE_SHAPES = [(24576, 1000, 32), (24600, 640, 25), (25000, 520, 20), (24576, 8192, 32), (24704, 64, 17),
-               (24576, 1000, 64), (24600, 640, 33)]
+               (24576, 1000, 64), (24600, 640, 33), (20480, 200, 64), (40960, 256, 40), (20736, 4096, 57)]
 
 
 @pytest.mark.parametrize("m,n,B", WIDE_SHAPES)
@@ -116,6 +117,35 @@ def test_server_eval_group_wide_tiles_match_oracle():
     outs = mvk.server_eval_group(mvk.pack_weights_group([dev(W) for W in Ws]), 2, dev(X))
     for W, Y in zip(Ws, outs):
         assert np.array_equal(host(Y), oracle.server_eval(W, X, nthreads=oracle.threads()))
+
+
+def test_server_eval_group_64_queries_match_oracle():
+    """A row stack of two matrices of 12304 rows (a row block of the streamed
+    kernel straddles them) with 50 queries: each matrix's rows go to its own
+    output."""
+    mg, n, B = 12304, 700, 50
+    Ws = [synth.weights(320 + g, mg, n) for g in range(2)]
+    X = synth.field_uniform(322, (B, n))
+    outs = mvk.server_eval_group(mvk.pack_weights_group([dev(W) for W in Ws]), 2, dev(X))
+    for W, Y in zip(Ws, outs):
+        assert np.array_equal(host(Y), oracle.server_eval(W, X, nthreads=oracle.threads()))
+
+
+@pytest.mark.parametrize("wv", [-128, 127])
+def test_server_eval_64_queries_extremes_closed_form(wv):
+    """Constant W = wv (20480 x 2048, packed) against 64 queries, each a
+    constant at an extreme of the balanced digits (every digit -128 or 127,
+    the centring boundary, 0, 1, p - 1): every row of query q is n wv x_q mod
+    p, on the streamed kernel."""
+    m, n = 20480, 2048
+    xs = [P - 8421504, 8421504 - 1, P - 1, 1, 0, 1073741823, 1073741824, 2139062143]
+    xs = [xs[q % len(xs)] if q < len(xs) else (xs[q % len(xs)] + q * 7919) % P for q in range(64)]
+    _say(f"server_eval 64-query extremes w={wv}")
+    W = torch.full((m, n), wv, dtype=torch.int8, device="cuda")
+    X = torch.tensor(np.repeat(np.array(xs, dtype=np.uint32)[:, None], n, axis=1).view(np.int32), device="cuda")
+    got = host(mvk.server_eval(mvk.pack_weights(W), X))
+    want = np.array([(n * wv * x) % P for x in xs], dtype=np.uint32)
+    assert np.array_equal(got, np.repeat(want[:, None], m, axis=1))
 
 
 @pytest.mark.parametrize("path", ["valu", "mfma"])

@@ -284,9 +284,11 @@ def test_batch_verification(cid, m, n, B, r, r2):
 
 
 # ---------------------------------------------------------------------------
-# The Sec. 7.1 workload at n = 2^14 (r = 8, t_x = 154): sampled outputs
+# The Sec. 7.1 workload at n = 2^14 (r = 8, t_x = 154): X^, Y^ and Y in full
+# (the oracle's product threaded over row blocks), P^T and Q on sampled
+# columns (a full oracle keygen would hold 2^31 words of each)
 # ---------------------------------------------------------------------------
-def test_paper_eval_n16384_sampled():
+def test_paper_eval_n16384():
     cfg = synth.PAPER_EVAL
     n = 16384
     _say(f"babybear paper workload n={n} r={cfg['r']} tx={cfg['tx'][n]}")
@@ -302,11 +304,13 @@ def test_paper_eval_n16384_sampled():
     dXh = mvk.encode(inst.key, inst.dX, inst.dexi, inst.dexv)
     Xh = oracle.encode(inst.cx, inst.X, inst.exi, inst.exv, p=Q)
     assert np.array_equal(host(dXh), Xh)
+    T = oracle.threads()
     dYh = mvk.server_eval(inst.dW, dXh, p=Q)
-    assert np.array_equal(host(dYh)[:, rows], oracle.server_eval(inst.W[rows], Xh, p=Q))
+    assert np.array_equal(host(dYh), oracle.server_eval(inst.W, Xh, p=Q, nthreads=T))
     Y, acc, _, _ = mvk.decode_verify(inst.key, dXh, dYh, inst.dexi, inst.dexv, inst.deyi, inst.deyv)
     assert host(acc).tolist() == [1]
-    assert np.array_equal(host(Y)[:, rows], oracle.server_eval(inst.W[rows], inst.X, p=Q))
+    # completeness (Thm. 6.1): the decryption of an honest response is W x
+    assert np.array_equal(host(Y), oracle.server_eval(inst.W, inst.X, p=Q, nthreads=T))
     bad = dYh.clone()
     bad[0, int(rows[1])] = (int(bad[0, int(rows[1])]) + 777) % Q
     _, acc2, _, _ = mvk.decode_verify(inst.key, dXh, bad, inst.dexi, inst.dexv, inst.deyi, inst.deyv)

@@ -148,6 +148,26 @@ def test_server_eval_64_queries_extremes_closed_form(wv):
     assert np.array_equal(got, np.repeat(want[:, None], m, axis=1))
 
 
+@pytest.mark.parametrize("B", [5, 16, 20, 64])
+@pytest.mark.parametrize("wv", [-128, 127])
+def test_server_eval_batched_extremes_at_max_n(B, wv):
+    """n at the exactness limit (every digit-plane sum up to n 128 128 - 1 <
+    2^31) on the batched kernels: 300 rows of constant W = wv, packed, against
+    B queries, each a constant at an extreme of the balanced digits; every
+    row of query q is n wv x_q mod p.  At this n no k-range of digit tiles
+    fits in LDS, so every B takes the streamed kernel (2, 4, 8 and 16 digit
+    tiles), k split where its plan splits it."""
+    m, n = 300, mvk.MVK_MAX_N
+    base = [P - 8421504, 1073741823, 1073741824, P - 1, 1, 0, 8421503, 2139062143]
+    xs = [base[q % len(base)] for q in range(B)]
+    _say(f"server_eval batched extremes n={n} B={B} w={wv}")
+    W = torch.full((m, n), wv, dtype=torch.int8, device="cuda")
+    X = torch.tensor(np.repeat(np.array(xs, dtype=np.uint32)[:, None], n, axis=1).view(np.int32), device="cuda")
+    got = host(mvk.server_eval(mvk.pack_weights(W), X))
+    want = np.array([(n * wv * x) % P for x in xs], dtype=np.uint32)
+    assert np.array_equal(got, np.repeat(want[:, None], m, axis=1))
+
+
 @pytest.mark.parametrize("path", ["valu", "mfma"])
 @pytest.mark.parametrize("wv,xv", [(-128, P - 8421504), (127, P - 1), (-127, P - 1), (-128, 1073741823),
                                    (127, 1073741824), (-1, 0)])

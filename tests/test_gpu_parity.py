@@ -131,16 +131,17 @@ def test_server_eval_group_64_queries_match_oracle():
         assert np.array_equal(host(Y), oracle.server_eval(W, X, nthreads=oracle.threads()))
 
 
+@pytest.mark.parametrize("m,n,B", [(4096, 16384, 8), (4096, 16384, 16), (24576, 1024, 32), (20480, 2048, 64)])
 @pytest.mark.parametrize("wv", [-128, 127])
-def test_server_eval_64_queries_extremes_closed_form(wv):
-    """Constant W = wv (20480 x 2048, packed) against 64 queries, each a
-    constant at an extreme of the balanced digits (every digit -128 or 127,
-    the centring boundary, 0, 1, p - 1): every row of query q is n wv x_q mod
-    p, on the streamed kernel."""
-    m, n = 20480, 2048
+def test_server_eval_batched_extremes_closed_form(m, n, B, wv):
+    """Constant W = wv (packed) against B queries, each a constant at an
+    extreme of the balanced digits (every digit -128 or 127, the centring
+    boundary, 0, 1, p - 1): every row of query q is n wv x_q mod p, on the
+    digits-stationary kernel (8 and 16 queries), the wide-tile kernel (32) and
+    the streamed kernel (64)."""
     xs = [P - 8421504, 8421504 - 1, P - 1, 1, 0, 1073741823, 1073741824, 2139062143]
-    xs = [xs[q % len(xs)] if q < len(xs) else (xs[q % len(xs)] + q * 7919) % P for q in range(64)]
-    _say(f"server_eval 64-query extremes w={wv}")
+    xs = [xs[q % len(xs)] if q < len(xs) else (xs[q % len(xs)] + q * 7919) % P for q in range(B)]
+    _say(f"server_eval batched extremes m={m} n={n} B={B} w={wv}")
     W = torch.full((m, n), wv, dtype=torch.int8, device="cuda")
     X = torch.tensor(np.repeat(np.array(xs, dtype=np.uint32)[:, None], n, axis=1).view(np.int32), device="cuda")
     got = host(mvk.server_eval(mvk.pack_weights(W), X))

@@ -427,3 +427,35 @@ def test_multi_preparation_matches_oracle():
             R = np.stack([oracle.syn(cy_h, _dense(cy_h["N"], ey_h[0][q], ey_h[1][q])) for q in range(ey_h[0].shape[0])])
             assert np.array_equal(host(preps[g].R), R), (g, "R")
             assert np.array_equal(host(preps[g].U), oracle.server_eval(np.ascontiguousarray(W.T), R)), (g, "U")
+
+
+# m, n, B, ell: the one-workgroup form (m != n: rejected), one workgroup per
+# column (ell 2 and 4, 8 and 40 columns), segmented sums (ell 2 and 3), the
+# element-block form (70000 rows: longer than one column's workgroup or
+# segments take) and the general form (ell = 6)
+MAXVAL = [(1000, 900, 2, 2), (4096, 4096, 8, 2), (4096, 4096, 8, 4), (3000, 3000, 40, 2), (12000, 12000, 4, 2),
+          (12000, 11000, 3, 3), (70000, 1000, 1, 2), (70000, 1000, 3, 4), (2000, 2000, 3, 6)]
+
+
+@pytest.mark.parametrize("m,n,B,ell", MAXVAL)
+def test_decode_verify_masked_at_max_values_closed_form(m, n, B, ell):
+    """Every input p - 1 (X^, Y^, the masks My and the challenge vectors R,
+    U): (p - 1)^2 = 1 mod p, so v_L = n and v_R = m mod p in every column and
+    repetition, Y = 0, and the columns are accepted exactly when m = n; the
+    64-bit sums of every check kernel run at their largest terms."""
+    _say(f"decode_verify_masked max values m={m} n={n} B={B} ell={ell}")
+    cx = code(synth.raa_code(synth.seed_for(62, synth.PURPOSE_CX, n), n, 1))
+    cy = code(synth.raa_code(synth.seed_for(62, synth.PURPOSE_CY, m), m, 1))
+    key = mvk.Key.allocate(m, n, cx, cy)  # P^T and Q are not read by the masked check
+    prep = mvk.Prepared(key, B, ell)
+    for t in (prep.My, prep.R, prep.U, prep.Mx):
+        t.fill_(P - 1)
+    Xh = torch.full((B, n), P - 1, dtype=torch.int32, device="cuda")
+    Yh = torch.full((B, m), P - 1, dtype=torch.int32, device="cuda")
+    vL = torch.full((ell, B), -1, dtype=torch.int32, device="cuda")
+    vR = torch.full_like(vL, -1)
+    Y, acc, _, _ = mvk.decode_verify_masked(key, Xh, Yh, prep, vL=vL, vR=vR)
+    torch.cuda.synchronize()
+    assert not host(Y).any()
+    assert (host(vL) == n % P).all() and (host(vR) == m % P).all()
+    assert host(acc).tolist() == [1 if m == n else 0] * B

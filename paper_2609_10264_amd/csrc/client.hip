@@ -590,7 +590,7 @@ __global__ __launch_bounds__(kSmallThreads) void decode_verify_small(
 // masked encode of the next query (add_masks_body, the other workgroups, with
 // the optional wait for its preparation's flag) in one launch.  The two roles
 // share no data.
-template <int EL, int PER, bool WAIT>
+template <int EL, int PER, bool WAIT, int APER>
 __global__ __launch_bounds__(kSmallThreads) void client_turn(
     uint32_t Gd, uint32_t m, uint32_t n, const uint32_t* __restrict__ Xhat, const uint32_t* __restrict__ Yhat,
     uint32_t B, const uint32_t* __restrict__ My, uint32_t ell, const uint32_t* __restrict__ R,
@@ -602,7 +602,7 @@ __global__ __launch_bounds__(kSmallThreads) void client_turn(
     if (blockIdx.x < Gd)
         dv_small_body<EL, PER>(blockIdx.x, Gd, m, n, Xhat, Yhat, B, My, ell, R, U, Y, acc, counter, vL, vR, accept);
     else
-        add_masks_body<WAIT, 4>(blockIdx.x - Gd, gridDim.x - Gd, Xn, Mxn, countn, Xhatn, flag, value, ticks,
+        add_masks_body<WAIT, APER>(blockIdx.x - Gd, gridDim.x - Gd, Xn, Mxn, countn, Xhatn, flag, value, ticks,
                                 timed_out, add_counter);
 }
 
@@ -1270,7 +1270,8 @@ hipError_t launch_client_turn(uint32_t m, uint32_t n, const uint32_t* Xhat, cons
     const uint32_t len = m > n ? m : n;
     uint32_t Gd = ceil_div(len, 4u * kSmallThreads);
     Gd = Gd < 1u ? 1u : (Gd > 8u ? 8u : Gd);
-    size_t Ga = (countn + 4u * kAddThreads - 1) / (4u * kAddThreads);
+    const int aper = add_masks_per(countn);
+    size_t Ga = (countn + (size_t)aper * kAddThreads - 1) / ((size_t)aper * kAddThreads);
     Ga = Ga > 256 ? 256 : (Ga == 0 ? 1 : Ga);
     uint64_t ticks = 0;
     if (flag) {
@@ -1278,15 +1279,18 @@ hipError_t launch_client_turn(uint32_t m, uint32_t n, const uint32_t* Xhat, cons
         if (e != hipSuccess) return e;
     }
     const dim3 grid(Gd + (uint32_t)Ga), block(kSmallThreads);
-#define MVK_TURN(EL, W)                                                                                          \
-    hipLaunchKernelGGL((client_turn<EL, 4, W>), grid, block, 0, s, Gd, m, n, Xhat, Yhat, B, My, ell, r, U, Y, acc, \
+#define MVK_TURN_A(EL, W, A)                                                                                        \
+    hipLaunchKernelGGL((client_turn<EL, 4, W, A>), grid, block, 0, s, Gd, m, n, Xhat, Yhat, B, My, ell, r, U, Y, acc, \
                        ctrl, vL, vR, accept, Xn, Mxn, countn, Xhatn, flag, value, ticks, timed_out, add_counter)
+#define MVK_TURN(EL, W) \
+    if (aper == 1) MVK_TURN_A(EL, W, 1); else if (aper == 2) MVK_TURN_A(EL, W, 2); else MVK_TURN_A(EL, W, 4)
     if (ell <= 2) {
-        if (flag) MVK_TURN(2, true); else MVK_TURN(2, false);
+        if (flag) { MVK_TURN(2, true); } else { MVK_TURN(2, false); }
     } else {
-        if (flag) MVK_TURN(4, true); else MVK_TURN(4, false);
+        if (flag) { MVK_TURN(4, true); } else { MVK_TURN(4, false); }
     }
 #undef MVK_TURN
+#undef MVK_TURN_A
     return hipGetLastError();
 }
 

@@ -29,6 +29,18 @@ __device__ inline bool poll_flag(const uint32_t* flag, uint32_t value, uint64_t 
 // finish (counted on `counter`, which it also clears).  The caller's
 // workgroup is number `bid` of the `nblocks` that share the elements.
 constexpr int kAddThreads = 1024;
+
+// Words per thread and pass of a masked encode of `count` words: the fewest
+// (1, 2 or 4) that still cover the words in one pass of at most 256
+// workgroups.  One word per thread spreads a stage's encode over more
+// compute units, whose loads are then in flight together (measured on the
+// 32-layer stack, whose encodes cover 32768 and 88064 words: 3.48 ms per
+// pass against 3.53-3.62 with four words per thread); past 256 workgroups a
+// second dependent pass would cost more than the wider threads.
+inline int add_masks_per(size_t count) {
+    const size_t one = (size_t)256 * kAddThreads;
+    return count <= one ? 1 : count <= 2 * one ? 2 : 4;
+}
 template <bool WAIT, int PER>
 __device__ __forceinline__ void add_masks_body(uint32_t bid, uint32_t nblocks, const uint32_t* X,
                                                const uint32_t* __restrict__ Mx, size_t count, uint32_t* Xhat,

@@ -709,9 +709,10 @@ hipError_t launch_add_masks(const uint32_t* X, const uint32_t* Mx, size_t count,
                             uint32_t value, uint32_t timeout_us, uint32_t* timed_out, uint32_t* counter,
                             hipStream_t s) {
     if (count == 0 && !flag) return hipSuccess;
-    // four words per thread, one pass per workgroup up to 256 workgroups (a
-    // single workgroup up to 4096 words clears the flag itself)
-    size_t blocks = (count + 4u * kAddThreads - 1) / (4u * kAddThreads);
+    // add_masks_per words per thread, one pass per workgroup up to 256
+    // workgroups (a single workgroup clears the flag itself)
+    const int per = add_masks_per(count);
+    size_t blocks = (count + (size_t)per * kAddThreads - 1) / ((size_t)per * kAddThreads);
     if (blocks > 256) blocks = 256;
     if (blocks == 0) blocks = 1;
     uint64_t ticks = 0;
@@ -722,7 +723,13 @@ hipError_t launch_add_masks(const uint32_t* X, const uint32_t* Mx, size_t count,
 #define MVK_ADD(W, P)                                                                                          \
     hipLaunchKernelGGL((add_masks<W, P>), dim3((uint32_t)blocks), dim3(kAddThreads), 0, s, X, Mx, count, Xhat, flag, \
                        value, ticks, timed_out, counter)
-    if (flag) MVK_ADD(true, 4); else MVK_ADD(false, 4);
+    if (per == 1) {
+        if (flag) MVK_ADD(true, 1); else MVK_ADD(false, 1);
+    } else if (per == 2) {
+        if (flag) MVK_ADD(true, 2); else MVK_ADD(false, 2);
+    } else {
+        if (flag) MVK_ADD(true, 4); else MVK_ADD(false, 4);
+    }
 #undef MVK_ADD
     return hipGetLastError();
 }

@@ -131,6 +131,18 @@ def test_server_eval_group_64_queries_match_oracle():
         assert np.array_equal(host(Y), oracle.server_eval(W, X, nthreads=oracle.threads()))
 
 
+def test_server_eval_16384_single_query_matches_oracle():
+    """The single-query shape the bench measures against the read floor
+    (16384 x 16384, packed W, one column): Y^ in full against the oracle,
+    threaded over row blocks."""
+    m = n = 16384
+    _say(f"server_eval {m}x{n} B=1 packed")
+    W = synth.weights(330, m, n)
+    X = synth.field_uniform(331, (1, n))
+    got = host(mvk.server_eval(mvk.pack_weights(dev(W)), dev(X)))
+    assert np.array_equal(got, oracle.server_eval(W, X, nthreads=oracle.threads()))
+
+
 @pytest.mark.parametrize("m,n,B", [(4096, 16384, 8), (4096, 16384, 16), (24576, 1024, 32), (20480, 2048, 64)])
 @pytest.mark.parametrize("wv", [-128, 127])
 def test_server_eval_batched_extremes_closed_form(m, n, B, wv):
